@@ -1,0 +1,256 @@
+/*
+ * kvk.h — C ABI of the per-layer compressed KV-cache library (KV-Kaizen decode path).
+ *
+ * The library implements the inference-time hot path of KV-Kaizen
+ * (arXiv 2609.37988): a plan assigns every layer one action, either `inherit`
+ * (read the nearest earlier anchor's cache, §2.1 "Depth") or a kept width and
+ * bit-width (d, b) (§2.2, eq. (1)–(3)).  Anchor layers write their K/V cache once
+ * at prefill, compressed as the plan says (§2.1 "Precision", App. C.3); every
+ * decode step then runs single-query softmax attention of each layer's own
+ * query against its anchor's compressed cache (§2.1).
+ *
+ * Conventions that hold for every entry point:
+ *   - All device buffers (inputs, arena, workspace, outputs) are owned by the
+ *     caller.  They must be device pointers valid on the current HIP device and
+ *     16-byte aligned.  The library never allocates or frees device memory and
+ *     never synchronises the stream on these calls.
+ *   - Calls that launch work enqueue it on `stream` and return at once.  All
+ *     argument validation happens synchronously on the host before any launch;
+ *     a failing call launches nothing.
+ *   - Errors are returned as kvk_status codes, never as aborts or C++
+ *     exceptions.  kvk_last_error() returns a thread-local message for the
+ *     last failing call on the calling thread.
+ *   - A kvk_table is immutable after creation; it may be shared between
+ *     threads for concurrent calls.
+ *   - Keys handed to the library are taken as they are (post-RoPE); the
+ *     library never applies a rotary embedding.
+ *   - GQA head map: query head h reads KV head h / (Hq / Hkv).
+ */
+#ifndef KVK_H
+#define KVK_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVK_MAX_LAYERS 64
+#define KVK_GROUP 32 /* quantisation group: 32 tokens (keys) / 32 channels (values) */
+
+typedef enum {
+  KVK_OK = 0,
+  KVK_ERR_INVALID = -1,     /* a plan, shape, pointer or size violates this header */
+  KVK_ERR_UNSUPPORTED = -2, /* valid in the paper's terms, not provided by this library */
+  KVK_ERR_DEVICE = -3,      /* a HIP launch or query failed; see kvk_last_error() */
+  KVK_ERR_BUFFER = -4       /* a caller buffer is too small (workspace) */
+} kvk_status;
+
+typedef enum { KVK_GQA = 0, KVK_MLA = 1 } kvk_kind;
+
+/* Quantiser used by every quantised layer of a table.
+ *  KVK_Q_KIVI32 — grouped asymmetric (App. C.3 "grouped asymmetric quantizer"):
+ *    keys: one (scale, zero) pair of fp16 per channel per 32 consecutive stored
+ *    tokens; values: one pair per token per 32 consecutive channels; codes use
+ *    all 2^b levels.
+ *  KVK_Q_SYMROW — the paper's own quantiser (App. B "Quantization", App. C.3):
+ *    symmetric, one bf16 scale per 128-element token-head row (per token, per
+ *    KV head, separately for K and V), codes in [-q, q] with q = 2^(b-1) - 1. */
+typedef enum { KVK_Q_KIVI32 = 0, KVK_Q_SYMROW = 1 } kvk_qscheme;
+
+typedef enum { KVK_BF16 = 0, KVK_F32 = 1 } kvk_dtype;
+
+/* One plan entry (§2.2, eq. (3)).  inherit != 0 selects the zero-cost action;
+ * otherwise bits is b in {2, 4, 8, 16} and rank is the kept width d.  For GQA
+ * the rank axis does not exist (§2.2): rank must be 0 or 2*Hkv*d_h. */
+typedef struct {
+  int32_t inherit;
+  int32_t bits;
+  int32_t rank;
+} kvk_action;
+
+/* Geometry of the cached model and of the arena. */
+typedef struct {
+  int32_t kind;        /* kvk_kind; KVK_MLA currently returns KVK_ERR_UNSUPPORTED */
+  int32_t n_layers;    /* L, 1..KVK_MAX_LAYERS */
+  int32_t n_q_heads;   /* Hq */
+  int32_t n_kv_heads;  /* Hkv; Hq % Hkv == 0; Hq/Hkv * (readers of one anchor) <= 64 */
+  int32_t head_dim;    /* d_h in {64, 128} */
+  int32_t latent_dim;  /* MLA r (unused for GQA, pass 0) */
+  int32_t rope_dim;    /* MLA d_R (unused for GQA, pass 0) */
+  int32_t nope_dim;    /* MLA per-head no-RoPE query/key width (unused for GQA) */
+  int32_t v_dim;       /* MLA per-head value width (unused for GQA) */
+  int32_t qscheme;     /* kvk_qscheme */
+  int32_t batch;       /* B >= 1 */
+  int32_t max_tokens;  /* prefill length capacity per sequence, >= 1 */
+  int32_t keep_tokens; /* 0: no eviction; else stored tokens per (sequence, KV head) */
+} kvk_dims;
+
+typedef struct kvk_table kvk_table;
+
+/* Everything the host needs to allocate and account for a table. */
+typedef struct {
+  int64_t arena_bytes;          /* bytes the caller allocates for the compressed cache */
+  int64_t workspace_bytes;      /* decode workspace for the full layer range [0, L) */
+  int32_t n_anchors;            /* layers that own a cache */
+  int32_t stored_tokens_cap;    /* stored tokens per (b, KV head): keep_tokens or max_tokens */
+  double cost_bits_per_token;   /* sum over layers of c(a_l), eq. (1) */
+  double c0_bits_per_token;     /* C0 = L * 2 * Hkv * d_h * 16, eq. (2) */
+  double rho;                   /* eq. (2): C0 / sum c(a_l), metadata excluded (§3) */
+  double rho_realized;          /* bf16 cache bytes / arena bytes actually stored at
+                                   capacity (metadata and bf16 tail included, eviction
+                                   included) */
+  int32_t anchor_of[KVK_MAX_LAYERS];   /* nearest anchor at or before l (§2.1) */
+  int64_t layer_offset[KVK_MAX_LAYERS];/* byte offset of the layer's region; -1 if it inherits */
+  int64_t layer_bytes[KVK_MAX_LAYERS]; /* region size (0 if it inherits) */
+  int64_t stream_bytes[KVK_MAX_LAYERS];/* bytes of one (b, KV head) stream of the layer */
+  double layer_cost_bits[KVK_MAX_LAYERS]; /* c(a_l), eq. (1), bits per token */
+  double layer_bits_per_elt[KVK_MAX_LAYERS]; /* stored bits per cached scalar at capacity,
+                                                metadata included (App. C.3 accounting) */
+} kvk_table_info;
+
+/*
+ * ARENA LAYOUT (GQA).  All multi-byte fields are little-endian.
+ *
+ * The region of anchor layer l (layer_offset[l], layer_bytes[l]) holds B*Hkv
+ * streams, stream s = b*Hkv + kvh at offset s*stream_bytes[l].  A stream holds
+ * the layer's stored tokens of one (sequence, KV head) in order: NB = cap/32
+ * full blocks of 32 tokens (cap = stored_tokens_cap), followed by one tail
+ * block.  With n stored tokens, blocks 0 .. n/32-1 are full and the tail block
+ * holds tokens 32*(n/32) .. n-1 (fewer than 32) in the bf16 block format, its
+ * unused slots zero.  Stream and region sizes are rounded up to 256 bytes.
+ *
+ * Within a 32-token block, positions are described by "lanes" lam = 16*kg + i
+ * with kg in 0..3 and i in 0..15, D = d_h, and
+ *   K slot map: lane lam, tile tau in {0,1}, sub-chunk j in 0..D/32-1, slot s in 0..7
+ *               holds token 16*tau + i, channel 32*j + 8*kg + s;
+ *   V slot map: lane lam, tile m in 0..D/16-1, slot s in 0..7
+ *               holds channel 16*m + i, token 16*(s/4) + 4*kg + (s%4).
+ *
+ * bf16 block (bits = 16, and every tail block), 128*D bytes:
+ *   [K: 64*D bytes][V: 64*D bytes]
+ *   K: tile tau at byte 32*D*tau; inside it lane lam at byte lam*(D/2); inside
+ *      that sub-chunk j at byte 16*j; slot s is the bf16 at byte 2*s.
+ *   V: lane lam at byte lam*D; tile m at byte 16*m; slot s the bf16 at byte 2*s.
+ *   A bf16 value is the round-to-nearest-even bf16 of the input value.
+ *
+ * quantised block (bits b in {2, 4, 8}):
+ *   [K codes: 4*D*b][V codes: 4*D*b][K meta][V meta]
+ *   K codes: tile tau at byte 2*D*b*tau; lane lam at byte lam*(D*b/32); sub-chunk
+ *      j occupies b bytes at byte j*b of the lane.
+ *   V codes: lane lam at byte lam*(D*b/16); tile m occupies b bytes at byte m*b.
+ *   Each such b-byte "chunk" holds 8 codes of b bits (slots s = 0..7):
+ *      b = 8: slot s is byte s.
+ *      b = 4: the chunk is one 32-bit word; slot s at bit 16*(s%2) + 4*(s/2).
+ *      b = 2: chunk pairs (j or m even, then odd) form one 32-bit word at the even
+ *             chunk's byte; slot s of chunk x at bit 16*(s%2) + 2*(s/2) + 8*(x%2).
+ *   KIVI32 meta (4*D bytes each):
+ *      K meta: fp16 scale[D] then fp16 zero[D], natural channel order; the pair
+ *              of channel c covers this block's 32 tokens.
+ *      V meta: fp16 at index ((g*2 + w)*4 + kg)*8 + s, w = 0 scale / 1 zero, for
+ *              channel group g (channels 32g..32g+31) and token
+ *              16*(s/4) + 4*kg + (s%4).
+ *   SYMROW meta (64 bytes each): K meta bf16 scale[32], V meta bf16 scale[32],
+ *      natural token order.
+ *   Block bytes: KIVI32 8*D*(b+1); SYMROW 8*D*b + 128.
+ *
+ * Codes (unsigned, b bits):
+ *   KIVI32 (App. C.3 grouped asymmetric): for a group x_1..x_32 (a channel over a
+ *   block's tokens for K, a token over 32 channels for V), in IEEE fp32
+ *   arithmetic with round-to-nearest-even:
+ *      mn = min x, mx = max x
+ *      scale = fp16( (mx - mn) / (2^b - 1) ),  zero = fp16( mn )
+ *      u = 0 if scale == 0 else clamp( rint( (x - zero) / scale ), 0, 2^b - 1 )
+ *      dequantised value = fmaf(u, scale, zero)
+ *   SYMROW (App. C.3 symmetric): for a 128-element row, q = 2^(b-1) - 1,
+ *      scale = bf16( max|x| / q ),
+ *      code = 0 if scale == 0 else clamp( rint( x / scale ), -q, q ),
+ *      u = code + 2^(b-1), dequantised value = code * scale.
+ *   Inputs with |x| beyond the fp16 range are outside the supported domain of
+ *   KIVI32 (the scale and zero are fp16).
+ */
+
+/* Build the layer table of a plan (§2.2): validate every action against
+ * eq. (3) (layer 0 must own a cache, §2.2/§2.3), resolve anchor_of, compute the
+ * per-layer cost eq. (1), the compression ratio eq. (2), the arena layout and
+ * the decode workspace size.  Host only; touches no device.
+ * Errors: KVK_ERR_INVALID on any violation (message via kvk_last_error()). */
+kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* plan, kvk_table** out);
+
+/* Copy the table's accounting and layout into *out.  Host only. */
+kvk_status kvk_table_query(const kvk_table* table, kvk_table_info* out);
+
+/* Free a table (NULL is accepted). */
+void kvk_table_destroy(kvk_table* table);
+
+/* Workspace bytes needed by kvk_decode_attention over [layer_begin, layer_end). */
+kvk_status kvk_workspace_bytes(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
+                               size_t* out_bytes);
+
+/* Prefill write of one layer's cache (§2.1: an anchor writes its cache, an
+ * inheriting layer writes nothing; App. C.3 quantisers).
+ *   k, v      : device [B][Hkv][n_tokens][d_h], dtype in_dtype (bf16 or fp32), contiguous.
+ *   n_tokens  : prefill length, 1..max_tokens.
+ *   keep_idx  : NULL when the table has no eviction; else device int32
+ *               [B][Hkv][keep_tokens], strictly increasing positions in
+ *               [0, n_tokens): the stored stream is k/v at these positions, in
+ *               order (composition with token eviction, §3 long context).
+ *   arena     : device, arena_bytes; only this layer's region is written.
+ * An inheriting layer returns KVK_OK without launching anything.
+ * keep_idx contents are trusted: the host cannot read device memory without a
+ * synchronisation, so out-of-range positions are clamped by the kernel.
+ * Errors: KVK_ERR_INVALID (layer, sizes, NULL pointers, keep_idx presence),
+ *         KVK_ERR_DEVICE (launch failure). */
+kvk_status kvk_compress_layer(const kvk_table* table, int32_t layer, const void* k, const void* v,
+                              int32_t in_dtype, int32_t n_tokens, const int32_t* keep_idx,
+                              void* arena, hipStream_t stream);
+
+/* One decode step of attention for layers [layer_begin, layer_end) (§2.1): layer l
+ * uses its own query and the cache of anchor_of[l].  Layers in the range that
+ * share an anchor are served by one read of that anchor's bytes.
+ *   q        : device [layer_end-layer_begin][B][Hq][d_h], dtype q_dtype.
+ *   n_stored : stored tokens per (b, KV head), 0..stored_tokens_cap (the prefill
+ *              n_tokens, or keep_tokens under eviction).  n_stored = 0 yields zeros.
+ *   scale    : softmax scale applied to q.k.
+ *   w_uk, w_uv: MLA up-projections; must be NULL for GQA.
+ *   out      : device fp32 [layer_end-layer_begin][B][Hq][d_h].
+ *   workspace: device, >= kvk_workspace_bytes(...) bytes, 256-byte aligned; its
+ *              contents on entry are ignored.
+ * Calls that overlap on one workspace race.
+ * Errors: KVK_ERR_INVALID, KVK_ERR_BUFFER (workspace too small), KVK_ERR_DEVICE. */
+kvk_status kvk_decode_attention(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
+                                const void* q, int32_t q_dtype, int32_t n_stored, float scale,
+                                const void* w_uk, const void* w_uv, const void* arena,
+                                float* out, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+
+/* Test support: dequantise the cache read by `layer` (its anchor's) into fp32
+ * k_out, v_out [B][Hkv][n_stored][d_h], using the rules above bit for bit. */
+kvk_status kvk_debug_dequantize(const kvk_table* table, int32_t layer, int32_t n_stored,
+                                const void* arena, float* k_out, float* v_out, hipStream_t stream);
+
+/* Storage accounting of App. C.3 (table of storage cost with quantisation
+ * metadata): bits per cached element for `bits`-bit codes with 32 bits of
+ * metadata per `group` elements (grouped scheme, KVK_Q_KIVI32) or one bf16 scale
+ * per 128-element row (KVK_Q_SYMROW, group ignored), with `window` of the
+ * `context` tokens kept in bf16.  Returns a negative value on invalid input. */
+double kvk_realized_bits(int32_t qscheme, int32_t bits, int32_t group, int64_t window,
+                         int64_t context);
+
+/* eq. (5): rho_min / rho_max over the actions a layer may take.
+ *   axes bit 0 = precision (B = {2,4,8,16}, else {16}), bit 1 = rank (MLA,
+ *   D = {r/8, r/4, r/2, r}, else {r} for MLA / the full GQA width), bit 2 = depth.
+ *   mla selects the MLA cost (d + d_R) b with r = latent_dim, else the GQA cost
+ *   2*Hkv*d_h*b.  C0 = L * kv_width * 16 with kv_width = 2*Hkv*d_h. */
+kvk_status kvk_rho_range(int32_t n_layers, int32_t kv_width, int32_t latent_dim, int32_t rope_dim,
+                         int32_t mla, int32_t axes, double* rho_min, double* rho_max);
+
+const char* kvk_last_error(void);
+const char* kvk_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* KVK_H */

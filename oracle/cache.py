@@ -1,0 +1,156 @@
+"""Compress a layer to arena bytes and run a decode step from them (oracle).
+
+TEST INFRASTRUCTURE ONLY (see oracle/__init__.py).
+
+Write side (§2.1, App. C.3): an anchor layer stores, per (sequence, KV head),
+its keys and values — after an optional eviction gather (§3 long context: the
+evictor runs on the same cache) — as 32-token blocks quantised by the table's
+scheme (or bf16 at b = 16) plus a bf16 tail of the last n % 32 tokens.  An
+inheriting layer stores nothing.
+
+Read side: dequantise the anchor's stream and attend (§2.1).
+
+Parity: dequantised values and arena bytes are defined exactly by the rules in
+include/kvk.h and are pinned through the quantiser and layout pins; attention
+outputs on compressed caches have no printed values in the paper (parity of
+those values rests on the attention pins plus this composition).
+"""
+import numpy as np
+
+from . import attention as att
+from . import layout, quant
+from .plan import GROUP, KIVI32, Dims, anchor_of, arena_offsets, layer_bytes, stream_bytes
+
+F32 = np.float32
+
+
+def quantise_blocks(dims: Dims, bits: int, K: np.ndarray, V: np.ndarray) -> dict:
+    """K, V fp32 [nb, 32, D] -> the fields of nb quantised blocks."""
+    D = dims.head_dim
+    nb = K.shape[0]
+    if dims.qscheme == KIVI32:
+        uk, ks, kz = quant.kivi_quantize(np.swapaxes(K, 1, 2), bits)  # groups: channel x 32 tokens
+        uv, vs, vz = quant.kivi_quantize(V.reshape(nb, 32, D // 32, 32), bits)  # token x 32 ch
+        return {"uk": np.swapaxes(uk, 1, 2), "uv": uv.reshape(nb, 32, D),
+                "ks": ks, "kz": kz, "vs": vs, "vz": vz}
+    uk, ks = quant.symrow_quantize(K, bits)  # one row = a token's D channels
+    uv, vs = quant.symrow_quantize(V, bits)
+    return {"uk": uk, "uv": uv, "ks": ks, "vs": vs}
+
+
+def dequantise_blocks(dims: Dims, bits: int, f: dict):
+    """Fields of nb quantised blocks -> K_hat, V_hat fp32 [nb, 32, D]."""
+    D = dims.head_dim
+    nb = f["uk"].shape[0]
+    if dims.qscheme == KIVI32:
+        kh = quant.kivi_dequantize(f["uk"], f["ks"][:, None, :], f["kz"][:, None, :])
+        uv = f["uv"].reshape(nb, 32, D // 32, 32)
+        vh = quant.kivi_dequantize(uv, f["vs"][..., None], f["vz"][..., None]).reshape(nb, 32, D)
+        return kh, vh
+    kh = quant.symrow_dequantize(f["uk"], f["ks"][..., None], bits)
+    vh = quant.symrow_dequantize(f["uv"], f["vs"][..., None], bits)
+    return kh, vh
+
+
+def compress_stream(dims: Dims, bits: int, K: np.ndarray, V: np.ndarray) -> np.ndarray:
+    """One stream's stored tokens K, V [n, D] (fp32 values) -> stream bytes."""
+    n, D = K.shape
+    nb, nt = divmod(n, GROUP)
+    K = np.asarray(K, dtype=F32)
+    V = np.asarray(V, dtype=F32)
+    Kf = K[:nb * GROUP].reshape(nb, GROUP, D)
+    Vf = V[:nb * GROUP].reshape(nb, GROUP, D)
+    if bits == 16:
+        blocks = layout.pack_bf16_blocks(quant.bf16_bits(Kf), quant.bf16_bits(Vf))
+    else:
+        blocks = layout.pack_quant_blocks(dims, bits, quantise_blocks(dims, bits, Kf, Vf))
+    kt = np.zeros((1, GROUP, D), dtype=np.uint16)
+    vt = np.zeros((1, GROUP, D), dtype=np.uint16)
+    kt[0, :nt] = quant.bf16_bits(K[nb * GROUP:])
+    vt[0, :nt] = quant.bf16_bits(V[nb * GROUP:])
+    tail = layout.pack_bf16_blocks(kt, vt)[0]
+    return layout.assemble_stream(dims, bits, blocks, tail)
+
+
+def dequant_stream(dims: Dims, bits: int, stream: np.ndarray, n_stored: int):
+    """Stream bytes -> K_hat, V_hat fp32 [n_stored, D]."""
+    D = dims.head_dim
+    blocks, tail = layout.split_stream(dims, bits, stream, n_stored)
+    nb = blocks.shape[0]
+    if bits == 16:
+        kb, vb = layout.unpack_bf16_blocks(blocks, D)
+        kh, vh = quant.bf16_value(kb), quant.bf16_value(vb)
+    else:
+        kh, vh = dequantise_blocks(dims, bits, layout.unpack_quant_blocks(dims, bits, blocks))
+    kt, vt = layout.unpack_bf16_blocks(tail[None], D)
+    nt = n_stored - nb * GROUP
+    K = np.concatenate([kh.reshape(-1, D), quant.bf16_value(kt[0, :nt])])
+    V = np.concatenate([vh.reshape(-1, D), quant.bf16_value(vt[0, :nt])])
+    return K, V
+
+
+def gather_kept(X: np.ndarray, keep: np.ndarray) -> np.ndarray:
+    """Eviction: the stored stream is X at the kept positions, in increasing order."""
+    return X[np.sort(np.asarray(keep))]
+
+
+def compress_layer(dims: Dims, bits: int, K: np.ndarray, V: np.ndarray, keep=None) -> np.ndarray:
+    """K, V [B, Hkv, n, D] -> the layer's region bytes (B*Hkv streams)."""
+    B, H = K.shape[:2]
+    sb = stream_bytes(dims, bits)
+    out = np.zeros(layer_bytes(dims, bits), dtype=np.uint8)
+    for b in range(B):
+        for h in range(H):
+            k, v = K[b, h], V[b, h]
+            if keep is not None:
+                k, v = gather_kept(k, keep[b, h]), gather_kept(v, keep[b, h])
+            s = b * H + h
+            out[s * sb:(s + 1) * sb] = compress_stream(dims, bits, k, v)
+    return out
+
+
+def compress_arena(dims: Dims, plan, Ks, Vs, keeps=None) -> np.ndarray:
+    """Whole arena for per-layer inputs Ks[l], Vs[l] (ignored for inheritors)."""
+    offs, total = arena_offsets(dims, plan)
+    arena = np.zeros(total, dtype=np.uint8)
+    for l, a in enumerate(plan):
+        if a.inherit:
+            continue
+        reg = compress_layer(dims, a.bits, Ks[l], Vs[l], None if keeps is None else keeps[l])
+        arena[offs[l]:offs[l] + reg.size] = reg
+    return arena
+
+
+def dequant_layer(dims: Dims, plan, arena: np.ndarray, layer: int, n_stored: int):
+    """K_hat, V_hat fp32 [B, Hkv, n_stored, D] of the cache `layer` reads."""
+    a = anchor_of(plan)[layer]
+    offs, _ = arena_offsets(dims, plan)
+    bits = plan[a].bits
+    sb = stream_bytes(dims, bits)
+    B, H, D = dims.batch, dims.n_kv_heads, dims.head_dim
+    Kh = np.zeros((B, H, n_stored, D), dtype=F32)
+    Vh = np.zeros_like(Kh)
+    for b in range(B):
+        for h in range(H):
+            s = offs[a] + (b * H + h) * sb
+            Kh[b, h], Vh[b, h] = dequant_stream(dims, bits, arena[s:s + sb], n_stored)
+    return Kh, Vh
+
+
+def decode_step(dims: Dims, plan, arena: np.ndarray, q: np.ndarray, n_stored: int,
+                scale: float, l0: int = 0, l1=None) -> np.ndarray:
+    """q [l1-l0, B, Hq, D] -> out fp64 [l1-l0, B, Hq, D]: each layer's own query
+    attends over its anchor's dequantised cache (§2.1)."""
+    l1 = dims.n_layers if l1 is None else l1
+    anc = anchor_of(plan)
+    out = np.zeros((l1 - l0, dims.batch, dims.n_q_heads, dims.head_dim))
+    cachebuf = {}
+    for l in range(l0, l1):
+        a = anc[l]
+        if a not in cachebuf:
+            cachebuf[a] = dequant_layer(dims, plan, arena, a, n_stored)
+        Kh, Vh = cachebuf[a]
+        for b in range(dims.batch):
+            out[l - l0, b] = att.gqa_attention(np.asarray(q[l - l0, b], np.float64),
+                                               Kh[b], Vh[b], scale)
+    return out

@@ -1,0 +1,143 @@
+"""Seeded synthetic inputs shared by the tests, the smoke check and the bench.
+
+This module only draws random numbers and fixes shapes; it holds none of the
+method's arithmetic (no quantisation, packing or attention).  Every draw is
+seeded.  Shapes follow the backbones of App. B (Qwen2.5-7B: 28 layers, 4 KV
+heads; Qwen2.5-14B: 48 layers, 8 KV heads; head dim 128) and the workloads of
+the decode benchmark; key tensors carry a per-channel log-normal outlier scale,
+the per-channel key structure App. A cites from KVQuant.
+
+Plans are drawn the way the workloads describe them: a random subset of layers
+inherits (never layer 0), anchor bit-widths are drawn uniformly.
+"""
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import numpy as np
+import torch
+
+GQA, MLA = 0, 1
+KIVI32, SYMROW = 0, 1
+
+
+@dataclass
+class Workload:
+    name: str
+    n_layers: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    batch: int
+    tokens: int
+    keep_tokens: int = 0
+    in_dtype: torch.dtype = torch.bfloat16
+    q_dtype: torch.dtype = torch.bfloat16
+    key_outliers: bool = True
+    scale: float = 0.0
+    qscheme: int = KIVI32
+    plan: List[tuple] = field(default_factory=list)  # (inherit, bits) per layer
+    seed: int = 0
+
+    def softmax_scale(self) -> float:
+        return self.scale if self.scale > 0 else 1.0 / float(np.sqrt(self.head_dim))
+
+
+def plan_uniform(n_layers: int, bits: int):
+    return [(0, bits)] * n_layers
+
+
+def plan_mixed(seed: int, n_layers: int, n_inherit: int, bit_choices=(16, 8, 4, 2)):
+    """A random plan: n_inherit layers drawn from 1..L-1 inherit; every anchor's
+    bit-width is drawn uniformly from bit_choices."""
+    rng = np.random.default_rng(seed)
+    inh = set(int(x) for x in rng.choice(np.arange(1, n_layers), n_inherit, replace=False))
+    plan = []
+    for l in range(n_layers):
+        if l in inh:
+            plan.append((1, 16))
+        else:
+            plan.append((0, int(rng.choice(bit_choices))))
+    return plan
+
+
+def plan_grouped(seed: int, group_sizes, anchor_bits):
+    """Anchors each followed by inheritors: group_sizes[i] consecutive layers share
+    one anchor whose bit-width is anchor_bits[i]; the order of the groups and of
+    the bit-widths is shuffled with the seed."""
+    rng = np.random.default_rng(seed)
+    sizes = list(rng.permutation(group_sizes))
+    bits = list(rng.permutation(anchor_bits))
+    plan = []
+    for g, b in zip(sizes, bits):
+        plan.append((0, int(b)))
+        plan.extend([(1, 16)] * (int(g) - 1))
+    return plan
+
+
+def workload(cfg: int, variant: Optional[str] = None) -> Workload:
+    """The five decode workloads.  cfg 0: tiny single layer; 1: Qwen2.5-7B-shaped
+    all-int4 (variant 'bf16': all bf16); 2: Qwen2.5-14B-shaped mixed plan with
+    depth sharing; 4: 14B-shaped, 128k context, half the positions evicted, an
+    int2/int4 plan in pairs and triples."""
+    if cfg == 0:
+        return Workload("tiny-gqa-int8", 1, 4, 1, 64, 1, 256, in_dtype=torch.float32,
+                        q_dtype=torch.float32, key_outliers=False, scale=1.0 / 8.0,
+                        plan=plan_uniform(1, 8), seed=1000)
+    if cfg == 1:
+        bits = 16 if variant == "bf16" else 4
+        return Workload("qwen2.5-7b-shape-int4" if bits == 4 else "qwen2.5-7b-shape-bf16",
+                        28, 28, 4, 128, 8, 8192, plan=plan_uniform(28, bits), seed=1001)
+    if cfg == 2:
+        return Workload("qwen2.5-14b-shape-mixed", 48, 40, 8, 128, 32, 8192,
+                        plan=plan_mixed(1002, 48, 16), seed=1002)
+    if cfg == 4:
+        plan = plan_grouped(1004, [2] * 12 + [3] * 8, [2] * 16 + [4] * 4)
+        return Workload("qwen2.5-14b-shape-128k-evict", 48, 40, 8, 128, 4, 131072,
+                        keep_tokens=65536, plan=plan, seed=1004)
+    raise ValueError(f"unknown workload {cfg}")
+
+
+def generator(seed: int, device) -> torch.Generator:
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    return g
+
+
+def kv_layer(w: Workload, layer: int, device="cpu", batch: Optional[int] = None,
+             tokens: Optional[int] = None):
+    """K, V [B, Hkv, T, D] of one layer in w.in_dtype: N(0,1) values; keys times a
+    per-(layer, KV head, channel) LogNormal(0,1) scale when w.key_outliers."""
+    B = w.batch if batch is None else batch
+    T = w.tokens if tokens is None else tokens
+    g = generator(w.seed * 1000 + layer, device)
+    shape = (B, w.n_kv_heads, T, w.head_dim)
+    k = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    v = torch.randn(shape, generator=g, device=device, dtype=torch.float32)
+    if w.key_outliers:
+        ch = torch.randn((1, w.n_kv_heads, 1, w.head_dim), generator=g, device=device,
+                         dtype=torch.float32).exp()
+        k = k * ch
+    return k.to(w.in_dtype), v.to(w.in_dtype)
+
+
+def queries(w: Workload, n_layers: int, device="cpu", seed_offset: int = 0,
+            batch: Optional[int] = None):
+    """q [n_layers, B, Hq, D] ~ N(0,1) in w.q_dtype."""
+    B = w.batch if batch is None else batch
+    g = generator(w.seed * 1000 + 999 + seed_offset, device)
+    q = torch.randn((n_layers, B, w.n_q_heads, w.head_dim), generator=g, device=device,
+                    dtype=torch.float32)
+    return q.to(w.q_dtype)
+
+
+def keep_positions(w: Workload, layer: int, device="cpu", batch: Optional[int] = None,
+                   tokens: Optional[int] = None, keep: Optional[int] = None):
+    """Sorted kept positions [B, Hkv, keep] (int32): a seeded uniform subset of
+    size keep of range(T) per (sequence, KV head)."""
+    B = w.batch if batch is None else batch
+    T = w.tokens if tokens is None else tokens
+    K = w.keep_tokens if keep is None else keep
+    g = generator(w.seed * 1000 + 500 + layer, device)
+    r = torch.rand((B, w.n_kv_heads, T), generator=g, device=device)
+    idx = torch.topk(r, K, dim=-1).indices
+    return torch.sort(idx, dim=-1).values.to(torch.int32)
