@@ -1,0 +1,144 @@
+// Device-side helpers of libkvk for gfx950: vector types, exact code unpacking,
+// and the block layout of include/kvk.h (which the write kernel produces and the
+// decode and dequantise kernels consume).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvkd {
+
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+
+template <typename To, typename From>
+__device__ __forceinline__ To bitcast(const From& x) {
+  static_assert(sizeof(To) == sizeof(From), "size mismatch");
+  return __builtin_bit_cast(To, x);
+}
+
+__device__ __forceinline__ half8 cat4(half2v a, half2v b, half2v c, half2v d) {
+  u4v r = {bitcast<uint32_t>(a), bitcast<uint32_t>(b), bitcast<uint32_t>(c), bitcast<uint32_t>(d)};
+  return bitcast<half8>(r);
+}
+
+__device__ __forceinline__ half2v h2(float a, float b) {
+  half2v r = {(_Float16)a, (_Float16)b};
+  return r;
+}
+
+__device__ __forceinline__ half2v h2s(float a) { return h2(a, a); }
+
+// fp16 1024 + n has the integer n (n < 1024) in its low mantissa bits.
+constexpr uint32_t kMagic = 0x64006400u;
+
+// b = 4: one 32-bit chunk, slot s at bit 16*(s%2) + 4*(s/2).  Returns the 8 codes
+// minus `off` as exact fp16 integers, slot pairs (0,1),(2,3),(4,5),(6,7).
+__device__ __forceinline__ half8 unpack4(uint32_t w, float off) {
+  const uint32_t w8 = w >> 8;
+  half2v a = bitcast<half2v>((w & 0x000F000Fu) | kMagic);   // 1024 + u
+  half2v b = bitcast<half2v>((w & 0x00F000F0u) | kMagic);   // 1024 + 16 u
+  half2v c = bitcast<half2v>((w8 & 0x000F000Fu) | kMagic);
+  half2v d = bitcast<half2v>((w8 & 0x00F000F0u) | kMagic);
+  const half2v lo = h2s(-1024.0f - off);
+  const half2v sx = h2s(0.0625f), hi = h2s(-64.0f - off);
+  a = a + lo;
+  c = c + lo;
+  b = __builtin_elementwise_fma(b, sx, hi);  // (1024 + 16u)/16 - 64 - off, exact
+  d = __builtin_elementwise_fma(d, sx, hi);
+  return cat4(a, b, c, d);
+}
+
+// b = 2: one 32-bit word holds two chunks (even chunk at bits 2*(s/2), odd chunk
+// 8 bits higher), slot s at bit 16*(s%2) + 2*(s/2) [+ 8].
+__device__ __forceinline__ half8 unpack2_half(uint32_t w, float off) {
+  half2v r[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const float scale = 1.0f / (float)(1 << (2 * v));
+    half2v x = bitcast<half2v>((w & (0x00030003u << (2 * v))) | kMagic);  // 1024 + u*4^v
+    r[v] = __builtin_elementwise_fma(x, h2s(scale), h2s(-1024.0f * scale - off));
+  }
+  return cat4(r[0], r[1], r[2], r[3]);
+}
+
+__device__ __forceinline__ void unpack2(uint32_t w, float off, half8& even, half8& odd) {
+  even = unpack2_half(w, off);
+  odd = unpack2_half(w >> 8, off);
+}
+
+// b = 8: two 32-bit words, slot s is byte s.
+__device__ __forceinline__ half8 unpack8(uint32_t a, uint32_t b, float off) {
+  const uint32_t M = 0x64646464u;
+  const half2v lo = h2s(-1024.0f - off);
+  half2v r0 = bitcast<half2v>(__builtin_amdgcn_perm(M, a, 0x04010400u)) + lo;
+  half2v r1 = bitcast<half2v>(__builtin_amdgcn_perm(M, a, 0x04030402u)) + lo;
+  half2v r2 = bitcast<half2v>(__builtin_amdgcn_perm(M, b, 0x04010400u)) + lo;
+  half2v r3 = bitcast<half2v>(__builtin_amdgcn_perm(M, b, 0x04030402u)) + lo;
+  return cat4(r0, r1, r2, r3);
+}
+
+// ---------------------------------------------------------------------------
+// Block layout (bytes from the start of a 32-token block).
+// ---------------------------------------------------------------------------
+
+__host__ __device__ inline int64_t block_bytes(int D, int bits, int kivi) {
+  if (bits == 16) return 128LL * D;
+  return kivi ? 8LL * D * (bits + 1) : 8LL * D * bits + 128;
+}
+
+// Bit address of the K code of (token t, channel c) in a quantised block.
+__device__ __forceinline__ int64_t k_code_bit(int D, int bits, int t, int c) {
+  const int tau = t >> 4, i = t & 15, j = c >> 5, kg = (c & 31) >> 3, s = c & 7;
+  const int lam = 16 * kg + i;
+  const int64_t chunk = 2LL * D * bits * tau + (int64_t)lam * (D * bits / 32) + j * bits;
+  if (bits == 8) return 8 * chunk + 8 * s;
+  if (bits == 4) return 8 * chunk + 16 * (s & 1) + 4 * (s >> 1);
+  return 8 * (chunk - (j & 1) * 2) + 16 * (s & 1) + 2 * (s >> 1) + 8 * (j & 1);
+}
+
+// Bit address of the V code of (token t, channel c) in a quantised block.
+__device__ __forceinline__ int64_t v_code_bit(int D, int bits, int t, int c) {
+  const int i = c & 15, m = c >> 4, kg = (t & 15) >> 2, s = 4 * (t >> 4) + (t & 3);
+  const int lam = 16 * kg + i;
+  const int64_t chunk = 4LL * D * bits + (int64_t)lam * (D * bits / 16) + m * bits;
+  if (bits == 8) return 8 * chunk + 8 * s;
+  if (bits == 4) return 8 * chunk + 16 * (s & 1) + 4 * (s >> 1);
+  return 8 * (chunk - (m & 1) * 2) + 16 * (s & 1) + 2 * (s >> 1) + 8 * (m & 1);
+}
+
+// Byte address of the bf16 K / V value of (t, c) in a bf16 block.
+__device__ __forceinline__ int k_bf16_byte(int D, int t, int c) {
+  const int tau = t >> 4, i = t & 15, j = c >> 5, kg = (c & 31) >> 3, s = c & 7;
+  return 32 * D * tau + (16 * kg + i) * (D / 2) + 16 * j + 2 * s;
+}
+__device__ __forceinline__ int v_bf16_byte(int D, int t, int c) {
+  const int i = c & 15, m = c >> 4, kg = (t & 15) >> 2, s = 4 * (t >> 4) + (t & 3);
+  return 64 * D + (16 * kg + i) * D + 16 * m + 2 * s;
+}
+
+// Index (in fp16 units) of the KIVI32 V-meta entry w (0 scale, 1 zero) of
+// (token t, channel group g).
+__device__ __forceinline__ int v_meta_index(int t, int g, int w) {
+  const int kg = (t & 15) >> 2, s = 4 * (t >> 4) + (t & 3);
+  return ((g * 2 + w) * 4 + kg) * 8 + s;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float((uint32_t)b << 16);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float x) {
+  __bf16 h = (__bf16)x;  // round to nearest even
+  return bitcast<uint16_t>(h);
+}
+
+__device__ __forceinline__ float f16_bits_to_f32(uint16_t b) {
+  return (float)bitcast<_Float16>(b);
+}
+
+}  // namespace kvkd

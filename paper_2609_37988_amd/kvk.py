@@ -1,0 +1,271 @@
+"""Python binding of libkvk (ctypes): argument marshalling only.
+
+Every function here calls the C ABI of include/kvk.h with the same name minus
+the `kvk_` prefix.  Device buffers are torch tensors on the current HIP device;
+the binding passes their data pointers and the current stream.  All compute runs
+in the library's HIP kernels.  If libkvk.so has not been built, loading fails
+with an error (there is no fallback path).
+"""
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libkvk.so")
+MAX_LAYERS = 64
+
+OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_DEVICE, ERR_BUFFER = 0, -1, -2, -3, -4
+GQA, MLA = 0, 1
+KIVI32, SYMROW = 0, 1
+BF16, F32 = 0, 1
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "kind", "n_layers", "n_q_heads", "n_kv_heads", "head_dim", "latent_dim", "rope_dim",
+        "nope_dim", "v_dim", "qscheme", "batch", "max_tokens", "keep_tokens")]
+
+
+class Action(ctypes.Structure):
+    _fields_ = [("inherit", ctypes.c_int32), ("bits", ctypes.c_int32), ("rank", ctypes.c_int32)]
+
+
+class TableInfo(ctypes.Structure):
+    _fields_ = [
+        ("arena_bytes", ctypes.c_int64), ("workspace_bytes", ctypes.c_int64),
+        ("n_anchors", ctypes.c_int32), ("stored_tokens_cap", ctypes.c_int32),
+        ("cost_bits_per_token", ctypes.c_double), ("c0_bits_per_token", ctypes.c_double),
+        ("rho", ctypes.c_double), ("rho_realized", ctypes.c_double),
+        ("anchor_of", ctypes.c_int32 * MAX_LAYERS), ("layer_offset", ctypes.c_int64 * MAX_LAYERS),
+        ("layer_bytes", ctypes.c_int64 * MAX_LAYERS), ("stream_bytes", ctypes.c_int64 * MAX_LAYERS),
+        ("layer_cost_bits", ctypes.c_double * MAX_LAYERS),
+        ("layer_bits_per_elt", ctypes.c_double * MAX_LAYERS),
+    ]
+
+
+class KvkError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"kvk status {status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libkvk.so (built in-tree by paper_2609_37988_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2609_37988_amd.build`")
+        lib = ctypes.CDLL(LIB_PATH)
+        P, I32, I64, F = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+        sig = {
+            "kvk_layer_table": (I32, [ctypes.POINTER(Dims), ctypes.POINTER(Action), ctypes.POINTER(P)]),
+            "kvk_table_query": (I32, [P, ctypes.POINTER(TableInfo)]),
+            "kvk_table_destroy": (None, [P]),
+            "kvk_workspace_bytes": (I32, [P, I32, I32, ctypes.POINTER(ctypes.c_size_t)]),
+            "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
+            "kvk_decode_attention": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P, ctypes.c_size_t, P]),
+            "kvk_debug_dequantize": (I32, [P, I32, I32, P, P, P, P]),
+            "kvk_realized_bits": (ctypes.c_double, [I32, I32, I32, I64, I64]),
+            "kvk_rho_range": (I32, [I32, I32, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_double),
+                                    ctypes.POINTER(ctypes.c_double)]),
+            "kvk_last_error": (ctypes.c_char_p, []),
+            "kvk_version": (ctypes.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def exported_symbols() -> List[str]:
+    """Names of the C entry points the binding expects libkvk to export."""
+    return ["kvk_layer_table", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
+            "kvk_compress_layer", "kvk_decode_attention", "kvk_debug_dequantize",
+            "kvk_realized_bits", "kvk_rho_range", "kvk_last_error", "kvk_version"]
+
+
+def last_error() -> str:
+    return load().kvk_last_error().decode()
+
+
+def version() -> str:
+    return load().kvk_version().decode()
+
+
+def _check(st: int):
+    if st != OK:
+        raise KvkError(st, last_error())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+@dataclass
+class Info:
+    arena_bytes: int
+    workspace_bytes: int
+    n_anchors: int
+    stored_tokens_cap: int
+    cost_bits_per_token: float
+    c0_bits_per_token: float
+    rho: float
+    rho_realized: float
+    anchor_of: List[int]
+    layer_offset: List[int]
+    layer_bytes: List[int]
+    stream_bytes: List[int]
+    layer_cost_bits: List[float]
+    layer_bits_per_elt: List[float]
+
+
+class Table:
+    """Owning handle of a kvk_table."""
+
+    def __init__(self, handle: ctypes.c_void_p, dims: Dims, plan: Sequence[Action]):
+        self._h = handle
+        self.dims = dims
+        self.plan = list(plan)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def __del__(self):
+        if getattr(self, "_h", None) and _lib is not None:
+            _lib.kvk_table_destroy(self._h)
+            self._h = None
+
+
+def make_dims(kind=GQA, n_layers=1, n_q_heads=1, n_kv_heads=1, head_dim=128, latent_dim=0,
+              rope_dim=0, nope_dim=0, v_dim=0, qscheme=KIVI32, batch=1, max_tokens=1,
+              keep_tokens=0) -> Dims:
+    return Dims(kind, n_layers, n_q_heads, n_kv_heads, head_dim, latent_dim, rope_dim, nope_dim,
+                v_dim, qscheme, batch, max_tokens, keep_tokens)
+
+
+def make_plan(entries: Sequence[tuple]) -> List[Action]:
+    """entries: (inherit, bits) or (inherit, bits, rank) per layer."""
+    out = []
+    for e in entries:
+        inherit, bits = int(e[0]), int(e[1])
+        rank = int(e[2]) if len(e) > 2 else 0
+        out.append(Action(inherit, bits, rank))
+    return out
+
+
+def layer_table(dims: Dims, plan: Sequence[Action]) -> Table:
+    lib = load()
+    arr = (Action * max(1, len(plan)))(*plan)
+    h = ctypes.c_void_p()
+    _check(lib.kvk_layer_table(ctypes.byref(dims), arr, ctypes.byref(h)))
+    return Table(h, dims, plan)
+
+
+def table_query(t: Table) -> Info:
+    inf = TableInfo()
+    _check(load().kvk_table_query(t.handle, ctypes.byref(inf)))
+    L = t.dims.n_layers
+    return Info(inf.arena_bytes, inf.workspace_bytes, inf.n_anchors, inf.stored_tokens_cap,
+                inf.cost_bits_per_token, inf.c0_bits_per_token, inf.rho, inf.rho_realized,
+                list(inf.anchor_of[:L]), list(inf.layer_offset[:L]), list(inf.layer_bytes[:L]),
+                list(inf.stream_bytes[:L]), list(inf.layer_cost_bits[:L]),
+                list(inf.layer_bits_per_elt[:L]))
+
+
+def workspace_bytes(t: Table, layer_begin: int, layer_end: int) -> int:
+    out = ctypes.c_size_t()
+    _check(load().kvk_workspace_bytes(t.handle, layer_begin, layer_end, ctypes.byref(out)))
+    return out.value
+
+
+def _dtype_code(x: torch.Tensor) -> int:
+    if x.dtype == torch.bfloat16:
+        return BF16
+    if x.dtype == torch.float32:
+        return F32
+    raise TypeError(f"unsupported dtype {x.dtype}")
+
+
+def _nbytes(x) -> int:
+    return x.numel() * x.element_size()
+
+
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def compress_layer(t: Table, layer: int, k: torch.Tensor, v: torch.Tensor, n_tokens: int,
+                   keep_idx: Optional[torch.Tensor], arena: torch.Tensor, stream=None):
+    """k, v: [B, Hkv, n_tokens, d_h] contiguous bf16/fp32 on the device."""
+    d = t.dims
+    _need(k.dtype == v.dtype and k.is_contiguous() and v.is_contiguous(),
+          "k and v must be contiguous tensors of one dtype")
+    _need(k.numel() == v.numel() == d.batch * d.n_kv_heads * n_tokens * d.head_dim,
+          "k/v size must be B*Hkv*n_tokens*d_h")
+    if keep_idx is not None:
+        _need(keep_idx.dtype == torch.int32 and keep_idx.is_contiguous(),
+              "keep_idx must be a contiguous int32 tensor")
+        _need(keep_idx.numel() == d.batch * d.n_kv_heads * d.keep_tokens,
+              "keep_idx size must be B*Hkv*keep_tokens")
+    _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
+    _check(load().kvk_compress_layer(t.handle, layer, _ptr(k), _ptr(v), _dtype_code(k), n_tokens,
+                                     _ptr(keep_idx), _ptr(arena), _stream(stream)))
+
+
+def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_stored: int,
+                     scale: float, arena: torch.Tensor, out: torch.Tensor, workspace: torch.Tensor,
+                     w_uk: Optional[torch.Tensor] = None, w_uv: Optional[torch.Tensor] = None,
+                     stream=None):
+    """q: [layers, B, Hq, d_h] bf16/fp32; out: fp32 of the same shape."""
+    d = t.dims
+    rows = (layer_end - layer_begin) * d.batch * d.n_q_heads * d.head_dim
+    _need(q.is_contiguous() and out.is_contiguous() and out.dtype == torch.float32,
+          "q must be contiguous; out contiguous fp32")
+    _need(q.numel() == rows and out.numel() == rows, "q/out size must be layers*B*Hq*d_h")
+    _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
+    _check(load().kvk_decode_attention(
+        t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
+        _ptr(w_uk), _ptr(w_uv), _ptr(arena), _ptr(out), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def debug_dequantize(t: Table, layer: int, n_stored: int, arena: torch.Tensor, k_out: torch.Tensor,
+                     v_out: torch.Tensor, stream=None):
+    d = t.dims
+    n = d.batch * d.n_kv_heads * max(n_stored, 0) * d.head_dim
+    _need(k_out.dtype == torch.float32 and v_out.dtype == torch.float32, "outputs must be fp32")
+    _need(k_out.numel() >= n and v_out.numel() >= n, "outputs smaller than B*Hkv*n_stored*d_h")
+    _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
+    _check(load().kvk_debug_dequantize(t.handle, layer, n_stored, _ptr(arena), _ptr(k_out),
+                                       _ptr(v_out), _stream(stream)))
+
+
+def realized_bits(qscheme: int, bits: int, group: int, window: int, context: int) -> float:
+    return load().kvk_realized_bits(qscheme, bits, group, window, context)
+
+
+def rho_range(n_layers: int, kv_width: int, latent_dim: int, rope_dim: int, mla: bool,
+              precision: bool, rank: bool, depth: bool):
+    lo, hi = ctypes.c_double(), ctypes.c_double()
+    axes = (1 if precision else 0) | (2 if rank else 0) | (4 if depth else 0)
+    _check(load().kvk_rho_range(n_layers, kv_width, latent_dim, rope_dim, int(mla), axes,
+                                ctypes.byref(lo), ctypes.byref(hi)))
+    return lo.value, hi.value

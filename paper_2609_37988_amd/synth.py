@@ -141,3 +141,29 @@ def keep_positions(w: Workload, layer: int, device="cpu", batch: Optional[int] =
     r = torch.rand((B, w.n_kv_heads, T), generator=g, device=device)
     idx = torch.topk(r, K, dim=-1).indices
     return torch.sort(idx, dim=-1).values.to(torch.int32)
+
+
+def kv_random(seed: int, B: int, H: int, T: int, D: int, dtype=torch.bfloat16, outliers=True,
+              device="cpu", scale: float = 1.0):
+    """K, V [B, H, T, D]: N(0, scale^2) values, keys times a per-(head, channel)
+    LogNormal(0,1) factor when outliers."""
+    g = generator(seed, device)
+    k = torch.randn((B, H, T, D), generator=g, device=device) * scale
+    v = torch.randn((B, H, T, D), generator=g, device=device) * scale
+    if outliers:
+        k = k * torch.randn((1, H, 1, D), generator=g, device=device).exp()
+    return k.to(dtype), v.to(dtype)
+
+
+def q_random(seed: int, L: int, B: int, Hq: int, D: int, dtype=torch.bfloat16, device="cpu"):
+    """q [L, B, Hq, D] ~ N(0, 1)."""
+    g = generator(seed, device)
+    return torch.randn((L, B, Hq, D), generator=g, device=device).to(dtype)
+
+
+def keep_random(seed: int, B: int, H: int, T: int, keep: int, device="cpu"):
+    """Sorted kept positions [B, H, keep] (int32), a uniform subset per (b, h)."""
+    g = generator(seed, device)
+    r = torch.rand((B, H, T), generator=g, device=device)
+    idx = torch.topk(r, keep, dim=-1).indices
+    return torch.sort(idx, dim=-1).values.to(torch.int32)

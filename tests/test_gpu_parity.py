@@ -1,0 +1,194 @@
+"""GPU parity of the HIP path against the oracle, through the C ABI.
+
+Bit-exact: arena bytes (codes, metadata, bf16 blocks) and dequantised values.
+Attention outputs: max|diff| <= 2e-3 * max|out| (fp32 accumulation).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cache as OC
+from paper_2609_37988_amd import kvk, synth
+
+from gpu_common import TOL, Case, meaningful, oracle_rows, oracle_stream, rel_err, say
+
+pytestmark = pytest.mark.gpu
+
+
+def _np(x):
+    return x.detach().float().cpu().numpy()
+
+
+def _check_layer(case: Case, layer, k, v, n, keep=None):
+    """Bytes of every stream and the dequantised cache of `layer` against the oracle."""
+    bits = case.plan[layer].bits
+    kn, vn = _np(k), _np(v)
+    kd, vd = case.dequant(layer, n)
+    kd, vd = _np(kd), _np(vd)
+    for b in range(case.dims.batch):
+        for h in range(case.dims.n_kv_heads):
+            ks = None if keep is None else keep[b, h].cpu().numpy()
+            ref = oracle_stream(case.odims, bits, kn[b, h], vn[b, h], ks)
+            got = case.stream_bytes_host(layer, b, h)
+            assert np.array_equal(meaningful(case.odims, bits, got, n), meaningful(case.odims, bits, ref, n)), \
+                f"arena bytes differ (layer {layer}, b {b}, h {h})"
+            Kr, Vr = OC.dequant_stream(case.odims, bits, ref, n)
+            assert np.array_equal(kd[b, h], Kr) and np.array_equal(vd[b, h], Vr), "dequantised values differ"
+
+
+def _oracle_out(case: Case, layer_inputs, q, n, scale, keeps=None):
+    d = case.dims
+    G = d.n_q_heads // d.n_kv_heads
+    qn = _np(q).astype(np.float64)
+    out = np.zeros(qn.shape)
+    anc = case.info.anchor_of
+    for l in range(d.n_layers):
+        a = anc[l]
+        bits = case.plan[a].bits
+        kn, vn = layer_inputs[a]
+        for b in range(d.batch):
+            for h in range(d.n_kv_heads):
+                ks = None if keeps is None else keeps[a][b, h].cpu().numpy()
+                st = oracle_stream(case.odims, bits, kn[b, h], vn[b, h], ks)
+                out[l, b, h * G:(h + 1) * G] = oracle_rows(case.odims, bits, st, n, qn[l, b, h * G:(h + 1) * G], scale)
+    return out
+
+
+def test_tiny_int8_workload():
+    """1 layer, 4 query heads / 1 KV head, d_h 64, 256 tokens, fp32 K/V, KIVI32 int8."""
+    w = synth.workload(0)
+    say("case tiny-gqa-int8")
+    c = Case(1, 4, 1, 64, 1, 256, w.plan)
+    k, v = synth.kv_layer(w, 0)
+    c.compress(0, k.cuda(), v.cuda(), 256)
+    _check_layer(c, 0, k, v, 256)
+    q = synth.queries(w, 1)
+    out = _np(c.decode(q.cuda(), 256, w.softmax_scale()))
+    ref = _oracle_out(c, {0: (_np(k), _np(v))}, q, 256, w.softmax_scale())
+    assert rel_err(out, ref) <= TOL
+
+
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW], ids=["kivi32", "symrow"])
+@pytest.mark.parametrize("bits", [2, 4, 8, 16])
+@pytest.mark.parametrize("D", [64, 128])
+def test_single_layer_ragged(qs, bits, D):
+    """B 2, 2 KV heads, 3 query heads each, 200 tokens (6 full blocks + 8-token tail)."""
+    say(f"case single-layer qs={qs} bits={bits} D={D}")
+    n = 200
+    c = Case(1, 6, 2, D, 2, 224, [(0, bits)], qscheme=qs)
+    k, v = synth.kv_random(10 + bits + D, 2, 2, n, D)
+    c.compress(0, k.cuda(), v.cuda(), n)
+    _check_layer(c, 0, k, v, n)
+    q = synth.q_random(20 + bits, 1, 2, 6, D)
+    scale = 1.0 / np.sqrt(D)
+    out = _np(c.decode(q.cuda(), n, scale))
+    ref = _oracle_out(c, {0: (_np(k), _np(v))}, q, n, scale)
+    assert rel_err(out, ref) <= TOL, rel_err(out, ref)
+
+
+def _stack_case(qs=kvk.KIVI32):
+    # anchor 0 read by 3 layers (21 rows: two 16-row chunks), anchor 3 by 2, anchor 5 alone
+    plan = [(0, 4), (1, 16), (1, 16), (0, 2), (1, 16), (0, 16)]
+    c = Case(6, 28, 4, 128, 2, 160, plan, qscheme=qs)
+    n = 150
+    inputs = {}
+    for l in (0, 3, 5):
+        k, v = synth.kv_random(100 + l, 2, 4, n, 128)
+        c.compress(l, k.cuda(), v.cuda(), n)
+        c.compress(l + 1 if l < 5 else l, k.cuda(), v.cuda(), n)  # inheritors: no-op
+        inputs[l] = (_np(k), _np(v))
+    return c, inputs, n
+
+
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW], ids=["kivi32", "symrow"])
+def test_depth_stacking_and_invariants(qs):
+    say(f"case depth-stacking qs={qs}")
+    c, inputs, n = _stack_case(qs)
+    q = synth.q_random(7, 6, 2, 28, 128)
+    scale = 1.0 / np.sqrt(128)
+    out = c.decode(q.cuda(), n, scale)
+    ref = _oracle_out(c, inputs, q, n, scale)
+    assert rel_err(_np(out), ref) <= TOL
+    # determinism: a second call gives the same bits
+    assert torch.equal(out, c.decode(q.cuda(), n, scale))
+    # per-layer calls (each re-reads its anchor) equal the stacked call bit for bit
+    for l in range(6):
+        one = c.decode(q[l:l + 1].cuda(), n, scale, l, l + 1)
+        assert torch.equal(one[0], out[l]), f"layer {l}"
+    # an inheritor given its anchor's query reproduces the anchor's output exactly
+    q2 = q.clone()
+    q2[1] = q2[0]
+    q2[2] = q2[0]
+    q2[4] = q2[3]
+    o2 = c.decode(q2.cuda(), n, scale)
+    assert torch.equal(o2[1], o2[0]) and torch.equal(o2[2], o2[0]) and torch.equal(o2[4], o2[3])
+
+
+def test_ten_readers_four_chunks():
+    """One anchor read by 10 layers x 5 query heads = 50 rows (four 16-row chunks)."""
+    say("case ten-readers")
+    plan = [(0, 8)] + [(1, 16)] * 9
+    c = Case(10, 10, 2, 128, 1, 96, plan)
+    n = 96
+    k, v = synth.kv_random(55, 1, 2, n, 128)
+    c.compress(0, k.cuda(), v.cuda(), n)
+    q = synth.q_random(56, 10, 1, 10, 128)
+    out = _np(c.decode(q.cuda(), n, 0.1))
+    ref = _oracle_out(c, {0: (_np(k), _np(v))}, q, n, 0.1)
+    assert rel_err(out, ref) <= TOL
+
+
+@pytest.mark.parametrize("bits", [2, 4, 16])
+def test_eviction_gather(bits):
+    """Keep 150 of 300 positions per (b, KV head): the stored stream is the gathered one."""
+    say(f"case eviction bits={bits}")
+    n, keep = 300, 150
+    c = Case(1, 8, 2, 128, 2, n, [(0, bits)], keep=keep)
+    k, v = synth.kv_random(60 + bits, 2, 2, n, 128)
+    kidx = synth.keep_random(61, 2, 2, n, keep)
+    c.compress(0, k.cuda(), v.cuda(), n, kidx.cuda())
+    _check_layer(c, 0, k, v, keep, kidx)
+    q = synth.q_random(62, 1, 2, 8, 128)
+    out = _np(c.decode(q.cuda(), keep, 0.09))
+    ref = _oracle_out(c, {0: (_np(k), _np(v))}, q, keep, 0.09, {0: kidx})
+    assert rel_err(out, ref) <= TOL
+
+
+@pytest.mark.parametrize("n", [1, 31, 32, 33, 64])
+def test_edge_lengths(n):
+    say(f"case edge n={n}")
+    c = Case(2, 4, 1, 128, 1, 64, [(0, 4), (0, 16)])
+    ins = {}
+    for l in range(2):
+        k, v = synth.kv_random(70 + l + n, 1, 1, n, 128)
+        c.compress(l, k.cuda(), v.cuda(), n)
+        ins[l] = (_np(k), _np(v))
+        _check_layer(c, l, k, v, n)
+    q = synth.q_random(72, 2, 1, 4, 128)
+    out = _np(c.decode(q.cuda(), n, 0.088))
+    ref = _oracle_out(c, ins, q, n, 0.088)
+    assert rel_err(out, ref) <= TOL
+    if n == 1:  # a single stored token: the output is its (dequantised) value row
+        kd, vd = c.dequant(1, 1)
+        assert np.allclose(out[1, 0], _np(vd)[0, 0].repeat(4, 0), rtol=0, atol=1e-6)
+
+
+def test_empty_cache_gives_zeros():
+    say("case empty")
+    c = Case(1, 4, 1, 128, 1, 64, [(0, 4)])
+    q = synth.q_random(80, 1, 1, 4, 128)
+    out = c.decode(q.cuda(), 0, 0.1)
+    assert torch.count_nonzero(out).item() == 0
+
+
+@pytest.mark.parametrize("bits,n", [(16, 2100), (2, 6000), (8, 3000)])
+def test_many_splits(bits, n):
+    """Streams longer than one split: partials merged by log-sum-exp."""
+    say(f"case splits bits={bits} n={n}")
+    c = Case(1, 4, 1, 128, 1, n, [(0, bits)])
+    k, v = synth.kv_random(90 + bits, 1, 1, n, 128)
+    c.compress(0, k.cuda(), v.cuda(), n)
+    q = synth.q_random(91, 1, 1, 4, 128)
+    out = _np(c.decode(q.cuda(), n, 0.088))
+    ref = _oracle_out(c, {0: (_np(k), _np(v))}, q, n, 0.088)
+    assert rel_err(out, ref) <= TOL

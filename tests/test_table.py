@@ -1,0 +1,179 @@
+"""Host side of the C ABI (no GPU): exports, plan tables, accounting, error codes."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import plan as P
+from paper_2609_37988_amd import kvk, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _header_functions():
+    with open(os.path.join(ROOT, "include", "kvk.h")) as f:
+        text = f.read()
+    return sorted(set(re.findall(r"\b(kvk_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = kvk.load()
+    declared = _header_functions()
+    assert declared, "no declarations found"
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert set(declared) == set(kvk.exported_symbols())
+    assert "gfx950" in kvk.version()
+
+
+def _oracle_dims(d):
+    return P.Dims(d.kind, d.n_layers, d.n_q_heads, d.n_kv_heads, d.head_dim, qscheme=d.qscheme,
+                  batch=d.batch, max_tokens=d.max_tokens, keep_tokens=d.keep_tokens)
+
+
+def _table_for(w):
+    d = kvk.make_dims(kvk.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, qscheme=w.qscheme,
+                      batch=w.batch, max_tokens=w.tokens, keep_tokens=w.keep_tokens)
+    plan = kvk.make_plan(w.plan)
+    return d, plan, kvk.layer_table(d, plan)
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2, 4])
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW])
+def test_table_matches_oracle_accounting(cfg, qs):
+    w = synth.workload(cfg)
+    w.qscheme = qs
+    d, plan, t = _table_for(w)
+    inf = kvk.table_query(t)
+    od = _oracle_dims(d)
+    oplan = [P.Action(bool(a.inherit), a.bits) for a in plan]
+    assert P.validate(od, oplan) is None
+    assert inf.anchor_of == P.anchor_of(oplan)
+    offs, total = P.arena_offsets(od, oplan)
+    assert inf.layer_offset == offs and inf.arena_bytes == total
+    for l, a in enumerate(oplan):
+        if not a.inherit:
+            assert inf.layer_bytes[l] == P.layer_bytes(od, a.bits)
+            assert inf.stream_bytes[l] == P.stream_bytes(od, a.bits)
+        assert inf.layer_cost_bits[l] == P.cost_bits(od, a)
+    assert inf.rho == pytest.approx(P.rho(od, oplan), rel=1e-15)
+    alg = P.read_bytes(od, oplan, 0, od.n_layers, od.stored_cap)
+    assert inf.rho_realized == pytest.approx(P.bf16_full_bytes(od) / alg, rel=1e-12)
+    assert inf.n_anchors == sum(1 for a in oplan if not a.inherit)
+
+
+def test_headline_plans():
+    """The 14B-shaped 128k plan is 16x by eq. (2) (32x with half the positions kept);
+    the 14B-shaped mixed plan has 16 inheriting layers."""
+    w4 = synth.workload(4)
+    t4 = _table_for(w4)[2]
+    i4 = kvk.table_query(t4)
+    assert i4.rho == pytest.approx(16.0) and i4.n_anchors == 20
+    assert i4.rho * w4.tokens / w4.keep_tokens == pytest.approx(32.0)
+    w2 = synth.workload(2)
+    assert sum(e[0] for e in w2.plan) == 16 and w2.plan[0][0] == 0
+
+
+def _gold(name):
+    with open(os.path.join(ROOT, "tests", "golden", name)) as f:
+        return [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+
+
+def test_realized_bits_entry_point_matches_table():
+    for scheme, g, b, bpe, _ in _gold("realized_bits_table.txt"):
+        if scheme == "symrow":
+            got = kvk.realized_bits(kvk.SYMROW, int(b), int(g), 0, 2048)
+        else:
+            got = kvk.realized_bits(kvk.KIVI32, int(b), int(g), 128, 2048)
+        assert round(got, 3) == pytest.approx(float(bpe))
+    assert kvk.realized_bits(kvk.KIVI32, 3, 32, 0, 10) < 0
+
+
+AXES = {
+    "precision": (True, False, False), "depth": (False, False, True),
+    "depth+precision": (True, False, True), "rank": (False, True, False),
+    "rank+precision": (True, True, False), "depth+rank": (False, True, True),
+    "depth+rank+precision": (True, True, True),
+}
+
+
+def test_rho_range_entry_point_matches_table():
+    for row in _gold("ranges_table.txt"):
+        prec, rank, depth = AXES[row[0]]
+        mla = row[1] == "MLA"
+        for (L, width, r), cols in (((48, 2048, 1024), row[4:6]), ((36, 512, 256), row[7:9])):
+            lo, hi = kvk.rho_range(L, width, r, 64, mla, prec, rank, depth)
+            for got, printed in ((lo, cols[0]), (hi, cols[1])):
+                nd = len(printed.split(".")[1]) if "." in printed else 0
+                assert round(got, nd) == pytest.approx(float(printed))
+
+
+def _expect(status, fn, *args):
+    with pytest.raises(kvk.KvkError) as e:
+        fn(*args)
+    assert e.value.status == status, str(e.value)
+    assert kvk.last_error()
+
+
+def test_invalid_plans_and_dims():
+    good = kvk.make_dims(kvk.GQA, 3, 8, 2, 128, batch=2, max_tokens=100)
+    ok_plan = kvk.make_plan([(0, 4), (1, 16), (0, 2)])
+    kvk.layer_table(good, ok_plan)
+    _expect(kvk.ERR_INVALID, kvk.layer_table, good, kvk.make_plan([(1, 16), (0, 4), (0, 4)]))
+    _expect(kvk.ERR_INVALID, kvk.layer_table, good, kvk.make_plan([(0, 3), (0, 4), (0, 4)]))
+    _expect(kvk.ERR_INVALID, kvk.layer_table, good, kvk.make_plan([(0, 4, 256), (0, 4), (0, 4)]))
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, kvk.make_dims(kvk.MLA, 3, 8, 2, 128, 512, 64, 128, 128,
+                                                                batch=1, max_tokens=8), ok_plan)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, kvk.make_dims(kvk.GQA, 3, 8, 2, 96, max_tokens=8), ok_plan)
+    _expect(kvk.ERR_INVALID, kvk.layer_table, kvk.make_dims(kvk.GQA, 3, 6, 4, 128, max_tokens=8), ok_plan)
+    _expect(kvk.ERR_INVALID, kvk.layer_table,
+            kvk.make_dims(kvk.GQA, 3, 8, 2, 128, max_tokens=8, keep_tokens=9), ok_plan)
+    _expect(kvk.ERR_INVALID, kvk.layer_table, kvk.make_dims(kvk.GQA, 0, 8, 2, 128, max_tokens=8), ok_plan)
+    # 17 layers sharing one anchor with 4 query heads per KV head: 68 rows > 64
+    d17 = kvk.make_dims(kvk.GQA, 17, 8, 2, 128, max_tokens=8)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, d17, kvk.make_plan([(0, 4)] + [(1, 16)] * 16))
+
+
+def _raw(status, name, *args):
+    lib = kvk.load()
+    assert getattr(lib, name)(*args) == status, kvk.last_error()
+    if status != kvk.OK:
+        assert kvk.last_error()
+
+
+def test_entry_points_reject_bad_arguments_without_launching():
+    """Validation happens on the host before any launch: these calls pass non-null
+    dummy pointers that no kernel ever sees."""
+    d = kvk.make_dims(kvk.GQA, 2, 4, 1, 64, batch=1, max_tokens=64)
+    t = kvk.layer_table(d, kvk.make_plan([(0, 8), (1, 16)]))
+    h, P = t.handle, ctypes.c_void_p
+    f = P(256)
+    I, B = kvk.ERR_INVALID, kvk.ERR_BUFFER
+    _raw(I, "kvk_compress_layer", h, 5, f, f, kvk.BF16, 64, None, f, None)     # layer
+    _raw(I, "kvk_compress_layer", h, 0, f, f, kvk.BF16, 65, None, f, None)     # n_tokens
+    _raw(I, "kvk_compress_layer", h, 0, f, f, kvk.BF16, 64, f, f, None)        # keep without eviction
+    _raw(I, "kvk_compress_layer", h, 0, None, f, kvk.BF16, 64, None, f, None)  # NULL input
+    _raw(I, "kvk_compress_layer", h, 0, f, f, 7, 64, None, f, None)            # dtype
+    _raw(kvk.OK, "kvk_compress_layer", h, 1, f, f, kvk.BF16, 64, None, f, None)  # inheritor: no-op
+    _raw(I, "kvk_decode_attention", h, 1, 1, f, kvk.BF16, 64, 0.1, None, None, f, f, f, 1 << 20, None)
+    _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 65, 0.1, None, None, f, f, f, 1 << 20, None)
+    _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, 0.1, f, None, f, f, f, 1 << 20, None)
+    _raw(I, "kvk_decode_attention", h, 0, 2, P(264), kvk.BF16, 64, 0.1, None, None, f, f, f, 1 << 20, None)
+    _raw(B, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, 0.1, None, None, f, f, f, 16, None)
+    _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, float("nan"), None, None, f, f, f, 1 << 20, None)
+    _raw(I, "kvk_debug_dequantize", h, 0, 65, f, f, f, None)
+    assert kvk.workspace_bytes(t, 0, 2) > 0
+
+
+def test_binding_rejects_mis_sized_tensors():
+    import torch
+    d = kvk.make_dims(kvk.GQA, 1, 4, 1, 64, batch=1, max_tokens=64)
+    t = kvk.layer_table(d, kvk.make_plan([(0, 8)]))
+    k = torch.zeros(1, 1, 63, 64, dtype=torch.bfloat16)
+    arena = torch.zeros(16, dtype=torch.uint8)
+    with pytest.raises(ValueError):
+        kvk.compress_layer(t, 0, k, k, 64, None, arena)
+    q = torch.zeros(1, 1, 4, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        kvk.decode_attention(t, 0, 1, q, 64, 0.1, arena, torch.zeros(1, 1, 4, 63), arena)
