@@ -1,0 +1,220 @@
+"""Decode-attention benchmark over a per-layer compressed KV cache on one MI355X.
+
+Workload (default): the Qwen2.5-14B-shaped mixed stack — 48 layers, 40 query /
+8 KV heads, head dim 128, batch 32, context 8192, a seeded plan with 16 layers
+inheriting an earlier anchor's cache and anchor precisions drawn from
+{bf16, int8, int4, int2} (KIVI32 grouped quantisation).  Synthetic seeded inputs
+of that shape (keys with per-channel log-normal outliers).
+
+A step is one decode step over all 48 layers: the split attention kernel (D1)
+and the log-sum-exp merge (C1).  The cache is written once beforehand by the
+prefill kernel (W1), which is timed separately and reported under
+"prefill_write".  `value` is algorithmic compressed-cache bytes read per step
+(each distinct anchor once) divided by the step time, with everything resident
+in HBM.  The CPU baseline is the oracle (test infrastructure) timed on a bounded
+sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode-attention cache GB/s (% of HBM peak) and µs/step, 14B-shaped b=32 ctx=8k"
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--config", type=int, default=2)
+    ap.add_argument("--variant", default=None)
+    ap.add_argument("--qscheme", default="kivi32", choices=["kivi32", "symrow"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=0, help="layers in the CPU sample (0: auto)")
+    return ap.parse_args()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, table, n_stored, scale, n_layers_sample):
+    """Time the oracle's decode (dequantise + fp64 attention) for batch element 0
+    over the first n_layers_sample layers; inputs drawn on the CPU with the same
+    recipe and compressed by the oracle beforehand (untimed)."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    from oracle import attention as OA
+    from oracle import cache as OC
+    from oracle import plan as OP
+    from paper_2609_37988_amd import kvk, synth
+
+    d = table.dims
+    od = OP.Dims(OP.GQA, d.n_layers, d.n_q_heads, d.n_kv_heads, d.head_dim, qscheme=d.qscheme,
+                 batch=1, max_tokens=d.max_tokens, keep_tokens=d.keep_tokens)
+    info = kvk.table_query(table)
+    anc = info.anchor_of[:n_layers_sample]
+    G = d.n_q_heads // d.n_kv_heads
+    streams = {}
+    for a in sorted(set(anc)):
+        k, v = synth.kv_layer(w, a, device="cpu", batch=1)
+        keep = None
+        if w.keep_tokens:
+            keep = synth.keep_positions(w, a, device="cpu", batch=1).numpy()
+        kn, vn = k.float().numpy(), v.float().numpy()
+        bits = w.plan[a][1]
+        for h in range(d.n_kv_heads):
+            kk, vv = kn[0, h], vn[0, h]
+            if keep is not None:
+                kk, vv = OC.gather_kept(kk, keep[0, h]), OC.gather_kept(vv, keep[0, h])
+            streams[(a, h)] = (bits, OC.compress_stream(od, bits, kk, vv))
+    q = synth.queries(w, n_layers_sample, device="cpu", batch=1).float().numpy().astype(np.float64)
+    t0 = time.perf_counter()
+    for l in range(n_layers_sample):
+        for h in range(d.n_kv_heads):
+            bits, st = streams[(anc[l], h)]
+            K, V = OC.dequant_stream(od, bits, st, n_stored)
+            OA.softmax_attention(q[l, 0, h * G:(h + 1) * G], K, V, scale)
+    dt = time.perf_counter() - t0
+    sample_bytes = kvk.read_bytes(table, 0, n_layers_sample, n_stored) // d.batch
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"batch element 0 of {d.batch}, layers 0..{n_layers_sample - 1} "
+                      f"({len(set(anc))} anchors x {d.n_kv_heads} KV heads), {n_stored} tokens: "
+                      f"{sample_bytes} algorithmic bytes in {dt:.2f} s (numpy fp64 oracle; "
+                      f"elementwise work single-threaded, BLAS threads = cores)",
+            "seconds": round(dt, 3)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for {args.gpus}); "
+              "the design for sharding is described in DESIGN.md.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2609_37988_amd import kvk, synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.workload(args.config, args.variant)
+    if args.qscheme == "symrow":
+        w.qscheme = kvk.SYMROW
+    n_tok = w.tokens
+    n_stored = w.keep_tokens if w.keep_tokens else n_tok
+    dims = kvk.make_dims(kvk.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, qscheme=w.qscheme,
+                         batch=w.batch, max_tokens=n_tok, keep_tokens=w.keep_tokens)
+    table = kvk.layer_table(dims, kvk.make_plan(w.plan))
+    info = kvk.table_query(table)
+    log(f"workload {w.name}: arena {info.arena_bytes / 1e9:.2f} GB, rho eq.(2) {info.rho:.2f}, "
+        f"realized {info.rho_realized:.2f}, anchors {info.n_anchors}")
+    arena = torch.empty(info.arena_bytes, dtype=torch.uint8, device=dev)
+
+    # ---- prefill write (W1), timed per anchor layer ----
+    w1_ms, w1_bytes = 0.0, 0
+    for l in range(w.n_layers):
+        if w.plan[l][0]:
+            continue
+        k, v = synth.kv_layer(w, l, device=dev)
+        keep = synth.keep_positions(w, l, device=dev) if w.keep_tokens else None
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        kvk.compress_layer(table, l, k, v, n_tok, keep, arena)
+        e1.record()
+        torch.cuda.synchronize()
+        w1_ms += e0.elapsed_time(e1)
+        w1_bytes += 2 * k.numel() * k.element_size() * n_stored // n_tok + info.layer_bytes[l]
+        del k, v, keep
+    torch.cuda.empty_cache()
+    log(f"prefill write: {w1_ms:.1f} ms over {info.n_anchors} anchors")
+
+    qs = [synth.queries(w, w.n_layers, device=dev, seed_offset=i) for i in range(2)]
+    out = torch.empty((w.n_layers, w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device=dev)
+    ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=dev)
+    scale = w.softmax_scale()
+    alg = kvk.read_bytes(table, 0, w.n_layers, n_stored)
+
+    for i in range(args.warmup):
+        kvk.decode_attention(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, out, ws)
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for i in range(K):
+        ev[i][0].record()
+        kvk.decode_splits(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, ws)
+        ev[i][1].record()
+        kvk.decode_merge(table, 0, w.n_layers, n_stored, ws, out)
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / K
+    d1_ms = [a.elapsed_time(b) for a, b in ev]
+    d1_avg = float(np.mean(d1_ms))
+    gbs = alg / (ms_step * 1e-3) / 1e9
+    d1_gbs = alg / (d1_avg * 1e-3) / 1e9
+    log(f"step {ms_step * 1e3:.1f} us, {gbs:.1f} GB/s ({100 * gbs / HBM_PEAK_GBS:.1f}% of HBM); "
+        f"D1 {d1_avg * 1e3:.1f} us ({d1_gbs:.1f} GB/s)")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        nl = args.cpu_layers or (24 if args.config in (1, 2) else 4)
+        cpu = cpu_baseline(w, table, n_stored, scale, nl)
+        log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
+
+    bits_mix = {}
+    for e in w.plan:
+        if not e[0]:
+            bits_mix[str(e[1])] = bits_mix.get(str(e[1]), 0) + 1
+    line = {
+        "metric": METRIC,
+        "value": round(gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "us_per_step": round(ms_step * 1e3, 2),
+        "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u2/u4/u8 codes + bf16 cache; f16/bf16 MFMA, f32 accumulate",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "layers": w.n_layers, "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads,
+            "head_dim": w.head_dim, "batch": w.batch, "context": n_tok, "stored_tokens": n_stored,
+            "qscheme": "KIVI32" if w.qscheme == kvk.KIVI32 else "SYMROW",
+            "anchors_by_bits": bits_mix, "inheriting_layers": sum(e[0] for e in w.plan),
+            "rho_eq2": round(info.rho, 3), "rho_realized": round(info.rho_realized, 3),
+            "alg_bytes_per_step": alg,
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "gqa_decode_kernel (D1)", "achieved": round(d1_gbs, 2),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(d1_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None, "launch_us": round(d1_avg * 1e3, 2), "bytes_per_launch": alg,
+        },
+        "cpu_baseline": cpu,
+        "prefill_write": {"ms": round(w1_ms, 3), "bytes": w1_bytes,
+                          "GB_per_s": round(w1_bytes / (w1_ms * 1e-3) / 1e9, 2)},
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -226,6 +226,27 @@ kvk_status kvk_decode_attention(const kvk_table* table, int32_t layer_begin, int
                                 float* out, void* workspace, size_t workspace_bytes,
                                 hipStream_t stream);
 
+/* The two phases of kvk_decode_attention, for callers that schedule or time them
+ * separately.  kvk_decode_splits runs the per-split attention (arguments as for
+ * kvk_decode_attention) and leaves the split partials in `workspace`;
+ * kvk_decode_merge then merges them by log-sum-exp into `out`.  The merge must use
+ * the same table, layer range, n_stored and workspace as the splits call before
+ * it on the same stream.  Errors as for kvk_decode_attention. */
+kvk_status kvk_decode_splits(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
+                             const void* q, int32_t q_dtype, int32_t n_stored, float scale,
+                             const void* w_uk, const void* w_uv, const void* arena,
+                             void* workspace, size_t workspace_bytes, hipStream_t stream);
+kvk_status kvk_decode_merge(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
+                            int32_t n_stored, const void* workspace, size_t workspace_bytes,
+                            float* out, hipStream_t stream);
+
+/* Algorithmic bytes one decode call over [layer_begin, layer_end) reads from the
+ * arena with n_stored tokens per stream: each distinct anchor's full blocks and
+ * bf16 tail tokens, counted once (split partials, queries and outputs excluded).
+ * Host only. */
+kvk_status kvk_read_bytes(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
+                          int32_t n_stored, int64_t* out_bytes);
+
 /* Test support: dequantise the cache read by `layer` (its anchor's) into fp32
  * k_out, v_out [B][Hkv][n_stored][d_h], using the rules above bit for bit. */
 kvk_status kvk_debug_dequantize(const kvk_table* table, int32_t layer, int32_t n_stored,

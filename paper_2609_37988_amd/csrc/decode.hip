@@ -45,9 +45,9 @@ struct DecodeItem {
   int32_t geff;          // query rows: G * readers
   int32_t nsplit;
   int32_t split_blocks;
-  int32_t wave_begin;    // first wave of this item within its launch
+  int32_t wave_begin;    // first wave of this item within the launch (a multiple of 4)
   int32_t ws_off;        // float offset of the item's partials
-  int32_t pad;
+  int32_t nchp;          // waves per (stream, split): 16-row chunks, padded to 1, 2 or 4
 };
 
 struct DecodeArgs {
@@ -437,7 +437,7 @@ __device__ __forceinline__ void run_stream(Unit<D, NCH>& u, const uint8_t* strea
   }
 }
 
-template <int D, int NCH, bool KIVI>
+template <int D, bool KIVI>
 __global__ __launch_bounds__(256) void gqa_decode_kernel(DecodeArgs a) {
   constexpr int NJ = D / 32, NM = D / 16;
   const int lane = threadIdx.x & 63;
@@ -447,19 +447,21 @@ __global__ __launch_bounds__(256) void gqa_decode_kernel(DecodeArgs a) {
   while (ii + 1 < a.n_items && a.items[ii + 1].wave_begin <= wave) ++ii;
   const DecodeItem& it = a.items[ii];
   const int local = wave - it.wave_begin;
-  const int split = local % it.nsplit;
-  const int sidx = local / it.nsplit;  // b * Hkv + kvh
+  const int chunk = local % it.nchp;
+  const int unit = local / it.nchp;
+  if (unit >= a.B * a.Hkv * it.nsplit || 16 * chunk >= it.geff) return;  // alignment padding
+  const int split = unit % it.nsplit;
+  const int sidx = unit / it.nsplit;  // b * Hkv + kvh
   const int b = sidx / a.Hkv, kvh = sidx % a.Hkv;
   const int i16 = lane & 15, kg = lane >> 4;
+  const int row = 16 * chunk + i16;  // query row of this lane: (reader layer, head in group)
 
-  Unit<D, NCH> u;
+  Unit<D, 1> u;
+  u.m[0] = -INFINITY;
+  u.l[0] = 0.0f;
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    u.m[c] = -INFINITY;
-    u.l[c] = 0.0f;
-#pragma unroll
-    for (int mt = 0; mt < NM; ++mt) u.o[c][mt] = f4{0.f, 0.f, 0.f, 0.f};
-    const int row = 16 * c + i16;
+  for (int mt = 0; mt < NM; ++mt) u.o[0][mt] = f4{0.f, 0.f, 0.f, 0.f};
+  {
     const bool valid = row < it.geff;
     const int r = row / a.G, gh = row % a.G;
     const int64_t qrow = (((int64_t)(it.q_layer0 + r) * a.B + b) * a.Hq + kvh * a.G + gh) * D;
@@ -468,19 +470,19 @@ __global__ __launch_bounds__(256) void gqa_decode_kernel(DecodeArgs a) {
       const int ch = 32 * j + 8 * kg;
       if (!valid) {
 #pragma unroll
-        for (int s = 0; s < 8; ++s) u.q[c][j][s] = 0.0f;
+        for (int s = 0; s < 8; ++s) u.q[0][j][s] = 0.0f;
       } else if (a.q_f32) {
         const float4* qp = reinterpret_cast<const float4*>(static_cast<const float*>(a.q) + qrow + ch);
         const float4 v0 = qp[0], v1 = qp[1];
-        u.q[c][j][0] = v0.x; u.q[c][j][1] = v0.y; u.q[c][j][2] = v0.z; u.q[c][j][3] = v0.w;
-        u.q[c][j][4] = v1.x; u.q[c][j][5] = v1.y; u.q[c][j][6] = v1.z; u.q[c][j][7] = v1.w;
+        u.q[0][j][0] = v0.x; u.q[0][j][1] = v0.y; u.q[0][j][2] = v0.z; u.q[0][j][3] = v0.w;
+        u.q[0][j][4] = v1.x; u.q[0][j][5] = v1.y; u.q[0][j][6] = v1.z; u.q[0][j][7] = v1.w;
       } else {
         const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.q) + qrow + ch);
         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
-          u.q[c][j][2 * p] = __uint_as_float(w[p] << 16);
-          u.q[c][j][2 * p + 1] = __uint_as_float(w[p] & 0xffff0000u);
+          u.q[0][j][2 * p] = __uint_as_float(w[p] << 16);
+          u.q[0][j][2 * p + 1] = __uint_as_float(w[p] & 0xffff0000u);
         }
       }
     }
@@ -491,27 +493,22 @@ __global__ __launch_bounds__(256) void gqa_decode_kernel(DecodeArgs a) {
   const int k1 = min(nblk, k0 + it.split_blocks);
   const uint8_t* stream = a.arena + it.region + (int64_t)sidx * it.stream_bytes;
   switch (it.bits) {
-    case 16: run_stream<D, NCH, 16, KIVI>(u, stream, a, it, k0, k1, lane); break;
-    case 8: run_stream<D, NCH, 8, KIVI>(u, stream, a, it, k0, k1, lane); break;
-    case 4: run_stream<D, NCH, 4, KIVI>(u, stream, a, it, k0, k1, lane); break;
-    default: run_stream<D, NCH, 2, KIVI>(u, stream, a, it, k0, k1, lane); break;
+    case 16: run_stream<D, 1, 16, KIVI>(u, stream, a, it, k0, k1, lane); break;
+    case 8: run_stream<D, 1, 8, KIVI>(u, stream, a, it, k0, k1, lane); break;
+    case 4: run_stream<D, 1, 4, KIVI>(u, stream, a, it, k0, k1, lane); break;
+    default: run_stream<D, 1, 2, KIVI>(u, stream, a, it, k0, k1, lane); break;
   }
 
   // partials: rows of (o[D], m, l, pad, pad)
   float* base = a.ws + it.ws_off + ((int64_t)sidx * it.nsplit + split) * it.geff * (D + 4);
+  const float lt = wave_sum_kg(u.l[0]);
+  if (row < it.geff) {
+    float* pr = base + (int64_t)row * (D + 4);
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    const int row = 16 * c + i16;
-    const float lt = wave_sum_kg(u.l[c]);
-    if (row < it.geff) {
-      float* pr = base + (int64_t)row * (D + 4);
-#pragma unroll
-      for (int mt = 0; mt < NM; ++mt)
-        *reinterpret_cast<f4*>(pr + 16 * mt + 4 * kg) = u.o[c][mt];
-      if (kg == 0) {
-        pr[D] = u.m[c];
-        pr[D + 1] = lt;
-      }
+    for (int mt = 0; mt < NM; ++mt) *reinterpret_cast<f4*>(pr + 16 * mt + 4 * kg) = u.o[0][mt];
+    if (kg == 0) {
+      pr[D] = u.m[0];
+      pr[D + 1] = lt;
     }
   }
 }
@@ -555,35 +552,26 @@ __global__ __launch_bounds__(256) void gqa_combine_kernel(CombineArgs a) {
   for (int e = 0; e < PER; ++e) o[lane + 64 * e] = acc[e] * inv;
 }
 
-template <int D, int NCH>
-void launch_decode(const DecodeArgs& a, int kivi, hipStream_t st) {
-  const unsigned grid = (unsigned)((a.total_waves + 3) / 4);
-  if (kivi)
-    hipLaunchKernelGGL((gqa_decode_kernel<D, NCH, true>), dim3(grid), dim3(256), 0, st, a);
-  else
-    hipLaunchKernelGGL((gqa_decode_kernel<D, NCH, false>), dim3(grid), dim3(256), 0, st, a);
-}
-
-template <int D>
-void launch_decode_nch(const DecodeArgs& a, int nch, int kivi, hipStream_t st) {
-  switch (nch) {
-    case 1: launch_decode<D, 1>(a, kivi, st); break;
-    case 2: launch_decode<D, 2>(a, kivi, st); break;
-    case 3: launch_decode<D, 3>(a, kivi, st); break;
-    default: launch_decode<D, 4>(a, kivi, st); break;
-  }
-}
-
 }  // namespace
 
 using namespace kvk;
 
-extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
-                                           int32_t q_dtype, int32_t n_stored, float scale,
-                                           const void* w_uk, const void* w_uv, const void* arena,
-                                           float* out, void* workspace, size_t ws_bytes,
-                                           hipStream_t stream) {
-  if (!t) return fail(KVK_ERR_INVALID, "kvk_decode_attention: NULL table");
+namespace {
+
+// Everything one decode call launches: the D1 arguments (all anchors of the
+// range in one launch) and the C1 arguments.
+struct DecodePlan {
+  DecodeArgs d1;
+  CombineArgs c1;
+  int kivi;
+  int head_dim;
+  bool any_blocks;
+};
+
+kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
+                   int32_t n_stored, float scale, const void* w_uk, const void* w_uv, const void* arena,
+                   float* out, void* workspace, size_t ws_bytes, DecodePlan& P) {
+  if (!t) return fail(KVK_ERR_INVALID, "decode: NULL table");
   const kvk_dims& d = t->d;
   if (l0 < 0 || l1 > d.n_layers || l0 >= l1)
     return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, d.n_layers);
@@ -601,12 +589,21 @@ extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32
   const int32_t D = d.head_dim;
   const int32_t nbf = n_stored / KVK_GROUP, ntail = n_stored % KVK_GROUP;
   const int32_t nblk = nbf + (ntail > 0 ? 1 : 0);
-
-  // Work items: one per distinct anchor read by the range (§2.1 depth sharing).
-  DecodeItem items[kMaxItems];
-  int item_of_anchor[KVK_MAX_LAYERS];
-  for (int l = 0; l < KVK_MAX_LAYERS; ++l) item_of_anchor[l] = -1;
-  CombineArgs ca;
+  DecodeArgs& a = P.d1;
+  CombineArgs& ca = P.c1;
+  a.arena = static_cast<const uint8_t*>(arena);
+  a.q = q;
+  a.ws = static_cast<float*>(workspace);
+  a.q_f32 = q_dtype == KVK_F32;
+  a.B = d.batch;
+  a.Hq = d.n_q_heads;
+  a.Hkv = d.n_kv_heads;
+  a.G = G;
+  a.nbf = nbf;
+  a.ntail = ntail;
+  a.nb_cap = t->nb_cap;
+  a.scale_log2 = scale * kLog2e;
+  a.n_items = 0;
   ca.out = out;
   ca.ws = static_cast<const float*>(workspace);
   ca.B = d.batch;
@@ -615,12 +612,16 @@ extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32
   ca.G = G;
   ca.n_layers = l1 - l0;
   ca.n_rows = (l1 - l0) * d.batch * d.n_q_heads;
-  int n_items = 0;
-  int64_t ws_floats = 0;
+
+  // One work item per distinct anchor read by the range (§2.1 depth sharing).
+  int item_of_anchor[KVK_MAX_LAYERS];
+  for (int l = 0; l < KVK_MAX_LAYERS; ++l) item_of_anchor[l] = -1;
+  int64_t ws_floats = 0, waves = 0;
   for (int l = l0; l < l1; ++l) {
     const int anc = t->info.anchor_of[l];
     if (item_of_anchor[anc] < 0) {
-      DecodeItem& it = items[n_items];
+      const int n = a.n_items++;
+      DecodeItem& it = a.items[n];
       const int rb = anc > l0 ? anc : l0;
       const int re = t->next_anchor[anc] < l1 ? t->next_anchor[anc] : l1;
       it.region = t->info.layer_offset[anc];
@@ -631,61 +632,115 @@ extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32
       it.geff = G * (re - rb);
       it.split_blocks = split_blocks_for(it.bits, d.qscheme, D);
       it.nsplit = n_splits(nblk, it.split_blocks);
-      it.wave_begin = 0;
+      const int nch = (it.geff + 15) / 16;
+      it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : 4);
+      waves = (waves + 3) / 4 * 4;  // a chunk group never straddles a workgroup
+      it.wave_begin = (int32_t)waves;
+      waves += (int64_t)d.batch * d.n_kv_heads * it.nsplit * it.nchp;
       it.ws_off = (int32_t)ws_floats;
-      it.pad = 0;
       ws_floats += (int64_t)d.batch * d.n_kv_heads * it.nsplit * it.geff * (D + 4);
-      ca.item_ws_off[n_items] = it.ws_off;
-      ca.item_nsplit[n_items] = it.nsplit;
-      ca.item_geff[n_items] = it.geff;
-      item_of_anchor[anc] = n_items++;
+      ca.item_ws_off[n] = it.ws_off;
+      ca.item_nsplit[n] = it.nsplit;
+      ca.item_geff[n] = it.geff;
+      item_of_anchor[anc] = n;
     }
     const int ii = item_of_anchor[anc];
     ca.layer_item[l - l0] = ii;
-    ca.layer_slot0[l - l0] = (l - l0 - items[ii].q_layer0) * G;
+    ca.layer_slot0[l - l0] = (l - l0 - a.items[ii].q_layer0) * G;
   }
   if ((size_t)ws_floats * sizeof(float) > ws_bytes)
     return fail(KVK_ERR_BUFFER, "workspace %zu bytes < %lld needed", ws_bytes,
                 (long long)(ws_floats * sizeof(float)));
   if (ws_floats > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "workspace exceeds 2^31 floats");
+  if (waves > 0x7ffffff0LL) return fail(KVK_ERR_UNSUPPORTED, "too many decode waves");
+  a.total_waves = (int32_t)waves;
+  P.kivi = d.qscheme == KVK_Q_KIVI32;
+  P.head_dim = D;
+  P.any_blocks = nblk > 0 && waves > 0;
+  return KVK_OK;
+}
 
-  // One decode launch per number of 16-row chunks present.
-  const int kivi = d.qscheme == KVK_Q_KIVI32;
-  for (int nch = 1; nch <= 4 && nblk > 0; ++nch) {
-    DecodeArgs a;
-    a.arena = static_cast<const uint8_t*>(arena);
-    a.q = q;
-    a.ws = static_cast<float*>(workspace);
-    a.q_f32 = q_dtype == KVK_F32;
-    a.B = d.batch;
-    a.Hq = d.n_q_heads;
-    a.Hkv = d.n_kv_heads;
-    a.G = G;
-    a.nbf = nbf;
-    a.ntail = ntail;
-    a.nb_cap = t->nb_cap;
-    a.scale_log2 = scale * kLog2e;
-    a.n_items = 0;
-    int64_t waves = 0;
-    for (int i = 0; i < n_items; ++i) {
-      if ((items[i].geff + 15) / 16 != nch) continue;
-      DecodeItem it = items[i];
-      it.wave_begin = (int32_t)waves;
-      waves += (int64_t)d.batch * d.n_kv_heads * it.nsplit;
-      a.items[a.n_items++] = it;
-    }
-    if (a.n_items == 0 || waves == 0) continue;
-    if (waves > 0x7ffffff0LL) return fail(KVK_ERR_UNSUPPORTED, "too many decode waves");
-    a.total_waves = (int32_t)waves;
-    if (D == 128) launch_decode_nch<128>(a, nch, kivi, stream);
-    else launch_decode_nch<64>(a, nch, kivi, stream);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "decode launch: %s", hipGetErrorString(e));
+kvk_status launch_d1(const DecodePlan& P, hipStream_t st) {
+  if (!P.any_blocks) return KVK_OK;
+  const unsigned grid = (unsigned)((P.d1.total_waves + 3) / 4);
+  if (P.head_dim == 128) {
+    if (P.kivi) hipLaunchKernelGGL((gqa_decode_kernel<128, true>), dim3(grid), dim3(256), 0, st, P.d1);
+    else hipLaunchKernelGGL((gqa_decode_kernel<128, false>), dim3(grid), dim3(256), 0, st, P.d1);
+  } else {
+    if (P.kivi) hipLaunchKernelGGL((gqa_decode_kernel<64, true>), dim3(grid), dim3(256), 0, st, P.d1);
+    else hipLaunchKernelGGL((gqa_decode_kernel<64, false>), dim3(grid), dim3(256), 0, st, P.d1);
   }
-  const unsigned cgrid = (unsigned)((ca.n_rows + 3) / 4);
-  if (D == 128) hipLaunchKernelGGL(gqa_combine_kernel<128>, dim3(cgrid), dim3(256), 0, stream, ca);
-  else hipLaunchKernelGGL(gqa_combine_kernel<64>, dim3(cgrid), dim3(256), 0, stream, ca);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "decode launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+kvk_status launch_c1(const DecodePlan& P, hipStream_t st) {
+  const unsigned grid = (unsigned)((P.c1.n_rows + 3) / 4);
+  if (P.head_dim == 128) hipLaunchKernelGGL(gqa_combine_kernel<128>, dim3(grid), dim3(256), 0, st, P.c1);
+  else hipLaunchKernelGGL(gqa_combine_kernel<64>, dim3(grid), dim3(256), 0, st, P.c1);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "combine launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+}  // namespace
+
+extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
+                                           int32_t q_dtype, int32_t n_stored, float scale,
+                                           const void* w_uk, const void* w_uv, const void* arena,
+                                           float* out, void* workspace, size_t ws_bytes,
+                                           hipStream_t stream) {
+  DecodePlan P;
+  kvk_status st = prepare(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
+                          ws_bytes, P);
+  if (st != KVK_OK) return st;
+  st = launch_d1(P, stream);
+  if (st != KVK_OK) return st;
+  return launch_c1(P, stream);
+}
+
+extern "C" kvk_status kvk_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
+                                        int32_t q_dtype, int32_t n_stored, float scale,
+                                        const void* w_uk, const void* w_uv, const void* arena,
+                                        void* workspace, size_t ws_bytes, hipStream_t stream) {
+  DecodePlan P;
+  float* dummy_out = static_cast<float*>(workspace);  // not written by this phase
+  kvk_status st = prepare(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, dummy_out,
+                          workspace, ws_bytes, P);
+  if (st != KVK_OK) return st;
+  return launch_d1(P, stream);
+}
+
+extern "C" kvk_status kvk_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored,
+                                       const void* workspace, size_t ws_bytes, float* out,
+                                       hipStream_t stream) {
+  DecodePlan P;
+  // q and arena are not read by the merge; the workspace stands in for them in validation.
+  kvk_status st = prepare(t, l0, l1, workspace, KVK_F32, n_stored, 1.0f, nullptr, nullptr, workspace,
+                          out, const_cast<void*>(workspace), ws_bytes, P);
+  if (st != KVK_OK) return st;
+  return launch_c1(P, stream);
+}
+
+extern "C" kvk_status kvk_read_bytes(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored,
+                                     int64_t* out_bytes) {
+  if (!t || !out_bytes) return fail(KVK_ERR_INVALID, "kvk_read_bytes: NULL argument");
+  const kvk_dims& d = t->d;
+  if (l0 < 0 || l1 > d.n_layers || l0 >= l1)
+    return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, d.n_layers);
+  if (n_stored < 0 || n_stored > t->cap)
+    return fail(KVK_ERR_INVALID, "n_stored %d outside 0..%d", n_stored, t->cap);
+  bool seen[KVK_MAX_LAYERS] = {false};
+  int64_t total = 0;
+  const int64_t per_stream_tail = (int64_t)(n_stored % KVK_GROUP) * 4 * d.head_dim;
+  for (int l = l0; l < l1; ++l) {
+    const int a = t->info.anchor_of[l];
+    if (seen[a]) continue;
+    seen[a] = true;
+    const int64_t per = (int64_t)(n_stored / KVK_GROUP) * t->block_bytes[a] + per_stream_tail;
+    total += per * d.batch * d.n_kv_heads;
+  }
+  *out_bytes = total;
   return KVK_OK;
 }

@@ -70,6 +70,9 @@ def load() -> ctypes.CDLL:
             "kvk_workspace_bytes": (I32, [P, I32, I32, ctypes.POINTER(ctypes.c_size_t)]),
             "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
             "kvk_decode_attention": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P, ctypes.c_size_t, P]),
+            "kvk_decode_splits": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P]),
+            "kvk_decode_merge": (I32, [P, I32, I32, I32, P, ctypes.c_size_t, P, P]),
+            "kvk_read_bytes": (I32, [P, I32, I32, I32, ctypes.POINTER(ctypes.c_int64)]),
             "kvk_debug_dequantize": (I32, [P, I32, I32, P, P, P, P]),
             "kvk_realized_bits": (ctypes.c_double, [I32, I32, I32, I64, I64]),
             "kvk_rho_range": (I32, [I32, I32, I32, I32, I32, I32, ctypes.POINTER(ctypes.c_double),
@@ -88,7 +91,8 @@ def load() -> ctypes.CDLL:
 def exported_symbols() -> List[str]:
     """Names of the C entry points the binding expects libkvk to export."""
     return ["kvk_layer_table", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
-            "kvk_compress_layer", "kvk_decode_attention", "kvk_debug_dequantize",
+            "kvk_compress_layer", "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge",
+            "kvk_read_bytes", "kvk_debug_dequantize",
             "kvk_realized_bits", "kvk_rho_range", "kvk_last_error", "kvk_version"]
 
 
@@ -245,6 +249,37 @@ def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor
         t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
         _ptr(w_uk), _ptr(w_uv), _ptr(arena), _ptr(out), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def decode_splits(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_stored: int,
+                  scale: float, arena: torch.Tensor, workspace: torch.Tensor,
+                  w_uk: Optional[torch.Tensor] = None, w_uv: Optional[torch.Tensor] = None,
+                  stream=None):
+    """First phase of decode_attention: split partials into `workspace`."""
+    d = t.dims
+    rows = (layer_end - layer_begin) * d.batch * d.n_q_heads * d.head_dim
+    _need(q.is_contiguous() and q.numel() == rows, "q must be contiguous, layers*B*Hq*d_h")
+    _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
+    _check(load().kvk_decode_splits(
+        t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
+        _ptr(w_uk), _ptr(w_uv), _ptr(arena), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def decode_merge(t: Table, layer_begin: int, layer_end: int, n_stored: int, workspace: torch.Tensor,
+                 out: torch.Tensor, stream=None):
+    """Second phase of decode_attention: merge the split partials into `out`."""
+    d = t.dims
+    rows = (layer_end - layer_begin) * d.batch * d.n_q_heads * d.head_dim
+    _need(out.is_contiguous() and out.dtype == torch.float32 and out.numel() == rows,
+          "out must be contiguous fp32, layers*B*Hq*d_h")
+    _check(load().kvk_decode_merge(t.handle, layer_begin, layer_end, n_stored, _ptr(workspace),
+                                   _nbytes(workspace), _ptr(out), _stream(stream)))
+
+
+def read_bytes(t: Table, layer_begin: int, layer_end: int, n_stored: int) -> int:
+    out = ctypes.c_int64()
+    _check(load().kvk_read_bytes(t.handle, layer_begin, layer_end, n_stored, ctypes.byref(out)))
+    return out.value
 
 
 def debug_dequantize(t: Table, layer: int, n_stored: int, arena: torch.Tensor, k_out: torch.Tensor,

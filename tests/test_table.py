@@ -61,6 +61,10 @@ def test_table_matches_oracle_accounting(cfg, qs):
     alg = P.read_bytes(od, oplan, 0, od.n_layers, od.stored_cap)
     assert inf.rho_realized == pytest.approx(P.bf16_full_bytes(od) / alg, rel=1e-12)
     assert inf.n_anchors == sum(1 for a in oplan if not a.inherit)
+    for n in (0, 1, 33, od.stored_cap):
+        for l0, l1 in ((0, od.n_layers), (1, min(5, od.n_layers)), (od.n_layers - 1, od.n_layers)):
+            if l1 > l0:
+                assert kvk.read_bytes(t, l0, l1, n) == P.read_bytes(od, oplan, l0, l1, n)
 
 
 def test_headline_plans():
