@@ -160,7 +160,7 @@ def main():
         ev[i][0].record()
         kvk.decode_splits(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, ws)
         ev[i][1].record()
-        kvk.decode_merge(table, 0, w.n_layers, n_stored, ws, out)
+        kvk.decode_merge(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, ws, out)
     t_end.record()
     torch.cuda.synchronize()
     ms_step = t_start.elapsed_time(t_end) / K

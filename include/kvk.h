@@ -227,18 +227,21 @@ kvk_status kvk_decode_attention(const kvk_table* table, int32_t layer_begin, int
                                 hipStream_t stream);
 
 /* The two phases of kvk_decode_attention, for callers that schedule or time them
- * separately.  kvk_decode_splits runs the per-split attention (arguments as for
- * kvk_decode_attention) and leaves the split partials in `workspace`;
- * kvk_decode_merge then merges them by log-sum-exp into `out`.  The merge must use
- * the same table, layer range, n_stored and workspace as the splits call before
- * it on the same stream.  Errors as for kvk_decode_attention. */
+ * separately.  kvk_decode_splits runs the attention over the full 32-token blocks,
+ * split along the context (arguments as for kvk_decode_attention), and leaves the
+ * split partials in `workspace`; kvk_decode_merge attends to the bf16 tail tokens
+ * and merges them with the partials by log-sum-exp into `out`.  The merge must use
+ * the same table, layer range, q, n_stored, scale, arena and workspace as the
+ * splits call before it on the same stream.  Errors as for kvk_decode_attention. */
 kvk_status kvk_decode_splits(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
                              const void* q, int32_t q_dtype, int32_t n_stored, float scale,
                              const void* w_uk, const void* w_uv, const void* arena,
                              void* workspace, size_t workspace_bytes, hipStream_t stream);
 kvk_status kvk_decode_merge(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
-                            int32_t n_stored, const void* workspace, size_t workspace_bytes,
-                            float* out, hipStream_t stream);
+                            const void* q, int32_t q_dtype, int32_t n_stored, float scale,
+                            const void* w_uk, const void* w_uv, const void* arena,
+                            const void* workspace, size_t workspace_bytes, float* out,
+                            hipStream_t stream);
 
 /* Algorithmic bytes one decode call over [layer_begin, layer_end) reads from the
  * arena with n_stored tokens per stream: each distinct anchor's full blocks and

@@ -68,9 +68,17 @@ struct DecodeArgs {
 struct CombineArgs {
   float* out;
   const float* ws;
+  const uint8_t* arena;
+  const void* q;
+  int32_t q_f32;
+  float scale_log2;
+  int32_t ntail;   // tokens in the bf16 tail block
+  int32_t nb_cap;
   int32_t B, Hq, Hkv, G;
   int32_t n_rows;  // layers * B * Hq
   int32_t n_layers;
+  int64_t item_tail[kMaxItems];  // byte offset of stream 0's tail block of each item
+  int32_t item_stream_bytes[kMaxItems];
   int32_t layer_item[kMaxItems];
   int32_t layer_slot0[kMaxItems];
   int32_t item_ws_off[kMaxItems];
@@ -103,345 +111,397 @@ __device__ __forceinline__ bf16x8 to_bf16x8(const float* x) {
   return r;
 }
 
-// Per-wave state of one work unit.
-template <int D, int NCH>
-struct Unit {
-  static constexpr int NJ = D / 32;  // K sub-chunks (MFMA k-steps over channels)
-  static constexpr int NM = D / 16;  // V channel tiles
-  float q[NCH][NJ][8];               // query rows, fp32, lane's channels
-  f4 o[NCH][NM];                     // output accumulators (O^T tiles)
-  float m[NCH];                      // running max (log2 domain), per row
-  float l[NCH];                      // lane-partial running sum
+// ---------------------------------------------------------------------------
+// Per-lane raw bytes of one 32-token block, loaded ahead of use.
+// ---------------------------------------------------------------------------
+
+template <int D, int BITS, bool KIVI>
+struct Raw {
+  static constexpr int KB = BITS == 16 ? D / 2 : D * BITS / 32;  // bytes per lane per K tile
+  static constexpr int VB = BITS == 16 ? D : D * BITS / 16;      // bytes per lane of V
+  static constexpr int MB = BITS == 16 ? 0 : (KIVI ? D / 8 : 32);  // metadata bytes per lane
+  uint32_t k[2][KB / 4];
+  uint32_t v[VB / 4];
+  uint32_t m[MB > 0 ? MB / 4 : 1];
 };
 
-// Online-softmax update from the 8 logits of a 32-token block (2 tiles x 4),
-// returning the probabilities in place.
-template <int D, int NCH>
-__device__ __forceinline__ void softmax_update(Unit<D, NCH>& u, float (&x)[NCH][8]) {
+template <int N>
+__device__ __forceinline__ void load_words(const uint8_t* p, uint32_t* w) {
+  if constexpr (N % 4 == 0) {
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    float mb = x[c][0];
-#pragma unroll
-    for (int e = 1; e < 8; ++e) mb = fmaxf(mb, x[c][e]);
-    mb = wave_max_kg(mb);
-    const float mnew = fmaxf(u.m[c], mb);
-    const float alpha = (u.m[c] == -INFINITY) ? 0.0f : exp2f(u.m[c] - mnew);
-    float ps = 0.0f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float p = (x[c][e] == -INFINITY) ? 0.0f : exp2f(x[c][e] - mnew);
-      x[c][e] = p;
-      ps += p;
+    for (int i = 0; i < N / 4; ++i) {
+      const uint4 x = reinterpret_cast<const uint4*>(p)[i];
+      w[4 * i] = x.x; w[4 * i + 1] = x.y; w[4 * i + 2] = x.z; w[4 * i + 3] = x.w;
     }
-    u.l[c] = u.l[c] * alpha + ps;
-    u.m[c] = mnew;
-    if (__any(alpha != 1.0f)) {
+  } else if constexpr (N == 2) {
+    const uint2 x = *reinterpret_cast<const uint2*>(p);
+    w[0] = x.x; w[1] = x.y;
+  } else {
+    w[0] = *reinterpret_cast<const uint32_t*>(p);
+  }
+}
+
+// Issue the loads of block `blk` for this lane (block layout of include/kvk.h).
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void load_raw(Raw<D, BITS, KIVI>& r, const uint8_t* blk, int lane) {
+  using R = Raw<D, BITS, KIVI>;
+  constexpr int tile = BITS == 16 ? 32 * D : 2 * D * BITS;
+  constexpr int vbase = BITS == 16 ? 64 * D : 4 * D * BITS;
 #pragma unroll
-      for (int mt = 0; mt < Unit<D, NCH>::NM; ++mt) u.o[c][mt] *= alpha;
+  for (int tau = 0; tau < 2; ++tau) load_words<R::KB / 4>(blk + tau * tile + lane * R::KB, r.k[tau]);
+  load_words<R::VB / 4>(blk + vbase + lane * R::VB, r.v);
+  if constexpr (BITS != 16) {
+    const uint8_t* meta = blk + 8 * D * BITS;
+    if constexpr (KIVI) {
+      load_words<R::MB / 4>(meta + lane * R::MB, r.m);  // the lane's share of the 8D-byte area
+    } else {
+      const int kg = lane >> 4;
+#pragma unroll
+      for (int tau = 0; tau < 2; ++tau) {
+        load_words<2>(meta + 2 * (16 * tau + 4 * kg), r.m + 2 * tau);       // K row scales
+        load_words<2>(meta + 64 + 2 * (16 * tau + 4 * kg), r.m + 4 + 2 * tau);  // V row scales
+      }
     }
   }
 }
 
-// The query rows as bf16 hi + lo pairs (for bf16 blocks).
-template <int D, int NCH>
-struct QB16 {
-  bf16x8 hi[NCH][D / 32], lo[NCH][D / 32];
-};
-
-template <int D, int NCH>
-__device__ __forceinline__ void make_qb16(const Unit<D, NCH>& u, QB16<D, NCH>& qb) {
-#pragma unroll
-  for (int c = 0; c < NCH; ++c)
-#pragma unroll
-    for (int j = 0; j < D / 32; ++j) {
-      float hi[8], lo[8];
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        hi[s] = (float)(__bf16)u.q[c][j][s];
-        lo[s] = u.q[c][j][s] - hi[s];
-      }
-      qb.hi[c][j] = to_bf16x8(hi);
-      qb.lo[c][j] = to_bf16x8(lo);
-    }
+// Unpack the 8 codes (one MFMA k-step) of chunk x from a lane's code words.
+template <int BITS>
+__device__ __forceinline__ half8 unpack_chunk(const uint32_t* w, int x, float off) {
+  if constexpr (BITS == 4) {
+    return unpack4(w[x], off);
+  } else if constexpr (BITS == 8) {
+    return unpack8(w[2 * x], w[2 * x + 1], off);
+  } else {
+    return unpack2_half(w[x >> 1] >> (8 * (x & 1)), off);
+  }
 }
 
-// A bf16 block (a b = 16 layer's block, or any layer's tail) with `nvalid` tokens.
-template <int D, int NCH>
-__device__ __forceinline__ void block_bf16(Unit<D, NCH>& u, const QB16<D, NCH>& qb, const uint8_t* blk,
-                                           int lane, int nvalid, float sl2) {
+// ---------------------------------------------------------------------------
+// Per-wave state of one work unit (16 query rows: lane row = lane % 16).
+// ---------------------------------------------------------------------------
+
+template <int D>
+struct State {
+  static constexpr int NJ = D / 32;  // MFMA k-steps over channels
+  static constexpr int NM = D / 16;  // value channel tiles
+  static constexpr int NG = D / 32;  // value channel groups (KIVI32)
+  f4 o[NM];                          // O^T tiles
+  float m;                           // running max, log2 domain
+  float l;                           // lane-partial running sum
+};
+
+// Extra accumulators rescaled with the output: KIVI32's value zero-point sums.
+template <int N>
+struct Extra {
+  f4 zo[N];
+};
+
+template <int D, int NX>
+__device__ __forceinline__ void softmax_update(State<D>& u, Extra<NX>& ex, float (&x)[8]) {
+  float mb = x[0];
+#pragma unroll
+  for (int e = 1; e < 8; ++e) mb = fmaxf(mb, x[e]);
+  mb = wave_max_kg(mb);
+  const float mnew = fmaxf(u.m, mb);
+  const float alpha = (u.m == -INFINITY) ? 0.0f : exp2f(u.m - mnew);
+  float ps = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float p = (x[e] == -INFINITY) ? 0.0f : exp2f(x[e] - mnew);
+    x[e] = p;
+    ps += p;
+  }
+  u.l = u.l * alpha + ps;
+  u.m = mnew;
+  if (__any(alpha != 1.0f)) {
+#pragma unroll
+    for (int mt = 0; mt < State<D>::NM; ++mt) u.o[mt] *= alpha;
+#pragma unroll
+    for (int g = 0; g < NX; ++g) ex.zo[g] *= alpha;
+  }
+}
+
+__device__ __forceinline__ half8 to_half8(const float (&x)[8]) {
+  half8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = (_Float16)x[e];
+  return r;
+}
+
+// bf16 block (a b = 16 layer's block, or any layer's tail) with `nvalid` tokens.
+template <int D, bool K>
+__device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D / 32],
+                                             const bf16x8 (&qbl)[D / 32], const Raw<D, 16, K>& r,
+                                             int lane, int nvalid, float sl2) {
   constexpr int NJ = D / 32, NM = D / 16;
   const int kg = lane >> 4;
-  float x[NCH][8];
+  float x[8];
 #pragma unroll
   for (int tau = 0; tau < 2; ++tau) {
-    const uint4* kp = reinterpret_cast<const uint4*>(blk + 32 * D * tau + lane * (D / 2));
-    bf16x8 kop[NJ];
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < NJ; ++j) kop[j] = bitcast<bf16x8>(kp[j]);
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      f4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        acc = mfmab(kop[j], qb.hi[c][j], acc);
-        acc = mfmab(kop[j], qb.lo[c][j], acc);
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int tok = 16 * tau + 4 * kg + r;
-        x[c][4 * tau + r] = tok < nvalid ? acc[r] * sl2 : -INFINITY;
-      }
+    for (int j = 0; j < NJ; ++j) {
+      const u4v w = {r.k[tau][4 * j], r.k[tau][4 * j + 1], r.k[tau][4 * j + 2], r.k[tau][4 * j + 3]};
+      const bf16x8 kop = bitcast<bf16x8>(w);
+      acc = mfmab(kop, qbh[j], acc);
+      acc = mfmab(kop, qbl[j], acc);
     }
-  }
-  softmax_update<D, NCH>(u, x);
-  bf16x8 phi[NCH], plo[NCH];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) {
-    float h[8], lw[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      h[e] = (float)(__bf16)x[c][e];
-      lw[e] = x[c][e] - h[e];
-    }
-    phi[c] = to_bf16x8(h);
-    plo[c] = to_bf16x8(lw);
+    for (int e = 0; e < 4; ++e)
+      x[4 * tau + e] = (16 * tau + 4 * kg + e) < nvalid ? acc[e] * sl2 : -INFINITY;
   }
-  const uint4* vp = reinterpret_cast<const uint4*>(blk + 64 * D + lane * D);
+  Extra<0> none;
+  softmax_update<D, 0>(u, none, x);
+  float h[8], lw[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    h[e] = (float)(__bf16)x[e];
+    lw[e] = x[e] - h[e];
+  }
+  const bf16x8 phi = to_bf16x8(h), plo = to_bf16x8(lw);
 #pragma unroll
   for (int mt = 0; mt < NM; ++mt) {
-    const bf16x8 vop = bitcast<bf16x8>(vp[mt]);
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      u.o[c][mt] = mfmab(vop, phi[c], u.o[c][mt]);
-      u.o[c][mt] = mfmab(vop, plo[c], u.o[c][mt]);
-    }
+    const u4v w = {r.v[4 * mt], r.v[4 * mt + 1], r.v[4 * mt + 2], r.v[4 * mt + 3]};
+    const bf16x8 vop = bitcast<bf16x8>(w);
+    u.o[mt] = mfmab(vop, phi, u.o[mt]);
+    u.o[mt] = mfmab(vop, plo, u.o[mt]);
   }
 }
 
-// Load the lane's K code chunks of tile tau and unpack them to exact fp16 (minus off).
+// KIVI32 block of BITS-bit codes.  The block's metadata goes through the wave's
+// LDS slot so that the 16 lanes sharing a channel (or token) group read it by
+// broadcast.
 template <int D, int BITS>
-__device__ __forceinline__ void load_k_codes(const uint8_t* blk, int tau, int lane, float off,
-                                             half8 (&kop)[D / 32]) {
-  constexpr int NJ = D / 32;
-  const uint8_t* p = blk + 2 * D * BITS * tau + lane * (D * BITS / 32);
-  if constexpr (BITS == 4) {
-    const uint32_t* w = reinterpret_cast<const uint32_t*>(p);
-    uint32_t wr[NJ];
-    if constexpr (NJ == 4) {
-      const uint4 v = *reinterpret_cast<const uint4*>(p);
-      wr[0] = v.x; wr[1] = v.y; wr[2] = v.z; wr[3] = v.w;
-    } else {
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) wr[j] = w[j];
-    }
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) kop[j] = unpack4(wr[j], off);
-  } else if constexpr (BITS == 8) {
-    const uint4* w = reinterpret_cast<const uint4*>(p);
-#pragma unroll
-    for (int j2 = 0; j2 < NJ / 2; ++j2) {
-      const uint4 v = w[j2];
-      kop[2 * j2] = unpack8(v.x, v.y, off);
-      kop[2 * j2 + 1] = unpack8(v.z, v.w, off);
-    }
-  } else {  // BITS == 2
-    const uint32_t* w = reinterpret_cast<const uint32_t*>(p);
-#pragma unroll
-    for (int j2 = 0; j2 < NJ / 2; ++j2) unpack2(w[j2], off, kop[2 * j2], kop[2 * j2 + 1]);
-  }
-}
-
-// Load the lane's V code chunks (all channel tiles) as exact fp16 (minus off).
-template <int D, int BITS>
-__device__ __forceinline__ void load_v_codes(const uint8_t* blk, int lane, float off,
-                                             half8 (&vop)[D / 16]) {
-  constexpr int NM = D / 16;
-  const uint8_t* p = blk + 4 * D * BITS + lane * (D * BITS / 16);
-  if constexpr (BITS == 4) {
-    const uint4* w = reinterpret_cast<const uint4*>(p);
-#pragma unroll
-    for (int m4 = 0; m4 < NM / 4; ++m4) {
-      const uint4 v = w[m4];
-      vop[4 * m4 + 0] = unpack4(v.x, off);
-      vop[4 * m4 + 1] = unpack4(v.y, off);
-      vop[4 * m4 + 2] = unpack4(v.z, off);
-      vop[4 * m4 + 3] = unpack4(v.w, off);
-    }
-  } else if constexpr (BITS == 8) {
-    const uint4* w = reinterpret_cast<const uint4*>(p);
-#pragma unroll
-    for (int m2 = 0; m2 < NM / 2; ++m2) {
-      const uint4 v = w[m2];
-      vop[2 * m2] = unpack8(v.x, v.y, off);
-      vop[2 * m2 + 1] = unpack8(v.z, v.w, off);
-    }
-  } else {
-    const uint32_t* w = reinterpret_cast<const uint32_t*>(p);
-#pragma unroll
-    for (int m2 = 0; m2 < NM / 2; ++m2) unpack2(w[m2], off, vop[2 * m2], vop[2 * m2 + 1]);
-  }
-}
-
-// A full KIVI32 block of `BITS`-bit codes.
-template <int D, int NCH, int BITS>
-__device__ __forceinline__ void block_kivi(Unit<D, NCH>& u, const uint8_t* blk, int lane, float sl2) {
-  constexpr int NJ = D / 32, NM = D / 16;
+__device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, const half8 (&qh)[D / 32],
+                                             const half8 (&ql)[D / 32], const Raw<D, BITS, true>& r,
+                                             uint32_t* lds, int lane, float sl2) {
+  using R = Raw<D, BITS, true>;
+  constexpr int NJ = D / 32, NG = D / 32;
   const int kg = lane >> 4;
-  const _Float16* kmeta = reinterpret_cast<const _Float16*>(blk + 8 * D * BITS);
-  const _Float16* vmeta = kmeta + 2 * D;
-  // q' = q * s (hi + lo in fp16) and the zero term sum_c q_c z_c, per row.
-  half8 qh[NCH][NJ], ql[NCH][NJ];
-  float zt[NCH];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) zt[c] = 0.0f;
+  for (int i = 0; i < R::MB / 4; ++i) lds[lane * (R::MB / 4) + i] = r.m[i];
+  const half8* kmeta = reinterpret_cast<const half8*>(lds);  // scale[D], zero[D], V meta[2D]
+  // K: S = sum_c (q_c s_c) u_c + sum_c q_c z_c.  q' = q s as fp16 hi + lo (error-free
+  // product of the fp16 hi part, rounded sum with the lo part).
+  f4 zt = {0.f, 0.f, 0.f, 0.f};
+  f4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
-    const half8 sv = *reinterpret_cast<const half8*>(kmeta + 32 * j + 8 * kg);
-    const half8 zv = *reinterpret_cast<const half8*>(kmeta + D + 32 * j + 8 * kg);
+    const half8 sv = kmeta[4 * j + kg];          // scales of channels 32j + 8kg + 0..7
+    const half8 zv = kmeta[D / 8 + 4 * j + kg];  // zeros of the same channels
+    const half8 hi = qh[j] * sv;
+    const half8 err = __builtin_elementwise_fma(qh[j], sv, -hi);
+    const half8 lo = __builtin_elementwise_fma(ql[j], sv, err);
+    zt = mfma16(zv, qh[j], zt);  // every token row gets sum_c z_c q_c
+    zt = mfma16(zv, ql[j], zt);
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-#pragma unroll
-      for (int s = 0; s < 8; ++s) {
-        const float qs = u.q[c][j][s] * (float)sv[s];
-        const _Float16 h = (_Float16)qs;
-        qh[c][j][s] = h;
-        ql[c][j][s] = (_Float16)(qs - (float)h);
-        zt[c] = fmaf(u.q[c][j][s], (float)zv[s], zt[c]);
-      }
+    for (int tau = 0; tau < 2; ++tau) {
+      const half8 kop = unpack_chunk<BITS>(r.k[tau], j, 0.0f);
+      acc[tau] = mfma16(kop, hi, acc[tau]);
+      acc[tau] = mfma16(kop, lo, acc[tau]);
     }
+    __builtin_amdgcn_sched_barrier(0);  // keep one k-step's operands live at a time
   }
+  float x[8];
 #pragma unroll
-  for (int c = 0; c < NCH; ++c) zt[c] = wave_sum_kg(zt[c]);
-
-  float x[NCH][8];
+  for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
-  for (int tau = 0; tau < 2; ++tau) {
-    half8 kop[NJ];
-    load_k_codes<D, BITS>(blk, tau, lane, 0.0f, kop);
+    for (int e = 0; e < 4; ++e) x[4 * tau + e] = (acc[tau][e] + zt[e]) * sl2;
+  softmax_update<D, D / 32>(u, ex, x);
+  const half8 p = to_half8(x);
+  // V: o_c = sum_t (p_t s_tg) u_tc + sum_t p_t z_tg, g = c / 32.
+  const half8* vmeta = kmeta + D / 4;
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      f4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        acc = mfma16(kop[j], qh[c][j], acc);
-        acc = mfma16(kop[j], ql[c][j], acc);
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) x[c][4 * tau + r] = (acc[r] + zt[c]) * sl2;
-    }
-  }
-  softmax_update<D, NCH>(u, x);
-  half8 p[NCH];
-#pragma unroll
-  for (int c = 0; c < NCH; ++c)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) p[c][e] = (_Float16)x[c][e];
-
-  half8 vop[NM];
-  load_v_codes<D, BITS>(blk, lane, 0.0f, vop);
-#pragma unroll
-  for (int g = 0; g < D / 32; ++g) {
-    const half8 vs = *reinterpret_cast<const half8*>(vmeta + ((g * 2 + 0) * 4 + kg) * 8);
-    const half8 vz = *reinterpret_cast<const half8*>(vmeta + ((g * 2 + 1) * 4 + kg) * 8);
+  for (int g = 0; g < NG; ++g) {
+    const half8 vs = vmeta[(g * 2 + 0) * 4 + kg];
+    const half8 vz = vmeta[(g * 2 + 1) * 4 + kg];
+    const half8 ps = p * vs;
+    ex.zo[g] = mfma16(vz, p, ex.zo[g]);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int mt = 2 * g + h;
-      const half8 vh = __builtin_elementwise_fma(vop[mt], vs, vz);  // fp16 dequantised values
-#pragma unroll
-      for (int c = 0; c < NCH; ++c) u.o[c][mt] = mfma16(vh, p[c], u.o[c][mt]);
+      u.o[mt] = mfma16(unpack_chunk<BITS>(r.v, mt, 0.0f), ps, u.o[mt]);
     }
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
-// A full SYMROW block: per-token scales factor out of both contractions.
-template <int D, int NCH, int BITS>
-__device__ __forceinline__ void block_symrow(Unit<D, NCH>& u, const half8 (&qh)[NCH][D / 32],
-                                             const half8 (&ql)[NCH][D / 32], const uint8_t* blk,
-                                             int lane, float sl2) {
+// SYMROW block: per-token scales factor out of both contractions.
+template <int D, int BITS>
+__device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D / 32],
+                                               const half8 (&ql)[D / 32], const Raw<D, BITS, false>& r,
+                                               int lane, float sl2) {
   constexpr int NJ = D / 32, NM = D / 16;
-  const int kg = lane >> 4;
   const float off = (float)(1 << (BITS - 1));
-  const uint16_t* ksc = reinterpret_cast<const uint16_t*>(blk + 8 * D * BITS);
-  const uint16_t* vsc = ksc + 32;
-  float x[NCH][8];
+  float x[8];
 #pragma unroll
   for (int tau = 0; tau < 2; ++tau) {
-    half8 kop[NJ];
-    load_k_codes<D, BITS>(blk, tau, lane, off, kop);
-    float sk[4];
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sk[r] = bf16_to_f32(ksc[16 * tau + 4 * kg + r]) * sl2;
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-      f4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        acc = mfma16(kop[j], qh[c][j], acc);
-        acc = mfma16(kop[j], ql[c][j], acc);
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) x[c][4 * tau + r] = acc[r] * sk[r];
+    for (int j = 0; j < NJ; ++j) {
+      const half8 kop = unpack_chunk<BITS>(r.k[tau], j, off);
+      acc = mfma16(kop, qh[j], acc);
+      acc = mfma16(kop, ql[j], acc);
     }
+    const uint32_t s01 = r.m[2 * tau], s23 = r.m[2 * tau + 1];
+    const float sk[4] = {__uint_as_float(s01 << 16), __uint_as_float(s01 & 0xffff0000u),
+                         __uint_as_float(s23 << 16), __uint_as_float(s23 & 0xffff0000u)};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[4 * tau + e] = acc[e] * (sk[e] * sl2);
   }
-  softmax_update<D, NCH>(u, x);
-  float sv[8];
+  Extra<0> none;
+  softmax_update<D, 0>(u, none, x);
+  float ps[8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) sv[e] = bf16_to_f32(vsc[16 * (e >> 2) + 4 * kg + (e & 3)]);
-  half8 p[NCH];
+  for (int tau = 0; tau < 2; ++tau) {
+    const uint32_t s01 = r.m[4 + 2 * tau], s23 = r.m[5 + 2 * tau];
+    ps[4 * tau + 0] = x[4 * tau + 0] * __uint_as_float(s01 << 16);
+    ps[4 * tau + 1] = x[4 * tau + 1] * __uint_as_float(s01 & 0xffff0000u);
+    ps[4 * tau + 2] = x[4 * tau + 2] * __uint_as_float(s23 << 16);
+    ps[4 * tau + 3] = x[4 * tau + 3] * __uint_as_float(s23 & 0xffff0000u);
+  }
+  const half8 p = to_half8(ps);
 #pragma unroll
-  for (int c = 0; c < NCH; ++c)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) p[c][e] = (_Float16)(x[c][e] * sv[e]);
-  half8 vop[NM];
-  load_v_codes<D, BITS>(blk, lane, off, vop);
-#pragma unroll
-  for (int mt = 0; mt < NM; ++mt)
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) u.o[c][mt] = mfma16(vop[mt], p[c], u.o[c][mt]);
+  for (int mt = 0; mt < NM; ++mt) u.o[mt] = mfma16(unpack_chunk<BITS>(r.v, mt, off), p, u.o[mt]);
 }
 
-template <int D, int NCH, int BITS, bool KIVI>
-__device__ __forceinline__ void run_stream(Unit<D, NCH>& u, const uint8_t* stream, const DecodeArgs& a,
-                                           const DecodeItem& it, int k0, int k1, int lane) {
-  constexpr int NJ = D / 32;
-  const float sl2 = a.scale_log2;
-  half8 qh[NCH][NJ], ql[NCH][NJ];
-  if constexpr (!KIVI && BITS != 16) {
+// Blocks kept in flight per wave (registers): about 8-16 KiB of cache ahead of use.
+template <int BITS>
+constexpr int ring_depth() {
+  return BITS == 16 ? 2 : (BITS == 8 ? 2 : (BITS == 4 ? 4 : 6));
+}
+
+// The query as fp16 hi + lo (integer-code paths) and as bf16 hi + lo (bf16 blocks).
+template <int D>
+__device__ __forceinline__ void split_bf16(const half8 (&qh)[D / 32], const half8 (&ql)[D / 32],
+                                           bf16x8 (&qbh)[D / 32], bf16x8 (&qbl)[D / 32]) {
 #pragma unroll
-    for (int c = 0; c < NCH; ++c)
+  for (int j = 0; j < D / 32; ++j) {
+    float hb[8], lb[8];
 #pragma unroll
-      for (int j = 0; j < NJ; ++j)
-#pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          const _Float16 h = (_Float16)u.q[c][j][s];
-          qh[c][j][s] = h;
-          ql[c][j][s] = (_Float16)(u.q[c][j][s] - (float)h);
-        }
+    for (int s = 0; s < 8; ++s) {
+      const float q = (float)qh[j][s] + (float)ql[j][s];
+      hb[s] = (float)(__bf16)q;
+      lb[s] = q - hb[s];
+    }
+    qbh[j] = to_bf16x8(hb);
+    qbl[j] = to_bf16x8(lb);
   }
-  QB16<D, NCH> qb;
-  if constexpr (BITS == 16) make_qb16<D, NCH>(u, qb);
-  const int kfull = min(k1, a.nbf);
-  for (int k = k0; k < kfull; ++k) {
-    const uint8_t* blk = stream + (int64_t)k * it.block_bytes;
-    if constexpr (BITS == 16) {
-      block_bf16<D, NCH>(u, qb, blk, lane, 32, sl2);
-    } else if constexpr (KIVI) {
-      block_kivi<D, NCH, BITS>(u, blk, lane, sl2);
+}
+
+// Load the lane's query row as fp16 hi + lo (~22 significant bits).
+template <int D>
+__device__ __forceinline__ void load_query(const DecodeArgs& a, const DecodeItem& it, int row, int b, int kvh,
+                                           int kg, half8 (&qh)[D / 32], half8 (&ql)[D / 32]) {
+  const bool valid = row < it.geff;
+  const int r = row / a.G, gh = row % a.G;
+  const int64_t qrow = (((int64_t)(it.q_layer0 + r) * a.B + b) * a.Hq + kvh * a.G + gh) * D;
+#pragma unroll
+  for (int j = 0; j < D / 32; ++j) {
+    const int ch = 32 * j + 8 * kg;
+    float q[8];
+    if (!valid) {
+#pragma unroll
+      for (int s = 0; s < 8; ++s) q[s] = 0.0f;
+    } else if (a.q_f32) {
+      const float4* qp = reinterpret_cast<const float4*>(static_cast<const float*>(a.q) + qrow + ch);
+      const float4 v0 = qp[0], v1 = qp[1];
+      q[0] = v0.x; q[1] = v0.y; q[2] = v0.z; q[3] = v0.w;
+      q[4] = v1.x; q[5] = v1.y; q[6] = v1.z; q[7] = v1.w;
     } else {
-      block_symrow<D, NCH, BITS>(u, qh, ql, blk, lane, sl2);
+      const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.q) + qrow + ch);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        q[2 * p] = __uint_as_float(w[p] << 16);
+        q[2 * p + 1] = __uint_as_float(w[p] & 0xffff0000u);
+      }
+    }
+    float h16[8], l16[8];
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      h16[s] = (float)(_Float16)q[s];
+      l16[s] = q[s] - h16[s];
+    }
+    qh[j] = to_half8(h16);
+    ql[j] = to_half8(l16);
+  }
+}
+
+// One work unit: 16 query rows over blocks [k0, k1) of one stream, ending with the
+// split partial (o[D], m, l) of every valid row.  Everything the unit keeps in
+// registers is local to this function, so that each precision gets its own
+// register allocation.
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& it, int sidx, int split,
+                                         int chunk, uint32_t* lds, int lane) {
+  constexpr int NR = ring_depth<BITS>();
+  constexpr int NM = D / 16;
+  constexpr int NX = (KIVI && BITS != 16) ? D / 32 : 0;
+  const int b = sidx / a.Hkv, kvh = sidx % a.Hkv;
+  const int i16 = lane & 15, kg = lane >> 4;
+  const int row = 16 * chunk + i16;
+  const int k0 = split * it.split_blocks;
+  const int k1 = min(a.nbf, k0 + it.split_blocks);
+  const uint8_t* stream = a.arena + it.region + (int64_t)sidx * it.stream_bytes;
+  const float sl2 = a.scale_log2;
+
+  Raw<D, BITS, KIVI> ring[NR];
+#pragma unroll
+  for (int i = 0; i < NR; ++i)
+    if (k0 + i < k1) load_raw<D, BITS, KIVI>(ring[i], stream + (int64_t)(k0 + i) * it.block_bytes, lane);
+
+  State<D> u;
+  u.m = -INFINITY;
+  u.l = 0.0f;
+#pragma unroll
+  for (int mt = 0; mt < NM; ++mt) u.o[mt] = f4{0.f, 0.f, 0.f, 0.f};
+  Extra<NX> ex;
+#pragma unroll
+  for (int g = 0; g < NX; ++g) ex.zo[g] = f4{0.f, 0.f, 0.f, 0.f};
+  half8 qh[D / 32], ql[D / 32];
+  load_query<D>(a, it, row, b, kvh, kg, qh, ql);
+  bf16x8 qbh[D / 32], qbl[D / 32];
+  if constexpr (BITS == 16) split_bf16<D>(qh, ql, qbh, qbl);
+
+  for (int k = k0; k < k1; k += NR) {
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      if (k + i < k1) {
+        if constexpr (BITS == 16) compute_bf16<D, KIVI>(u, qbh, qbl, ring[i], lane, 32, sl2);
+        else if constexpr (KIVI) compute_kivi<D, BITS>(u, ex, qh, ql, ring[i], lds, lane, sl2);
+        else compute_symrow<D, BITS>(u, qh, ql, ring[i], lane, sl2);
+        const int kn = k + i + NR;
+        if (kn < k1) load_raw<D, BITS, KIVI>(ring[i], stream + (int64_t)kn * it.block_bytes, lane);
+      }
     }
   }
-  if (k1 > a.nbf) {  // this split holds the tail block
-    if constexpr (BITS != 16) make_qb16<D, NCH>(u, qb);
-    block_bf16<D, NCH>(u, qb, stream + (int64_t)a.nb_cap * it.block_bytes, lane, a.ntail, sl2);
+
+  // partial: (o[D], m, l, pad, pad) per row
+  float* base = a.ws + it.ws_off + ((int64_t)sidx * it.nsplit + split) * it.geff * (D + 4);
+  const float lt = wave_sum_kg(u.l);
+  if (row < it.geff) {
+    float* pr = base + (int64_t)row * (D + 4);
+#pragma unroll
+    for (int mt = 0; mt < NM; ++mt) {
+      f4 o = u.o[mt];
+      if constexpr (NX > 0) o += ex.zo[mt / 2];  // value zero-point sums of the channel group
+      *reinterpret_cast<f4*>(pr + 16 * mt + 4 * kg) = o;
+    }
+    if (kg == 0) {
+      pr[D] = u.m;
+      pr[D + 1] = lt;
+    }
   }
 }
 
 template <int D, bool KIVI>
-__global__ __launch_bounds__(256) void gqa_decode_kernel(DecodeArgs a) {
-  constexpr int NJ = D / 32, NM = D / 16;
+__global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
+  __shared__ uint32_t lds_meta[4][2 * D];  // per-wave KIVI32 metadata slot (8D bytes)
   const int lane = threadIdx.x & 63;
-  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wslot = threadIdx.x >> 6;
+  const int wave = blockIdx.x * 4 + wslot;
   if (wave >= a.total_waves) return;
   int ii = 0;
   while (ii + 1 < a.n_items && a.items[ii + 1].wave_begin <= wave) ++ii;
@@ -452,68 +512,18 @@ __global__ __launch_bounds__(256) void gqa_decode_kernel(DecodeArgs a) {
   if (unit >= a.B * a.Hkv * it.nsplit || 16 * chunk >= it.geff) return;  // alignment padding
   const int split = unit % it.nsplit;
   const int sidx = unit / it.nsplit;  // b * Hkv + kvh
-  const int b = sidx / a.Hkv, kvh = sidx % a.Hkv;
-  const int i16 = lane & 15, kg = lane >> 4;
-  const int row = 16 * chunk + i16;  // query row of this lane: (reader layer, head in group)
-
-  Unit<D, 1> u;
-  u.m[0] = -INFINITY;
-  u.l[0] = 0.0f;
-#pragma unroll
-  for (int mt = 0; mt < NM; ++mt) u.o[0][mt] = f4{0.f, 0.f, 0.f, 0.f};
-  {
-    const bool valid = row < it.geff;
-    const int r = row / a.G, gh = row % a.G;
-    const int64_t qrow = (((int64_t)(it.q_layer0 + r) * a.B + b) * a.Hq + kvh * a.G + gh) * D;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int ch = 32 * j + 8 * kg;
-      if (!valid) {
-#pragma unroll
-        for (int s = 0; s < 8; ++s) u.q[0][j][s] = 0.0f;
-      } else if (a.q_f32) {
-        const float4* qp = reinterpret_cast<const float4*>(static_cast<const float*>(a.q) + qrow + ch);
-        const float4 v0 = qp[0], v1 = qp[1];
-        u.q[0][j][0] = v0.x; u.q[0][j][1] = v0.y; u.q[0][j][2] = v0.z; u.q[0][j][3] = v0.w;
-        u.q[0][j][4] = v1.x; u.q[0][j][5] = v1.y; u.q[0][j][6] = v1.z; u.q[0][j][7] = v1.w;
-      } else {
-        const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(a.q) + qrow + ch);
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          u.q[0][j][2 * p] = __uint_as_float(w[p] << 16);
-          u.q[0][j][2 * p + 1] = __uint_as_float(w[p] & 0xffff0000u);
-        }
-      }
-    }
-  }
-
-  const int nblk = a.nbf + (a.ntail > 0 ? 1 : 0);
-  const int k0 = split * it.split_blocks;
-  const int k1 = min(nblk, k0 + it.split_blocks);
-  const uint8_t* stream = a.arena + it.region + (int64_t)sidx * it.stream_bytes;
+  uint32_t* lds = lds_meta[wslot];
   switch (it.bits) {
-    case 16: run_stream<D, 1, 16, KIVI>(u, stream, a, it, k0, k1, lane); break;
-    case 8: run_stream<D, 1, 8, KIVI>(u, stream, a, it, k0, k1, lane); break;
-    case 4: run_stream<D, 1, 4, KIVI>(u, stream, a, it, k0, k1, lane); break;
-    default: run_stream<D, 1, 2, KIVI>(u, stream, a, it, k0, k1, lane); break;
-  }
-
-  // partials: rows of (o[D], m, l, pad, pad)
-  float* base = a.ws + it.ws_off + ((int64_t)sidx * it.nsplit + split) * it.geff * (D + 4);
-  const float lt = wave_sum_kg(u.l[0]);
-  if (row < it.geff) {
-    float* pr = base + (int64_t)row * (D + 4);
-#pragma unroll
-    for (int mt = 0; mt < NM; ++mt) *reinterpret_cast<f4*>(pr + 16 * mt + 4 * kg) = u.o[0][mt];
-    if (kg == 0) {
-      pr[D] = u.m[0];
-      pr[D + 1] = lt;
-    }
+    case 16: run_unit<D, 16, KIVI>(a, it, sidx, split, chunk, lds, lane); break;
+    case 8: run_unit<D, 8, KIVI>(a, it, sidx, split, chunk, lds, lane); break;
+    case 4: run_unit<D, 4, KIVI>(a, it, sidx, split, chunk, lds, lane); break;
+    default: run_unit<D, 2, KIVI>(a, it, sidx, split, chunk, lds, lane); break;
   }
 }
 
-// Merge the splits of every output row by log-sum-exp: one wave per (layer, b, head).
+// Merge the splits of every output row by log-sum-exp, together with the bf16 tail
+// tokens (fewer than 32), which this kernel attends to directly: one wave per
+// (layer, b, head).
 template <int D>
 __global__ __launch_bounds__(256) void gqa_combine_kernel(CombineArgs a) {
   const int lane = threadIdx.x & 63;
@@ -525,19 +535,45 @@ __global__ __launch_bounds__(256) void gqa_combine_kernel(CombineArgs a) {
   const int item = a.layer_item[li];
   const int slot = a.layer_slot0[li] + h % a.G;
   const int kvh = h / a.G;
+  const int sidx = b * a.Hkv + kvh;
   const int nsplit = a.item_nsplit[item], geff = a.item_geff[item];
-  const float* base = a.ws + a.item_ws_off[item] +
-                      (((int64_t)(b * a.Hkv + kvh) * nsplit) * geff + slot) * (D + 4);
+  const float* base = a.ws + a.item_ws_off[item] + (((int64_t)sidx * nsplit) * geff + slot) * (D + 4);
   const int64_t stride = (int64_t)geff * (D + 4);
-  float mstar = -INFINITY;
+
+  // tail scores: lane t < ntail takes token t
+  const uint8_t* tail = a.arena + a.item_tail[item] + (int64_t)sidx * a.item_stream_bytes[item];
+  float st = -INFINITY;
+  if (lane < a.ntail) {
+    const int64_t qoff = (int64_t)row * D;
+    float acc = 0.0f;
+    for (int c0 = 0; c0 < D; c0 += 8) {
+      const uint4 kw = *reinterpret_cast<const uint4*>(tail + k_bf16_byte(D, lane, c0));
+      const uint32_t w[4] = {kw.x, kw.y, kw.z, kw.w};
+      float q[8];
+      if (a.q_f32) {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) q[s] = static_cast<const float*>(a.q)[qoff + c0 + s];
+      } else {
+#pragma unroll
+        for (int s = 0; s < 8; ++s) q[s] = bf16_to_f32(static_cast<const uint16_t*>(a.q)[qoff + c0 + s]);
+      }
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        acc = fmaf(q[2 * p], __uint_as_float(w[p] << 16), acc);
+        acc = fmaf(q[2 * p + 1], __uint_as_float(w[p] & 0xffff0000u), acc);
+      }
+    }
+    st = acc * a.scale_log2;
+  }
+  float mstar = st;
   for (int s = lane; s < nsplit; s += 64) mstar = fmaxf(mstar, base[s * stride + D]);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) mstar = fmaxf(mstar, __shfl_xor(mstar, off));
-  float lsum = 0.0f;
   constexpr int PER = D / 64;
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.0f;
+  float lsum = 0.0f;
   for (int s = 0; s < nsplit; ++s) {
     const float* p = base + s * stride;
     const float ms = p[D];
@@ -545,6 +581,16 @@ __global__ __launch_bounds__(256) void gqa_combine_kernel(CombineArgs a) {
     lsum = fmaf(w, p[D + 1], lsum);
 #pragma unroll
     for (int e = 0; e < PER; ++e) acc[e] = fmaf(w, p[lane + 64 * e], acc[e]);
+  }
+  const float pt = (st == -INFINITY) ? 0.0f : exp2f(st - mstar);
+  for (int t = 0; t < a.ntail; ++t) {
+    const float w = __shfl(pt, t);
+    lsum += w;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) {
+      const uint16_t vb = *reinterpret_cast<const uint16_t*>(tail + v_bf16_byte(D, t, lane + 64 * e));
+      acc[e] = fmaf(w, bf16_to_f32(vb), acc[e]);
+    }
   }
   const float inv = lsum > 0.0f ? 1.0f / lsum : 0.0f;
   float* o = a.out + (int64_t)row * D;
@@ -588,7 +634,6 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   const int32_t G = d.n_q_heads / d.n_kv_heads;
   const int32_t D = d.head_dim;
   const int32_t nbf = n_stored / KVK_GROUP, ntail = n_stored % KVK_GROUP;
-  const int32_t nblk = nbf + (ntail > 0 ? 1 : 0);
   DecodeArgs& a = P.d1;
   CombineArgs& ca = P.c1;
   a.arena = static_cast<const uint8_t*>(arena);
@@ -606,6 +651,12 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   a.n_items = 0;
   ca.out = out;
   ca.ws = static_cast<const float*>(workspace);
+  ca.arena = static_cast<const uint8_t*>(arena);
+  ca.q = q;
+  ca.q_f32 = q_dtype == KVK_F32;
+  ca.scale_log2 = scale * kLog2e;
+  ca.ntail = ntail;
+  ca.nb_cap = t->nb_cap;
   ca.B = d.batch;
   ca.Hq = d.n_q_heads;
   ca.Hkv = d.n_kv_heads;
@@ -631,7 +682,7 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
       it.q_layer0 = rb - l0;
       it.geff = G * (re - rb);
       it.split_blocks = split_blocks_for(it.bits, d.qscheme, D);
-      it.nsplit = n_splits(nblk, it.split_blocks);
+      it.nsplit = n_splits(nbf, it.split_blocks);
       const int nch = (it.geff + 15) / 16;
       it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : 4);
       waves = (waves + 3) / 4 * 4;  // a chunk group never straddles a workgroup
@@ -642,6 +693,8 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
       ca.item_ws_off[n] = it.ws_off;
       ca.item_nsplit[n] = it.nsplit;
       ca.item_geff[n] = it.geff;
+      ca.item_tail[n] = it.region + (int64_t)t->nb_cap * it.block_bytes;
+      ca.item_stream_bytes[n] = it.stream_bytes;
       item_of_anchor[anc] = n;
     }
     const int ii = item_of_anchor[anc];
@@ -656,7 +709,7 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   a.total_waves = (int32_t)waves;
   P.kivi = d.qscheme == KVK_Q_KIVI32;
   P.head_dim = D;
-  P.any_blocks = nblk > 0 && waves > 0;
+  P.any_blocks = nbf > 0 && waves > 0;
   return KVK_OK;
 }
 
@@ -712,13 +765,14 @@ extern "C" kvk_status kvk_decode_splits(const kvk_table* t, int32_t l0, int32_t 
   return launch_d1(P, stream);
 }
 
-extern "C" kvk_status kvk_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored,
+extern "C" kvk_status kvk_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
+                                       int32_t q_dtype, int32_t n_stored, float scale,
+                                       const void* w_uk, const void* w_uv, const void* arena,
                                        const void* workspace, size_t ws_bytes, float* out,
                                        hipStream_t stream) {
   DecodePlan P;
-  // q and arena are not read by the merge; the workspace stands in for them in validation.
-  kvk_status st = prepare(t, l0, l1, workspace, KVK_F32, n_stored, 1.0f, nullptr, nullptr, workspace,
-                          out, const_cast<void*>(workspace), ws_bytes, P);
+  kvk_status st = prepare(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out,
+                          const_cast<void*>(workspace), ws_bytes, P);
   if (st != KVK_OK) return st;
   return launch_c1(P, stream);
 }

@@ -178,7 +178,7 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
   const kvk_dims& d = t->d;
   const int32_t G = d.n_q_heads / d.n_kv_heads;
   // Split partials: per query row (layer, b, head) and split, (o[d_h], m, l, 2 pad) in fp32.
-  const int32_t nblk = t->nb_cap + 1;
+  const int32_t nblk = t->nb_cap;  // full blocks; the tail is merged by the combine kernel
   size_t floats = 0;
   for (int l = l0; l < l1; ++l) {
     const int32_t a = t->info.anchor_of[l];

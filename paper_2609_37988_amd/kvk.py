@@ -71,7 +71,7 @@ def load() -> ctypes.CDLL:
             "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
             "kvk_decode_attention": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_splits": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P]),
-            "kvk_decode_merge": (I32, [P, I32, I32, I32, P, ctypes.c_size_t, P, P]),
+            "kvk_decode_merge": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P, P]),
             "kvk_read_bytes": (I32, [P, I32, I32, I32, ctypes.POINTER(ctypes.c_int64)]),
             "kvk_debug_dequantize": (I32, [P, I32, I32, P, P, P, P]),
             "kvk_realized_bits": (ctypes.c_double, [I32, I32, I32, I64, I64]),
@@ -265,15 +265,21 @@ def decode_splits(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n
         _ptr(w_uk), _ptr(w_uv), _ptr(arena), _ptr(workspace), _nbytes(workspace), _stream(stream)))
 
 
-def decode_merge(t: Table, layer_begin: int, layer_end: int, n_stored: int, workspace: torch.Tensor,
-                 out: torch.Tensor, stream=None):
-    """Second phase of decode_attention: merge the split partials into `out`."""
+def decode_merge(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_stored: int,
+                 scale: float, arena: torch.Tensor, workspace: torch.Tensor, out: torch.Tensor,
+                 w_uk: Optional[torch.Tensor] = None, w_uv: Optional[torch.Tensor] = None,
+                 stream=None):
+    """Second phase of decode_attention: tail tokens + merge of the split partials."""
     d = t.dims
     rows = (layer_end - layer_begin) * d.batch * d.n_q_heads * d.head_dim
+    _need(q.is_contiguous() and q.numel() == rows, "q must be contiguous, layers*B*Hq*d_h")
     _need(out.is_contiguous() and out.dtype == torch.float32 and out.numel() == rows,
           "out must be contiguous fp32, layers*B*Hq*d_h")
-    _check(load().kvk_decode_merge(t.handle, layer_begin, layer_end, n_stored, _ptr(workspace),
-                                   _nbytes(workspace), _ptr(out), _stream(stream)))
+    _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
+    _check(load().kvk_decode_merge(
+        t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
+        _ptr(w_uk), _ptr(w_uv), _ptr(arena), _ptr(workspace), _nbytes(workspace), _ptr(out),
+        _stream(stream)))
 
 
 def read_bytes(t: Table, layer_begin: int, layer_end: int, n_stored: int) -> int:
