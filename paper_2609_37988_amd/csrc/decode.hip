@@ -203,12 +203,14 @@ __device__ __forceinline__ void softmax_update(State<D>& u, Extra<NX>& ex, float
 #pragma unroll
   for (int e = 1; e < 8; ++e) mb = fmaxf(mb, x[e]);
   mb = wave_max_kg(mb);
+  // Every logit of a full block is finite; the first block has u.m = -inf and
+  // alpha = 2^-inf = 0.
   const float mnew = fmaxf(u.m, mb);
-  const float alpha = (u.m == -INFINITY) ? 0.0f : exp2f(u.m - mnew);
+  const float alpha = __builtin_amdgcn_exp2f(u.m - mnew);
   float ps = 0.0f;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const float p = (x[e] == -INFINITY) ? 0.0f : exp2f(x[e] - mnew);
+    const float p = __builtin_amdgcn_exp2f(x[e] - mnew);
     x[e] = p;
     ps += p;
   }
@@ -229,11 +231,11 @@ __device__ __forceinline__ half8 to_half8(const float (&x)[8]) {
   return r;
 }
 
-// bf16 block (a b = 16 layer's block, or any layer's tail) with `nvalid` tokens.
+// A bf16 block (b = 16 layers).
 template <int D, bool K>
 __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D / 32],
                                              const bf16x8 (&qbl)[D / 32], const Raw<D, 16, K>& r,
-                                             int lane, int nvalid, float sl2) {
+                                             int lane) {
   constexpr int NJ = D / 32, NM = D / 16;
   const int kg = lane >> 4;
   float x[8];
@@ -248,8 +250,7 @@ __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D 
       acc = mfmab(kop, qbl[j], acc);
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e)
-      x[4 * tau + e] = (16 * tau + 4 * kg + e) < nvalid ? acc[e] * sl2 : -INFINITY;
+    for (int e = 0; e < 4; ++e) x[4 * tau + e] = acc[e];  // the query carries scale * log2(e)
   }
   Extra<0> none;
   softmax_update<D, 0>(u, none, x);
@@ -275,7 +276,7 @@ __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D 
 template <int D, int BITS>
 __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, const half8 (&qh)[D / 32],
                                              const half8 (&ql)[D / 32], const Raw<D, BITS, true>& r,
-                                             uint32_t* lds, int lane, float sl2) {
+                                             uint32_t* lds, int lane) {
   using R = Raw<D, BITS, true>;
   constexpr int NJ = D / 32, NG = D / 32;
   const int kg = lane >> 4;
@@ -307,7 +308,7 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
 #pragma unroll
   for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) x[4 * tau + e] = (acc[tau][e] + zt[e]) * sl2;
+    for (int e = 0; e < 4; ++e) x[4 * tau + e] = acc[tau][e] + zt[e];
   softmax_update<D, D / 32>(u, ex, x);
   const half8 p = to_half8(x);
   // V: o_c = sum_t (p_t s_tg) u_tc + sum_t p_t z_tg, g = c / 32.
@@ -331,7 +332,7 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
 template <int D, int BITS>
 __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D / 32],
                                                const half8 (&ql)[D / 32], const Raw<D, BITS, false>& r,
-                                               int lane, float sl2) {
+                                               int lane) {
   constexpr int NJ = D / 32, NM = D / 16;
   const float off = (float)(1 << (BITS - 1));
   float x[8];
@@ -348,7 +349,7 @@ __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D 
     const float sk[4] = {__uint_as_float(s01 << 16), __uint_as_float(s01 & 0xffff0000u),
                          __uint_as_float(s23 << 16), __uint_as_float(s23 & 0xffff0000u)};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) x[4 * tau + e] = acc[e] * (sk[e] * sl2);
+    for (int e = 0; e < 4; ++e) x[4 * tau + e] = acc[e] * sk[e];
   }
   Extra<0> none;
   softmax_update<D, 0>(u, none, x);
@@ -390,7 +391,8 @@ __device__ __forceinline__ void split_bf16(const half8 (&qh)[D / 32], const half
   }
 }
 
-// Load the lane's query row as fp16 hi + lo (~22 significant bits).
+// Load the lane's query row times scale * log2(e), as fp16 hi + lo (~22 significant
+// bits), so that the score MFMAs produce base-2 logits directly.
 template <int D>
 __device__ __forceinline__ void load_query(const DecodeArgs& a, const DecodeItem& it, int row, int b, int kvh,
                                            int kg, half8 (&qh)[D / 32], half8 (&ql)[D / 32]) {
@@ -421,8 +423,9 @@ __device__ __forceinline__ void load_query(const DecodeArgs& a, const DecodeItem
     float h16[8], l16[8];
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
-      h16[s] = (float)(_Float16)q[s];
-      l16[s] = q[s] - h16[s];
+      const float qs = q[s] * a.scale_log2;
+      h16[s] = (float)(_Float16)qs;
+      l16[s] = qs - h16[s];
     }
     qh[j] = to_half8(h16);
     ql[j] = to_half8(l16);
@@ -445,8 +448,6 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
   const int k0 = split * it.split_blocks;
   const int k1 = min(a.nbf, k0 + it.split_blocks);
   const uint8_t* stream = a.arena + it.region + (int64_t)sidx * it.stream_bytes;
-  const float sl2 = a.scale_log2;
-
   Raw<D, BITS, KIVI> ring[NR];
 #pragma unroll
   for (int i = 0; i < NR; ++i)
@@ -469,9 +470,9 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
 #pragma unroll
     for (int i = 0; i < NR; ++i) {
       if (k + i < k1) {
-        if constexpr (BITS == 16) compute_bf16<D, KIVI>(u, qbh, qbl, ring[i], lane, 32, sl2);
-        else if constexpr (KIVI) compute_kivi<D, BITS>(u, ex, qh, ql, ring[i], lds, lane, sl2);
-        else compute_symrow<D, BITS>(u, qh, ql, ring[i], lane, sl2);
+        if constexpr (BITS == 16) compute_bf16<D, KIVI>(u, qbh, qbl, ring[i], lane);
+        else if constexpr (KIVI) compute_kivi<D, BITS>(u, ex, qh, ql, ring[i], lds, lane);
+        else compute_symrow<D, BITS>(u, qh, ql, ring[i], lane);
         const int kn = k + i + NR;
         if (kn < k1) load_raw<D, BITS, KIVI>(ring[i], stream + (int64_t)kn * it.block_bytes, lane);
       }

@@ -36,14 +36,23 @@ __device__ __forceinline__ half2v h2s(float a) { return h2(a, a); }
 // fp16 1024 + n has the integer n (n < 1024) in its low mantissa bits.
 constexpr uint32_t kMagic = 0x64006400u;
 
+// (a & b) | c in one v_and_or_b32.  The operands are register operands: the gfx9
+// VOP3 encoding takes no 32-bit literal, so constant masks would otherwise split
+// the operation into a separate AND and OR.
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // b = 4: one 32-bit chunk, slot s at bit 16*(s%2) + 4*(s/2).  Returns the 8 codes
 // minus `off` as exact fp16 integers, slot pairs (0,1),(2,3),(4,5),(6,7).
 __device__ __forceinline__ half8 unpack4(uint32_t w, float off) {
   const uint32_t w8 = w >> 8;
-  half2v a = bitcast<half2v>((w & 0x000F000Fu) | kMagic);   // 1024 + u
-  half2v b = bitcast<half2v>((w & 0x00F000F0u) | kMagic);   // 1024 + 16 u
-  half2v c = bitcast<half2v>((w8 & 0x000F000Fu) | kMagic);
-  half2v d = bitcast<half2v>((w8 & 0x00F000F0u) | kMagic);
+  half2v a = bitcast<half2v>(and_or(w, 0x000F000Fu, kMagic));   // 1024 + u
+  half2v b = bitcast<half2v>(and_or(w, 0x00F000F0u, kMagic));   // 1024 + 16 u
+  half2v c = bitcast<half2v>(and_or(w8, 0x000F000Fu, kMagic));
+  half2v d = bitcast<half2v>(and_or(w8, 0x00F000F0u, kMagic));
   const half2v lo = h2s(-1024.0f - off);
   const half2v sx = h2s(0.0625f), hi = h2s(-64.0f - off);
   a = a + lo;
@@ -60,7 +69,7 @@ __device__ __forceinline__ half8 unpack2_half(uint32_t w, float off) {
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const float scale = 1.0f / (float)(1 << (2 * v));
-    half2v x = bitcast<half2v>((w & (0x00030003u << (2 * v))) | kMagic);  // 1024 + u*4^v
+    half2v x = bitcast<half2v>(and_or(w, 0x00030003u << (2 * v), kMagic));  // 1024 + u*4^v
     r[v] = __builtin_elementwise_fma(x, h2s(scale), h2s(-1024.0f * scale - off));
   }
   return cat4(r[0], r[1], r[2], r[3]);
