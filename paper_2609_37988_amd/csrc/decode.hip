@@ -125,44 +125,77 @@ struct Raw {
   uint32_t m[MB > 0 ? MB / 4 : 1];
 };
 
+// Stream loads go through a buffer resource whose range ends at the last byte of
+// the split: a prefetch past the split returns zeros without touching memory, so
+// the prefetch ring is reloaded without branches and the compiler can count the
+// outstanding loads exactly (a branch around a reload makes it wait for all of
+// them).
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+
+__device__ __forceinline__ Rsrc stream_rsrc(const uint8_t* base, int nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, nbytes, 0x00020000);
+}
+
+// voff: the lane's byte offset inside the part (a vector register shared by all
+// blocks); soff: the block and part offset (a scalar register).
 template <int N>
-__device__ __forceinline__ void load_words(const uint8_t* p, uint32_t* w) {
+__device__ __forceinline__ void load_words(Rsrc rs, int voff, int soff, uint32_t* w) {
   if constexpr (N % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < N / 4; ++i) {
-      const uint4 x = reinterpret_cast<const uint4*>(p)[i];
-      w[4 * i] = x.x; w[4 * i + 1] = x.y; w[4 * i + 2] = x.z; w[4 * i + 3] = x.w;
+      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + 16 * i, soff, 0);
+      w[4 * i] = x[0]; w[4 * i + 1] = x[1]; w[4 * i + 2] = x[2]; w[4 * i + 3] = x[3];
     }
   } else if constexpr (N == 2) {
-    const uint2 x = *reinterpret_cast<const uint2*>(p);
-    w[0] = x.x; w[1] = x.y;
+    const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, 0);
+    w[0] = x[0]; w[1] = x[1];
   } else {
-    w[0] = *reinterpret_cast<const uint32_t*>(p);
+    w[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0);
   }
 }
 
-// Issue the loads of block `blk` for this lane (block layout of include/kvk.h).
+// Loads of the block at byte offset `blk` (wave-uniform) of the stream (block
+// layout of include/kvk.h), in the parts that are consumed at different times:
+// key codes (score phase), value codes (value phase), metadata.
 template <int D, int BITS, bool KIVI>
-__device__ __forceinline__ void load_raw(Raw<D, BITS, KIVI>& r, const uint8_t* blk, int lane) {
+__device__ __forceinline__ void load_k(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane) {
   using R = Raw<D, BITS, KIVI>;
   constexpr int tile = BITS == 16 ? 32 * D : 2 * D * BITS;
-  constexpr int vbase = BITS == 16 ? 64 * D : 4 * D * BITS;
 #pragma unroll
-  for (int tau = 0; tau < 2; ++tau) load_words<R::KB / 4>(blk + tau * tile + lane * R::KB, r.k[tau]);
-  load_words<R::VB / 4>(blk + vbase + lane * R::VB, r.v);
+  for (int tau = 0; tau < 2; ++tau) load_words<R::KB / 4>(rs, lane * R::KB, blk + tau * tile, r.k[tau]);
+}
+
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void load_v(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane) {
+  using R = Raw<D, BITS, KIVI>;
+  constexpr int vbase = BITS == 16 ? 64 * D : 4 * D * BITS;
+  load_words<R::VB / 4>(rs, lane * R::VB, blk + vbase, r.v);
+}
+
+// KIVI32: the lane's share of the 8D-byte metadata area.  SYMROW: part 0 the K
+// row scales (m[0..3]), part 1 the V row scales (m[4..7]) of the lane's tokens.
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void load_m(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane, int part) {
+  using R = Raw<D, BITS, KIVI>;
   if constexpr (BITS != 16) {
-    const uint8_t* meta = blk + 8 * D * BITS;
+    const int meta = blk + 8 * D * BITS;
     if constexpr (KIVI) {
-      load_words<R::MB / 4>(meta + lane * R::MB, r.m);  // the lane's share of the 8D-byte area
+      load_words<R::MB / 4>(rs, lane * R::MB, meta, r.m);
     } else {
       const int kg = lane >> 4;
 #pragma unroll
-      for (int tau = 0; tau < 2; ++tau) {
-        load_words<2>(meta + 2 * (16 * tau + 4 * kg), r.m + 2 * tau);       // K row scales
-        load_words<2>(meta + 64 + 2 * (16 * tau + 4 * kg), r.m + 4 + 2 * tau);  // V row scales
-      }
+      for (int tau = 0; tau < 2; ++tau)
+        load_words<2>(rs, 8 * kg, meta + 64 * part + 32 * tau, r.m + 4 * part + 2 * tau);
     }
   }
+}
+
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void load_raw(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane) {
+  load_k<D, BITS, KIVI>(r, rs, blk, lane);
+  load_v<D, BITS, KIVI>(r, rs, blk, lane);
+  load_m<D, BITS, KIVI>(r, rs, blk, lane, 0);
+  if constexpr (!KIVI) load_m<D, BITS, KIVI>(r, rs, blk, lane, 1);
 }
 
 // Unpack the 8 codes (one MFMA k-step) of chunk x from a lane's code words.
@@ -203,8 +236,8 @@ __device__ __forceinline__ void softmax_update(State<D>& u, Extra<NX>& ex, float
 #pragma unroll
   for (int e = 1; e < 8; ++e) mb = fmaxf(mb, x[e]);
   mb = wave_max_kg(mb);
-  // Every logit of a full block is finite; the first block has u.m = -inf and
-  // alpha = 2^-inf = 0.
+  // The first block of a unit is always a stored block, so mnew is finite from
+  // then on: the first alpha is 2^-inf = 0 and masked logits give p = 0.
   const float mnew = fmaxf(u.m, mb);
   const float alpha = __builtin_amdgcn_exp2f(u.m - mnew);
   float ps = 0.0f;
@@ -232,10 +265,13 @@ __device__ __forceinline__ half8 to_half8(const float (&x)[8]) {
 }
 
 // A bf16 block (b = 16 layers).
-template <int D, bool K>
+// Each compute_* function consumes ring entry `r` and, with RELOAD, refills each
+// part of it from the block at byte offset `next` as soon as that part has been
+// read, so that the registers stay in flight for as long as possible.
+template <int D, bool K, bool RELOAD>
 __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D / 32],
-                                             const bf16x8 (&qbl)[D / 32], const Raw<D, 16, K>& r,
-                                             int lane) {
+                                             const bf16x8 (&qbl)[D / 32], Raw<D, 16, K>& r, Rsrc rs,
+                                             int next, bool valid, int lane) {
   constexpr int NJ = D / 32, NM = D / 16;
   const int kg = lane >> 4;
   float x[8];
@@ -250,7 +286,11 @@ __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D 
       acc = mfmab(kop, qbl[j], acc);
     }
 #pragma unroll
-    for (int e = 0; e < 4; ++e) x[4 * tau + e] = acc[e];  // the query carries scale * log2(e)
+    for (int e = 0; e < 4; ++e) x[4 * tau + e] = valid ? acc[e] : -INFINITY;  // q carries scale*log2(e)
+  }
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);  // the refill may not rise above the reads it replaces
+    load_k<D, 16, K>(r, rs, next, lane);
   }
   Extra<0> none;
   softmax_update<D, 0>(u, none, x);
@@ -268,20 +308,28 @@ __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D 
     u.o[mt] = mfmab(vop, phi, u.o[mt]);
     u.o[mt] = mfmab(vop, plo, u.o[mt]);
   }
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_v<D, 16, K>(r, rs, next, lane);
+  }
 }
 
 // KIVI32 block of BITS-bit codes.  The block's metadata goes through the wave's
 // LDS slot so that the 16 lanes sharing a channel (or token) group read it by
 // broadcast.
-template <int D, int BITS>
+template <int D, int BITS, bool RELOAD>
 __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, const half8 (&qh)[D / 32],
-                                             const half8 (&ql)[D / 32], const Raw<D, BITS, true>& r,
-                                             uint32_t* lds, int lane) {
+                                             const half8 (&ql)[D / 32], Raw<D, BITS, true>& r, Rsrc rs,
+                                             int next, bool valid, uint32_t* lds, int lane) {
   using R = Raw<D, BITS, true>;
   constexpr int NJ = D / 32, NG = D / 32;
   const int kg = lane >> 4;
 #pragma unroll
   for (int i = 0; i < R::MB / 4; ++i) lds[lane * (R::MB / 4) + i] = r.m[i];
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_m<D, BITS, true>(r, rs, next, lane, 0);
+  }
   const half8* kmeta = reinterpret_cast<const half8*>(lds);  // scale[D], zero[D], V meta[2D]
   // K: S = sum_c (q_c s_c) u_c + sum_c q_c z_c.  q' = q s as fp16 hi + lo (error-free
   // product of the fp16 hi part, rounded sum with the lo part).
@@ -304,11 +352,15 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
     }
     __builtin_amdgcn_sched_barrier(0);  // keep one k-step's operands live at a time
   }
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_k<D, BITS, true>(r, rs, next, lane);
+  }
   float x[8];
 #pragma unroll
   for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
-    for (int e = 0; e < 4; ++e) x[4 * tau + e] = acc[tau][e] + zt[e];
+    for (int e = 0; e < 4; ++e) x[4 * tau + e] = valid ? acc[tau][e] + zt[e] : -INFINITY;
   softmax_update<D, D / 32>(u, ex, x);
   const half8 p = to_half8(x);
   // V: o_c = sum_t (p_t s_tg) u_tc + sum_t p_t z_tg, g = c / 32.
@@ -326,13 +378,17 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
     }
     __builtin_amdgcn_sched_barrier(0);
   }
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_v<D, BITS, true>(r, rs, next, lane);
+  }
 }
 
 // SYMROW block: per-token scales factor out of both contractions.
-template <int D, int BITS>
+template <int D, int BITS, bool RELOAD>
 __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D / 32],
-                                               const half8 (&ql)[D / 32], const Raw<D, BITS, false>& r,
-                                               int lane) {
+                                               const half8 (&ql)[D / 32], Raw<D, BITS, false>& r,
+                                               Rsrc rs, int next, bool valid, int lane) {
   constexpr int NJ = D / 32, NM = D / 16;
   const float off = (float)(1 << (BITS - 1));
   float x[8];
@@ -349,7 +405,12 @@ __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D 
     const float sk[4] = {__uint_as_float(s01 << 16), __uint_as_float(s01 & 0xffff0000u),
                          __uint_as_float(s23 << 16), __uint_as_float(s23 & 0xffff0000u)};
 #pragma unroll
-    for (int e = 0; e < 4; ++e) x[4 * tau + e] = acc[e] * sk[e];
+    for (int e = 0; e < 4; ++e) x[4 * tau + e] = valid ? acc[e] * sk[e] : -INFINITY;
+  }
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_k<D, BITS, false>(r, rs, next, lane);
+    load_m<D, BITS, false>(r, rs, next, lane, 0);
   }
   Extra<0> none;
   softmax_update<D, 0>(u, none, x);
@@ -363,11 +424,20 @@ __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D 
     ps[4 * tau + 3] = x[4 * tau + 3] * __uint_as_float(s23 & 0xffff0000u);
   }
   const half8 p = to_half8(ps);
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_m<D, BITS, false>(r, rs, next, lane, 1);
+  }
 #pragma unroll
   for (int mt = 0; mt < NM; ++mt) u.o[mt] = mfma16(unpack_chunk<BITS>(r.v, mt, off), p, u.o[mt]);
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_v<D, BITS, false>(r, rs, next, lane);
+  }
 }
 
 // Blocks kept in flight per wave (registers): about 8-16 KiB of cache ahead of use.
+// The host rounds split lengths to a multiple of this depth (kvk::ring_depth_for).
 template <int BITS>
 constexpr int ring_depth() {
   return BITS == 16 ? 2 : (BITS == 8 ? 2 : (BITS == 4 ? 4 : 6));
@@ -448,11 +518,6 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
   const int k0 = split * it.split_blocks;
   const int k1 = min(a.nbf, k0 + it.split_blocks);
   const uint8_t* stream = a.arena + it.region + (int64_t)sidx * it.stream_bytes;
-  Raw<D, BITS, KIVI> ring[NR];
-#pragma unroll
-  for (int i = 0; i < NR; ++i)
-    if (k0 + i < k1) load_raw<D, BITS, KIVI>(ring[i], stream + (int64_t)(k0 + i) * it.block_bytes, lane);
-
   State<D> u;
   u.m = -INFINITY;
   u.l = 0.0f;
@@ -461,21 +526,28 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
   Extra<NX> ex;
 #pragma unroll
   for (int g = 0; g < NX; ++g) ex.zo[g] = f4{0.f, 0.f, 0.f, 0.f};
+  const int bb = it.block_bytes;
+  const Rsrc rs = stream_rsrc(stream, k1 * bb);  // loads past block k1-1 read zeros
+  Raw<D, BITS, KIVI> ring[NR];
+#pragma unroll
+  for (int i = 0; i < NR; ++i) load_raw<D, BITS, KIVI>(ring[i], rs, (k0 + i) * bb, lane);
+  // The query is issued after the ring so that both are waited for together.
   half8 qh[D / 32], ql[D / 32];
   load_query<D>(a, it, row, b, kvh, kg, qh, ql);
   bf16x8 qbh[D / 32], qbl[D / 32];
   if constexpr (BITS == 16) split_bf16<D>(qh, ql, qbh, qbl);
 
+  // Every reload is unconditional: ring entries past block k1-1 read zeros, and the
+  // blocks they stand for (only in a stream's last split, since splits are a
+  // multiple of NR blocks) enter with masked logits.
   for (int k = k0; k < k1; k += NR) {
 #pragma unroll
     for (int i = 0; i < NR; ++i) {
-      if (k + i < k1) {
-        if constexpr (BITS == 16) compute_bf16<D, KIVI>(u, qbh, qbl, ring[i], lane);
-        else if constexpr (KIVI) compute_kivi<D, BITS>(u, ex, qh, ql, ring[i], lds, lane);
-        else compute_symrow<D, BITS>(u, qh, ql, ring[i], lane);
-        const int kn = k + i + NR;
-        if (kn < k1) load_raw<D, BITS, KIVI>(ring[i], stream + (int64_t)kn * it.block_bytes, lane);
-      }
+      const int next = (k + i + NR) * bb;
+      const bool valid = k + i < k1;
+      if constexpr (BITS == 16) compute_bf16<D, KIVI, true>(u, qbh, qbl, ring[i], rs, next, valid, lane);
+      else if constexpr (KIVI) compute_kivi<D, BITS, true>(u, ex, qh, ql, ring[i], rs, next, valid, lds, lane);
+      else compute_symrow<D, BITS, true>(u, qh, ql, ring[i], rs, next, valid, lane);
     }
   }
 
@@ -501,12 +573,18 @@ template <int D, bool KIVI>
 __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
   __shared__ uint32_t lds_meta[4][2 * D];  // per-wave KIVI32 metadata slot (8D bytes)
   const int lane = threadIdx.x & 63;
-  const int wslot = threadIdx.x >> 6;
+  // Wave-uniform by construction; readfirstlane lets the compiler keep everything
+  // derived from it (work item, stream address, buffer resource) in scalar registers.
+  const int wslot = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wave = blockIdx.x * 4 + wslot;
   if (wave >= a.total_waves) return;
-  int ii = 0;
-  while (ii + 1 < a.n_items && a.items[ii + 1].wave_begin <= wave) ++ii;
-  const DecodeItem& it = a.items[ii];
+  int lo = 0, hi = a.n_items - 1;  // last item with wave_begin <= wave
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.items[mid].wave_begin <= wave) lo = mid;
+    else hi = mid - 1;
+  }
+  const DecodeItem& it = a.items[lo];
   const int local = wave - it.wave_begin;
   const int chunk = local % it.nchp;
   const int unit = local / it.nchp;
@@ -682,7 +760,7 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
       it.bits = t->bits[anc];
       it.q_layer0 = rb - l0;
       it.geff = G * (re - rb);
-      it.split_blocks = split_blocks_for(it.bits, d.qscheme, D);
+      it.split_blocks = split_blocks_for(it.bits, d.qscheme, D, nbf);
       it.nsplit = n_splits(nbf, it.split_blocks);
       const int nch = (it.geff + 15) / 16;
       it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : 4);

@@ -29,8 +29,14 @@ inline int64_t round256(int64_t n) { return (n + 255) / 256 * 256; }
 // Bytes of one 32-token block of a GQA stream with `bits`-bit codes.
 int64_t gqa_block_bytes(int32_t head_dim, int32_t bits, int32_t qscheme);
 
-// Tokens processed per split of the decode kernel for a `bits`-bit anchor.
-int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim);
+// Blocks the decode kernel keeps in flight per wave for a `bits`-bit anchor
+// (must equal the kernel's ring depth).
+int32_t ring_depth_for(int32_t bits);
+
+// Blocks processed per split of the decode kernel for a `bits`-bit anchor whose
+// streams hold n_blocks full blocks.  The split count never exceeds the one at a
+// larger n_blocks, so workspace sized at capacity covers every n_stored.
+int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks);
 
 // Number of decode splits of one stream holding `n_blocks` blocks.
 inline int32_t n_splits(int32_t n_blocks, int32_t split_blocks) {

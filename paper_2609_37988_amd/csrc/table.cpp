@@ -42,15 +42,28 @@ int64_t gqa_block_bytes(int32_t head_dim, int32_t bits, int32_t qscheme) {
   return 8 * D * bits + 128;                      // codes + bf16 row scales
 }
 
-int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim) {
-  // About 256 KiB of cache per wave: enough to amortise the query preparation and
-  // the split partial, small enough that the last wave of a launch ends soon.
-  const int64_t target = 256 * 1024;
-  int64_t bb = gqa_block_bytes(head_dim, bits, qscheme);
-  int64_t nb = target / bb;
-  if (nb < 4) nb = 4;
-  if (nb > 256) nb = 256;
-  return (int32_t)nb;
+int32_t ring_depth_for(int32_t bits) {
+  return bits == 16 ? 2 : (bits == 8 ? 2 : (bits == 4 ? 4 : 6));
+}
+
+int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks) {
+  // About 1 MiB of cache per wave: a wave pays one memory latency to start, so
+  // longer splits amortise it (and the split partial); the stream's blocks are
+  // divided evenly so that no split is a short remainder, in a multiple of the
+  // decode kernel's prefetch depth so that only a stream's last split runs past
+  // its end.
+#ifndef KVK_SPLIT_TARGET
+#define KVK_SPLIT_TARGET (1024 * 1024)
+#endif
+  const int64_t bb = gqa_block_bytes(head_dim, bits, qscheme);
+  const int64_t nr = ring_depth_for(bits);
+  int64_t target = KVK_SPLIT_TARGET / bb;
+  if (target < nr) target = nr;
+  const int64_t nb = n_blocks > 0 ? n_blocks : 1;
+  const int64_t nsplit = (nb + target - 1) / target;
+  int64_t per = (nb + nsplit - 1) / nsplit;
+  per = (per + nr - 1) / nr * nr;
+  return (int32_t)per;
 }
 
 }  // namespace kvk
@@ -182,7 +195,7 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
   size_t floats = 0;
   for (int l = l0; l < l1; ++l) {
     const int32_t a = t->info.anchor_of[l];
-    const int32_t sb = split_blocks_for(t->bits[a], d.qscheme, d.head_dim);
+    const int32_t sb = split_blocks_for(t->bits[a], d.qscheme, d.head_dim, nblk);
     floats += (size_t)d.batch * d.n_kv_heads * G * n_splits(nblk, sb) * (d.head_dim + 4);
   }
   *out = (size_t)round256((int64_t)(floats * sizeof(float)));

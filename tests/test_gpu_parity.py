@@ -181,7 +181,7 @@ def test_empty_cache_gives_zeros():
     assert torch.count_nonzero(out).item() == 0
 
 
-@pytest.mark.parametrize("bits,n", [(16, 2100), (2, 6000), (8, 3000)])
+@pytest.mark.parametrize("bits,n", [(16, 6000), (2, 23000), (8, 12000), (4, 9000)])
 def test_many_splits(bits, n):
     """Streams longer than one split: partials merged by log-sum-exp."""
     say(f"case splits bits={bits} n={n}")
