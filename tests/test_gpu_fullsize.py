@@ -1,0 +1,99 @@
+"""Full-size parity: the benchmark workloads at their real sizes, in the launch
+configuration bench.py times (all layers of the plan in one decode call), checked on
+sampled streams and output rows that the oracle computes one by one.
+
+For each sampled (layer, sequence, KV head): the layer's inputs are regenerated from
+the seeded generator, the anchor's stream is compressed by the oracle and compared
+byte for byte with the GPU arena, and the G output rows of that layer are compared
+with the oracle's attention (max|diff| <= 2e-3 * max|out| over the sampled rows).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import cache as OC
+from oracle import plan as OP
+from paper_2609_37988_amd import kvk, synth
+
+from gpu_common import TOL, meaningful, oracle_rows, say
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _run_workload(w, n_samples, seed):
+    n_tok = w.tokens
+    n_stored = w.keep_tokens if w.keep_tokens else n_tok
+    dims = kvk.make_dims(kvk.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, qscheme=w.qscheme,
+                         batch=w.batch, max_tokens=n_tok, keep_tokens=w.keep_tokens)
+    table = kvk.layer_table(dims, kvk.make_plan(w.plan))
+    info = kvk.table_query(table)
+    arena = torch.empty(info.arena_bytes, dtype=torch.uint8, device=DEV)
+    for l in range(w.n_layers):
+        if w.plan[l][0]:
+            continue
+        k, v = synth.kv_layer(w, l, device=DEV)
+        keep = synth.keep_positions(w, l, device=DEV) if w.keep_tokens else None
+        kvk.compress_layer(table, l, k, v, n_tok, keep, arena)
+        del k, v, keep
+    q = synth.queries(w, w.n_layers, device=DEV)
+    out = torch.empty((w.n_layers, w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device=DEV)
+    ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=DEV)
+    kvk.decode_attention(table, 0, w.n_layers, q, n_stored, w.softmax_scale(), arena, out, ws)
+    torch.cuda.synchronize()
+
+    od = OP.Dims(OP.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, qscheme=w.qscheme,
+                 batch=w.batch, max_tokens=n_tok, keep_tokens=w.keep_tokens)
+    G = w.n_q_heads // w.n_kv_heads
+    rng = np.random.default_rng(seed)
+    got_rows, ref_rows = [], []
+    for _ in range(n_samples):
+        l = int(rng.integers(w.n_layers))
+        b = int(rng.integers(w.batch))
+        h = int(rng.integers(w.n_kv_heads))
+        a = info.anchor_of[l]
+        bits = w.plan[a][1]
+        say(f"  sample layer {l} (anchor {a}, {bits} bits) b {b} kv head {h}")
+        k, v = synth.kv_layer(w, a, device=DEV)
+        ks, vs = k[b, h].float().cpu().numpy(), v[b, h].float().cpu().numpy()
+        del k, v
+        if w.keep_tokens:
+            keep = synth.keep_positions(w, a, device=DEV)[b, h].cpu().numpy()
+            ks, vs = OC.gather_kept(ks, keep), OC.gather_kept(vs, keep)
+        ref_stream = OC.compress_stream(od, bits, ks, vs)
+        sb = info.stream_bytes[a]
+        off = info.layer_offset[a] + (b * w.n_kv_heads + h) * sb
+        gpu_stream = arena[off:off + sb].cpu().numpy()
+        assert np.array_equal(meaningful(od, bits, gpu_stream, n_stored),
+                              meaningful(od, bits, ref_stream, n_stored)), f"stream bytes differ: {(l, b, h)}"
+        qrows = q[l, b, h * G:(h + 1) * G].float().cpu().numpy().astype(np.float64)
+        ref_rows.append(oracle_rows(od, bits, ref_stream, n_stored, qrows, w.softmax_scale()))
+        got_rows.append(out[l, b, h * G:(h + 1) * G].cpu().numpy())
+    got, ref = np.stack(got_rows), np.stack(ref_rows)
+    err = np.abs(got - ref).max() / np.abs(ref).max()
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
+    del arena, ws, out
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("variant", [None, "bf16"], ids=["int4", "bf16"])
+def test_qwen7b_shaped_stack(variant):
+    """28 layers, 28/4 heads, batch 8, context 8192."""
+    w = synth.workload(1, variant)
+    say(f"case {w.name}")
+    _run_workload(w, 6, 11)
+
+
+def test_qwen14b_shaped_mixed_stack():
+    """The benchmark workload: 48 layers, 40/8 heads, batch 32, context 8192, mixed plan."""
+    w = synth.workload(2)
+    say(f"case {w.name}")
+    _run_workload(w, 8, 12)
+
+
+def test_qwen14b_shaped_128k_eviction():
+    """48 layers, batch 4, context 131072 with half the positions kept, int2/int4 plan."""
+    w = synth.workload(4)
+    say(f"case {w.name}")
+    _run_workload(w, 4, 14)
