@@ -22,7 +22,8 @@ Modules:
   layout    — the arena byte layout (pack / unpack)
   attention — softmax attention, split/LSE merge, depth, eviction
   cache     — compress a layer to arena bytes and decode a step from them
+  mla       — the rank axis: MLA latent caches, their storage and attention
 
 Parity status per function is stated in each module's docstring.
 """
-from . import plan, quant, layout, attention, cache  # noqa: F401
+from . import plan, quant, layout, attention, cache, mla  # noqa: F401

@@ -1,0 +1,340 @@
+"""The rank axis: MLA latent caches, their storage and their attention (oracle).
+
+TEST INFRASTRUCTURE ONLY (see oracle/__init__.py).
+
+What an MLA layer stores (§2.1 "Rank", App. C.2): per token a latent c of width r,
+shared by every head, and a positional key k^R of width d_R, held after RoPE.  A
+layer that keeps width d stores only c[:d] (App. C.2: training zeroes the
+coordinates after d with a prefix mask, a deployed kernel writes only the first
+d).  Precision composes with rank (§2.2, eq. (1): cost (d + d_R) b):
+  * KIVI32: the grouped asymmetric quantiser of App. C.3 with groups of 32
+    consecutive stored channels of one token (the d latent coordinates followed
+    by the d_R positional ones; d and d_R are multiples of 32);
+  * SYMROW: the paper's own quantiser, one bf16 scale per stored vector, that is
+    one for c[:d] and one for k^R of each token.
+A layer at b = 16 stores the bf16 values.  The fp32 chains are those of
+oracle/quant.py.
+
+Attention (§2.1, App. C.2).  Head h has its own up-projections W_UK_h
+[nope, r] and W_UV_h [v, r].  Its content key of token t is W_UK_h c_t, its
+value W_UV_h c_t, its key the concatenation [W_UK_h c_t ; k^R_t], and its query
+[q_nope_h ; q_rope_h].  The oracle attends with exactly these reconstructed keys
+and values, the latent zero-padded beyond d.  Because the content key undergoes
+no RoPE the projection can be moved onto the query (App. C.2); the absorbed form
+is written out separately and agrees with the reconstruction to rounding, which
+is one of the pins.
+
+Storage layout: the one documented in include/kvk.h (MLA section), restated from
+its text as explicit (token, channel) -> address maps.
+
+Pins (tests/test_oracle_mla.py): absorbed == reconstructed; prefix mask ==
+truncation; a full-rank MLA whose up-projections select disjoint latent slices is
+multi-head attention over those slices (checked against the GQA oracle); T = 1
+gives W_UV c_0; q = 0 gives W_UV of the mean latent; the layout maps are
+bijections; the quantiser closed forms; block sizes against eq. (1) plus the
+stated metadata.
+"""
+from functools import lru_cache
+
+import numpy as np
+
+from . import attention as att
+from . import quant
+from .plan import (GROUP, KIVI32, MLA, Dims, anchor_of, arena_offsets, block_bytes, layer_bytes,
+                   stored_width, stream_bytes, tail_bytes)
+
+F32 = np.float32
+
+
+# ---------------------------------------------------------------------------
+# Layout of one 32-token block (include/kvk.h, MLA section)
+# ---------------------------------------------------------------------------
+
+@lru_cache(maxsize=None)
+def code_bitaddr(W: int, bits: int) -> np.ndarray:
+    """Bit address, from the block start, of the code of (token t, stored channel
+    c): int64 [32, W].  Token t's codes fill W*b/32 consecutive 32-bit words; word
+    w holds channels (32/b) w .. (32/b) (w+1) - 1 at:
+      b = 8: channel 4w + s at bit 8 s;
+      b = 4: channel 8w + s at bit 16 (s%2) + 4 (s/2);
+      b = 2: channel 16w + 8x + s at bit 16 (s%2) + 2 (s/2) + 8 x."""
+    per = 32 // bits
+    addr = np.full((32, W), -1, dtype=np.int64)
+    for t in range(32):
+        for c in range(W):
+            word = t * (W // per) + c // per
+            k = c % per
+            if bits == 8:
+                bit = 8 * k
+            elif bits == 4:
+                bit = 16 * (k % 2) + 4 * (k // 2)
+            else:
+                x, s = k // 8, k % 8
+                bit = 16 * (s % 2) + 2 * (s // 2) + 8 * x
+            addr[t, c] = 32 * word + bit
+    return addr
+
+
+def codes_bytes(W: int, bits: int) -> int:
+    return 32 * W * bits // 8
+
+
+def _pack(u: np.ndarray, addr: np.ndarray, bits: int, nbytes: int) -> np.ndarray:
+    """Codes u [n, 32, W] -> uint8 [n, nbytes], each code placed at its bit
+    address.  The map must cover every bit of the region exactly once."""
+    n = u.shape[0]
+    nwords = nbytes // 4
+    flat = addr.reshape(-1)
+    word = flat // 32
+    vals = u.reshape(n, -1).astype(np.uint64) << (flat % 32).astype(np.uint64)
+    order = np.argsort(word, kind="stable")
+    per = 32 // bits
+    assert np.array_equal(word[order], np.repeat(np.arange(nwords), per)), "layout not dense"
+    words = vals[:, order].reshape(n, nwords, per).sum(axis=-1)  # disjoint bits: sum == or
+    return np.ascontiguousarray(words.astype(np.uint32)).view(np.uint8).reshape(n, nbytes)
+
+
+def _unpack(raw: np.ndarray, addr: np.ndarray, bits: int) -> np.ndarray:
+    n = raw.shape[0]
+    words = np.ascontiguousarray(raw).view(np.uint32).reshape(n, -1).astype(np.int64)
+    flat = addr.reshape(-1)
+    return ((words[:, flat // 32] >> (flat % 32)) & ((1 << bits) - 1)).reshape(n, *addr.shape)
+
+
+def _u16_put(region, byte_off, vals):
+    v = np.asarray(vals).astype(np.uint16)
+    region[..., byte_off] = (v & 0xFF).astype(np.uint8)
+    region[..., byte_off + 1] = (v >> 8).astype(np.uint8)
+
+
+def _u16_get(region, byte_off):
+    return region[..., byte_off].astype(np.uint16) | (region[..., byte_off + 1].astype(np.uint16) << 8)
+
+
+def pack_bf16_block(x16: np.ndarray) -> np.ndarray:
+    """bf16 patterns [n, 32, W] -> uint8 [n, 64 W]: token-major, channel order."""
+    n, _, W = x16.shape
+    return np.ascontiguousarray(x16.astype(np.uint16)).view(np.uint8).reshape(n, 64 * W)
+
+
+def unpack_bf16_block(raw: np.ndarray, W: int) -> np.ndarray:
+    n = raw.shape[0]
+    return np.ascontiguousarray(raw[:, :64 * W]).view(np.uint16).reshape(n, 32, W)
+
+
+# ---------------------------------------------------------------------------
+# Quantisation of stored rows
+# ---------------------------------------------------------------------------
+
+def quantise_rows(dims: Dims, bits: int, d: int, X: np.ndarray) -> dict:
+    """X fp32 [n, 32, W] (W = d + d_R stored channels) -> fields of n blocks."""
+    n, _, W = X.shape
+    if dims.qscheme == KIVI32:
+        u, s, z = quant.kivi_quantize(X.reshape(n, 32, W // 32, 32), bits)
+        return {"u": u.reshape(n, 32, W), "s": s, "z": z}  # s, z fp16 [n, 32, W/32]
+    ul, sl = quant.symrow_quantize(X[..., :d], bits)
+    ur, sr = quant.symrow_quantize(X[..., d:], bits)
+    return {"u": np.concatenate([ul, ur], axis=-1), "sl": sl, "sr": sr}  # bf16 bits [n, 32]
+
+
+def dequantise_rows(dims: Dims, bits: int, d: int, f: dict) -> np.ndarray:
+    n, _, W = f["u"].shape
+    if dims.qscheme == KIVI32:
+        u = f["u"].reshape(n, 32, W // 32, 32)
+        return quant.kivi_dequantize(u, f["s"][..., None], f["z"][..., None]).reshape(n, 32, W)
+    lat = quant.symrow_dequantize(f["u"][..., :d], f["sl"][..., None], bits)
+    rope = quant.symrow_dequantize(f["u"][..., d:], f["sr"][..., None], bits)
+    return np.concatenate([lat, rope], axis=-1)
+
+
+def pack_quant_blocks(dims: Dims, bits: int, f: dict) -> np.ndarray:
+    """[codes: 32 W b / 8 bytes][meta]: KIVI32 meta holds per token, per group g of
+    32 stored channels, the fp16 scale then the fp16 zero at byte
+    4 (t (W/32) + g); SYMROW meta holds per token the bf16 scale of c[:d] then
+    that of k^R at byte 4 t."""
+    n, _, W = f["u"].shape
+    cb = codes_bytes(W, bits)
+    out = np.zeros((n, block_bytes(dims, bits, W - dims.rope_dim)), dtype=np.uint8)
+    out[:, :cb] = _pack(f["u"], code_bitaddr(W, bits), bits, cb)
+    if dims.qscheme == KIVI32:
+        G = W // 32
+        t, g = np.meshgrid(np.arange(32), np.arange(G), indexing="ij")
+        off = cb + 4 * (t * G + g)
+        _u16_put(out, off, f["s"].view(np.uint16))
+        _u16_put(out, off + 2, f["z"].view(np.uint16))
+    else:
+        off = cb + 4 * np.arange(32)
+        _u16_put(out, off, f["sl"])
+        _u16_put(out, off + 2, f["sr"])
+    return out
+
+
+def unpack_quant_blocks(dims: Dims, bits: int, d: int, raw: np.ndarray) -> dict:
+    W = d + dims.rope_dim
+    cb = codes_bytes(W, bits)
+    f = {"u": _unpack(raw[:, :cb], code_bitaddr(W, bits), bits)}
+    if dims.qscheme == KIVI32:
+        G = W // 32
+        t, g = np.meshgrid(np.arange(32), np.arange(G), indexing="ij")
+        off = cb + 4 * (t * G + g)
+        f["s"] = _u16_get(raw, off).view(np.float16)
+        f["z"] = _u16_get(raw, off + 2).view(np.float16)
+    else:
+        off = cb + 4 * np.arange(32)
+        f["sl"] = _u16_get(raw, off)
+        f["sr"] = _u16_get(raw, off + 2)
+    return f
+
+
+# ---------------------------------------------------------------------------
+# Streams (one per sequence)
+# ---------------------------------------------------------------------------
+
+def compress_stream(dims: Dims, bits: int, d: int, C: np.ndarray, R: np.ndarray) -> np.ndarray:
+    """Stored tokens of one sequence: latent C [n, >= d] and positional key
+    R [n, d_R] (fp32 values) -> stream bytes.  Only C[:, :d] is written."""
+    X = np.concatenate([np.asarray(C, F32)[:, :d], np.asarray(R, F32)], axis=1)
+    n, W = X.shape
+    nb, nt = divmod(n, GROUP)
+    Xf = X[:nb * GROUP].reshape(nb, GROUP, W)
+    if bits == 16:
+        blocks = pack_bf16_block(quant.bf16_bits(Xf))
+    else:
+        blocks = pack_quant_blocks(dims, bits, quantise_rows(dims, bits, d, Xf))
+    tail = np.zeros((1, GROUP, W), dtype=np.uint16)
+    tail[0, :nt] = quant.bf16_bits(X[nb * GROUP:])
+    sb = stream_bytes(dims, bits, d)
+    out = np.zeros(sb, dtype=np.uint8)
+    blk = block_bytes(dims, bits, d)
+    out[:nb * blk] = blocks.reshape(-1)
+    t0 = (dims.stored_cap // GROUP) * blk
+    out[t0:t0 + tail_bytes(dims, d)] = pack_bf16_block(tail)[0]
+    return out
+
+
+def dequant_stream(dims: Dims, bits: int, d: int, stream: np.ndarray, n_stored: int):
+    """Stream bytes -> (C_hat [n_stored, d], R_hat [n_stored, d_R]) fp32."""
+    W = d + dims.rope_dim
+    blk = block_bytes(dims, bits, d)
+    nb, nt = divmod(n_stored, GROUP)
+    raw = stream[:nb * blk].reshape(nb, blk)
+    if bits == 16:
+        X = quant.bf16_value(unpack_bf16_block(raw, W))
+    else:
+        X = dequantise_rows(dims, bits, d, unpack_quant_blocks(dims, bits, d, raw))
+    t0 = (dims.stored_cap // GROUP) * blk
+    tail = quant.bf16_value(unpack_bf16_block(stream[None, t0:t0 + tail_bytes(dims, d)], W))[0]
+    X = np.concatenate([X.reshape(-1, W), tail[:nt]])
+    return X[:, :d], X[:, d:]
+
+
+def compress_layer(dims: Dims, bits: int, d: int, C: np.ndarray, R: np.ndarray,
+                   keep=None) -> np.ndarray:
+    """C [B, n, r], R [B, n, d_R] -> the layer's region (B streams).  keep
+    [B, n_keep]: the stored stream is the tokens at these positions, in order."""
+    sb = stream_bytes(dims, bits, d)
+    out = np.zeros(layer_bytes(dims, bits, d), dtype=np.uint8)
+    for b in range(C.shape[0]):
+        c, r = C[b], R[b]
+        if keep is not None:
+            idx = np.sort(np.asarray(keep[b]))
+            c, r = c[idx], r[idx]
+        out[b * sb:(b + 1) * sb] = compress_stream(dims, bits, d, c, r)
+    return out
+
+
+def compress_arena(dims: Dims, plan, Cs, Rs, keeps=None) -> np.ndarray:
+    offs, total = arena_offsets(dims, plan)
+    arena = np.zeros(total, dtype=np.uint8)
+    for l, a in enumerate(plan):
+        if a.inherit:
+            continue
+        reg = compress_layer(dims, a.bits, a.rank, Cs[l], Rs[l], None if keeps is None else keeps[l])
+        arena[offs[l]:offs[l] + reg.size] = reg
+    return arena
+
+
+def dequant_layer(dims: Dims, plan, arena: np.ndarray, layer: int, n_stored: int):
+    """(C_hat [B, n, d], R_hat [B, n, d_R]) of the cache `layer` reads."""
+    a = anchor_of(plan)[layer]
+    offs, _ = arena_offsets(dims, plan)
+    bits, d = plan[a].bits, plan[a].rank
+    sb = stream_bytes(dims, bits, d)
+    Cs, Rs = [], []
+    for b in range(dims.batch):
+        s = offs[a] + b * sb
+        c, r = dequant_stream(dims, bits, d, arena[s:s + sb], n_stored)
+        Cs.append(c)
+        Rs.append(r)
+    return np.stack(Cs), np.stack(Rs)
+
+
+# ---------------------------------------------------------------------------
+# Attention
+# ---------------------------------------------------------------------------
+
+def attention_reconstructed(q_nope, q_rope, Chat, Rhat, W_UK, W_UV, scale):
+    """Explicit reconstruction (§2.1, App. C.2).  q_nope [H, nope], q_rope [H, d_R],
+    Chat [T, d], Rhat [T, d_R], W_UK [H, nope, r], W_UV [H, v, r] -> [H, v].
+    The latent is zero-padded from d to r; head h attends with keys
+    [W_UK_h c_t ; k^R_t] and values W_UV_h c_t."""
+    H, _, r = W_UK.shape
+    T, d = Chat.shape
+    C = np.zeros((T, r))
+    C[:, :d] = Chat
+    out = np.zeros((H, W_UV.shape[1]))
+    for h in range(H):
+        K = np.concatenate([C @ np.asarray(W_UK[h], np.float64).T, np.asarray(Rhat, np.float64)], axis=1)
+        V = C @ np.asarray(W_UV[h], np.float64).T
+        q = np.concatenate([q_nope[h], q_rope[h]])[None]
+        out[h] = att.softmax_attention(q, K, V, scale)[0]
+    return out
+
+
+def attention_absorbed(q_nope, q_rope, Chat, Rhat, W_UK, W_UV, scale):
+    """The same attention with the projections moved onto the query and the
+    output (App. C.2): q~_h = W_UK_h[:, :d]^T q_nope_h; scores
+    scale (q~_h . c_t + q_rope_h . k^R_t); o_lat = softmax . C; o_h = W_UV_h[:, :d] o_lat."""
+    H = W_UK.shape[0]
+    T, d = Chat.shape
+    C = np.asarray(Chat, np.float64)
+    R = np.asarray(Rhat, np.float64)
+    out = np.zeros((H, W_UV.shape[1]))
+    if T == 0:
+        return out
+    for h in range(H):
+        qt = np.asarray(W_UK[h], np.float64)[:, :d].T @ np.asarray(q_nope[h], np.float64)
+        s = scale * (C @ qt + R @ np.asarray(q_rope[h], np.float64))
+        p = np.exp(s - s.max())
+        olat = (p @ C) / p.sum()
+        out[h] = np.asarray(W_UV[h], np.float64)[:, :d] @ olat
+    return out
+
+
+def decode_step(dims: Dims, plan, arena: np.ndarray, q: np.ndarray, w_uk: np.ndarray,
+                w_uv: np.ndarray, n_stored: int, scale: float, l0: int = 0, l1=None) -> np.ndarray:
+    """q [l1-l0, B, Hq, nope + d_R], w_uk [l1-l0, Hq, nope, r], w_uv [l1-l0, Hq, v, r]
+    -> out fp64 [l1-l0, B, Hq, v]: each layer's own query and up-projections against
+    its anchor's stored latent (§2.1)."""
+    assert dims.kind == MLA
+    l1 = dims.n_layers if l1 is None else l1
+    anc = anchor_of(plan)
+    nope = dims.nope_dim
+    out = np.zeros((l1 - l0, dims.batch, dims.n_q_heads, dims.v_dim))
+    cache = {}
+    for l in range(l0, l1):
+        a = anc[l]
+        if a not in cache:
+            cache[a] = dequant_layer(dims, plan, arena, a, n_stored)
+        Ch, Rh = cache[a]
+        for b in range(dims.batch):
+            qb = np.asarray(q[l - l0, b], np.float64)
+            out[l - l0, b] = attention_reconstructed(qb[:, :nope], qb[:, nope:], Ch[b], Rh[b],
+                                                     w_uk[l - l0], w_uv[l - l0], scale)
+    return out
+
+
+__all__ = ["code_bitaddr", "codes_bytes", "quantise_rows", "dequantise_rows", "pack_quant_blocks",
+           "unpack_quant_blocks", "pack_bf16_block", "unpack_bf16_block", "compress_stream",
+           "dequant_stream", "compress_layer", "compress_arena", "dequant_layer",
+           "attention_reconstructed", "attention_absorbed", "decode_step", "stored_width"]

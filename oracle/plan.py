@@ -161,8 +161,23 @@ def round256(n: int) -> int:
     return (n + 255) // 256 * 256
 
 
-def block_bytes(dims: Dims, bits: int) -> int:
-    """Bytes of one 32-token block of one (b, KV head) stream."""
+def stored_width(dims: Dims, rank: int) -> int:
+    """MLA: scalars stored per token by a layer that keeps width d = rank, namely
+    the first d latent coordinates and the positional key, d + d_R (§2.1, App. C.2)."""
+    return rank + dims.rope_dim
+
+
+def block_bytes(dims: Dims, bits: int, rank: int = 0) -> int:
+    """Bytes of one 32-token block of one stream.  GQA: a (b, KV head) stream
+    holding K and V of width D; MLA: a (b) stream holding d + d_R scalars per
+    token."""
+    if dims.kind == MLA:
+        W = stored_width(dims, rank)
+        if bits == 16:
+            return 64 * W
+        if dims.qscheme == KIVI32:
+            return 4 * W * (bits + 1)
+        return 4 * W * bits + 128
     D = dims.head_dim
     if bits == 16:
         return 128 * D
@@ -171,17 +186,25 @@ def block_bytes(dims: Dims, bits: int) -> int:
     return 8 * D * bits + 128
 
 
-def tail_bytes(dims: Dims) -> int:
+def tail_bytes(dims: Dims, rank: int = 0) -> int:
+    if dims.kind == MLA:
+        return 64 * stored_width(dims, rank)
     return 128 * dims.head_dim
 
 
-def stream_bytes(dims: Dims, bits: int) -> int:
+def stream_bytes(dims: Dims, bits: int, rank: int = 0) -> int:
     nb = dims.stored_cap // GROUP
-    return round256(nb * block_bytes(dims, bits) + tail_bytes(dims))
+    return round256(nb * block_bytes(dims, bits, rank) + tail_bytes(dims, rank))
 
 
-def layer_bytes(dims: Dims, bits: int) -> int:
-    return dims.batch * dims.n_kv_heads * stream_bytes(dims, bits)
+def streams_per_layer(dims: Dims) -> int:
+    """GQA: one stream per (sequence, KV head); MLA: one per sequence (the latent
+    is shared by every head, §2.1)."""
+    return dims.batch * (dims.n_kv_heads if dims.kind == GQA else 1)
+
+
+def layer_bytes(dims: Dims, bits: int, rank: int = 0) -> int:
+    return streams_per_layer(dims) * stream_bytes(dims, bits, rank)
 
 
 def arena_offsets(dims: Dims, plan: Sequence[Action]):
@@ -192,15 +215,16 @@ def arena_offsets(dims: Dims, plan: Sequence[Action]):
             offs.append(-1)
         else:
             offs.append(cur)
-            cur += round256(layer_bytes(dims, a.bits))
+            cur += round256(layer_bytes(dims, a.bits, a.rank))
     return offs, cur
 
 
-def read_bytes_stream(dims: Dims, bits: int, n_stored: int) -> int:
+def read_bytes_stream(dims: Dims, bits: int, n_stored: int, rank: int = 0) -> int:
     """Algorithmic bytes a decode step reads from one stream holding n_stored
-    tokens: the full blocks plus the bf16 K and V of the tail tokens."""
+    tokens: the full blocks plus the bf16 values of the tail tokens."""
     nb, nt = divmod(n_stored, GROUP)
-    return nb * block_bytes(dims, bits) + nt * 4 * dims.head_dim
+    per_tail_token = 2 * stored_width(dims, rank) if dims.kind == MLA else 4 * dims.head_dim
+    return nb * block_bytes(dims, bits, rank) + nt * per_tail_token
 
 
 def read_bytes(dims: Dims, plan: Sequence[Action], l0: int, l1: int, n_stored: int) -> int:
@@ -208,8 +232,8 @@ def read_bytes(dims: Dims, plan: Sequence[Action], l0: int, l1: int, n_stored: i
     read by the range, read once."""
     anc = anchor_of(plan)
     used = sorted(set(anc[l] for l in range(l0, l1)))
-    per = dims.batch * dims.n_kv_heads
-    return sum(per * read_bytes_stream(dims, plan[a].bits, n_stored) for a in used)
+    per = streams_per_layer(dims)
+    return sum(per * read_bytes_stream(dims, plan[a].bits, n_stored, plan[a].rank) for a in used)
 
 
 def bf16_full_bytes(dims: Dims) -> int:
