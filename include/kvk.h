@@ -64,7 +64,8 @@ typedef enum { KVK_BF16 = 0, KVK_F32 = 1 } kvk_dtype;
 
 /* One plan entry (§2.2, eq. (3)).  inherit != 0 selects the zero-cost action;
  * otherwise bits is b in {2, 4, 8, 16} and rank is the kept width d.  For GQA
- * the rank axis does not exist (§2.2): rank must be 0 or 2*Hkv*d_h. */
+ * the rank axis does not exist (§2.2): rank must be 0 or 2*Hkv*d_h.  For MLA
+ * rank is d in {r/8, r/4, r/2, r} (eq. (3)). */
 typedef struct {
   int32_t inherit;
   int32_t bits;
@@ -73,19 +74,22 @@ typedef struct {
 
 /* Geometry of the cached model and of the arena. */
 typedef struct {
-  int32_t kind;        /* kvk_kind; KVK_MLA currently returns KVK_ERR_UNSUPPORTED */
+  int32_t kind;        /* kvk_kind */
   int32_t n_layers;    /* L, 1..KVK_MAX_LAYERS */
-  int32_t n_q_heads;   /* Hq */
-  int32_t n_kv_heads;  /* Hkv; Hq % Hkv == 0; Hq/Hkv * (readers of one anchor) <= 64 */
-  int32_t head_dim;    /* d_h in {64, 128} */
-  int32_t latent_dim;  /* MLA r (unused for GQA, pass 0) */
-  int32_t rope_dim;    /* MLA d_R (unused for GQA, pass 0) */
-  int32_t nope_dim;    /* MLA per-head no-RoPE query/key width (unused for GQA) */
-  int32_t v_dim;       /* MLA per-head value width (unused for GQA) */
+  int32_t n_q_heads;   /* Hq; MLA: a multiple of 32, at most 256 */
+  int32_t n_kv_heads;  /* GQA: Hkv; Hq % Hkv == 0; Hq/Hkv * (readers of one anchor) <= 64.
+                          MLA: KV heads of the bf16 GQA model the ratio eq. (2) is
+                          quoted against (C0 = L * 2 * Hkv * d_h * 16); >= 1 */
+  int32_t head_dim;    /* GQA: d_h in {64, 128}.  MLA: d_h of that reference model, >= 1 */
+  int32_t latent_dim;  /* MLA r: a multiple of 256, at most 512 (unused for GQA, pass 0) */
+  int32_t rope_dim;    /* MLA d_R: 64 (unused for GQA, pass 0) */
+  int32_t nope_dim;    /* MLA per-head no-RoPE query/key width: a multiple of 32, <= 256 */
+  int32_t v_dim;       /* MLA per-head value width: a multiple of 16, <= 256 */
   int32_t qscheme;     /* kvk_qscheme */
   int32_t batch;       /* B >= 1 */
   int32_t max_tokens;  /* prefill length capacity per sequence, >= 1 */
-  int32_t keep_tokens; /* 0: no eviction; else stored tokens per (sequence, KV head) */
+  int32_t keep_tokens; /* 0: no eviction; else stored tokens per stream (GQA: per
+                          (sequence, KV head); MLA: per sequence) */
 } kvk_dims;
 
 typedef struct kvk_table kvk_table;
@@ -95,7 +99,7 @@ typedef struct {
   int64_t arena_bytes;          /* bytes the caller allocates for the compressed cache */
   int64_t workspace_bytes;      /* decode workspace for the full layer range [0, L) */
   int32_t n_anchors;            /* layers that own a cache */
-  int32_t stored_tokens_cap;    /* stored tokens per (b, KV head): keep_tokens or max_tokens */
+  int32_t stored_tokens_cap;    /* stored tokens per stream: keep_tokens or max_tokens */
   double cost_bits_per_token;   /* sum over layers of c(a_l), eq. (1) */
   double c0_bits_per_token;     /* C0 = L * 2 * Hkv * d_h * 16, eq. (2) */
   double rho;                   /* eq. (2): C0 / sum c(a_l), metadata excluded (§3) */
@@ -105,7 +109,8 @@ typedef struct {
   int32_t anchor_of[KVK_MAX_LAYERS];   /* nearest anchor at or before l (§2.1) */
   int64_t layer_offset[KVK_MAX_LAYERS];/* byte offset of the layer's region; -1 if it inherits */
   int64_t layer_bytes[KVK_MAX_LAYERS]; /* region size (0 if it inherits) */
-  int64_t stream_bytes[KVK_MAX_LAYERS];/* bytes of one (b, KV head) stream of the layer */
+  int64_t stream_bytes[KVK_MAX_LAYERS];/* bytes of one stream of the layer (GQA: one
+                                          (b, KV head); MLA: one sequence b) */
   double layer_cost_bits[KVK_MAX_LAYERS]; /* c(a_l), eq. (1), bits per token */
   double layer_bits_per_elt[KVK_MAX_LAYERS]; /* stored bits per cached scalar at capacity,
                                                 metadata included (App. C.3 accounting) */
@@ -121,6 +126,8 @@ typedef struct {
  * block.  With n stored tokens, blocks 0 .. n/32-1 are full and the tail block
  * holds tokens 32*(n/32) .. n-1 (fewer than 32) in the bf16 block format, its
  * unused slots zero.  Stream and region sizes are rounded up to 256 bytes.
+ * Regions follow each other in layer order from offset 0; arena_bytes is their
+ * total.
  *
  * Within a 32-token block, positions are described by "lanes" lam = 16*kg + i
  * with kg in 0..3 and i in 0..15, D = d_h, and
@@ -172,6 +179,38 @@ typedef struct {
  *   KIVI32 (the scale and zero are fp16).
  */
 
+/*
+ * ARENA LAYOUT (MLA).  Rank axis, §2.1 and App. C.2: an MLA layer stores per token
+ * the first d coordinates of its latent c (d = the action's rank; the remaining
+ * r - d are never written) and the positional key k^R of width d_R (stored as
+ * given, after RoPE).  The W = d + d_R stored channels of a token are, in order,
+ * c[0..d-1] then k^R[0..d_R-1].
+ *
+ * The region of anchor layer l holds B streams, stream b (sequence b) at offset
+ * b*stream_bytes[l].  A stream holds NB = cap/32 full blocks of 32 tokens and one
+ * bf16 tail block, as for GQA; stream and region sizes are rounded up to 256.
+ *
+ * bf16 block (bits = 16, and every tail block), 64*W bytes: token t's W bf16
+ *   values at byte 2*W*t, channel c at byte 2*W*t + 2*c (round-to-nearest-even
+ *   bf16 of the input).  Unused tail rows are zero.
+ * quantised block (bits b in {2, 4, 8}): [codes: 4*W*b bytes][meta]
+ *   codes: token t's codes fill the W*b/32 consecutive 32-bit words starting at
+ *     word t*(W*b/32); word w of the token holds its channels (32/b)*w + k,
+ *     k = 0 .. 32/b - 1:
+ *       b = 8: k at bit 8*k;
+ *       b = 4: k at bit 16*(k%2) + 4*(k/2);
+ *       b = 2: k = 8*x + s (x in {0,1}, s in 0..7) at bit 16*(s%2) + 2*(s/2) + 8*x.
+ *   KIVI32 meta, 4*W bytes: for token t and channel group g (stored channels
+ *     32g .. 32g+31; d and d_R are multiples of 32 so no group mixes the latent
+ *     and k^R), the fp16 scale at byte 4*(t*(W/32) + g) and the fp16 zero 2
+ *     bytes after it.  Codes and values follow the KIVI32 rules above with the
+ *     group being these 32 channels of one token.
+ *   SYMROW meta, 128 bytes: for token t the bf16 scale of c[0..d-1] at byte 4*t
+ *     and the bf16 scale of k^R at byte 4*t + 2 (one scale per stored vector,
+ *     App. C.3), each under the SYMROW rules above with the vector as the row.
+ *   Block bytes: KIVI32 4*W*(b+1); SYMROW 4*W*b + 128; bf16 64*W.
+ */
+
 /* Build the layer table of a plan (§2.2): validate every action against
  * eq. (3) (layer 0 must own a cache, §2.2/§2.3), resolve anchor_of, compute the
  * per-layer cost eq. (1), the compression ratio eq. (2), the arena layout and
@@ -191,12 +230,19 @@ kvk_status kvk_workspace_bytes(const kvk_table* table, int32_t layer_begin, int3
 
 /* Prefill write of one layer's cache (§2.1: an anchor writes its cache, an
  * inheriting layer writes nothing; App. C.3 quantisers).
+ * GQA:
  *   k, v      : device [B][Hkv][n_tokens][d_h], dtype in_dtype (bf16 or fp32), contiguous.
- *   n_tokens  : prefill length, 1..max_tokens.
  *   keep_idx  : NULL when the table has no eviction; else device int32
  *               [B][Hkv][keep_tokens], strictly increasing positions in
  *               [0, n_tokens): the stored stream is k/v at these positions, in
  *               order (composition with token eviction, §3 long context).
+ * MLA (rank axis, §2.1, App. C.2):
+ *   k         : the latent, device [B][n_tokens][r], dtype in_dtype; only the
+ *               first d = rank coordinates of each token are read and stored.
+ *   v         : the positional key k^R after RoPE, device [B][n_tokens][d_R].
+ *   keep_idx  : NULL, or device int32 [B][keep_tokens] as above, per sequence.
+ * Both:
+ *   n_tokens  : prefill length, 1..max_tokens.
  *   arena     : device, arena_bytes; only this layer's region is written.
  * An inheriting layer returns KVK_OK without launching anything.
  * keep_idx contents are trusted: the host cannot read device memory without a
@@ -210,12 +256,27 @@ kvk_status kvk_compress_layer(const kvk_table* table, int32_t layer, const void*
 /* One decode step of attention for layers [layer_begin, layer_end) (§2.1): layer l
  * uses its own query and the cache of anchor_of[l].  Layers in the range that
  * share an anchor are served by one read of that anchor's bytes.
+ * GQA:
  *   q        : device [layer_end-layer_begin][B][Hq][d_h], dtype q_dtype.
- *   n_stored : stored tokens per (b, KV head), 0..stored_tokens_cap (the prefill
- *              n_tokens, or keep_tokens under eviction).  n_stored = 0 yields zeros.
- *   scale    : softmax scale applied to q.k.
- *   w_uk, w_uv: MLA up-projections; must be NULL for GQA.
+ *   w_uk, w_uv: must be NULL.
  *   out      : device fp32 [layer_end-layer_begin][B][Hq][d_h].
+ * MLA (§2.1, App. C.2), with nl = layer_end - layer_begin:
+ *   q        : device [nl][B][Hq][nope_dim + d_R], dtype q_dtype: per head the
+ *              no-RoPE part q_nope then the RoPE part q_rope.
+ *   w_uk     : device bf16 [nl][Hq][nope_dim][r]: layer l's W_UK, the map from the
+ *              latent to head h's content key (k = W_UK[h] c).
+ *   w_uv     : device bf16 [nl][Hq][v_dim][r]: layer l's W_UV (v = W_UV[h] c).
+ *   out      : device fp32 [nl][B][Hq][v_dim].
+ *   Head h of layer l attends with query [q_nope ; q_rope] to keys
+ *   [W_UK[h] c_t ; k^R_t] and values W_UV[h] c_t, where c_t is the stored latent
+ *   of token t zero-extended from the anchor's d to r.  The library computes it
+ *   with the projections moved onto the query and the output (App. C.2):
+ *   q~ = W_UK[h][:, :d]^T q_nope, scores over [c_t[:d] ; k^R_t], then
+ *   out = W_UV[h][:, :d] (softmax-weighted sum of c_t[:d]).
+ * Both:
+ *   n_stored : stored tokens per stream, 0..stored_tokens_cap (the prefill
+ *              n_tokens, or keep_tokens under eviction).  n_stored = 0 yields zeros.
+ *   scale    : softmax scale applied to the query-key dot product.
  *   workspace: device, >= kvk_workspace_bytes(...) bytes, 256-byte aligned; its
  *              contents on entry are ignored.
  * Calls that overlap on one workspace race.
@@ -227,12 +288,14 @@ kvk_status kvk_decode_attention(const kvk_table* table, int32_t layer_begin, int
                                 hipStream_t stream);
 
 /* The two phases of kvk_decode_attention, for callers that schedule or time them
- * separately.  kvk_decode_splits runs the attention over the full 32-token blocks,
- * split along the context (arguments as for kvk_decode_attention), and leaves the
- * split partials in `workspace`; kvk_decode_merge attends to the bf16 tail tokens
- * and merges them with the partials by log-sum-exp into `out`.  The merge must use
- * the same table, layer range, q, n_stored, scale, arena and workspace as the
- * splits call before it on the same stream.  Errors as for kvk_decode_attention. */
+ * separately.  kvk_decode_splits runs the attention split along the context and
+ * leaves the split partials in `workspace` (GQA: over the full 32-token blocks;
+ * MLA: the absorbed queries, then every stored token, tail included);
+ * kvk_decode_merge merges the partials by log-sum-exp into `out` (GQA: after
+ * attending to the bf16 tail tokens; MLA: followed by the W_UV up-projection).
+ * The merge must use the same table, layer range, q, n_stored, scale, weights,
+ * arena and workspace as the splits call before it on the same stream.  Errors
+ * as for kvk_decode_attention. */
 kvk_status kvk_decode_splits(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
                              const void* q, int32_t q_dtype, int32_t n_stored, float scale,
                              const void* w_uk, const void* w_uv, const void* arena,
@@ -245,13 +308,14 @@ kvk_status kvk_decode_merge(const kvk_table* table, int32_t layer_begin, int32_t
 
 /* Algorithmic bytes one decode call over [layer_begin, layer_end) reads from the
  * arena with n_stored tokens per stream: each distinct anchor's full blocks and
- * bf16 tail tokens, counted once (split partials, queries and outputs excluded).
- * Host only. */
+ * bf16 tail tokens, counted once (split partials, queries, MLA up-projection
+ * weights and outputs excluded).  Host only. */
 kvk_status kvk_read_bytes(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
                           int32_t n_stored, int64_t* out_bytes);
 
-/* Test support: dequantise the cache read by `layer` (its anchor's) into fp32
- * k_out, v_out [B][Hkv][n_stored][d_h], using the rules above bit for bit. */
+/* Test support: dequantise the cache read by `layer` (its anchor's) into fp32,
+ * using the rules above bit for bit.  GQA: k_out, v_out [B][Hkv][n_stored][d_h].
+ * MLA: k_out = the stored latent [B][n_stored][d], v_out = k^R [B][n_stored][d_R]. */
 kvk_status kvk_debug_dequantize(const kvk_table* table, int32_t layer, int32_t n_stored,
                                 const void* arena, float* k_out, float* v_out, hipStream_t stream);
 

@@ -86,7 +86,7 @@ def _pack(u: np.ndarray, addr: np.ndarray, bits: int, nbytes: int) -> np.ndarray
     nwords = nbytes // 4
     flat = addr.reshape(-1)
     word = flat // 32
-    vals = u.reshape(n, -1).astype(np.uint64) << (flat % 32).astype(np.uint64)
+    vals = u.reshape(n, flat.size).astype(np.uint64) << (flat % 32).astype(np.uint64)
     order = np.argsort(word, kind="stable")
     per = 32 // bits
     assert np.array_equal(word[order], np.repeat(np.arange(nwords), per)), "layout not dense"
@@ -96,7 +96,7 @@ def _pack(u: np.ndarray, addr: np.ndarray, bits: int, nbytes: int) -> np.ndarray
 
 def _unpack(raw: np.ndarray, addr: np.ndarray, bits: int) -> np.ndarray:
     n = raw.shape[0]
-    words = np.ascontiguousarray(raw).view(np.uint32).reshape(n, -1).astype(np.int64)
+    words = np.ascontiguousarray(raw).view(np.uint32).reshape(n, raw.shape[1] // 4).astype(np.int64)
     flat = addr.reshape(-1)
     return ((words[:, flat // 32] >> (flat % 32)) & ((1 << bits) - 1)).reshape(n, *addr.shape)
 
@@ -312,10 +312,13 @@ def attention_absorbed(q_nope, q_rope, Chat, Rhat, W_UK, W_UV, scale):
 
 
 def decode_step(dims: Dims, plan, arena: np.ndarray, q: np.ndarray, w_uk: np.ndarray,
-                w_uv: np.ndarray, n_stored: int, scale: float, l0: int = 0, l1=None) -> np.ndarray:
+                w_uv: np.ndarray, n_stored: int, scale: float, l0: int = 0, l1=None,
+                absorbed: bool = False) -> np.ndarray:
     """q [l1-l0, B, Hq, nope + d_R], w_uk [l1-l0, Hq, nope, r], w_uv [l1-l0, Hq, v, r]
     -> out fp64 [l1-l0, B, Hq, v]: each layer's own query and up-projections against
-    its anchor's stored latent (§2.1)."""
+    its anchor's stored latent (§2.1).  absorbed=True evaluates the same attention
+    in the absorbed form (cheaper for long contexts; pinned equal to the
+    reconstruction)."""
     assert dims.kind == MLA
     l1 = dims.n_layers if l1 is None else l1
     anc = anchor_of(plan)
@@ -329,8 +332,8 @@ def decode_step(dims: Dims, plan, arena: np.ndarray, q: np.ndarray, w_uk: np.nda
         Ch, Rh = cache[a]
         for b in range(dims.batch):
             qb = np.asarray(q[l - l0, b], np.float64)
-            out[l - l0, b] = attention_reconstructed(qb[:, :nope], qb[:, nope:], Ch[b], Rh[b],
-                                                     w_uk[l - l0], w_uv[l - l0], scale)
+            f = attention_absorbed if absorbed else attention_reconstructed
+            out[l - l0, b] = f(qb[:, :nope], qb[:, nope:], Ch[b], Rh[b], w_uk[l - l0], w_uv[l - l0], scale)
     return out
 
 

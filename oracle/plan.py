@@ -208,7 +208,8 @@ def layer_bytes(dims: Dims, bits: int, rank: int = 0) -> int:
 
 
 def arena_offsets(dims: Dims, plan: Sequence[Action]):
-    """Byte offset of each anchor's region (anchors in layer order), -1 for inheritors."""
+    """Byte offset of each anchor's region (anchors in layer order, from 0), -1 for
+    inheritors, and the arena size (the regions' total)."""
     offs, cur = [], 0
     for a in plan:
         if a.inherit:

@@ -303,6 +303,8 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
   if ((reinterpret_cast<uintptr_t>(arena) & 15) || (reinterpret_cast<uintptr_t>(k) & 3) ||
       (reinterpret_cast<uintptr_t>(v) & 3))
     return fail(KVK_ERR_INVALID, "misaligned buffer");
+  if (d.kind == KVK_MLA)
+    return mla_compress_layer(t, layer, k, v, in_dtype, n_tokens, keep_idx, arena, stream);
 
   CompressArgs a;
   a.k = k;
@@ -341,6 +343,7 @@ extern "C" kvk_status kvk_debug_dequantize(const kvk_table* t, int32_t layer, in
   if (n_stored < 0 || n_stored > t->cap)
     return fail(KVK_ERR_INVALID, "n_stored %d outside 0..%d", n_stored, t->cap);
   if (n_stored == 0) return KVK_OK;
+  if (d.kind == KVK_MLA) return mla_debug_dequantize(t, layer, n_stored, arena, k_out, v_out, stream);
   const int a = t->info.anchor_of[layer];
   const uint8_t* region = static_cast<const uint8_t*>(arena) + t->info.layer_offset[a];
   const int nstreams = d.batch * d.n_kv_heads;

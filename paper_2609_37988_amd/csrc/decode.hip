@@ -5,7 +5,7 @@
 // share an anchor are served together: their query rows are stacked so that the
 // anchor's bytes are read once per step.  Decode is bound by reading the cache
 // (§1), so the kernel streams each (sequence, KV head) stream once, split along
-// the context into pieces of about 256 KiB; a second kernel merges the splits by
+// the context into pieces of about 1 MiB; a second kernel merges the splits by
 // log-sum-exp.
 //
 // Work unit: one 64-lane wave per (anchor item, sequence, KV head, split).  The
@@ -126,10 +126,11 @@ struct Raw {
 };
 
 // Stream loads go through a buffer resource whose range ends at the last byte of
-// the split: a prefetch past the split returns zeros without touching memory, so
-// the prefetch ring is reloaded without branches and the compiler can count the
-// outstanding loads exactly (a branch around a reload makes it wait for all of
-// them).
+// the split: a prefetch past the split returns zeros without touching memory (the
+// range check covers the vector and the scalar offset together; checked on
+// gfx950 with an in-bounds probe), so the prefetch ring is reloaded without
+// branches and the compiler can count the outstanding loads exactly (a branch
+// around a reload makes it wait for all of them).
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 
 __device__ __forceinline__ Rsrc stream_rsrc(const uint8_t* base, int nbytes) {
@@ -816,6 +817,30 @@ kvk_status launch_c1(const DecodePlan& P, hipStream_t st) {
   return KVK_OK;
 }
 
+// Argument checks shared by the MLA decode entry points.
+kvk_status mla_check(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
+                     int32_t n_stored, float scale, const void* w_uk, const void* w_uv,
+                     const void* arena, const void* out, const void* workspace, size_t ws_bytes) {
+  const kvk_dims& d = t->d;
+  if (l0 < 0 || l1 > d.n_layers || l0 >= l1)
+    return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, d.n_layers);
+  if (!q || !arena || !out || !workspace || !w_uk || !w_uv)
+    return fail(KVK_ERR_INVALID, "NULL buffer (an MLA table needs q, w_uk, w_uv, arena, out, workspace)");
+  if (q_dtype != KVK_BF16 && q_dtype != KVK_F32) return fail(KVK_ERR_INVALID, "q_dtype %d", q_dtype);
+  if (n_stored < 0 || n_stored > t->cap)
+    return fail(KVK_ERR_INVALID, "n_stored %d outside 0..%d", n_stored, t->cap);
+  if (!(scale == scale)) return fail(KVK_ERR_INVALID, "scale is NaN");
+  if ((reinterpret_cast<uintptr_t>(q) & 15) || (reinterpret_cast<uintptr_t>(arena) & 15) ||
+      (reinterpret_cast<uintptr_t>(out) & 15) || (reinterpret_cast<uintptr_t>(w_uk) & 15) ||
+      (reinterpret_cast<uintptr_t>(w_uv) & 15) || (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return fail(KVK_ERR_INVALID, "misaligned buffer (q/w_uk/w_uv/arena/out 16 B, workspace 256 B)");
+  MlaWorkspace ws;
+  mla_workspace(t, l0, l1, &ws);
+  if ((size_t)ws.total > ws_bytes)
+    return fail(KVK_ERR_BUFFER, "workspace %zu bytes < %lld needed", ws_bytes, (long long)ws.total);
+  return KVK_OK;
+}
+
 }  // namespace
 
 extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
@@ -823,6 +848,14 @@ extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32
                                            const void* w_uk, const void* w_uv, const void* arena,
                                            float* out, void* workspace, size_t ws_bytes,
                                            hipStream_t stream) {
+  if (t && t->d.kind == KVK_MLA) {
+    kvk_status st = mla_check(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
+                              ws_bytes);
+    if (st != KVK_OK) return st;
+    st = mla_decode_splits(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, arena, workspace, stream);
+    if (st != KVK_OK) return st;
+    return mla_decode_merge(t, l0, l1, n_stored, w_uv, workspace, out, stream);
+  }
   DecodePlan P;
   kvk_status st = prepare(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
                           ws_bytes, P);
@@ -836,6 +869,12 @@ extern "C" kvk_status kvk_decode_splits(const kvk_table* t, int32_t l0, int32_t 
                                         int32_t q_dtype, int32_t n_stored, float scale,
                                         const void* w_uk, const void* w_uv, const void* arena,
                                         void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (t && t->d.kind == KVK_MLA) {
+    const kvk_status st = mla_check(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, workspace,
+                                    workspace, ws_bytes);
+    if (st != KVK_OK) return st;
+    return mla_decode_splits(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, arena, workspace, stream);
+  }
   DecodePlan P;
   float* dummy_out = static_cast<float*>(workspace);  // not written by this phase
   kvk_status st = prepare(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, dummy_out,
@@ -849,6 +888,12 @@ extern "C" kvk_status kvk_decode_merge(const kvk_table* t, int32_t l0, int32_t l
                                        const void* w_uk, const void* w_uv, const void* arena,
                                        const void* workspace, size_t ws_bytes, float* out,
                                        hipStream_t stream) {
+  if (t && t->d.kind == KVK_MLA) {
+    const kvk_status st = mla_check(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out,
+                                    workspace, ws_bytes);
+    if (st != KVK_OK) return st;
+    return mla_decode_merge(t, l0, l1, n_stored, w_uv, workspace, out, stream);
+  }
   DecodePlan P;
   kvk_status st = prepare(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out,
                           const_cast<void*>(workspace), ws_bytes, P);
@@ -866,13 +911,17 @@ extern "C" kvk_status kvk_read_bytes(const kvk_table* t, int32_t l0, int32_t l1,
     return fail(KVK_ERR_INVALID, "n_stored %d outside 0..%d", n_stored, t->cap);
   bool seen[KVK_MAX_LAYERS] = {false};
   int64_t total = 0;
-  const int64_t per_stream_tail = (int64_t)(n_stored % KVK_GROUP) * 4 * d.head_dim;
+  const bool mla = d.kind == KVK_MLA;
+  const int64_t streams = mla ? (int64_t)d.batch : (int64_t)d.batch * d.n_kv_heads;
   for (int l = l0; l < l1; ++l) {
     const int a = t->info.anchor_of[l];
     if (seen[a]) continue;
     seen[a] = true;
-    const int64_t per = (int64_t)(n_stored / KVK_GROUP) * t->block_bytes[a] + per_stream_tail;
-    total += per * d.batch * d.n_kv_heads;
+    // bf16 tail tokens: K and V of one head (GQA), or the d + d_R stored channels (MLA)
+    const int64_t tail_tok = mla ? 2LL * (t->rank[a] + d.rope_dim) : 4LL * d.head_dim;
+    const int64_t per = (int64_t)(n_stored / KVK_GROUP) * t->block_bytes[a] +
+                        (int64_t)(n_stored % KVK_GROUP) * tail_tok;
+    total += per * streams;
   }
   *out_bytes = total;
   return KVK_OK;

@@ -12,6 +12,7 @@ struct kvk_table {
   kvk_action plan[KVK_MAX_LAYERS];
   kvk_table_info info;
   int32_t bits[KVK_MAX_LAYERS];         // bits of each layer's own action (anchors)
+  int32_t rank[KVK_MAX_LAYERS];         // MLA: kept latent width d of each anchor
   int64_t block_bytes[KVK_MAX_LAYERS];  // bytes of one 32-token block (anchors)
   int32_t next_anchor[KVK_MAX_LAYERS];  // first anchor after l (n_layers if none)
   int32_t cap;                          // stored tokens capacity per stream
@@ -42,5 +43,62 @@ int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_
 inline int32_t n_splits(int32_t n_blocks, int32_t split_blocks) {
   return (n_blocks + split_blocks - 1) / split_blocks;
 }
+
+// ---------------------------------------------------------------------------
+// MLA (rank axis)
+// ---------------------------------------------------------------------------
+
+// Bytes of one 32-token block of an MLA stream storing W = d + d_R channels.
+int64_t mla_block_bytes(int32_t W, int32_t bits, int32_t qscheme);
+
+// Blocks the MLA decode kernel keeps in flight per workgroup (registers) for a
+// stream of W stored channels per token at `bits`: about 40 KiB of cache, at most
+// 64 registers per thread (40 at the widest rows, whose query and accumulators
+// take the most).  Shared by the host (split sizes) and the kernel.
+constexpr int mla_ring_depth(int W, int bits, int kivi) {
+  const int nch = bits == 16 ? 4 * W : W * bits / 4;  // 16-byte chunks per block
+  const int nc = (nch + 255) / 256;                     // per thread
+  const int regs = nc * (bits == 16 ? 4 : 6);
+  const long bb = bits == 16 ? 64L * W : (kivi ? 4L * W * (bits + 1) : 4L * W * bits + 128);
+  const int cap = W > 320 ? 40 : 64;
+  const int by_regs = regs > cap ? 1 : cap / regs;
+  const int by_bytes = (int)((40960 + bb - 1) / bb);
+  const int nr = by_regs < by_bytes ? by_regs : by_bytes;
+  return nr < 1 ? 1 : nr;
+}
+
+// Full blocks per split of the MLA decode kernel for an anchor whose streams hold
+// n_blocks full blocks: about 4 MiB per split, balanced over the stream, rounded
+// up to a multiple of the ring depth (so only a stream's last split prefetches
+// past its end); the split count is monotone in n_blocks.
+int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_blocks);
+
+// Work units (splits) of one MLA stream holding n_stored tokens: the full blocks
+// in balanced splits, the tail tokens in the last one; at least one unit.
+int32_t mla_units(const kvk_table* t, int32_t anchor, int32_t n_stored);
+
+// Workspace layout of an MLA decode over [l0, l1): the absorbed queries of each
+// layer (fp16 [B][Hq][W]) then the split partials of each layer (fp32, per
+// (b, split): m[Hq], l[Hq], o[Hq][d]), each layer's part 256-byte aligned.
+// Offsets are sized for the table's capacity.
+struct MlaWorkspace {
+  int64_t q_off[KVK_MAX_LAYERS];
+  int64_t part_off[KVK_MAX_LAYERS];
+  int32_t units_cap[KVK_MAX_LAYERS];  // splits per (layer, b) at capacity
+  int64_t total;
+};
+void mla_workspace(const kvk_table* t, int32_t l0, int32_t l1, MlaWorkspace* ws);
+
+kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* latent,
+                              const void* rope, int32_t in_dtype, int32_t n_tokens,
+                              const int32_t* keep_idx, void* arena, hipStream_t stream);
+kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
+                             int32_t q_dtype, int32_t n_stored, float scale, const void* w_uk,
+                             const void* arena, void* workspace, hipStream_t stream);
+kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored,
+                            const void* w_uv, const void* workspace, float* out,
+                            hipStream_t stream);
+kvk_status mla_debug_dequantize(const kvk_table* t, int32_t layer, int32_t n_stored,
+                                const void* arena, float* c_out, float* r_out, hipStream_t stream);
 
 }  // namespace kvk

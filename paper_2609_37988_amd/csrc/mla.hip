@@ -1,0 +1,929 @@
+// The rank axis: MLA latent caches (KV-Kaizen §2.1 "Rank", App. C.2).
+//
+// An MLA layer stores per token the first d coordinates of its latent c (shared
+// by every head) and the positional key k^R (d_R = 64, after RoPE), at b bits
+// (App. C.3 quantisers: KIVI32 groups of 32 stored channels of one token, or the
+// paper's symmetric scale per stored vector) or bf16.  Head h attends with query
+// [q_nope ; q_rope] to keys [W_UK[h] c_t ; k^R_t] and values W_UV[h] c_t.  The
+// content key takes no RoPE, so its projection moves onto the query (App. C.2):
+//
+//   q~_h = W_UK[h][:, :d]^T q_nope_h                    (A1: absorb, MFMA)
+//   s_t  = scale (q~_h . c_t[:d] + q_rope_h . k^R_t)     (D2: MFMA, M = tokens,
+//   o_lat = sum_t softmax(s)_t c_t[:d]                        N = heads, K = d + 64)
+//   o_h  = W_UV[h][:, :d] o_lat                          (C2: merge + up-projection, MFMA)
+//
+// and the latent is read once per decode step for all heads: a dense contraction
+// of the heads against the tokens, which is what the matrix cores are for.
+//
+// D2 work unit: one workgroup of 4 waves per (anchor, reader layer and 32-head
+// chunk, sequence, split).  Per 32-token block the workgroup stages the block in
+// LDS as fp16 (dequantised, or converted from bf16), then
+//   S^T[token, head] = C[token, :] . q~[head, :]   wave w: tokens 16 (w/2).., heads 16 (w%2)..
+//   online softmax over the block                  256 threads: 8 per head
+//   O^T[chan, head] += C^T[chan, token] P^T[token, head]   wave w: channel tiles w, w+4, ...
+// Register ring: the next blocks' raw bytes are loaded while the current block
+// is computed.  The absorbed query and the probabilities enter the MFMAs as
+// fp16; accumulation is fp32.
+#include <hip/hip_runtime.h>
+
+#include "kvk_device.h"
+#include "kvk_internal.h"
+
+using namespace kvkd;
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kRope = 64;
+constexpr int kMaxW = 512 + kRope;  // widest stored row
+constexpr int kMaxItems = 32;       // anchors per decode launch (kernel-argument size)
+
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+
+__device__ __forceinline__ Rsrc buffer_rsrc(const uint8_t* base, int nbytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, nbytes, 0x00020000);
+}
+
+__device__ __forceinline__ f4 mfma16(half8 a, half8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f4 mfmab(bf16x8 a, bf16x8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float load_in(const void* p, int f32, int64_t i) {
+  return f32 ? static_cast<const float*>(p)[i] : bf16_to_f32(static_cast<const uint16_t*>(p)[i]);
+}
+
+// Two bf16 values of a word -> fp16 pair (exact for values in the fp16 range).
+__device__ __forceinline__ half2v bf16x2_to_half2(uint32_t w) {
+  return h2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+}
+
+__device__ __forceinline__ uint16_t bf16_bits_rne(float x) { return f32_to_bf16_bits(x); }
+
+// ---------------------------------------------------------------------------
+// W2: prefill write of one MLA layer
+// ---------------------------------------------------------------------------
+
+struct MlaCompressArgs {
+  const void* latent;  // [B][n_tokens][r]
+  const void* rope;    // [B][n_tokens][64]
+  const int32_t* keep; // [B][n_stored] or null
+  uint8_t* region;
+  int64_t stream_bytes;
+  int64_t block_bytes;
+  int32_t in_f32;
+  int32_t n_tokens;
+  int32_t n_stored;
+  int32_t nbf;
+  int32_t nb_cap;
+  int32_t r;
+  int32_t d;
+  int32_t bits;
+  int32_t kivi;
+};
+
+__device__ __forceinline__ uint32_t kivi_code(float x, float s, float z, float levels) {
+  if (s == 0.0f) return 0u;
+  const float t = (x - z) / s;  // IEEE fp32, correctly rounded
+  return (uint32_t)fminf(fmaxf(rintf(t), 0.0f), levels);
+}
+
+__device__ __forceinline__ uint32_t sym_code(float x, float s, int bits) {
+  const float q = (float)((1 << (bits - 1)) - 1);
+  float r = 0.0f;
+  if (s != 0.0f) r = fminf(fmaxf(rintf(x / s), -q), q);
+  return (uint32_t)((int)r + (1 << (bits - 1)));
+}
+
+// One workgroup per (32-token block, sequence): stage the block's stored channels
+// (latent[:d] then k^R) in LDS as fp32, compute the metadata, then assemble whole
+// 32-bit code words (coalesced stores).
+__global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
+#pragma clang fp contract(off)
+  constexpr int LD = kMaxW + 1;
+  __shared__ float X[32 * LD];
+  __shared__ float gs[32 * (kMaxW / 32)];  // KIVI32 scale / SYMROW group max|x|
+  __shared__ float gz[32 * (kMaxW / 32)];  // KIVI32 zero
+  __shared__ float ssc[64];                // SYMROW: scale of (token, latent|rope)
+  const int tid = threadIdx.x;
+  const int blk = blockIdx.x, b = blockIdx.y;
+  const bool tail = blk == a.nbf;
+  const int tok0 = 32 * blk;
+  const int ntok = tail ? a.n_stored - tok0 : 32;
+  const int d = a.d, W = d + kRope, G = W / 32;
+
+  for (int idx = tid; idx < 32 * W; idx += 256) {
+    const int t = idx / W, c = idx - t * W;
+    float x = 0.0f;
+    if (t < ntok) {
+      int pos = tok0 + t;
+      if (a.keep) {
+        pos = a.keep[(int64_t)b * a.n_stored + pos];
+        pos = pos < 0 ? 0 : (pos >= a.n_tokens ? a.n_tokens - 1 : pos);
+      }
+      const int64_t row = (int64_t)b * a.n_tokens + pos;
+      x = c < d ? load_in(a.latent, a.in_f32, row * a.r + c)
+                : load_in(a.rope, a.in_f32, row * kRope + (c - d));
+    }
+    X[t * LD + c] = x;
+  }
+  __syncthreads();
+
+  uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
+                 (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
+  if (tail || a.bits == 16) {  // bf16 block: token-major rows of W values
+    uint32_t* o = reinterpret_cast<uint32_t*>(out);
+    const int half = W / 2;
+    for (int idx = tid; idx < 32 * half; idx += 256) {
+      const int t = idx / half, c = 2 * (idx - t * half);
+      o[idx] = (uint32_t)bf16_bits_rne(X[t * LD + c]) | ((uint32_t)bf16_bits_rne(X[t * LD + c + 1]) << 16);
+    }
+    return;
+  }
+
+  const int bits = a.bits;
+  const float levels = (float)((1 << bits) - 1);
+  const int cb = 4 * W * bits;  // code bytes of the block
+  for (int p = tid; p < 32 * G; p += 256) {  // (token, group of 32 stored channels)
+    const int t = p / G, g = p - t * G;
+    const float* row = &X[t * LD + 32 * g];
+    float mn = row[0], mx = row[0], am = fabsf(row[0]);
+    for (int c = 1; c < 32; ++c) {
+      mn = fminf(mn, row[c]);
+      mx = fmaxf(mx, row[c]);
+      am = fmaxf(am, fabsf(row[c]));
+    }
+    if (a.kivi) {
+      const _Float16 sh = (_Float16)((mx - mn) / levels);
+      const _Float16 zh = (_Float16)mn;
+      gs[p] = (float)sh;
+      gz[p] = (float)zh;
+      reinterpret_cast<uint32_t*>(out + cb)[p] =
+          (uint32_t)bitcast<uint16_t>(sh) | ((uint32_t)bitcast<uint16_t>(zh) << 16);
+    } else {
+      gs[p] = am;
+    }
+  }
+  __syncthreads();
+  if (!a.kivi) {
+    if (tid < 64) {  // one scale per stored vector: c[:d] (part 0) and k^R (part 1)
+      const int t = tid >> 1, part = tid & 1;
+      const int g0 = part ? d / 32 : 0, g1 = part ? G : d / 32;
+      float am = 0.0f;
+      for (int g = g0; g < g1; ++g) am = fmaxf(am, gs[t * G + g]);
+      const float q = (float)((1 << (bits - 1)) - 1);
+      const uint16_t sb = bf16_bits_rne(am / q);
+      ssc[tid] = bf16_to_f32(sb);
+      reinterpret_cast<uint16_t*>(out + cb)[tid] = sb;  // byte 4t + 2 part
+    }
+    __syncthreads();
+  }
+  const int per = 32 / bits, wpt = W / per;  // codes per word, words per token
+  uint32_t* ow = reinterpret_cast<uint32_t*>(out);
+  for (int wi = tid; wi < 32 * wpt; wi += 256) {
+    const int t = wi / wpt, w = wi - t * wpt;
+    uint32_t word = 0;
+    for (int k = 0; k < per; ++k) {
+      const int c = per * w + k;
+      const float x = X[t * LD + c];
+      uint32_t u;
+      if (a.kivi) {
+        const int p = t * G + (c >> 5);
+        u = kivi_code(x, gs[p], gz[p], levels);
+      } else {
+        u = sym_code(x, ssc[2 * t + (c >= d ? 1 : 0)], bits);
+      }
+      int bit;
+      if (bits == 8) bit = 8 * k;
+      else if (bits == 4) bit = 16 * (k & 1) + 4 * (k >> 1);
+      else bit = 16 * (k & 1) + 2 * ((k & 7) >> 1) + 8 * (k >> 3);
+      word |= u << bit;
+    }
+    ow[wi] = word;
+  }
+}
+
+// Test-only dequantiser: one thread per (sequence, token, stored channel).
+__global__ __launch_bounds__(256) void mla_dequant_kernel(const uint8_t* region, int64_t stream_bytes,
+                                                          int64_t block_bytes, int nb_cap, int n_stored,
+                                                          int B, int d, int bits, int kivi, float* cout,
+                                                          float* rout) {
+  const int W = d + kRope;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)B * n_stored * W) return;
+  const int c = (int)(idx % W);
+  const int64_t bt = idx / W;
+  const int tok = (int)(bt % n_stored);
+  const int b = (int)(bt / n_stored);
+  const int blk = tok >> 5, t = tok & 31;
+  const int nbf = n_stored >> 5;
+  const uint8_t* base = region + (int64_t)b * stream_bytes;
+  float x;
+  if (blk >= nbf || bits == 16) {
+    const uint8_t* bb = base + (blk >= nbf ? (int64_t)nb_cap * block_bytes : (int64_t)blk * block_bytes);
+    x = bf16_to_f32(*reinterpret_cast<const uint16_t*>(bb + 2 * (W * t + c)));
+  } else {
+    const uint8_t* bb = base + (int64_t)blk * block_bytes;
+    const int per = 32 / bits, k = c % per;
+    const uint32_t word = reinterpret_cast<const uint32_t*>(bb)[t * (W / per) + c / per];
+    int bit;
+    if (bits == 8) bit = 8 * k;
+    else if (bits == 4) bit = 16 * (k & 1) + 4 * (k >> 1);
+    else bit = 16 * (k & 1) + 2 * ((k & 7) >> 1) + 8 * (k >> 3);
+    const uint32_t u = (word >> bit) & ((1u << bits) - 1u);
+    const uint16_t* meta = reinterpret_cast<const uint16_t*>(bb + 4 * W * bits);
+    if (kivi) {
+      const int p = t * (W / 32) + (c >> 5);
+      x = fmaf((float)u, f16_bits_to_f32(meta[2 * p]), f16_bits_to_f32(meta[2 * p + 1]));
+    } else {
+      x = (float)((int)u - (1 << (bits - 1))) * bf16_to_f32(meta[2 * t + (c >= d ? 1 : 0)]);
+    }
+  }
+  if (c < d) cout[bt * d + c] = x;
+  else rout[bt * kRope + (c - d)] = x;
+}
+
+// ---------------------------------------------------------------------------
+// A1: absorbed queries, q~ = W_UK[h][:, :d]^T q_nope (scaled into the exp2 domain)
+// ---------------------------------------------------------------------------
+
+struct MlaAbsorbArgs {
+  const void* q;          // [nl][B][Hq][nope + 64]
+  const uint16_t* w_uk;   // [nl][Hq][nope][r] bf16
+  uint8_t* ws;
+  int64_t q_off[KVK_MAX_LAYERS];  // per relative layer: fp16 [B][Hq][d + 64]
+  int32_t d_of[KVK_MAX_LAYERS];
+  int32_t q_f32;
+  int32_t B, Hq, nope, r;
+  float scale_log2;
+};
+
+// One workgroup per (layer, head, 64-channel chunk of the latent).  The chunk of
+// W_UK[h] (nope rows x 64 channels) is staged in LDS and read transposed into the
+// MFMA A operand (M = channels, K = nope); the queries of 16 sequences are the B
+// operand, split into bf16 hi + lo.
+__global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
+  constexpr int PW = 72;  // LDS row pitch (bf16 elements)
+  __shared__ uint16_t wt[256 * PW];
+  const int li = blockIdx.x, h = blockIdx.y, c0 = 64 * blockIdx.z;
+  const int d = a.d_of[li], W = d + kRope;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
+  const int qw = a.nope + kRope;
+  _Float16* qa = reinterpret_cast<_Float16*>(a.ws + a.q_off[li]);
+  if (c0 >= d) return;
+  if (blockIdx.z == 0) {
+    for (int e = tid; e < a.B * kRope; e += 256) {
+      const int b = e / kRope, j = e - b * kRope;
+      const float x = load_in(a.q, a.q_f32, (((int64_t)li * a.B + b) * a.Hq + h) * qw + a.nope + j);
+      qa[((int64_t)b * a.Hq + h) * W + d + j] = (_Float16)(x * a.scale_log2);
+    }
+  }
+  const uint16_t* wk = a.w_uk + ((int64_t)li * a.Hq + h) * a.nope * a.r;
+  for (int e = tid; e < a.nope * 8; e += 256) {  // 16-byte pieces: row i, 8 channels
+    const int i = e >> 3, pc = 8 * (e & 7);
+    u4v v = {0u, 0u, 0u, 0u};
+    if (c0 + pc < d) v = *reinterpret_cast<const u4v*>(wk + (int64_t)i * a.r + c0 + pc);
+    *reinterpret_cast<u4v*>(&wt[i * PW + pc]) = v;
+  }
+  __syncthreads();
+  const int nks = a.nope / 32;
+  const int ct = 16 * wv;  // this wave's 16 channels of the chunk
+  if (c0 + ct >= d) return;
+  for (int b0 = 0; b0 < a.B; b0 += 16) {
+    const int bq = b0 + i16;
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int ks = 0; ks < nks; ++ks) {
+      uint16_t ah[8], qh[8], ql[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int i = 32 * ks + 8 * g + j;
+        ah[j] = wt[i * PW + ct + i16];
+        float x = 0.0f;
+        if (bq < a.B) x = load_in(a.q, a.q_f32, (((int64_t)li * a.B + bq) * a.Hq + h) * qw + i);
+        qh[j] = bf16_bits_rne(x);
+        ql[j] = bf16_bits_rne(x - bf16_to_f32(qh[j]));
+      }
+      bf16x8 av, bh, bl;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        av[j] = bitcast<__bf16>(ah[j]);
+        bh[j] = bitcast<__bf16>(qh[j]);
+        bl[j] = bitcast<__bf16>(ql[j]);
+      }
+      acc = mfmab(av, bh, acc);
+      acc = mfmab(av, bl, acc);
+    }
+    if (bq < a.B) {  // D[chan 4g + e][seq i16]
+      _Float16* dst = qa + ((int64_t)bq * a.Hq + h) * W + c0 + ct + 4 * g;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) dst[e] = (_Float16)(acc[e] * a.scale_log2);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// D2: decode over the stored latent
+// ---------------------------------------------------------------------------
+
+struct MlaItem {
+  int64_t region;       // anchor's region in the arena
+  int64_t q_off0;       // absorbed queries of the first reader layer
+  int64_t q_stride;     // ... and between consecutive readers
+  int64_t part_off0;    // split partials of the first reader layer
+  int64_t part_stride;
+  int32_t stream_bytes;
+  int32_t block_bytes;
+  int32_t d;
+  int32_t bits;
+  int32_t nreaders;     // reader layers (consecutive)
+  int32_t nhc;          // 32-head chunks per layer
+  int32_t units;        // splits per stream
+  int32_t units_cap;    // partial records per stream
+  int32_t split_blocks;
+  int32_t wg_begin;
+};
+
+struct MlaDecodeArgs {
+  const uint8_t* arena;
+  uint8_t* ws;
+  MlaItem items[kMaxItems];
+  int32_t n_items;
+  int32_t n_wg;
+  int32_t B, Hq;
+  int32_t nbf;          // full blocks per stream
+  int32_t ntail;        // tail tokens
+  int32_t nb_cap;
+};
+
+constexpr int kSP = 36;  // score buffer row pitch (floats)
+constexpr int kPP = 40;  // probability buffer row pitch (halfs)
+
+struct MlaLds {
+  _Float16 tile[32 * (kMaxW + 16)];
+  float s[32 * kSP];
+  _Float16 p[32 * kPP];
+  float alpha[32];
+};
+
+// Raw bytes of one block held by one thread: 16-byte chunks (+ two metadata words
+// per chunk for quantised blocks).
+template <int D, int BITS>
+struct MlaRaw {
+  static constexpr int W = D + kRope;
+  static constexpr int NCH = BITS == 16 ? 4 * W : W * BITS / 4;  // chunks per block
+  static constexpr int NC = (NCH + 255) / 256;                  // per thread
+  u4v w[NC];
+  uint32_t m[BITS == 16 ? 1 : NC][2];
+};
+
+// Byte offsets (inside a block) of a thread's chunk j and of the metadata words
+// of its two word pairs; recomputed per block rather than held in registers.
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ int chunk_off(int tid, int j) {
+  constexpr int NCH = MlaRaw<D, BITS>::NCH;
+  return 16 * min(tid + 256 * j, NCH - 1);
+}
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ int meta_off(int tid, int j, int p) {
+  constexpr int W = D + kRope, NCH = MlaRaw<D, BITS>::NCH;
+  constexpr int per = 32 / BITS, wpt = W / per, cb = 4 * W * BITS;
+  const int c = min(tid + 256 * j, NCH - 1);
+  const int fw = 4 * c + 2 * p, t = fw / wpt, wi = fw - t * wpt;
+  return KIVI ? cb + 4 * (t * (W / 32) + (per * wi) / 32) : cb + 4 * t;
+}
+
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void mla_issue(MlaRaw<D, BITS>& r, Rsrc rs, int blk, int tid) {
+#pragma unroll
+  for (int j = 0; j < MlaRaw<D, BITS>::NC; ++j) {
+    r.w[j] = __builtin_amdgcn_raw_buffer_load_b128(rs, chunk_off<D, BITS, KIVI>(tid, j), blk, 0);
+    if constexpr (BITS != 16) {
+      r.m[j][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, meta_off<D, BITS, KIVI>(tid, j, 0), blk, 0);
+      r.m[j][1] = __builtin_amdgcn_raw_buffer_load_b32(rs, meta_off<D, BITS, KIVI>(tid, j, 1), blk, 0);
+    }
+  }
+}
+
+// bf16 chunk -> 8 fp16 values of one token row.
+__device__ __forceinline__ void put_bf16_chunk(_Float16* tile, int ph, int W, int c, u4v v, bool zero) {
+  const int t = c / (W / 8), c0 = 8 * (c - t * (W / 8));
+  u4v o = {0u, 0u, 0u, 0u};
+  if (!zero) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = bitcast<uint32_t>(bf16x2_to_half2(v[e]));
+  }
+  *reinterpret_cast<u4v*>(tile + t * ph + c0) = o;
+}
+
+// Write the block held in `r` into the LDS tile as fp16 rows.
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void mla_store(const MlaRaw<D, BITS>& r, _Float16* tile, int tid) {
+  constexpr int W = D + kRope, PH = W + 16;
+  constexpr int NCH = MlaRaw<D, BITS>::NCH, NC = MlaRaw<D, BITS>::NC;
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    const int c = tid + 256 * j;
+    if (NCH % 256 != 0 && c >= NCH) break;
+    if constexpr (BITS == 16) {
+      put_bf16_chunk(tile, PH, W, c, r.w[j], false);
+    } else {
+      constexpr int per = 32 / BITS, wpt = W / per;
+      constexpr float off = KIVI ? 0.0f : (float)(1 << (BITS - 1));
+#pragma unroll
+      for (int k = 0; k < 4; k += (BITS == 8 ? 2 : 1)) {
+        const int fw = 4 * c + k, t = fw / wpt, wi = fw - t * wpt, c0 = per * wi;
+        const uint32_t mm = r.m[j][k >> 1];
+        half2v s2, z2;
+        if constexpr (KIVI) {
+          s2 = h2s((float)bitcast<_Float16>((uint16_t)(mm & 0xFFFFu)));
+          z2 = h2s((float)bitcast<_Float16>((uint16_t)(mm >> 16)));
+        } else {
+          const uint32_t sb = c0 < D ? (mm & 0xFFFFu) : (mm >> 16);
+          s2 = h2s(__uint_as_float(sb << 16));
+          z2 = h2s(0.0f);
+        }
+        _Float16* dst = tile + t * PH + c0;
+        if constexpr (BITS == 4) {
+          const half8 u = unpack4(r.w[j][k], off);
+          half8 x;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            half2v pr = {u[2 * e], u[2 * e + 1]};
+            pr = __builtin_elementwise_fma(pr, s2, z2);
+            x[2 * e] = pr[0];
+            x[2 * e + 1] = pr[1];
+          }
+          *reinterpret_cast<half8*>(dst) = x;
+        } else if constexpr (BITS == 8) {
+          const half8 u = unpack8(r.w[j][k], r.w[j][k + 1], off);
+          half8 x;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            half2v pr = {u[2 * e], u[2 * e + 1]};
+            pr = __builtin_elementwise_fma(pr, s2, z2);
+            x[2 * e] = pr[0];
+            x[2 * e + 1] = pr[1];
+          }
+          *reinterpret_cast<half8*>(dst) = x;
+        } else {
+          half8 ue, uo;
+          unpack2(r.w[j][k], off, ue, uo);
+          half8 xe, xo;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            half2v pe = {ue[2 * e], ue[2 * e + 1]};
+            half2v po = {uo[2 * e], uo[2 * e + 1]};
+            pe = __builtin_elementwise_fma(pe, s2, z2);
+            po = __builtin_elementwise_fma(po, s2, z2);
+            xe[2 * e] = pe[0];
+            xe[2 * e + 1] = pe[1];
+            xo[2 * e] = po[0];
+            xo[2 * e + 1] = po[1];
+          }
+          *reinterpret_cast<half8*>(dst) = xe;
+          *reinterpret_cast<half8*>(dst + 8) = xo;
+        }
+      }
+    }
+  }
+}
+
+// Per-workgroup running state of a unit.
+template <int D>
+struct MlaState {
+  static constexpr int NCT = D / 16;            // latent channel tiles
+  static constexpr int NCTW = (NCT + 3) / 4;    // per wave
+  f4 o[NCTW][2];                                // O^T tiles (channel tile, head tile)
+  float m, l;                                   // softmax threads: running max (log2), sum
+};
+
+// One block already in the LDS tile: scores, online softmax, probabilities x latent.
+template <int D>
+__device__ __forceinline__ void mla_block(MlaState<D>& st, const half8* qreg, MlaLds& L, int nvalid,
+                                          int tid) {
+  constexpr int W = D + kRope, PH = W + 16, NK = W / 32;
+  const int lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
+  {
+    const int tt = wv >> 1, ht = wv & 1;
+    const _Float16* trow = L.tile + (16 * tt + i16) * PH + 8 * g;
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks) acc = mfma16(*reinterpret_cast<const half8*>(trow + 32 * ks), qreg[ks], acc);
+    *reinterpret_cast<f4*>(&L.s[(16 * ht + i16) * kSP + 16 * tt + 4 * g]) = acc;
+  }
+  __syncthreads();
+  {
+    const int h = tid >> 3, part = tid & 7;
+    const f4 sv = *reinterpret_cast<const f4*>(&L.s[h * kSP + 4 * part]);
+    float x[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = 4 * part + e < nvalid ? sv[e] : -INFINITY;
+    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    mx = fmaxf(mx, __shfl_xor(mx, 1));
+    mx = fmaxf(mx, __shfl_xor(mx, 2));
+    mx = fmaxf(mx, __shfl_xor(mx, 4));
+    const float mnew = fmaxf(st.m, mx);  // finite: the block holds a stored token
+    const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
+    float ps = 0.0f;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const _Float16 p = (_Float16)__builtin_amdgcn_exp2f(x[e] - mnew);
+      ps += (float)p;
+      L.p[h * kPP + 8 * e + part] = p;  // token 4 part + e at k-slot 8 (t % 4) + t / 4
+    }
+    ps += __shfl_xor(ps, 1);
+    ps += __shfl_xor(ps, 2);
+    ps += __shfl_xor(ps, 4);
+    st.l = st.l * alpha + ps;
+    st.m = mnew;
+    if (part == 0) L.alpha[h] = alpha;
+  }
+  __syncthreads();
+  {
+    half8 pb[2];
+    float al[2];
+#pragma unroll
+    for (int ht = 0; ht < 2; ++ht) {
+      pb[ht] = *reinterpret_cast<const half8*>(&L.p[(16 * ht + i16) * kPP + 8 * g]);
+      al[ht] = L.alpha[16 * ht + i16];
+    }
+#pragma unroll
+    for (int i = 0; i < MlaState<D>::NCTW; ++i) {
+      const int ct = wv + 4 * i;
+      if (ct < MlaState<D>::NCT) {
+        half8 av;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) av[j] = L.tile[(4 * j + g) * PH + 16 * ct + i16];
+#pragma unroll
+        for (int ht = 0; ht < 2; ++ht) st.o[i][ht] = mfma16(av, pb[ht], st.o[i][ht] * al[ht]);
+      }
+    }
+  }
+}
+
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& it, int rl, int hc,
+                                        int b, int u, MlaLds& L) {
+  constexpr int W = D + kRope, PH = W + 16, NK = W / 32;
+  constexpr int NR = kvk::mla_ring_depth(W, BITS, KIVI ? 1 : 0);
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
+  const int k0 = u * it.split_blocks;
+  const int k1 = min(a.nbf, k0 + it.split_blocks);
+  const int bb = it.block_bytes;
+  const uint8_t* stream = a.arena + it.region + (int64_t)b * it.stream_bytes;
+  const Rsrc rs = buffer_rsrc(stream, k1 > 0 ? k1 * bb : 0);  // loads past block k1-1 read zeros
+
+  MlaRaw<D, BITS> ring[NR];
+#pragma unroll
+  for (int i = 0; i < NR; ++i) mla_issue<D, BITS, KIVI>(ring[i], rs, (k0 + i) * bb, tid);
+
+  // this wave's 16 heads (S phase): absorbed query rows, fp16
+  half8 qreg[NK];
+  {
+    const int head = 32 * hc + 16 * (wv & 1) + i16;
+    const _Float16* qrow = reinterpret_cast<const _Float16*>(a.ws + it.q_off0 + (int64_t)rl * it.q_stride) +
+                           ((int64_t)b * a.Hq + head) * W + 8 * g;
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks) qreg[ks] = *reinterpret_cast<const half8*>(qrow + 32 * ks);
+  }
+  MlaState<D> st;
+  st.m = -INFINITY;
+  st.l = 0.0f;
+#pragma unroll
+  for (int i = 0; i < MlaState<D>::NCTW; ++i) st.o[i][0] = st.o[i][1] = f4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k = k0; k < k1; k += NR) {
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+      const bool valid = k + i < k1;  // uniform
+      __syncthreads();                // the tile is free
+      if (valid) mla_store<D, BITS, KIVI>(ring[i], L.tile, tid);
+      mla_issue<D, BITS, KIVI>(ring[i], rs, (k + i + NR) * bb, tid);
+      __syncthreads();                // the tile is written
+      if (valid) mla_block<D>(st, qreg, L, 32, tid);
+    }
+  }
+  if (u == it.units - 1 && a.ntail > 0) {  // bf16 tail block of the stream
+    const uint8_t* tb = stream + (int64_t)a.nb_cap * bb;
+    constexpr int NCH = 4 * W, NC = (NCH + 255) / 256;
+    u4v v[NC];
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      const int c = min(tid + 256 * j, NCH - 1);
+      v[j] = *reinterpret_cast<const u4v*>(tb + 16 * c);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < NC; ++j) {
+      const int c = tid + 256 * j;
+      if (c < NCH) put_bf16_chunk(L.tile, PH, W, c, v[j], c / (W / 8) >= a.ntail);
+    }
+    __syncthreads();
+    mla_block<D>(st, qreg, L, a.ntail, tid);
+  }
+
+  // split partial: m[Hq], l[Hq], o[Hq][D] of this (reader, sequence, split)
+  float* rec = reinterpret_cast<float*>(a.ws + it.part_off0 + (int64_t)rl * it.part_stride) +
+               ((int64_t)b * it.units_cap + u) * a.Hq * (D + 2);
+  if ((tid & 7) == 0) {
+    const int h = 32 * hc + (tid >> 3);
+    rec[h] = st.m;
+    rec[a.Hq + h] = st.l;
+  }
+  float* orec = rec + 2 * a.Hq;
+#pragma unroll
+  for (int i = 0; i < MlaState<D>::NCTW; ++i) {
+    const int ct = wv + 4 * i;
+    if (ct < MlaState<D>::NCT) {
+#pragma unroll
+      for (int ht = 0; ht < 2; ++ht) {
+        const int h = 32 * hc + 16 * ht + i16;
+        *reinterpret_cast<f4*>(orec + (int64_t)h * D + 16 * ct + 4 * g) = st.o[i][ht];
+      }
+    }
+  }
+}
+
+template <bool KIVI>
+__global__ __launch_bounds__(256, 2) void mla_decode_kernel(MlaDecodeArgs a) {
+  __shared__ MlaLds L;
+  const int wg = blockIdx.x;
+  if (wg >= a.n_wg) return;
+  int lo = 0, hi = a.n_items - 1;  // last item with wg_begin <= wg
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.items[mid].wg_begin <= wg) lo = mid;
+    else hi = mid - 1;
+  }
+  const MlaItem& it = a.items[lo];
+  // Workgroups of one (sequence, split) for the different readers and head chunks
+  // sit 8 apart, so that they run on one XCD at about the same time and share the
+  // stream through its L2.
+  const int R = it.nreaders * it.nhc;
+  const int local = wg - it.wg_begin;
+  const int grp = local / (8 * R), rem = local - grp * 8 * R;
+  const int row = rem >> 3;
+  const int unit = 8 * grp + (rem & 7);
+  if (unit >= a.B * it.units) return;
+  const int b = unit / it.units, u = unit - b * it.units;
+  const int rl = row / it.nhc, hc = row - rl * it.nhc;
+#define KVK_MLA_CASE(DD, BB)                                        \
+  if (it.d == DD && it.bits == BB) {                                \
+    run_mla<DD, BB, KIVI>(a, it, rl, hc, b, u, L);                  \
+    return;                                                         \
+  }
+#define KVK_MLA_D(DD) KVK_MLA_CASE(DD, 16) KVK_MLA_CASE(DD, 8) KVK_MLA_CASE(DD, 4) KVK_MLA_CASE(DD, 2)
+  KVK_MLA_D(512)
+  KVK_MLA_D(256)
+  KVK_MLA_D(128)
+  KVK_MLA_D(64)
+  KVK_MLA_D(32)
+#undef KVK_MLA_D
+#undef KVK_MLA_CASE
+}
+
+// ---------------------------------------------------------------------------
+// C2: merge the splits, then o_h = W_UV[h][:, :d] o_lat
+// ---------------------------------------------------------------------------
+
+struct MlaCombineArgs {
+  const uint8_t* ws;
+  const uint16_t* w_uv;  // [nl][Hq][v][r] bf16
+  float* out;            // [nl][B][Hq][v]
+  int64_t part_off[KVK_MAX_LAYERS];
+  int32_t d_of[KVK_MAX_LAYERS];
+  int32_t units[KVK_MAX_LAYERS];
+  int32_t units_cap[KVK_MAX_LAYERS];
+  int32_t B, Hq, v, r;
+};
+
+// One workgroup per (layer, head): for 16 sequences at a time, merge the split
+// partials by log-sum-exp into o_lat (LDS, bf16 hi + lo), then multiply by
+// W_UV[h] on the matrix cores (M = value channels, K = d, N = sequences).
+__global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
+  constexpr int PO = 512 + 8;  // LDS row pitch (bf16)
+  __shared__ uint16_t oh[16 * PO], ol[16 * PO];
+  __shared__ float mstar[16], linv[16];
+  const int li = blockIdx.x, h = blockIdx.y;
+  const int d = a.d_of[li], U = a.units[li], UC = a.units_cap[li];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
+  const float* part = reinterpret_cast<const float*>(a.ws + a.part_off[li]);
+  const int64_t rec = (int64_t)a.Hq * (d + 2);
+  const uint16_t* wv_h = a.w_uv + ((int64_t)li * a.Hq + h) * a.v * a.r;
+  for (int b0 = 0; b0 < a.B; b0 += 16) {
+    const int nb = min(16, a.B - b0);
+    __syncthreads();
+    if (tid < nb) {
+      const float* p0 = part + (int64_t)(b0 + tid) * UC * rec;
+      float m = -INFINITY;
+      for (int u = 0; u < U; ++u) m = fmaxf(m, p0[u * rec + h]);
+      float l = 0.0f;
+      if (m > -INFINITY)
+        for (int u = 0; u < U; ++u) l += __builtin_amdgcn_exp2f(p0[u * rec + h] - m) * p0[u * rec + a.Hq + h];
+      mstar[tid] = m;
+      linv[tid] = l > 0.0f ? 1.0f / l : 0.0f;
+    }
+    __syncthreads();
+    for (int e = tid; e < 16 * d; e += 256) {
+      const int bi = e / d, c = e - bi * d;
+      float x = 0.0f;
+      if (bi < nb && linv[bi] > 0.0f) {
+        const float* p0 = part + (int64_t)(b0 + bi) * UC * rec;
+        for (int u = 0; u < U; ++u) {
+          const float w = __builtin_amdgcn_exp2f(p0[u * rec + h] - mstar[bi]);
+          x += w * p0[u * rec + 2 * a.Hq + (int64_t)h * d + c];
+        }
+        x *= linv[bi];
+      }
+      const uint16_t hb = bf16_bits_rne(x);
+      oh[bi * PO + c] = hb;
+      ol[bi * PO + c] = bf16_bits_rne(x - bf16_to_f32(hb));
+    }
+    __syncthreads();
+    for (int jt = wv; jt < a.v / 16; jt += 4) {
+      f4 acc = {0.f, 0.f, 0.f, 0.f};
+      const uint16_t* wrow = wv_h + (int64_t)(16 * jt + i16) * a.r + 8 * g;
+      for (int ks = 0; ks < d / 32; ++ks) {
+        const bf16x8 av = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(wrow + 32 * ks));
+        const bf16x8 bh = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&oh[i16 * PO + 32 * ks + 8 * g]));
+        const bf16x8 bl = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&ol[i16 * PO + 32 * ks + 8 * g]));
+        acc = mfmab(av, bh, acc);
+        acc = mfmab(av, bl, acc);
+      }
+      if (i16 < nb)  // D[value channel 16 jt + 4g + e][sequence b0 + i16]
+        *reinterpret_cast<f4*>(a.out + (((int64_t)li * a.B + b0 + i16) * a.Hq + h) * a.v + 16 * jt + 4 * g) = acc;
+    }
+  }
+}
+
+}  // namespace
+
+namespace kvk {
+
+kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* latent, const void* rope,
+                              int32_t in_dtype, int32_t n_tokens, const int32_t* keep_idx, void* arena,
+                              hipStream_t stream) {
+  const kvk_dims& d = t->d;
+  MlaCompressArgs a;
+  a.latent = latent;
+  a.rope = rope;
+  a.keep = keep_idx;
+  a.region = static_cast<uint8_t*>(arena) + t->info.layer_offset[layer];
+  a.stream_bytes = t->info.stream_bytes[layer];
+  a.block_bytes = t->block_bytes[layer];
+  a.in_f32 = in_dtype == KVK_F32;
+  a.n_tokens = n_tokens;
+  a.n_stored = d.keep_tokens > 0 ? d.keep_tokens : n_tokens;
+  a.nbf = a.n_stored / KVK_GROUP;
+  a.nb_cap = t->nb_cap;
+  a.r = d.latent_dim;
+  a.d = t->rank[layer];
+  a.bits = t->bits[layer];
+  a.kivi = d.qscheme == KVK_Q_KIVI32;
+  hipLaunchKernelGGL(mla_compress_kernel, dim3((unsigned)(a.nbf + 1), (unsigned)d.batch), dim3(256), 0,
+                     stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA compress launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+kvk_status mla_debug_dequantize(const kvk_table* t, int32_t layer, int32_t n_stored, const void* arena,
+                                float* c_out, float* r_out, hipStream_t stream) {
+  const kvk_dims& d = t->d;
+  const int a = t->info.anchor_of[layer];
+  const int W = t->rank[a] + d.rope_dim;
+  const int64_t total = (int64_t)d.batch * n_stored * W;
+  const int64_t grid = (total + 255) / 256;
+  if (grid > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "grid too large");
+  hipLaunchKernelGGL(mla_dequant_kernel, dim3((unsigned)grid), dim3(256), 0, stream,
+                     static_cast<const uint8_t*>(arena) + t->info.layer_offset[a], t->info.stream_bytes[a],
+                     t->block_bytes[a], t->nb_cap, n_stored, d.batch, t->rank[a], t->bits[a],
+                     d.qscheme == KVK_Q_KIVI32 ? 1 : 0, c_out, r_out);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA dequantise launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
+                             int32_t n_stored, float scale, const void* w_uk, const void* arena,
+                             void* workspace, hipStream_t stream) {
+  const kvk_dims& d = t->d;
+  MlaWorkspace ws;
+  mla_workspace(t, l0, l1, &ws);
+  uint8_t* wsb = static_cast<uint8_t*>(workspace);
+
+  // A1: absorbed queries of every layer of the range
+  MlaAbsorbArgs aa;
+  aa.q = q;
+  aa.w_uk = static_cast<const uint16_t*>(w_uk);
+  aa.ws = wsb;
+  aa.q_f32 = q_dtype == KVK_F32;
+  aa.B = d.batch;
+  aa.Hq = d.n_q_heads;
+  aa.nope = d.nope_dim;
+  aa.r = d.latent_dim;
+  aa.scale_log2 = scale * kLog2e;
+  int dmax = 0;
+  for (int l = l0; l < l1; ++l) {
+    const int dl = t->rank[t->info.anchor_of[l]];
+    aa.q_off[l - l0] = ws.q_off[l];
+    aa.d_of[l - l0] = dl;
+    dmax = dl > dmax ? dl : dmax;
+  }
+  hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)(l1 - l0), (unsigned)d.n_q_heads, (unsigned)(dmax / 64 + (dmax % 64 ? 1 : 0))),
+                     dim3(256), 0, stream, aa);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA absorb launch: %s", hipGetErrorString(e));
+
+  // D2: one item per distinct anchor read by the range (depth sharing, §2.1)
+  const int nbf = n_stored / KVK_GROUP, ntail = n_stored % KVK_GROUP;
+  if (n_stored == 0) {
+    // no tokens: every partial is (m = -inf, l = 0, o = 0); the merge then yields zeros
+    // and needs no partials, so nothing is launched here.
+    return KVK_OK;
+  }
+  MlaDecodeArgs a;
+  a.arena = static_cast<const uint8_t*>(arena);
+  a.ws = wsb;
+  a.B = d.batch;
+  a.Hq = d.n_q_heads;
+  a.nbf = nbf;
+  a.ntail = ntail;
+  a.nb_cap = t->nb_cap;
+  a.n_items = 0;
+  int64_t wgs = 0;
+  auto flush = [&]() -> kvk_status {
+    if (a.n_items == 0) return KVK_OK;
+    if (wgs > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "too many MLA decode workgroups");
+    a.n_wg = (int32_t)wgs;
+    if (d.qscheme == KVK_Q_KIVI32)
+      hipLaunchKernelGGL(mla_decode_kernel<true>, dim3((unsigned)wgs), dim3(256), 0, stream, a);
+    else
+      hipLaunchKernelGGL(mla_decode_kernel<false>, dim3((unsigned)wgs), dim3(256), 0, stream, a);
+    const hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA decode launch: %s", hipGetErrorString(err));
+    a.n_items = 0;
+    wgs = 0;
+    return KVK_OK;
+  };
+  const int nhc = d.n_q_heads / 32;
+  for (int l = l0; l < l1;) {
+    const int anc = t->info.anchor_of[l];
+    const int re = t->next_anchor[anc] < l1 ? t->next_anchor[anc] : l1;  // readers [l, re)
+    if (a.n_items == kMaxItems) {
+      const kvk_status st = flush();
+      if (st != KVK_OK) return st;
+    }
+    MlaItem& it = a.items[a.n_items++];
+    it.region = t->info.layer_offset[anc];
+    it.q_off0 = ws.q_off[l];
+    it.q_stride = re - l > 1 ? ws.q_off[l + 1] - ws.q_off[l] : 0;
+    it.part_off0 = ws.part_off[l];
+    it.part_stride = re - l > 1 ? ws.part_off[l + 1] - ws.part_off[l] : 0;
+    it.stream_bytes = (int32_t)t->info.stream_bytes[anc];
+    it.block_bytes = (int32_t)t->block_bytes[anc];
+    it.d = t->rank[anc];
+    it.bits = t->bits[anc];
+    it.nreaders = re - l;
+    it.nhc = nhc;
+    it.split_blocks = mla_split_blocks_for(t, anc, nbf);
+    it.units = mla_units(t, anc, n_stored);
+    it.units_cap = ws.units_cap[l];
+    it.wg_begin = (int32_t)wgs;
+    const int64_t units = (int64_t)d.batch * it.units;
+    wgs += (units + 7) / 8 * 8 * it.nreaders * nhc;
+    l = re;
+  }
+  return flush();
+}
+
+kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored, const void* w_uv,
+                            const void* workspace, float* out, hipStream_t stream) {
+  const kvk_dims& d = t->d;
+  MlaWorkspace ws;
+  mla_workspace(t, l0, l1, &ws);
+  MlaCombineArgs c;
+  c.ws = static_cast<const uint8_t*>(workspace);
+  c.w_uv = static_cast<const uint16_t*>(w_uv);
+  c.out = out;
+  c.B = d.batch;
+  c.Hq = d.n_q_heads;
+  c.v = d.v_dim;
+  c.r = d.latent_dim;
+  for (int l = l0; l < l1; ++l) {
+    const int anc = t->info.anchor_of[l];
+    c.part_off[l - l0] = ws.part_off[l];
+    c.d_of[l - l0] = t->rank[anc];
+    c.units[l - l0] = n_stored > 0 ? mla_units(t, anc, n_stored) : 0;  // none: o = 0
+    c.units_cap[l - l0] = ws.units_cap[l];
+  }
+  hipLaunchKernelGGL(mla_combine_kernel, dim3((unsigned)(l1 - l0), (unsigned)d.n_q_heads), dim3(256), 0,
+                     stream, c);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA combine launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+}  // namespace kvk

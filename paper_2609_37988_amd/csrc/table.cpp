@@ -66,9 +66,85 @@ int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_
   return (int32_t)per;
 }
 
+int64_t mla_block_bytes(int32_t W, int32_t bits, int32_t qscheme) {
+  if (bits == 16) return 64LL * W;                          // bf16, 32 tokens
+  if (qscheme == KVK_Q_KIVI32) return 4LL * W * (bits + 1);  // codes + fp16 (scale, zero) / 32 ch
+  return 4LL * W * bits + 128;                              // codes + two bf16 scales / token
+}
+
+int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_blocks) {
+  // About 4 MiB of cache per workgroup: the split partial of the heads is
+  // Hq * (d + 2) * 4 bytes (66 KiB at Hq = 32, d = 512), so long splits keep its
+  // write and read a few percent of the cache bytes.
+#ifndef KVK_MLA_SPLIT_TARGET
+#define KVK_MLA_SPLIT_TARGET (4 * 1024 * 1024)
+#endif
+  const int64_t bb = t->block_bytes[anchor];
+  const int64_t nr = mla_ring_depth(t->rank[anchor] + t->d.rope_dim, t->bits[anchor],
+                                    t->d.qscheme == KVK_Q_KIVI32);
+  int64_t target = KVK_MLA_SPLIT_TARGET / bb;
+  if (target < nr) target = nr;
+  const int64_t nb = n_blocks > 0 ? n_blocks : 1;
+  const int64_t nsplit = (nb + target - 1) / target;
+  int64_t per = (nb + nsplit - 1) / nsplit;
+  per = (per + nr - 1) / nr * nr;
+  return (int32_t)per;
+}
+
+int32_t mla_units(const kvk_table* t, int32_t anchor, int32_t n_stored) {
+  const int32_t nb = n_stored / KVK_GROUP;
+  const int32_t u = n_splits(nb, mla_split_blocks_for(t, anchor, nb));
+  return u > 0 ? u : 1;
+}
+
+void mla_workspace(const kvk_table* t, int32_t l0, int32_t l1, MlaWorkspace* ws) {
+  const kvk_dims& d = t->d;
+  int64_t off = 0;
+  for (int l = l0; l < l1; ++l) {
+    const int32_t a = t->info.anchor_of[l];
+    ws->q_off[l] = off;
+    off += round256((int64_t)d.batch * d.n_q_heads * (t->rank[a] + d.rope_dim) * 2);
+  }
+  for (int l = l0; l < l1; ++l) {
+    const int32_t a = t->info.anchor_of[l];
+    ws->units_cap[l] = mla_units(t, a, t->cap);
+    ws->part_off[l] = off;
+    off += round256((int64_t)d.batch * ws->units_cap[l] * d.n_q_heads * (t->rank[a] + 2) * 4);
+  }
+  ws->total = off;
+}
+
 }  // namespace kvk
 
 using namespace kvk;
+
+static kvk_status validate_mla(const kvk_dims& d, const kvk_action* plan) {
+  if (d.n_q_heads < 32 || d.n_q_heads % 32 != 0 || d.n_q_heads > 256)
+    return fail(KVK_ERR_UNSUPPORTED, "MLA n_q_heads %d must be a multiple of 32 up to 256",
+                d.n_q_heads);
+  if (d.n_kv_heads < 1 || d.head_dim < 1)
+    return fail(KVK_ERR_INVALID, "MLA n_kv_heads/head_dim (the bf16 GQA reference of eq. (2)) must be >= 1");
+  if (d.latent_dim < 256 || d.latent_dim % 256 != 0)
+    return fail(KVK_ERR_INVALID,
+                "latent_dim %d must be a positive multiple of 256 (every rank in {r/8..r} a multiple of 32)",
+                d.latent_dim);
+  if (d.rope_dim != 64) return fail(KVK_ERR_UNSUPPORTED, "rope_dim %d: only 64 is provided", d.rope_dim);
+  if (d.nope_dim < 32 || d.nope_dim % 32 != 0 || d.nope_dim > 256)
+    return fail(KVK_ERR_UNSUPPORTED, "nope_dim %d must be a multiple of 32 up to 256", d.nope_dim);
+  if (d.v_dim < 16 || d.v_dim % 16 != 0 || d.v_dim > 256)
+    return fail(KVK_ERR_UNSUPPORTED, "v_dim %d must be a multiple of 16 up to 256", d.v_dim);
+  const int32_t r = d.latent_dim;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const kvk_action& a = plan[l];
+    if (a.inherit) continue;
+    if (a.rank != r && a.rank != r / 2 && a.rank != r / 4 && a.rank != r / 8)
+      return fail(KVK_ERR_INVALID, "layer %d: rank %d not in {r/8, r/4, r/2, r} with r = %d", l,
+                  a.rank, r);
+    if (a.rank > 512)
+      return fail(KVK_ERR_UNSUPPORTED, "layer %d: kept width %d above 512 is not provided", l, a.rank);
+  }
+  return KVK_OK;
+}
 
 static bool is_bits(int32_t b) { return b == 2 || b == 4 || b == 8 || b == 16; }
 
@@ -79,32 +155,38 @@ extern "C" kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* pl
   const kvk_dims& d = *dims;
   if (d.kind != KVK_GQA && d.kind != KVK_MLA)
     return fail(KVK_ERR_INVALID, "kind %d is neither GQA nor MLA", d.kind);
-  if (d.kind == KVK_MLA)
-    return fail(KVK_ERR_UNSUPPORTED, "MLA latent caches are not provided by this build");
+  const bool mla = d.kind == KVK_MLA;
   if (d.n_layers < 1 || d.n_layers > KVK_MAX_LAYERS)
     return fail(KVK_ERR_INVALID, "n_layers %d outside 1..%d", d.n_layers, KVK_MAX_LAYERS);
-  if (d.n_kv_heads < 1 || d.n_q_heads < 1 || d.n_q_heads % d.n_kv_heads != 0)
-    return fail(KVK_ERR_INVALID, "n_q_heads %d must be a positive multiple of n_kv_heads %d",
-                d.n_q_heads, d.n_kv_heads);
-  if (d.head_dim != 64 && d.head_dim != 128)
-    return fail(KVK_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", d.head_dim);
+  if (!mla) {
+    if (d.n_kv_heads < 1 || d.n_q_heads < 1 || d.n_q_heads % d.n_kv_heads != 0)
+      return fail(KVK_ERR_INVALID, "n_q_heads %d must be a positive multiple of n_kv_heads %d",
+                  d.n_q_heads, d.n_kv_heads);
+    if (d.head_dim != 64 && d.head_dim != 128)
+      return fail(KVK_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", d.head_dim);
+  }
   if (d.qscheme != KVK_Q_KIVI32 && d.qscheme != KVK_Q_SYMROW)
     return fail(KVK_ERR_INVALID, "qscheme %d unknown", d.qscheme);
   if (d.batch < 1 || d.max_tokens < 1)
     return fail(KVK_ERR_INVALID, "batch %d and max_tokens %d must be >= 1", d.batch, d.max_tokens);
   if (d.keep_tokens < 0 || d.keep_tokens > d.max_tokens)
     return fail(KVK_ERR_INVALID, "keep_tokens %d outside 0..max_tokens", d.keep_tokens);
-  const int32_t G = d.n_q_heads / d.n_kv_heads;
   if (plan[0].inherit)
     return fail(KVK_ERR_INVALID, "layer 0 must own a cache (it has no earlier anchor)");
-  const int32_t width = 2 * d.n_kv_heads * d.head_dim;
+  const int32_t width = 2 * d.n_kv_heads * d.head_dim;  // cached scalars per token, bf16 GQA
   for (int l = 0; l < d.n_layers; ++l) {
     const kvk_action& a = plan[l];
     if (a.inherit) continue;
     if (!is_bits(a.bits)) return fail(KVK_ERR_INVALID, "layer %d: bits %d not in {2,4,8,16}", l, a.bits);
-    if (a.rank != 0 && a.rank != width)
+    if (!mla && a.rank != 0 && a.rank != width)
       return fail(KVK_ERR_INVALID, "layer %d: GQA has no rank axis (rank %d)", l, a.rank);
   }
+  if (mla) {
+    const kvk_status st = validate_mla(d, plan);
+    if (st != KVK_OK) return st;
+  }
+  const int32_t G = mla ? 1 : d.n_q_heads / d.n_kv_heads;
+  const int64_t streams = mla ? (int64_t)d.batch : (int64_t)d.batch * d.n_kv_heads;
 
   kvk_table* t = new (std::nothrow) kvk_table();
   if (!t) return fail(KVK_ERR_INVALID, "out of host memory");
@@ -129,20 +211,26 @@ extern "C" kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* pl
       last = l;
       run = 0;
       t->bits[l] = a.bits;
-      t->block_bytes[l] = gqa_block_bytes(d.head_dim, a.bits, d.qscheme);
-      const int64_t sb = round256(t->nb_cap * t->block_bytes[l] + 128LL * d.head_dim);
+      // Scalars one stream stores per token: GQA K and V of one head; MLA c[:d] and k^R.
+      const int32_t per_tok = mla ? a.rank + d.rope_dim : 2 * d.head_dim;
+      t->rank[l] = mla ? a.rank : 0;
+      t->block_bytes[l] = mla ? mla_block_bytes(per_tok, a.bits, d.qscheme)
+                              : gqa_block_bytes(d.head_dim, a.bits, d.qscheme);
+      const int64_t sb = round256(t->nb_cap * t->block_bytes[l] + 64LL * per_tok);
       inf.stream_bytes[l] = sb;
-      inf.layer_bytes[l] = sb * d.batch * d.n_kv_heads;
+      inf.layer_bytes[l] = sb * streams;
       inf.layer_offset[l] = offset;
       offset += round256(inf.layer_bytes[l]);
-      inf.layer_cost_bits[l] = (double)width * a.bits;  // eq. (1) with d = 2 n_kv d_h, d_R = 0
+      // eq. (1): (d + d_R) b; for GQA d = 2 n_kv d_h and d_R = 0.
+      inf.layer_cost_bits[l] = mla ? (double)per_tok * a.bits : (double)width * a.bits;
       const int64_t per_stream = (int64_t)t->nb_cap * t->block_bytes[l] +
-                                 (int64_t)(t->cap % KVK_GROUP) * 4 * d.head_dim;
-      inf.layer_bits_per_elt[l] = t->cap ? per_stream * 8.0 / ((double)t->cap * 2 * d.head_dim) : 0.0;
-      stored_alg += per_stream * d.batch * d.n_kv_heads;
+                                 (int64_t)(t->cap % KVK_GROUP) * 2 * per_tok;
+      inf.layer_bits_per_elt[l] = t->cap ? per_stream * 8.0 / ((double)t->cap * per_tok) : 0.0;
+      stored_alg += per_stream * streams;
       inf.n_anchors++;
     } else {
       t->bits[l] = 0;
+      t->rank[l] = 0;
       inf.layer_cost_bits[l] = 0.0;
     }
     ++run;
@@ -154,7 +242,7 @@ extern "C" kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* pl
     t->next_anchor[l] = nxt;
     if (!plan[l].inherit) nxt = l;
   }
-  if ((int64_t)G * max_readers > 64) {
+  if (!mla && (int64_t)G * max_readers > 64) {
     delete t;
     return fail(KVK_ERR_UNSUPPORTED,
                 "an anchor serves %d layers x %d query heads per KV head = %d > 64 query rows",
@@ -189,6 +277,12 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
   if (l0 < 0 || l1 > t->d.n_layers || l0 >= l1)
     return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, t->d.n_layers);
   const kvk_dims& d = t->d;
+  if (d.kind == KVK_MLA) {
+    MlaWorkspace ws;
+    mla_workspace(t, l0, l1, &ws);
+    *out = (size_t)ws.total;
+    return KVK_OK;
+  }
   const int32_t G = d.n_q_heads / d.n_kv_heads;
   // Split partials: per query row (layer, b, head) and split, (o[d_h], m, l, 2 pad) in fp32.
   const int32_t nblk = t->nb_cap;  // full blocks; the tail is merged by the combine kernel

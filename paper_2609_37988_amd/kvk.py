@@ -216,19 +216,49 @@ def _need(cond: bool, msg: str):
         raise ValueError(msg)
 
 
+def _q_width(d: Dims) -> int:
+    """Per-head query width: d_h (GQA) or nope_dim + rope_dim (MLA)."""
+    return d.nope_dim + d.rope_dim if d.kind == MLA else d.head_dim
+
+
+def _out_width(d: Dims) -> int:
+    """Per-head output width: d_h (GQA) or v_dim (MLA)."""
+    return d.v_dim if d.kind == MLA else d.head_dim
+
+
+def _check_weights(t: Table, nl: int, w_uk, w_uv):
+    d = t.dims
+    if d.kind != MLA:
+        _need(w_uk is None and w_uv is None, "w_uk / w_uv are for MLA tables only")
+        return
+    _need(w_uk is not None and w_uv is not None, "an MLA table needs w_uk and w_uv")
+    _need(w_uk.dtype == torch.bfloat16 and w_uv.dtype == torch.bfloat16 and w_uk.is_contiguous()
+          and w_uv.is_contiguous(), "w_uk / w_uv must be contiguous bf16")
+    _need(w_uk.numel() == nl * d.n_q_heads * d.nope_dim * d.latent_dim,
+          "w_uk size must be layers*Hq*nope_dim*latent_dim")
+    _need(w_uv.numel() == nl * d.n_q_heads * d.v_dim * d.latent_dim,
+          "w_uv size must be layers*Hq*v_dim*latent_dim")
+
+
 def compress_layer(t: Table, layer: int, k: torch.Tensor, v: torch.Tensor, n_tokens: int,
                    keep_idx: Optional[torch.Tensor], arena: torch.Tensor, stream=None):
-    """k, v: [B, Hkv, n_tokens, d_h] contiguous bf16/fp32 on the device."""
+    """GQA: k, v [B, Hkv, n_tokens, d_h].  MLA: k = latent [B, n_tokens, r], v = positional
+    key [B, n_tokens, d_R].  Contiguous bf16/fp32 on the device."""
     d = t.dims
     _need(k.dtype == v.dtype and k.is_contiguous() and v.is_contiguous(),
           "k and v must be contiguous tensors of one dtype")
-    _need(k.numel() == v.numel() == d.batch * d.n_kv_heads * n_tokens * d.head_dim,
-          "k/v size must be B*Hkv*n_tokens*d_h")
+    if d.kind == MLA:
+        _need(k.numel() == d.batch * n_tokens * d.latent_dim and v.numel() == d.batch * n_tokens * d.rope_dim,
+              "latent size must be B*n_tokens*r and k^R size B*n_tokens*d_R")
+        streams = d.batch
+    else:
+        _need(k.numel() == v.numel() == d.batch * d.n_kv_heads * n_tokens * d.head_dim,
+              "k/v size must be B*Hkv*n_tokens*d_h")
+        streams = d.batch * d.n_kv_heads
     if keep_idx is not None:
         _need(keep_idx.dtype == torch.int32 and keep_idx.is_contiguous(),
               "keep_idx must be a contiguous int32 tensor")
-        _need(keep_idx.numel() == d.batch * d.n_kv_heads * d.keep_tokens,
-              "keep_idx size must be B*Hkv*keep_tokens")
+        _need(keep_idx.numel() == streams * d.keep_tokens, "keep_idx size must be streams*keep_tokens")
     _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
     _check(load().kvk_compress_layer(t.handle, layer, _ptr(k), _ptr(v), _dtype_code(k), n_tokens,
                                      _ptr(keep_idx), _ptr(arena), _stream(stream)))
@@ -238,12 +268,15 @@ def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor
                      scale: float, arena: torch.Tensor, out: torch.Tensor, workspace: torch.Tensor,
                      w_uk: Optional[torch.Tensor] = None, w_uv: Optional[torch.Tensor] = None,
                      stream=None):
-    """q: [layers, B, Hq, d_h] bf16/fp32; out: fp32 of the same shape."""
+    """q: [layers, B, Hq, d_h] (MLA: [layers, B, Hq, nope + d_R]) bf16/fp32; out fp32
+    [layers, B, Hq, d_h] (MLA: v_dim); w_uk/w_uv: MLA up-projections, bf16."""
     d = t.dims
-    rows = (layer_end - layer_begin) * d.batch * d.n_q_heads * d.head_dim
+    nl = layer_end - layer_begin
     _need(q.is_contiguous() and out.is_contiguous() and out.dtype == torch.float32,
           "q must be contiguous; out contiguous fp32")
-    _need(q.numel() == rows and out.numel() == rows, "q/out size must be layers*B*Hq*d_h")
+    _need(q.numel() == nl * d.batch * d.n_q_heads * _q_width(d), "q size must be layers*B*Hq*width")
+    _need(out.numel() == nl * d.batch * d.n_q_heads * _out_width(d), "out size must be layers*B*Hq*width")
+    _check_weights(t, nl, w_uk, w_uv)
     _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
     _check(load().kvk_decode_attention(
         t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
@@ -257,8 +290,10 @@ def decode_splits(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n
                   stream=None):
     """First phase of decode_attention: split partials into `workspace`."""
     d = t.dims
-    rows = (layer_end - layer_begin) * d.batch * d.n_q_heads * d.head_dim
-    _need(q.is_contiguous() and q.numel() == rows, "q must be contiguous, layers*B*Hq*d_h")
+    nl = layer_end - layer_begin
+    _need(q.is_contiguous() and q.numel() == nl * d.batch * d.n_q_heads * _q_width(d),
+          "q must be contiguous, layers*B*Hq*width")
+    _check_weights(t, nl, w_uk, w_uv)
     _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
     _check(load().kvk_decode_splits(
         t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
@@ -269,12 +304,16 @@ def decode_merge(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_
                  scale: float, arena: torch.Tensor, workspace: torch.Tensor, out: torch.Tensor,
                  w_uk: Optional[torch.Tensor] = None, w_uv: Optional[torch.Tensor] = None,
                  stream=None):
-    """Second phase of decode_attention: tail tokens + merge of the split partials."""
+    """Second phase of decode_attention: merge of the split partials (GQA: with the
+    tail tokens; MLA: then the W_UV up-projection)."""
     d = t.dims
-    rows = (layer_end - layer_begin) * d.batch * d.n_q_heads * d.head_dim
-    _need(q.is_contiguous() and q.numel() == rows, "q must be contiguous, layers*B*Hq*d_h")
-    _need(out.is_contiguous() and out.dtype == torch.float32 and out.numel() == rows,
-          "out must be contiguous fp32, layers*B*Hq*d_h")
+    nl = layer_end - layer_begin
+    _need(q.is_contiguous() and q.numel() == nl * d.batch * d.n_q_heads * _q_width(d),
+          "q must be contiguous, layers*B*Hq*width")
+    _need(out.is_contiguous() and out.dtype == torch.float32 and
+          out.numel() == nl * d.batch * d.n_q_heads * _out_width(d),
+          "out must be contiguous fp32, layers*B*Hq*width")
+    _check_weights(t, nl, w_uk, w_uv)
     _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
     _check(load().kvk_decode_merge(
         t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
@@ -290,10 +329,17 @@ def read_bytes(t: Table, layer_begin: int, layer_end: int, n_stored: int) -> int
 
 def debug_dequantize(t: Table, layer: int, n_stored: int, arena: torch.Tensor, k_out: torch.Tensor,
                      v_out: torch.Tensor, stream=None):
+    """GQA: k_out, v_out fp32 [B, Hkv, n_stored, d_h].  MLA: k_out = latent fp32
+    [B, n_stored, d] (the anchor's kept width), v_out = k^R fp32 [B, n_stored, d_R]."""
     d = t.dims
-    n = d.batch * d.n_kv_heads * max(n_stored, 0) * d.head_dim
+    n = max(n_stored, 0)
+    if d.kind == MLA:
+        a = table_query(t).anchor_of[layer]
+        nk, nv = d.batch * n * t.plan[a].rank, d.batch * n * d.rope_dim
+    else:
+        nk = nv = d.batch * d.n_kv_heads * n * d.head_dim
     _need(k_out.dtype == torch.float32 and v_out.dtype == torch.float32, "outputs must be fp32")
-    _need(k_out.numel() >= n and v_out.numel() >= n, "outputs smaller than B*Hkv*n_stored*d_h")
+    _need(k_out.numel() >= nk and v_out.numel() >= nv, "outputs smaller than the dequantised cache")
     _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
     _check(load().kvk_debug_dequantize(t.handle, layer, n_stored, _ptr(arena), _ptr(k_out),
                                        _ptr(v_out), _stream(stream)))

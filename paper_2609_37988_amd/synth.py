@@ -8,7 +8,10 @@ the decode benchmark; key tensors carry a per-channel log-normal outlier scale,
 the per-channel key structure App. A cites from KVQuant.
 
 Plans are drawn the way the workloads describe them: a random subset of layers
-inherits (never layer 0), anchor bit-widths are drawn uniformly.
+inherits (never layer 0), anchor bit-widths (and, for the MLA-style stack, kept
+latent widths) are drawn uniformly.  The MLA-style stack follows the paper's
+converted 7B geometry (latent 512 + 64, App. C.2) with 32 heads and 128-wide
+no-RoPE and value heads; its up-projections are N(0, 1/r).
 """
 from dataclasses import dataclass, field
 from typing import List, Optional
@@ -97,6 +100,81 @@ def workload(cfg: int, variant: Optional[str] = None) -> Workload:
     raise ValueError(f"unknown workload {cfg}")
 
 
+@dataclass
+class MlaWorkload:
+    """An MLA-style stack (§2.1 rank axis): one latent of width r per token shared by
+    the heads, a 64-wide positional key, per-head no-RoPE query/key width 128 and
+    value width 128.  plan entries are (inherit, bits, rank)."""
+    name: str
+    n_layers: int
+    n_q_heads: int
+    latent_dim: int
+    batch: int
+    tokens: int
+    plan: List[tuple]
+    rope_dim: int = 64
+    nope_dim: int = 128
+    v_dim: int = 128
+    keep_tokens: int = 0
+    qscheme: int = KIVI32
+    ref_kv_heads: int = 4    # the bf16 GQA model eq. (2) is quoted against
+    ref_head_dim: int = 128
+    in_dtype: torch.dtype = torch.bfloat16
+    q_dtype: torch.dtype = torch.bfloat16
+    seed: int = 1003
+
+    def softmax_scale(self) -> float:
+        return 1.0 / float(np.sqrt(self.nope_dim + self.rope_dim))
+
+
+def plan_ranks(seed: int, n_layers: int, latent_dim: int, bits: int, n_inherit: int = 0):
+    """Every anchor's kept width drawn uniformly from {r, r/2, r/4, r/8}; n_inherit
+    layers drawn from 1..L-1 inherit."""
+    rng = np.random.default_rng(seed)
+    inh = set()
+    if n_inherit:
+        inh = set(int(x) for x in rng.choice(np.arange(1, n_layers), n_inherit, replace=False))
+    ranks = [latent_dim, latent_dim // 2, latent_dim // 4, latent_dim // 8]
+    return [(1, 16, 0) if l in inh else (0, bits, int(rng.choice(ranks))) for l in range(n_layers)]
+
+
+def mla_workload(variant: Optional[str] = None) -> MlaWorkload:
+    """The MLA-style decode workload: 32 layers, 32 query heads, latent 512 + 64,
+    batch 16, context 16384, per-layer kept width drawn from {512, 256, 128, 64};
+    variant None: bf16 cache, 'int4': KIVI32 4-bit latent and positional key."""
+    bits = 4 if variant == "int4" else 16
+    return MlaWorkload("mla-32l-r512-bf16" if bits == 16 else "mla-32l-r512-int4", 32, 32, 512, 16,
+                       16384, plan_ranks(1003, 32, 512, bits))
+
+
+def mla_layer(w: MlaWorkload, layer: int, device="cpu", batch: Optional[int] = None,
+              tokens: Optional[int] = None):
+    """Latent [B, T, r] and positional key [B, T, d_R] of one layer, N(0,1), in w.in_dtype."""
+    B = w.batch if batch is None else batch
+    T = w.tokens if tokens is None else tokens
+    g = generator(w.seed * 1000 + layer, device)
+    c = torch.randn((B, T, w.latent_dim), generator=g, device=device, dtype=torch.float32)
+    r = torch.randn((B, T, w.rope_dim), generator=g, device=device, dtype=torch.float32)
+    return c.to(w.in_dtype), r.to(w.in_dtype)
+
+
+def mla_weights(w: MlaWorkload, n_layers: int, device="cpu"):
+    """W_UK [L, Hq, nope, r] and W_UV [L, Hq, v, r], N(0, 1/r), bf16."""
+    g = generator(w.seed * 1000 + 777, device)
+    sd = 1.0 / float(np.sqrt(w.latent_dim))
+    wk = torch.randn((n_layers, w.n_q_heads, w.nope_dim, w.latent_dim), generator=g, device=device) * sd
+    wv = torch.randn((n_layers, w.n_q_heads, w.v_dim, w.latent_dim), generator=g, device=device) * sd
+    return wk.to(torch.bfloat16), wv.to(torch.bfloat16)
+
+
+def mla_queries(w: MlaWorkload, n_layers: int, device="cpu", batch: Optional[int] = None):
+    """q [L, B, Hq, nope + d_R] ~ N(0,1): per head q_nope then q_rope."""
+    B = w.batch if batch is None else batch
+    g = generator(w.seed * 1000 + 999, device)
+    q = torch.randn((n_layers, B, w.n_q_heads, w.nope_dim + w.rope_dim), generator=g, device=device)
+    return q.to(w.q_dtype)
+
+
 def generator(seed: int, device) -> torch.Generator:
     g = torch.Generator(device=device)
     g.manual_seed(int(seed))
@@ -153,6 +231,18 @@ def kv_random(seed: int, B: int, H: int, T: int, D: int, dtype=torch.bfloat16, o
     if outliers:
         k = k * torch.randn((1, H, 1, D), generator=g, device=device).exp()
     return k.to(dtype), v.to(dtype)
+
+
+def latent_random(seed: int, B: int, T: int, W: int, dtype=torch.bfloat16, device="cpu", scale: float = 1.0):
+    """[B, T, W] ~ N(0, scale^2) (latents or positional keys)."""
+    g = generator(seed, device)
+    return (torch.randn((B, T, W), generator=g, device=device) * scale).to(dtype)
+
+
+def weights_random(seed: int, L: int, H: int, rows: int, r: int, device="cpu"):
+    """[L, H, rows, r] ~ N(0, 1/r), bf16 (up-projections)."""
+    g = generator(seed, device)
+    return (torch.randn((L, H, rows, r), generator=g, device=device) / float(np.sqrt(r))).to(torch.bfloat16)
 
 
 def q_random(seed: int, L: int, B: int, Hq: int, D: int, dtype=torch.bfloat16, device="cpu"):

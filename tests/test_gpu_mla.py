@@ -1,0 +1,220 @@
+"""GPU parity of the MLA (rank-axis) path against the oracle, through the C ABI.
+
+Bit-exact: arena bytes (codes, metadata, bf16 blocks) and dequantised values.
+Attention outputs: max|diff| <= 2e-3 * max|out| (fp32 accumulation; the absorbed
+query, the latent tile and the probabilities enter the matrix cores as fp16).
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import mla as OM
+from oracle import plan as OP
+from paper_2609_37988_amd import kvk, synth
+
+from gpu_common import TOL, rel_err, say
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _np(x):
+    return x.detach().float().cpu().numpy()
+
+
+class MlaCase:
+    """An MLA table plus its device buffers and the oracle's view of it."""
+
+    def __init__(self, n_layers, Hq, r, B, max_tokens, plan, qscheme=kvk.KIVI32, keep=0, nope=128, v=128):
+        self.dims = kvk.make_dims(kvk.MLA, n_layers, Hq, 4, 128, r, 64, nope, v, qscheme=qscheme, batch=B,
+                                  max_tokens=max_tokens, keep_tokens=keep)
+        self.plan = kvk.make_plan(plan)
+        self.table = kvk.layer_table(self.dims, self.plan)
+        self.info = kvk.table_query(self.table)
+        self.arena = torch.zeros(max(self.info.arena_bytes, 256), dtype=torch.uint8, device=DEV)
+        self.odims = OP.Dims(OP.MLA, n_layers, Hq, 4, 128, latent_dim=r, rope_dim=64, nope_dim=nope,
+                             v_dim=v, qscheme=qscheme, batch=B, max_tokens=max_tokens, keep_tokens=keep)
+        self.oplan = [OP.Action(bool(a.inherit), a.bits, a.rank) for a in self.plan]
+        self.inputs = {}
+
+    def compress(self, layer, C, R, n, keep=None):
+        kvk.compress_layer(self.table, layer, C.to(DEV).contiguous(), R.to(DEV).contiguous(), n,
+                           None if keep is None else keep.to(DEV).contiguous(), self.arena)
+        self.inputs[layer] = (_np(C), _np(R), None if keep is None else keep.cpu().numpy())
+
+    def oracle_arena(self):
+        """The oracle's arena from the inputs written so far (other regions zero)."""
+        offs, total = OP.arena_offsets(self.odims, self.oplan)
+        arena = np.zeros(total, dtype=np.uint8)
+        for l, (C, R, keep) in self.inputs.items():
+            a = self.oplan[l]
+            reg = OM.compress_layer(self.odims, a.bits, a.rank, C, R, keep)
+            arena[offs[l]:offs[l] + reg.size] = reg
+        return arena
+
+    def decode(self, q, wk, wv, n, scale, l0=0, l1=None):
+        l1 = self.dims.n_layers if l1 is None else l1
+        d = self.dims
+        out = torch.empty((l1 - l0, d.batch, d.n_q_heads, d.v_dim), dtype=torch.float32, device=DEV)
+        ws = torch.empty(max(kvk.workspace_bytes(self.table, l0, l1), 256), dtype=torch.uint8, device=DEV)
+        kvk.decode_attention(self.table, l0, l1, q.to(DEV).contiguous(), n, scale, self.arena, out, ws,
+                             w_uk=wk.to(DEV).contiguous(), w_uv=wv.to(DEV).contiguous())
+        return out
+
+    def dequant(self, layer, n):
+        d = self.dims
+        rank = self.plan[self.info.anchor_of[layer]].rank
+        c = torch.empty((d.batch, max(n, 1), rank), dtype=torch.float32, device=DEV)
+        r = torch.empty((d.batch, max(n, 1), 64), dtype=torch.float32, device=DEV)
+        kvk.debug_dequantize(self.table, layer, n, self.arena, c, r)
+        return _np(c[:, :n]), _np(r[:, :n])
+
+    def check_layer(self, layer, n):
+        """Stream bytes and dequantised values of `layer` equal the oracle's bit for bit."""
+        a = self.info.anchor_of[layer]
+        ref = self.oracle_arena()
+        off, nb = self.info.layer_offset[a], self.info.layer_bytes[a]
+        got = self.arena[off:off + nb].cpu().numpy()
+        assert np.array_equal(got, ref[off:off + nb]), f"arena bytes differ (layer {layer})"
+        Cr, Rr = OM.dequant_layer(self.odims, self.oplan, ref, layer, n)
+        Cg, Rg = self.dequant(layer, n)
+        assert np.array_equal(Cg, Cr) and np.array_equal(Rg, Rr), "dequantised values differ"
+
+    def oracle_out(self, q, wk, wv, n, scale, l0=0, l1=None, absorbed=False):
+        return OM.decode_step(self.odims, self.oplan, self.oracle_arena(), _np(q).astype(np.float64),
+                              _np(wk).astype(np.float64), _np(wv).astype(np.float64), n, scale, l0, l1,
+                              absorbed=absorbed)
+
+
+SCALE = 1.0 / np.sqrt(192.0)
+
+
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW], ids=["kivi32", "symrow"])
+@pytest.mark.parametrize("bits", [16, 8, 4, 2])
+@pytest.mark.parametrize("d", [64, 512])
+def test_single_layer_ragged(qs, bits, d):
+    """B 2, 32 heads, r 512 kept to d, 200 tokens (6 full blocks + an 8-token tail)."""
+    say(f"case mla single-layer qs={qs} bits={bits} d={d}")
+    n = 200
+    c = MlaCase(1, 32, 512, 2, 224, [(0, bits, d)], qscheme=qs)
+    C = synth.latent_random(10 + bits + d, 2, n, 512)
+    R = synth.latent_random(11 + bits + d, 2, n, 64)
+    c.compress(0, C, R, n)
+    c.check_layer(0, n)
+    q = synth.q_random(12 + bits, 1, 2, 32, 192)
+    wk = synth.weights_random(13, 1, 32, 128, 512)
+    wv = synth.weights_random(14, 1, 32, 128, 512)
+    out = _np(c.decode(q, wk, wv, n, SCALE))
+    ref = c.oracle_out(q, wk, wv, n, SCALE)
+    err = rel_err(out, ref)
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
+
+
+def test_rank_stack_depth_and_invariants():
+    """Anchors at every kept width (512, 256, 128, 64) and bit-width, two inheritors,
+    one decode call over all layers; determinism; per-layer calls equal the stacked
+    call bit for bit; an inheritor given its anchor's query and up-projections
+    reproduces the anchor's output exactly."""
+    say("case mla rank-stack")
+    plan = [(0, 16, 512), (1, 16, 0), (0, 4, 256), (0, 8, 128), (1, 16, 0), (0, 2, 64)]
+    n = 150
+    c = MlaCase(6, 32, 512, 2, 160, plan)
+    for l in (0, 2, 3, 5):
+        c.compress(l, synth.latent_random(100 + l, 2, n, 512), synth.latent_random(200 + l, 2, n, 64), n)
+        c.check_layer(l, n)
+    q = synth.q_random(7, 6, 2, 32, 192)
+    wk = synth.weights_random(8, 6, 32, 128, 512)
+    wv = synth.weights_random(9, 6, 32, 128, 512)
+    out = c.decode(q, wk, wv, n, SCALE)
+    ref = c.oracle_out(q, wk, wv, n, SCALE)
+    err = rel_err(_np(out), ref)
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
+    assert torch.equal(out, c.decode(q, wk, wv, n, SCALE))
+    for l in range(6):
+        one = c.decode(q[l:l + 1], wk[l:l + 1], wv[l:l + 1], n, SCALE, l, l + 1)
+        assert torch.equal(one[0], out[l]), f"layer {l}"
+    q2, wk2, wv2 = q.clone(), wk.clone(), wv.clone()
+    for dst, src in ((1, 0), (4, 3)):
+        q2[dst], wk2[dst], wv2[dst] = q2[src], wk2[src], wv2[src]
+    o2 = c.decode(q2, wk2, wv2, n, SCALE)
+    assert torch.equal(o2[1], o2[0]) and torch.equal(o2[4], o2[3])
+
+
+@pytest.mark.parametrize("bits,n", [(16, 4000), (4, 12000)])
+def test_many_heads_and_splits(bits, n):
+    """64 heads (two 32-head chunks) and streams longer than one split."""
+    say(f"case mla splits bits={bits} n={n}")
+    c = MlaCase(1, 64, 512, 1, n, [(0, bits, 512)])
+    c.compress(0, synth.latent_random(30 + bits, 1, n, 512), synth.latent_random(31, 1, n, 64), n)
+    q = synth.q_random(32, 1, 1, 64, 192)
+    wk = synth.weights_random(33, 1, 64, 128, 512)
+    wv = synth.weights_random(34, 1, 64, 128, 512)
+    out = _np(c.decode(q, wk, wv, n, SCALE))
+    ref = c.oracle_out(q, wk, wv, n, SCALE, absorbed=True)
+    err = rel_err(out, ref)
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("n", [1, 31, 32, 33])
+def test_edge_lengths(n):
+    say(f"case mla edge n={n}")
+    c = MlaCase(1, 32, 256, 1, 64, [(0, 4, 128)])
+    C, R = synth.latent_random(40 + n, 1, n, 256), synth.latent_random(41 + n, 1, n, 64)
+    c.compress(0, C, R, n)
+    c.check_layer(0, n)
+    q = synth.q_random(42, 1, 1, 32, 192)
+    wk = synth.weights_random(43, 1, 32, 128, 256)
+    wv = synth.weights_random(44, 1, 32, 128, 256)
+    out = _np(c.decode(q, wk, wv, n, SCALE))
+    ref = c.oracle_out(q, wk, wv, n, SCALE)
+    assert rel_err(out, ref) <= TOL
+    if n == 1:  # one stored token: head h's output is W_UV[h][:, :d] c_0
+        Cd, _ = c.dequant(0, 1)
+        want = np.einsum("hvr,r->hv", _np(wv)[0][:, :, :128].astype(np.float64), Cd[0, 0].astype(np.float64))
+        assert rel_err(out[0, 0], want) <= TOL
+
+
+def test_empty_cache_gives_zeros():
+    say("case mla empty")
+    c = MlaCase(1, 32, 256, 2, 64, [(0, 4, 256)])
+    q = synth.q_random(50, 1, 2, 32, 192)
+    wk = synth.weights_random(51, 1, 32, 128, 256)
+    wv = synth.weights_random(52, 1, 32, 128, 256)
+    out = c.decode(q, wk, wv, 0, SCALE)
+    assert torch.count_nonzero(out).item() == 0
+
+
+@pytest.mark.parametrize("bits", [2, 16])
+def test_eviction_gather(bits):
+    """Keep 150 of 300 positions per sequence: the stored stream is the gathered one."""
+    say(f"case mla eviction bits={bits}")
+    n, keep = 300, 150
+    c = MlaCase(1, 32, 512, 2, n, [(0, bits, 256)], keep=keep)
+    kidx = synth.keep_random(61, 2, 1, n, keep).reshape(2, keep)
+    c.compress(0, synth.latent_random(62, 2, n, 512), synth.latent_random(63, 2, n, 64), n, kidx)
+    c.check_layer(0, keep)
+    q = synth.q_random(64, 1, 2, 32, 192)
+    wk = synth.weights_random(65, 1, 32, 128, 512)
+    wv = synth.weights_random(66, 1, 32, 128, 512)
+    out = _np(c.decode(q, wk, wv, keep, SCALE))
+    assert rel_err(out, c.oracle_out(q, wk, wv, keep, SCALE)) <= TOL
+
+
+def test_fp32_inputs_and_symrow_stack():
+    """fp32 latents and queries, the paper's own quantiser, two 32-head chunks."""
+    say("case mla fp32 symrow")
+    plan = [(0, 4, 256), (0, 8, 32), (1, 16, 0)]
+    n = 96
+    c = MlaCase(3, 64, 256, 2, 96, plan, qscheme=kvk.SYMROW)
+    for l in (0, 1):
+        c.compress(l, synth.latent_random(70 + l, 2, n, 256, dtype=torch.float32),
+                   synth.latent_random(72 + l, 2, n, 64, dtype=torch.float32), n)
+        c.check_layer(l, n)
+    q = synth.q_random(74, 3, 2, 64, 192, dtype=torch.float32)
+    wk = synth.weights_random(75, 3, 64, 128, 256)
+    wv = synth.weights_random(76, 3, 64, 128, 256)
+    out = _np(c.decode(q, wk, wv, n, SCALE))
+    assert rel_err(out, c.oracle_out(q, wk, wv, n, SCALE)) <= TOL

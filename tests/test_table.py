@@ -181,3 +181,94 @@ def test_binding_rejects_mis_sized_tensors():
     q = torch.zeros(1, 1, 4, 64, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         kvk.decode_attention(t, 0, 1, q, 64, 0.1, arena, torch.zeros(1, 1, 4, 63), arena)
+
+
+# ---------------------------------------------------------------------------
+# MLA tables (rank axis)
+# ---------------------------------------------------------------------------
+
+def _mla_dims(w):
+    return kvk.make_dims(kvk.MLA, w.n_layers, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, w.latent_dim,
+                         w.rope_dim, w.nope_dim, w.v_dim, qscheme=w.qscheme, batch=w.batch,
+                         max_tokens=w.tokens, keep_tokens=w.keep_tokens)
+
+
+def _mla_oracle_dims(w):
+    return P.Dims(P.MLA, w.n_layers, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, latent_dim=w.latent_dim,
+                  rope_dim=w.rope_dim, nope_dim=w.nope_dim, v_dim=w.v_dim, qscheme=w.qscheme, batch=w.batch,
+                  max_tokens=w.tokens, keep_tokens=w.keep_tokens)
+
+
+@pytest.mark.parametrize("variant,inherit", [(None, 0), ("int4", 0), ("int4", 10)])
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW])
+def test_mla_table_matches_oracle_accounting(variant, inherit, qs):
+    w = synth.mla_workload(variant)
+    w.qscheme = qs
+    if inherit:
+        w.plan = synth.plan_ranks(77, w.n_layers, w.latent_dim, 4, n_inherit=inherit)
+    t = kvk.layer_table(_mla_dims(w), kvk.make_plan(w.plan))
+    inf = kvk.table_query(t)
+    od = _mla_oracle_dims(w)
+    oplan = [P.Action(bool(i), b, r) for i, b, r in w.plan]
+    assert P.validate(od, oplan) is None
+    assert inf.anchor_of == P.anchor_of(oplan)
+    offs, total = P.arena_offsets(od, oplan)
+    assert inf.layer_offset == offs and inf.arena_bytes == total
+    for l, a in enumerate(oplan):
+        if not a.inherit:
+            assert inf.layer_bytes[l] == P.layer_bytes(od, a.bits, a.rank)
+            assert inf.stream_bytes[l] == P.stream_bytes(od, a.bits, a.rank)
+        assert inf.layer_cost_bits[l] == P.cost_bits(od, a)
+    assert inf.rho == pytest.approx(P.rho(od, oplan), rel=1e-15)
+    alg = P.read_bytes(od, oplan, 0, od.n_layers, od.stored_cap)
+    assert inf.rho_realized == pytest.approx(P.bf16_full_bytes(od) / alg, rel=1e-12)
+    for n in (0, 1, 33, od.stored_cap):
+        for l0, l1 in ((0, od.n_layers), (3, 9), (od.n_layers - 1, od.n_layers)):
+            assert kvk.read_bytes(t, l0, l1, n) == P.read_bytes(od, oplan, l0, l1, n)
+    assert kvk.workspace_bytes(t, 0, od.n_layers) == inf.workspace_bytes > 0
+
+
+def test_mla_workload_bytes():
+    """The MLA-style workload: 32 layers of bf16 latents at widths drawn from
+    {512, 256, 128, 64} + 64 hold about 5.1 GB at 16 x 16384 tokens."""
+    w = synth.mla_workload()
+    t = kvk.layer_table(_mla_dims(w), kvk.make_plan(w.plan))
+    alg = kvk.read_bytes(t, 0, w.n_layers, w.tokens)
+    assert alg == sum(w.batch * w.tokens * (r + 64) * 2 for _, _, r in w.plan)
+    assert 4.5e9 < alg < 5.7e9
+
+
+def test_mla_invalid_plans_and_dims():
+    def dims(**kw):
+        a = dict(n_layers=2, Hq=32, Hkv=4, hd=128, r=512, rope=64, nope=128, v=128)
+        a.update(kw)
+        return kvk.make_dims(kvk.MLA, a["n_layers"], a["Hq"], a["Hkv"], a["hd"], a["r"], a["rope"], a["nope"],
+                             a["v"], batch=1, max_tokens=64)
+    ok = kvk.make_plan([(0, 4, 512), (1, 16, 0)])
+    kvk.layer_table(dims(), ok)
+    _expect(kvk.ERR_INVALID, kvk.layer_table, dims(), kvk.make_plan([(0, 4, 100), (1, 16, 0)]))
+    _expect(kvk.ERR_INVALID, kvk.layer_table, dims(), kvk.make_plan([(0, 4, 0), (1, 16, 0)]))
+    _expect(kvk.ERR_INVALID, kvk.layer_table, dims(r=300), ok)
+    _expect(kvk.ERR_INVALID, kvk.layer_table, dims(Hkv=0), ok)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(rope=32), ok)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(Hq=16), ok)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(nope=100), ok)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(r=1024), kvk.make_plan([(0, 4, 1024), (1, 16, 0)]))
+    kvk.layer_table(dims(r=1024), kvk.make_plan([(0, 4, 512), (0, 2, 128)]))
+
+
+def test_mla_entry_points_reject_bad_arguments_without_launching():
+    d = kvk.make_dims(kvk.MLA, 2, 32, 4, 128, 256, 64, 128, 128, batch=1, max_tokens=64)
+    t = kvk.layer_table(d, kvk.make_plan([(0, 8, 128), (1, 16, 0)]))
+    h, Pv = t.handle, ctypes.c_void_p
+    f = Pv(256)
+    I, B = kvk.ERR_INVALID, kvk.ERR_BUFFER
+    need = kvk.workspace_bytes(t, 0, 2)
+    _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, 0.1, None, f, f, f, f, need, None)  # no w_uk
+    _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, 0.1, f, None, f, f, f, need, None)  # no w_uv
+    _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 65, 0.1, f, f, f, f, f, need, None)    # n_stored
+    _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, 0.1, Pv(264), f, f, f, f, need, None)  # align
+    _raw(B, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, 0.1, f, f, f, f, f, need - 1, None)
+    _raw(B, "kvk_decode_splits", h, 0, 2, f, kvk.BF16, 64, 0.1, f, f, f, f, need - 1, None)
+    _raw(I, "kvk_compress_layer", h, 0, f, f, kvk.BF16, 65, None, f, None)
+    _raw(kvk.OK, "kvk_compress_layer", h, 1, f, f, kvk.BF16, 64, None, f, None)  # inheritor: no-op
