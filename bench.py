@@ -14,6 +14,11 @@ prefill kernel (W1), which is timed separately and reported under
 in HBM.  The CPU baseline is the oracle (test infrastructure) timed on a bounded
 sample of the same workload.
 
+With --config 3 the workload is the MLA-style stack instead (32 layers, 32 heads,
+latent 512 + 64 kept to a per-layer width drawn from {512, 256, 128, 64}, batch 16,
+context 16384; --variant int4 for a KIVI32 4-bit latent): a step is the absorbed
+query (A1), the latent decode (D2) and the merge with the W_UV up-projection (C2).
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
 """
 import argparse
@@ -140,6 +145,154 @@ def cpu_baseline(w, table, n_stored, scale, n_layers_sample):
             "seconds": round(dt, 3)}
 
 
+def cpu_baseline_mla(w, table, n_stored, scale, n_layers_sample):
+    """Time the oracle's MLA decode (dequantise, reconstruct keys and values with the
+    up-projections, fp64 attention) for batch element 0 over the first
+    n_layers_sample layers; inputs compressed by the oracle beforehand (untimed)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import mla as OM
+    from oracle import plan as OP
+    from paper_2609_37988_amd import kvk, synth
+
+    d = table.dims
+    od = OP.Dims(OP.MLA, d.n_layers, d.n_q_heads, d.n_kv_heads, d.head_dim, latent_dim=d.latent_dim,
+                 rope_dim=d.rope_dim, nope_dim=d.nope_dim, v_dim=d.v_dim, qscheme=d.qscheme, batch=1,
+                 max_tokens=d.max_tokens, keep_tokens=d.keep_tokens)
+    info = kvk.table_query(table)
+    anc = info.anchor_of[:n_layers_sample]
+    streams = {}
+    for a in sorted(set(anc)):
+        c, r = synth.mla_layer(w, a, device="cpu", batch=1)
+        _, bits, rank = w.plan[a]
+        streams[a] = (bits, rank, OM.compress_stream(od, bits, rank, c[0].float().numpy(), r[0].float().numpy()))
+    q = synth.mla_queries(w, n_layers_sample, device="cpu", batch=1).float().numpy().astype(np.float64)
+    wk, wv = synth.mla_weights(w, n_layers_sample, device="cpu")
+    wk, wv = wk.float().numpy().astype(np.float64), wv.float().numpy().astype(np.float64)
+    nope = d.nope_dim
+    t0 = time.perf_counter()
+    for l in range(n_layers_sample):
+        bits, rank, st = streams[anc[l]]
+        C, R = OM.dequant_stream(od, bits, rank, st, n_stored)
+        OM.attention_reconstructed(q[l, 0, :, :nope], q[l, 0, :, nope:], C, R, wk[l], wv[l], scale)
+    dt = time.perf_counter() - t0
+    sample_bytes = kvk.read_bytes(table, 0, n_layers_sample, n_stored) // d.batch
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"batch element 0 of {d.batch}, layers 0..{n_layers_sample - 1} "
+                      f"({len(set(anc))} anchors), {n_stored} tokens: {sample_bytes} algorithmic bytes "
+                      f"in {dt:.2f} s (numpy fp64 oracle, keys and values reconstructed with the "
+                      f"up-projections; BLAS threads = cores)",
+            "seconds": round(dt, 3)}
+
+
+def run_mla(args):
+    """The MLA-style stack: prefill write (W2), then timed decode steps (A1 + D2, C2)."""
+    import numpy as np
+    import torch
+
+    from paper_2609_37988_amd import kvk, synth
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = synth.mla_workload(args.variant)
+    if args.qscheme == "symrow":
+        w.qscheme = kvk.SYMROW
+    n_tok = w.tokens
+    n_stored = w.keep_tokens if w.keep_tokens else n_tok
+    dims = kvk.make_dims(kvk.MLA, w.n_layers, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, w.latent_dim,
+                         w.rope_dim, w.nope_dim, w.v_dim, qscheme=w.qscheme, batch=w.batch,
+                         max_tokens=n_tok, keep_tokens=w.keep_tokens)
+    table = kvk.layer_table(dims, kvk.make_plan(w.plan))
+    info = kvk.table_query(table)
+    log(f"workload {w.name}: arena {info.arena_bytes / 1e9:.2f} GB, rho eq.(2) {info.rho:.2f}, "
+        f"anchors {info.n_anchors}")
+    arena = torch.empty(info.arena_bytes, dtype=torch.uint8, device=dev)
+    w2_ms, w2_bytes = 0.0, 0
+    for l in range(w.n_layers):
+        if w.plan[l][0]:
+            continue
+        c, r = synth.mla_layer(w, l, device=dev)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        kvk.compress_layer(table, l, c, r, n_tok, None, arena)
+        e1.record()
+        torch.cuda.synchronize()
+        w2_ms += e0.elapsed_time(e1)
+        rank = w.plan[l][2]
+        w2_bytes += w.batch * n_tok * (rank + w.rope_dim) * c.element_size() + info.layer_bytes[l]
+        del c, r
+    torch.cuda.empty_cache()
+    log(f"prefill write: {w2_ms:.1f} ms over {info.n_anchors} anchors")
+
+    qs = [synth.mla_queries(w, w.n_layers, device=dev) for _ in range(1)]
+    qs.append(qs[0].flip(1).contiguous())  # a second query set: sequences reversed
+    wk, wv = synth.mla_weights(w, w.n_layers, device=dev)
+    out = torch.empty((w.n_layers, w.batch, w.n_q_heads, w.v_dim), dtype=torch.float32, device=dev)
+    ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=dev)
+    scale = w.softmax_scale()
+    alg = kvk.read_bytes(table, 0, w.n_layers, n_stored)
+    for i in range(args.warmup):
+        kvk.decode_attention(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, out, ws, w_uk=wk, w_uv=wv)
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for i in range(K):
+        ev[i][0].record()
+        kvk.decode_splits(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, ws, w_uk=wk, w_uv=wv)
+        ev[i][1].record()
+        kvk.decode_merge(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, ws, out, w_uk=wk, w_uv=wv)
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / K
+    sp_avg = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    gbs = alg / (ms_step * 1e-3) / 1e9
+    sp_gbs = alg / (sp_avg * 1e-3) / 1e9
+    wbytes = sum(w.n_q_heads * (w.nope_dim + w.v_dim) * w.plan[info.anchor_of[l]][2] * 2
+                 for l in range(w.n_layers))
+    log(f"step {ms_step * 1e3:.1f} us, {gbs:.1f} GB/s ({100 * gbs / HBM_PEAK_GBS:.1f}% of HBM); "
+        f"A1+D2 {sp_avg * 1e3:.1f} us ({sp_gbs:.1f} GB/s)")
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline_mla(w, table, n_stored, scale, min(args.cpu_layers or 32, w.n_layers))
+        log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
+    ranks = {}
+    for e in w.plan:
+        if not e[0]:
+            ranks[str(e[2])] = ranks.get(str(e[2]), 0) + 1
+    line = {
+        "metric": METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "us_per_step": round(ms_step * 1e3, 2),
+        "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": ("bf16" if w.plan[0][1] == 16 else f"u{w.plan[0][1]}") + " latent cache; f16/bf16 MFMA, f32 accumulate",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name, "layers": w.n_layers, "q_heads": w.n_q_heads, "latent_dim": w.latent_dim,
+            "rope_dim": w.rope_dim, "batch": w.batch, "context": n_tok, "stored_tokens": n_stored,
+            "qscheme": "KIVI32" if w.qscheme == kvk.KIVI32 else "SYMROW", "anchors_by_rank": ranks,
+            "bits": w.plan[0][1], "rho_eq2": round(info.rho, 3), "alg_bytes_per_step": alg,
+            "up_projection_bytes_per_step": wbytes,
+        },
+        "roofline": {
+            "bound": "hbm", "kernel": "mla_absorb_kernel + mla_decode_kernel (A1 + D2)",
+            "achieved": round(sp_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(sp_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "launch_us": round(sp_avg * 1e3, 2), "bytes_per_launch": alg,
+        },
+        "cpu_baseline": cpu,
+        "prefill_write": {"ms": round(w2_ms, 3), "bytes": w2_bytes,
+                          "GB_per_s": round(w2_bytes / (w2_ms * 1e-3) / 1e9, 2)},
+    }
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse()
     if args.calibrate_copy:
@@ -149,6 +302,9 @@ def main():
         print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for {args.gpus}); "
               "the design for sharding is described in DESIGN.md.", file=sys.stderr)
         sys.exit(2)
+    if args.config == 3:
+        run_mla(args)
+        return
     import numpy as np
     import torch
 

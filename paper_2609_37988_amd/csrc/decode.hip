@@ -93,16 +93,8 @@ __device__ __forceinline__ f4 mfmab(bf16x8 a, bf16x8 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ float wave_max_kg(float x) {
-  x = fmaxf(x, __shfl_xor(x, 16));
-  x = fmaxf(x, __shfl_xor(x, 32));
-  return x;
-}
-__device__ __forceinline__ float wave_sum_kg(float x) {
-  x += __shfl_xor(x, 16);
-  x += __shfl_xor(x, 32);
-  return x;
-}
+__device__ __forceinline__ float wave_max_kg(float x) { return rows_max(x); }
+__device__ __forceinline__ float wave_sum_kg(float x) { return rows_sum(x); }
 
 __device__ __forceinline__ bf16x8 to_bf16x8(const float* x) {
   bf16x8 r;

@@ -92,6 +92,48 @@ __device__ __forceinline__ half8 unpack8(uint32_t a, uint32_t b, float off) {
 }
 
 // ---------------------------------------------------------------------------
+// Cross-lane reductions without LDS round trips.
+// ---------------------------------------------------------------------------
+
+// Over the four 16-lane rows (lanes l % 16 + 16 k): v_permlane16_swap exchanges
+// neighbouring rows and v_permlane32_swap the two halves of the wave; with both
+// operands equal, each swap leaves a lane and its partner in the two results.
+__device__ __forceinline__ float rows_max(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float rows_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// DPP lane permutation of x (CTRL: a DPP control word; every source lane valid).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+constexpr int kQuadXor1 = 0xB1;       // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;       // quad_perm [2,3,0,1]
+constexpr int kHalfRowMirror = 0x141; // lane i of each 8-lane half row <- lane 7 - i
+
+// Over 8 consecutive lanes (8-aligned): two quad steps, then the half-row mirror
+// pairs each quad with the other one.
+__device__ __forceinline__ float max8(float x) {
+  x = fmaxf(x, dpp<kQuadXor1>(x));
+  x = fmaxf(x, dpp<kQuadXor2>(x));
+  return fmaxf(x, dpp<kHalfRowMirror>(x));
+}
+__device__ __forceinline__ float sum8(float x) {
+  x += dpp<kQuadXor1>(x);
+  x += dpp<kQuadXor2>(x);
+  return x + dpp<kHalfRowMirror>(x);
+}
+
+// ---------------------------------------------------------------------------
 // Block layout (bytes from the start of a 32-token block).
 // ---------------------------------------------------------------------------
 

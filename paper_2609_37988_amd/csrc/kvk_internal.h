@@ -68,9 +68,10 @@ constexpr int mla_ring_depth(int W, int bits, int kivi) {
 }
 
 // Full blocks per split of the MLA decode kernel for an anchor whose streams hold
-// n_blocks full blocks: about 4 MiB per split, balanced over the stream, rounded
-// up to a multiple of the ring depth (so only a stream's last split prefetches
-// past its end); the split count is monotone in n_blocks.
+// n_blocks full blocks: sized so that splits of every width take about the same
+// time, balanced over the stream, rounded up to a multiple of the ring depth (so
+// only a stream's last split prefetches past its end); the split count is
+// monotone in n_blocks.
 int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_blocks);
 
 // Work units (splits) of one MLA stream holding n_stored tokens: the full blocks

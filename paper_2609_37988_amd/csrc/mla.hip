@@ -265,14 +265,16 @@ struct MlaAbsorbArgs {
 // MFMA A operand (M = channels, K = nope); the queries of 16 sequences are the B
 // operand, split into bf16 hi + lo.
 __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
-  constexpr int PW = 72;  // LDS row pitch (bf16 elements)
+  constexpr int PW = 72;   // LDS row pitch of the W_UK chunk (bf16 elements)
+  constexpr int PQ = 264;  // LDS row pitch of the queries (floats)
   __shared__ uint16_t wt[256 * PW];
+  __shared__ float qs[16 * PQ];
   const int li = blockIdx.x, h = blockIdx.y, c0 = 64 * blockIdx.z;
   const int d = a.d_of[li], W = d + kRope;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
   const int qw = a.nope + kRope;
   _Float16* qa = reinterpret_cast<_Float16*>(a.ws + a.q_off[li]);
-  if (c0 >= d) return;
+  if (c0 >= d) return;  // uniform over the workgroup
   if (blockIdx.z == 0) {
     for (int e = tid; e < a.B * kRope; e += 256) {
       const int b = e / kRope, j = e - b * kRope;
@@ -287,30 +289,29 @@ __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
     if (c0 + pc < d) v = *reinterpret_cast<const u4v*>(wk + (int64_t)i * a.r + c0 + pc);
     *reinterpret_cast<u4v*>(&wt[i * PW + pc]) = v;
   }
-  __syncthreads();
   const int nks = a.nope / 32;
   const int ct = 16 * wv;  // this wave's 16 channels of the chunk
-  if (c0 + ct >= d) return;
+  const bool active = c0 + ct < d;
   for (int b0 = 0; b0 < a.B; b0 += 16) {
+    __syncthreads();  // the previous tile's queries are consumed
+    for (int e = tid; e < 16 * a.nope; e += 256) {  // q_nope of 16 sequences, coalesced
+      const int bi = e / a.nope, i = e - bi * a.nope;
+      qs[bi * PQ + i] = b0 + bi < a.B ? load_in(a.q, a.q_f32, (((int64_t)li * a.B + b0 + bi) * a.Hq + h) * qw + i) : 0.0f;
+    }
+    __syncthreads();
+    if (!active) continue;
     const int bq = b0 + i16;
     f4 acc = {0.f, 0.f, 0.f, 0.f};
     for (int ks = 0; ks < nks; ++ks) {
-      uint16_t ah[8], qh[8], ql[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int i = 32 * ks + 8 * g + j;
-        ah[j] = wt[i * PW + ct + i16];
-        float x = 0.0f;
-        if (bq < a.B) x = load_in(a.q, a.q_f32, (((int64_t)li * a.B + bq) * a.Hq + h) * qw + i);
-        qh[j] = bf16_bits_rne(x);
-        ql[j] = bf16_bits_rne(x - bf16_to_f32(qh[j]));
-      }
       bf16x8 av, bh, bl;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        av[j] = bitcast<__bf16>(ah[j]);
-        bh[j] = bitcast<__bf16>(qh[j]);
-        bl[j] = bitcast<__bf16>(ql[j]);
+        const int i = 32 * ks + 8 * g + j;
+        av[j] = bitcast<__bf16>(wt[i * PW + ct + i16]);
+        const float x = qs[i16 * PQ + i];
+        const uint16_t hb = bf16_bits_rne(x);
+        bh[j] = bitcast<__bf16>(hb);
+        bl[j] = bitcast<__bf16>(bf16_bits_rne(x - bf16_to_f32(hb)));
       }
       acc = mfmab(av, bh, acc);
       acc = mfmab(av, bl, acc);
@@ -424,8 +425,10 @@ __device__ __forceinline__ void mla_store(const MlaRaw<D, BITS>& r, _Float16* ti
   constexpr int NCH = MlaRaw<D, BITS>::NCH, NC = MlaRaw<D, BITS>::NC;
 #pragma unroll
   for (int j = 0; j < NC; ++j) {
-    const int c = tid + 256 * j;
-    if (NCH % 256 != 0 && c >= NCH) break;
+    // Threads past the last chunk loaded the last chunk again and store it again
+    // (the same bytes to the same place): no branch, so the outstanding loads of
+    // the other ring entries stay counted exactly.
+    const int c = min(tid + 256 * j, NCH - 1);
     if constexpr (BITS == 16) {
       put_bf16_chunk(tile, PH, W, c, r.w[j], false);
     } else {
@@ -508,10 +511,11 @@ __device__ __forceinline__ void mla_block(MlaState<D>& st, const half8* qreg, Ml
   {
     const int tt = wv >> 1, ht = wv & 1;
     const _Float16* trow = L.tile + (16 * tt + i16) * PH + 8 * g;
-    f4 acc = {0.f, 0.f, 0.f, 0.f};
+    f4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};  // two chains in flight
 #pragma unroll
-    for (int ks = 0; ks < NK; ++ks) acc = mfma16(*reinterpret_cast<const half8*>(trow + 32 * ks), qreg[ks], acc);
-    *reinterpret_cast<f4*>(&L.s[(16 * ht + i16) * kSP + 16 * tt + 4 * g]) = acc;
+    for (int ks = 0; ks < NK; ++ks)
+      acc[ks & 1] = mfma16(*reinterpret_cast<const half8*>(trow + 32 * ks), qreg[ks], acc[ks & 1]);
+    *reinterpret_cast<f4*>(&L.s[(16 * ht + i16) * kSP + 16 * tt + 4 * g]) = acc[0] + acc[1];
   }
   __syncthreads();
   {
@@ -520,10 +524,7 @@ __device__ __forceinline__ void mla_block(MlaState<D>& st, const half8* qreg, Ml
     float x[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) x[e] = 4 * part + e < nvalid ? sv[e] : -INFINITY;
-    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-    mx = fmaxf(mx, __shfl_xor(mx, 1));
-    mx = fmaxf(mx, __shfl_xor(mx, 2));
-    mx = fmaxf(mx, __shfl_xor(mx, 4));
+    const float mx = max8(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));  // the head's 8 threads
     const float mnew = fmaxf(st.m, mx);  // finite: the block holds a stored token
     const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
     float ps = 0.0f;
@@ -533,10 +534,7 @@ __device__ __forceinline__ void mla_block(MlaState<D>& st, const half8* qreg, Ml
       ps += (float)p;
       L.p[h * kPP + 8 * e + part] = p;  // token 4 part + e at k-slot 8 (t % 4) + t / 4
     }
-    ps += __shfl_xor(ps, 1);
-    ps += __shfl_xor(ps, 2);
-    ps += __shfl_xor(ps, 4);
-    st.l = st.l * alpha + ps;
+    st.l = st.l * alpha + sum8(ps);
     st.m = mnew;
     if (part == 0) L.alpha[h] = alpha;
   }
@@ -587,6 +585,11 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
                            ((int64_t)b * a.Hq + head) * W + 8 * g;
 #pragma unroll
     for (int ks = 0; ks < NK; ++ks) qreg[ks] = *reinterpret_cast<const half8*>(qrow + 32 * ks);
+    // Consume the query here: its first use is then outside the block loop, so the
+    // loop waits only for the ring entry it stores (a first use inside the loop
+    // would make every iteration wait for every load in flight).
+#pragma unroll
+    for (int ks = 0; ks < NK; ++ks) asm volatile("" ::"v"(qreg[ks]));
   }
   MlaState<D> st;
   st.m = -INFINITY;
@@ -599,7 +602,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
     for (int i = 0; i < NR; ++i) {
       const bool valid = k + i < k1;  // uniform
       __syncthreads();                // the tile is free
-      if (valid) mla_store<D, BITS, KIVI>(ring[i], L.tile, tid);
+      mla_store<D, BITS, KIVI>(ring[i], L.tile, tid);  // zeros past the unit's blocks
       mla_issue<D, BITS, KIVI>(ring[i], rs, (k + i + NR) * bb, tid);
       __syncthreads();                // the tile is written
       if (valid) mla_block<D>(st, qreg, L, 32, tid);
@@ -731,6 +734,7 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
       float x = 0.0f;
       if (bi < nb && linv[bi] > 0.0f) {
         const float* p0 = part + (int64_t)(b0 + bi) * UC * rec;
+#pragma unroll 4
         for (int u = 0; u < U; ++u) {
           const float w = __builtin_amdgcn_exp2f(p0[u * rec + h] - mstar[bi]);
           x += w * p0[u * rec + 2 * a.Hq + (int64_t)h * d + c];
@@ -743,14 +747,22 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
     }
     __syncthreads();
     for (int jt = wv; jt < a.v / 16; jt += 4) {
-      f4 acc = {0.f, 0.f, 0.f, 0.f};
+      // A operands of the whole row tile first (independent loads), then the products
       const uint16_t* wrow = wv_h + (int64_t)(16 * jt + i16) * a.r + 8 * g;
-      for (int ks = 0; ks < d / 32; ++ks) {
-        const bf16x8 av = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(wrow + 32 * ks));
-        const bf16x8 bh = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&oh[i16 * PO + 32 * ks + 8 * g]));
-        const bf16x8 bl = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&ol[i16 * PO + 32 * ks + 8 * g]));
-        acc = mfmab(av, bh, acc);
-        acc = mfmab(av, bl, acc);
+      const int nks = d / 32;
+      u4v wa[16];
+#pragma unroll
+      for (int ks = 0; ks < 16; ++ks)
+        if (ks < nks) wa[ks] = *reinterpret_cast<const u4v*>(wrow + 32 * ks);
+      f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 16; ++ks) {
+        if (ks < nks) {
+          const bf16x8 bh = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&oh[i16 * PO + 32 * ks + 8 * g]));
+          const bf16x8 bl = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&ol[i16 * PO + 32 * ks + 8 * g]));
+          acc = mfmab(bitcast<bf16x8>(wa[ks]), bh, acc);
+          acc = mfmab(bitcast<bf16x8>(wa[ks]), bl, acc);
+        }
       }
       if (i16 < nb)  // D[value channel 16 jt + 4g + e][sequence b0 + i16]
         *reinterpret_cast<f4*>(a.out + (((int64_t)li * a.B + b0 + i16) * a.Hq + h) * a.v + 16 * jt + 4 * g) = acc;

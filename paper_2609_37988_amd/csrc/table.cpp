@@ -73,16 +73,18 @@ int64_t mla_block_bytes(int32_t W, int32_t bits, int32_t qscheme) {
 }
 
 int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_blocks) {
-  // About 4 MiB of cache per workgroup: the split partial of the heads is
-  // Hq * (d + 2) * 4 bytes (66 KiB at Hq = 32, d = 512), so long splits keep its
-  // write and read a few percent of the cache bytes.
-#ifndef KVK_MLA_SPLIT_TARGET
-#define KVK_MLA_SPLIT_TARGET (4 * 1024 * 1024)
+  // A workgroup's time per block grows with the stored width W (scores over W
+  // channels, the latent product over d) on top of a fixed part (softmax,
+  // barriers): about W + 192 units.  Splits hold about 73728 units (96 blocks at
+  // W = 576, 230 at W = 128), so that the workgroups of all widths take about the
+  // same time and a step launches enough of them to balance the GPU; the split
+  // partial (Hq * (d + 2) * 4 bytes) stays a few percent of a bf16 split.
+#ifndef KVK_MLA_SPLIT_UNITS
+#define KVK_MLA_SPLIT_UNITS 73728
 #endif
-  const int64_t bb = t->block_bytes[anchor];
-  const int64_t nr = mla_ring_depth(t->rank[anchor] + t->d.rope_dim, t->bits[anchor],
-                                    t->d.qscheme == KVK_Q_KIVI32);
-  int64_t target = KVK_MLA_SPLIT_TARGET / bb;
+  const int32_t W = t->rank[anchor] + t->d.rope_dim;
+  const int64_t nr = mla_ring_depth(W, t->bits[anchor], t->d.qscheme == KVK_Q_KIVI32);
+  int64_t target = KVK_MLA_SPLIT_UNITS / (W + 192);
   if (target < nr) target = nr;
   const int64_t nb = n_blocks > 0 ? n_blocks : 1;
   const int64_t nsplit = (nb + target - 1) / target;

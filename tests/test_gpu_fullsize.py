@@ -97,3 +97,58 @@ def test_qwen14b_shaped_128k_eviction():
     w = synth.workload(4)
     say(f"case {w.name}")
     _run_workload(w, 4, 14)
+
+
+@pytest.mark.parametrize("variant", [None, "int4"], ids=["bf16", "int4"])
+def test_mla_shaped_stack(variant):
+    """The MLA-style stack at full size: 32 layers, 32 heads, latent 512 + 64 kept to
+    per-layer widths, batch 16, context 16384, one decode call over all layers;
+    sampled (layer, sequence) streams bit-exact and their 32 output heads within
+    tolerance (oracle in the absorbed form, pinned equal to the reconstruction)."""
+    from oracle import mla as OM
+    w = synth.mla_workload(variant)
+    say(f"case {w.name}")
+    n = w.tokens
+    dims = kvk.make_dims(kvk.MLA, w.n_layers, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, w.latent_dim,
+                         w.rope_dim, w.nope_dim, w.v_dim, qscheme=w.qscheme, batch=w.batch, max_tokens=n)
+    table = kvk.layer_table(dims, kvk.make_plan(w.plan))
+    info = kvk.table_query(table)
+    arena = torch.empty(info.arena_bytes, dtype=torch.uint8, device=DEV)
+    for l in range(w.n_layers):
+        c, r = synth.mla_layer(w, l, device=DEV)
+        kvk.compress_layer(table, l, c, r, n, None, arena)
+        del c, r
+    q = synth.mla_queries(w, w.n_layers, device=DEV)
+    wk, wv = synth.mla_weights(w, w.n_layers, device=DEV)
+    out = torch.empty((w.n_layers, w.batch, w.n_q_heads, w.v_dim), dtype=torch.float32, device=DEV)
+    ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=DEV)
+    kvk.decode_attention(table, 0, w.n_layers, q, n, w.softmax_scale(), arena, out, ws, w_uk=wk, w_uv=wv)
+    torch.cuda.synchronize()
+    od = OP.Dims(OP.MLA, w.n_layers, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, latent_dim=w.latent_dim,
+                 rope_dim=w.rope_dim, nope_dim=w.nope_dim, v_dim=w.v_dim, qscheme=w.qscheme, batch=w.batch,
+                 max_tokens=n)
+    rng = np.random.default_rng(13)
+    got_rows, ref_rows = [], []
+    for _ in range(4):
+        l, b = int(rng.integers(w.n_layers)), int(rng.integers(w.batch))
+        _, bits, d = w.plan[l]
+        say(f"  sample layer {l} (d {d}, {bits} bits) b {b}")
+        c, r = synth.mla_layer(w, l, device=DEV)
+        cs, rs = c[b].float().cpu().numpy(), r[b].float().cpu().numpy()
+        del c, r
+        ref_stream = OM.compress_stream(od, bits, d, cs, rs)
+        sb = info.stream_bytes[l]
+        off = info.layer_offset[l] + b * sb
+        assert np.array_equal(arena[off:off + sb].cpu().numpy(), ref_stream), f"stream bytes differ: {(l, b)}"
+        C, R = OM.dequant_stream(od, bits, d, ref_stream, n)
+        qb = q[l, b].float().cpu().numpy().astype(np.float64)
+        ref_rows.append(OM.attention_absorbed(qb[:, :w.nope_dim], qb[:, w.nope_dim:], C, R,
+                                              wk[l].float().cpu().numpy(), wv[l].float().cpu().numpy(),
+                                              w.softmax_scale()))
+        got_rows.append(out[l, b].cpu().numpy())
+    got, ref = np.stack(got_rows), np.stack(ref_rows)
+    err = np.abs(got - ref).max() / np.abs(ref).max()
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
+    del arena, ws, out
+    torch.cuda.empty_cache()
