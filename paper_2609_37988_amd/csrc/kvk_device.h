@@ -133,6 +133,19 @@ __device__ __forceinline__ float sum8(float x) {
   return x + dpp<kHalfRowMirror>(x);
 }
 
+constexpr int kRowMirror = 0x140;  // lane i of each 16-lane row <- lane 15 - i
+
+// Over 16 consecutive lanes (16-aligned): the 8-lane reduction, then the row mirror
+// pairs each half row with the other one.
+__device__ __forceinline__ float max16(float x) {
+  x = max8(x);
+  return fmaxf(x, dpp<kRowMirror>(x));
+}
+__device__ __forceinline__ float sum16(float x) {
+  x = sum8(x);
+  return x + dpp<kRowMirror>(x);
+}
+
 // ---------------------------------------------------------------------------
 // Block layout (bytes from the start of a 32-token block).
 // ---------------------------------------------------------------------------

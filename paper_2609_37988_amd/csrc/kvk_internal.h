@@ -51,18 +51,23 @@ inline int32_t n_splits(int32_t n_blocks, int32_t split_blocks) {
 // Bytes of one 32-token block of an MLA stream storing W = d + d_R channels.
 int64_t mla_block_bytes(int32_t W, int32_t bits, int32_t qscheme);
 
-// Blocks the MLA decode kernel keeps in flight per workgroup (registers) for a
-// stream of W stored channels per token at `bits`: about 40 KiB of cache, at most
-// 64 registers per thread (40 at the widest rows, whose query and accumulators
-// take the most).  Shared by the host (split sizes) and the kernel.
+// MLA decode workgroup geometry for W = d + d_R stored channels: the channel
+// parts a 16-token tile is split into (2 for the widest rows), and the 32-token
+// blocks one iteration of the four waves covers (16 tokens per tile part).
+constexpr int mla_ksplit(int W) { return W > 320 ? 2 : 1; }
+constexpr int mla_iter_blocks(int W) { return 2 / mla_ksplit(W); }
+
+// Iterations the MLA decode kernel keeps in flight per workgroup (registers) for
+// a stream of W stored channels at `bits`: about 32 KiB of cache, at most 64
+// registers per thread (40 from d = 256 on, whose query and accumulators take
+// the most).  Shared by the host (split sizes) and the kernel.
 constexpr int mla_ring_depth(int W, int bits, int kivi) {
-  const int nch = bits == 16 ? 4 * W : W * bits / 4;  // 16-byte chunks per block
-  const int nc = (nch + 255) / 256;                     // per thread
-  const int regs = nc * (bits == 16 ? 4 : 6);
-  const long bb = bits == 16 ? 64L * W : (kivi ? 4L * W * (bits + 1) : 4L * W * bits + 128);
-  const int cap = W > 320 ? 40 : 64;
+  const int nkw = W / 32 / mla_ksplit(W);                        // k-steps per wave
+  const int regs = bits == 16 ? 4 * nkw : (bits == 8 ? 2 * nkw : nkw) + (bits == 16 ? 0 : (kivi ? nkw : 1));
+  const long wg_bytes = 4L * 16 * (W / mla_ksplit(W)) * bits / 8;  // codes of one iteration
+  const int cap = W > 192 ? 40 : 64;
   const int by_regs = regs > cap ? 1 : cap / regs;
-  const int by_bytes = (int)((40960 + bb - 1) / bb);
+  const int by_bytes = (int)((32768 + wg_bytes - 1) / wg_bytes);
   const int nr = by_regs < by_bytes ? by_regs : by_bytes;
   return nr < 1 ? 1 : nr;
 }

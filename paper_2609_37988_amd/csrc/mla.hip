@@ -358,204 +358,239 @@ struct MlaDecodeArgs {
   int32_t nb_cap;
 };
 
-constexpr int kSP = 36;  // score buffer row pitch (floats)
-constexpr int kPP = 40;  // probability buffer row pitch (halfs)
+constexpr int kWaves = 4;  // waves per D2 workgroup (two workgroups share a CU)
 
-struct MlaLds {
-  _Float16 tile[32 * (kMaxW + 16)];
-  float s[32 * kSP];
-  _Float16 p[32 * kPP];
-  float alpha[32];
-};
-
-// Raw bytes of one block held by one thread: 16-byte chunks (+ two metadata words
-// per chunk for quantised blocks).
-template <int D, int BITS>
-struct MlaRaw {
+// Geometry of the D2 workgroup for a kept width D (W = D + 64 stored channels).
+// Wave w takes the 16 tokens of tile w / KS of the iteration and the channel part
+// w % KS of them (KS = 2 for the widest rows, whose query for both head tiles would
+// not fit the registers otherwise).
+template <int D>
+struct Geo {
   static constexpr int W = D + kRope;
-  static constexpr int NCH = BITS == 16 ? 4 * W : W * BITS / 4;  // chunks per block
-  static constexpr int NC = (NCH + 255) / 256;                  // per thread
-  u4v w[NC];
-  uint32_t m[BITS == 16 ? 1 : NC][2];
+  static constexpr int NK = W / 32;                 // k-steps over the stored channels
+  static constexpr int KS = kvk::mla_ksplit(W);     // channel parts per token tile
+  static constexpr int NKW = NK / KS;               // k-steps per wave
+  static constexpr int TT = 16 * kWaves / KS;       // tokens per iteration
+  static constexpr int NBI = TT / 32;               // blocks per iteration
+  static constexpr int PH = W + 16;                 // tile row pitch (halfs): W/2 + 8 dwords
+  static constexpr int NCT = D / 16;                // latent channel tiles of the product
+  static constexpr int NCTW = (NCT + kWaves - 1) / kWaves;  // per wave
+  static_assert(NK % KS == 0, "channel parts must split the k-steps evenly");
 };
 
-// Byte offsets (inside a block) of a thread's chunk j and of the metadata words
-// of its two word pairs; recomputed per block rather than held in registers.
-template <int D, int BITS, bool KIVI>
-__device__ __forceinline__ int chunk_off(int tid, int j) {
-  constexpr int NCH = MlaRaw<D, BITS>::NCH;
-  return 16 * min(tid + 256 * j, NCH - 1);
-}
-template <int D, int BITS, bool KIVI>
-__device__ __forceinline__ int meta_off(int tid, int j, int p) {
-  constexpr int W = D + kRope, NCH = MlaRaw<D, BITS>::NCH;
-  constexpr int per = 32 / BITS, wpt = W / per, cb = 4 * W * BITS;
-  const int c = min(tid + 256 * j, NCH - 1);
-  const int fw = 4 * c + 2 * p, t = fw / wpt, wi = fw - t * wpt;
-  return KIVI ? cb + 4 * (t * (W / 32) + (per * wi) / 32) : cb + 4 * t;
+constexpr int kMaxTT = 16 * kWaves;                   // tokens per iteration at KS = 1
+constexpr int kTileHalfs = kMaxTT * (256 + kRope + 16);  // the largest TT * PH over the widths
+constexpr int kSP = 20;                               // score rows: 16 tokens + pad (floats)
+constexpr int kPP = kMaxTT + 8;                       // probability rows: TT + pad (halfs)
+
+// Vector-typed so that 16-byte accesses compile to single b128 LDS instructions.
+struct MlaLds {
+  half8 tile[kTileHalfs / 8];   // fp16 latent rows of the iteration (swizzled)
+  f4 s[kWaves * 32 * kSP / 4];  // per wave: scores (partial over its channels) [head][token]
+  half8 p[32 * kPP / 8];        // probabilities [head][k-slot]
+  float alpha[32];
+  __device__ __forceinline__ _Float16* tile_h() { return reinterpret_cast<_Float16*>(tile); }
+  __device__ __forceinline__ _Float16* p_h() { return reinterpret_cast<_Float16*>(p); }
+};
+
+// Element (t, c) of the tile: rows of PH halfs; within a row the 16-byte chunks of
+// rows 4..7 of every 8 swap in pairs, so that the eight rows one score read or
+// tile write touches fall in different banks, while the four rows the product's
+// transposed reads touch together (4j .. 4j+3) keep one arrangement.
+template <int PH>
+__device__ __forceinline__ int tile_at(int t, int c) {
+  return t * PH + ((((c >> 3) ^ ((t >> 2) & 1))) << 3) + (c & 7);
 }
 
+// Raw bytes of one wave's share of an iteration (16 tokens x its channel part).
 template <int D, int BITS, bool KIVI>
-__device__ __forceinline__ void mla_issue(MlaRaw<D, BITS>& r, Rsrc rs, int blk, int tid) {
+struct MlaRaw {
+  static constexpr int NKW = Geo<D>::NKW;
+  // per k-step: bf16 8 channels (4 words); int8 2 words; int4 1 word; int2 1 word (half used)
+  static constexpr int CW = BITS == 16 ? 4 : (BITS == 8 ? 2 : 1);
+  static constexpr int MW = BITS == 16 ? 0 : (KIVI ? NKW : 1);  // metadata words
+  uint32_t c[NKW][CW];
+  uint32_t m[MW > 0 ? MW : 1];
+};
+
+// Lane (t = lane % 16, g = lane / 16) of wave part kh holds, at its k-step ks, the
+// 8 channels 32 (kh NKW + ks) + 8 g .. + 7 of token t: the MFMA A-operand layout.
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void mla_issue(MlaRaw<D, BITS, KIVI>& r, Rsrc rs, int soff, int t, int g, int kh) {
+  constexpr int W = D + kRope, NKW = Geo<D>::NKW;
+  const int j0 = kh * NKW;
+  if constexpr (BITS == 16) {
+    const int v = t * 2 * W + 16 * g + 64 * j0;
 #pragma unroll
-  for (int j = 0; j < MlaRaw<D, BITS>::NC; ++j) {
-    r.w[j] = __builtin_amdgcn_raw_buffer_load_b128(rs, chunk_off<D, BITS, KIVI>(tid, j), blk, 0);
-    if constexpr (BITS != 16) {
-      r.m[j][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, meta_off<D, BITS, KIVI>(tid, j, 0), blk, 0);
-      r.m[j][1] = __builtin_amdgcn_raw_buffer_load_b32(rs, meta_off<D, BITS, KIVI>(tid, j, 1), blk, 0);
+    for (int ks = 0; ks < NKW; ++ks) {
+      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, v + 64 * ks, soff, 0);
+      r.c[ks][0] = x[0]; r.c[ks][1] = x[1]; r.c[ks][2] = x[2]; r.c[ks][3] = x[3];
     }
-  }
-}
-
-// bf16 chunk -> 8 fp16 values of one token row.
-__device__ __forceinline__ void put_bf16_chunk(_Float16* tile, int ph, int W, int c, u4v v, bool zero) {
-  const int t = c / (W / 8), c0 = 8 * (c - t * (W / 8));
-  u4v o = {0u, 0u, 0u, 0u};
-  if (!zero) {
+  } else {
+    constexpr int rowb = W * BITS / 8, cb = 4 * W * BITS;
+    if constexpr (BITS == 8) {
+      const int v = t * rowb + 8 * g + 32 * j0;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) o[e] = bitcast<uint32_t>(bf16x2_to_half2(v[e]));
-  }
-  *reinterpret_cast<u4v*>(tile + t * ph + c0) = o;
-}
-
-// Write the block held in `r` into the LDS tile as fp16 rows.
-template <int D, int BITS, bool KIVI>
-__device__ __forceinline__ void mla_store(const MlaRaw<D, BITS>& r, _Float16* tile, int tid) {
-  constexpr int W = D + kRope, PH = W + 16;
-  constexpr int NCH = MlaRaw<D, BITS>::NCH, NC = MlaRaw<D, BITS>::NC;
-#pragma unroll
-  for (int j = 0; j < NC; ++j) {
-    // Threads past the last chunk loaded the last chunk again and store it again
-    // (the same bytes to the same place): no branch, so the outstanding loads of
-    // the other ring entries stay counted exactly.
-    const int c = min(tid + 256 * j, NCH - 1);
-    if constexpr (BITS == 16) {
-      put_bf16_chunk(tile, PH, W, c, r.w[j], false);
-    } else {
-      constexpr int per = 32 / BITS, wpt = W / per;
-      constexpr float off = KIVI ? 0.0f : (float)(1 << (BITS - 1));
-#pragma unroll
-      for (int k = 0; k < 4; k += (BITS == 8 ? 2 : 1)) {
-        const int fw = 4 * c + k, t = fw / wpt, wi = fw - t * wpt, c0 = per * wi;
-        const uint32_t mm = r.m[j][k >> 1];
-        half2v s2, z2;
-        if constexpr (KIVI) {
-          s2 = h2s((float)bitcast<_Float16>((uint16_t)(mm & 0xFFFFu)));
-          z2 = h2s((float)bitcast<_Float16>((uint16_t)(mm >> 16)));
-        } else {
-          const uint32_t sb = c0 < D ? (mm & 0xFFFFu) : (mm >> 16);
-          s2 = h2s(__uint_as_float(sb << 16));
-          z2 = h2s(0.0f);
-        }
-        _Float16* dst = tile + t * PH + c0;
-        if constexpr (BITS == 4) {
-          const half8 u = unpack4(r.w[j][k], off);
-          half8 x;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            half2v pr = {u[2 * e], u[2 * e + 1]};
-            pr = __builtin_elementwise_fma(pr, s2, z2);
-            x[2 * e] = pr[0];
-            x[2 * e + 1] = pr[1];
-          }
-          *reinterpret_cast<half8*>(dst) = x;
-        } else if constexpr (BITS == 8) {
-          const half8 u = unpack8(r.w[j][k], r.w[j][k + 1], off);
-          half8 x;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            half2v pr = {u[2 * e], u[2 * e + 1]};
-            pr = __builtin_elementwise_fma(pr, s2, z2);
-            x[2 * e] = pr[0];
-            x[2 * e + 1] = pr[1];
-          }
-          *reinterpret_cast<half8*>(dst) = x;
-        } else {
-          half8 ue, uo;
-          unpack2(r.w[j][k], off, ue, uo);
-          half8 xe, xo;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            half2v pe = {ue[2 * e], ue[2 * e + 1]};
-            half2v po = {uo[2 * e], uo[2 * e + 1]};
-            pe = __builtin_elementwise_fma(pe, s2, z2);
-            po = __builtin_elementwise_fma(po, s2, z2);
-            xe[2 * e] = pe[0];
-            xe[2 * e + 1] = pe[1];
-            xo[2 * e] = po[0];
-            xo[2 * e + 1] = po[1];
-          }
-          *reinterpret_cast<half8*>(dst) = xe;
-          *reinterpret_cast<half8*>(dst + 8) = xo;
-        }
+      for (int ks = 0; ks < NKW; ++ks) {
+        const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, v + 32 * ks, soff, 0);
+        r.c[ks][0] = x[0]; r.c[ks][1] = x[1];
       }
+    } else if constexpr (BITS == 4) {
+      const int v = t * rowb + 4 * g + 16 * j0;
+#pragma unroll
+      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 16 * ks, soff, 0);
+    } else {
+      const int v = t * rowb + 4 * (g >> 1) + 8 * j0;
+#pragma unroll
+      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 8 * ks, soff, 0);
+    }
+    if constexpr (KIVI) {
+      const int v = cb + 4 * (t * (W / 32) + j0);
+#pragma unroll
+      for (int ks = 0; ks < NKW; ++ks) r.m[ks] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 4 * ks, soff, 0);
+    } else {
+      r.m[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, cb + 4 * t, soff, 0);
     }
   }
 }
 
-// Per-workgroup running state of a unit.
+// The 8 fp16 values of k-step ks (see mla_issue).
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ half8 mla_values(const MlaRaw<D, BITS, KIVI>& r, int ks, int g, int kh) {
+  if constexpr (BITS == 16) {
+    u4v o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = bitcast<uint32_t>(bf16x2_to_half2(r.c[ks][e]));
+    return bitcast<half8>(o);
+  } else {
+    constexpr float off = KIVI ? 0.0f : (float)(1 << (BITS - 1));
+    half8 u;
+    if constexpr (BITS == 8) {
+      u = unpack8(r.c[ks][0], r.c[ks][1], off);
+    } else if constexpr (BITS == 4) {
+      u = unpack4(r.c[ks][0], off);
+    } else {
+      u = unpack2_half(r.c[ks][0] >> (8 * (g & 1)), off);
+    }
+    half2v s2, z2;
+    if constexpr (KIVI) {
+      const uint32_t mm = r.m[ks];
+      s2 = bitcast<half2v>(__builtin_amdgcn_perm(mm, mm, 0x01000100u));  // (scale, scale)
+      z2 = bitcast<half2v>(__builtin_amdgcn_perm(mm, mm, 0x03020302u));  // (zero, zero)
+    } else {
+      constexpr int W = D + kRope;
+      const int c0 = 32 * (kh * Geo<D>::NKW + ks);  // first channel of the k-step (wave-uniform)
+      const uint32_t sb = c0 < D ? (r.m[0] << 16) : (r.m[0] & 0xFFFF0000u);
+      s2 = h2s(__uint_as_float(sb));
+      z2 = h2s(0.0f);
+      (void)W;
+    }
+    half8 x;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      half2v pr = {u[2 * e], u[2 * e + 1]};
+      pr = __builtin_elementwise_fma(pr, s2, z2);
+      x[2 * e] = pr[0];
+      x[2 * e + 1] = pr[1];
+    }
+    return x;
+  }
+}
+
+// Running state of a unit: the product accumulators of the wave's channel tiles
+// and, in the softmax threads (16 per head), the head's running max and sum.
 template <int D>
 struct MlaState {
-  static constexpr int NCT = D / 16;            // latent channel tiles
-  static constexpr int NCTW = (NCT + 3) / 4;    // per wave
-  f4 o[NCTW][2];                                // O^T tiles (channel tile, head tile)
-  float m, l;                                   // softmax threads: running max (log2), sum
+  f4 o[Geo<D>::NCTW][2];
+  float m, l;
 };
 
-// One block already in the LDS tile: scores, online softmax, probabilities x latent.
-template <int D>
-__device__ __forceinline__ void mla_block(MlaState<D>& st, const half8* qreg, MlaLds& L, int nvalid,
-                                          int tid) {
-  constexpr int W = D + kRope, PH = W + 16, NK = W / 32;
-  const int lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
-  {
-    const int tt = wv >> 1, ht = wv & 1;
-    const _Float16* trow = L.tile + (16 * tt + i16) * PH + 8 * g;
-    f4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};  // two chains in flight
+// Phase A of an iteration for one wave: values of its 16 tokens x channel part into
+// the tile, and its partial scores S^T[token, head] over those channels.
+template <int D, int BITS, bool KIVI>
+__device__ __forceinline__ void mla_phase_a(const MlaRaw<D, BITS, KIVI>& r, const half8 (&qreg)[Geo<D>::NKW][2],
+                                            MlaLds& L, int wv, int tt, int kh, int lane) {
+  using G = Geo<D>;
+  const int g = lane >> 4, i16 = lane & 15;
+  const int row = 16 * tt + i16;
+  f4 acc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-    for (int ks = 0; ks < NK; ++ks)
-      acc[ks & 1] = mfma16(*reinterpret_cast<const half8*>(trow + 32 * ks), qreg[ks], acc[ks & 1]);
-    *reinterpret_cast<f4*>(&L.s[(16 * ht + i16) * kSP + 16 * tt + 4 * g]) = acc[0] + acc[1];
+  for (int ks = 0; ks < G::NKW; ++ks) {
+    const half8 x = mla_values<D, BITS, KIVI>(r, ks, g, kh);
+    const int c0 = 32 * (kh * G::NKW + ks) + 8 * g;
+    L.tile[tile_at<G::PH>(row, c0) >> 3] = x;
+    acc[0] = mfma16(x, qreg[ks][0], acc[0]);
+    acc[1] = mfma16(x, qreg[ks][1], acc[1]);
   }
-  __syncthreads();
-  {
-    const int h = tid >> 3, part = tid & 7;
-    const f4 sv = *reinterpret_cast<const f4*>(&L.s[h * kSP + 4 * part]);
-    float x[4];
 #pragma unroll
-    for (int e = 0; e < 4; ++e) x[e] = 4 * part + e < nvalid ? sv[e] : -INFINITY;
-    const float mx = max8(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));  // the head's 8 threads
-    const float mnew = fmaxf(st.m, mx);  // finite: the block holds a stored token
+  for (int ht = 0; ht < 2; ++ht)
+    L.s[((wv * 32 + 16 * ht + i16) * kSP + 4 * g) >> 2] = acc[ht];
+}
+
+// Phases B (online softmax over the iteration's tokens; the first nvalid count)
+// and C (probabilities x latent), after phase A and a barrier.
+template <int D>
+__device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, MlaLds& L, int nvalid, int tid) {
+  using G = Geo<D>;
+  constexpr int TPB = 2 * kWaves;      // softmax threads per head
+  constexpr int TPT = G::TT / TPB;     // tokens per softmax thread
+  static_assert(TPT % 4 == 0, "softmax threads read whole f4 score groups");
+  const int lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6), g = lane >> 4, i16 = lane & 15;
+  {
+    const int h = tid / TPB, p = tid % TPB;
+    float x[TPT];
+#pragma unroll
+    for (int q4 = 0; q4 < TPT / 4; ++q4) {
+      const int tok = TPT * p + 4 * q4;  // 4 tokens of one 16-token tile
+      const int tt = tok >> 4, r = tok & 15;
+      f4 s = L.s[(((tt * G::KS) * 32 + h) * kSP + r) >> 2];
+      if constexpr (G::KS == 2) s += L.s[(((tt * 2 + 1) * 32 + h) * kSP + r) >> 2];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[4 * q4 + e] = tok + e < nvalid ? s[e] : -INFINITY;
+    }
+    float mx = x[0];
+#pragma unroll
+    for (int e = 1; e < TPT; ++e) mx = fmaxf(mx, x[e]);
+    mx = TPB == 8 ? max8(mx) : max16(mx);
+    const float mnew = fmaxf(st.m, mx);  // finite: the iteration holds a stored token
     const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
     float ps = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const _Float16 p = (_Float16)__builtin_amdgcn_exp2f(x[e] - mnew);
-      ps += (float)p;
-      L.p[h * kPP + 8 * e + part] = p;  // token 4 part + e at k-slot 8 (t % 4) + t / 4
+    for (int e = 0; e < TPT; ++e) {
+      const int tok = TPT * p + e;
+      const _Float16 pv = (_Float16)__builtin_amdgcn_exp2f(x[e] - mnew);
+      ps += (float)pv;
+      // k-step tok / 32, slot 8 (tok % 4) + (tok % 32) / 4
+      L.p_h()[h * kPP + (tok & ~31) + 8 * (tok & 3) + ((tok & 31) >> 2)] = pv;
     }
-    st.l = st.l * alpha + sum8(ps);
+    st.l = st.l * alpha + (TPB == 8 ? sum8(ps) : sum16(ps));
     st.m = mnew;
-    if (part == 0) L.alpha[h] = alpha;
+    if (p == 0) L.alpha[h] = alpha;
   }
   __syncthreads();
   {
-    half8 pb[2];
     float al[2];
+    half8 pb[G::TT / 32][2];  // the probabilities, read once for all channel tiles
 #pragma unroll
     for (int ht = 0; ht < 2; ++ht) {
-      pb[ht] = *reinterpret_cast<const half8*>(&L.p[(16 * ht + i16) * kPP + 8 * g]);
       al[ht] = L.alpha[16 * ht + i16];
+#pragma unroll
+      for (int kk = 0; kk < G::TT / 32; ++kk) pb[kk][ht] = L.p[((16 * ht + i16) * kPP + 32 * kk + 8 * g) >> 3];
     }
 #pragma unroll
-    for (int i = 0; i < MlaState<D>::NCTW; ++i) {
-      const int ct = wv + 4 * i;
-      if (ct < MlaState<D>::NCT) {
-        half8 av;
+    for (int i = 0; i < G::NCTW; ++i) {
+      const int ct = wv + kWaves * i;
+      if (ct < G::NCT) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) av[j] = L.tile[(4 * j + g) * PH + 16 * ct + i16];
+        for (int ht = 0; ht < 2; ++ht) st.o[i][ht] *= al[ht];
 #pragma unroll
-        for (int ht = 0; ht < 2; ++ht) st.o[i][ht] = mfma16(av, pb[ht], st.o[i][ht] * al[ht]);
+        for (int kk = 0; kk < G::TT / 32; ++kk) {
+          half8 av;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) av[j] = L.tile_h()[tile_at<G::PH>(32 * kk + 4 * j + g, 16 * ct + i16)];
+#pragma unroll
+          for (int ht = 0; ht < 2; ++ht) st.o[i][ht] = mfma16(av, pb[kk][ht], st.o[i][ht]);
+        }
       }
     }
   }
@@ -564,82 +599,82 @@ __device__ __forceinline__ void mla_block(MlaState<D>& st, const half8* qreg, Ml
 template <int D, int BITS, bool KIVI>
 __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& it, int rl, int hc,
                                         int b, int u, MlaLds& L) {
-  constexpr int W = D + kRope, PH = W + 16, NK = W / 32;
-  constexpr int NR = kvk::mla_ring_depth(W, BITS, KIVI ? 1 : 0);
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
+  using G = Geo<D>;
+  constexpr int NR = kvk::mla_ring_depth(G::W, BITS, KIVI ? 1 : 0);
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, i16 = lane & 15;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int tt = wv / G::KS, kh = wv % G::KS;
   const int k0 = u * it.split_blocks;
   const int k1 = min(a.nbf, k0 + it.split_blocks);
   const int bb = it.block_bytes;
   const uint8_t* stream = a.arena + it.region + (int64_t)b * it.stream_bytes;
   const Rsrc rs = buffer_rsrc(stream, k1 > 0 ? k1 * bb : 0);  // loads past block k1-1 read zeros
+  const int trow = 16 * (tt & 1) + i16;                         // token row inside its block
+  const int tblk = tt >> 1;                                     // block of the tile in the iteration
 
-  MlaRaw<D, BITS> ring[NR];
+  MlaRaw<D, BITS, KIVI> ring[NR];
 #pragma unroll
-  for (int i = 0; i < NR; ++i) mla_issue<D, BITS, KIVI>(ring[i], rs, (k0 + i) * bb, tid);
+  for (int i = 0; i < NR; ++i) mla_issue<D, BITS, KIVI>(ring[i], rs, (k0 + G::NBI * i + tblk) * bb, trow, g, kh);
 
-  // this wave's 16 heads (S phase): absorbed query rows, fp16
-  half8 qreg[NK];
+  // absorbed query of the 32 heads over this wave's channel part, fp16
+  half8 qreg[G::NKW][2];
   {
-    const int head = 32 * hc + 16 * (wv & 1) + i16;
-    const _Float16* qrow = reinterpret_cast<const _Float16*>(a.ws + it.q_off0 + (int64_t)rl * it.q_stride) +
-                           ((int64_t)b * a.Hq + head) * W + 8 * g;
+    const _Float16* qb = reinterpret_cast<const _Float16*>(a.ws + it.q_off0 + (int64_t)rl * it.q_stride) +
+                         ((int64_t)b * a.Hq + 32 * hc) * G::W + 32 * kh * G::NKW + 8 * g;
 #pragma unroll
-    for (int ks = 0; ks < NK; ++ks) qreg[ks] = *reinterpret_cast<const half8*>(qrow + 32 * ks);
-    // Consume the query here: its first use is then outside the block loop, so the
-    // loop waits only for the ring entry it stores (a first use inside the loop
-    // would make every iteration wait for every load in flight).
+    for (int ht = 0; ht < 2; ++ht)
 #pragma unroll
-    for (int ks = 0; ks < NK; ++ks) asm volatile("" ::"v"(qreg[ks]));
+      for (int ks = 0; ks < G::NKW; ++ks)
+        qreg[ks][ht] = *reinterpret_cast<const half8*>(qb + (int64_t)(16 * ht + i16) * G::W + 32 * ks);
+    // Consume the query here: its first use is then outside the loop, so the loop
+    // waits only for the ring entry it uses (a first use inside the loop would make
+    // every iteration wait for every load in flight).
+#pragma unroll
+    for (int ht = 0; ht < 2; ++ht)
+#pragma unroll
+      for (int ks = 0; ks < G::NKW; ++ks) asm volatile("" ::"v"(qreg[ks][ht]));
   }
   MlaState<D> st;
   st.m = -INFINITY;
   st.l = 0.0f;
 #pragma unroll
-  for (int i = 0; i < MlaState<D>::NCTW; ++i) st.o[i][0] = st.o[i][1] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int i = 0; i < G::NCTW; ++i) st.o[i][0] = st.o[i][1] = f4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k = k0; k < k1; k += NR) {
+  for (int k = k0; k < k1; k += G::NBI * NR) {
 #pragma unroll
     for (int i = 0; i < NR; ++i) {
-      const bool valid = k + i < k1;  // uniform
-      __syncthreads();                // the tile is free
-      mla_store<D, BITS, KIVI>(ring[i], L.tile, tid);  // zeros past the unit's blocks
-      mla_issue<D, BITS, KIVI>(ring[i], rs, (k + i + NR) * bb, tid);
-      __syncthreads();                // the tile is written
-      if (valid) mla_block<D>(st, qreg, L, 32, tid);
+      const int kb = k + G::NBI * i;                   // first block of the iteration
+      const int nvalid = max(0, min(G::TT, 32 * (k1 - kb)));  // uniform
+      __syncthreads();                                 // the tile, scores and p are free
+      mla_phase_a<D, BITS, KIVI>(ring[i], qreg, L, wv, tt, kh, lane);
+      mla_issue<D, BITS, KIVI>(ring[i], rs, (kb + G::NBI * NR + tblk) * bb, trow, g, kh);
+      __syncthreads();
+      if (nvalid > 0) mla_phase_bc<D>(st, L, nvalid, tid);
     }
   }
-  if (u == it.units - 1 && a.ntail > 0) {  // bf16 tail block of the stream
-    const uint8_t* tb = stream + (int64_t)a.nb_cap * bb;
-    constexpr int NCH = 4 * W, NC = (NCH + 255) / 256;
-    u4v v[NC];
-#pragma unroll
-    for (int j = 0; j < NC; ++j) {
-      const int c = min(tid + 256 * j, NCH - 1);
-      v[j] = *reinterpret_cast<const u4v*>(tb + 16 * c);
-    }
+  if (u == it.units - 1 && a.ntail > 0) {  // the bf16 tail block as one more iteration
+    MlaRaw<D, 16, false> tr;
+    const Rsrc rt = buffer_rsrc(stream + (int64_t)a.nb_cap * bb, tblk == 0 ? 64 * G::W : 0);
+    mla_issue<D, 16, false>(tr, rt, 0, trow, g, kh);
     __syncthreads();
-#pragma unroll
-    for (int j = 0; j < NC; ++j) {
-      const int c = tid + 256 * j;
-      if (c < NCH) put_bf16_chunk(L.tile, PH, W, c, v[j], c / (W / 8) >= a.ntail);
-    }
+    mla_phase_a<D, 16, false>(tr, qreg, L, wv, tt, kh, lane);
     __syncthreads();
-    mla_block<D>(st, qreg, L, a.ntail, tid);
+    mla_phase_bc<D>(st, L, a.ntail, tid);
   }
 
   // split partial: m[Hq], l[Hq], o[Hq][D] of this (reader, sequence, split)
   float* rec = reinterpret_cast<float*>(a.ws + it.part_off0 + (int64_t)rl * it.part_stride) +
                ((int64_t)b * it.units_cap + u) * a.Hq * (D + 2);
-  if ((tid & 7) == 0) {
-    const int h = 32 * hc + (tid >> 3);
+  if (tid % (2 * kWaves) == 0) {
+    const int h = 32 * hc + tid / (2 * kWaves);
     rec[h] = st.m;
     rec[a.Hq + h] = st.l;
   }
   float* orec = rec + 2 * a.Hq;
 #pragma unroll
-  for (int i = 0; i < MlaState<D>::NCTW; ++i) {
-    const int ct = wv + 4 * i;
-    if (ct < MlaState<D>::NCT) {
+  for (int i = 0; i < G::NCTW; ++i) {
+    const int ct = wv + kWaves * i;
+    if (ct < G::NCT) {
 #pragma unroll
       for (int ht = 0; ht < 2; ++ht) {
         const int h = 32 * hc + 16 * ht + i16;
@@ -650,7 +685,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
 }
 
 template <bool KIVI>
-__global__ __launch_bounds__(256, 2) void mla_decode_kernel(MlaDecodeArgs a) {
+__global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(MlaDecodeArgs a) {
   __shared__ MlaLds L;
   const int wg = blockIdx.x;
   if (wg >= a.n_wg) return;
@@ -871,9 +906,9 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     if (wgs > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "too many MLA decode workgroups");
     a.n_wg = (int32_t)wgs;
     if (d.qscheme == KVK_Q_KIVI32)
-      hipLaunchKernelGGL(mla_decode_kernel<true>, dim3((unsigned)wgs), dim3(256), 0, stream, a);
+      hipLaunchKernelGGL(mla_decode_kernel<true>, dim3((unsigned)wgs), dim3(64 * kWaves), 0, stream, a);
     else
-      hipLaunchKernelGGL(mla_decode_kernel<false>, dim3((unsigned)wgs), dim3(256), 0, stream, a);
+      hipLaunchKernelGGL(mla_decode_kernel<false>, dim3((unsigned)wgs), dim3(64 * kWaves), 0, stream, a);
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA decode launch: %s", hipGetErrorString(err));
     a.n_items = 0;
