@@ -231,6 +231,7 @@ def run_mla(args):
     qs = [synth.mla_queries(w, w.n_layers, device=dev) for _ in range(1)]
     qs.append(qs[0].flip(1).contiguous())  # a second query set: sequences reversed
     wk, wv = synth.mla_weights(w, w.n_layers, device=dev)
+    wk = kvk.mla_weights_for_library(wk)  # arranged once, as at weight load
     out = torch.empty((w.n_layers, w.batch, w.n_q_heads, w.v_dim), dtype=torch.float32, device=dev)
     ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=dev)
     scale = w.softmax_scale()

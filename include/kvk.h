@@ -263,8 +263,11 @@ kvk_status kvk_compress_layer(const kvk_table* table, int32_t layer, const void*
  * MLA (§2.1, App. C.2), with nl = layer_end - layer_begin:
  *   q        : device [nl][B][Hq][nope_dim + d_R], dtype q_dtype: per head the
  *              no-RoPE part q_nope then the RoPE part q_rope.
- *   w_uk     : device bf16 [nl][Hq][nope_dim][r]: layer l's W_UK, the map from the
- *              latent to head h's content key (k = W_UK[h] c).
+ *   w_uk     : device bf16 [nl][Hq][r][nope_dim]: layer l's W_UK, the map from the
+ *              latent to head h's content key (k = W_UK[h] c), stored transposed
+ *              (latent-major: element (i, c) of W_UK[h] at [h][c][i]), the layout the
+ *              query absorption reads contiguously; callers arrange it once when
+ *              they load the weights.
  *   w_uv     : device bf16 [nl][Hq][v_dim][r]: layer l's W_UV (v = W_UV[h] c).
  *   out      : device fp32 [nl][B][Hq][v_dim].
  *   Head h of layer l attends with query [q_nope ; q_rope] to keys

@@ -72,6 +72,9 @@ constexpr int mla_ring_depth(int W, int bits, int kivi) {
   return nr < 1 ? 1 : nr;
 }
 
+// Most splits of one MLA stream (the merge holds one weight per split in LDS).
+constexpr int kMlaMaxUnits = 128;
+
 // Full blocks per split of the MLA decode kernel for an anchor whose streams hold
 // n_blocks full blocks: sized so that splits of every width take about the same
 // time, balanced over the stream, rounded up to a multiple of the ring depth (so

@@ -251,7 +251,7 @@ __global__ __launch_bounds__(256) void mla_dequant_kernel(const uint8_t* region,
 
 struct MlaAbsorbArgs {
   const void* q;          // [nl][B][Hq][nope + 64]
-  const uint16_t* w_uk;   // [nl][Hq][nope][r] bf16
+  const uint16_t* w_ukt;  // [nl][Hq][r][nope] bf16: W_UK[h] transposed (latent-major)
   uint8_t* ws;
   int64_t q_off[KVK_MAX_LAYERS];  // per relative layer: fp16 [B][Hq][d + 64]
   int32_t d_of[KVK_MAX_LAYERS];
@@ -260,66 +260,65 @@ struct MlaAbsorbArgs {
   float scale_log2;
 };
 
-// One workgroup per (layer, head, 64-channel chunk of the latent).  The chunk of
-// W_UK[h] (nope rows x 64 channels) is staged in LDS and read transposed into the
-// MFMA A operand (M = channels, K = nope); the queries of 16 sequences are the B
-// operand, split into bf16 hi + lo.
+// One workgroup per (layer, head).  The queries of 16 sequences are staged once in
+// LDS and split into bf16 hi + lo B operands (K = nope); wave w then runs the
+// 16-channel tiles w, w + 4, ... of the latent: A = rows of W_UK[h]^T (latent
+// channel x nope, contiguous in the latent-major layout).
 __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
-  constexpr int PW = 72;   // LDS row pitch of the W_UK chunk (bf16 elements)
-  constexpr int PQ = 264;  // LDS row pitch of the queries (floats)
-  __shared__ uint16_t wt[256 * PW];
+  constexpr int PQ = 256 + 8;  // LDS row pitch of the queries (floats)
   __shared__ float qs[16 * PQ];
-  const int li = blockIdx.x, h = blockIdx.y, c0 = 64 * blockIdx.z;
+  const int li = blockIdx.x, h = blockIdx.y;
   const int d = a.d_of[li], W = d + kRope;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
   const int qw = a.nope + kRope;
-  _Float16* qa = reinterpret_cast<_Float16*>(a.ws + a.q_off[li]);
-  if (c0 >= d) return;  // uniform over the workgroup
-  if (blockIdx.z == 0) {
-    for (int e = tid; e < a.B * kRope; e += 256) {
-      const int b = e / kRope, j = e - b * kRope;
-      const float x = load_in(a.q, a.q_f32, (((int64_t)li * a.B + b) * a.Hq + h) * qw + a.nope + j);
-      qa[((int64_t)b * a.Hq + h) * W + d + j] = (_Float16)(x * a.scale_log2);
-    }
-  }
-  const uint16_t* wk = a.w_uk + ((int64_t)li * a.Hq + h) * a.nope * a.r;
-  for (int e = tid; e < a.nope * 8; e += 256) {  // 16-byte pieces: row i, 8 channels
-    const int i = e >> 3, pc = 8 * (e & 7);
-    u4v v = {0u, 0u, 0u, 0u};
-    if (c0 + pc < d) v = *reinterpret_cast<const u4v*>(wk + (int64_t)i * a.r + c0 + pc);
-    *reinterpret_cast<u4v*>(&wt[i * PW + pc]) = v;
-  }
   const int nks = a.nope / 32;
-  const int ct = 16 * wv;  // this wave's 16 channels of the chunk
-  const bool active = c0 + ct < d;
+  _Float16* qa = reinterpret_cast<_Float16*>(a.ws + a.q_off[li]);
+  for (int e = tid; e < a.B * kRope; e += 256) {
+    const int b = e / kRope, j = e - b * kRope;
+    const float x = load_in(a.q, a.q_f32, (((int64_t)li * a.B + b) * a.Hq + h) * qw + a.nope + j);
+    qa[((int64_t)b * a.Hq + h) * W + d + j] = (_Float16)(x * a.scale_log2);
+  }
+  const uint16_t* wt = a.w_ukt + ((int64_t)li * a.Hq + h) * a.r * a.nope;
   for (int b0 = 0; b0 < a.B; b0 += 16) {
-    __syncthreads();  // the previous tile's queries are consumed
-    for (int e = tid; e < 16 * a.nope; e += 256) {  // q_nope of 16 sequences, coalesced
+    __syncthreads();
+    for (int e = tid; e < 16 * a.nope; e += 256) {
       const int bi = e / a.nope, i = e - bi * a.nope;
       qs[bi * PQ + i] = b0 + bi < a.B ? load_in(a.q, a.q_f32, (((int64_t)li * a.B + b0 + bi) * a.Hq + h) * qw + i) : 0.0f;
     }
     __syncthreads();
-    if (!active) continue;
-    const int bq = b0 + i16;
-    f4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int ks = 0; ks < nks; ++ks) {
-      bf16x8 av, bh, bl;
+    bf16x8 bh[8], bl[8];  // nope <= 256
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const int i = 32 * ks + 8 * g + j;
-        av[j] = bitcast<__bf16>(wt[i * PW + ct + i16]);
-        const float x = qs[i16 * PQ + i];
-        const uint16_t hb = bf16_bits_rne(x);
-        bh[j] = bitcast<__bf16>(hb);
-        bl[j] = bitcast<__bf16>(bf16_bits_rne(x - bf16_to_f32(hb)));
+    for (int ks = 0; ks < 8; ++ks) {
+      if (ks < nks) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float x = qs[i16 * PQ + 32 * ks + 8 * g + j];
+          const uint16_t hb = bf16_bits_rne(x);
+          bh[ks][j] = bitcast<__bf16>(hb);
+          bl[ks][j] = bitcast<__bf16>(bf16_bits_rne(x - bf16_to_f32(hb)));
+        }
       }
-      acc = mfmab(av, bh, acc);
-      acc = mfmab(av, bl, acc);
     }
-    if (bq < a.B) {  // D[chan 4g + e][seq i16]
-      _Float16* dst = qa + ((int64_t)bq * a.Hq + h) * W + c0 + ct + 4 * g;
+    const int bq = b0 + i16;
+    for (int c = 16 * wv; c < d; c += 64) {
+      const uint16_t* wrow = wt + (int64_t)(c + i16) * a.nope + 8 * g;
+      u4v wa[8];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) dst[e] = (_Float16)(acc[e] * a.scale_log2);
+      for (int ks = 0; ks < 8; ++ks)
+        if (ks < nks) wa[ks] = *reinterpret_cast<const u4v*>(wrow + 32 * ks);
+      f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        if (ks < nks) {
+          acc = mfmab(bitcast<bf16x8>(wa[ks]), bh[ks], acc);
+          acc = mfmab(bitcast<bf16x8>(wa[ks]), bl[ks], acc);
+        }
+      }
+      if (bq < a.B) {  // D[chan c + 4g + e][seq i16]
+        _Float16* dst = qa + ((int64_t)bq * a.Hq + h) * W + c + 4 * g;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) dst[e] = (_Float16)(acc[e] * a.scale_log2);
+      }
     }
   }
 }
@@ -742,8 +741,9 @@ struct MlaCombineArgs {
 // W_UV[h] on the matrix cores (M = value channels, K = d, N = sequences).
 __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
   constexpr int PO = 512 + 8;  // LDS row pitch (bf16)
+  constexpr int kMaxU = kvk::kMlaMaxUnits;  // split weights held in LDS per sequence
   __shared__ uint16_t oh[16 * PO], ol[16 * PO];
-  __shared__ float mstar[16], linv[16];
+  __shared__ float wgt[16 * kMaxU];
   const int li = blockIdx.x, h = blockIdx.y;
   const int d = a.d_of[li], U = a.units[li], UC = a.units_cap[li];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
@@ -753,32 +753,37 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
   for (int b0 = 0; b0 < a.B; b0 += 16) {
     const int nb = min(16, a.B - b0);
     __syncthreads();
-    if (tid < nb) {
-      const float* p0 = part + (int64_t)(b0 + tid) * UC * rec;
+    // split weights w_u = 2^(m_u - m*) / sum_u 2^(m_u - m*) l_u, one sequence per 16 threads
+    {
+      const int bi = tid >> 4, p = tid & 15;
+      const float* p0 = part + (int64_t)(b0 + bi) * UC * rec;
       float m = -INFINITY;
-      for (int u = 0; u < U; ++u) m = fmaxf(m, p0[u * rec + h]);
+      if (bi < nb)
+        for (int u = p; u < U; u += 16) m = fmaxf(m, p0[u * rec + h]);
+      m = max16(m);
       float l = 0.0f;
-      if (m > -INFINITY)
-        for (int u = 0; u < U; ++u) l += __builtin_amdgcn_exp2f(p0[u * rec + h] - m) * p0[u * rec + a.Hq + h];
-      mstar[tid] = m;
-      linv[tid] = l > 0.0f ? 1.0f / l : 0.0f;
+      if (bi < nb && m > -INFINITY)
+        for (int u = p; u < U; u += 16) l += __builtin_amdgcn_exp2f(p0[u * rec + h] - m) * p0[u * rec + a.Hq + h];
+      l = sum16(l);
+      const float inv = l > 0.0f ? 1.0f / l : 0.0f;
+      for (int u = p; u < min(U, kMaxU); u += 16)
+        wgt[bi * kMaxU + u] = (bi < nb && inv > 0.0f) ? __builtin_amdgcn_exp2f(p0[u * rec + h] - m) * inv : 0.0f;
     }
     __syncthreads();
-    for (int e = tid; e < 16 * d; e += 256) {
-      const int bi = e / d, c = e - bi * d;
-      float x = 0.0f;
-      if (bi < nb && linv[bi] > 0.0f) {
-        const float* p0 = part + (int64_t)(b0 + bi) * UC * rec;
+    for (int e = tid; e < 4 * d; e += 256) {  // 16 sequences x d channels, 4 channels per step
+      const int bi = e / (d / 4), c = 4 * (e - bi * (d / 4));
+      f4 x = {0.f, 0.f, 0.f, 0.f};
+      if (bi < nb) {
+        const float* o0 = part + (int64_t)(b0 + bi) * UC * rec + 2 * a.Hq + (int64_t)h * d + c;
 #pragma unroll 4
-        for (int u = 0; u < U; ++u) {
-          const float w = __builtin_amdgcn_exp2f(p0[u * rec + h] - mstar[bi]);
-          x += w * p0[u * rec + 2 * a.Hq + (int64_t)h * d + c];
-        }
-        x *= linv[bi];
+        for (int u = 0; u < U; ++u) x += wgt[bi * kMaxU + u] * *reinterpret_cast<const f4*>(o0 + u * rec);
       }
-      const uint16_t hb = bf16_bits_rne(x);
-      oh[bi * PO + c] = hb;
-      ol[bi * PO + c] = bf16_bits_rne(x - bf16_to_f32(hb));
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint16_t hb = bf16_bits_rne(x[k]);
+        oh[bi * PO + c + k] = hb;
+        ol[bi * PO + c + k] = bf16_bits_rne(x[k] - bf16_to_f32(hb));
+      }
     }
     __syncthreads();
     for (int jt = wv; jt < a.v / 16; jt += 4) {
@@ -864,7 +869,7 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
   // A1: absorbed queries of every layer of the range
   MlaAbsorbArgs aa;
   aa.q = q;
-  aa.w_uk = static_cast<const uint16_t*>(w_uk);
+  aa.w_ukt = static_cast<const uint16_t*>(w_uk);
   aa.ws = wsb;
   aa.q_f32 = q_dtype == KVK_F32;
   aa.B = d.batch;
@@ -872,15 +877,12 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
   aa.nope = d.nope_dim;
   aa.r = d.latent_dim;
   aa.scale_log2 = scale * kLog2e;
-  int dmax = 0;
   for (int l = l0; l < l1; ++l) {
-    const int dl = t->rank[t->info.anchor_of[l]];
     aa.q_off[l - l0] = ws.q_off[l];
-    aa.d_of[l - l0] = dl;
-    dmax = dl > dmax ? dl : dmax;
+    aa.d_of[l - l0] = t->rank[t->info.anchor_of[l]];
   }
-  hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)(l1 - l0), (unsigned)d.n_q_heads, (unsigned)(dmax / 64 + (dmax % 64 ? 1 : 0))),
-                     dim3(256), 0, stream, aa);
+  hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)(l1 - l0), (unsigned)d.n_q_heads), dim3(256), 0,
+                     stream, aa);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA absorb launch: %s", hipGetErrorString(e));
 

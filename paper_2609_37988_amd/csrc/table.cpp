@@ -88,6 +88,7 @@ int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_block
   int64_t target = KVK_MLA_SPLIT_UNITS / (W + 192);
   if (target < nr) target = nr;
   const int64_t nb = n_blocks > 0 ? n_blocks : 1;
+  if (target * kMlaMaxUnits < nb) target = (nb + kMlaMaxUnits - 1) / kMlaMaxUnits;  // merge limit
   const int64_t nsplit = (nb + target - 1) / target;
   int64_t per = (nb + nsplit - 1) / nsplit;
   per = (per + nr - 1) / nr * nr;

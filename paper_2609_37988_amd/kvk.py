@@ -226,6 +226,12 @@ def _out_width(d: Dims) -> int:
     return d.v_dim if d.kind == MLA else d.head_dim
 
 
+def mla_weights_for_library(w_uk: torch.Tensor) -> torch.Tensor:
+    """W_UK [layers, Hq, nope, r] in the model's layout -> the latent-major layout the
+    library reads ([layers, Hq, r, nope], contiguous); done once at weight load."""
+    return w_uk.transpose(-1, -2).contiguous()
+
+
 def _check_weights(t: Table, nl: int, w_uk, w_uv):
     d = t.dims
     if d.kind != MLA:
@@ -234,8 +240,8 @@ def _check_weights(t: Table, nl: int, w_uk, w_uv):
     _need(w_uk is not None and w_uv is not None, "an MLA table needs w_uk and w_uv")
     _need(w_uk.dtype == torch.bfloat16 and w_uv.dtype == torch.bfloat16 and w_uk.is_contiguous()
           and w_uv.is_contiguous(), "w_uk / w_uv must be contiguous bf16")
-    _need(w_uk.numel() == nl * d.n_q_heads * d.nope_dim * d.latent_dim,
-          "w_uk size must be layers*Hq*nope_dim*latent_dim")
+    _need(w_uk.numel() == nl * d.n_q_heads * d.latent_dim * d.nope_dim,
+          "w_uk size must be layers*Hq*latent_dim*nope_dim (W_UK transposed, latent-major)")
     _need(w_uv.numel() == nl * d.n_q_heads * d.v_dim * d.latent_dim,
           "w_uv size must be layers*Hq*v_dim*latent_dim")
 
@@ -269,7 +275,8 @@ def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor
                      w_uk: Optional[torch.Tensor] = None, w_uv: Optional[torch.Tensor] = None,
                      stream=None):
     """q: [layers, B, Hq, d_h] (MLA: [layers, B, Hq, nope + d_R]) bf16/fp32; out fp32
-    [layers, B, Hq, d_h] (MLA: v_dim); w_uk/w_uv: MLA up-projections, bf16."""
+    [layers, B, Hq, d_h] (MLA: v_dim); w_uk: MLA W_UK transposed [layers, Hq, r, nope]
+    and w_uv [layers, Hq, v, r], bf16 (see mla_weights_for_library)."""
     d = t.dims
     nl = layer_end - layer_begin
     _need(q.is_contiguous() and out.is_contiguous() and out.dtype == torch.float32,

@@ -122,7 +122,8 @@ def test_mla_shaped_stack(variant):
     wk, wv = synth.mla_weights(w, w.n_layers, device=DEV)
     out = torch.empty((w.n_layers, w.batch, w.n_q_heads, w.v_dim), dtype=torch.float32, device=DEV)
     ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=DEV)
-    kvk.decode_attention(table, 0, w.n_layers, q, n, w.softmax_scale(), arena, out, ws, w_uk=wk, w_uv=wv)
+    kvk.decode_attention(table, 0, w.n_layers, q, n, w.softmax_scale(), arena, out, ws,
+                         w_uk=kvk.mla_weights_for_library(wk), w_uv=wv)
     torch.cuda.synchronize()
     od = OP.Dims(OP.MLA, w.n_layers, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, latent_dim=w.latent_dim,
                  rope_dim=w.rope_dim, nope_dim=w.nope_dim, v_dim=w.v_dim, qscheme=w.qscheme, batch=w.batch,

@@ -58,7 +58,7 @@ class MlaCase:
         out = torch.empty((l1 - l0, d.batch, d.n_q_heads, d.v_dim), dtype=torch.float32, device=DEV)
         ws = torch.empty(max(kvk.workspace_bytes(self.table, l0, l1), 256), dtype=torch.uint8, device=DEV)
         kvk.decode_attention(self.table, l0, l1, q.to(DEV).contiguous(), n, scale, self.arena, out, ws,
-                             w_uk=wk.to(DEV).contiguous(), w_uv=wv.to(DEV).contiguous())
+                             w_uk=kvk.mla_weights_for_library(wk.to(DEV)), w_uv=wv.to(DEV).contiguous())
         return out
 
     def dequant(self, layer, n):
