@@ -392,13 +392,25 @@ struct MlaLds {
   __device__ __forceinline__ _Float16* p_h() { return reinterpret_cast<_Float16*>(p); }
 };
 
-// Element (t, c) of the tile: rows of PH halfs; within a row the 16-byte chunks of
-// rows 4..7 of every 8 swap in pairs, so that the eight rows one score read or
-// tile write touches fall in different banks, while the four rows the product's
-// transposed reads touch together (4j .. 4j+3) keep one arrangement.
+// Element (t, c) of the tile: rows of PH halfs (W/2 + 8 dwords, so consecutive rows
+// start 8 banks apart); within a row the 16-byte chunks of rows 4..7 of every 8 swap
+// in pairs, so that the tile writes of one phase-A step fall in different banks.  A
+// transposed read of the product takes 4 consecutive rows x 16 channels per 16 lanes:
+// one swap state, 4 distinct 8-bank windows.
 template <int PH>
 __device__ __forceinline__ int tile_at(int t, int c) {
   return t * PH + ((((c >> 3) ^ ((t >> 2) & 1))) << 3) + (c & 7);
+}
+
+typedef short short4v __attribute__((ext_vector_type(4)));
+
+// Transposed LDS read (ds_read_b64_tr_b16).  Per 16 lanes, lane m names 4 halfs
+// (8 bytes); lane i receives, in order, half i % 4 of the lanes i / 4, i / 4 + 4,
+// i / 4 + 8 and i / 4 + 12.  So when lane m points at 4 consecutive channels
+// 4 (m % 4) .. + 3 of row r0 + m / 4, lane i gets channel i of rows r0 .. r0 + 3.
+__device__ __forceinline__ short4v ds_read_tr4(const _Float16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) short4v*)(const_cast<_Float16*>(p)));
 }
 
 // Raw bytes of one wave's share of an iteration (16 tokens x its channel part).
@@ -554,13 +566,22 @@ __device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, MlaLds& L, int nva
     const float mnew = fmaxf(st.m, mx);  // finite: the iteration holds a stored token
     const float alpha = __builtin_amdgcn_exp2f(st.m - mnew);
     float ps = 0.0f;
+    _Float16 pv[TPT];  // k-slot j of k-step kk holds token 32 kk + j
 #pragma unroll
     for (int e = 0; e < TPT; ++e) {
-      const int tok = TPT * p + e;
-      const _Float16 pv = (_Float16)__builtin_amdgcn_exp2f(x[e] - mnew);
-      ps += (float)pv;
-      // k-step tok / 32, slot 8 (tok % 4) + (tok % 32) / 4
-      L.p_h()[h * kPP + (tok & ~31) + 8 * (tok & 3) + ((tok & 31) >> 2)] = pv;
+      pv[e] = (_Float16)__builtin_amdgcn_exp2f(x[e] - mnew);
+      ps += (float)pv[e];
+    }
+    if constexpr (TPT == 8) {
+      half8 w8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) w8[e] = pv[e];
+      L.p[(h * kPP + TPT * p) >> 3] = w8;
+    } else {
+      short4v w4;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w4[e] = bitcast<short>(pv[e]);
+      *reinterpret_cast<short4v*>(L.p_h() + h * kPP + TPT * p) = w4;
     }
     st.l = st.l * alpha + (TPB == 8 ? sum8(ps) : sum16(ps));
     st.m = mnew;
@@ -576,17 +597,32 @@ __device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, MlaLds& L, int nva
 #pragma unroll
       for (int kk = 0; kk < G::TT / 32; ++kk) pb[kk][ht] = L.p[((16 * ht + i16) * kPP + 32 * kk + 8 * g) >> 3];
     }
+    // Rescale only when some head's running max moved (rare once it has settled).
+    if (__builtin_amdgcn_ballot_w64(al[0] != 1.0f || al[1] != 1.0f)) {
+#pragma unroll
+      for (int i = 0; i < G::NCTW; ++i)
+#pragma unroll
+        for (int ht = 0; ht < 2; ++ht) st.o[i][ht] *= al[ht];
+    }
+    // A operand: lane (channel i16, k-group g) holds tokens 32 kk + 8 g .. + 7.  The
+    // swizzle only touches bit 3 of the channel, so tile ct sits 16 kWaves (ct - wv)
+    // halfs after tile wv in every row.
+    const _Float16* abase[G::TT / 32][2];
+#pragma unroll
+    for (int kk = 0; kk < G::TT / 32; ++kk) {
+      const int r0 = 32 * kk + 8 * g + (i16 >> 2), c = 16 * wv + 4 * (i16 & 3);
+      abase[kk][0] = L.tile_h() + tile_at<G::PH>(r0, c);
+      abase[kk][1] = L.tile_h() + tile_at<G::PH>(r0 + 4, c);
+    }
 #pragma unroll
     for (int i = 0; i < G::NCTW; ++i) {
       const int ct = wv + kWaves * i;
-      if (ct < G::NCT) {
-#pragma unroll
-        for (int ht = 0; ht < 2; ++ht) st.o[i][ht] *= al[ht];
+      if (G::NCT % kWaves == 0 || ct < G::NCT) {
 #pragma unroll
         for (int kk = 0; kk < G::TT / 32; ++kk) {
-          half8 av;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) av[j] = L.tile_h()[tile_at<G::PH>(32 * kk + 4 * j + g, 16 * ct + i16)];
+          const short4v lo = ds_read_tr4(abase[kk][0] + 16 * kWaves * i);
+          const short4v hi = ds_read_tr4(abase[kk][1] + 16 * kWaves * i);
+          const half8 av = bitcast<half8>(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
           for (int ht = 0; ht < 2; ++ht) st.o[i][ht] = mfma16(av, pb[kk][ht], st.o[i][ht]);
         }
