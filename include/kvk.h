@@ -190,19 +190,25 @@ typedef struct {
  * b*stream_bytes[l].  A stream holds NB = cap/32 full blocks of 32 tokens and one
  * bf16 tail block, as for GQA; stream and region sizes are rounded up to 256.
  *
- * bf16 block (bits = 16, and every tail block), 64*W bytes: token t's W bf16
- *   values at byte 2*W*t, channel c at byte 2*W*t + 2*c (round-to-nearest-even
- *   bf16 of the input).  Unused tail rows are zero.
+ * Inside a block the bytes are ordered by the decode kernel's MFMA operand
+ * lanes, so that each of its load instructions reads one contiguous run.  Token t
+ * (0..31) of a block lies in tile T = t/16 at row i = t%16; stored channel c lies
+ * in k-step K = c/32 (NK = W/32 k-steps), sub-group g = (c/8)%4, position s = c%8.
+ * The slot of (t, c) is  S = (T*NK + K)*64 + i + 16*g.
+ *
+ * bf16 block (bits = 16, and every tail block), 64*W bytes: the 8 values of slot
+ *   S at bytes 16*S .. 16*S + 15, channel position s at byte 16*S + 2*s
+ *   (round-to-nearest-even bf16 of the input).  Unused tail rows are zero.
  * quantised block (bits b in {2, 4, 8}): [codes: 4*W*b bytes][meta]
- *   codes: token t's codes fill the W*b/32 consecutive 32-bit words starting at
- *     word t*(W*b/32); word w of the token holds its channels (32/b)*w + k,
- *     k = 0 .. 32/b - 1:
- *       b = 8: k at bit 8*k;
- *       b = 4: k at bit 16*(k%2) + 4*(k/2);
- *       b = 2: k = 8*x + s (x in {0,1}, s in 0..7) at bit 16*(s%2) + 2*(s/2) + 8*x.
- *   KIVI32 meta, 4*W bytes: for token t and channel group g (stored channels
- *     32g .. 32g+31; d and d_R are multiples of 32 so no group mixes the latent
- *     and k^R), the fp16 scale at byte 4*(t*(W/32) + g) and the fp16 zero 2
+ *   codes (32-bit little-endian words):
+ *     b = 8: slot S fills words 2*S and 2*S + 1; position s at word 2*S + s/4,
+ *            bit 8*(s%4);
+ *     b = 4: slot S is word S; position s at bit 16*(s%2) + 4*(s/2);
+ *     b = 2: sub-groups g = 2*y + x (x in {0,1}) of (t, K) share word
+ *            ((T*NK + K)*16 + i)*2 + y; position s at bit 16*(s%2) + 2*(s/2) + 8*x.
+ *   KIVI32 meta, 4*W bytes: for token t and channel group K (stored channels
+ *     32K .. 32K+31; d and d_R are multiples of 32 so no group mixes the latent
+ *     and k^R), the fp16 scale at byte 4*((T*NK + K)*16 + i) and the fp16 zero 2
  *     bytes after it.  Codes and values follow the KIVI32 rules above with the
  *     group being these 32 channels of one token.
  *   SYMROW meta, 128 bytes: for token t the bf16 scale of c[0..d-1] at byte 4*t

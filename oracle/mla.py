@@ -25,7 +25,9 @@ is written out separately and agrees with the reconstruction to rounding, which
 is one of the pins.
 
 Storage layout: the one documented in include/kvk.h (MLA section), restated from
-its text as explicit (token, channel) -> address maps.
+its text as explicit (token, channel) -> address maps: inside a block, bytes are
+ordered by slots of 8 channels of one token, slot S = (T NK + K) 64 + i + 16 g for
+token 16 T + i and channels 32 K + 8 g .. + 7.
 
 Pins (tests/test_oracle_mla.py): absorbed == reconstructed; prefix mask ==
 truncation; a full-rank MLA whose up-projections select disjoint latent slices is
@@ -50,29 +52,48 @@ F32 = np.float32
 # Layout of one 32-token block (include/kvk.h, MLA section)
 # ---------------------------------------------------------------------------
 
+def slot_index(W: int) -> np.ndarray:
+    """Slot S of (token t, stored channel c) in a block: int64 [32, W].  With tile
+    T = t // 16, row i = t % 16, k-step K = c // 32 (NK = W / 32 of them) and
+    sub-group g = (c // 8) % 4:  S = (T NK + K) 64 + i + 16 g.  A slot holds 8
+    consecutive channels c = 32 K + 8 g + s, s = c % 8."""
+    NK = W // 32
+    t = np.arange(32)[:, None]
+    c = np.arange(W)[None, :]
+    return (t // 16 * NK + c // 32) * 64 + t % 16 + 16 * (c // 8 % 4)
+
+
 @lru_cache(maxsize=None)
 def code_bitaddr(W: int, bits: int) -> np.ndarray:
     """Bit address, from the block start, of the code of (token t, stored channel
-    c): int64 [32, W].  Token t's codes fill W*b/32 consecutive 32-bit words; word
-    w holds channels (32/b) w .. (32/b) (w+1) - 1 at:
-      b = 8: channel 4w + s at bit 8 s;
-      b = 4: channel 8w + s at bit 16 (s%2) + 4 (s/2);
-      b = 2: channel 16w + 8x + s at bit 16 (s%2) + 2 (s/2) + 8 x."""
-    per = 32 // bits
-    addr = np.full((32, W), -1, dtype=np.int64)
-    for t in range(32):
-        for c in range(W):
-            word = t * (W // per) + c // per
-            k = c % per
-            if bits == 8:
-                bit = 8 * k
-            elif bits == 4:
-                bit = 16 * (k % 2) + 4 * (k // 2)
-            else:
-                x, s = k // 8, k % 8
-                bit = 16 * (s % 2) + 2 * (s // 2) + 8 * x
-            addr[t, c] = 32 * word + bit
-    return addr
+    c): int64 [32, W], on 32-bit little-endian words:
+      b = 8: slot S fills words 2 S, 2 S + 1; position s at word 2 S + s // 4,
+             bit 8 (s % 4);
+      b = 4: slot S is word S; position s at bit 16 (s % 2) + 4 (s // 2);
+      b = 2: sub-groups g = 2 y + x of (t, K) share word ((T NK + K) 16 + i) 2 + y;
+             position s at bit 16 (s % 2) + 2 (s // 2) + 8 x."""
+    NK = W // 32
+    t = np.arange(32)[:, None]
+    c = np.arange(W)[None, :]
+    S = slot_index(W)
+    s, g = c % 8, c // 8 % 4
+    if bits == 8:
+        word, bit = 2 * S + s // 4, 8 * (s % 4)
+    elif bits == 4:
+        word, bit = S, 16 * (s % 2) + 4 * (s // 2)
+    else:
+        word = ((t // 16 * NK + c // 32) * 16 + t % 16) * 2 + g // 2
+        bit = 16 * (s % 2) + 2 * (s // 2) + 8 * (g % 2)
+    return (32 * word + bit).astype(np.int64)
+
+
+def kivi_meta_offset(W: int) -> np.ndarray:
+    """Byte offset, from the start of the metadata, of the (scale, zero) pair of
+    (token t, channel group K): int64 [32, W / 32] = 4 ((T NK + K) 16 + i)."""
+    NK = W // 32
+    t = np.arange(32)[:, None]
+    K = np.arange(NK)[None, :]
+    return 4 * ((t // 16 * NK + K) * 16 + t % 16)
 
 
 def codes_bytes(W: int, bits: int) -> int:
@@ -111,15 +132,24 @@ def _u16_get(region, byte_off):
     return region[..., byte_off].astype(np.uint16) | (region[..., byte_off + 1].astype(np.uint16) << 8)
 
 
+def _bf16_index(W: int) -> np.ndarray:
+    """bf16 element index (2-byte units) of (t, c) in a bf16 block: 8 S + c % 8."""
+    return 8 * slot_index(W) + np.arange(W)[None, :] % 8
+
+
 def pack_bf16_block(x16: np.ndarray) -> np.ndarray:
-    """bf16 patterns [n, 32, W] -> uint8 [n, 64 W]: token-major, channel order."""
+    """bf16 patterns [n, 32, W] -> uint8 [n, 64 W]: the 8 values of slot S at bytes
+    16 S .. 16 S + 15."""
     n, _, W = x16.shape
-    return np.ascontiguousarray(x16.astype(np.uint16)).view(np.uint8).reshape(n, 64 * W)
+    out = np.zeros((n, 32 * W), dtype=np.uint16)
+    out[:, _bf16_index(W).reshape(-1)] = x16.astype(np.uint16).reshape(n, 32 * W)
+    return out.view(np.uint8).reshape(n, 64 * W)
 
 
 def unpack_bf16_block(raw: np.ndarray, W: int) -> np.ndarray:
     n = raw.shape[0]
-    return np.ascontiguousarray(raw[:, :64 * W]).view(np.uint16).reshape(n, 32, W)
+    v = np.ascontiguousarray(raw[:, :64 * W]).view(np.uint16).reshape(n, 32 * W)
+    return v[:, _bf16_index(W).reshape(-1)].reshape(n, 32, W)
 
 
 # ---------------------------------------------------------------------------
@@ -148,18 +178,16 @@ def dequantise_rows(dims: Dims, bits: int, d: int, f: dict) -> np.ndarray:
 
 
 def pack_quant_blocks(dims: Dims, bits: int, f: dict) -> np.ndarray:
-    """[codes: 32 W b / 8 bytes][meta]: KIVI32 meta holds per token, per group g of
-    32 stored channels, the fp16 scale then the fp16 zero at byte
-    4 (t (W/32) + g); SYMROW meta holds per token the bf16 scale of c[:d] then
-    that of k^R at byte 4 t."""
+    """[codes: 32 W b / 8 bytes][meta]: KIVI32 meta holds per token t, per group K
+    of 32 stored channels, the fp16 scale then the fp16 zero at
+    kivi_meta_offset(W)[t, K]; SYMROW meta holds per token the bf16 scale of c[:d]
+    then that of k^R at byte 4 t."""
     n, _, W = f["u"].shape
     cb = codes_bytes(W, bits)
     out = np.zeros((n, block_bytes(dims, bits, W - dims.rope_dim)), dtype=np.uint8)
     out[:, :cb] = _pack(f["u"], code_bitaddr(W, bits), bits, cb)
     if dims.qscheme == KIVI32:
-        G = W // 32
-        t, g = np.meshgrid(np.arange(32), np.arange(G), indexing="ij")
-        off = cb + 4 * (t * G + g)
+        off = cb + kivi_meta_offset(W)
         _u16_put(out, off, f["s"].view(np.uint16))
         _u16_put(out, off + 2, f["z"].view(np.uint16))
     else:
@@ -174,9 +202,7 @@ def unpack_quant_blocks(dims: Dims, bits: int, d: int, raw: np.ndarray) -> dict:
     cb = codes_bytes(W, bits)
     f = {"u": _unpack(raw[:, :cb], code_bitaddr(W, bits), bits)}
     if dims.qscheme == KIVI32:
-        G = W // 32
-        t, g = np.meshgrid(np.arange(32), np.arange(G), indexing="ij")
-        off = cb + 4 * (t * G + g)
+        off = cb + kivi_meta_offset(W)
         f["s"] = _u16_get(raw, off).view(np.float16)
         f["z"] = _u16_get(raw, off + 2).view(np.float16)
     else:

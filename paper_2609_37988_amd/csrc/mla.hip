@@ -97,6 +97,16 @@ __device__ __forceinline__ uint32_t sym_code(float x, float s, int bits) {
   return (uint32_t)((int)r + (1 << (bits - 1)));
 }
 
+// Slot n of a block (lane-ordered layout): token 16 T + i and the first of the 8
+// channels 32 K + 8 g .. + 7, for n = (T NK + K) 64 + i + 16 g.
+struct MlaSlot {
+  int t, c;
+};
+__device__ __forceinline__ MlaSlot mla_slot(int n, int NK) {
+  const int kq = n >> 6, T = kq / NK;
+  return {16 * T + (n & 15), 32 * (kq - T * NK) + 8 * ((n >> 4) & 3)};
+}
+
 // One workgroup per (32-token block, sequence): stage the block's stored channels
 // (latent[:d] then k^R) in LDS as fp32, compute the metadata, then assemble whole
 // 32-bit code words (coalesced stores).
@@ -133,11 +143,11 @@ __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
 
   uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
                  (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
-  if (tail || a.bits == 16) {  // bf16 block: token-major rows of W values
+  if (tail || a.bits == 16) {  // bf16 block: 16 bytes (8 channels) per slot
     uint32_t* o = reinterpret_cast<uint32_t*>(out);
-    const int half = W / 2;
-    for (int idx = tid; idx < 32 * half; idx += 256) {
-      const int t = idx / half, c = 2 * (idx - t * half);
+    for (int idx = tid; idx < 16 * W; idx += 256) {
+      const MlaSlot q = mla_slot(idx >> 2, G);
+      const int t = q.t, c = q.c + 2 * (idx & 3);
       o[idx] = (uint32_t)bf16_bits_rne(X[t * LD + c]) | ((uint32_t)bf16_bits_rne(X[t * LD + c + 1]) << 16);
     }
     return;
@@ -160,7 +170,7 @@ __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
       const _Float16 zh = (_Float16)mn;
       gs[p] = (float)sh;
       gz[p] = (float)zh;
-      reinterpret_cast<uint32_t*>(out + cb)[p] =
+      reinterpret_cast<uint32_t*>(out + cb)[((t >> 4) * G + g) * 16 + (t & 15)] =
           (uint32_t)bitcast<uint16_t>(sh) | ((uint32_t)bitcast<uint16_t>(zh) << 16);
     } else {
       gs[p] = am;
@@ -180,13 +190,24 @@ __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
     }
     __syncthreads();
   }
-  const int per = 32 / bits, wpt = W / per;  // codes per word, words per token
+  const int per = 32 / bits;  // codes per word
   uint32_t* ow = reinterpret_cast<uint32_t*>(out);
-  for (int wi = tid; wi < 32 * wpt; wi += 256) {
-    const int t = wi / wpt, w = wi - t * wpt;
+  for (int wi = tid; wi < W * bits; wi += 256) {
+    // the word's token and the channel of its first code (see mla_word)
+    int t, c0;
+    if (bits == 8) {
+      const MlaSlot q = mla_slot(wi >> 1, G);
+      t = q.t, c0 = q.c + 4 * (wi & 1);
+    } else if (bits == 4) {
+      const MlaSlot q = mla_slot(wi, G);
+      t = q.t, c0 = q.c;
+    } else {
+      const int kq = wi >> 5, T = kq / G;
+      t = 16 * T + ((wi >> 1) & 15), c0 = 32 * (kq - T * G) + 16 * (wi & 1);
+    }
     uint32_t word = 0;
     for (int k = 0; k < per; ++k) {
-      const int c = per * w + k;
+      const int c = c0 + k;
       const float x = X[t * LD + c];
       uint32_t u;
       if (a.kivi) {
@@ -221,21 +242,25 @@ __global__ __launch_bounds__(256) void mla_dequant_kernel(const uint8_t* region,
   const int nbf = n_stored >> 5;
   const uint8_t* base = region + (int64_t)b * stream_bytes;
   float x;
+  const int NK = W / 32, T = t >> 4, i = t & 15, K = c >> 5, g = (c >> 3) & 3, s = c & 7;
+  const int slot = (T * NK + K) * 64 + i + 16 * g;
   if (blk >= nbf || bits == 16) {
     const uint8_t* bb = base + (blk >= nbf ? (int64_t)nb_cap * block_bytes : (int64_t)blk * block_bytes);
-    x = bf16_to_f32(*reinterpret_cast<const uint16_t*>(bb + 2 * (W * t + c)));
+    x = bf16_to_f32(*reinterpret_cast<const uint16_t*>(bb + 16 * slot + 2 * s));
   } else {
     const uint8_t* bb = base + (int64_t)blk * block_bytes;
-    const int per = 32 / bits, k = c % per;
-    const uint32_t word = reinterpret_cast<const uint32_t*>(bb)[t * (W / per) + c / per];
-    int bit;
-    if (bits == 8) bit = 8 * k;
-    else if (bits == 4) bit = 16 * (k & 1) + 4 * (k >> 1);
-    else bit = 16 * (k & 1) + 2 * ((k & 7) >> 1) + 8 * (k >> 3);
-    const uint32_t u = (word >> bit) & ((1u << bits) - 1u);
+    int wi, bit;
+    if (bits == 8) {
+      wi = 2 * slot + (s >> 2), bit = 8 * (s & 3);
+    } else if (bits == 4) {
+      wi = slot, bit = 16 * (s & 1) + 4 * (s >> 1);
+    } else {
+      wi = ((T * NK + K) * 16 + i) * 2 + (g >> 1), bit = 16 * (s & 1) + 2 * (s >> 1) + 8 * (g & 1);
+    }
+    const uint32_t u = (reinterpret_cast<const uint32_t*>(bb)[wi] >> bit) & ((1u << bits) - 1u);
     const uint16_t* meta = reinterpret_cast<const uint16_t*>(bb + 4 * W * bits);
     if (kivi) {
-      const int p = t * (W / 32) + (c >> 5);
+      const int p = (T * NK + K) * 16 + i;
       x = fmaf((float)u, f16_bits_to_f32(meta[2 * p]), f16_bits_to_f32(meta[2 * p + 1]));
     } else {
       x = (float)((int)u - (1 << (bits - 1))) * bf16_to_f32(meta[2 * t + (c >= d ? 1 : 0)]);
@@ -424,41 +449,44 @@ struct MlaRaw {
   uint32_t m[MW > 0 ? MW : 1];
 };
 
-// Lane (t = lane % 16, g = lane / 16) of wave part kh holds, at its k-step ks, the
-// 8 channels 32 (kh NKW + ks) + 8 g .. + 7 of token t: the MFMA A-operand layout.
+// Lane (i = lane % 16, g = lane / 16) of wave part kh holds, at its k-step ks, the
+// 8 channels 32 (kh NKW + ks) + 8 g .. + 7 of block row t (its tile's row i): the
+// MFMA A-operand layout, which the block's lane-ordered slots follow, so every load
+// of a k-step reads one contiguous run of the block.
 template <int D, int BITS, bool KIVI>
 __device__ __forceinline__ void mla_issue(MlaRaw<D, BITS, KIVI>& r, Rsrc rs, int soff, int t, int g, int kh) {
   constexpr int W = D + kRope, NKW = Geo<D>::NKW;
   const int j0 = kh * NKW;
+  const int kq = (t >> 4) * (W / 32) + j0, i = t & 15;  // first k-step of the part in its tile
   if constexpr (BITS == 16) {
-    const int v = t * 2 * W + 16 * g + 64 * j0;
+    const int v = 16 * (kq * 64 + i + 16 * g);
 #pragma unroll
     for (int ks = 0; ks < NKW; ++ks) {
-      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, v + 64 * ks, soff, 0);
+      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, v + 1024 * ks, soff, 0);
       r.c[ks][0] = x[0]; r.c[ks][1] = x[1]; r.c[ks][2] = x[2]; r.c[ks][3] = x[3];
     }
   } else {
-    constexpr int rowb = W * BITS / 8, cb = 4 * W * BITS;
+    constexpr int cb = 4 * W * BITS;
     if constexpr (BITS == 8) {
-      const int v = t * rowb + 8 * g + 32 * j0;
+      const int v = 8 * (kq * 64 + i + 16 * g);
 #pragma unroll
       for (int ks = 0; ks < NKW; ++ks) {
-        const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, v + 32 * ks, soff, 0);
+        const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, v + 512 * ks, soff, 0);
         r.c[ks][0] = x[0]; r.c[ks][1] = x[1];
       }
     } else if constexpr (BITS == 4) {
-      const int v = t * rowb + 4 * g + 16 * j0;
+      const int v = 4 * (kq * 64 + i + 16 * g);
 #pragma unroll
-      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 16 * ks, soff, 0);
+      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 256 * ks, soff, 0);
     } else {
-      const int v = t * rowb + 4 * (g >> 1) + 8 * j0;
+      const int v = 4 * ((kq * 16 + i) * 2 + (g >> 1));
 #pragma unroll
-      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 8 * ks, soff, 0);
+      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 128 * ks, soff, 0);
     }
     if constexpr (KIVI) {
-      const int v = cb + 4 * (t * (W / 32) + j0);
+      const int v = cb + 4 * (kq * 16 + i);
 #pragma unroll
-      for (int ks = 0; ks < NKW; ++ks) r.m[ks] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 4 * ks, soff, 0);
+      for (int ks = 0; ks < NKW; ++ks) r.m[ks] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 64 * ks, soff, 0);
     } else {
       r.m[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, cb + 4 * t, soff, 0);
     }

@@ -42,6 +42,21 @@ def test_code_map_is_a_bijection(W, bits):
     assert np.unique(occupied).size == occupied.size
 
 
+@pytest.mark.parametrize("W", [96, 128, 192, 320, 576])
+def test_slot_bf16_and_meta_maps_are_bijections(W):
+    """Slots hold 8 channels of one token each and cover 4 W slots; the bf16 block
+    and the KIVI32 (scale, zero) pairs fill their regions exactly once."""
+    S = M.slot_index(W)
+    assert np.array_equal(np.sort(np.unique(S)), np.arange(4 * W))
+    assert np.all(np.bincount(S.reshape(-1)) == 8)
+    rows, cols = np.nonzero(S == S[17, 40 % W])
+    assert np.unique(rows).size == 1 and np.ptp(cols) == 7
+    b16 = (8 * S + np.arange(W)[None, :] % 8).reshape(-1)
+    assert np.array_equal(np.sort(b16), np.arange(32 * W))
+    meta = M.kivi_meta_offset(W).reshape(-1)
+    assert np.array_equal(np.sort(meta), 4 * np.arange(32 * W // 32))
+
+
 def test_layout_hand_examples():
     dims = {s: _dims(qs=(P.KIVI32 if s == "kivi" else P.SYMROW)) for s in ("kivi", "symrow", "bf16")}
     n = 0
@@ -49,6 +64,13 @@ def test_layout_hand_examples():
         if row[0] == "code":
             W, bits, t, c, want = map(int, row[1:])
             assert M.code_bitaddr(W, bits)[t, c] == want, row
+        elif row[0] == "bf16":
+            W, t, c, want = map(int, row[1:])
+            x = np.zeros((1, 32, W), dtype=np.uint16)
+            x[0, t, c] = 0x3F00  # bf16 0.5: low byte zero
+            nz = np.nonzero(M.pack_bf16_block(x)[0])[0]
+            assert nz.size == 1 and nz[0] == want + 1, (row, nz)  # little-endian: high byte second
+            assert M.unpack_bf16_block(M.pack_bf16_block(x), W)[0, t, c] == 0x3F00
         elif row[0] == "meta":
             scheme, W, bits, t, g, field, want = row[1], int(row[2]), int(row[3]), int(row[4]), int(row[5]), row[6], int(row[7])
             # place a marker in one field through the packer and find its byte
