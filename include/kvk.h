@@ -136,18 +136,26 @@ typedef struct {
  *   V slot map: lane lam, tile m in 0..D/16-1, slot s in 0..7
  *               holds channel 16*m + i, token 16*(s/4) + 4*kg + (s%4).
  *
+ * Each lane owns a share of P bytes of a part (a K tile's codes or values, or
+ * the V codes or values).  "Share byte o of lane lam" below is stored at part
+ * byte 1024*(o/16) + 16*lam + o%16 when P > 16 (the shares are dealt out to the
+ * 64 lanes in 16-byte pieces, so that each 16-byte load of all lanes reads one
+ * contiguous kilobyte), and at part byte lam*P + o when P <= 16.
+ *
  * bf16 block (bits = 16, and every tail block), 128*D bytes:
  *   [K: 64*D bytes][V: 64*D bytes]
- *   K: tile tau at byte 32*D*tau; inside it lane lam at byte lam*(D/2); inside
- *      that sub-chunk j at byte 16*j; slot s is the bf16 at byte 2*s.
- *   V: lane lam at byte lam*D; tile m at byte 16*m; slot s the bf16 at byte 2*s.
+ *   K: tile tau is the part at byte 32*D*tau (P = D/2); sub-chunk j of lane lam
+ *      is share bytes 16*j .. 16*j + 15, slot s the bf16 at share byte 16*j + 2*s.
+ *   V: the part at byte 64*D (P = D); tile m of lane lam is share bytes
+ *      16*m .. 16*m + 15, slot s the bf16 at share byte 16*m + 2*s.
  *   A bf16 value is the round-to-nearest-even bf16 of the input value.
  *
  * quantised block (bits b in {2, 4, 8}):
  *   [K codes: 4*D*b][V codes: 4*D*b][K meta][V meta]
- *   K codes: tile tau at byte 2*D*b*tau; lane lam at byte lam*(D*b/32); sub-chunk
- *      j occupies b bytes at byte j*b of the lane.
- *   V codes: lane lam at byte lam*(D*b/16); tile m occupies b bytes at byte m*b.
+ *   K codes: tile tau is the part at byte 2*D*b*tau (P = D*b/32); sub-chunk j of
+ *      lane lam occupies share bytes j*b .. j*b + b - 1.
+ *   V codes: the part at byte 4*D*b (P = D*b/16); tile m of lane lam occupies
+ *      share bytes m*b .. m*b + b - 1.
  *   Each such b-byte "chunk" holds 8 codes of b bits (slots s = 0..7):
  *      b = 8: slot s is byte s.
  *      b = 4: the chunk is one 32-bit word; slot s at bit 16*(s%2) + 4*(s/2).

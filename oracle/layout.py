@@ -52,6 +52,16 @@ def v_slots(D: int):
     return out
 
 
+def part_byte(P: int, lam: int, o: int) -> int:
+    """Byte of a part that holds byte o of lane lam's P-byte share: shares longer
+    than 16 bytes are dealt to the 64 lanes in 16-byte pieces (piece o // 16 of
+    every lane, in lane order, then the next piece); shorter shares are stored
+    one lane after another."""
+    if P > 16:
+        return 1024 * (o // 16) + 16 * lam + o % 16
+    return lam * P + o
+
+
 def _bit_in_chunk(bits: int, x: int, s: int) -> int:
     """Bit offset of slot s relative to the start of its chunk's 32-bit word (or
     of the chunk for b = 8), chunk index x (j or m)."""
@@ -70,13 +80,13 @@ def code_bitaddr(D: int, bits: int):
     arrays [32 tokens, D channels]."""
     kaddr = np.full((32, D), -1, dtype=np.int64)
     for tau, lam, j, s, t, c in k_slots(D):
-        chunk = 2 * D * bits * tau + lam * (D * bits // 32) + j * bits
+        chunk = 2 * D * bits * tau + part_byte(D * bits // 32, lam, j * bits)
         word = chunk - (j % 2) * bits if bits == 2 else chunk
         kaddr[t, c] = 8 * word + _bit_in_chunk(bits, j, s)
     vaddr = np.full((32, D), -1, dtype=np.int64)
     vbase = 4 * D * bits
     for lam, m, s, t, c in v_slots(D):
-        chunk = vbase + lam * (D * bits // 16) + m * bits
+        chunk = vbase + part_byte(D * bits // 16, lam, m * bits)
         word = chunk - (m % 2) * bits if bits == 2 else chunk
         vaddr[t, c] = 8 * word + _bit_in_chunk(bits, m, s)
     return kaddr, vaddr
@@ -87,10 +97,10 @@ def bf16_byteaddr(D: int):
     """Byte addresses of every K and V bf16 value of a bf16 block: [32, D] each."""
     kaddr = np.full((32, D), -1, dtype=np.int64)
     for tau, lam, j, s, t, c in k_slots(D):
-        kaddr[t, c] = 32 * D * tau + lam * (D // 2) + 16 * j + 2 * s
+        kaddr[t, c] = 32 * D * tau + part_byte(D // 2, lam, 16 * j + 2 * s)
     vaddr = np.full((32, D), -1, dtype=np.int64)
     for lam, m, s, t, c in v_slots(D):
-        vaddr[t, c] = 64 * D + lam * D + 16 * m + 2 * s
+        vaddr[t, c] = 64 * D + part_byte(D, lam, 16 * m + 2 * s)
     return kaddr, vaddr
 
 

@@ -101,17 +101,17 @@ __global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
     uint4* o4 = reinterpret_cast<uint4*>(out);
     for (int ci = tid; ci < 8 * D; ci += 256) {
       uint32_t w[4];
-      if (ci < 4 * D) {
+      if (ci < 4 * D) {  // K tile tau: lane shares of D/2 bytes, dealt out in 16-byte pieces
         const int tau = ci / (2 * D), rem = ci % (2 * D);
-        const int lam = rem / (D / 32), j = rem % (D / 32);
+        const int lam = rem & 63, j = rem >> 6;
         const int t = 16 * tau + (lam & 15), c0 = 32 * j + 8 * (lam >> 4);
 #pragma unroll
         for (int p = 0; p < 4; ++p)
           w[p] = (uint32_t)f32_to_bf16_bits(Ks[t * LD + c0 + 2 * p]) |
                  ((uint32_t)f32_to_bf16_bits(Ks[t * LD + c0 + 2 * p + 1]) << 16);
       } else {
-        const int cv = ci - 4 * D;
-        const int lam = cv / (D / 16), m = cv % (D / 16);
+        const int cv = ci - 4 * D;  // V: lane shares of D bytes
+        const int lam = cv & 63, m = cv >> 6;
         const int c = 16 * m + (lam & 15), kg = lam >> 4;
 #pragma unroll
         for (int p = 0; p < 4; ++p) {
@@ -174,15 +174,12 @@ __global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
   for (int wi = tid; wi < 2 * cb / 4; wi += 256) {
     const bool isv = wi >= cb / 4;
     const int wb = 4 * (isv ? wi - cb / 4 : wi);  // byte offset inside the region
-    int lam, r2, tau = 0;
+    int lam, r2, tau = 0;  // lane and byte of its share held by this word
     if (!isv) {
       tau = wb / (2 * D * bits);
-      const int r1 = wb % (2 * D * bits);
-      lam = r1 / lane_bytes_k;
-      r2 = r1 % lane_bytes_k;
+      share_of(lane_bytes_k, wb % (2 * D * bits), lam, r2);
     } else {
-      lam = wb / lane_bytes_v;
-      r2 = wb % lane_bytes_v;
+      share_of(lane_bytes_v, wb, lam, r2);
     }
     const int i = lam & 15, kg = lam >> 4;
     // the slots held by this word: (chunk x, slot s, bit)

@@ -131,64 +131,79 @@ __device__ __forceinline__ Rsrc stream_rsrc(const uint8_t* base, int nbytes) {
 
 // voff: the lane's byte offset inside the part (a vector register shared by all
 // blocks); soff: the block and part offset (a scalar register).
-template <int N>
+template <int N, int POL>
 __device__ __forceinline__ void load_words(Rsrc rs, int voff, int soff, uint32_t* w) {
   if constexpr (N % 4 == 0) {
 #pragma unroll
     for (int i = 0; i < N / 4; ++i) {
-      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + 16 * i, soff, 0);
+      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, voff + 16 * i, soff, POL);
       w[4 * i] = x[0]; w[4 * i + 1] = x[1]; w[4 * i + 2] = x[2]; w[4 * i + 3] = x[3];
     }
   } else if constexpr (N == 2) {
-    const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, 0);
+    const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, voff, soff, POL);
     w[0] = x[0]; w[1] = x[1];
   } else {
-    w[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, 0);
+    w[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, voff, soff, POL);
+  }
+}
+
+// The lane's share of a part (N words at soff, share_byte rules): shares above 16
+// bytes are dealt out in 16-byte pieces, so each load of the wave reads 1 KiB.
+template <int N, int POL>
+__device__ __forceinline__ void load_share(Rsrc rs, int lane, int soff, uint32_t* w) {
+  if constexpr (N % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < N / 4; ++i) {
+      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, 16 * lane, soff + 1024 * i, POL);
+      w[4 * i] = x[0]; w[4 * i + 1] = x[1]; w[4 * i + 2] = x[2]; w[4 * i + 3] = x[3];
+    }
+  } else {
+    load_words<N, POL>(rs, 4 * N * lane, soff, w);
   }
 }
 
 // Loads of the block at byte offset `blk` (wave-uniform) of the stream (block
 // layout of include/kvk.h), in the parts that are consumed at different times:
 // key codes (score phase), value codes (value phase), metadata.
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, bool KIVI, int POL>
 __device__ __forceinline__ void load_k(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane) {
   using R = Raw<D, BITS, KIVI>;
   constexpr int tile = BITS == 16 ? 32 * D : 2 * D * BITS;
 #pragma unroll
-  for (int tau = 0; tau < 2; ++tau) load_words<R::KB / 4>(rs, lane * R::KB, blk + tau * tile, r.k[tau]);
+  for (int tau = 0; tau < 2; ++tau) load_share<R::KB / 4, POL>(rs, lane, blk + tau * tile, r.k[tau]);
 }
 
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, bool KIVI, int POL>
 __device__ __forceinline__ void load_v(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane) {
   using R = Raw<D, BITS, KIVI>;
   constexpr int vbase = BITS == 16 ? 64 * D : 4 * D * BITS;
-  load_words<R::VB / 4>(rs, lane * R::VB, blk + vbase, r.v);
+  load_share<R::VB / 4, POL>(rs, lane, blk + vbase, r.v);
 }
 
 // KIVI32: the lane's share of the 8D-byte metadata area.  SYMROW: part 0 the K
 // row scales (m[0..3]), part 1 the V row scales (m[4..7]) of the lane's tokens.
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, bool KIVI, int POL>
 __device__ __forceinline__ void load_m(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane, int part) {
   using R = Raw<D, BITS, KIVI>;
   if constexpr (BITS != 16) {
     const int meta = blk + 8 * D * BITS;
     if constexpr (KIVI) {
-      load_words<R::MB / 4>(rs, lane * R::MB, meta, r.m);
+      load_share<R::MB / 4, POL>(rs, lane, meta, r.m);
     } else {
       const int kg = lane >> 4;
 #pragma unroll
       for (int tau = 0; tau < 2; ++tau)
-        load_words<2>(rs, 8 * kg, meta + 64 * part + 32 * tau, r.m + 4 * part + 2 * tau);
+        load_words<2, POL>(rs, 8 * kg, meta + 64 * part + 32 * tau, r.m + 4 * part + 2 * tau);
     }
   }
 }
 
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, bool KIVI, int POL>
 __device__ __forceinline__ void load_raw(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane) {
-  load_k<D, BITS, KIVI>(r, rs, blk, lane);
-  load_v<D, BITS, KIVI>(r, rs, blk, lane);
-  load_m<D, BITS, KIVI>(r, rs, blk, lane, 0);
-  if constexpr (!KIVI) load_m<D, BITS, KIVI>(r, rs, blk, lane, 1);
+  load_k<D, BITS, KIVI, POL>(r, rs, blk, lane);
+  load_v<D, BITS, KIVI, POL>(r, rs, blk, lane);
+  load_m<D, BITS, KIVI, POL>(r, rs, blk, lane, 0);
+  if constexpr (!KIVI) load_m<D, BITS, KIVI, POL>(r, rs, blk, lane, 1);
 }
 
 // Unpack the 8 codes (one MFMA k-step) of chunk x from a lane's code words.
@@ -261,7 +276,7 @@ __device__ __forceinline__ half8 to_half8(const float (&x)[8]) {
 // Each compute_* function consumes ring entry `r` and, with RELOAD, refills each
 // part of it from the block at byte offset `next` as soon as that part has been
 // read, so that the registers stay in flight for as long as possible.
-template <int D, bool K, bool RELOAD>
+template <int D, bool K, bool RELOAD, int POL>
 __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D / 32],
                                              const bf16x8 (&qbl)[D / 32], Raw<D, 16, K>& r, Rsrc rs,
                                              int next, bool valid, int lane) {
@@ -283,7 +298,7 @@ __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D 
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);  // the refill may not rise above the reads it replaces
-    load_k<D, 16, K>(r, rs, next, lane);
+    load_k<D, 16, K, POL>(r, rs, next, lane);
   }
   Extra<0> none;
   softmax_update<D, 0>(u, none, x);
@@ -303,14 +318,14 @@ __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D 
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_v<D, 16, K>(r, rs, next, lane);
+    load_v<D, 16, K, POL>(r, rs, next, lane);
   }
 }
 
 // KIVI32 block of BITS-bit codes.  The block's metadata goes through the wave's
 // LDS slot so that the 16 lanes sharing a channel (or token) group read it by
 // broadcast.
-template <int D, int BITS, bool RELOAD>
+template <int D, int BITS, bool RELOAD, int POL>
 __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, const half8 (&qh)[D / 32],
                                              const half8 (&ql)[D / 32], Raw<D, BITS, true>& r, Rsrc rs,
                                              int next, bool valid, uint32_t* lds, int lane) {
@@ -321,7 +336,7 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
   for (int i = 0; i < R::MB / 4; ++i) lds[lane * (R::MB / 4) + i] = r.m[i];
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_m<D, BITS, true>(r, rs, next, lane, 0);
+    load_m<D, BITS, true, POL>(r, rs, next, lane, 0);
   }
   const half8* kmeta = reinterpret_cast<const half8*>(lds);  // scale[D], zero[D], V meta[2D]
   // K: S = sum_c (q_c s_c) u_c + sum_c q_c z_c.  q' = q s as fp16 hi + lo (error-free
@@ -347,7 +362,7 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_k<D, BITS, true>(r, rs, next, lane);
+    load_k<D, BITS, true, POL>(r, rs, next, lane);
   }
   float x[8];
 #pragma unroll
@@ -373,12 +388,12 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_v<D, BITS, true>(r, rs, next, lane);
+    load_v<D, BITS, true, POL>(r, rs, next, lane);
   }
 }
 
 // SYMROW block: per-token scales factor out of both contractions.
-template <int D, int BITS, bool RELOAD>
+template <int D, int BITS, bool RELOAD, int POL>
 __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D / 32],
                                                const half8 (&ql)[D / 32], Raw<D, BITS, false>& r,
                                                Rsrc rs, int next, bool valid, int lane) {
@@ -402,8 +417,8 @@ __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D 
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_k<D, BITS, false>(r, rs, next, lane);
-    load_m<D, BITS, false>(r, rs, next, lane, 0);
+    load_k<D, BITS, false, POL>(r, rs, next, lane);
+    load_m<D, BITS, false, POL>(r, rs, next, lane, 0);
   }
   Extra<0> none;
   softmax_update<D, 0>(u, none, x);
@@ -419,13 +434,13 @@ __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D 
   const half8 p = to_half8(ps);
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_m<D, BITS, false>(r, rs, next, lane, 1);
+    load_m<D, BITS, false, POL>(r, rs, next, lane, 1);
   }
 #pragma unroll
   for (int mt = 0; mt < NM; ++mt) u.o[mt] = mfma16(unpack_chunk<BITS>(r.v, mt, off), p, u.o[mt]);
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_v<D, BITS, false>(r, rs, next, lane);
+    load_v<D, BITS, false, POL>(r, rs, next, lane);
   }
 }
 
@@ -499,7 +514,7 @@ __device__ __forceinline__ void load_query(const DecodeArgs& a, const DecodeItem
 // split partial (o[D], m, l) of every valid row.  Everything the unit keeps in
 // registers is local to this function, so that each precision gets its own
 // register allocation.
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, bool KIVI, int POL>
 __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& it, int sidx, int split,
                                          int chunk, uint32_t* lds, int lane) {
   constexpr int NR = ring_depth<BITS>();
@@ -523,7 +538,7 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
   const Rsrc rs = stream_rsrc(stream, k1 * bb);  // loads past block k1-1 read zeros
   Raw<D, BITS, KIVI> ring[NR];
 #pragma unroll
-  for (int i = 0; i < NR; ++i) load_raw<D, BITS, KIVI>(ring[i], rs, (k0 + i) * bb, lane);
+  for (int i = 0; i < NR; ++i) load_raw<D, BITS, KIVI, POL>(ring[i], rs, (k0 + i) * bb, lane);
   // The query is issued after the ring so that both are waited for together.
   half8 qh[D / 32], ql[D / 32];
   load_query<D>(a, it, row, b, kvh, kg, qh, ql);
@@ -538,9 +553,9 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
     for (int i = 0; i < NR; ++i) {
       const int next = (k + i + NR) * bb;
       const bool valid = k + i < k1;
-      if constexpr (BITS == 16) compute_bf16<D, KIVI, true>(u, qbh, qbl, ring[i], rs, next, valid, lane);
-      else if constexpr (KIVI) compute_kivi<D, BITS, true>(u, ex, qh, ql, ring[i], rs, next, valid, lds, lane);
-      else compute_symrow<D, BITS, true>(u, qh, ql, ring[i], rs, next, valid, lane);
+      if constexpr (BITS == 16) compute_bf16<D, KIVI, true, POL>(u, qbh, qbl, ring[i], rs, next, valid, lane);
+      else if constexpr (KIVI) compute_kivi<D, BITS, true, POL>(u, ex, qh, ql, ring[i], rs, next, valid, lds, lane);
+      else compute_symrow<D, BITS, true, POL>(u, qh, ql, ring[i], rs, next, valid, lane);
     }
   }
 
@@ -585,11 +600,22 @@ __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
   const int split = unit % it.nsplit;
   const int sidx = unit / it.nsplit;  // b * Hkv + kvh
   uint32_t* lds = lds_meta[wslot];
-  switch (it.bits) {
-    case 16: run_unit<D, 16, KIVI>(a, it, sidx, split, chunk, lds, lane); break;
-    case 8: run_unit<D, 8, KIVI>(a, it, sidx, split, chunk, lds, lane); break;
-    case 4: run_unit<D, 4, KIVI>(a, it, sidx, split, chunk, lds, lane); break;
-    default: run_unit<D, 2, KIVI>(a, it, sidx, split, chunk, lds, lane); break;
+  // A stream read by one wave is streamed non-temporally; the waves of a stream read
+  // by several row chunks read it through the caches (the later reads hit).
+  if (it.nchp == 1) {
+    switch (it.bits) {
+      case 16: run_unit<D, 16, KIVI, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
+      case 8: run_unit<D, 8, KIVI, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
+      case 4: run_unit<D, 4, KIVI, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
+      default: run_unit<D, 2, KIVI, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
+    }
+  } else {
+    switch (it.bits) {
+      case 16: run_unit<D, 16, KIVI, 0>(a, it, sidx, split, chunk, lds, lane); break;
+      case 8: run_unit<D, 8, KIVI, 0>(a, it, sidx, split, chunk, lds, lane); break;
+      case 4: run_unit<D, 4, KIVI, 0>(a, it, sidx, split, chunk, lds, lane); break;
+      default: run_unit<D, 2, KIVI, 0>(a, it, sidx, split, chunk, lds, lane); break;
+    }
   }
 }
 

@@ -91,6 +91,11 @@ __device__ __forceinline__ half8 unpack8(uint32_t a, uint32_t b, float off) {
   return cat4(r0, r1, r2, r3);
 }
 
+// Cache policy of the loads that stream a compressed cache: non-temporal.  Each
+// byte is read once per decode step, and on gfx950 a plain streaming read with
+// this hint measured 7.1 TB/s against 6.3 TB/s without it.
+constexpr int kStreamPolicy = 2;
+
 // ---------------------------------------------------------------------------
 // Cross-lane reductions without LDS round trips.
 // ---------------------------------------------------------------------------
@@ -155,11 +160,27 @@ __host__ __device__ inline int64_t block_bytes(int D, int bits, int kivi) {
   return kivi ? 8LL * D * (bits + 1) : 8LL * D * bits + 128;
 }
 
+// Byte of a part holding share byte o of lane lam, for P-byte lane shares: shares
+// above 16 bytes are dealt out to the 64 lanes in 16-byte pieces.
+__host__ __device__ inline int share_byte(int P, int lam, int o) {
+  return P > 16 ? 1024 * (o >> 4) + 16 * lam + (o & 15) : lam * P + o;
+}
+// Inverse: the lane and share byte held at byte b of a part.
+__host__ __device__ inline void share_of(int P, int b, int& lam, int& o) {
+  if (P > 16) {
+    lam = (b & 1023) >> 4;
+    o = 16 * (b >> 10) + (b & 15);
+  } else {
+    lam = b / P;
+    o = b % P;
+  }
+}
+
 // Bit address of the K code of (token t, channel c) in a quantised block.
 __device__ __forceinline__ int64_t k_code_bit(int D, int bits, int t, int c) {
   const int tau = t >> 4, i = t & 15, j = c >> 5, kg = (c & 31) >> 3, s = c & 7;
   const int lam = 16 * kg + i;
-  const int64_t chunk = 2LL * D * bits * tau + (int64_t)lam * (D * bits / 32) + j * bits;
+  const int64_t chunk = 2LL * D * bits * tau + share_byte(D * bits / 32, lam, j * bits);
   if (bits == 8) return 8 * chunk + 8 * s;
   if (bits == 4) return 8 * chunk + 16 * (s & 1) + 4 * (s >> 1);
   return 8 * (chunk - (j & 1) * 2) + 16 * (s & 1) + 2 * (s >> 1) + 8 * (j & 1);
@@ -169,7 +190,7 @@ __device__ __forceinline__ int64_t k_code_bit(int D, int bits, int t, int c) {
 __device__ __forceinline__ int64_t v_code_bit(int D, int bits, int t, int c) {
   const int i = c & 15, m = c >> 4, kg = (t & 15) >> 2, s = 4 * (t >> 4) + (t & 3);
   const int lam = 16 * kg + i;
-  const int64_t chunk = 4LL * D * bits + (int64_t)lam * (D * bits / 16) + m * bits;
+  const int64_t chunk = 4LL * D * bits + share_byte(D * bits / 16, lam, m * bits);
   if (bits == 8) return 8 * chunk + 8 * s;
   if (bits == 4) return 8 * chunk + 16 * (s & 1) + 4 * (s >> 1);
   return 8 * (chunk - (m & 1) * 2) + 16 * (s & 1) + 2 * (s >> 1) + 8 * (m & 1);
@@ -178,11 +199,11 @@ __device__ __forceinline__ int64_t v_code_bit(int D, int bits, int t, int c) {
 // Byte address of the bf16 K / V value of (t, c) in a bf16 block.
 __device__ __forceinline__ int k_bf16_byte(int D, int t, int c) {
   const int tau = t >> 4, i = t & 15, j = c >> 5, kg = (c & 31) >> 3, s = c & 7;
-  return 32 * D * tau + (16 * kg + i) * (D / 2) + 16 * j + 2 * s;
+  return 32 * D * tau + share_byte(D / 2, 16 * kg + i, 16 * j) + 2 * s;
 }
 __device__ __forceinline__ int v_bf16_byte(int D, int t, int c) {
   const int i = c & 15, m = c >> 4, kg = (t & 15) >> 2, s = 4 * (t >> 4) + (t & 3);
-  return 64 * D + (16 * kg + i) * D + 16 * m + 2 * s;
+  return 64 * D + share_byte(D, 16 * kg + i, 16 * m) + 2 * s;
 }
 
 // Index (in fp16 units) of the KIVI32 V-meta entry w (0 scale, 1 zero) of

@@ -462,7 +462,7 @@ __device__ __forceinline__ void mla_issue(MlaRaw<D, BITS, KIVI>& r, Rsrc rs, int
     const int v = 16 * (kq * 64 + i + 16 * g);
 #pragma unroll
     for (int ks = 0; ks < NKW; ++ks) {
-      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, v + 1024 * ks, soff, 0);
+      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, v + 1024 * ks, soff, kStreamPolicy);
       r.c[ks][0] = x[0]; r.c[ks][1] = x[1]; r.c[ks][2] = x[2]; r.c[ks][3] = x[3];
     }
   } else {
@@ -471,24 +471,24 @@ __device__ __forceinline__ void mla_issue(MlaRaw<D, BITS, KIVI>& r, Rsrc rs, int
       const int v = 8 * (kq * 64 + i + 16 * g);
 #pragma unroll
       for (int ks = 0; ks < NKW; ++ks) {
-        const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, v + 512 * ks, soff, 0);
+        const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, v + 512 * ks, soff, kStreamPolicy);
         r.c[ks][0] = x[0]; r.c[ks][1] = x[1];
       }
     } else if constexpr (BITS == 4) {
       const int v = 4 * (kq * 64 + i + 16 * g);
 #pragma unroll
-      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 256 * ks, soff, 0);
+      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 256 * ks, soff, kStreamPolicy);
     } else {
       const int v = 4 * ((kq * 16 + i) * 2 + (g >> 1));
 #pragma unroll
-      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 128 * ks, soff, 0);
+      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 128 * ks, soff, kStreamPolicy);
     }
     if constexpr (KIVI) {
       const int v = cb + 4 * (kq * 16 + i);
 #pragma unroll
-      for (int ks = 0; ks < NKW; ++ks) r.m[ks] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 64 * ks, soff, 0);
+      for (int ks = 0; ks < NKW; ++ks) r.m[ks] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 64 * ks, soff, kStreamPolicy);
     } else {
-      r.m[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, cb + 4 * t, soff, 0);
+      r.m[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, cb + 4 * t, soff, kStreamPolicy);
     }
   }
 }
