@@ -49,29 +49,40 @@ def parse():
     return ap.parse_args()
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gqa_decode_14b_mixed_traffic.json")
-SOURCES = ["table.cpp", "decode.hip", "kvk_device.h", "kvk_internal.h"]
+# Counter records (scaled FETCH_SIZE + WRITE_SIZE per launch of the roofline kernel),
+# per workload, with the sources that determine that kernel and its launch shape.
+GQA_SOURCES = ["table.cpp", "decode.hip", "kvk_device.h", "kvk_internal.h"]
+MLA_SOURCES = ["table.cpp", "mla.hip", "kvk_device.h", "kvk_internal.h"]
+TRAFFIC = {
+    (2, None): ("gqa_decode_14b_mixed_traffic.json", GQA_SOURCES),
+    (3, None): ("mla_decode_32l_bf16_traffic.json", MLA_SOURCES),
+    (3, "int4"): ("mla_decode_32l_int4_traffic.json", MLA_SOURCES),
+}
 
 
-def kernel_source_hash() -> str:
-    """sha256 over the sources that determine the decode kernel and its splits."""
+def kernel_source_hash(sources=GQA_SOURCES) -> str:
+    """sha256 over the sources that determine a decode kernel and its splits."""
     import hashlib
     h = hashlib.sha256()
-    for f in SOURCES:
+    for f in sources:
         with open(os.path.join(ROOT, "paper_2609_37988_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
-def recorded_traffic(config: int):
-    """HBM bytes per D1 launch from the committed counter record, or None when the
-    record is missing, for another workload, or taken on different kernel sources."""
+def recorded_traffic(config: int, variant=None):
+    """HBM bytes per launch of the roofline kernel from the committed counter record,
+    or None when there is no record for this workload or it was taken on different
+    kernel sources."""
+    if (config, variant) not in TRAFFIC:
+        return None
+    name, sources = TRAFFIC[(config, variant)]
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(os.path.join(ROOT, "profiles", name)) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_source_sha256") != kernel_source_hash() or rec.get("config") != config:
+    if rec.get("kernel_source_sha256") != kernel_source_hash(sources) or rec.get("config") != config:
         return None
     return rec.get("traffic_bytes_per_launch")
 
@@ -284,7 +295,8 @@ def run_mla(args):
         "roofline": {
             "bound": "hbm", "kernel": "mla_absorb_kernel + mla_decode_kernel (A1 + D2)",
             "achieved": round(sp_gbs, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(sp_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+            "frac": round(sp_gbs / HBM_PEAK_GBS, 4),
+            "traffic": recorded_traffic(3, args.variant) if args.qscheme == "kivi32" else None,
             "launch_us": round(sp_avg * 1e3, 2), "bytes_per_launch": alg,
         },
         "cpu_baseline": cpu,
@@ -410,7 +422,7 @@ def main():
         "roofline": {
             "bound": "hbm", "kernel": "gqa_decode_kernel (D1)", "achieved": round(d1_gbs, 2),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(d1_gbs / HBM_PEAK_GBS, 4),
-            "traffic": recorded_traffic(args.config) if args.qscheme == "kivi32" and args.variant is None else None,
+            "traffic": recorded_traffic(args.config, args.variant) if args.qscheme == "kivi32" else None,
             "launch_us": round(d1_avg * 1e3, 2), "bytes_per_launch": alg,
         },
         "cpu_baseline": cpu,
