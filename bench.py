@@ -32,6 +32,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decode-attention cache GB/s (% of HBM peak) and µs/step, 14B-shaped b=32 ctx=8k"
 HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16/bf16 matrix peak
 
 
 def parse():
@@ -105,10 +106,10 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def cpu_baseline(w, table, n_stored, scale, n_layers_sample):
-    """Time the oracle's decode (dequantise + fp64 attention) for batch element 0
-    over the first n_layers_sample layers; inputs drawn on the CPU with the same
-    recipe and compressed by the oracle beforehand (untimed)."""
+def cpu_baseline(w, table, n_stored, scale, n_layers_sample, n_batch=1):
+    """Time the oracle's decode (dequantise + fp64 attention) for the first n_batch
+    batch elements over the first n_layers_sample layers; inputs drawn on the CPU
+    with the same recipe and compressed by the oracle beforehand (untimed)."""
     import numpy as np
     import torch
     from threadpoolctl import threadpool_info
@@ -126,30 +127,32 @@ def cpu_baseline(w, table, n_stored, scale, n_layers_sample):
     G = d.n_q_heads // d.n_kv_heads
     streams = {}
     for a in sorted(set(anc)):
-        k, v = synth.kv_layer(w, a, device="cpu", batch=1)
+        k, v = synth.kv_layer(w, a, device="cpu", batch=n_batch)
         keep = None
         if w.keep_tokens:
-            keep = synth.keep_positions(w, a, device="cpu", batch=1).numpy()
+            keep = synth.keep_positions(w, a, device="cpu", batch=n_batch).numpy()
         kn, vn = k.float().numpy(), v.float().numpy()
         bits = w.plan[a][1]
-        for h in range(d.n_kv_heads):
-            kk, vv = kn[0, h], vn[0, h]
-            if keep is not None:
-                kk, vv = OC.gather_kept(kk, keep[0, h]), OC.gather_kept(vv, keep[0, h])
-            streams[(a, h)] = (bits, OC.compress_stream(od, bits, kk, vv))
-    q = synth.queries(w, n_layers_sample, device="cpu", batch=1).float().numpy().astype(np.float64)
+        for b in range(n_batch):
+            for h in range(d.n_kv_heads):
+                kk, vv = kn[b, h], vn[b, h]
+                if keep is not None:
+                    kk, vv = OC.gather_kept(kk, keep[b, h]), OC.gather_kept(vv, keep[b, h])
+                streams[(a, b, h)] = (bits, OC.compress_stream(od, bits, kk, vv))
+    q = synth.queries(w, n_layers_sample, device="cpu", batch=n_batch).float().numpy().astype(np.float64)
     t0 = time.perf_counter()
-    for l in range(n_layers_sample):
-        for h in range(d.n_kv_heads):
-            bits, st = streams[(anc[l], h)]
-            K, V = OC.dequant_stream(od, bits, st, n_stored)
-            OA.softmax_attention(q[l, 0, h * G:(h + 1) * G], K, V, scale)
+    for b in range(n_batch):
+        for l in range(n_layers_sample):
+            for h in range(d.n_kv_heads):
+                bits, st = streams[(anc[l], b, h)]
+                K, V = OC.dequant_stream(od, bits, st, n_stored)
+                OA.softmax_attention(q[l, b, h * G:(h + 1) * G], K, V, scale)
     dt = time.perf_counter() - t0
-    sample_bytes = kvk.read_bytes(table, 0, n_layers_sample, n_stored) // d.batch
+    sample_bytes = kvk.read_bytes(table, 0, n_layers_sample, n_stored) // d.batch * n_batch
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": round(sample_bytes / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"batch element 0 of {d.batch}, layers 0..{n_layers_sample - 1} "
+            "sample": f"batch elements 0..{n_batch - 1} of {d.batch}, layers 0..{n_layers_sample - 1} "
                       f"({len(set(anc))} anchors x {d.n_kv_heads} KV heads), {n_stored} tokens: "
                       f"{sample_bytes} algorithmic bytes in {dt:.2f} s (numpy fp64 oracle; "
                       f"elementwise work single-threaded, BLAS threads = cores)",
@@ -268,6 +271,10 @@ def run_mla(args):
     sp_gbs = alg / (sp_avg * 1e-3) / 1e9
     wbytes = sum(w.n_q_heads * (w.nope_dim + w.v_dim) * w.plan[info.anchor_of[l]][2] * 2
                  for l in range(w.n_layers))
+    # matrix-core work of D2 per step: scores over the W = d + d_R stored channels and
+    # the probability-by-latent product over d, per (token, head), 2 flops per MAC
+    d2_flops = sum(2 * w.batch * n_stored * w.n_q_heads *
+                   (2 * w.plan[info.anchor_of[l]][2] + w.rope_dim) for l in range(w.n_layers))
     log(f"step {ms_step * 1e3:.1f} us, {gbs:.1f} GB/s ({100 * gbs / HBM_PEAK_GBS:.1f}% of HBM); "
         f"A1+D2 {sp_avg * 1e3:.1f} us ({sp_gbs:.1f} GB/s)")
     cpu = None
@@ -299,6 +306,9 @@ def run_mla(args):
             "traffic": recorded_traffic(3, args.variant) if args.qscheme == "kivi32" else None,
             "launch_us": round(sp_avg * 1e3, 2), "bytes_per_launch": alg,
         },
+        "mfma": {"flops_per_step": d2_flops, "achieved": round(d2_flops / (sp_avg * 1e-3) / 1e12, 1),
+                 "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                 "frac": round(d2_flops / (sp_avg * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 4)},
         "cpu_baseline": cpu,
         "prefill_write": {"ms": round(w2_ms, 3), "bytes": w2_bytes,
                           "GB_per_s": round(w2_bytes / (w2_ms * 1e-3) / 1e9, 2)},
@@ -388,8 +398,8 @@ def main():
 
     cpu = None
     if not args.no_cpu_baseline:
-        nl = args.cpu_layers or (24 if args.config in (1, 2) else 4)
-        cpu = cpu_baseline(w, table, n_stored, scale, nl)
+        nl = args.cpu_layers or (w.n_layers if args.config in (1, 2) else 4)
+        cpu = cpu_baseline(w, table, n_stored, scale, nl, n_batch=2 if args.config in (1, 2) else 1)
         log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
 
     bits_mix = {}
