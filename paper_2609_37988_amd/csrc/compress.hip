@@ -8,9 +8,11 @@
 // The layout written is the one documented in include/kvk.h.
 //
 // One workgroup of 256 threads writes one 32-token block of one stream: it stages
-// the block's K and V in LDS as fp32, computes the group metadata, then every
-// thread assembles whole 32-bit words of codes so that the global stores are
-// coalesced.
+// the block's K and V in LDS as fp32 (16-byte loads), computes the group metadata
+// with several threads per group and lane reductions, then every thread assembles
+// whole 32-bit words of codes so that the global stores are coalesced.  The kernel
+// is specialised per head width, bit-width and scheme, so that the layout address
+// arithmetic reduces to shifts and masks.
 #include <hip/hip_runtime.h>
 
 #include "kvk_device.h"
@@ -53,9 +55,94 @@ __device__ __forceinline__ uint32_t sym_code(float x, float s, int bits) {
   return (uint32_t)((int)r + (1 << (bits - 1)));
 }
 
-template <int D>
+// Stage the 32 tokens of a block (K and V, fp32) in LDS: thread (token t, chunk q)
+// moves channels 8q .. 8q+7 with 16-byte loads; tokens past ntok are zero.
+template <int D, int LD>
+__device__ __forceinline__ void stage_block(const CompressArgs& a, int stream, int tok0, int ntok, float* Ks,
+                                            float* Vs, int tid) {
+  constexpr int NQ = D / 8, TPP = 256 / NQ;  // chunks per row, tokens per pass
+  const int q = tid % NQ;
+  for (int t = tid / NQ; t < 32; t += TPP) {
+    f4 k0 = {0.f, 0.f, 0.f, 0.f}, k1 = k0, v0 = k0, v1 = k0;
+    if (t < ntok) {
+      int pos = tok0 + t;
+      if (a.keep) {
+        pos = a.keep[(int64_t)stream * a.n_stored + pos];
+        pos = pos < 0 ? 0 : (pos >= a.n_tokens ? a.n_tokens - 1 : pos);
+      }
+      const int64_t e = ((int64_t)stream * a.n_tokens + pos) * D + 8 * q;
+      if (a.in_f32) {
+        const f4* kp = reinterpret_cast<const f4*>(static_cast<const float*>(a.k) + e);
+        const f4* vp = reinterpret_cast<const f4*>(static_cast<const float*>(a.v) + e);
+        k0 = kp[0], k1 = kp[1], v0 = vp[0], v1 = vp[1];
+      } else {
+        const u4v kw = *reinterpret_cast<const u4v*>(static_cast<const uint16_t*>(a.k) + e);
+        const u4v vw = *reinterpret_cast<const u4v*>(static_cast<const uint16_t*>(a.v) + e);
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          k0[2 * p] = __uint_as_float(kw[p] << 16), k0[2 * p + 1] = __uint_as_float(kw[p] & 0xffff0000u);
+          k1[2 * p] = __uint_as_float(kw[p + 2] << 16), k1[2 * p + 1] = __uint_as_float(kw[p + 2] & 0xffff0000u);
+          v0[2 * p] = __uint_as_float(vw[p] << 16), v0[2 * p + 1] = __uint_as_float(vw[p] & 0xffff0000u);
+          v1[2 * p] = __uint_as_float(vw[p + 2] << 16), v1[2 * p + 1] = __uint_as_float(vw[p + 2] & 0xffff0000u);
+        }
+      }
+    }
+    *reinterpret_cast<f4*>(&Ks[t * LD + 8 * q]) = k0;
+    *reinterpret_cast<f4*>(&Ks[t * LD + 8 * q + 4]) = k1;
+    *reinterpret_cast<f4*>(&Vs[t * LD + 8 * q]) = v0;
+    *reinterpret_cast<f4*>(&Vs[t * LD + 8 * q + 4]) = v1;
+  }
+}
+
+// bf16 block: 16-byte chunks of 8 values (see the bf16 block layout).
+template <int D, int LD>
+__device__ __forceinline__ void write_bf16_block(const float* Ks, const float* Vs, uint8_t* out, int tid) {
+  uint4* o4 = reinterpret_cast<uint4*>(out);
+  for (int ci = tid; ci < 8 * D; ci += 256) {
+    uint32_t w[4];
+    if (ci < 4 * D) {  // K tile tau: lane shares of D/2 bytes, dealt out in 16-byte pieces
+      const int tau = ci / (2 * D), rem = ci % (2 * D);
+      const int lam = rem & 63, j = rem >> 6;
+      const int t = 16 * tau + (lam & 15), c0 = 32 * j + 8 * (lam >> 4);
+#pragma unroll
+      for (int p = 0; p < 4; ++p)
+        w[p] = (uint32_t)f32_to_bf16_bits(Ks[t * LD + c0 + 2 * p]) |
+               ((uint32_t)f32_to_bf16_bits(Ks[t * LD + c0 + 2 * p + 1]) << 16);
+    } else {
+      const int cv = ci - 4 * D;  // V: lane shares of D bytes
+      const int lam = cv & 63, m = cv >> 6;
+      const int c = 16 * m + (lam & 15), kg = lam >> 4;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int s0 = 2 * p, s1 = 2 * p + 1;
+        const int t0 = 16 * (s0 >> 2) + 4 * kg + (s0 & 3), t1 = 16 * (s1 >> 2) + 4 * kg + (s1 & 3);
+        w[p] = (uint32_t)f32_to_bf16_bits(Vs[t0 * LD + c]) | ((uint32_t)f32_to_bf16_bits(Vs[t1 * LD + c]) << 16);
+      }
+    }
+    o4[ci] = make_uint4(w[0], w[1], w[2], w[3]);
+  }
+}
+
+// min / max over the N consecutive lanes of a group (N = 1, 2, 4), every lane of the
+// group ending with the result.
+template <int N>
+__device__ __forceinline__ float group_min(float x) {
+  if constexpr (N >= 2) x = fminf(x, dpp<kQuadXor1>(x));
+  if constexpr (N >= 4) x = fminf(x, dpp<kQuadXor2>(x));
+  return x;
+}
+template <int N>
+__device__ __forceinline__ float group_max(float x) {
+  if constexpr (N >= 2) x = fmaxf(x, dpp<kQuadXor1>(x));
+  if constexpr (N >= 4) x = fmaxf(x, dpp<kQuadXor2>(x));
+  return x;
+}
+
+// One workgroup writes one 32-token block of one stream, with BITS-bit codes (or
+// bf16 at BITS = 16; a stream's tail block is always bf16).
+template <int D, int BITS, bool KIVI>
 __global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
-  constexpr int LD = D + 1;  // padded LDS row
+  constexpr int LD = D + 4;  // padded LDS row (floats), rows 16-byte aligned
   __shared__ float Ks[32 * LD];
   __shared__ float Vs[32 * LD];
   __shared__ float kmeta[2 * D];          // KIVI: scale, zero per channel; SYMROW: row scale
@@ -69,167 +156,144 @@ __global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
   const int tok0 = blk * 32;
   const int ntok = tail ? a.n_stored - tok0 : 32;  // valid tokens of this block
 
-  // ---- stage K and V (fp32) ----
-  for (int idx = tid; idx < 32 * D; idx += 256) {
-    const int t = idx / D, c = idx % D;
-    float kv = 0.0f, vv = 0.0f;
-    if (t < ntok) {
-      int pos = tok0 + t;
-      if (a.keep) {
-        pos = a.keep[(int64_t)stream * a.n_stored + pos];
-        pos = pos < 0 ? 0 : (pos >= a.n_tokens ? a.n_tokens - 1 : pos);
-      }
-      const int64_t e = ((int64_t)stream * a.n_tokens + pos) * D + c;
-      if (a.in_f32) {
-        kv = static_cast<const float*>(a.k)[e];
-        vv = static_cast<const float*>(a.v)[e];
-      } else {
-        kv = bf16_to_f32(static_cast<const uint16_t*>(a.k)[e]);
-        vv = bf16_to_f32(static_cast<const uint16_t*>(a.v)[e]);
-      }
-    }
-    Ks[t * LD + c] = kv;
-    Vs[t * LD + c] = vv;
-  }
+  stage_block<D, LD>(a, stream, tok0, ntok, Ks, Vs, tid);
   __syncthreads();
 
   uint8_t* out = a.region + (int64_t)stream * a.stream_bytes +
                  (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
-
-  if (tail || a.bits == 16) {
-    // bf16 block: 16-byte chunks of 8 values, see the bf16 block layout.
-    uint4* o4 = reinterpret_cast<uint4*>(out);
-    for (int ci = tid; ci < 8 * D; ci += 256) {
-      uint32_t w[4];
-      if (ci < 4 * D) {  // K tile tau: lane shares of D/2 bytes, dealt out in 16-byte pieces
-        const int tau = ci / (2 * D), rem = ci % (2 * D);
-        const int lam = rem & 63, j = rem >> 6;
-        const int t = 16 * tau + (lam & 15), c0 = 32 * j + 8 * (lam >> 4);
-#pragma unroll
-        for (int p = 0; p < 4; ++p)
-          w[p] = (uint32_t)f32_to_bf16_bits(Ks[t * LD + c0 + 2 * p]) |
-                 ((uint32_t)f32_to_bf16_bits(Ks[t * LD + c0 + 2 * p + 1]) << 16);
-      } else {
-        const int cv = ci - 4 * D;  // V: lane shares of D bytes
-        const int lam = cv & 63, m = cv >> 6;
-        const int c = 16 * m + (lam & 15), kg = lam >> 4;
-#pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const int s0 = 2 * p, s1 = 2 * p + 1;
-          const int t0 = 16 * (s0 >> 2) + 4 * kg + (s0 & 3), t1 = 16 * (s1 >> 2) + 4 * kg + (s1 & 3);
-          w[p] = (uint32_t)f32_to_bf16_bits(Vs[t0 * LD + c]) |
-                 ((uint32_t)f32_to_bf16_bits(Vs[t1 * LD + c]) << 16);
-        }
-      }
-      o4[ci] = make_uint4(w[0], w[1], w[2], w[3]);
-    }
+  if (BITS == 16 || tail) {
+    write_bf16_block<D, LD>(Ks, Vs, out, tid);
     return;
   }
+  if constexpr (BITS != 16) {
+    constexpr float levels = (float)((1 << BITS) - 1);
 
-  const int bits = a.bits;
-  const float levels = (float)((1 << bits) - 1);
-
-  // ---- group metadata ----
-  if (a.kivi) {
-    if (tid < D) {  // K: channel tid over the block's 32 tokens
-      float mn = Ks[tid], mx = Ks[tid];
-      for (int t = 1; t < 32; ++t) {
-        const float x = Ks[t * LD + tid];
-        mn = fminf(mn, x);
-        mx = fmaxf(mx, x);
-      }
-      const _Float16 sh = (_Float16)((mx - mn) / levels);
-      const _Float16 zh = (_Float16)mn;
-      kmeta[tid] = (float)sh;
-      kmeta[D + tid] = (float)zh;
-    } else if (tid < 2 * D) {  // V: token t, channel group g
-      const int r = tid - D, t = r / (D / 32), g = r % (D / 32);
-      const float* row = &Vs[t * LD + 32 * g];
-      float mn = row[0], mx = row[0];
-      for (int c = 1; c < 32; ++c) {
-        mn = fminf(mn, row[c]);
-        mx = fmaxf(mx, row[c]);
-      }
-      const _Float16 sh = (_Float16)((mx - mn) / levels);
-      const _Float16 zh = (_Float16)mn;
-      vmeta[2 * (t * (D / 32) + g)] = (float)sh;
-      vmeta[2 * (t * (D / 32) + g) + 1] = (float)zh;
-    }
-  } else if (tid < 64) {  // SYMROW: one scale per token row, K (tid < 32) and V
-    const float* row = tid < 32 ? &Ks[tid * LD] : &Vs[(tid - 32) * LD];
-    float amax = 0.0f;
-    for (int c = 0; c < D; ++c) amax = fmaxf(amax, fabsf(row[c]));
-    const float q = (float)((1 << (bits - 1)) - 1);
-    const float sc = bf16_to_f32(f32_to_bf16_bits(amax / q));
-    if (tid < 32) kmeta[tid] = sc;
-    else vmeta[tid - 32] = sc;
-  }
-  __syncthreads();
-
-  // ---- codes: whole 32-bit words ----
-  uint32_t* ow = reinterpret_cast<uint32_t*>(out);
-  const int cb = 4 * D * bits;          // bytes per code region
-  const int lane_bytes_k = D * bits / 32;
-  const int lane_bytes_v = D * bits / 16;
-  for (int wi = tid; wi < 2 * cb / 4; wi += 256) {
-    const bool isv = wi >= cb / 4;
-    const int wb = 4 * (isv ? wi - cb / 4 : wi);  // byte offset inside the region
-    int lam, r2, tau = 0;  // lane and byte of its share held by this word
-    if (!isv) {
-      tau = wb / (2 * D * bits);
-      share_of(lane_bytes_k, wb % (2 * D * bits), lam, r2);
-    } else {
-      share_of(lane_bytes_v, wb, lam, r2);
-    }
-    const int i = lam & 15, kg = lam >> 4;
-    // the slots held by this word: (chunk x, slot s, bit)
-    int nslot, x0, s0;
-    if (bits == 8) { nslot = 4; x0 = r2 / 8; s0 = 4 * ((r2 % 8) / 4); }
-    else if (bits == 4) { nslot = 8; x0 = r2 / 4; s0 = 0; }
-    else { nslot = 16; x0 = r2 / 2; s0 = 0; }
-    uint32_t word = 0;
-    for (int q = 0; q < nslot; ++q) {
-      int x, s, bit;
-      if (bits == 8) { x = x0; s = s0 + q; bit = 8 * q; }
-      else if (bits == 4) { x = x0; s = q; bit = 16 * (s & 1) + 4 * (s >> 1); }
-      else { x = x0 + (q >> 3); s = q & 7; bit = 16 * (s & 1) + 2 * (s >> 1) + 8 * (q >> 3); }
-      uint32_t u;
-      if (!isv) {
-        const int t = 16 * tau + i, c = 32 * x + 8 * kg + s;
-        const float xv = Ks[t * LD + c];
-        u = a.kivi ? kivi_code(xv, kmeta[c], kmeta[D + c], levels) : sym_code(xv, kmeta[t], bits);
-      } else {
-        const int c = 16 * x + i, t = 16 * (s >> 2) + 4 * kg + (s & 3);
-        const float xv = Vs[t * LD + c];
-        if (a.kivi) {
-          const int g = c >> 5;
-          u = kivi_code(xv, vmeta[2 * (t * (D / 32) + g)], vmeta[2 * (t * (D / 32) + g) + 1], levels);
-        } else {
-          u = sym_code(xv, vmeta[t], bits);
+    // ---- group metadata ----
+    if constexpr (KIVI) {
+      {  // K: channel c over the block's 32 tokens, TPC threads per channel
+        constexpr int TPC = 256 / D, TOK = 32 / TPC;
+        const int c = tid / TPC, t0 = TOK * (tid % TPC);
+        float mn = Ks[t0 * LD + c], mx = mn;
+#pragma unroll
+        for (int t = 1; t < TOK; ++t) {
+          const float x = Ks[(t0 + t) * LD + c];
+          mn = fminf(mn, x);
+          mx = fmaxf(mx, x);
+        }
+        mn = group_min<TPC>(mn);
+        mx = group_max<TPC>(mx);
+        if (tid % TPC == 0) {
+          kmeta[c] = (float)(_Float16)((mx - mn) / levels);
+          kmeta[D + c] = (float)(_Float16)mn;
         }
       }
-      word |= u << bit;
-    }
-    ow[wi] = word;
-  }
-
-  // ---- metadata stores ----
-  uint16_t* om = reinterpret_cast<uint16_t*>(out + 2 * cb);
-  if (a.kivi) {
-    for (int idx = tid; idx < 4 * D; idx += 256) {
-      float val;
-      if (idx < 2 * D) {
-        val = kmeta[idx];  // scale[0..D) then zero[0..D)
-      } else {
-        const int e = idx - 2 * D;  // ((g*2 + w)*4 + kg)*8 + s
-        const int s = e & 7, kg = (e >> 3) & 3, w = (e >> 5) & 1, g = e >> 6;
-        const int t = 16 * (s >> 2) + 4 * kg + (s & 3);
-        val = vmeta[2 * (t * (D / 32) + g) + w];
+      {  // V: token t, channel group g (32 channels), TPG threads per group
+        constexpr int NG = D / 32, TPG = 256 / (32 * NG), CH = 32 / TPG;
+        const int pr = tid / TPG, t = pr / NG, g = pr % NG;
+        const float* row = &Vs[t * LD + 32 * g + CH * (tid % TPG)];
+        f4 x = *reinterpret_cast<const f4*>(row);
+        float mn = fminf(fminf(x[0], x[1]), fminf(x[2], x[3])), mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+#pragma unroll
+        for (int c = 4; c < CH; c += 4) {
+          x = *reinterpret_cast<const f4*>(row + c);
+          mn = fminf(mn, fminf(fminf(x[0], x[1]), fminf(x[2], x[3])));
+          mx = fmaxf(mx, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+        }
+        mn = group_min<TPG>(mn);
+        mx = group_max<TPG>(mx);
+        if (tid % TPG == 0) {
+          vmeta[2 * (t * NG + g)] = (float)(_Float16)((mx - mn) / levels);
+          vmeta[2 * (t * NG + g) + 1] = (float)(_Float16)mn;
+        }
       }
-      om[idx] = bitcast<uint16_t>((_Float16)val);  // exact: the value is an fp16
+    } else {  // SYMROW: one scale per token row of K (rows 0..31) and V (rows 32..63), 4 threads per row
+      constexpr int CH = D / 4;
+      const int r = tid >> 2;
+      const float* row = (r < 32 ? &Ks[r * LD] : &Vs[(r - 32) * LD]) + CH * (tid & 3);
+      float am = 0.0f;
+#pragma unroll
+      for (int c = 0; c < CH; c += 4) {
+        const f4 x = *reinterpret_cast<const f4*>(row + c);
+        am = fmaxf(am, fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3]))));
+      }
+      am = group_max<4>(am);
+      if ((tid & 3) == 0) {
+        constexpr float q = (float)((1 << (BITS - 1)) - 1);
+        const float sc = bf16_to_f32(f32_to_bf16_bits(am / q));
+        if (r < 32) kmeta[r] = sc;
+        else vmeta[r - 32] = sc;
+      }
     }
-  } else if (tid < 64) {
-    om[tid] = f32_to_bf16_bits(tid < 32 ? kmeta[tid] : vmeta[tid - 32]);
+    __syncthreads();
+
+    // ---- codes: whole 32-bit words ----
+    uint32_t* ow = reinterpret_cast<uint32_t*>(out);
+    constexpr int cb = 4 * D * BITS;          // bytes per code region
+    constexpr int lane_bytes_k = D * BITS / 32;
+    constexpr int lane_bytes_v = D * BITS / 16;
+    constexpr int nslot = 32 / BITS;          // codes per word
+    for (int wi = tid; wi < 2 * cb / 4; wi += 256) {
+      const bool isv = wi >= cb / 4;
+      const int wb = 4 * (isv ? wi - cb / 4 : wi);  // byte offset inside the region
+      int lam, r2, tau = 0;  // lane and byte of its share held by this word
+      if (!isv) {
+        tau = wb / (2 * D * BITS);
+        share_of(lane_bytes_k, wb % (2 * D * BITS), lam, r2);
+      } else {
+        share_of(lane_bytes_v, wb, lam, r2);
+      }
+      const int i = lam & 15, kg = lam >> 4;
+      // the chunk x and first slot s0 of the word's codes
+      int x0, s0;
+      if constexpr (BITS == 8) { x0 = r2 / 8; s0 = 4 * ((r2 % 8) / 4); }
+      else if constexpr (BITS == 4) { x0 = r2 / 4; s0 = 0; }
+      else { x0 = r2 / 2; s0 = 0; }
+      uint32_t word = 0;
+#pragma unroll
+      for (int qq = 0; qq < nslot; ++qq) {
+        int x, sl, bit;
+        if constexpr (BITS == 8) { x = x0; sl = s0 + qq; bit = 8 * qq; }
+        else if constexpr (BITS == 4) { x = x0; sl = qq; bit = 16 * (sl & 1) + 4 * (sl >> 1); }
+        else { x = x0 + (qq >> 3); sl = qq & 7; bit = 16 * (sl & 1) + 2 * (sl >> 1) + 8 * (qq >> 3); }
+        uint32_t u;
+        if (!isv) {
+          const int t = 16 * tau + i, c = 32 * x + 8 * kg + sl;
+          const float xv = Ks[t * LD + c];
+          if constexpr (KIVI) u = kivi_code(xv, kmeta[c], kmeta[D + c], levels);
+          else u = sym_code(xv, kmeta[t], BITS);
+        } else {
+          const int c = 16 * x + i, t = 16 * (sl >> 2) + 4 * kg + (sl & 3);
+          const float xv = Vs[t * LD + c];
+          if constexpr (KIVI) {
+            const int g = c >> 5;
+            u = kivi_code(xv, vmeta[2 * (t * (D / 32) + g)], vmeta[2 * (t * (D / 32) + g) + 1], levels);
+          } else {
+            u = sym_code(xv, vmeta[t], BITS);
+          }
+        }
+        word |= u << bit;
+      }
+      ow[wi] = word;
+    }
+
+    // ---- metadata stores ----
+    uint16_t* om = reinterpret_cast<uint16_t*>(out + 2 * cb);
+    if constexpr (KIVI) {
+      for (int idx = tid; idx < 4 * D; idx += 256) {
+        float val;
+        if (idx < 2 * D) {
+          val = kmeta[idx];  // scale[0..D) then zero[0..D)
+        } else {
+          const int e = idx - 2 * D;  // ((g*2 + w)*4 + kg)*8 + s
+          const int sl = e & 7, kg = (e >> 3) & 3, w = (e >> 5) & 1, g = e >> 6;
+          const int t = 16 * (sl >> 2) + 4 * kg + (sl & 3);
+          val = vmeta[2 * (t * (D / 32) + g) + w];
+        }
+        om[idx] = bitcast<uint16_t>((_Float16)val);  // exact: the value is an fp16
+      }
+    } else if (tid < 64) {
+      om[tid] = f32_to_bf16_bits(tid < 32 ? kmeta[tid] : vmeta[tid - 32]);
+    }
   }
 }
 
@@ -297,9 +361,9 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
   if (!evict && keep_idx) return fail(KVK_ERR_INVALID, "the table does not evict: keep_idx must be NULL");
   if (evict && n_tokens < d.keep_tokens)
     return fail(KVK_ERR_INVALID, "n_tokens %d < keep_tokens %d", n_tokens, d.keep_tokens);
-  if ((reinterpret_cast<uintptr_t>(arena) & 15) || (reinterpret_cast<uintptr_t>(k) & 3) ||
-      (reinterpret_cast<uintptr_t>(v) & 3))
-    return fail(KVK_ERR_INVALID, "misaligned buffer");
+  if ((reinterpret_cast<uintptr_t>(arena) & 15) || (reinterpret_cast<uintptr_t>(k) & 15) ||
+      (reinterpret_cast<uintptr_t>(v) & 15))
+    return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
   if (d.kind == KVK_MLA)
     return mla_compress_layer(t, layer, k, v, in_dtype, n_tokens, keep_idx, arena, stream);
 
@@ -321,10 +385,19 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
   const int64_t nstreams = (int64_t)d.batch * d.n_kv_heads;
   const int64_t grid = nstreams * (a.nbf + 1);
   if (grid > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "grid too large");
-  if (d.head_dim == 128)
-    hipLaunchKernelGGL(compress_kernel<128>, dim3((unsigned)grid), dim3(256), 0, stream, a);
-  else
-    hipLaunchKernelGGL(compress_kernel<64>, dim3((unsigned)grid), dim3(256), 0, stream, a);
+  const dim3 g3((unsigned)grid), b3(256);
+#define KVK_W1(DD, BB, KK) \
+  if (d.head_dim == DD && a.bits == BB && (BB == 16 || a.kivi == (KK ? 1 : 0))) { \
+    hipLaunchKernelGGL((compress_kernel<DD, BB, KK>), g3, b3, 0, stream, a); \
+    launched = true; \
+  }
+  bool launched = false;
+  KVK_W1(128, 16, true) else KVK_W1(128, 8, true) else KVK_W1(128, 4, true) else KVK_W1(128, 2, true)
+  else KVK_W1(128, 8, false) else KVK_W1(128, 4, false) else KVK_W1(128, 2, false)
+  else KVK_W1(64, 16, true) else KVK_W1(64, 8, true) else KVK_W1(64, 4, true) else KVK_W1(64, 2, true)
+  else KVK_W1(64, 8, false) else KVK_W1(64, 4, false) else KVK_W1(64, 2, false)
+#undef KVK_W1
+  if (!launched) return fail(KVK_ERR_UNSUPPORTED, "no write kernel for d_h %d, %d bits", d.head_dim, a.bits);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "compress launch: %s", hipGetErrorString(e));
   return KVK_OK;
