@@ -107,122 +107,140 @@ __device__ __forceinline__ MlaSlot mla_slot(int n, int NK) {
   return {16 * T + (n & 15), 32 * (kq - T * NK) + 8 * ((n >> 4) & 3)};
 }
 
-// One workgroup per (32-token block, sequence): stage the block's stored channels
-// (latent[:d] then k^R) in LDS as fp32, compute the metadata, then assemble whole
-// 32-bit code words (coalesced stores).
+// The 8 stored channels c0 .. c0+7 of block row t (zeros past the stored tokens).
+__device__ __forceinline__ void mla_load8(const MlaCompressArgs& a, int b, int tok0, int ntok, int t, int c0,
+                                          float (&x)[8]) {
+  if (t >= ntok) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+    return;
+  }
+  int pos = tok0 + t;
+  if (a.keep) {
+    pos = a.keep[(int64_t)b * a.n_stored + pos];
+    pos = pos < 0 ? 0 : (pos >= a.n_tokens ? a.n_tokens - 1 : pos);
+  }
+  const int64_t row = (int64_t)b * a.n_tokens + pos;
+  const void* src = c0 < a.d ? a.latent : a.rope;
+  const int64_t e0 = c0 < a.d ? row * a.r + c0 : row * kRope + (c0 - a.d);
+  if (a.in_f32) {
+    const f4* p = reinterpret_cast<const f4*>(static_cast<const float*>(src) + e0);
+    const f4 lo = p[0], hi = p[1];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[e] = lo[e], x[4 + e] = hi[e];
+  } else {
+    const u4v w = *reinterpret_cast<const u4v*>(static_cast<const uint16_t*>(src) + e0);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(w[e] << 16);
+      x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  }
+}
+
+// One workgroup per (32-token block, sequence).  Each wave takes (tile T, k-step K)
+// tasks: lane (i, g) moves the 8 channels 32 K + 8 g .. + 7 of block row 16 T + i,
+// i.e. exactly slot (T NK + K) 64 + i + 16 g, so loads and stores need no staging.
+// KIVI32 groups (32 channels of one token) are the 4 lanes i, i + 16, i + 32, i + 48;
+// SYMROW scales (one per token and vector) come from a first pass through LDS.
+template <int BITS, bool KIVI>
 __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
 #pragma clang fp contract(off)
-  constexpr int LD = kMaxW + 1;
-  __shared__ float X[32 * LD];
-  __shared__ float gs[32 * (kMaxW / 32)];  // KIVI32 scale / SYMROW group max|x|
-  __shared__ float gz[32 * (kMaxW / 32)];  // KIVI32 zero
-  __shared__ float ssc[64];                // SYMROW: scale of (token, latent|rope)
-  const int tid = threadIdx.x;
+  __shared__ uint32_t amax[2][32];  // SYMROW: max |x| bits of (c[:d] | k^R, token)
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, i = lane & 15, g = lane >> 4;
   const int blk = blockIdx.x, b = blockIdx.y;
   const bool tail = blk == a.nbf;
   const int tok0 = 32 * blk;
   const int ntok = tail ? a.n_stored - tok0 : 32;
-  const int d = a.d, W = d + kRope, G = W / 32;
-
-  for (int idx = tid; idx < 32 * W; idx += 256) {
-    const int t = idx / W, c = idx - t * W;
-    float x = 0.0f;
-    if (t < ntok) {
-      int pos = tok0 + t;
-      if (a.keep) {
-        pos = a.keep[(int64_t)b * a.n_stored + pos];
-        pos = pos < 0 ? 0 : (pos >= a.n_tokens ? a.n_tokens - 1 : pos);
-      }
-      const int64_t row = (int64_t)b * a.n_tokens + pos;
-      x = c < d ? load_in(a.latent, a.in_f32, row * a.r + c)
-                : load_in(a.rope, a.in_f32, row * kRope + (c - d));
-    }
-    X[t * LD + c] = x;
-  }
-  __syncthreads();
-
+  const int d = a.d, W = d + kRope, NK = W / 32;
   uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
                  (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
-  if (tail || a.bits == 16) {  // bf16 block: 16 bytes (8 channels) per slot
-    uint32_t* o = reinterpret_cast<uint32_t*>(out);
-    for (int idx = tid; idx < 16 * W; idx += 256) {
-      const MlaSlot q = mla_slot(idx >> 2, G);
-      const int t = q.t, c = q.c + 2 * (idx & 3);
-      o[idx] = (uint32_t)bf16_bits_rne(X[t * LD + c]) | ((uint32_t)bf16_bits_rne(X[t * LD + c + 1]) << 16);
+
+  if (BITS == 16 || tail) {  // bf16 block: 16 bytes (8 channels) per slot
+    for (int task = wv; task < 2 * NK; task += 4) {
+      const int T = task / NK, K = task - T * NK;
+      float x[8];
+      mla_load8(a, b, tok0, ntok, 16 * T + i, 32 * K + 8 * g, x);
+      u4v o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[e] = (uint32_t)bf16_bits_rne(x[2 * e]) | ((uint32_t)bf16_bits_rne(x[2 * e + 1]) << 16);
+      *reinterpret_cast<u4v*>(out + 16 * ((T * NK + K) * 64 + i + 16 * g)) = o;
     }
     return;
   }
-
-  const int bits = a.bits;
-  const float levels = (float)((1 << bits) - 1);
-  const int cb = 4 * W * bits;  // code bytes of the block
-  for (int p = tid; p < 32 * G; p += 256) {  // (token, group of 32 stored channels)
-    const int t = p / G, g = p - t * G;
-    const float* row = &X[t * LD + 32 * g];
-    float mn = row[0], mx = row[0], am = fabsf(row[0]);
-    for (int c = 1; c < 32; ++c) {
-      mn = fminf(mn, row[c]);
-      mx = fmaxf(mx, row[c]);
-      am = fmaxf(am, fabsf(row[c]));
-    }
-    if (a.kivi) {
-      const _Float16 sh = (_Float16)((mx - mn) / levels);
-      const _Float16 zh = (_Float16)mn;
-      gs[p] = (float)sh;
-      gz[p] = (float)zh;
-      reinterpret_cast<uint32_t*>(out + cb)[((t >> 4) * G + g) * 16 + (t & 15)] =
-          (uint32_t)bitcast<uint16_t>(sh) | ((uint32_t)bitcast<uint16_t>(zh) << 16);
-    } else {
-      gs[p] = am;
-    }
-  }
-  __syncthreads();
-  if (!a.kivi) {
-    if (tid < 64) {  // one scale per stored vector: c[:d] (part 0) and k^R (part 1)
-      const int t = tid >> 1, part = tid & 1;
-      const int g0 = part ? d / 32 : 0, g1 = part ? G : d / 32;
-      float am = 0.0f;
-      for (int g = g0; g < g1; ++g) am = fmaxf(am, gs[t * G + g]);
-      const float q = (float)((1 << (bits - 1)) - 1);
-      const uint16_t sb = bf16_bits_rne(am / q);
-      ssc[tid] = bf16_to_f32(sb);
-      reinterpret_cast<uint16_t*>(out + cb)[tid] = sb;  // byte 4t + 2 part
-    }
-    __syncthreads();
-  }
-  const int per = 32 / bits;  // codes per word
-  uint32_t* ow = reinterpret_cast<uint32_t*>(out);
-  for (int wi = tid; wi < W * bits; wi += 256) {
-    // the word's token and the channel of its first code (see mla_word)
-    int t, c0;
-    if (bits == 8) {
-      const MlaSlot q = mla_slot(wi >> 1, G);
-      t = q.t, c0 = q.c + 4 * (wi & 1);
-    } else if (bits == 4) {
-      const MlaSlot q = mla_slot(wi, G);
-      t = q.t, c0 = q.c;
-    } else {
-      const int kq = wi >> 5, T = kq / G;
-      t = 16 * T + ((wi >> 1) & 15), c0 = 32 * (kq - T * G) + 16 * (wi & 1);
-    }
-    uint32_t word = 0;
-    for (int k = 0; k < per; ++k) {
-      const int c = c0 + k;
-      const float x = X[t * LD + c];
-      uint32_t u;
-      if (a.kivi) {
-        const int p = t * G + (c >> 5);
-        u = kivi_code(x, gs[p], gz[p], levels);
-      } else {
-        u = sym_code(x, ssc[2 * t + (c >= d ? 1 : 0)], bits);
+  if constexpr (BITS != 16) {
+    constexpr float levels = (float)((1 << BITS) - 1);
+    constexpr int cb_per_w = 4 * BITS;  // code bytes of the block per stored channel
+    uint8_t* meta = out + cb_per_w * W;
+    if constexpr (!KIVI) {
+      if (tid < 64) amax[tid >> 5][tid & 31] = 0u;
+      __syncthreads();
+      for (int task = wv; task < 2 * NK; task += 4) {
+        const int T = task / NK, K = task - T * NK;
+        float x[8];
+        mla_load8(a, b, tok0, ntok, 16 * T + i, 32 * K + 8 * g, x);
+        float am = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) am = fmaxf(am, fabsf(x[e]));
+        am = rows_max(am);
+        if (g == 0) atomicMax(&amax[32 * K < d ? 0 : 1][16 * T + i], __float_as_uint(am));  // am >= 0
       }
-      int bit;
-      if (bits == 8) bit = 8 * k;
-      else if (bits == 4) bit = 16 * (k & 1) + 4 * (k >> 1);
-      else bit = 16 * (k & 1) + 2 * ((k & 7) >> 1) + 8 * (k >> 3);
-      word |= u << bit;
+      __syncthreads();
     }
-    ow[wi] = word;
+    for (int task = wv; task < 2 * NK; task += 4) {
+      const int T = task / NK, K = task - T * NK, t = 16 * T + i;
+      float x[8];
+      mla_load8(a, b, tok0, ntok, t, 32 * K + 8 * g, x);
+      uint32_t u[8];
+      if constexpr (KIVI) {
+        float mn = x[0], mx = x[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) mn = fminf(mn, x[e]), mx = fmaxf(mx, x[e]);
+        mn = rows_min(mn);
+        mx = rows_max(mx);
+        const _Float16 sh = (_Float16)((mx - mn) / levels);
+        const _Float16 zh = (_Float16)mn;
+        const float sc = (float)sh, zf = (float)zh;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) u[e] = kivi_code(x[e], sc, zf, levels);
+        if (g == 0)
+          *reinterpret_cast<uint32_t*>(meta + 4 * ((T * NK + K) * 16 + i)) =
+              (uint32_t)bitcast<uint16_t>(sh) | ((uint32_t)bitcast<uint16_t>(zh) << 16);
+      } else {
+        constexpr float q = (float)((1 << (BITS - 1)) - 1);
+        const float sc = bf16_to_f32(bf16_bits_rne(__uint_as_float(amax[32 * K < d ? 0 : 1][t]) / q));
+#pragma unroll
+        for (int e = 0; e < 8; ++e) u[e] = sym_code(x[e], sc, BITS);
+      }
+      const int S = (T * NK + K) * 64 + i + 16 * g;
+      if constexpr (BITS == 8) {
+        uint32_t w0 = 0, w1 = 0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w0 |= u[e] << (8 * e), w1 |= u[4 + e] << (8 * e);
+        *reinterpret_cast<u2v*>(out + 8 * S) = u2v{w0, w1};
+      } else if constexpr (BITS == 4) {
+        uint32_t w = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) w |= u[e] << (16 * (e & 1) + 4 * (e >> 1));
+        *reinterpret_cast<uint32_t*>(out + 4 * S) = w;
+      } else {
+        uint32_t w = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) w |= u[e] << (16 * (e & 1) + 2 * (e >> 1) + 8 * (g & 1));
+        // sub-groups 2y and 2y + 1 (lanes 16 apart) share one word
+        const auto sw = __builtin_amdgcn_permlane16_swap(w, w, false, false);
+        w = sw[0] | sw[1];
+        if ((g & 1) == 0) *reinterpret_cast<uint32_t*>(out + 4 * (((T * NK + K) * 16 + i) * 2 + (g >> 1))) = w;
+      }
+    }
+    if constexpr (!KIVI) {
+      if (tid < 64) {  // per token: the bf16 scale of c[:d] at byte 4t, of k^R at 4t + 2
+        const int t = tid >> 1, part = tid & 1;
+        constexpr float q = (float)((1 << (BITS - 1)) - 1);
+        reinterpret_cast<uint16_t*>(meta)[tid] = bf16_bits_rne(__uint_as_float(amax[part][t]) / q);
+      }
+    }
   }
 }
 
@@ -898,8 +916,14 @@ kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* lat
   a.d = t->rank[layer];
   a.bits = t->bits[layer];
   a.kivi = d.qscheme == KVK_Q_KIVI32;
-  hipLaunchKernelGGL(mla_compress_kernel, dim3((unsigned)(a.nbf + 1), (unsigned)d.batch), dim3(256), 0,
-                     stream, a);
+  const dim3 g3((unsigned)(a.nbf + 1), (unsigned)d.batch), b3(256);
+  if (a.bits == 16) hipLaunchKernelGGL((mla_compress_kernel<16, true>), g3, b3, 0, stream, a);
+  else if (a.kivi && a.bits == 8) hipLaunchKernelGGL((mla_compress_kernel<8, true>), g3, b3, 0, stream, a);
+  else if (a.kivi && a.bits == 4) hipLaunchKernelGGL((mla_compress_kernel<4, true>), g3, b3, 0, stream, a);
+  else if (a.kivi) hipLaunchKernelGGL((mla_compress_kernel<2, true>), g3, b3, 0, stream, a);
+  else if (a.bits == 8) hipLaunchKernelGGL((mla_compress_kernel<8, false>), g3, b3, 0, stream, a);
+  else if (a.bits == 4) hipLaunchKernelGGL((mla_compress_kernel<4, false>), g3, b3, 0, stream, a);
+  else hipLaunchKernelGGL((mla_compress_kernel<2, false>), g3, b3, 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA compress launch: %s", hipGetErrorString(e));
   return KVK_OK;
