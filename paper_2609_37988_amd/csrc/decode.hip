@@ -799,6 +799,40 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
     ca.layer_item[l - l0] = ii;
     ca.layer_slot0[l - l0] = (l - l0 - a.items[ii].q_layer0) * G;
   }
+  // Launch order: the waves that take longest per split (the low-bit items, whose
+  // unpacking makes them compute-bound) first, so that the launch ends on short
+  // waves.  Item indices follow the new order; wave_begin stays increasing.
+  {
+    auto cost_rank = [](int bits) { return bits == 2 ? 0 : (bits == 4 ? 1 : (bits == 8 ? 2 : 3)); };
+    int order[kMaxItems], n_it = a.n_items;
+    for (int k = 0; k < n_it; ++k) order[k] = k;
+    for (int k = 1; k < n_it; ++k)  // stable insertion sort by cost rank
+      for (int m = k; m > 0 && cost_rank(a.items[order[m]].bits) < cost_rank(a.items[order[m - 1]].bits); --m) {
+        const int tmp = order[m];
+        order[m] = order[m - 1];
+        order[m - 1] = tmp;
+      }
+    DecodeItem sorted[kMaxItems];
+    int new_index[kMaxItems];
+    int64_t wv = 0;
+    for (int k = 0; k < n_it; ++k) {
+      DecodeItem it = a.items[order[k]];
+      wv = (wv + 3) / 4 * 4;
+      const int64_t nw = (int64_t)d.batch * d.n_kv_heads * it.nsplit * it.nchp;
+      it.wave_begin = (int32_t)wv;
+      wv += nw;
+      sorted[k] = it;
+      new_index[order[k]] = k;
+      ca.item_ws_off[k] = it.ws_off;
+      ca.item_nsplit[k] = it.nsplit;
+      ca.item_geff[k] = it.geff;
+      ca.item_tail[k] = it.region + (int64_t)t->nb_cap * it.block_bytes;
+      ca.item_stream_bytes[k] = it.stream_bytes;
+    }
+    for (int k = 0; k < n_it; ++k) a.items[k] = sorted[k];
+    for (int l = l0; l < l1; ++l) ca.layer_item[l - l0] = new_index[ca.layer_item[l - l0]];
+    waves = wv;
+  }
   if ((size_t)ws_floats * sizeof(float) > ws_bytes)
     return fail(KVK_ERR_BUFFER, "workspace %zu bytes < %lld needed", ws_bytes,
                 (long long)(ws_floats * sizeof(float)));
