@@ -762,6 +762,7 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   ca.n_layers = l1 - l0;
   ca.n_rows = (l1 - l0) * d.batch * d.n_q_heads;
 
+  const int64_t split_target = gqa_split_target(t, l0, l1);
   // One work item per distinct anchor read by the range (§2.1 depth sharing).
   int item_of_anchor[KVK_MAX_LAYERS];
   for (int l = 0; l < KVK_MAX_LAYERS; ++l) item_of_anchor[l] = -1;
@@ -779,7 +780,7 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
       it.bits = t->bits[anc];
       it.q_layer0 = rb - l0;
       it.geff = G * (re - rb);
-      it.split_blocks = split_blocks_for(it.bits, d.qscheme, D, nbf);
+      it.split_blocks = split_blocks_for(it.bits, d.qscheme, D, nbf, split_target);
       it.nsplit = n_splits(nbf, it.split_blocks);
       const int nch = (it.geff + 15) / 16;
       it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : 4);

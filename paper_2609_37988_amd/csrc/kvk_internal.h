@@ -37,7 +37,9 @@ int32_t ring_depth_for(int32_t bits);
 // Blocks processed per split of the decode kernel for a `bits`-bit anchor whose
 // streams hold n_blocks full blocks.  The split count never exceeds the one at a
 // larger n_blocks, so workspace sized at capacity covers every n_stored.
-int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks);
+int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes);
+// Bytes per D1 split for a decode over layers [l0, l1) of a GQA table (see table.cpp).
+int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1);
 
 // Number of decode splits of one stream holding `n_blocks` blocks.
 inline int32_t n_splits(int32_t n_blocks, int32_t split_blocks) {

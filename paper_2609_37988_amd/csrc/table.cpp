@@ -46,18 +46,38 @@ int32_t ring_depth_for(int32_t bits) {
   return bits == 16 ? 2 : (bits == 8 ? 2 : (bits == 4 ? 4 : 6));
 }
 
-int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks) {
-  // About 1 MiB of cache per wave: a wave pays one memory latency to start, so
-  // longer splits amortise it (and the split partial); the stream's blocks are
+int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1) {
+  // A wave pays its start (query, filling its prefetch ring) and its split
+  // partial once, so splits are as long as the launch allows while it still has
+  // about kSplitWaves waves: two rounds of the D1 wave slots of an MI355X (256 CUs
+  // x 8 waves).  Measured on the 14B mixed stack: 1 MiB splits 3.54 ms, 2 MiB 3.44,
+  // one split per stream (<= 4 MiB) 3.35.  Between 1 MiB and 16 MiB; computed from
+  // the capacity, so the workspace size bounds every n_stored.
+  constexpr int64_t kSplitWaves = 4096;
+  bool seen[KVK_MAX_LAYERS] = {};
+  int64_t total = 0;
+  for (int l = l0; l < l1; ++l) {
+    const int32_t a = t->info.anchor_of[l];
+    if (seen[a]) continue;
+    seen[a] = true;
+    total += (int64_t)t->d.batch * t->d.n_kv_heads * t->nb_cap * t->block_bytes[a];
+  }
+  int64_t target = total / kSplitWaves;
+  if (target < (1LL << 20)) target = 1LL << 20;
+  if (target > (16LL << 20)) target = 16LL << 20;
+  return target;
+}
+
+int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes) {
+  // target_bytes of cache per wave (gqa_split_target); the stream's blocks are
   // divided evenly so that no split is a short remainder, in a multiple of the
   // decode kernel's prefetch depth so that only a stream's last split runs past
   // its end.
-#ifndef KVK_SPLIT_TARGET
-#define KVK_SPLIT_TARGET (1024 * 1024)
-#endif
   const int64_t bb = gqa_block_bytes(head_dim, bits, qscheme);
   const int64_t nr = ring_depth_for(bits);
-  int64_t target = KVK_SPLIT_TARGET / bb;
+  // The 2- and 4-bit paths are bound by their unpacking, not by the stream: longer
+  // splits do not pay there (14B eviction stack: 1 MiB 1.14 ms, 1.1 MiB 1.17 ms).
+  int64_t target = (bits <= 4 ? (1LL << 20) : target_bytes) / bb;
   if (target < nr) target = nr;
   const int64_t nb = n_blocks > 0 ? n_blocks : 1;
   const int64_t nsplit = (nb + target - 1) / target;
@@ -290,10 +310,11 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
   const int32_t G = d.n_q_heads / d.n_kv_heads;
   // Split partials: per query row (layer, b, head) and split, (o[d_h], m, l, 2 pad) in fp32.
   const int32_t nblk = t->nb_cap;  // full blocks; the tail is merged by the combine kernel
+  const int64_t target = gqa_split_target(t, l0, l1);
   size_t floats = 0;
   for (int l = l0; l < l1; ++l) {
     const int32_t a = t->info.anchor_of[l];
-    const int32_t sb = split_blocks_for(t->bits[a], d.qscheme, d.head_dim, nblk);
+    const int32_t sb = split_blocks_for(t->bits[a], d.qscheme, d.head_dim, nblk, target);
     floats += (size_t)d.batch * d.n_kv_heads * G * n_splits(nblk, sb) * (d.head_dim + 4);
   }
   *out = (size_t)round256((int64_t)(floats * sizeof(float)));
