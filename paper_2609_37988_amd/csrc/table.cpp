@@ -105,7 +105,9 @@ int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_block
   const int32_t W = t->rank[anchor] + t->d.rope_dim;
   const int64_t nr = (int64_t)mla_ring_depth(W, t->bits[anchor], t->d.qscheme == KVK_Q_KIVI32) *
                      mla_iter_blocks(W);  // blocks per pass of the ring
-  int64_t target = KVK_MLA_SPLIT_UNITS / (W + 192);
+  // bf16 streams are bound by HBM and take twice as long splits (fewer workgroup
+  // starts: MLA stack 0.96 -> 0.93 ms); the dequantising paths keep the shorter ones.
+  int64_t target = (t->bits[anchor] == 16 ? 2 : 1) * (int64_t)KVK_MLA_SPLIT_UNITS / (W + 192);
   if (target < nr) target = nr;
   const int64_t nb = n_blocks > 0 ? n_blocks : 1;
   if (target * kMlaMaxUnits < nb) target = (nb + kMlaMaxUnits - 1) / kMlaMaxUnits;  // merge limit
