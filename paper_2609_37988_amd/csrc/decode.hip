@@ -371,18 +371,32 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
     for (int e = 0; e < 4; ++e) x[4 * tau + e] = valid ? acc[tau][e] + zt[e] : -INFINITY;
   softmax_update<D, D / 32>(u, ex, x);
   const half8 p = to_half8(x);
-  // V: o_c = sum_t (p_t s_tg) u_tc + sum_t p_t z_tg, g = c / 32.
+  // V: o_c = sum_t (p_t s_tg) u_tc + sum_t p_t z_tg, g = c / 32.  At 2 and 4 bits
+  // the value codes enter raw (1024 + u / c per slot, raw_codes), the probabilities
+  // carry the slot factors c, and 1024 sum_t c_t p_t s_tg comes off in the same
+  // block through one more product per channel tile, so the accumulators never hold
+  // the 1024 offset across blocks (fp32 rounding stays relative to the block's own
+  // mass).  At 8 bits the unpacking fix-up is cheap and the path is bound by HBM.
   const half8* vmeta = kmeta + D / 4;
+  const half8 pc = BITS == 8 ? p : p * raw_factors<BITS>();
+  const _Float16 m1024 = (_Float16)-1024.0f;
+  const half8 neg = {m1024, m1024, m1024, m1024, m1024, m1024, m1024, m1024};
 #pragma unroll
   for (int g = 0; g < NG; ++g) {
     const half8 vs = vmeta[(g * 2 + 0) * 4 + kg];
     const half8 vz = vmeta[(g * 2 + 1) * 4 + kg];
-    const half8 ps = p * vs;
+    const half8 ps = pc * vs;
     ex.zo[g] = mfma16(vz, p, ex.zo[g]);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int mt = 2 * g + h;
-      u.o[mt] = mfma16(unpack_chunk<BITS>(r.v, mt, 0.0f), ps, u.o[mt]);
+      if constexpr (BITS == 8) {
+        u.o[mt] = mfma16(unpack_chunk<BITS>(r.v, mt, 0.0f), ps, u.o[mt]);
+      } else {
+        const uint32_t w0 = BITS == 4 ? r.v[mt] : r.v[mt >> 1] >> (8 * (mt & 1));
+        u.o[mt] = mfma16(neg, ps, u.o[mt]);
+        u.o[mt] = mfma16(raw_codes<BITS>(w0, 0u), ps, u.o[mt]);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
   }

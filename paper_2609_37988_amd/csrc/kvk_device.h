@@ -47,6 +47,41 @@ __device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
 
 // b = 4: one 32-bit chunk, slot s at bit 16*(s%2) + 4*(s/2).  Returns the 8 codes
 // minus `off` as exact fp16 integers, slot pairs (0,1),(2,3),(4,5),(6,7).
+// The and_or halves of the unpackers above without their fix-up: slot s holds
+// 1024 + u_s / c_s exactly, with the slot factors c = raw_factors<BITS>() (powers
+// of two).  A product over the slots then needs its other operand scaled by c and
+// 1024 times that operand's slot sum taken off.
+template <int BITS>
+__device__ __forceinline__ half8 raw_codes(uint32_t w0, uint32_t w1) {
+  if constexpr (BITS == 8) {
+    const uint32_t M = 0x64646464u;
+    return cat4(bitcast<half2v>(__builtin_amdgcn_perm(M, w0, 0x04010400u)),
+                bitcast<half2v>(__builtin_amdgcn_perm(M, w0, 0x04030402u)),
+                bitcast<half2v>(__builtin_amdgcn_perm(M, w1, 0x04010400u)),
+                bitcast<half2v>(__builtin_amdgcn_perm(M, w1, 0x04030402u)));
+  } else if constexpr (BITS == 4) {
+    const uint32_t w8 = w0 >> 8;
+    return cat4(bitcast<half2v>(and_or(w0, 0x000F000Fu, kMagic)), bitcast<half2v>(and_or(w0, 0x00F000F0u, kMagic)),
+                bitcast<half2v>(and_or(w8, 0x000F000Fu, kMagic)), bitcast<half2v>(and_or(w8, 0x00F000F0u, kMagic)));
+  } else {
+    return cat4(bitcast<half2v>(and_or(w0, 0x00030003u, kMagic)), bitcast<half2v>(and_or(w0, 0x000C000Cu, kMagic)),
+                bitcast<half2v>(and_or(w0, 0x00300030u, kMagic)), bitcast<half2v>(and_or(w0, 0x00C000C0u, kMagic)));
+  }
+}
+template <int BITS>
+__device__ __forceinline__ half8 raw_factors() {
+  const _Float16 one = (_Float16)1.0f;
+  if constexpr (BITS == 8) {
+    return half8{one, one, one, one, one, one, one, one};
+  } else if constexpr (BITS == 4) {
+    const _Float16 s = (_Float16)0.0625f;
+    return half8{one, one, s, s, one, one, s, s};
+  } else {
+    return half8{one, one, (_Float16)0.25f, (_Float16)0.25f, (_Float16)0.0625f, (_Float16)0.0625f,
+                 (_Float16)0.015625f, (_Float16)0.015625f};
+  }
+}
+
 __device__ __forceinline__ half8 unpack4(uint32_t w, float off) {
   const uint32_t w8 = w >> 8;
   half2v a = bitcast<half2v>(and_or(w, 0x000F000Fu, kMagic));   // 1024 + u
