@@ -160,6 +160,8 @@ def test_entry_points_reject_bad_arguments_without_launching():
     _raw(I, "kvk_compress_layer", h, 0, None, f, kvk.BF16, 64, None, f, None)  # NULL input
     _raw(I, "kvk_compress_layer", h, 0, f, f, 7, 64, None, f, None)            # dtype
     _raw(kvk.OK, "kvk_compress_layer", h, 1, f, f, kvk.BF16, 64, None, f, None)  # inheritor: no-op
+    _raw(I, "kvk_compress_layer", h, 0, P(264), f, kvk.BF16, 64, None, f, None)  # K not 16-byte aligned
+    _raw(I, "kvk_compress_layer", h, 0, f, P(260), kvk.BF16, 64, None, f, None)  # V not 16-byte aligned
     _raw(I, "kvk_decode_attention", h, 1, 1, f, kvk.BF16, 64, 0.1, None, None, f, f, f, 1 << 20, None)
     _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 65, 0.1, None, None, f, f, f, 1 << 20, None)
     _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, 0.1, f, None, f, f, f, 1 << 20, None)
@@ -271,4 +273,5 @@ def test_mla_entry_points_reject_bad_arguments_without_launching():
     _raw(B, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, 0.1, f, f, f, f, f, need - 1, None)
     _raw(B, "kvk_decode_splits", h, 0, 2, f, kvk.BF16, 64, 0.1, f, f, f, f, need - 1, None)
     _raw(I, "kvk_compress_layer", h, 0, f, f, kvk.BF16, 65, None, f, None)
+    _raw(I, "kvk_compress_layer", h, 0, Pv(264), f, kvk.BF16, 64, None, f, None)  # latent misaligned
     _raw(kvk.OK, "kvk_compress_layer", h, 1, f, f, kvk.BF16, 64, None, f, None)  # inheritor: no-op
