@@ -458,11 +458,11 @@ __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D 
   }
 }
 
-// Blocks kept in flight per wave (registers): about 8-16 KiB of cache ahead of use.
-// The host rounds split lengths to a multiple of this depth (kvk::ring_depth_for).
+// Blocks kept in flight per wave (registers); the host rounds split lengths to a
+// multiple of this depth.
 template <int BITS>
 constexpr int ring_depth() {
-  return BITS == 16 ? 2 : (BITS == 8 ? 2 : (BITS == 4 ? 4 : 6));
+  return kvk::gqa_ring_depth(BITS);
 }
 
 // The query as fp16 hi + lo (integer-code paths) and as bf16 hi + lo (bf16 blocks).

@@ -32,7 +32,11 @@ int64_t gqa_block_bytes(int32_t head_dim, int32_t bits, int32_t qscheme);
 
 // Blocks the decode kernel keeps in flight per wave for a `bits`-bit anchor
 // (must equal the kernel's ring depth).
-int32_t ring_depth_for(int32_t bits);
+// Blocks the GQA decode kernel keeps in flight per wave (registers), by bit-width:
+// about 8-16 KiB of cache ahead of use within the register budget of two waves per
+// SIMD.  Shared by the host (split lengths) and the kernel.
+constexpr int gqa_ring_depth(int bits) { return bits == 16 ? 2 : (bits == 8 ? 2 : (bits == 4 ? 4 : 6)); }
+inline int32_t ring_depth_for(int32_t bits) { return gqa_ring_depth(bits); }
 
 // Blocks processed per split of the decode kernel for a `bits`-bit anchor whose
 // streams hold n_blocks full blocks.  The split count never exceeds the one at a

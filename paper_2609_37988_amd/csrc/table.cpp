@@ -42,10 +42,6 @@ int64_t gqa_block_bytes(int32_t head_dim, int32_t bits, int32_t qscheme) {
   return 8 * D * bits + 128;                      // codes + bf16 row scales
 }
 
-int32_t ring_depth_for(int32_t bits) {
-  return bits == 16 ? 2 : (bits == 8 ? 2 : (bits == 4 ? 4 : 6));
-}
-
 int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1) {
   // A wave pays its start (query, filling its prefetch ring) and its split
   // partial once, so splits are as long as the launch allows while it still has
