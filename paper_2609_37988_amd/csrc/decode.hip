@@ -5,8 +5,8 @@
 // share an anchor are served together: their query rows are stacked so that the
 // anchor's bytes are read once per step.  Decode is bound by reading the cache
 // (§1), so the kernel streams each (sequence, KV head) stream once, split along
-// the context into pieces of about 1 MiB; a second kernel merges the splits by
-// log-sum-exp.
+// the context into pieces of 1-16 MiB (the split rule is in table.cpp); a second
+// kernel merges the splits by log-sum-exp.
 //
 // Work unit: one 64-lane wave per (anchor item, sequence, KV head, split).  The
 // query rows of the unit (G query heads x the layers that read the anchor, up to
