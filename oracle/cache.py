@@ -19,7 +19,8 @@ import numpy as np
 
 from . import attention as att
 from . import layout, quant
-from .plan import GROUP, KIVI32, Dims, anchor_of, arena_offsets, layer_bytes, stream_bytes
+from .plan import (GROUP, KIVI32, Dims, anchor_of, arena_offsets, block_bytes, layer_bytes, stream_bytes,
+                   tail_bytes)
 
 F32 = np.float32
 
@@ -87,6 +88,38 @@ def dequant_stream(dims: Dims, bits: int, stream: np.ndarray, n_stored: int):
     K = np.concatenate([kh.reshape(-1, D), quant.bf16_value(kt[0, :nt])])
     V = np.concatenate([vh.reshape(-1, D), quant.bf16_value(vt[0, :nt])])
     return K, V
+
+
+def append_token(dims: Dims, bits: int, stream: np.ndarray, n_stored: int, k_tok, v_tok) -> np.ndarray:
+    """Decode-time append of the token at position n_stored to one stream.
+
+    The plan holds for the whole generation (§2.3), so the stream keeps its
+    configuration.  The new token (key and value [D], rounded to bf16) goes to slot
+    n_stored % 32 of the bf16 tail, the window of recent tokens kept in full
+    precision (App. C.3).  When that slot is the last one, the 32 tail tokens form a
+    complete group: they are quantised from their bf16 values into full block
+    n_stored // 32 by the block quantiser of the prefill write, and the tail is
+    empty again.  Returns the new stream bytes (the input is not modified)."""
+    D = dims.head_dim
+    out = np.array(stream, dtype=np.uint8, copy=True)
+    blk = block_bytes(dims, bits)
+    t0 = (dims.stored_cap // GROUP) * blk
+    kt, vt = layout.unpack_bf16_blocks(out[None, t0:t0 + tail_bytes(dims)], D)
+    slot = n_stored % GROUP
+    kt[0, slot] = quant.bf16_bits(np.asarray(k_tok, F32))
+    vt[0, slot] = quant.bf16_bits(np.asarray(v_tok, F32))
+    if slot < GROUP - 1:
+        out[t0:t0 + tail_bytes(dims)] = layout.pack_bf16_blocks(kt, vt)[0]
+        return out
+    j = n_stored // GROUP
+    if bits == 16:
+        block = layout.pack_bf16_blocks(kt, vt)[0]
+    else:
+        Kg = quant.bf16_value(kt)  # [1, 32, D] fp32
+        Vg = quant.bf16_value(vt)
+        block = layout.pack_quant_blocks(dims, bits, quantise_blocks(dims, bits, Kg, Vg))[0]
+    out[j * blk:(j + 1) * blk] = block
+    return out
 
 
 def gather_kept(X: np.ndarray, keep: np.ndarray) -> np.ndarray:

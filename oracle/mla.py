@@ -238,6 +238,34 @@ def compress_stream(dims: Dims, bits: int, d: int, C: np.ndarray, R: np.ndarray)
     return out
 
 
+def append_token(dims: Dims, bits: int, d: int, stream: np.ndarray, n_stored: int, c_tok, r_tok) -> np.ndarray:
+    """Decode-time append of the token at position n_stored (latent c_tok [>= d],
+    positional key r_tok [d_R]) to one MLA stream, by the rule of the GQA append
+    (oracle.cache.append_token): the stored row [c[:d] ; k^R], rounded to bf16,
+    enters tail slot n_stored % 32, and the token that fills the tail completes a
+    group that is written, from its bf16 rows, as full block n_stored // 32.
+    Returns the new stream bytes (the input is not modified)."""
+    W = d + dims.rope_dim
+    out = np.array(stream, dtype=np.uint8, copy=True)
+    blk = block_bytes(dims, bits, d)
+    t0 = (dims.stored_cap // GROUP) * blk
+    tb = tail_bytes(dims, d)
+    tail = unpack_bf16_block(out[None, t0:t0 + tb], W)  # [1, 32, W] bf16 patterns
+    slot = n_stored % GROUP
+    row = np.concatenate([np.asarray(c_tok, F32)[:d], np.asarray(r_tok, F32)])
+    tail[0, slot] = quant.bf16_bits(row)
+    if slot < GROUP - 1:
+        out[t0:t0 + tb] = pack_bf16_block(tail)[0]
+        return out
+    j = n_stored // GROUP
+    if bits == 16:
+        block = pack_bf16_block(tail)[0]
+    else:
+        block = pack_quant_blocks(dims, bits, quantise_rows(dims, bits, d, quant.bf16_value(tail)))[0]
+    out[j * blk:(j + 1) * blk] = block
+    return out
+
+
 def dequant_stream(dims: Dims, bits: int, d: int, stream: np.ndarray, n_stored: int):
     """Stream bytes -> (C_hat [n_stored, d], R_hat [n_stored, d_R]) fp32."""
     W = d + dims.rope_dim
