@@ -9,7 +9,9 @@ of that shape (keys with per-channel log-normal outliers).
 A step is one decode step over all 48 layers: the split attention kernel (D1)
 and the log-sum-exp merge (C1).  The cache is written once beforehand by the
 prefill kernel (W1), which is timed separately and reported under
-"prefill_write".  `value` is algorithmic compressed-cache bytes read per step
+"prefill_write"; the decode-time append of one token to every layer (the tail
+write, and every 32nd token the group write) is timed after the decode steps and
+reported under "append".  `value` is algorithmic compressed-cache bytes read per step
 (each distinct anchor once) divided by the step time, with everything resident
 in HBM.  The CPU baseline is the oracle (test infrastructure) timed on a bounded
 sample of the same workload.
@@ -59,6 +61,32 @@ TRAFFIC = {
     (3, None): ("mla_decode_32l_bf16_traffic.json", MLA_SOURCES),
     (3, "int4"): ("mla_decode_32l_int4_traffic.json", MLA_SOURCES),
 }
+
+
+def time_append(kvk, torch, table, n_layers, arena, n_stored, k_shape, v_shape, dev):
+    """Decode-time append of one token to every layer (one kvk_append_token call per
+    token), timed over the last 32-token group of the streams: positions
+    n_stored - 32 .. n_stored - 1, 31 tail writes then the write that completes the
+    group and quantises it into the last full block.  Runs after the decode timing
+    (it rewrites that block with new tokens)."""
+    if n_stored < 32:
+        return None
+    g = torch.Generator(device=dev)
+    g.manual_seed(77)
+    kn = torch.randn(k_shape, generator=g, device=dev).to(torch.bfloat16)
+    vn = torch.randn(v_shape, generator=g, device=dev).to(torch.bfloat16)
+    p0 = n_stored - 32
+    kvk.append_token(table, 0, n_layers, kn, vn, p0, arena)  # warm-up (a tail write)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(32)]
+    torch.cuda.synchronize()
+    for i in range(32):
+        ev[i][0].record()
+        kvk.append_token(table, 0, n_layers, kn, vn, p0 + i, arena)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    us = [a.elapsed_time(b) * 1e3 for a, b in ev]
+    return {"layers": n_layers, "us_tail_write": round(sum(us[:31]) / 31, 2), "us_group_write": round(us[31], 2),
+            "us_per_token": round(sum(us) / 32, 2)}
 
 
 def kernel_source_hash(sources=GQA_SOURCES) -> str:
@@ -281,6 +309,9 @@ def run_mla(args):
     if not args.no_cpu_baseline:
         cpu = cpu_baseline_mla(w, table, n_stored, scale, min(args.cpu_layers or 32, w.n_layers))
         log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
+    app = time_append(kvk, torch, table, w.n_layers, arena, n_stored, (w.n_layers, w.batch, w.latent_dim),
+                      (w.n_layers, w.batch, w.rope_dim), dev)
+    log(f"append: {app}")
     ranks = {}
     for e in w.plan:
         if not e[0]:
@@ -312,6 +343,7 @@ def run_mla(args):
         "cpu_baseline": cpu,
         "prefill_write": {"ms": round(w2_ms, 3), "bytes": w2_bytes,
                           "GB_per_s": round(w2_bytes / (w2_ms * 1e-3) / 1e9, 2)},
+        "append": app,
     }
     print(json.dumps(line), flush=True)
 
@@ -401,6 +433,10 @@ def main():
         nl = args.cpu_layers or (w.n_layers if args.config in (1, 2) else 4)
         cpu = cpu_baseline(w, table, n_stored, scale, nl, n_batch=2 if args.config in (1, 2) else 1)
         log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
+    app = time_append(kvk, torch, table, w.n_layers, arena, n_stored,
+                      (w.n_layers, w.batch, w.n_kv_heads, w.head_dim), (w.n_layers, w.batch, w.n_kv_heads, w.head_dim),
+                      dev)
+    log(f"append: {app}")
 
     bits_mix = {}
     for e in w.plan:
@@ -438,6 +474,7 @@ def main():
         "cpu_baseline": cpu,
         "prefill_write": {"ms": round(w1_ms, 3), "bytes": w1_bytes,
                           "GB_per_s": round(w1_bytes / (w1_ms * 1e-3) / 1e9, 2)},
+        "append": app,
     }
     print(json.dumps(line), flush=True)
 

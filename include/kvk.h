@@ -267,6 +267,38 @@ kvk_status kvk_compress_layer(const kvk_table* table, int32_t layer, const void*
                               int32_t in_dtype, int32_t n_tokens, const int32_t* keep_idx,
                               void* arena, hipStream_t stream);
 
+/* Decode-time append of one generated token to every anchor layer in
+ * [layer_begin, layer_end).  The plan chosen at prefill holds for the whole
+ * generation (§2.3), so each anchor keeps its configuration: the new token enters
+ * the stream's bf16 tail (the recent-token window that grouped quantisers keep in
+ * full precision, App. C.3), and the token that fills the tail completes a
+ * 32-token group, which is quantised into the next full block exactly as the
+ * prefill write quantises a block (keys per channel over the group's tokens,
+ * values per token).  The group is quantised from its bf16 values, so a stream
+ * built by appends equals the prefill write of the same tokens rounded to bf16.
+ * GQA:
+ *   k, v     : device [layer_end-layer_begin][B][Hkv][d_h], dtype in_dtype: the
+ *              new token's key and value per layer (rows of inheriting layers are
+ *              not read).
+ * MLA:
+ *   k        : the new latent, device [nl][B][r] (first d = rank coordinates used);
+ *   v        : the new positional key after RoPE, device [nl][B][d_R].
+ * Both:
+ *   n_stored : tokens stored per stream before the call (the new token's
+ *              position in the stream), 0 .. stored_tokens_cap - 1; the same for
+ *              every layer of the range.  Afterwards the streams hold n_stored + 1.
+ *   arena    : device; only the anchors' tails and, when n_stored % 32 == 31,
+ *              their full block n_stored / 32 are written.  Tail slots at and after
+ *              (n_stored + 1) % 32 are left undefined; nothing reads them.
+ * Under eviction the appended token is always kept (the keep list applies at
+ * prefill).  Layers that inherit an anchor outside the range see the new token
+ * only once that anchor's layer has been appended.
+ * Errors: KVK_ERR_INVALID (range, NULL pointers, dtype, n_stored + 1 beyond the
+ *         capacity, misalignment: k, v and arena 16 B), KVK_ERR_DEVICE. */
+kvk_status kvk_append_token(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
+                            const void* k, const void* v, int32_t in_dtype, int32_t n_stored,
+                            void* arena, hipStream_t stream);
+
 /* One decode step of attention for layers [layer_begin, layer_end) (§2.1): layer l
  * uses its own query and the cache of anchor_of[l].  Layers in the range that
  * share an anchor are served by one read of that anchor's bytes.

@@ -138,34 +138,13 @@ __device__ __forceinline__ float group_max(float x) {
   return x;
 }
 
-// One workgroup writes one 32-token block of one stream, with BITS-bit codes (or
-// bf16 at BITS = 16; a stream's tail block is always bf16).
+// Quantise the 32 tokens staged in LDS (Ks, Vs: fp32 rows of LD floats) into one
+// block of BITS-bit codes plus metadata at `out`.  Called by all 256 threads.
 template <int D, int BITS, bool KIVI>
-__global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
-  constexpr int LD = D + 4;  // padded LDS row (floats), rows 16-byte aligned
-  __shared__ float Ks[32 * LD];
-  __shared__ float Vs[32 * LD];
-  __shared__ float kmeta[2 * D];          // KIVI: scale, zero per channel; SYMROW: row scale
-  __shared__ float vmeta[2 * 32 * (D / 32)];
-
-  const int tid = threadIdx.x;
-  const int nblk = a.nbf + 1;
-  const int stream = blockIdx.x / nblk;
-  const int blk = blockIdx.x % nblk;
-  const bool tail = blk == a.nbf;
-  const int tok0 = blk * 32;
-  const int ntok = tail ? a.n_stored - tok0 : 32;  // valid tokens of this block
-
-  stage_block<D, LD>(a, stream, tok0, ntok, Ks, Vs, tid);
-  __syncthreads();
-
-  uint8_t* out = a.region + (int64_t)stream * a.stream_bytes +
-                 (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
-  if (BITS == 16 || tail) {
-    write_bf16_block<D, LD>(Ks, Vs, out, tid);
-    return;
-  }
-  if constexpr (BITS != 16) {
+__device__ __forceinline__ void write_quant_block(const float* Ks, const float* Vs, float* kmeta, float* vmeta,
+                                                  uint8_t* out, int tid) {
+  constexpr int LD = D + 4;
+  {
     constexpr float levels = (float)((1 << BITS) - 1);
 
     // ---- group metadata ----
@@ -297,6 +276,108 @@ __global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
   }
 }
 
+// One workgroup writes one 32-token block of one stream, with BITS-bit codes (or
+// bf16 at BITS = 16; a stream's tail block is always bf16).
+template <int D, int BITS, bool KIVI>
+__global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
+  constexpr int LD = D + 4;  // padded LDS row (floats), rows 16-byte aligned
+  __shared__ float Ks[32 * LD];
+  __shared__ float Vs[32 * LD];
+  __shared__ float kmeta[2 * D];          // KIVI: scale, zero per channel; SYMROW: row scale
+  __shared__ float vmeta[2 * 32 * (D / 32)];
+
+  const int tid = threadIdx.x;
+  const int nblk = a.nbf + 1;
+  const int stream = blockIdx.x / nblk;
+  const int blk = blockIdx.x % nblk;
+  const bool tail = blk == a.nbf;
+  const int tok0 = blk * 32;
+  const int ntok = tail ? a.n_stored - tok0 : 32;  // valid tokens of this block
+
+  stage_block<D, LD>(a, stream, tok0, ntok, Ks, Vs, tid);
+  __syncthreads();
+
+  uint8_t* out = a.region + (int64_t)stream * a.stream_bytes +
+                 (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
+  if (BITS == 16 || tail) {
+    write_bf16_block<D, LD>(Ks, Vs, out, tid);
+    return;
+  }
+  if constexpr (BITS != 16) write_quant_block<D, BITS, KIVI>(Ks, Vs, kmeta, vmeta, out, tid);
+}
+
+// Decode-time append of one token to every anchor of a layer range.
+struct AppendItem {
+  int64_t region;        // byte offset of the anchor's region in the arena
+  int32_t stream_bytes;
+  int32_t block_bytes;
+  int32_t bits;
+  int32_t row;           // the anchor's row in the new-token input (layer - layer_begin)
+};
+
+struct AppendArgs {
+  const void* k;         // [rows][B][Hkv][D] new keys
+  const void* v;         // [rows][B][Hkv][D] new values
+  uint8_t* arena;
+  int32_t in_f32;
+  int32_t pos;           // stored tokens before the call: the new token's position
+  int32_t nb_cap;
+  int32_t n_streams;     // B * Hkv
+  AppendItem items[KVK_MAX_LAYERS];
+};
+
+__device__ __forceinline__ uint16_t new_token_bf16(const void* p, int64_t e, int in_f32) {
+  return in_f32 ? f32_to_bf16_bits(static_cast<const float*>(p)[e]) : static_cast<const uint16_t*>(p)[e];
+}
+
+// One workgroup per (anchor, stream).  The token goes to slot pos % 32 of the bf16
+// tail block; the token that fills the tail instead completes a 32-token group,
+// which is quantised from the tail's bf16 values (plus the new token, rounded to
+// bf16) into full block pos / 32, exactly as the prefill write quantises a block.
+// The tail is then empty (its stale slots are never read).
+template <int D, bool KIVI>
+__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
+  constexpr int LD = D + 4;
+  __shared__ float Ks[32 * LD];
+  __shared__ float Vs[32 * LD];
+  __shared__ float kmeta[2 * D];
+  __shared__ float vmeta[2 * 32 * (D / 32)];
+  const int tid = threadIdx.x, sidx = blockIdx.x;
+  const AppendItem& it = a.items[blockIdx.y];
+  uint8_t* base = a.arena + it.region + (int64_t)sidx * it.stream_bytes;
+  uint8_t* tailb = base + (int64_t)a.nb_cap * it.block_bytes;
+  const int64_t e0 = ((int64_t)it.row * a.n_streams + sidx) * D;
+  const int t = a.pos & 31;
+  if (t != 31) {
+    for (int c = tid; c < D; c += 256) {
+      *reinterpret_cast<uint16_t*>(tailb + k_bf16_byte(D, t, c)) = new_token_bf16(a.k, e0 + c, a.in_f32);
+      *reinterpret_cast<uint16_t*>(tailb + v_bf16_byte(D, t, c)) = new_token_bf16(a.v, e0 + c, a.in_f32);
+    }
+    return;
+  }
+  for (int idx = tid; idx < 32 * D; idx += 256) {
+    const int tt = idx / D, c = idx % D;
+    uint16_t kb, vb;
+    if (tt < 31) {
+      kb = *reinterpret_cast<const uint16_t*>(tailb + k_bf16_byte(D, tt, c));
+      vb = *reinterpret_cast<const uint16_t*>(tailb + v_bf16_byte(D, tt, c));
+    } else {
+      kb = new_token_bf16(a.k, e0 + c, a.in_f32);
+      vb = new_token_bf16(a.v, e0 + c, a.in_f32);
+    }
+    Ks[tt * LD + c] = bf16_to_f32(kb);
+    Vs[tt * LD + c] = bf16_to_f32(vb);
+  }
+  __syncthreads();
+  uint8_t* out = base + (int64_t)(a.pos >> 5) * it.block_bytes;
+  switch (it.bits) {
+    case 16: write_bf16_block<D, LD>(Ks, Vs, out, tid); break;
+    case 8: write_quant_block<D, 8, KIVI>(Ks, Vs, kmeta, vmeta, out, tid); break;
+    case 4: write_quant_block<D, 4, KIVI>(Ks, Vs, kmeta, vmeta, out, tid); break;
+    default: write_quant_block<D, 2, KIVI>(Ks, Vs, kmeta, vmeta, out, tid); break;
+  }
+}
+
 // Test-only dequantiser: one thread per (stream, token, channel).
 template <int D>
 __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* region, int64_t stream_bytes,
@@ -400,6 +481,54 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
   if (!launched) return fail(KVK_ERR_UNSUPPORTED, "no write kernel for d_h %d, %d bits", d.head_dim, a.bits);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "compress launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+extern "C" kvk_status kvk_append_token(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
+                                       int32_t in_dtype, int32_t n_stored, void* arena, hipStream_t stream) {
+  if (!t) return fail(KVK_ERR_INVALID, "kvk_append_token: NULL table");
+  const kvk_dims& d = t->d;
+  if (l0 < 0 || l1 > d.n_layers || l0 >= l1)
+    return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, d.n_layers);
+  if (!k || !v || !arena) return fail(KVK_ERR_INVALID, "kvk_append_token: NULL buffer");
+  if (in_dtype != KVK_BF16 && in_dtype != KVK_F32) return fail(KVK_ERR_INVALID, "in_dtype %d", in_dtype);
+  if (n_stored < 0 || n_stored >= t->cap)
+    return fail(KVK_ERR_INVALID, "n_stored %d: the stream holds at most %d tokens", n_stored, t->cap);
+  if ((reinterpret_cast<uintptr_t>(arena) & 15) || (reinterpret_cast<uintptr_t>(k) & 15) ||
+      (reinterpret_cast<uintptr_t>(v) & 15))
+    return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
+  if (d.kind == KVK_MLA) return mla_append_token(t, l0, l1, k, v, in_dtype, n_stored, arena, stream);
+
+  AppendArgs a;
+  a.k = k;
+  a.v = v;
+  a.arena = static_cast<uint8_t*>(arena);
+  a.in_f32 = in_dtype == KVK_F32;
+  a.pos = n_stored;
+  a.nb_cap = t->nb_cap;
+  a.n_streams = d.batch * d.n_kv_heads;
+  int n = 0;
+  for (int l = l0; l < l1; ++l) {
+    if (t->plan[l].inherit) continue;  // an inheriting layer stores nothing (§2.1)
+    AppendItem& it = a.items[n++];
+    it.region = t->info.layer_offset[l];
+    it.stream_bytes = (int32_t)t->info.stream_bytes[l];
+    it.block_bytes = (int32_t)t->block_bytes[l];
+    it.bits = t->bits[l];
+    it.row = l - l0;
+  }
+  if (n == 0) return KVK_OK;
+  const dim3 g3((unsigned)a.n_streams, (unsigned)n), b3(256);
+  const bool kivi = d.qscheme == KVK_Q_KIVI32;
+  if (d.head_dim == 128) {
+    if (kivi) hipLaunchKernelGGL((append_kernel<128, true>), g3, b3, 0, stream, a);
+    else hipLaunchKernelGGL((append_kernel<128, false>), g3, b3, 0, stream, a);
+  } else {
+    if (kivi) hipLaunchKernelGGL((append_kernel<64, true>), g3, b3, 0, stream, a);
+    else hipLaunchKernelGGL((append_kernel<64, false>), g3, b3, 0, stream, a);
+  }
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "append launch: %s", hipGetErrorString(e));
   return KVK_OK;
 }
 

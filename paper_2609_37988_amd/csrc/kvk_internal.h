@@ -107,6 +107,9 @@ void mla_workspace(const kvk_table* t, int32_t l0, int32_t l1, MlaWorkspace* ws)
 kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* latent,
                               const void* rope, int32_t in_dtype, int32_t n_tokens,
                               const int32_t* keep_idx, void* arena, hipStream_t stream);
+kvk_status mla_append_token(const kvk_table* t, int32_t l0, int32_t l1, const void* latent,
+                            const void* rope, int32_t in_dtype, int32_t n_stored, void* arena,
+                            hipStream_t stream);
 kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
                              int32_t q_dtype, int32_t n_stored, float scale, const void* w_uk,
                              const void* arena, void* workspace, hipStream_t stream);

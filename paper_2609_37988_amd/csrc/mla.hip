@@ -138,29 +138,31 @@ __device__ __forceinline__ void mla_load8(const MlaCompressArgs& a, int b, int t
   }
 }
 
-// One workgroup per (32-token block, sequence).  Each wave takes (tile T, k-step K)
-// tasks: lane (i, g) moves the 8 channels 32 K + 8 g .. + 7 of block row 16 T + i,
-// i.e. exactly slot (T NK + K) 64 + i + 16 g, so loads and stores need no staging.
+// The prefill source of a block: rows tok0 .. tok0 + 31 of sequence b of the input.
+struct PrefillRows {
+  const MlaCompressArgs& a;
+  int b, tok0, ntok;
+  __device__ __forceinline__ void load8(int t, int c0, float (&x)[8]) const { mla_load8(a, b, tok0, ntok, t, c0, x); }
+};
+
+// Write one 32-token block whose rows come from src.load8(t, c0, x) (the 8 stored
+// channels c0 .. c0+7 of block row t).  Each wave takes (tile T, k-step K) tasks:
+// lane (i, g) moves the 8 channels 32 K + 8 g .. + 7 of block row 16 T + i, i.e.
+// exactly slot (T NK + K) 64 + i + 16 g, so loads and stores need no staging.
 // KIVI32 groups (32 channels of one token) are the 4 lanes i, i + 16, i + 32, i + 48;
 // SYMROW scales (one per token and vector) come from a first pass through LDS.
-template <int BITS, bool KIVI>
-__global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
+// Called by all 256 threads; as_bf16 writes the bf16 block instead.
+template <int BITS, bool KIVI, class Src>
+__device__ __forceinline__ void mla_write_block(const Src& src, uint8_t* out, int d, bool as_bf16,
+                                                uint32_t (&amax)[2][32]) {
 #pragma clang fp contract(off)
-  __shared__ uint32_t amax[2][32];  // SYMROW: max |x| bits of (c[:d] | k^R, token)
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, i = lane & 15, g = lane >> 4;
-  const int blk = blockIdx.x, b = blockIdx.y;
-  const bool tail = blk == a.nbf;
-  const int tok0 = 32 * blk;
-  const int ntok = tail ? a.n_stored - tok0 : 32;
-  const int d = a.d, W = d + kRope, NK = W / 32;
-  uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
-                 (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
-
-  if (BITS == 16 || tail) {  // bf16 block: 16 bytes (8 channels) per slot
+  const int W = d + kRope, NK = W / 32;
+  if (BITS == 16 || as_bf16) {  // bf16 block: 16 bytes (8 channels) per slot
     for (int task = wv; task < 2 * NK; task += 4) {
       const int T = task / NK, K = task - T * NK;
       float x[8];
-      mla_load8(a, b, tok0, ntok, 16 * T + i, 32 * K + 8 * g, x);
+      src.load8(16 * T + i, 32 * K + 8 * g, x);
       u4v o;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
@@ -179,7 +181,7 @@ __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
       for (int task = wv; task < 2 * NK; task += 4) {
         const int T = task / NK, K = task - T * NK;
         float x[8];
-        mla_load8(a, b, tok0, ntok, 16 * T + i, 32 * K + 8 * g, x);
+        src.load8(16 * T + i, 32 * K + 8 * g, x);
         float am = 0.0f;
 #pragma unroll
         for (int e = 0; e < 8; ++e) am = fmaxf(am, fabsf(x[e]));
@@ -191,7 +193,7 @@ __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
     for (int task = wv; task < 2 * NK; task += 4) {
       const int T = task / NK, K = task - T * NK, t = 16 * T + i;
       float x[8];
-      mla_load8(a, b, tok0, ntok, t, 32 * K + 8 * g, x);
+      src.load8(t, 32 * K + 8 * g, x);
       uint32_t u[8];
       if constexpr (KIVI) {
         float mn = x[0], mx = x[0];
@@ -241,6 +243,112 @@ __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
         reinterpret_cast<uint16_t*>(meta)[tid] = bf16_bits_rne(__uint_as_float(amax[part][t]) / q);
       }
     }
+  }
+}
+
+// One workgroup per (32-token block, sequence); a stream's tail block is bf16.
+template <int BITS, bool KIVI>
+__global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
+  __shared__ uint32_t amax[2][32];  // SYMROW: max |x| bits of (c[:d] | k^R, token)
+  const int blk = blockIdx.x, b = blockIdx.y;
+  const bool tail = blk == a.nbf;
+  const int tok0 = 32 * blk;
+  const PrefillRows src{a, b, tok0, tail ? a.n_stored - tok0 : 32};
+  uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
+                 (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
+  mla_write_block<BITS, KIVI>(src, out, a.d, tail, amax);
+}
+
+// Decode-time append of one token to every MLA anchor of a layer range.
+struct MlaAppendItem {
+  int64_t region;
+  int32_t stream_bytes;
+  int32_t block_bytes;
+  int32_t bits;
+  int32_t row;  // the anchor's row in the new-token input (layer - layer_begin)
+  int32_t d;    // kept latent width
+};
+
+struct MlaAppendArgs {
+  const void* latent;  // [rows][B][r] new latents
+  const void* rope;    // [rows][B][d_R] new positional keys
+  uint8_t* arena;
+  int32_t in_f32;
+  int32_t pos;         // stored tokens before the call: the new token's position
+  int32_t nb_cap;
+  int32_t B, r;
+  MlaAppendItem items[KVK_MAX_LAYERS];
+};
+
+// The 8 stored channels c0 .. c0+7 of the new token, rounded to bf16 (the tail's
+// precision), as fp32.
+__device__ __forceinline__ void new_token8(const MlaAppendArgs& a, const MlaAppendItem& it, int b, int c0,
+                                           float (&x)[8]) {
+  const int64_t row = (int64_t)it.row * a.B + b;
+  const void* src = c0 < it.d ? a.latent : a.rope;
+  const int64_t e0 = c0 < it.d ? row * a.r + c0 : row * kRope + (c0 - it.d);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const uint16_t hb = a.in_f32 ? bf16_bits_rne(static_cast<const float*>(src)[e0 + e])
+                                 : static_cast<const uint16_t*>(src)[e0 + e];
+    x[e] = bf16_to_f32(hb);
+  }
+}
+
+__device__ __forceinline__ int mla_slot_of(int t, int c0, int NK) {
+  return ((t >> 4) * NK + (c0 >> 5)) * 64 + (t & 15) + 16 * ((c0 >> 3) & 3);
+}
+
+// The rows of a completed group: tail slots 0..30 and the new token as row 31.
+struct TailRows {
+  const MlaAppendArgs& a;
+  const MlaAppendItem& it;
+  const uint8_t* tail;
+  int b, NK;
+  __device__ __forceinline__ void load8(int t, int c0, float (&x)[8]) const {
+    if (t == 31) {
+      new_token8(a, it, b, c0, x);
+      return;
+    }
+    const u4v w = *reinterpret_cast<const u4v*>(tail + 16 * mla_slot_of(t, c0, NK));
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(w[e] << 16);
+      x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  }
+};
+
+// One workgroup per (anchor, sequence): the token goes to slot pos % 32 of the bf16
+// tail; the token that fills the tail completes a 32-token group, written as full
+// block pos / 32 from the tail's bf16 rows exactly as the prefill write does.
+template <bool KIVI>
+__global__ __launch_bounds__(256) void mla_append_kernel(MlaAppendArgs a) {
+  __shared__ uint32_t amax[2][32];
+  const int b = blockIdx.x;
+  const MlaAppendItem& it = a.items[blockIdx.y];
+  const int W = it.d + kRope, NK = W / 32, t = a.pos & 31;
+  uint8_t* base = a.arena + it.region + (int64_t)b * it.stream_bytes;
+  uint8_t* tail = base + (int64_t)a.nb_cap * it.block_bytes;
+  if (t != 31) {
+    for (int ch = threadIdx.x; ch < W / 8; ch += 256) {
+      float x[8];
+      new_token8(a, it, b, 8 * ch, x);
+      u4v o;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        o[e] = (uint32_t)bf16_bits_rne(x[2 * e]) | ((uint32_t)bf16_bits_rne(x[2 * e + 1]) << 16);
+      *reinterpret_cast<u4v*>(tail + 16 * mla_slot_of(t, 8 * ch, NK)) = o;
+    }
+    return;
+  }
+  const TailRows src{a, it, tail, b, NK};
+  uint8_t* out = base + (int64_t)(a.pos >> 5) * it.block_bytes;
+  switch (it.bits) {
+    case 16: mla_write_block<16, KIVI>(src, out, it.d, true, amax); break;
+    case 8: mla_write_block<8, KIVI>(src, out, it.d, false, amax); break;
+    case 4: mla_write_block<4, KIVI>(src, out, it.d, false, amax); break;
+    default: mla_write_block<2, KIVI>(src, out, it.d, false, amax); break;
   }
 }
 
@@ -926,6 +1034,38 @@ kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* lat
   else hipLaunchKernelGGL((mla_compress_kernel<2, false>), g3, b3, 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA compress launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+kvk_status mla_append_token(const kvk_table* t, int32_t l0, int32_t l1, const void* latent, const void* rope,
+                            int32_t in_dtype, int32_t n_stored, void* arena, hipStream_t stream) {
+  const kvk_dims& d = t->d;
+  MlaAppendArgs a;
+  a.latent = latent;
+  a.rope = rope;
+  a.arena = static_cast<uint8_t*>(arena);
+  a.in_f32 = in_dtype == KVK_F32;
+  a.pos = n_stored;
+  a.nb_cap = t->nb_cap;
+  a.B = d.batch;
+  a.r = d.latent_dim;
+  int n = 0;
+  for (int l = l0; l < l1; ++l) {
+    if (t->plan[l].inherit) continue;
+    MlaAppendItem& it = a.items[n++];
+    it.region = t->info.layer_offset[l];
+    it.stream_bytes = (int32_t)t->info.stream_bytes[l];
+    it.block_bytes = (int32_t)t->block_bytes[l];
+    it.bits = t->bits[l];
+    it.row = l - l0;
+    it.d = t->rank[l];
+  }
+  if (n == 0) return KVK_OK;
+  const dim3 g3((unsigned)d.batch, (unsigned)n), b3(256);
+  if (d.qscheme == KVK_Q_KIVI32) hipLaunchKernelGGL(mla_append_kernel<true>, g3, b3, 0, stream, a);
+  else hipLaunchKernelGGL(mla_append_kernel<false>, g3, b3, 0, stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA append launch: %s", hipGetErrorString(e));
   return KVK_OK;
 }
 

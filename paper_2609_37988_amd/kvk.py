@@ -69,6 +69,7 @@ def load() -> ctypes.CDLL:
             "kvk_table_destroy": (None, [P]),
             "kvk_workspace_bytes": (I32, [P, I32, I32, ctypes.POINTER(ctypes.c_size_t)]),
             "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
+            "kvk_append_token": (I32, [P, I32, I32, P, P, I32, I32, P, P]),
             "kvk_decode_attention": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_splits": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_merge": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P, P]),
@@ -91,7 +92,7 @@ def load() -> ctypes.CDLL:
 def exported_symbols() -> List[str]:
     """Names of the C entry points the binding expects libkvk to export."""
     return ["kvk_layer_table", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
-            "kvk_compress_layer", "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge",
+            "kvk_compress_layer", "kvk_append_token", "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge",
             "kvk_read_bytes", "kvk_debug_dequantize",
             "kvk_realized_bits", "kvk_rho_range", "kvk_last_error", "kvk_version"]
 
@@ -268,6 +269,27 @@ def compress_layer(t: Table, layer: int, k: torch.Tensor, v: torch.Tensor, n_tok
     _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
     _check(load().kvk_compress_layer(t.handle, layer, _ptr(k), _ptr(v), _dtype_code(k), n_tokens,
                                      _ptr(keep_idx), _ptr(arena), _stream(stream)))
+
+
+def append_token(t: Table, layer_begin: int, layer_end: int, k: torch.Tensor, v: torch.Tensor,
+                 n_stored: int, arena: torch.Tensor, stream=None):
+    """Append one decoded token at position n_stored to every anchor in
+    [layer_begin, layer_end).  GQA: k, v [layers, B, Hkv, d_h].  MLA: k = latent
+    [layers, B, r], v = positional key [layers, B, d_R].  Contiguous bf16/fp32 on the
+    device; the rows of inheriting layers are not read."""
+    d = t.dims
+    nl = layer_end - layer_begin
+    _need(k.dtype == v.dtype and k.is_contiguous() and v.is_contiguous(),
+          "k and v must be contiguous tensors of one dtype")
+    if d.kind == MLA:
+        _need(k.numel() == nl * d.batch * d.latent_dim and v.numel() == nl * d.batch * d.rope_dim,
+              "latent size must be layers*B*r and k^R size layers*B*d_R")
+    else:
+        _need(k.numel() == v.numel() == nl * d.batch * d.n_kv_heads * d.head_dim,
+              "k/v size must be layers*B*Hkv*d_h")
+    _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
+    _check(load().kvk_append_token(t.handle, layer_begin, layer_end, _ptr(k), _ptr(v), _dtype_code(k),
+                                   n_stored, _ptr(arena), _stream(stream)))
 
 
 def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_stored: int,

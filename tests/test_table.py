@@ -170,6 +170,15 @@ def test_entry_points_reject_bad_arguments_without_launching():
     _raw(I, "kvk_decode_attention", h, 0, 2, f, kvk.BF16, 64, float("nan"), None, None, f, f, f, 1 << 20, None)
     _raw(I, "kvk_debug_dequantize", h, 0, 65, f, f, f, None)
     assert kvk.workspace_bytes(t, 0, 2) > 0
+    _raw(I, "kvk_append_token", h, 0, 3, f, f, kvk.BF16, 10, f, None)        # layer range
+    _raw(I, "kvk_append_token", h, 1, 1, f, f, kvk.BF16, 10, f, None)        # empty range
+    _raw(I, "kvk_append_token", h, 0, 2, f, f, kvk.BF16, 64, f, None)        # stream full (cap 64)
+    _raw(I, "kvk_append_token", h, 0, 2, f, f, kvk.BF16, -1, f, None)        # negative position
+    _raw(I, "kvk_append_token", h, 0, 2, None, f, kvk.BF16, 10, f, None)     # NULL input
+    _raw(I, "kvk_append_token", h, 0, 2, f, f, 7, 10, f, None)               # dtype
+    _raw(I, "kvk_append_token", h, 0, 2, P(264), f, kvk.BF16, 10, f, None)   # K not 16-byte aligned
+    _raw(I, "kvk_append_token", h, 0, 2, f, f, kvk.BF16, 10, P(260), None)   # arena not 16-byte aligned
+    _raw(kvk.OK, "kvk_append_token", h, 1, 2, f, f, kvk.BF16, 63, f, None)   # inheritors only: no-op
 
 
 def test_binding_rejects_mis_sized_tensors():
@@ -275,3 +284,6 @@ def test_mla_entry_points_reject_bad_arguments_without_launching():
     _raw(I, "kvk_compress_layer", h, 0, f, f, kvk.BF16, 65, None, f, None)
     _raw(I, "kvk_compress_layer", h, 0, Pv(264), f, kvk.BF16, 64, None, f, None)  # latent misaligned
     _raw(kvk.OK, "kvk_compress_layer", h, 1, f, f, kvk.BF16, 64, None, f, None)  # inheritor: no-op
+    _raw(I, "kvk_append_token", h, 0, 2, f, f, kvk.BF16, 64, f, None)        # stream full
+    _raw(I, "kvk_append_token", h, 0, 2, f, Pv(264), kvk.BF16, 10, f, None)  # k^R misaligned
+    _raw(kvk.OK, "kvk_append_token", h, 1, 2, f, f, kvk.BF16, 10, f, None)   # inheritors only: no-op
