@@ -123,6 +123,37 @@ __device__ __forceinline__ void write_bf16_block(const float* Ks, const float* V
   }
 }
 
+// The inverse of write_bf16_block: a bf16 block (16-byte loads) into LDS rows as fp32.
+template <int D, int LD>
+__device__ __forceinline__ void stage_bf16_block(const uint8_t* in, float* Ks, float* Vs, int tid) {
+  const uint4* i4 = reinterpret_cast<const uint4*>(in);
+  for (int ci = tid; ci < 8 * D; ci += 256) {
+    const uint4 q = i4[ci];
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+    if (ci < 4 * D) {
+      const int tau = ci / (2 * D), rem = ci % (2 * D);
+      const int lam = rem & 63, j = rem >> 6;
+      const int t = 16 * tau + (lam & 15), c0 = 32 * j + 8 * (lam >> 4);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        Ks[t * LD + c0 + 2 * p] = __uint_as_float(w[p] << 16);
+        Ks[t * LD + c0 + 2 * p + 1] = __uint_as_float(w[p] & 0xffff0000u);
+      }
+    } else {
+      const int cv = ci - 4 * D;
+      const int lam = cv & 63, m = cv >> 6;
+      const int c = 16 * m + (lam & 15), kg = lam >> 4;
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int s0 = 2 * p, s1 = 2 * p + 1;
+        const int t0 = 16 * (s0 >> 2) + 4 * kg + (s0 & 3), t1 = 16 * (s1 >> 2) + 4 * kg + (s1 & 3);
+        Vs[t0 * LD + c] = __uint_as_float(w[p] << 16);
+        Vs[t1 * LD + c] = __uint_as_float(w[p] & 0xffff0000u);
+      }
+    }
+  }
+}
+
 // min / max over the N consecutive lanes of a group (N = 1, 2, 4), every lane of the
 // group ending with the result.
 template <int N>
@@ -330,13 +361,26 @@ __device__ __forceinline__ uint16_t new_token_bf16(const void* p, int64_t e, int
   return in_f32 ? f32_to_bf16_bits(static_cast<const float*>(p)[e]) : static_cast<const uint16_t*>(p)[e];
 }
 
-// One workgroup per (anchor, stream).  The token goes to slot pos % 32 of the bf16
-// tail block; the token that fills the tail instead completes a 32-token group,
-// which is quantised from the tail's bf16 values (plus the new token, rounded to
-// bf16) into full block pos / 32, exactly as the prefill write quantises a block.
-// The tail is then empty (its stale slots are never read).
+// The new token to slot pos % 32 of the bf16 tail block of every stream: one
+// thread per (stream, channel), grid (streams * D / 256, anchors).
+template <int D>
+__global__ __launch_bounds__(256) void tail_write_kernel(AppendArgs a) {
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= a.n_streams * D) return;
+  const int sidx = idx / D, c = idx % D, t = a.pos & 31;
+  const AppendItem& it = a.items[blockIdx.y];
+  uint8_t* tailb = a.arena + it.region + (int64_t)sidx * it.stream_bytes + (int64_t)a.nb_cap * it.block_bytes;
+  const int64_t e = ((int64_t)it.row * a.n_streams + sidx) * D + c;
+  *reinterpret_cast<uint16_t*>(tailb + k_bf16_byte(D, t, c)) = new_token_bf16(a.k, e, a.in_f32);
+  *reinterpret_cast<uint16_t*>(tailb + v_bf16_byte(D, t, c)) = new_token_bf16(a.v, e, a.in_f32);
+}
+
+// The token that fills the tail (pos % 32 == 31) completes a 32-token group: one
+// workgroup per (stream, anchor) quantises the tail's bf16 values plus the new
+// token (rounded to bf16) into full block pos / 32, exactly as the prefill write
+// quantises a block.  The tail is then empty (its stale slots are never read).
 template <int D, bool KIVI>
-__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
+__global__ __launch_bounds__(256) void group_write_kernel(AppendArgs a) {
   constexpr int LD = D + 4;
   __shared__ float Ks[32 * LD];
   __shared__ float Vs[32 * LD];
@@ -347,26 +391,11 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
   uint8_t* base = a.arena + it.region + (int64_t)sidx * it.stream_bytes;
   uint8_t* tailb = base + (int64_t)a.nb_cap * it.block_bytes;
   const int64_t e0 = ((int64_t)it.row * a.n_streams + sidx) * D;
-  const int t = a.pos & 31;
-  if (t != 31) {
-    for (int c = tid; c < D; c += 256) {
-      *reinterpret_cast<uint16_t*>(tailb + k_bf16_byte(D, t, c)) = new_token_bf16(a.k, e0 + c, a.in_f32);
-      *reinterpret_cast<uint16_t*>(tailb + v_bf16_byte(D, t, c)) = new_token_bf16(a.v, e0 + c, a.in_f32);
-    }
-    return;
-  }
-  for (int idx = tid; idx < 32 * D; idx += 256) {
-    const int tt = idx / D, c = idx % D;
-    uint16_t kb, vb;
-    if (tt < 31) {
-      kb = *reinterpret_cast<const uint16_t*>(tailb + k_bf16_byte(D, tt, c));
-      vb = *reinterpret_cast<const uint16_t*>(tailb + v_bf16_byte(D, tt, c));
-    } else {
-      kb = new_token_bf16(a.k, e0 + c, a.in_f32);
-      vb = new_token_bf16(a.v, e0 + c, a.in_f32);
-    }
-    Ks[tt * LD + c] = bf16_to_f32(kb);
-    Vs[tt * LD + c] = bf16_to_f32(vb);
+  stage_bf16_block<D, LD>(tailb, Ks, Vs, tid);  // row 31 holds a stale slot until replaced
+  __syncthreads();
+  for (int c = tid; c < D; c += 256) {
+    Ks[31 * LD + c] = bf16_to_f32(new_token_bf16(a.k, e0 + c, a.in_f32));
+    Vs[31 * LD + c] = bf16_to_f32(new_token_bf16(a.v, e0 + c, a.in_f32));
   }
   __syncthreads();
   uint8_t* out = base + (int64_t)(a.pos >> 5) * it.block_bytes;
@@ -518,14 +547,21 @@ extern "C" kvk_status kvk_append_token(const kvk_table* t, int32_t l0, int32_t l
     it.row = l - l0;
   }
   if (n == 0) return KVK_OK;
-  const dim3 g3((unsigned)a.n_streams, (unsigned)n), b3(256);
   const bool kivi = d.qscheme == KVK_Q_KIVI32;
-  if (d.head_dim == 128) {
-    if (kivi) hipLaunchKernelGGL((append_kernel<128, true>), g3, b3, 0, stream, a);
-    else hipLaunchKernelGGL((append_kernel<128, false>), g3, b3, 0, stream, a);
+  const dim3 b3(256);
+  if (n_stored % KVK_GROUP != KVK_GROUP - 1) {
+    const dim3 g3((unsigned)((a.n_streams * d.head_dim + 255) / 256), (unsigned)n);
+    if (d.head_dim == 128) hipLaunchKernelGGL(tail_write_kernel<128>, g3, b3, 0, stream, a);
+    else hipLaunchKernelGGL(tail_write_kernel<64>, g3, b3, 0, stream, a);
   } else {
-    if (kivi) hipLaunchKernelGGL((append_kernel<64, true>), g3, b3, 0, stream, a);
-    else hipLaunchKernelGGL((append_kernel<64, false>), g3, b3, 0, stream, a);
+    const dim3 g3((unsigned)a.n_streams, (unsigned)n);
+    if (d.head_dim == 128) {
+      if (kivi) hipLaunchKernelGGL((group_write_kernel<128, true>), g3, b3, 0, stream, a);
+      else hipLaunchKernelGGL((group_write_kernel<128, false>), g3, b3, 0, stream, a);
+    } else {
+      if (kivi) hipLaunchKernelGGL((group_write_kernel<64, true>), g3, b3, 0, stream, a);
+      else hipLaunchKernelGGL((group_write_kernel<64, false>), g3, b3, 0, stream, a);
+    }
   }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "append launch: %s", hipGetErrorString(e));
