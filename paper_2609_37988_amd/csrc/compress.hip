@@ -1,4 +1,6 @@
-// Prefill write of a layer's compressed cache (W1) and the test-only dequantiser.
+// Prefill write of a layer's compressed cache (W1), the decode-time append of one
+// token (W3: a bf16 tail write, or on the 32nd token the quantisation of the
+// completed group with W1's block quantiser), and the test-only dequantiser.
 //
 // An anchor layer stores, per (sequence, KV head), its keys and values — after an
 // optional eviction gather (KV-Kaizen §3, long context: the evictor runs on the

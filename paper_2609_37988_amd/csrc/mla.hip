@@ -24,6 +24,9 @@
 // Register ring: the next blocks' raw bytes are loaded while the current block
 // is computed.  The absorbed query and the probabilities enter the MFMAs as
 // fp16; accumulation is fp32.
+//
+// Writes: the prefill write (W2) and the decode-time append (W3) share one block
+// writer that takes its rows from the input or from the stream's bf16 tail.
 #include <hip/hip_runtime.h>
 
 #include "kvk_device.h"
