@@ -23,7 +23,8 @@ Modules:
   attention — softmax attention, split/LSE merge, depth, eviction
   cache     — compress a layer to arena bytes and decode a step from them
   mla       — the rank axis: MLA latent caches, their storage and attention
+  snapkv    — query-aware token selection at prefill (the eviction composed with)
 
 Parity status per function is stated in each module's docstring.
 """
-from . import plan, quant, layout, attention, cache, mla  # noqa: F401
+from . import plan, quant, layout, attention, cache, mla, snapkv  # noqa: F401
