@@ -299,6 +299,37 @@ kvk_status kvk_append_token(const kvk_table* table, int32_t layer_begin, int32_t
                             const void* k, const void* v, int32_t in_dtype, int32_t n_stored,
                             void* arena, hipStream_t stream);
 
+/* Query-aware keep list of one anchor layer at prefill, for a table that evicts
+ * (keep_tokens > 0): the eviction the paper composes with its configurations
+ * (§3.4: the configurations drop no positions, so an evictor runs on the same
+ * cache and the reductions multiply), computed as its eviction implementations do,
+ * by summing attention over a 32-query observation window (App. F.3).  Per
+ * sequence and KV head: the queries of the last 32 prompt positions of the G query
+ * heads attend causally (window slot w sees positions <= n_tokens - 32 + w) with
+ * softmax(scale q.k); a position's importance is the sum of its probabilities over
+ * those 32 G rows; the 32 window positions are kept, plus the keep_tokens - 32
+ * earlier positions of largest importance (ties to the lower position).  No
+ * pooling (the paper names none).  The result feeds kvk_compress_layer's keep_idx.
+ *   k         : device bf16 [B][Hkv][n_tokens][d_h], the prompt's keys after RoPE
+ *               (the same tensor kvk_compress_layer takes).
+ *   q_obs     : device bf16 [B][Hq][32][d_h], the queries of the last 32 positions.
+ *   n_tokens  : keep_tokens .. max_tokens.
+ *   scale     : softmax scale.
+ *   keep_out  : device int32 [B][Hkv][keep_tokens], written in increasing order.
+ *   importance: NULL, or device fp32 [B][Hkv][n_tokens] receiving the importances.
+ *   workspace : device, >= kvk_snapkv_workspace_bytes(table, n_tokens), 256-byte aligned.
+ * Scores are products of the bf16 inputs accumulated in fp32; the selection is
+ * exact for the importances it computes (fp32).  An inheriting layer returns
+ * KVK_OK and writes nothing.
+ * Errors: KVK_ERR_INVALID (table without eviction or keep_tokens < 32, sizes, NULL
+ *         pointers, misalignment), KVK_ERR_UNSUPPORTED (MLA table, dtype other than
+ *         bf16, more than 8 query heads per KV head, d_h other than 64 or 128),
+ *         KVK_ERR_BUFFER (workspace), KVK_ERR_DEVICE. */
+kvk_status kvk_snapkv_workspace_bytes(const kvk_table* table, int32_t n_tokens, size_t* out_bytes);
+kvk_status kvk_snapkv_select(const kvk_table* table, int32_t layer, const void* k, const void* q_obs,
+                             int32_t in_dtype, int32_t n_tokens, float scale, int32_t* keep_out,
+                             float* importance, void* workspace, size_t ws_bytes, hipStream_t stream);
+
 /* One decode step of attention for layers [layer_begin, layer_end) (§2.1): layer l
  * uses its own query and the cache of anchor_of[l].  Layers in the range that
  * share an anchor are served by one read of that anchor's bytes.

@@ -1,0 +1,378 @@
+// Query-aware token selection at prefill (the eviction composed with the cache
+// configurations, KV-Kaizen §3.4; the paper's eviction implementations sum
+// attention over a 32-query observation window, App. F.3).
+//
+// Per (sequence b, KV head h), from the prompt's keys K [n, D] and the queries of
+// its last 32 positions (the G query heads of h, 32 each: R = 32 G rows):
+//   importance(t) = sum over the R rows of softmax(scale q . k)(t), each window
+//                   query attending causally (row of window slot w sees t <= n-32+w);
+//   keep = the 32 window positions + the keep-32 prefix positions of largest
+//          importance (ties to the lower position), in increasing order.
+//
+// Kernels (all sizes from the table; one call per anchor layer):
+//   snap_scores_kernel<D, 0>: S = Q K^T on MFMA (bf16 in, fp32 out) over a
+//       2048-token chunk per workgroup; per row the chunk's max and sum of 2^(s-max)
+//       (online, rescaled only when the max moves).
+//   snap_merge_kernel: per row, the chunks' (max, sum) merged into (M, 1/L).
+//   snap_scores_kernel<D, 1>: S again, p = 2^(s - M) / L summed over the rows.
+//   snap_topk_kernel: one 1024-thread workgroup per (b, h): radix select (8-bit
+//       digits of the fp32 pattern, importance >= 0) of the threshold, then an
+//       in-order pass that writes the kept positions already sorted.
+// The keys are read twice from HBM; the queries sit in LDS.
+#include <hip/hip_runtime.h>
+
+#include "kvk_device.h"
+#include "kvk_internal.h"
+
+using namespace kvkd;
+
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kWin = 32;      // observation window
+constexpr int kChunk = 2048;  // tokens per workgroup in the score passes
+constexpr int kMaxRT = 16;    // row tiles of 16: up to 8 query heads per KV head
+
+struct SnapArgs {
+  const uint16_t* k;  // [BH][n][D] bf16
+  const uint16_t* q;  // [B][Hq][32][D] bf16
+  float* part;        // [BH][P][R] x (max, sum)
+  float* stats;       // [BH][R] x (M, 1/L)
+  float* imp;         // [BH][n]
+  int32_t* keep;      // [BH][keep_n]
+  int32_t n, P, R, Hkv, Hq, keep_n;
+  float scale_log2;
+};
+
+__device__ __forceinline__ f4 mfma_bf16(bf16x8 a, bf16x8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// PASS 0: per-chunk row statistics.  PASS 1: importance of every token.
+// Wave w of the workgroup takes token tiles of 16 at chunk offsets 16 w, 16 w + 64, ..
+// S^T tile layout (A = 16 query rows, B = 16 tokens): lane (token i16, row group kg)
+// holds rows 4 kg .. 4 kg + 3 of its token.
+template <int D, int PASS>
+__global__ __launch_bounds__(256) void snap_scores_kernel(SnapArgs a) {
+  constexpr int PQ = D + 8;  // LDS row pitch (bf16): consecutive rows 16 bytes apart in bank space
+  __shared__ uint16_t qs[kMaxRT * 16 * PQ];
+  __shared__ float red[4][kMaxRT * 16][2];
+  const int tid = threadIdx.x, lane = tid & 63, i16 = lane & 15, kg = lane >> 4;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int bh = blockIdx.y, p = blockIdx.x;
+  const int b = bh / a.Hkv, h = bh % a.Hkv, G = a.Hq / a.Hkv;
+  const int R = a.R, RT = R / 16;
+  const uint16_t* qb = a.q + (int64_t)(b * a.Hq + h * G) * kWin * D;
+  for (int c = tid; c < R * (D / 8); c += 256) {
+    const int r = c / (D / 8), o = 8 * (c % (D / 8));
+    *reinterpret_cast<uint4*>(&qs[r * PQ + o]) = *reinterpret_cast<const uint4*>(qb + (int64_t)r * D + o);
+  }
+  __syncthreads();
+
+  float m[kMaxRT][4], l[kMaxRT][4];  // PASS 0: running max / sum of 2^(s - max)
+  float sm[kMaxRT][4], sl[kMaxRT][4];  // PASS 1: M and 1/L of the lane's rows
+#pragma unroll
+  for (int rt = 0; rt < kMaxRT; ++rt)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if constexpr (PASS == 0) {
+        m[rt][e] = -INFINITY;
+        l[rt][e] = 0.0f;
+      } else {
+        const int r = 16 * rt + 4 * kg + e;
+        const float* st = a.stats + ((int64_t)bh * R + (r < R ? r : 0)) * 2;
+        sm[rt][e] = st[0];
+        sl[rt][e] = st[1];
+      }
+    }
+
+  const int t0 = p * kChunk, t1 = min(a.n, t0 + kChunk);
+  const uint16_t* kb = a.k + (int64_t)bh * a.n * D;
+  for (int tt = t0 + 16 * wv; tt < t1; tt += 64) {
+    const int t = tt + i16;
+    bf16x8 kv[D / 32];
+#pragma unroll
+    for (int j = 0; j < D / 32; ++j) {
+      if (t < a.n) kv[j] = *reinterpret_cast<const bf16x8*>(kb + (int64_t)t * D + 32 * j + 8 * kg);
+      else kv[j] = bf16x8{};
+    }
+    float imp = 0.0f;
+#pragma unroll
+    for (int rt = 0; rt < kMaxRT; ++rt) {
+      if (rt < RT) {
+        f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < D / 32; ++j) {
+          const bf16x8 qa = *reinterpret_cast<const bf16x8*>(&qs[(16 * rt + i16) * PQ + 32 * j + 8 * kg]);
+          acc = mfma_bf16(qa, kv[j], acc);
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int w = (16 * rt + 4 * kg + e) & (kWin - 1);  // window slot of the row (rows are head-major)
+          const bool vis = t < a.n && t <= a.n - kWin + w;
+          const float s = acc[e] * a.scale_log2;
+          if constexpr (PASS == 0) {
+            if (vis) {
+              if (s > m[rt][e]) {
+                l[rt][e] *= __builtin_amdgcn_exp2f(m[rt][e] - s);
+                m[rt][e] = s;
+              }
+              l[rt][e] += __builtin_amdgcn_exp2f(s - m[rt][e]);
+            }
+          } else {
+            if (vis) imp += __builtin_amdgcn_exp2f(s - sm[rt][e]) * sl[rt][e];
+          }
+        }
+      }
+    }
+    if constexpr (PASS == 1) {
+      imp = rows_sum(imp);  // over the four row groups
+      if (kg == 0 && t < a.n) a.imp[(int64_t)bh * a.n + t] = imp;
+    }
+  }
+
+  if constexpr (PASS == 0) {
+    // over the 16 tokens of a row group (lanes i16), then over the 4 waves
+#pragma unroll
+    for (int rt = 0; rt < kMaxRT; ++rt) {
+      if (rt < RT) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float M = max16(m[rt][e]);
+          const float x = M == -INFINITY ? 0.0f : l[rt][e] * __builtin_amdgcn_exp2f(m[rt][e] - M);
+          const float L = sum16(x);
+          if (i16 == 0) {
+            red[wv][16 * rt + 4 * kg + e][0] = M;
+            red[wv][16 * rt + 4 * kg + e][1] = L;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    if (tid < R) {
+      float M = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) M = fmaxf(M, red[w][tid][0]);
+      float L = 0.0f;
+      if (M != -INFINITY) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          if (red[w][tid][0] != -INFINITY) L += red[w][tid][1] * __builtin_amdgcn_exp2f(red[w][tid][0] - M);
+      }
+      float* out = a.part + (((int64_t)bh * a.P + p) * R + tid) * 2;
+      out[0] = M;
+      out[1] = L;
+    }
+  }
+}
+
+// Per (b, h) and row: merge the chunks' (max, sum) into (M, 1/L).
+__global__ __launch_bounds__(256) void snap_merge_kernel(SnapArgs a) {
+  const int bh = blockIdx.x, r = threadIdx.x;
+  if (r >= a.R) return;
+  const float* pp = a.part + (int64_t)bh * a.P * a.R * 2;
+  float M = -INFINITY;
+  for (int p = 0; p < a.P; ++p) M = fmaxf(M, pp[((int64_t)p * a.R + r) * 2]);
+  float L = 0.0f;
+  for (int p = 0; p < a.P; ++p) {
+    const float mp = pp[((int64_t)p * a.R + r) * 2];
+    if (mp != -INFINITY) L += pp[((int64_t)p * a.R + r) * 2 + 1] * __builtin_amdgcn_exp2f(mp - M);
+  }
+  float* st = a.stats + ((int64_t)bh * a.R + r) * 2;
+  st[0] = M;
+  st[1] = 1.0f / L;  // every row sees position 0, so L >= 1
+}
+
+// Exclusive prefix sum over the 1024 threads of a workgroup (16 waves); total out.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* wsum, uint32_t& total) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  if (lane == 63) wsum[wv] = x;
+  __syncthreads();
+  uint32_t before = 0, all = 0;
+  for (int w = 0; w < 16; ++w) {
+    const uint32_t s = wsum[w];
+    if (w < wv) before += s;
+    all += s;
+  }
+  __syncthreads();
+  total = all;
+  return before + x - v;
+}
+
+// One workgroup per (b, h): the keep - 32 largest prefix importances (ties to the
+// lower position) and the window, in increasing order.
+__global__ __launch_bounds__(1024) void snap_topk_kernel(SnapArgs a) {
+  __shared__ uint32_t hist[16][256];
+  __shared__ uint32_t wsum[16];
+  __shared__ uint32_t sh_prefix, sh_remaining;
+  const int tid = threadIdx.x, wv = tid >> 6;
+  const int bh = blockIdx.x;
+  const int np = a.n - kWin, k = a.keep_n - kWin;
+  const uint32_t* key = reinterpret_cast<const uint32_t*>(a.imp + (int64_t)bh * a.n);  // >= 0: bits are monotone
+  int32_t* out = a.keep + (int64_t)bh * a.keep_n;
+  if (k > 0) {
+    uint32_t prefix = 0, mask = 0, remaining = (uint32_t)k;
+    for (int d = 3; d >= 0; --d) {
+      for (int i = tid; i < 16 * 256; i += 1024) (&hist[0][0])[i] = 0u;
+      __syncthreads();
+      for (int i = tid; i < np; i += 1024) {
+        const uint32_t u = key[i];
+        if ((u & mask) == prefix) atomicAdd(&hist[wv][(u >> (8 * d)) & 255u], 1u);
+      }
+      __syncthreads();
+      if (tid < 256) {  // fold the per-wave histograms into row 0
+        uint32_t s = 0;
+        for (int w = 0; w < 16; ++w) s += hist[w][tid];
+        hist[0][tid] = s;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        uint32_t cum = 0, sel = 0;
+        for (int v = 255; v >= 0; --v) {
+          const uint32_t c = hist[0][v];
+          if (cum + c >= remaining) {
+            sel = (uint32_t)v;
+            break;
+          }
+          cum += c;
+        }
+        sh_prefix = prefix | (sel << (8 * d));
+        sh_remaining = remaining - cum;
+      }
+      __syncthreads();
+      prefix = sh_prefix;
+      remaining = sh_remaining;
+      mask |= 255u << (8 * d);
+    }
+    // prefix = the threshold pattern; take every larger key and the first
+    // `remaining` keys equal to it, in position order.
+    const int per = (np + 1023) / 1024;
+    const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
+    uint32_t c_gt = 0, c_eq = 0;
+    for (int i = i0; i < i1; ++i) {
+      const uint32_t u = key[i];
+      c_gt += u > prefix;
+      c_eq += u == prefix;
+    }
+    uint32_t tot;
+    const uint32_t eq_before = block_exclusive_scan(c_eq, wsum, tot);
+    const uint32_t take_eq = eq_before >= remaining ? 0u : min(c_eq, remaining - eq_before);
+    uint32_t off = block_exclusive_scan(c_gt + take_eq, wsum, tot);
+    uint32_t eq_seen = 0;
+    for (int i = i0; i < i1; ++i) {
+      const uint32_t u = key[i];
+      bool take = u > prefix;
+      if (u == prefix) {
+        take = eq_seen < take_eq;
+        ++eq_seen;
+      }
+      if (take && off < (uint32_t)k) out[off++] = i;  // the bound holds by construction; kept as a guard
+    }
+  }
+  for (int i = tid; i < kWin; i += 1024) out[k + i] = np + i;
+}
+
+}  // namespace
+
+using namespace kvk;
+
+namespace {
+
+struct SnapSizes {
+  int64_t part, stats, imp;  // floats
+  int32_t P, R;
+};
+
+SnapSizes snap_sizes(const kvk_table* t, int32_t n_tokens) {
+  const kvk_dims& d = t->d;
+  SnapSizes s;
+  s.P = (n_tokens + kChunk - 1) / kChunk;
+  s.R = kWin * (d.n_q_heads / d.n_kv_heads);
+  const int64_t bh = (int64_t)d.batch * d.n_kv_heads;
+  s.part = bh * s.P * s.R * 2;
+  s.stats = bh * s.R * 2;
+  s.imp = bh * n_tokens;
+  return s;
+}
+
+kvk_status snap_check(const kvk_table* t, int32_t n_tokens) {
+  if (!t) return fail(KVK_ERR_INVALID, "snapkv: NULL table");
+  const kvk_dims& d = t->d;
+  if (d.kind != KVK_GQA) return fail(KVK_ERR_UNSUPPORTED, "snapkv: GQA tables only");
+  if (d.keep_tokens < kWin)
+    return fail(KVK_ERR_INVALID, "snapkv: the table must evict with keep_tokens >= %d (has %d)", kWin,
+                d.keep_tokens);
+  if (n_tokens < d.keep_tokens || n_tokens > d.max_tokens)
+    return fail(KVK_ERR_INVALID, "snapkv: n_tokens %d outside keep_tokens..max_tokens (%d..%d)", n_tokens,
+                d.keep_tokens, d.max_tokens);
+  if (d.n_q_heads / d.n_kv_heads > kMaxRT / 2)
+    return fail(KVK_ERR_UNSUPPORTED, "snapkv: at most %d query heads per KV head", kMaxRT / 2);
+  if (d.head_dim != 64 && d.head_dim != 128) return fail(KVK_ERR_UNSUPPORTED, "snapkv: head_dim %d", d.head_dim);
+  return KVK_OK;
+}
+
+}  // namespace
+
+extern "C" kvk_status kvk_snapkv_workspace_bytes(const kvk_table* t, int32_t n_tokens, size_t* out) {
+  const kvk_status st = snap_check(t, n_tokens);
+  if (st != KVK_OK) return st;
+  if (!out) return fail(KVK_ERR_INVALID, "snapkv: NULL output");
+  const SnapSizes s = snap_sizes(t, n_tokens);
+  *out = (size_t)(round256(s.part * 4) + round256(s.stats * 4) + round256(s.imp * 4));
+  return KVK_OK;
+}
+
+extern "C" kvk_status kvk_snapkv_select(const kvk_table* t, int32_t layer, const void* k, const void* q_obs,
+                                        int32_t in_dtype, int32_t n_tokens, float scale, int32_t* keep_out,
+                                        float* importance_out, void* workspace, size_t ws_bytes,
+                                        hipStream_t stream) {
+  kvk_status st = snap_check(t, n_tokens);
+  if (st != KVK_OK) return st;
+  const kvk_dims& d = t->d;
+  if (layer < 0 || layer >= d.n_layers) return fail(KVK_ERR_INVALID, "layer %d out of range", layer);
+  if (t->plan[layer].inherit) return KVK_OK;  // an inheriting layer stores nothing to select from
+  if (!k || !q_obs || !keep_out || !workspace) return fail(KVK_ERR_INVALID, "snapkv: NULL buffer");
+  if (in_dtype != KVK_BF16) return fail(KVK_ERR_UNSUPPORTED, "snapkv: keys and queries must be bf16");
+  if (!(scale == scale)) return fail(KVK_ERR_INVALID, "snapkv: scale is NaN");
+  if ((reinterpret_cast<uintptr_t>(k) & 15) || (reinterpret_cast<uintptr_t>(q_obs) & 15) ||
+      (reinterpret_cast<uintptr_t>(keep_out) & 3) || (reinterpret_cast<uintptr_t>(importance_out) & 3) ||
+      (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return fail(KVK_ERR_INVALID, "snapkv: misaligned buffer (k/q 16 B, keep/importance 4 B, workspace 256 B)");
+  size_t need = 0;
+  kvk_snapkv_workspace_bytes(t, n_tokens, &need);
+  if (need > ws_bytes) return fail(KVK_ERR_BUFFER, "snapkv: workspace %zu bytes < %zu needed", ws_bytes, need);
+  const SnapSizes s = snap_sizes(t, n_tokens);
+  const int64_t bh = (int64_t)d.batch * d.n_kv_heads;
+  if (bh > 65535 || s.P > 0x7fffffff) return fail(KVK_ERR_UNSUPPORTED, "snapkv: grid too large");
+  SnapArgs a;
+  a.k = static_cast<const uint16_t*>(k);
+  a.q = static_cast<const uint16_t*>(q_obs);
+  uint8_t* w = static_cast<uint8_t*>(workspace);
+  a.part = reinterpret_cast<float*>(w);
+  a.stats = reinterpret_cast<float*>(w + round256(s.part * 4));
+  a.imp = importance_out ? importance_out : reinterpret_cast<float*>(w + round256(s.part * 4) + round256(s.stats * 4));
+  a.keep = keep_out;
+  a.n = n_tokens;
+  a.P = s.P;
+  a.R = s.R;
+  a.Hkv = d.n_kv_heads;
+  a.Hq = d.n_q_heads;
+  a.keep_n = d.keep_tokens;
+  a.scale_log2 = scale * kLog2e;
+  const dim3 gs((unsigned)s.P, (unsigned)bh), b256(256);
+  if (d.head_dim == 128) hipLaunchKernelGGL((snap_scores_kernel<128, 0>), gs, b256, 0, stream, a);
+  else hipLaunchKernelGGL((snap_scores_kernel<64, 0>), gs, b256, 0, stream, a);
+  hipLaunchKernelGGL(snap_merge_kernel, dim3((unsigned)bh), b256, 0, stream, a);
+  if (d.head_dim == 128) hipLaunchKernelGGL((snap_scores_kernel<128, 1>), gs, b256, 0, stream, a);
+  else hipLaunchKernelGGL((snap_scores_kernel<64, 1>), gs, b256, 0, stream, a);
+  hipLaunchKernelGGL(snap_topk_kernel, dim3((unsigned)bh), dim3(1024), 0, stream, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "snapkv launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}

@@ -70,6 +70,8 @@ def load() -> ctypes.CDLL:
             "kvk_workspace_bytes": (I32, [P, I32, I32, ctypes.POINTER(ctypes.c_size_t)]),
             "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
             "kvk_append_token": (I32, [P, I32, I32, P, P, I32, I32, P, P]),
+            "kvk_snapkv_workspace_bytes": (I32, [P, I32, ctypes.POINTER(ctypes.c_size_t)]),
+            "kvk_snapkv_select": (I32, [P, I32, P, P, I32, I32, F, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_attention": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_splits": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_merge": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P, P]),
@@ -92,7 +94,8 @@ def load() -> ctypes.CDLL:
 def exported_symbols() -> List[str]:
     """Names of the C entry points the binding expects libkvk to export."""
     return ["kvk_layer_table", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
-            "kvk_compress_layer", "kvk_append_token", "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge",
+            "kvk_compress_layer", "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
+            "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge",
             "kvk_read_bytes", "kvk_debug_dequantize",
             "kvk_realized_bits", "kvk_rho_range", "kvk_last_error", "kvk_version"]
 
@@ -290,6 +293,33 @@ def append_token(t: Table, layer_begin: int, layer_end: int, k: torch.Tensor, v:
     _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
     _check(load().kvk_append_token(t.handle, layer_begin, layer_end, _ptr(k), _ptr(v), _dtype_code(k),
                                    n_stored, _ptr(arena), _stream(stream)))
+
+
+def snapkv_workspace_bytes(t: Table, n_tokens: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().kvk_snapkv_workspace_bytes(t.handle, n_tokens, ctypes.byref(out)))
+    return out.value
+
+
+def snapkv_select(t: Table, layer: int, k: torch.Tensor, q_obs: torch.Tensor, n_tokens: int, scale: float,
+                  keep_out: torch.Tensor, workspace: torch.Tensor, importance: Optional[torch.Tensor] = None,
+                  stream=None):
+    """Query-aware keep list of one anchor layer at prefill.  k [B, Hkv, n_tokens, d_h]
+    and q_obs [B, Hq, 32, d_h] (the last 32 prompt positions' queries) bf16; keep_out
+    int32 [B, Hkv, keep_tokens]; importance (optional) fp32 [B, Hkv, n_tokens]."""
+    d = t.dims
+    _need(k.dtype == q_obs.dtype == torch.bfloat16 and k.is_contiguous() and q_obs.is_contiguous(),
+          "k and q_obs must be contiguous bf16 tensors")
+    _need(k.numel() == d.batch * d.n_kv_heads * n_tokens * d.head_dim, "k size must be B*Hkv*n_tokens*d_h")
+    _need(q_obs.numel() == d.batch * d.n_q_heads * 32 * d.head_dim, "q_obs size must be B*Hq*32*d_h")
+    _need(keep_out.dtype == torch.int32 and keep_out.is_contiguous() and
+          keep_out.numel() == d.batch * d.n_kv_heads * d.keep_tokens, "keep_out must be int32 B*Hkv*keep_tokens")
+    if importance is not None:
+        _need(importance.dtype == torch.float32 and importance.is_contiguous() and
+              importance.numel() == d.batch * d.n_kv_heads * n_tokens, "importance must be fp32 B*Hkv*n_tokens")
+    _check(load().kvk_snapkv_select(t.handle, layer, _ptr(k), _ptr(q_obs), _dtype_code(k), n_tokens, float(scale),
+                                    _ptr(keep_out), _ptr(importance), _ptr(workspace), _nbytes(workspace),
+                                    _stream(stream)))
 
 
 def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_stored: int,

@@ -181,6 +181,30 @@ def test_entry_points_reject_bad_arguments_without_launching():
     _raw(kvk.OK, "kvk_append_token", h, 1, 2, f, f, kvk.BF16, 63, f, None)   # inheritors only: no-op
 
 
+def test_snapkv_rejects_bad_arguments_without_launching():
+    P = ctypes.c_void_p
+    f = P(256)
+    I, U, B = kvk.ERR_INVALID, kvk.ERR_UNSUPPORTED, kvk.ERR_BUFFER
+    ev = kvk.layer_table(kvk.make_dims(kvk.GQA, 2, 10, 2, 128, batch=1, max_tokens=256, keep_tokens=64),
+                         kvk.make_plan([(0, 4), (1, 16)]))
+    need = kvk.snapkv_workspace_bytes(ev, 256)
+    assert need > 0
+    h = ev.handle
+    _raw(I, "kvk_snapkv_select", h, 0, f, f, kvk.BF16, 63, 0.1, f, None, f, need, None)     # n < keep
+    _raw(I, "kvk_snapkv_select", h, 0, f, f, kvk.BF16, 257, 0.1, f, None, f, need, None)    # n > max
+    _raw(I, "kvk_snapkv_select", h, 2, f, f, kvk.BF16, 256, 0.1, f, None, f, need, None)    # layer
+    _raw(I, "kvk_snapkv_select", h, 0, None, f, kvk.BF16, 256, 0.1, f, None, f, need, None)  # NULL keys
+    _raw(U, "kvk_snapkv_select", h, 0, f, f, kvk.F32, 256, 0.1, f, None, f, need, None)     # fp32
+    _raw(I, "kvk_snapkv_select", h, 0, P(264), f, kvk.BF16, 256, 0.1, f, None, f, need, None)  # align
+    _raw(B, "kvk_snapkv_select", h, 0, f, f, kvk.BF16, 256, 0.1, f, None, f, need - 1, None)
+    _raw(kvk.OK, "kvk_snapkv_select", h, 1, f, f, kvk.BF16, 256, 0.1, f, None, f, need, None)  # inheritor
+    no_ev = kvk.layer_table(kvk.make_dims(kvk.GQA, 1, 4, 1, 128, batch=1, max_tokens=256), kvk.make_plan([(0, 4)]))
+    _raw(I, "kvk_snapkv_select", no_ev.handle, 0, f, f, kvk.BF16, 256, 0.1, f, None, f, need, None)
+    wide = kvk.layer_table(kvk.make_dims(kvk.GQA, 1, 18, 2, 128, batch=1, max_tokens=256, keep_tokens=64),
+                           kvk.make_plan([(0, 4)]))
+    _raw(U, "kvk_snapkv_select", wide.handle, 0, f, f, kvk.BF16, 256, 0.1, f, None, f, 1 << 30, None)  # G 9
+
+
 def test_binding_rejects_mis_sized_tensors():
     import torch
     d = kvk.make_dims(kvk.GQA, 1, 4, 1, 64, batch=1, max_tokens=64)
