@@ -31,7 +31,7 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kWin = 32;      // observation window
 constexpr int kChunk = 2048;  // tokens per workgroup in the score passes
-constexpr int kMaxRT = 16;    // row tiles of 16: up to 8 query heads per KV head
+constexpr int kMaxG = 8;      // query heads per KV head
 
 struct SnapArgs {
   const uint16_t* k;  // [BH][n][D] bf16
@@ -52,16 +52,17 @@ __device__ __forceinline__ f4 mfma_bf16(bf16x8 a, bf16x8 b, f4 c) {
 // Wave w of the workgroup takes token tiles of 16 at chunk offsets 16 w, 16 w + 64, ..
 // S^T tile layout (A = 16 query rows, B = 16 tokens): lane (token i16, row group kg)
 // holds rows 4 kg .. 4 kg + 3 of its token.
-template <int D, int PASS>
+template <int D, int PASS, int G>
 __global__ __launch_bounds__(256) void snap_scores_kernel(SnapArgs a) {
+  constexpr int RT = 2 * G;  // row tiles of 16
+  constexpr int R = 32 * G;  // window rows of the KV head
   constexpr int PQ = D + 8;  // LDS row pitch (bf16): consecutive rows 16 bytes apart in bank space
-  __shared__ uint16_t qs[kMaxRT * 16 * PQ];
-  __shared__ float red[4][kMaxRT * 16][2];
+  extern __shared__ uint16_t qs[];  // [R][PQ], sized by the launch
+  __shared__ float red[4][R][2];
   const int tid = threadIdx.x, lane = tid & 63, i16 = lane & 15, kg = lane >> 4;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int bh = blockIdx.y, p = blockIdx.x;
-  const int b = bh / a.Hkv, h = bh % a.Hkv, G = a.Hq / a.Hkv;
-  const int R = a.R, RT = R / 16;
+  const int b = bh / a.Hkv, h = bh % a.Hkv;
   const uint16_t* qb = a.q + (int64_t)(b * a.Hq + h * G) * kWin * D;
   for (int c = tid; c < R * (D / 8); c += 256) {
     const int r = c / (D / 8), o = 8 * (c % (D / 8));
@@ -69,10 +70,10 @@ __global__ __launch_bounds__(256) void snap_scores_kernel(SnapArgs a) {
   }
   __syncthreads();
 
-  float m[kMaxRT][4], l[kMaxRT][4];  // PASS 0: running max / sum of 2^(s - max)
-  float sm[kMaxRT][4], sl[kMaxRT][4];  // PASS 1: M and 1/L of the lane's rows
+  float m[RT][4], l[RT][4];  // PASS 0: running max / sum of 2^(s - max)
+  float sm[RT][4], sl[RT][4];  // PASS 1: M and 1/L of the lane's rows
 #pragma unroll
-  for (int rt = 0; rt < kMaxRT; ++rt)
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       if constexpr (PASS == 0) {
@@ -80,7 +81,7 @@ __global__ __launch_bounds__(256) void snap_scores_kernel(SnapArgs a) {
         l[rt][e] = 0.0f;
       } else {
         const int r = 16 * rt + 4 * kg + e;
-        const float* st = a.stats + ((int64_t)bh * R + (r < R ? r : 0)) * 2;
+        const float* st = a.stats + ((int64_t)bh * R + r) * 2;
         sm[rt][e] = st[0];
         sl[rt][e] = st[1];
       }
@@ -88,18 +89,26 @@ __global__ __launch_bounds__(256) void snap_scores_kernel(SnapArgs a) {
 
   const int t0 = p * kChunk, t1 = min(a.n, t0 + kChunk);
   const uint16_t* kb = a.k + (int64_t)bh * a.n * D;
+  // The key operand of the next tile is loaded while the current one is computed.
+  bf16x8 kn[D / 32];
+  auto load_keys = [&](int t) {
+#pragma unroll
+    for (int j = 0; j < D / 32; ++j) {
+      if (t < t1) kn[j] = *reinterpret_cast<const bf16x8*>(kb + (int64_t)t * D + 32 * j + 8 * kg);
+      else kn[j] = bf16x8{};
+    }
+  };
+  load_keys(t0 + 16 * wv + i16);
   for (int tt = t0 + 16 * wv; tt < t1; tt += 64) {
     const int t = tt + i16;
     bf16x8 kv[D / 32];
 #pragma unroll
-    for (int j = 0; j < D / 32; ++j) {
-      if (t < a.n) kv[j] = *reinterpret_cast<const bf16x8*>(kb + (int64_t)t * D + 32 * j + 8 * kg);
-      else kv[j] = bf16x8{};
-    }
+    for (int j = 0; j < D / 32; ++j) kv[j] = kn[j];
+    load_keys(t + 64);
     float imp = 0.0f;
 #pragma unroll
-    for (int rt = 0; rt < kMaxRT; ++rt) {
-      if (rt < RT) {
+    for (int rt = 0; rt < RT; ++rt) {
+      {
         f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < D / 32; ++j) {
@@ -124,6 +133,7 @@ __global__ __launch_bounds__(256) void snap_scores_kernel(SnapArgs a) {
           }
         }
       }
+      __builtin_amdgcn_sched_barrier(0);  // one row tile's operands live at a time
     }
     if constexpr (PASS == 1) {
       imp = rows_sum(imp);  // over the four row groups
@@ -134,8 +144,8 @@ __global__ __launch_bounds__(256) void snap_scores_kernel(SnapArgs a) {
   if constexpr (PASS == 0) {
     // over the 16 tokens of a row group (lanes i16), then over the 4 waves
 #pragma unroll
-    for (int rt = 0; rt < kMaxRT; ++rt) {
-      if (rt < RT) {
+    for (int rt = 0; rt < RT; ++rt) {
+      {
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float M = max16(m[rt][e]);
@@ -301,6 +311,20 @@ SnapSizes snap_sizes(const kvk_table* t, int32_t n_tokens) {
   return s;
 }
 
+template <int PASS>
+void launch_scores(int D, int G, dim3 gs, size_t lds, hipStream_t stream, const SnapArgs& a) {
+#define KVK_SNAP(DD, GG) \
+  if (D == DD && G == GG) { \
+    hipLaunchKernelGGL((snap_scores_kernel<DD, PASS, GG>), gs, dim3(256), lds, stream, a); \
+    return; \
+  }
+  KVK_SNAP(128, 1) KVK_SNAP(128, 2) KVK_SNAP(128, 3) KVK_SNAP(128, 4)
+  KVK_SNAP(128, 5) KVK_SNAP(128, 6) KVK_SNAP(128, 7) KVK_SNAP(128, 8)
+  KVK_SNAP(64, 1) KVK_SNAP(64, 2) KVK_SNAP(64, 3) KVK_SNAP(64, 4)
+  KVK_SNAP(64, 5) KVK_SNAP(64, 6) KVK_SNAP(64, 7) KVK_SNAP(64, 8)
+#undef KVK_SNAP
+}
+
 kvk_status snap_check(const kvk_table* t, int32_t n_tokens) {
   if (!t) return fail(KVK_ERR_INVALID, "snapkv: NULL table");
   const kvk_dims& d = t->d;
@@ -311,8 +335,8 @@ kvk_status snap_check(const kvk_table* t, int32_t n_tokens) {
   if (n_tokens < d.keep_tokens || n_tokens > d.max_tokens)
     return fail(KVK_ERR_INVALID, "snapkv: n_tokens %d outside keep_tokens..max_tokens (%d..%d)", n_tokens,
                 d.keep_tokens, d.max_tokens);
-  if (d.n_q_heads / d.n_kv_heads > kMaxRT / 2)
-    return fail(KVK_ERR_UNSUPPORTED, "snapkv: at most %d query heads per KV head", kMaxRT / 2);
+  if (d.n_q_heads / d.n_kv_heads > kMaxG)
+    return fail(KVK_ERR_UNSUPPORTED, "snapkv: at most %d query heads per KV head", kMaxG);
   if (d.head_dim != 64 && d.head_dim != 128) return fail(KVK_ERR_UNSUPPORTED, "snapkv: head_dim %d", d.head_dim);
   return KVK_OK;
 }
@@ -366,11 +390,11 @@ extern "C" kvk_status kvk_snapkv_select(const kvk_table* t, int32_t layer, const
   a.keep_n = d.keep_tokens;
   a.scale_log2 = scale * kLog2e;
   const dim3 gs((unsigned)s.P, (unsigned)bh), b256(256);
-  if (d.head_dim == 128) hipLaunchKernelGGL((snap_scores_kernel<128, 0>), gs, b256, 0, stream, a);
-  else hipLaunchKernelGGL((snap_scores_kernel<64, 0>), gs, b256, 0, stream, a);
+  const size_t lds_q = (size_t)s.R * (d.head_dim + 8) * sizeof(uint16_t);  // the window queries
+  const int G = d.n_q_heads / d.n_kv_heads;
+  launch_scores<0>(d.head_dim, G, gs, lds_q, stream, a);
   hipLaunchKernelGGL(snap_merge_kernel, dim3((unsigned)bh), b256, 0, stream, a);
-  if (d.head_dim == 128) hipLaunchKernelGGL((snap_scores_kernel<128, 1>), gs, b256, 0, stream, a);
-  else hipLaunchKernelGGL((snap_scores_kernel<64, 1>), gs, b256, 0, stream, a);
+  launch_scores<1>(d.head_dim, G, gs, lds_q, stream, a);
   hipLaunchKernelGGL(snap_topk_kernel, dim3((unsigned)bh), dim3(1024), 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "snapkv launch: %s", hipGetErrorString(e));
