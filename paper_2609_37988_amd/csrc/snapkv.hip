@@ -15,9 +15,9 @@
 //       (online, rescaled only when the max moves).
 //   snap_merge_kernel: per row, the chunks' (max, sum) merged into (M, 1/L).
 //   snap_scores_kernel<D, 1>: S again, p = 2^(s - M) / L summed over the rows.
-//   snap_topk_kernel: one 1024-thread workgroup per (b, h): radix select (8-bit
-//       digits of the fp32 pattern, importance >= 0) of the threshold, then an
-//       in-order pass that writes the kept positions already sorted.
+//   snap_topk_kernel: one 1024-thread workgroup per (b, h): radix select (12-, 10-
+//       and 9-bit digits of the fp32 pattern, importance >= 0) of the threshold,
+//       then an in-order pass that writes the kept positions already sorted.
 // The keys are read twice from HBM; the queries sit in LDS.
 #include <hip/hip_runtime.h>
 
@@ -215,74 +215,99 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* w
   return before + x - v;
 }
 
+// Lanes of the wave below this one whose bit is set in the ballot.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t ballot, int lane) {
+  return (uint32_t)__popcll(ballot & ((1ull << lane) - 1ull));
+}
+
 // One workgroup per (b, h): the keep - 32 largest prefix importances (ties to the
-// lower position) and the window, in increasing order.
+// lower position) and the window, in increasing order.  The threshold is found by
+// radix select over the fp32 pattern (importance >= 0, so patterns order as values):
+// digits of 12, 10 and 9 bits below the sign, one LDS histogram per digit.  Then
+// each wave takes a contiguous sixteenth of the positions, counts what it keeps,
+// and after one exchange of counts writes its positions in order (ballots give the
+// ranks inside each 64-position step).
 __global__ __launch_bounds__(1024) void snap_topk_kernel(SnapArgs a) {
-  __shared__ uint32_t hist[16][256];
-  __shared__ uint32_t wsum[16];
+  __shared__ uint32_t hist[4096];
+  __shared__ uint32_t wsum[16], wgt[16], weq[16];
   __shared__ uint32_t sh_prefix, sh_remaining;
-  const int tid = threadIdx.x, wv = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int bh = blockIdx.x;
   const int np = a.n - kWin, k = a.keep_n - kWin;
-  const uint32_t* key = reinterpret_cast<const uint32_t*>(a.imp + (int64_t)bh * a.n);  // >= 0: bits are monotone
+  const uint32_t* key = reinterpret_cast<const uint32_t*>(a.imp + (int64_t)bh * a.n);
   int32_t* out = a.keep + (int64_t)bh * a.keep_n;
   if (k > 0) {
     uint32_t prefix = 0, mask = 0, remaining = (uint32_t)k;
-    for (int d = 3; d >= 0; --d) {
-      for (int i = tid; i < 16 * 256; i += 1024) (&hist[0][0])[i] = 0u;
+    for (int dg = 0; dg < 3; ++dg) {
+      const int sh = dg == 0 ? 19 : (dg == 1 ? 9 : 0);
+      const int nb = dg == 0 ? 4096 : (dg == 1 ? 1024 : 512);
+      for (int i = tid; i < nb; i += 1024) hist[i] = 0u;
       __syncthreads();
       for (int i = tid; i < np; i += 1024) {
         const uint32_t u = key[i];
-        if ((u & mask) == prefix) atomicAdd(&hist[wv][(u >> (8 * d)) & 255u], 1u);
+        if ((u & mask) == prefix) atomicAdd(&hist[(u >> sh) & (uint32_t)(nb - 1)], 1u);
       }
       __syncthreads();
-      if (tid < 256) {  // fold the per-wave histograms into row 0
-        uint32_t s = 0;
-        for (int w = 0; w < 16; ++w) s += hist[w][tid];
-        hist[0][tid] = s;
-      }
-      __syncthreads();
-      if (tid == 0) {
-        uint32_t cum = 0, sel = 0;
-        for (int v = 255; v >= 0; --v) {
-          const uint32_t c = hist[0][v];
+      // digits in descending order, four per thread; the thread whose range holds
+      // the remaining-th largest element fixes the digit
+      const int top = nb - 1 - 4 * tid;
+      uint32_t c4 = 0;
+      if (top >= 0)
+        for (int j = 0; j < 4; ++j) c4 += hist[top - j];
+      uint32_t tot;
+      const uint32_t above = block_exclusive_scan(c4, wsum, tot);
+      if (top >= 0 && above < remaining && above + c4 >= remaining) {
+        uint32_t cum = above;
+        for (int j = 0; j < 4; ++j) {
+          const uint32_t c = hist[top - j];
           if (cum + c >= remaining) {
-            sel = (uint32_t)v;
+            sh_prefix = prefix | ((uint32_t)(top - j) << sh);
+            sh_remaining = remaining - cum;
             break;
           }
           cum += c;
         }
-        sh_prefix = prefix | (sel << (8 * d));
-        sh_remaining = remaining - cum;
       }
       __syncthreads();
       prefix = sh_prefix;
       remaining = sh_remaining;
-      mask |= 255u << (8 * d);
+      mask |= (uint32_t)(nb - 1) << sh;
+      __syncthreads();
     }
-    // prefix = the threshold pattern; take every larger key and the first
-    // `remaining` keys equal to it, in position order.
-    const int per = (np + 1023) / 1024;
-    const int i0 = min(np, tid * per), i1 = min(np, i0 + per);
-    uint32_t c_gt = 0, c_eq = 0;
-    for (int i = i0; i < i1; ++i) {
-      const uint32_t u = key[i];
-      c_gt += u > prefix;
-      c_eq += u == prefix;
+    // prefix = the threshold pattern: keep every larger key and the first
+    // `remaining` keys equal to it, in position order
+    const int seg = (np + 15) / 16;
+    const int r0 = min(np, wv * seg), r1 = min(np, r0 + seg);
+    uint32_t n_gt = 0, n_eq = 0;
+    for (int base = r0; base < r1; base += 64) {
+      const int i = base + lane;
+      const uint32_t u = i < r1 ? key[i] : 0u;
+      n_gt += (uint32_t)__popcll(__ballot(i < r1 && u > prefix));
+      n_eq += (uint32_t)__popcll(__ballot(i < r1 && u == prefix));
     }
-    uint32_t tot;
-    const uint32_t eq_before = block_exclusive_scan(c_eq, wsum, tot);
-    const uint32_t take_eq = eq_before >= remaining ? 0u : min(c_eq, remaining - eq_before);
-    uint32_t off = block_exclusive_scan(c_gt + take_eq, wsum, tot);
-    uint32_t eq_seen = 0;
-    for (int i = i0; i < i1; ++i) {
-      const uint32_t u = key[i];
-      bool take = u > prefix;
-      if (u == prefix) {
-        take = eq_seen < take_eq;
-        ++eq_seen;
-      }
-      if (take && off < (uint32_t)k) out[off++] = i;  // the bound holds by construction; kept as a guard
+    if (lane == 0) {
+      wgt[wv] = n_gt;
+      weq[wv] = n_eq;
+    }
+    __syncthreads();
+    uint32_t gt_before = 0, eq_before = 0;
+    for (int w = 0; w < wv; ++w) {
+      gt_before += wgt[w];
+      eq_before += weq[w];
+    }
+    uint32_t off = gt_before + min(eq_before, remaining), eq_seen = eq_before;
+    for (int base = r0; base < r1; base += 64) {
+      const int i = base + lane;
+      const bool in = i < r1;
+      const uint32_t u = in ? key[i] : 0u;
+      const bool eq = in && u == prefix;
+      const uint64_t beq = __ballot(eq);
+      const bool take = in && (u > prefix || (eq && eq_seen + lanes_below(beq, lane) < remaining));
+      const uint64_t bt = __ballot(take);
+      const uint32_t o = off + lanes_below(bt, lane);
+      if (take && o < (uint32_t)k) out[o] = i;  // o < k holds by construction; kept as a guard
+      off += (uint32_t)__popcll(bt);
+      eq_seen += (uint32_t)__popcll(beq);
     }
   }
   for (int i = tid; i < kWin; i += 1024) out[k + i] = np + i;
