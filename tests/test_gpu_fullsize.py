@@ -153,3 +153,107 @@ def test_mla_shaped_stack(variant):
     assert err <= TOL
     del arena, ws, out
     torch.cuda.empty_cache()
+
+
+def test_qwen14b_shaped_append_last_group():
+    """Decode-time append at the benchmark's size and launch shape: the 14B mixed
+    stack prefilled with 8160 tokens, then 32 appended tokens (one kvk_append_token
+    call per token over all 48 layers, the last one completing block 255), then one
+    decode over all layers at 8192.  Sampled streams equal the oracle's prefill of
+    8160 tokens followed by its appends of the same 32 tokens; sampled output rows
+    match the oracle's attention over them."""
+    w = synth.workload(2)
+    say(f"case {w.name} + 32 appended tokens")
+    n_tok, n0 = w.tokens, w.tokens - 32
+    dims = kvk.make_dims(kvk.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, qscheme=w.qscheme,
+                         batch=w.batch, max_tokens=n_tok)
+    table = kvk.layer_table(dims, kvk.make_plan(w.plan))
+    info = kvk.table_query(table)
+    arena = torch.empty(info.arena_bytes, dtype=torch.uint8, device=DEV)
+    for l in range(w.n_layers):
+        if w.plan[l][0]:
+            continue
+        k, v = synth.kv_layer(w, l, device=DEV)
+        kvk.compress_layer(table, l, k[:, :, :n0].contiguous(), v[:, :, :n0].contiguous(), n0, None, arena)
+        del k, v
+    kn, vn = synth.kv_random(77, w.n_layers * w.batch, w.n_kv_heads, 32, w.head_dim, device=DEV)
+    kn = kn.reshape(w.n_layers, w.batch, w.n_kv_heads, 32, w.head_dim)
+    vn = vn.reshape(w.n_layers, w.batch, w.n_kv_heads, 32, w.head_dim)
+    for i in range(32):
+        kvk.append_token(table, 0, w.n_layers, kn[:, :, :, i].contiguous(), vn[:, :, :, i].contiguous(), n0 + i,
+                         arena)
+    q = synth.queries(w, w.n_layers, device=DEV)
+    out = torch.empty((w.n_layers, w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device=DEV)
+    ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=DEV)
+    kvk.decode_attention(table, 0, w.n_layers, q, n_tok, w.softmax_scale(), arena, out, ws)
+    torch.cuda.synchronize()
+    od = OP.Dims(OP.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, qscheme=w.qscheme,
+                 batch=w.batch, max_tokens=n_tok)
+    G = w.n_q_heads // w.n_kv_heads
+    rng = np.random.default_rng(15)
+    got_rows, ref_rows = [], []
+    for _ in range(6):
+        l, b, h = int(rng.integers(w.n_layers)), int(rng.integers(w.batch)), int(rng.integers(w.n_kv_heads))
+        a = info.anchor_of[l]
+        bits = w.plan[a][1]
+        say(f"  sample layer {l} (anchor {a}, {bits} bits) b {b} kv head {h}")
+        k, v = synth.kv_layer(w, a, device=DEV)
+        ks, vs = k[b, h, :n0].float().cpu().numpy(), v[b, h, :n0].float().cpu().numpy()
+        del k, v
+        st = OC.compress_stream(od, bits, ks, vs)
+        kt, vt = kn[a, b, h].float().cpu().numpy(), vn[a, b, h].float().cpu().numpy()
+        for i in range(32):
+            st = OC.append_token(od, bits, st, n0 + i, kt[i], vt[i])
+        sb = info.stream_bytes[a]
+        off = info.layer_offset[a] + (b * w.n_kv_heads + h) * sb
+        blocks_gpu = arena[off:off + sb].cpu().numpy()[:(n_tok // 32) * OP.block_bytes(od, bits)]
+        assert np.array_equal(blocks_gpu, st[:blocks_gpu.size]), f"stream blocks differ: {(l, b, h)}"
+        qrows = q[l, b, h * G:(h + 1) * G].float().cpu().numpy().astype(np.float64)
+        ref_rows.append(oracle_rows(od, bits, st, n_tok, qrows, w.softmax_scale()))
+        got_rows.append(out[l, b, h * G:(h + 1) * G].cpu().numpy())
+    got, ref = np.stack(got_rows), np.stack(ref_rows)
+    err = np.abs(got - ref).max() / np.abs(ref).max()
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
+    del arena, ws, out
+    torch.cuda.empty_cache()
+
+
+def test_snapkv_at_128k():
+    """The query-aware keep list at the eviction workload's size (batch 4, 131072
+    positions, 8 KV heads, 40 query heads, keep 65536) on one anchor's keys:
+    sampled streams' importances within 1e-4 of the oracle's largest, the selection
+    exactly the rule applied to the kernel's importances, and any difference from
+    the oracle's own selection at its threshold."""
+    from oracle import snapkv as S
+    w = synth.workload(4)
+    say(f"case snapkv {w.name}")
+    n, keep, G = w.tokens, w.keep_tokens, w.n_q_heads // w.n_kv_heads
+    dims = kvk.make_dims(kvk.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, batch=w.batch,
+                         max_tokens=n, keep_tokens=keep)
+    table = kvk.layer_table(dims, kvk.make_plan(w.plan))
+    k, _ = synth.kv_layer(w, 0, device=DEV)
+    q = synth.q_random(4242, w.batch, w.n_q_heads, 32, w.head_dim, device=DEV)
+    keep_out = torch.empty((w.batch, w.n_kv_heads, keep), dtype=torch.int32, device=DEV)
+    imp = torch.empty((w.batch, w.n_kv_heads, n), dtype=torch.float32, device=DEV)
+    ws = torch.empty(kvk.snapkv_workspace_bytes(table, n), dtype=torch.uint8, device=DEV)
+    kvk.snapkv_select(table, 0, k, q, n, w.softmax_scale(), keep_out, ws, importance=imp)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(16)
+    for _ in range(2):
+        b, h = int(rng.integers(w.batch)), int(rng.integers(w.n_kv_heads))
+        say(f"  sample b {b} kv head {h}")
+        kb = k[b, h:h + 1].float().cpu().numpy().astype(np.float64)
+        qb = q[b, h * G:(h + 1) * G].float().cpu().numpy().astype(np.float64)
+        ref = S.importance(qb, kb, w.softmax_scale())[0]
+        got = imp[b, h].cpu().numpy()
+        top = ref.max()
+        assert np.abs(got - ref).max() <= 1e-4 * top
+        kl = keep_out[b, h].cpu().numpy()
+        assert np.array_equal(kl, S.select(got.astype(np.float64), keep))
+        diff = np.setxor1d(kl, S.select(ref, keep))
+        if diff.size:
+            theta = np.sort(ref[:n - 32])[::-1][keep - 33]
+            assert np.all(np.abs(ref[diff] - theta) <= 1e-4 * top)
+    del k, ws, imp
+    torch.cuda.empty_cache()
