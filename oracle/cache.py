@@ -187,3 +187,34 @@ def decode_step(dims: Dims, plan, arena: np.ndarray, q: np.ndarray, n_stored: in
             out[l - l0, b] = att.gqa_attention(np.asarray(q[l - l0, b], np.float64),
                                                Kh[b], Vh[b], scale)
     return out
+
+
+def compress_arena_batched(dims: Dims, plans, Ks, Vs, keeps=None) -> np.ndarray:
+    """Arena of a batch with per-sequence plans: Ks[l], Vs[l] [B, Hkv, n, D]; the
+    arena of sequence b (plans[b], its rows of the inputs) at its base."""
+    from .plan import batched_arena_bases, sequence_dims
+    sd = sequence_dims(dims)
+    bases, total = batched_arena_bases(dims, plans)
+    arena = np.zeros(total, dtype=np.uint8)
+    for b, pl in enumerate(plans):
+        sub = compress_arena(sd, pl, [None if K is None else K[b:b + 1] for K in Ks],
+                             [None if V is None else V[b:b + 1] for V in Vs],
+                             None if keeps is None else [None if k is None else k[b:b + 1] for k in keeps])
+        arena[bases[b]:bases[b] + sub.size] = sub
+    return arena
+
+
+def decode_step_batched(dims: Dims, plans, arena: np.ndarray, q: np.ndarray, n_stored: int,
+                        scale: float, l0: int = 0, l1=None) -> np.ndarray:
+    """q [l1-l0, B, Hq, D] -> out fp64 [l1-l0, B, Hq, D]: sequence b decodes its own
+    arena with its own plan (the uniform decode step of a one-sequence table)."""
+    from .plan import batched_arena_bases, sequence_dims
+    l1 = dims.n_layers if l1 is None else l1
+    sd = sequence_dims(dims)
+    bases, _ = batched_arena_bases(dims, plans)
+    out = np.zeros((l1 - l0, dims.batch, dims.n_q_heads, dims.head_dim))
+    for b, pl in enumerate(plans):
+        size = arena_offsets(sd, pl)[1]
+        out[:, b:b + 1] = decode_step(sd, pl, arena[bases[b]:bases[b] + size], q[:, b:b + 1], n_stored,
+                                      scale, l0, l1)
+    return out

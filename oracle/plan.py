@@ -240,3 +240,34 @@ def read_bytes(dims: Dims, plan: Sequence[Action], l0: int, l1: int, n_stored: i
 def bf16_full_bytes(dims: Dims) -> int:
     """Uncompressed bf16 GQA cache of all L layers at the full prefill length."""
     return dims.n_layers * dims.batch * dims.max_tokens * dims.kv_width * 2
+
+
+# ---------------------------------------------------------------------------
+# Per-sequence plans in one batch (§2.3: the selector maps each input sequence to
+# its own plan; eq. (4) takes the realized cost per sequence i).
+# ---------------------------------------------------------------------------
+
+def sequence_dims(dims: Dims) -> Dims:
+    """The dims of one sequence of a batch (batch 1, everything else equal)."""
+    from dataclasses import replace
+    return replace(dims, batch=1)
+
+
+def batched_arena_bases(dims: Dims, plans) -> tuple:
+    """A batch whose sequences carry their own plans stores, for sequence b, the
+    arena of a one-sequence table with plans[b] at base_b; the bases are the
+    running sums of those arenas, each rounded up to 256 bytes.  Returns (bases,
+    total)."""
+    sd = sequence_dims(dims)
+    bases, cur = [], 0
+    for pl in plans:
+        bases.append(cur)
+        cur += round256(arena_offsets(sd, pl)[1])
+    return bases, cur
+
+
+def read_bytes_batched(dims: Dims, plans, l0: int, l1: int, n_stored: int) -> int:
+    """Algorithmic bytes of a decode step over [l0, l1) of a per-sequence batch: each
+    sequence reads its own distinct anchors once."""
+    sd = sequence_dims(dims)
+    return sum(read_bytes(sd, pl, l0, l1, n_stored) for pl in plans)
