@@ -38,6 +38,7 @@ extern "C" {
 #endif
 
 #define KVK_MAX_LAYERS 64
+#define KVK_MAX_BATCH_PLANS 256  /* sequences of a batch with per-sequence plans */
 #define KVK_GROUP 32 /* quantisation group: 32 tokens (keys) / 32 channels (values) */
 
 typedef enum {
@@ -231,6 +232,32 @@ typedef struct {
  * the decode workspace size.  Host only; touches no device.
  * Errors: KVK_ERR_INVALID on any violation (message via kvk_last_error()). */
 kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* plan, kvk_table** out);
+
+/* A batch whose sequences carry their own plans (§2.3: the selector maps each
+ * input sequence to its own configuration; eq. (4) takes the realized cost per
+ * sequence).  plans: host [batch][n_layers] actions, sequence b's plan at
+ * plans + b * n_layers, each validated as by kvk_layer_table.  GQA only; batch
+ * 1..KVK_MAX_BATCH_PLANS.  Sequence b is stored exactly as a one-sequence table
+ * (dims with batch 1) of plans[b] would store it, at byte base_b of the arena:
+ * base_0 = 0, base_{b+1} = base_b + that table's arena_bytes rounded up to 256.
+ * Every other entry point accepts the table: kvk_compress_layer, kvk_append_token
+ * and kvk_debug_dequantize take the batch's tensors as for one plan and serve each
+ * sequence by its own plan (a sequence whose layer inherits writes nothing there);
+ * one kvk_decode_attention call decodes the whole batch in one launch, each
+ * sequence reading its own anchors once (its work list, one item per sequence and
+ * anchor, is copied to the head of the workspace on the stream; kvk_decode_merge
+ * reads the list that kvk_decode_splits left there); kvk_read_bytes sums the
+ * sequences.  kvk_table_query reports the batch (arena_bytes, workspace_bytes,
+ * n_anchors over all sequences, rho of the mean plan); its per-layer fields are
+ * empty (anchor_of and layer_offset -1): use kvk_table_sequence_query.
+ * Errors: KVK_ERR_INVALID, KVK_ERR_UNSUPPORTED (MLA). */
+kvk_status kvk_layer_table_batched(const kvk_dims* dims, const kvk_action* plans, kvk_table** out);
+
+/* Per-sequence plans: the accounting of sequence b as its one-sequence table
+ * reports it, with layer_offset made absolute (base_b added): stream h of layer l
+ * of sequence b starts at layer_offset[l] + h * stream_bytes[l].
+ * Errors: KVK_ERR_INVALID (not a per-sequence table, b out of range). */
+kvk_status kvk_table_sequence_query(const kvk_table* table, int32_t b, kvk_table_info* out);
 
 /* Copy the table's accounting and layout into *out.  Host only. */
 kvk_status kvk_table_query(const kvk_table* table, kvk_table_info* out);

@@ -356,6 +356,7 @@ struct AppendArgs {
   int32_t pos;           // stored tokens before the call: the new token's position
   int32_t nb_cap;
   int32_t n_streams;     // B * Hkv
+  int64_t row_stride;    // elements between the rows of consecutive layers in k and v
   AppendItem items[KVK_MAX_LAYERS];
 };
 
@@ -372,7 +373,7 @@ __global__ __launch_bounds__(256) void tail_write_kernel(AppendArgs a) {
   const int sidx = idx / D, c = idx % D, t = a.pos & 31;
   const AppendItem& it = a.items[blockIdx.y];
   uint8_t* tailb = a.arena + it.region + (int64_t)sidx * it.stream_bytes + (int64_t)a.nb_cap * it.block_bytes;
-  const int64_t e = ((int64_t)it.row * a.n_streams + sidx) * D + c;
+  const int64_t e = (int64_t)it.row * a.row_stride + (int64_t)sidx * D + c;
   *reinterpret_cast<uint16_t*>(tailb + k_bf16_byte(D, t, c)) = new_token_bf16(a.k, e, a.in_f32);
   *reinterpret_cast<uint16_t*>(tailb + v_bf16_byte(D, t, c)) = new_token_bf16(a.v, e, a.in_f32);
 }
@@ -392,7 +393,7 @@ __global__ __launch_bounds__(256) void group_write_kernel(AppendArgs a) {
   const AppendItem& it = a.items[blockIdx.y];
   uint8_t* base = a.arena + it.region + (int64_t)sidx * it.stream_bytes;
   uint8_t* tailb = base + (int64_t)a.nb_cap * it.block_bytes;
-  const int64_t e0 = ((int64_t)it.row * a.n_streams + sidx) * D;
+  const int64_t e0 = (int64_t)it.row * a.row_stride + (int64_t)sidx * D;
   stage_bf16_block<D, LD>(tailb, Ks, Vs, tid);  // row 31 holds a stale slot until replaced
   __syncthreads();
   for (int c = tid; c < D; c += 256) {
@@ -478,6 +479,19 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
     return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
   if (d.kind == KVK_MLA)
     return mla_compress_layer(t, layer, k, v, in_dtype, n_tokens, keep_idx, arena, stream);
+  if (!t->seq.empty()) {  // per-sequence plans: each sequence's own table and arena
+    const int64_t elt = in_dtype == KVK_F32 ? 4 : 2;
+    const int64_t in_seq = (int64_t)d.n_kv_heads * n_tokens * d.head_dim * elt;
+    const int64_t keep_seq = (int64_t)d.n_kv_heads * d.keep_tokens;
+    for (int b = 0; b < d.batch; ++b) {
+      const kvk_status st = kvk_compress_layer(
+          t->seq[b], layer, static_cast<const uint8_t*>(k) + b * in_seq, static_cast<const uint8_t*>(v) + b * in_seq,
+          in_dtype, n_tokens, keep_idx ? keep_idx + b * keep_seq : nullptr,
+          static_cast<uint8_t*>(arena) + t->seq_base[b], stream);
+      if (st != KVK_OK) return st;
+    }
+    return KVK_OK;
+  }
 
   CompressArgs a;
   a.k = k;
@@ -515,6 +529,10 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
   return KVK_OK;
 }
 
+static kvk_status append_gqa(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
+                             int32_t in_dtype, int32_t n_stored, void* arena, int64_t row_stride,
+                             hipStream_t stream);
+
 extern "C" kvk_status kvk_append_token(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
                                        int32_t in_dtype, int32_t n_stored, void* arena, hipStream_t stream) {
   if (!t) return fail(KVK_ERR_INVALID, "kvk_append_token: NULL table");
@@ -529,7 +547,26 @@ extern "C" kvk_status kvk_append_token(const kvk_table* t, int32_t l0, int32_t l
       (reinterpret_cast<uintptr_t>(v) & 15))
     return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
   if (d.kind == KVK_MLA) return mla_append_token(t, l0, l1, k, v, in_dtype, n_stored, arena, stream);
+  if (!t->seq.empty()) {  // per-sequence plans: each sequence's rows into its own arena
+    const int64_t elt = in_dtype == KVK_F32 ? 4 : 2;
+    const int64_t row = (int64_t)d.batch * d.n_kv_heads * d.head_dim;
+    for (int b = 0; b < d.batch; ++b) {
+      const int64_t off = (int64_t)b * d.n_kv_heads * d.head_dim * elt;
+      const kvk_status st = append_gqa(t->seq[b], l0, l1, static_cast<const uint8_t*>(k) + off,
+                                       static_cast<const uint8_t*>(v) + off, in_dtype, n_stored,
+                                       static_cast<uint8_t*>(arena) + t->seq_base[b], row, stream);
+      if (st != KVK_OK) return st;
+    }
+    return KVK_OK;
+  }
+  return append_gqa(t, l0, l1, k, v, in_dtype, n_stored, arena,
+                    (int64_t)d.batch * d.n_kv_heads * d.head_dim, stream);
+}
 
+static kvk_status append_gqa(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
+                             int32_t in_dtype, int32_t n_stored, void* arena, int64_t row_stride,
+                             hipStream_t stream) {
+  const kvk_dims& d = t->d;
   AppendArgs a;
   a.k = k;
   a.v = v;
@@ -538,6 +575,7 @@ extern "C" kvk_status kvk_append_token(const kvk_table* t, int32_t l0, int32_t l
   a.pos = n_stored;
   a.nb_cap = t->nb_cap;
   a.n_streams = d.batch * d.n_kv_heads;
+  a.row_stride = row_stride;
   int n = 0;
   for (int l = l0; l < l1; ++l) {
     if (t->plan[l].inherit) continue;  // an inheriting layer stores nothing (§2.1)
@@ -581,6 +619,16 @@ extern "C" kvk_status kvk_debug_dequantize(const kvk_table* t, int32_t layer, in
     return fail(KVK_ERR_INVALID, "n_stored %d outside 0..%d", n_stored, t->cap);
   if (n_stored == 0) return KVK_OK;
   if (d.kind == KVK_MLA) return mla_debug_dequantize(t, layer, n_stored, arena, k_out, v_out, stream);
+  if (!t->seq.empty()) {
+    const int64_t per = (int64_t)d.n_kv_heads * n_stored * d.head_dim;
+    for (int b = 0; b < d.batch; ++b) {
+      const kvk_status st = kvk_debug_dequantize(t->seq[b], layer, n_stored,
+                                                 static_cast<const uint8_t*>(arena) + t->seq_base[b],
+                                                 k_out + b * per, v_out + b * per, stream);
+      if (st != KVK_OK) return st;
+    }
+    return KVK_OK;
+  }
   const int a = t->info.anchor_of[layer];
   const uint8_t* region = static_cast<const uint8_t*>(arena) + t->info.layer_offset[a];
   const int nstreams = d.batch * d.n_kv_heads;

@@ -26,6 +26,9 @@
 // fp32.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "kvk_device.h"
 #include "kvk_internal.h"
 
@@ -48,6 +51,8 @@ struct DecodeItem {
   int32_t wave_begin;    // first wave of this item within the launch (a multiple of 4)
   int32_t ws_off;        // float offset of the item's partials
   int32_t nchp;          // waves per (stream, split): 16-row chunks, padded to 1, 2 or 4
+  int32_t b0;            // first sequence of the item's streams
+  int32_t nb;            // sequences of the item (all B, or one under per-sequence plans)
 };
 
 struct DecodeArgs {
@@ -62,7 +67,15 @@ struct DecodeArgs {
   int32_t total_waves;
   int32_t n_items;
   float scale_log2;  // softmax scale * log2(e)
-  DecodeItem items[kMaxItems];
+  const DecodeItem* items_dev;  // per-sequence plans: the work list in device memory
+  DecodeItem items[kMaxItems];  // one plan: the work list in the arguments
+};
+static_assert(sizeof(DecodeArgs) <= 4096, "kernel arguments");
+
+// Combine-side fields of a work item (device memory, per-sequence plans).
+struct CombItem {
+  int64_t tail;  // byte offset of stream 0's tail block of the item
+  int32_t ws_off, nsplit, geff, stream_bytes, b0, pad;
 };
 
 struct CombineArgs {
@@ -84,6 +97,8 @@ struct CombineArgs {
   int32_t item_ws_off[kMaxItems];
   int32_t item_nsplit[kMaxItems];
   int32_t item_geff[kMaxItems];
+  const CombItem* citems;  // per-sequence plans: per item, and per (layer, sequence)
+  const int32_t* map;      // the item and the first query slot of the row group
 };
 
 __device__ __forceinline__ f4 mfma16(half8 a, half8 b, f4 c) {
@@ -534,7 +549,7 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
   constexpr int NR = ring_depth<BITS>();
   constexpr int NM = D / 16;
   constexpr int NX = (KIVI && BITS != 16) ? D / 32 : 0;
-  const int b = sidx / a.Hkv, kvh = sidx % a.Hkv;
+  const int b = it.b0 + sidx / a.Hkv, kvh = sidx % a.Hkv;  // sidx: the item's own stream index
   const int i16 = lane & 15, kg = lane >> 4;
   const int row = 16 * chunk + i16;
   const int k0 = split * it.split_blocks;
@@ -591,7 +606,13 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
   }
 }
 
-template <int D, bool KIVI>
+template <bool BATCHED>
+__device__ __forceinline__ const DecodeItem& item_at(const DecodeArgs& a, int i) {
+  if constexpr (BATCHED) return a.items_dev[i];
+  else return a.items[i];
+}
+
+template <int D, bool KIVI, bool BATCHED>
 __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
   __shared__ uint32_t lds_meta[4][2 * D];  // per-wave KIVI32 metadata slot (8D bytes)
   const int lane = threadIdx.x & 63;
@@ -603,16 +624,16 @@ __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
   int lo = 0, hi = a.n_items - 1;  // last item with wave_begin <= wave
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (a.items[mid].wave_begin <= wave) lo = mid;
+    if (item_at<BATCHED>(a, mid).wave_begin <= wave) lo = mid;
     else hi = mid - 1;
   }
-  const DecodeItem& it = a.items[lo];
+  const DecodeItem& it = item_at<BATCHED>(a, lo);
   const int local = wave - it.wave_begin;
   const int chunk = local % it.nchp;
   const int unit = local / it.nchp;
-  if (unit >= a.B * a.Hkv * it.nsplit || 16 * chunk >= it.geff) return;  // alignment padding
+  if (unit >= it.nb * a.Hkv * it.nsplit || 16 * chunk >= it.geff) return;  // alignment padding
   const int split = unit % it.nsplit;
-  const int sidx = unit / it.nsplit;  // b * Hkv + kvh
+  const int sidx = unit / it.nsplit;  // (b - b0) * Hkv + kvh
   uint32_t* lds = lds_meta[wslot];
   // A stream read by one wave is streamed non-temporally; the waves of a stream read
   // by several row chunks read it through the caches (the later reads hit).
@@ -636,7 +657,7 @@ __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
 // Merge the splits of every output row by log-sum-exp, together with the bf16 tail
 // tokens (fewer than 32), which this kernel attends to directly: one wave per
 // (layer, b, head).
-template <int D>
+template <int D, bool BATCHED>
 __global__ __launch_bounds__(256) void gqa_combine_kernel(CombineArgs a) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -644,16 +665,29 @@ __global__ __launch_bounds__(256) void gqa_combine_kernel(CombineArgs a) {
   const int li = row / (a.B * a.Hq);
   const int rem = row % (a.B * a.Hq);
   const int b = rem / a.Hq, h = rem % a.Hq;
-  const int item = a.layer_item[li];
-  const int slot = a.layer_slot0[li] + h % a.G;
+  int item, slot, nsplit, geff, ws_off, b0, sbytes;
+  int64_t tail_off;
+  if constexpr (BATCHED) {
+    const int32_t* m = a.map + ((int64_t)li * a.B + b) * 2;
+    item = m[0];
+    slot = m[1] + h % a.G;
+    const CombItem& ci = a.citems[item];
+    nsplit = ci.nsplit, geff = ci.geff, ws_off = ci.ws_off, b0 = ci.b0, sbytes = ci.stream_bytes;
+    tail_off = ci.tail;
+  } else {
+    item = a.layer_item[li];
+    slot = a.layer_slot0[li] + h % a.G;
+    nsplit = a.item_nsplit[item], geff = a.item_geff[item], ws_off = a.item_ws_off[item], b0 = 0;
+    sbytes = a.item_stream_bytes[item];
+    tail_off = a.item_tail[item];
+  }
   const int kvh = h / a.G;
-  const int sidx = b * a.Hkv + kvh;
-  const int nsplit = a.item_nsplit[item], geff = a.item_geff[item];
-  const float* base = a.ws + a.item_ws_off[item] + (((int64_t)sidx * nsplit) * geff + slot) * (D + 4);
+  const int sidx = (b - b0) * a.Hkv + kvh;  // the item's own stream index
+  const float* base = a.ws + ws_off + (((int64_t)sidx * nsplit) * geff + slot) * (D + 4);
   const int64_t stride = (int64_t)geff * (D + 4);
 
   // tail scores: lane t < ntail takes token t
-  const uint8_t* tail = a.arena + a.item_tail[item] + (int64_t)sidx * a.item_stream_bytes[item];
+  const uint8_t* tail = a.arena + tail_off + (int64_t)sidx * sbytes;
   float st = -INFINITY;
   if (lane < a.ntail) {
     const int64_t qoff = (int64_t)row * D;
@@ -717,14 +751,46 @@ using namespace kvk;
 namespace {
 
 // Everything one decode call launches: the D1 arguments (all anchors of the
-// range in one launch) and the C1 arguments.
+// range in one launch) and the C1 arguments.  Under per-sequence plans the work
+// list (one item per sequence and anchor: more than the arguments hold) goes to the
+// head of the workspace, copied there before D1 on the same stream.
 struct DecodePlan {
   DecodeArgs d1;
   CombineArgs c1;
   int kivi;
   int head_dim;
   bool any_blocks;
+  bool batched;
+  std::vector<uint8_t> list;  // the host image of the work list (per-sequence plans)
+  void* list_dev;
 };
+
+int64_t batched_items(const kvk_table* t, int32_t l0, int32_t l1) {
+  int64_t n = 0;
+  for (const kvk_table* s : t->seq) {
+    bool seen[KVK_MAX_LAYERS] = {};
+    for (int l = l0; l < l1; ++l) {
+      const int a = s->info.anchor_of[l];
+      if (!seen[a]) ++n;
+      seen[a] = true;
+    }
+  }
+  return n;
+}
+
+struct ListLayout {
+  int64_t items, citems, map, total;  // byte offsets of the sections, and the size
+};
+
+ListLayout list_layout(const kvk_table* t, int32_t l0, int32_t l1) {
+  const int64_t n = batched_items(t, l0, l1);
+  ListLayout L;
+  L.items = 0;
+  L.citems = round256(n * (int64_t)sizeof(DecodeItem));
+  L.map = L.citems + round256(n * (int64_t)sizeof(CombItem));
+  L.total = L.map + round256((int64_t)(l1 - l0) * t->d.batch * 2 * (int64_t)sizeof(int32_t));
+  return L;
+}
 
 kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
                    int32_t n_stored, float scale, const void* w_uk, const void* w_uv, const void* arena,
@@ -746,11 +812,16 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   const int32_t G = d.n_q_heads / d.n_kv_heads;
   const int32_t D = d.head_dim;
   const int32_t nbf = n_stored / KVK_GROUP, ntail = n_stored % KVK_GROUP;
+  const int32_t nl = l1 - l0;
+  const bool batched = !t->seq.empty();
+  P.batched = batched;
+  const ListLayout LL = batched ? list_layout(t, l0, l1) : ListLayout{0, 0, 0, 0};
+  float* ws = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + LL.total);  // the partials
   DecodeArgs& a = P.d1;
   CombineArgs& ca = P.c1;
   a.arena = static_cast<const uint8_t*>(arena);
   a.q = q;
-  a.ws = static_cast<float*>(workspace);
+  a.ws = ws;
   a.q_f32 = q_dtype == KVK_F32;
   a.B = d.batch;
   a.Hq = d.n_q_heads;
@@ -761,8 +832,9 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   a.nb_cap = t->nb_cap;
   a.scale_log2 = scale * kLog2e;
   a.n_items = 0;
+  a.items_dev = nullptr;
   ca.out = out;
-  ca.ws = static_cast<const float*>(workspace);
+  ca.ws = ws;
   ca.arena = static_cast<const uint8_t*>(arena);
   ca.q = q;
   ca.q_f32 = q_dtype == KVK_F32;
@@ -773,87 +845,122 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   ca.Hq = d.n_q_heads;
   ca.Hkv = d.n_kv_heads;
   ca.G = G;
-  ca.n_layers = l1 - l0;
-  ca.n_rows = (l1 - l0) * d.batch * d.n_q_heads;
+  ca.n_layers = nl;
+  ca.n_rows = nl * d.batch * d.n_q_heads;
+  ca.citems = nullptr;
+  ca.map = nullptr;
 
   const int64_t split_target = gqa_split_target(t, l0, l1);
-  // One work item per distinct anchor read by the range (§2.1 depth sharing).
-  int item_of_anchor[KVK_MAX_LAYERS];
-  for (int l = 0; l < KVK_MAX_LAYERS; ++l) item_of_anchor[l] = -1;
-  int64_t ws_floats = 0, waves = 0;
-  for (int l = l0; l < l1; ++l) {
-    const int anc = t->info.anchor_of[l];
-    if (item_of_anchor[anc] < 0) {
-      const int n = a.n_items++;
-      DecodeItem& it = a.items[n];
-      const int rb = anc > l0 ? anc : l0;
-      const int re = t->next_anchor[anc] < l1 ? t->next_anchor[anc] : l1;
-      it.region = t->info.layer_offset[anc];
-      it.stream_bytes = (int32_t)t->info.stream_bytes[anc];
-      it.block_bytes = (int32_t)t->block_bytes[anc];
-      it.bits = t->bits[anc];
-      it.q_layer0 = rb - l0;
-      it.geff = G * (re - rb);
-      it.split_blocks = split_blocks_for(it.bits, d.qscheme, D, nbf, split_target);
-      it.nsplit = n_splits(nbf, it.split_blocks);
-      const int nch = (it.geff + 15) / 16;
-      it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : 4);
-      waves = (waves + 3) / 4 * 4;  // a chunk group never straddles a workgroup
-      it.wave_begin = (int32_t)waves;
-      waves += (int64_t)d.batch * d.n_kv_heads * it.nsplit * it.nchp;
-      it.ws_off = (int32_t)ws_floats;
-      ws_floats += (int64_t)d.batch * d.n_kv_heads * it.nsplit * it.geff * (D + 4);
-      ca.item_ws_off[n] = it.ws_off;
-      ca.item_nsplit[n] = it.nsplit;
-      ca.item_geff[n] = it.geff;
-      ca.item_tail[n] = it.region + (int64_t)t->nb_cap * it.block_bytes;
-      ca.item_stream_bytes[n] = it.stream_bytes;
-      item_of_anchor[anc] = n;
+  // One work item per distinct anchor read by the range (§2.1 depth sharing): per
+  // anchor for all sequences, or per (sequence, anchor) under per-sequence plans.
+  std::vector<DecodeItem> items;
+  const int ngroups = batched ? d.batch : 1;
+  std::vector<int32_t> l_item((size_t)ngroups * nl), l_slot((size_t)ngroups * nl);
+  int64_t ws_floats = 0;
+  auto add_group = [&](const kvk_table* s, int g, int b0, int nb, int64_t base) {
+    int item_of_anchor[KVK_MAX_LAYERS];
+    for (int l = 0; l < KVK_MAX_LAYERS; ++l) item_of_anchor[l] = -1;
+    for (int l = l0; l < l1; ++l) {
+      const int anc = s->info.anchor_of[l];
+      if (item_of_anchor[anc] < 0) {
+        DecodeItem it;
+        const int rb = anc > l0 ? anc : l0;
+        const int re = s->next_anchor[anc] < l1 ? s->next_anchor[anc] : l1;
+        it.region = base + s->info.layer_offset[anc];
+        it.stream_bytes = (int32_t)s->info.stream_bytes[anc];
+        it.block_bytes = (int32_t)s->block_bytes[anc];
+        it.bits = s->bits[anc];
+        it.q_layer0 = rb - l0;
+        it.geff = G * (re - rb);
+        it.split_blocks = split_blocks_for(it.bits, d.qscheme, D, nbf, split_target);
+        it.nsplit = n_splits(nbf, it.split_blocks);
+        const int nch = (it.geff + 15) / 16;
+        it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : 4);
+        it.b0 = b0;
+        it.nb = nb;
+        it.ws_off = (int32_t)ws_floats;
+        ws_floats += (int64_t)nb * d.n_kv_heads * it.nsplit * it.geff * (D + 4);
+        it.wave_begin = 0;
+        item_of_anchor[anc] = (int)items.size();
+        items.push_back(it);
+      }
+      const int ii = item_of_anchor[anc];
+      l_item[(size_t)g * nl + (l - l0)] = ii;
+      l_slot[(size_t)g * nl + (l - l0)] = (l - l0 - items[ii].q_layer0) * G;
     }
-    const int ii = item_of_anchor[anc];
-    ca.layer_item[l - l0] = ii;
-    ca.layer_slot0[l - l0] = (l - l0 - a.items[ii].q_layer0) * G;
-  }
+  };
+  if (!batched) add_group(t, 0, 0, d.batch, 0);
+  else
+    for (int b = 0; b < d.batch; ++b) add_group(t->seq[b], b, b, 1, t->seq_base[b]);
+  const int n_it = (int)items.size();
+
   // Launch order: the waves that take longest per split (the low-bit items, whose
   // unpacking makes them compute-bound) first, so that the launch ends on short
   // waves.  Item indices follow the new order; wave_begin stays increasing.
-  {
-    auto cost_rank = [](int bits) { return bits == 2 ? 0 : (bits == 4 ? 1 : (bits == 8 ? 2 : 3)); };
-    int order[kMaxItems], n_it = a.n_items;
-    for (int k = 0; k < n_it; ++k) order[k] = k;
-    for (int k = 1; k < n_it; ++k)  // stable insertion sort by cost rank
-      for (int m = k; m > 0 && cost_rank(a.items[order[m]].bits) < cost_rank(a.items[order[m - 1]].bits); --m) {
-        const int tmp = order[m];
-        order[m] = order[m - 1];
-        order[m - 1] = tmp;
-      }
-    DecodeItem sorted[kMaxItems];
-    int new_index[kMaxItems];
-    int64_t wv = 0;
+  auto cost_rank = [](int bits) { return bits == 2 ? 0 : (bits == 4 ? 1 : (bits == 8 ? 2 : 3)); };
+  std::vector<int> order(n_it), new_index(n_it);
+  for (int k = 0; k < n_it; ++k) order[k] = k;
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int x, int y) { return cost_rank(items[x].bits) < cost_rank(items[y].bits); });
+  std::vector<DecodeItem> sorted(n_it);
+  int64_t waves = 0;
+  for (int k = 0; k < n_it; ++k) {
+    DecodeItem it = items[order[k]];
+    waves = (waves + 3) / 4 * 4;  // a chunk group never straddles a workgroup
+    it.wave_begin = (int32_t)waves;
+    waves += (int64_t)it.nb * d.n_kv_heads * it.nsplit * it.nchp;
+    sorted[k] = it;
+    new_index[order[k]] = k;
+  }
+  if ((size_t)LL.total + (size_t)ws_floats * sizeof(float) > ws_bytes)
+    return fail(KVK_ERR_BUFFER, "workspace %zu bytes < %lld needed", ws_bytes,
+                (long long)(LL.total + ws_floats * (int64_t)sizeof(float)));
+  if (ws_floats > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "workspace exceeds 2^31 floats");
+  if (waves > 0x7ffffff0LL) return fail(KVK_ERR_UNSUPPORTED, "too many decode waves");
+  a.n_items = n_it;
+  a.total_waves = (int32_t)waves;
+  if (!batched) {
     for (int k = 0; k < n_it; ++k) {
-      DecodeItem it = a.items[order[k]];
-      wv = (wv + 3) / 4 * 4;
-      const int64_t nw = (int64_t)d.batch * d.n_kv_heads * it.nsplit * it.nchp;
-      it.wave_begin = (int32_t)wv;
-      wv += nw;
-      sorted[k] = it;
-      new_index[order[k]] = k;
+      const DecodeItem& it = sorted[k];
+      a.items[k] = it;
       ca.item_ws_off[k] = it.ws_off;
       ca.item_nsplit[k] = it.nsplit;
       ca.item_geff[k] = it.geff;
       ca.item_tail[k] = it.region + (int64_t)t->nb_cap * it.block_bytes;
       ca.item_stream_bytes[k] = it.stream_bytes;
     }
-    for (int k = 0; k < n_it; ++k) a.items[k] = sorted[k];
-    for (int l = l0; l < l1; ++l) ca.layer_item[l - l0] = new_index[ca.layer_item[l - l0]];
-    waves = wv;
+    for (int l = 0; l < nl; ++l) {
+      ca.layer_item[l] = new_index[l_item[l]];
+      ca.layer_slot0[l] = l_slot[l];
+    }
+  } else {
+    if ((int64_t)n_it * (int64_t)sizeof(DecodeItem) > LL.citems) return fail(KVK_ERR_DEVICE, "work list size");
+    P.list.assign((size_t)LL.total, 0);
+    DecodeItem* di = reinterpret_cast<DecodeItem*>(P.list.data() + LL.items);
+    CombItem* ci = reinterpret_cast<CombItem*>(P.list.data() + LL.citems);
+    int32_t* map = reinterpret_cast<int32_t*>(P.list.data() + LL.map);
+    for (int k = 0; k < n_it; ++k) {
+      const DecodeItem& it = sorted[k];
+      di[k] = it;
+      ci[k].tail = it.region + (int64_t)t->nb_cap * it.block_bytes;
+      ci[k].ws_off = it.ws_off;
+      ci[k].nsplit = it.nsplit;
+      ci[k].geff = it.geff;
+      ci[k].stream_bytes = it.stream_bytes;
+      ci[k].b0 = it.b0;
+      ci[k].pad = 0;
+    }
+    for (int l = 0; l < nl; ++l)
+      for (int b = 0; b < d.batch; ++b) {
+        map[((int64_t)l * d.batch + b) * 2] = new_index[l_item[(size_t)b * nl + l]];
+        map[((int64_t)l * d.batch + b) * 2 + 1] = l_slot[(size_t)b * nl + l];
+      }
+    P.list_dev = workspace;
+    uint8_t* wsb = static_cast<uint8_t*>(workspace);
+    a.items_dev = reinterpret_cast<const DecodeItem*>(wsb + LL.items);
+    ca.citems = reinterpret_cast<const CombItem*>(wsb + LL.citems);
+    ca.map = reinterpret_cast<const int32_t*>(wsb + LL.map);
   }
-  if ((size_t)ws_floats * sizeof(float) > ws_bytes)
-    return fail(KVK_ERR_BUFFER, "workspace %zu bytes < %lld needed", ws_bytes,
-                (long long)(ws_floats * sizeof(float)));
-  if (ws_floats > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "workspace exceeds 2^31 floats");
-  if (waves > 0x7ffffff0LL) return fail(KVK_ERR_UNSUPPORTED, "too many decode waves");
-  a.total_waves = (int32_t)waves;
   P.kivi = d.qscheme == KVK_Q_KIVI32;
   P.head_dim = D;
   P.any_blocks = nbf > 0 && waves > 0;
@@ -861,15 +968,21 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
 }
 
 kvk_status launch_d1(const DecodePlan& P, hipStream_t st) {
+  if (P.batched) {  // the work list D1 and C1 read (C1 reads what D1's call copied)
+    const hipError_t e = hipMemcpyAsync(P.list_dev, P.list.data(), P.list.size(), hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "work list copy: %s", hipGetErrorString(e));
+  }
   if (!P.any_blocks) return KVK_OK;
   const unsigned grid = (unsigned)((P.d1.total_waves + 3) / 4);
+#define KVK_D1(DD, KK, BB) hipLaunchKernelGGL((gqa_decode_kernel<DD, KK, BB>), dim3(grid), dim3(256), 0, st, P.d1)
   if (P.head_dim == 128) {
-    if (P.kivi) hipLaunchKernelGGL((gqa_decode_kernel<128, true>), dim3(grid), dim3(256), 0, st, P.d1);
-    else hipLaunchKernelGGL((gqa_decode_kernel<128, false>), dim3(grid), dim3(256), 0, st, P.d1);
+    if (P.kivi) { if (P.batched) KVK_D1(128, true, true); else KVK_D1(128, true, false); }
+    else { if (P.batched) KVK_D1(128, false, true); else KVK_D1(128, false, false); }
   } else {
-    if (P.kivi) hipLaunchKernelGGL((gqa_decode_kernel<64, true>), dim3(grid), dim3(256), 0, st, P.d1);
-    else hipLaunchKernelGGL((gqa_decode_kernel<64, false>), dim3(grid), dim3(256), 0, st, P.d1);
+    if (P.kivi) { if (P.batched) KVK_D1(64, true, true); else KVK_D1(64, true, false); }
+    else { if (P.batched) KVK_D1(64, false, true); else KVK_D1(64, false, false); }
   }
+#undef KVK_D1
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "decode launch: %s", hipGetErrorString(e));
   return KVK_OK;
@@ -877,8 +990,13 @@ kvk_status launch_d1(const DecodePlan& P, hipStream_t st) {
 
 kvk_status launch_c1(const DecodePlan& P, hipStream_t st) {
   const unsigned grid = (unsigned)((P.c1.n_rows + 3) / 4);
-  if (P.head_dim == 128) hipLaunchKernelGGL(gqa_combine_kernel<128>, dim3(grid), dim3(256), 0, st, P.c1);
-  else hipLaunchKernelGGL(gqa_combine_kernel<64>, dim3(grid), dim3(256), 0, st, P.c1);
+  if (P.head_dim == 128) {
+    if (P.batched) hipLaunchKernelGGL((gqa_combine_kernel<128, true>), dim3(grid), dim3(256), 0, st, P.c1);
+    else hipLaunchKernelGGL((gqa_combine_kernel<128, false>), dim3(grid), dim3(256), 0, st, P.c1);
+  } else {
+    if (P.batched) hipLaunchKernelGGL((gqa_combine_kernel<64, true>), dim3(grid), dim3(256), 0, st, P.c1);
+    else hipLaunchKernelGGL((gqa_combine_kernel<64, false>), dim3(grid), dim3(256), 0, st, P.c1);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "combine launch: %s", hipGetErrorString(e));
   return KVK_OK;
@@ -909,6 +1027,12 @@ kvk_status mla_check(const kvk_table* t, int32_t l0, int32_t l1, const void* q, 
 }
 
 }  // namespace
+
+namespace kvk {
+int64_t gqa_batched_list_bytes(const kvk_table* t, int32_t l0, int32_t l1) {
+  return t->seq.empty() ? 0 : list_layout(t, l0, l1).total;
+}
+}  // namespace kvk
 
 extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
                                            int32_t q_dtype, int32_t n_stored, float scale,
@@ -976,6 +1100,17 @@ extern "C" kvk_status kvk_read_bytes(const kvk_table* t, int32_t l0, int32_t l1,
     return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, d.n_layers);
   if (n_stored < 0 || n_stored > t->cap)
     return fail(KVK_ERR_INVALID, "n_stored %d outside 0..%d", n_stored, t->cap);
+  if (!t->seq.empty()) {  // per-sequence plans: each sequence's distinct anchors, once
+    int64_t sum = 0;
+    for (const kvk_table* s : t->seq) {
+      int64_t one = 0;
+      const kvk_status st = kvk_read_bytes(s, l0, l1, n_stored, &one);
+      if (st != KVK_OK) return st;
+      sum += one;
+    }
+    *out_bytes = sum;
+    return KVK_OK;
+  }
   bool seen[KVK_MAX_LAYERS] = {false};
   int64_t total = 0;
   const bool mla = d.kind == KVK_MLA;

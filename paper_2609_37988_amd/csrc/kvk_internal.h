@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <string>
+#include <vector>
 
 #include "kvk.h"
 
@@ -17,6 +18,13 @@ struct kvk_table {
   int32_t next_anchor[KVK_MAX_LAYERS];  // first anchor after l (n_layers if none)
   int32_t cap;                          // stored tokens capacity per stream
   int32_t nb_cap;                       // full-block capacity per stream (cap / 32)
+  // Per-sequence plans: sequence b is the one-sequence table seq[b], whose arena sits
+  // at byte seq_base[b] of the batch's arena.  Empty for a table with one plan.
+  std::vector<kvk_table*> seq;
+  std::vector<int64_t> seq_base;
+  ~kvk_table() {
+    for (kvk_table* s : seq) delete s;
+  }
 };
 
 namespace kvk {
@@ -44,6 +52,10 @@ inline int32_t ring_depth_for(int32_t bits) { return gqa_ring_depth(bits); }
 int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes);
 // Bytes per D1 split for a decode over layers [l0, l1) of a GQA table (see table.cpp).
 int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1);
+
+// Bytes at the head of the workspace that hold the device-side work list of a
+// decode over [l0, l1) of a per-sequence table (decode.hip).
+int64_t gqa_batched_list_bytes(const kvk_table* t, int32_t l0, int32_t l1);
 
 // Number of decode splits of one stream holding `n_blocks` blocks.
 inline int32_t n_splits(int32_t n_blocks, int32_t split_blocks) {

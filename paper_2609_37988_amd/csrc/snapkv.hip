@@ -385,7 +385,9 @@ extern "C" kvk_status kvk_snapkv_select(const kvk_table* t, int32_t layer, const
   if (st != KVK_OK) return st;
   const kvk_dims& d = t->d;
   if (layer < 0 || layer >= d.n_layers) return fail(KVK_ERR_INVALID, "layer %d out of range", layer);
-  if (t->plan[layer].inherit) return KVK_OK;  // an inheriting layer stores nothing to select from
+  // an inheriting layer stores nothing to select from (per-sequence plans: every
+  // sequence is scored; the write uses the lists of the sequences that store)
+  if (t->seq.empty() && t->plan[layer].inherit) return KVK_OK;
   if (!k || !q_obs || !keep_out || !workspace) return fail(KVK_ERR_INVALID, "snapkv: NULL buffer");
   if (in_dtype != KVK_BF16) return fail(KVK_ERR_UNSUPPORTED, "snapkv: keys and queries must be bf16");
   if (!(scale == scale)) return fail(KVK_ERR_INVALID, "snapkv: scale is NaN");

@@ -48,15 +48,19 @@ int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1) {
   // about kSplitWaves waves: two rounds of the D1 wave slots of an MI355X (256 CUs
   // x 8 waves).  Measured on the 14B mixed stack: 1 MiB splits 3.54 ms, 2 MiB 3.44,
   // one split per stream (<= 4 MiB) 3.35.  Between 1 MiB and 16 MiB; computed from
-  // the capacity, so the workspace size bounds every n_stored.
+  // the capacity, so the workspace size bounds every n_stored.  A per-sequence
+  // table counts every sequence's distinct anchors.
   constexpr int64_t kSplitWaves = 4096;
-  bool seen[KVK_MAX_LAYERS] = {};
   int64_t total = 0;
-  for (int l = l0; l < l1; ++l) {
-    const int32_t a = t->info.anchor_of[l];
-    if (seen[a]) continue;
-    seen[a] = true;
-    total += (int64_t)t->d.batch * t->d.n_kv_heads * t->nb_cap * t->block_bytes[a];
+  const std::vector<kvk_table*> one(1, const_cast<kvk_table*>(t));
+  for (const kvk_table* s : t->seq.empty() ? one : t->seq) {
+    bool seen[KVK_MAX_LAYERS] = {};
+    for (int l = l0; l < l1; ++l) {
+      const int32_t a = s->info.anchor_of[l];
+      if (seen[a]) continue;
+      seen[a] = true;
+      total += (int64_t)s->d.batch * s->d.n_kv_heads * s->nb_cap * s->block_bytes[a];
+    }
   }
   int64_t target = total / kSplitWaves;
   if (target < (1LL << 20)) target = 1LL << 20;
@@ -294,6 +298,75 @@ extern "C" kvk_status kvk_table_query(const kvk_table* t, kvk_table_info* out) {
 
 extern "C" void kvk_table_destroy(kvk_table* t) { delete t; }
 
+extern "C" kvk_status kvk_layer_table_batched(const kvk_dims* dims, const kvk_action* plans,
+                                              kvk_table** out) {
+  if (!dims || !plans || !out) return fail(KVK_ERR_INVALID, "kvk_layer_table_batched: NULL argument");
+  *out = nullptr;
+  const kvk_dims& d = *dims;
+  if (d.kind != KVK_GQA) return fail(KVK_ERR_UNSUPPORTED, "per-sequence plans: GQA tables only");
+  if (d.batch < 1 || d.batch > KVK_MAX_BATCH_PLANS)
+    return fail(KVK_ERR_INVALID, "batch %d outside 1..%d for per-sequence plans", d.batch, KVK_MAX_BATCH_PLANS);
+  if (d.n_layers < 1 || d.n_layers > KVK_MAX_LAYERS)
+    return fail(KVK_ERR_INVALID, "n_layers %d outside 1..%d", d.n_layers, KVK_MAX_LAYERS);
+  kvk_table* t = new (std::nothrow) kvk_table();
+  if (!t) return fail(KVK_ERR_INVALID, "out of host memory");
+  kvk_dims one = d;
+  one.batch = 1;
+  int64_t base = 0;
+  double cost = 0.0, stored = 0.0;
+  for (int b = 0; b < d.batch; ++b) {
+    kvk_table* s = nullptr;
+    const kvk_status st = kvk_layer_table(&one, plans + (int64_t)b * d.n_layers, &s);
+    if (st != KVK_OK) {
+      delete t;
+      return st;
+    }
+    t->seq.push_back(s);
+    t->seq_base.push_back(base);
+    base += round256(s->info.arena_bytes);
+    cost += s->info.cost_bits_per_token;
+    stored += s->info.rho_realized > 0 ? (double)d.n_layers * d.max_tokens * 4.0 * d.n_kv_heads * d.head_dim /
+                                             s->info.rho_realized
+                                       : 0.0;
+  }
+  t->d = d;
+  t->cap = t->seq[0]->cap;
+  t->nb_cap = t->seq[0]->nb_cap;
+  kvk_table_info& inf = t->info;
+  std::memset(&inf, 0, sizeof(inf));
+  for (int l = 0; l < d.n_layers; ++l) {
+    inf.anchor_of[l] = -1;
+    inf.layer_offset[l] = -1;
+  }
+  inf.arena_bytes = base;
+  inf.stored_tokens_cap = t->cap;
+  inf.c0_bits_per_token = t->seq[0]->info.c0_bits_per_token;
+  inf.cost_bits_per_token = cost / d.batch;  // the batch's mean plan
+  inf.rho = inf.c0_bits_per_token / inf.cost_bits_per_token;
+  const double bf16_full = (double)d.n_layers * d.batch * d.max_tokens * 4.0 * d.n_kv_heads * d.head_dim;
+  inf.rho_realized = stored > 0 ? bf16_full / stored : 0.0;
+  for (const kvk_table* s : t->seq) inf.n_anchors += s->info.n_anchors;
+  size_t ws = 0;
+  const kvk_status st = kvk_workspace_bytes(t, 0, d.n_layers, &ws);
+  if (st != KVK_OK) {
+    delete t;
+    return st;
+  }
+  inf.workspace_bytes = (int64_t)ws;
+  *out = t;
+  return KVK_OK;
+}
+
+extern "C" kvk_status kvk_table_sequence_query(const kvk_table* t, int32_t b, kvk_table_info* out) {
+  if (!t || !out) return fail(KVK_ERR_INVALID, "kvk_table_sequence_query: NULL argument");
+  if (t->seq.empty()) return fail(KVK_ERR_INVALID, "not a table with per-sequence plans");
+  if (b < 0 || b >= (int32_t)t->seq.size()) return fail(KVK_ERR_INVALID, "sequence %d out of range", b);
+  *out = t->seq[b]->info;
+  for (int l = 0; l < t->d.n_layers; ++l)
+    if (out->layer_offset[l] >= 0) out->layer_offset[l] += t->seq_base[b];
+  return KVK_OK;
+}
+
 extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_t l1, size_t* out) {
   if (!t || !out) return fail(KVK_ERR_INVALID, "kvk_workspace_bytes: NULL argument");
   if (l0 < 0 || l1 > t->d.n_layers || l0 >= l1)
@@ -303,6 +376,19 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
     MlaWorkspace ws;
     mla_workspace(t, l0, l1, &ws);
     *out = (size_t)ws.total;
+    return KVK_OK;
+  }
+  if (!t->seq.empty()) {
+    // the device-side work list, then every sequence's split partials (each sized
+    // with its own, smaller, split target: the batch's longer splits need no more)
+    size_t total = (size_t)gqa_batched_list_bytes(t, l0, l1);
+    for (const kvk_table* s : t->seq) {
+      size_t one = 0;
+      const kvk_status st = kvk_workspace_bytes(s, l0, l1, &one);
+      if (st != KVK_OK) return st;
+      total += one;
+    }
+    *out = total;
     return KVK_OK;
   }
   const int32_t G = d.n_q_heads / d.n_kv_heads;

@@ -68,6 +68,8 @@ def load() -> ctypes.CDLL:
             "kvk_table_query": (I32, [P, ctypes.POINTER(TableInfo)]),
             "kvk_table_destroy": (None, [P]),
             "kvk_workspace_bytes": (I32, [P, I32, I32, ctypes.POINTER(ctypes.c_size_t)]),
+            "kvk_layer_table_batched": (I32, [P, P, ctypes.POINTER(P)]),
+            "kvk_table_sequence_query": (I32, [P, I32, P]),
             "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
             "kvk_append_token": (I32, [P, I32, I32, P, P, I32, I32, P, P]),
             "kvk_snapkv_workspace_bytes": (I32, [P, I32, ctypes.POINTER(ctypes.c_size_t)]),
@@ -93,7 +95,7 @@ def load() -> ctypes.CDLL:
 
 def exported_symbols() -> List[str]:
     """Names of the C entry points the binding expects libkvk to export."""
-    return ["kvk_layer_table", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
+    return ["kvk_layer_table", "kvk_layer_table_batched", "kvk_table_sequence_query", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
             "kvk_compress_layer", "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
             "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge",
             "kvk_read_bytes", "kvk_debug_dequantize",
@@ -184,6 +186,34 @@ def layer_table(dims: Dims, plan: Sequence[Action]) -> Table:
     h = ctypes.c_void_p()
     _check(lib.kvk_layer_table(ctypes.byref(dims), arr, ctypes.byref(h)))
     return Table(h, dims, plan)
+
+
+def layer_table_batched(dims: Dims, plans: Sequence[Sequence[Action]]) -> Table:
+    """A batch whose sequences carry their own plans: plans[b] is sequence b's plan."""
+    _need(len(plans) == dims.batch and all(len(p) == dims.n_layers for p in plans),
+          "plans must hold batch plans of n_layers actions")
+    flat = [a for p in plans for a in p]
+    arr = (Action * len(flat))(*flat)
+    h = ctypes.c_void_p()
+    _check(load().kvk_layer_table_batched(ctypes.byref(dims), arr, ctypes.byref(h)))
+    t = Table(h, dims, plans[0])
+    t.plans = [list(p) for p in plans]
+    return t
+
+
+def _info(inf, L) -> Info:
+    return Info(inf.arena_bytes, inf.workspace_bytes, inf.n_anchors, inf.stored_tokens_cap,
+                inf.cost_bits_per_token, inf.c0_bits_per_token, inf.rho, inf.rho_realized,
+                list(inf.anchor_of[:L]), list(inf.layer_offset[:L]), list(inf.layer_bytes[:L]),
+                list(inf.stream_bytes[:L]), list(inf.layer_cost_bits[:L]),
+                list(inf.layer_bits_per_elt[:L]))
+
+
+def table_sequence_query(t: Table, b: int) -> Info:
+    """Per-sequence plans: sequence b's accounting, layer offsets absolute in the arena."""
+    inf = TableInfo()
+    _check(load().kvk_table_sequence_query(t.handle, b, ctypes.byref(inf)))
+    return _info(inf, t.dims.n_layers)
 
 
 def table_query(t: Table) -> Info:

@@ -311,3 +311,48 @@ def test_mla_entry_points_reject_bad_arguments_without_launching():
     _raw(I, "kvk_append_token", h, 0, 2, f, f, kvk.BF16, 64, f, None)        # stream full
     _raw(I, "kvk_append_token", h, 0, 2, f, Pv(264), kvk.BF16, 10, f, None)  # k^R misaligned
     _raw(kvk.OK, "kvk_append_token", h, 1, 2, f, f, kvk.BF16, 10, f, None)   # inheritors only: no-op
+
+
+def test_batched_table_accounting_matches_oracle():
+    """Per-sequence plans: sequence b's region starts at the oracle's base_b, its
+    per-layer offsets and stream sizes are those of its one-sequence table, and the
+    algorithmic read bytes are the sum over the sequences."""
+    from oracle import plan as OP
+    plans = [[(0, 4), (1, 16), (0, 8), (0, 2)], [(0, 16), (0, 2), (1, 16), (1, 16)],
+             [(0, 8), (0, 8), (0, 4), (1, 16)]]
+    d = kvk.make_dims(kvk.GQA, 4, 8, 2, 128, batch=3, max_tokens=300)
+    t = kvk.layer_table_batched(d, [kvk.make_plan(p) for p in plans])
+    od = OP.Dims(OP.GQA, 4, 8, 2, 128, batch=3, max_tokens=300)
+    oplans = [[OP.Action(bool(a), b) for a, b in p] for p in plans]
+    bases, total = OP.batched_arena_bases(od, oplans)
+    info = kvk.table_query(t)
+    assert info.arena_bytes == total and info.n_anchors == 8 and info.workspace_bytes > 0
+    sd = OP.sequence_dims(od)
+    for b in range(3):
+        si = kvk.table_sequence_query(t, b)
+        offs, _ = OP.arena_offsets(sd, oplans[b])
+        assert si.layer_offset == [o + bases[b] if o >= 0 else -1 for o in offs]
+        assert si.anchor_of == OP.anchor_of(oplans[b])
+        for l, (inh, bits) in enumerate(plans[b]):
+            if not inh:
+                assert si.stream_bytes[l] == OP.stream_bytes(sd, bits)
+    for n in (0, 31, 200, 300):
+        assert kvk.read_bytes(t, 0, 4, n) == OP.read_bytes_batched(od, oplans, 0, 4, n)
+        assert kvk.read_bytes(t, 1, 3, n) == OP.read_bytes_batched(od, oplans, 1, 3, n)
+
+
+def test_batched_table_rejects_bad_input():
+    d = kvk.make_dims(kvk.GQA, 2, 4, 1, 128, batch=2, max_tokens=64)
+    with pytest.raises(kvk.KvkError):
+        kvk.layer_table_batched(d, [kvk.make_plan([(0, 4), (1, 16)]), kvk.make_plan([(1, 16), (0, 4)])])
+    with pytest.raises(kvk.KvkError):
+        kvk.layer_table_batched(d, [kvk.make_plan([(0, 4), (1, 16)]), kvk.make_plan([(0, 3), (1, 16)])])
+    m = kvk.make_dims(kvk.MLA, 2, 32, 4, 128, 256, 64, 128, 128, batch=2, max_tokens=64)
+    with pytest.raises(kvk.KvkError):
+        kvk.layer_table_batched(m, [kvk.make_plan([(0, 8, 128), (1, 16, 0)])] * 2)
+    t = kvk.layer_table_batched(d, [kvk.make_plan([(0, 4), (1, 16)]), kvk.make_plan([(0, 8), (0, 2)])])
+    with pytest.raises(kvk.KvkError):
+        kvk.table_sequence_query(t, 2)
+    u = kvk.layer_table(d, kvk.make_plan([(0, 4), (1, 16)]))
+    with pytest.raises(kvk.KvkError):
+        kvk.table_sequence_query(u, 0)
