@@ -46,6 +46,8 @@ def parse():
     ap.add_argument("--variant", default=None)
     ap.add_argument("--qscheme", default="kivi32", choices=["kivi32", "symrow"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--per-sequence", action="store_true",
+                    help="workload 2 with a plan per sequence (each drawn like the shared one)")
     ap.add_argument("--cpu-layers", type=int, default=0, help="layers in the CPU sample (0: auto)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
@@ -374,7 +376,15 @@ def main():
     n_stored = w.keep_tokens if w.keep_tokens else n_tok
     dims = kvk.make_dims(kvk.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, qscheme=w.qscheme,
                          batch=w.batch, max_tokens=n_tok, keep_tokens=w.keep_tokens)
-    table = kvk.layer_table(dims, kvk.make_plan(w.plan))
+    plans = None
+    if args.per_sequence:
+        if args.config != 2:
+            print("--per-sequence applies to workload 2", file=sys.stderr)
+            sys.exit(2)
+        plans = synth.plans_per_sequence(w)
+        table = kvk.layer_table_batched(dims, [kvk.make_plan(p) for p in plans])
+    else:
+        table = kvk.layer_table(dims, kvk.make_plan(w.plan))
     info = kvk.table_query(table)
     log(f"workload {w.name}: arena {info.arena_bytes / 1e9:.2f} GB, rho eq.(2) {info.rho:.2f}, "
         f"realized {info.rho_realized:.2f}, anchors {info.n_anchors}")
@@ -390,7 +400,7 @@ def main():
         snap_keep = torch.empty((w.batch, w.n_kv_heads, w.keep_tokens), dtype=torch.int32, device=dev)
         q_obs = synth.q_random(4242, w.batch, w.n_q_heads, 32, w.head_dim, device=dev)
     for l in range(w.n_layers):
-        if w.plan[l][0]:
+        if (w.plan[l][0] if plans is None else all(p[l][0] for p in plans)):
             continue
         k, v = synth.kv_layer(w, l, device=dev)
         keep = synth.keep_positions(w, l, device=dev) if w.keep_tokens else None
@@ -412,7 +422,13 @@ def main():
         e1.record()
         torch.cuda.synchronize()
         w1_ms += e0.elapsed_time(e1)
-        w1_bytes += 2 * k.numel() * k.element_size() * n_stored // n_tok + info.layer_bytes[l]
+        if plans is None:
+            w1_bytes += 2 * k.numel() * k.element_size() * n_stored // n_tok + info.layer_bytes[l]
+        else:
+            for b, p in enumerate(plans):
+                if not p[l][0]:
+                    w1_bytes += (2 * k[b].numel() * k.element_size() * n_stored // n_tok +
+                                 kvk.table_sequence_query(table, b).layer_bytes[l])
         del k, v, keep
     torch.cuda.empty_cache()
     log(f"prefill write: {w1_ms:.1f} ms over {info.n_anchors} anchors")
@@ -447,7 +463,7 @@ def main():
         f"D1 {d1_avg * 1e3:.1f} us ({d1_gbs:.1f} GB/s)")
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and plans is None:
         nl = args.cpu_layers or (w.n_layers if args.config in (1, 2) else 4)
         cpu = cpu_baseline(w, table, n_stored, scale, nl, n_batch=2 if args.config in (1, 2) else 1)
         log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
@@ -457,9 +473,10 @@ def main():
     log(f"append: {app}")
 
     bits_mix = {}
-    for e in w.plan:
-        if not e[0]:
-            bits_mix[str(e[1])] = bits_mix.get(str(e[1]), 0) + 1
+    for p in ([w.plan] if plans is None else plans):
+        for e in p:
+            if not e[0]:
+                bits_mix[str(e[1])] = bits_mix.get(str(e[1]), 0) + 1
     line = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -476,17 +493,20 @@ def main():
         "dtype": "u2/u4/u8 codes + bf16 cache; f16/bf16 MFMA, f32 accumulate",
         "data": "synthetic",
         "config": {
-            "workload": w.name, "layers": w.n_layers, "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads,
+            "workload": w.name + ("-per-sequence-plans" if plans else ""), "layers": w.n_layers,
+            "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads,
             "head_dim": w.head_dim, "batch": w.batch, "context": n_tok, "stored_tokens": n_stored,
             "qscheme": "KIVI32" if w.qscheme == kvk.KIVI32 else "SYMROW",
-            "anchors_by_bits": bits_mix, "inheriting_layers": sum(e[0] for e in w.plan),
+            "anchors_by_bits": bits_mix,
+            "inheriting_layers": sum(e[0] for p in ([w.plan] if plans is None else plans) for e in p),
             "rho_eq2": round(info.rho, 3), "rho_realized": round(info.rho_realized, 3),
             "alg_bytes_per_step": alg,
         },
         "roofline": {
             "bound": "hbm", "kernel": "gqa_decode_kernel (D1)", "achieved": round(d1_gbs, 2),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(d1_gbs / HBM_PEAK_GBS, 4),
-            "traffic": recorded_traffic(args.config, args.variant) if args.qscheme == "kivi32" else None,
+            "traffic": (recorded_traffic(args.config, args.variant)
+                        if args.qscheme == "kivi32" and plans is None else None),
             "launch_us": round(d1_avg * 1e3, 2), "bytes_per_launch": alg,
         },
         "cpu_baseline": cpu,

@@ -100,6 +100,12 @@ def workload(cfg: int, variant: Optional[str] = None) -> Workload:
     raise ValueError(f"unknown workload {cfg}")
 
 
+def plans_per_sequence(w: Workload, n_inherit: int = 16):
+    """One plan per sequence of the 14B-shaped mixed workload, each drawn like the
+    shared plan (its own seed): the selector maps every prompt to its own plan."""
+    return [plan_mixed(w.seed * 1000 + b, w.n_layers, n_inherit) for b in range(w.batch)]
+
+
 @dataclass
 class MlaWorkload:
     """An MLA-style stack (§2.1 rank axis): one latent of width r per token shared by
