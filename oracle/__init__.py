@@ -24,7 +24,8 @@ Modules:
   cache     — compress a layer to arena bytes and decode a step from them
   mla       — the rank axis: MLA latent caches, their storage and attention
   snapkv    — query-aware token selection at prefill (the eviction composed with)
+  selector  — the selector forward pass (prompt embeddings -> per-layer plan)
 
 Parity status per function is stated in each module's docstring.
 """
-from . import plan, quant, layout, attention, cache, mla, snapkv  # noqa: F401
+from . import plan, quant, layout, attention, cache, mla, snapkv, selector  # noqa: F401
