@@ -357,6 +357,36 @@ kvk_status kvk_snapkv_select(const kvk_table* table, int32_t layer, const void* 
                              int32_t in_dtype, int32_t n_tokens, float scale, int32_t* keep_out,
                              float* importance, void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* The selector's forward pass (§2.3): the prompt's token embeddings (the backbone's
+ * own) -> a linear map to width 256 -> two bidirectional transformer blocks ->
+ * average over the prompt -> one linear head per layer -> the argmax action of
+ * each layer, the depth action's logit at -inf for layer 0.  Run once per prompt
+ * at prefill; the actions build the plan that is held for the whole generation.
+ * Blocks: pre-normalised (LayerNorm with gain and bias, eps 1e-5), attention of
+ * 4 heads of 64 over every position with scale 1/8, feed-forward 256 -> 1024 ->
+ * 256 with the tanh form of GELU, residual additions; no positional encoding.
+ * Actions: 0 inherit (depth), 1 bf16, 2 int8, 3 int4, 4 int2 (GQA plans).
+ *   weights : device bf16, kvk_selector_weight_elems(d_model, n_layers) elements,
+ *             packed in this order, each matrix [out][in] row-major:
+ *             w_in [256][d_model], b_in [256]; then per block (two):
+ *             ln1_gain [256], ln1_bias [256], w_qkv [768][256] (q, k, v rows;
+ *             head h uses rows 64h .. 64h+63 of each), b_qkv [768], w_o [256][256],
+ *             b_o [256], ln2_gain [256], ln2_bias [256], w_1 [1024][256],
+ *             b_1 [1024], w_2 [256][1024], b_2 [256]; then w_head [n_layers][256][5]
+ *             (layer l's head maps feature c to action a at [l][c][a]), b_head
+ *             [n_layers][5].
+ *   emb     : device bf16 [n_tokens][d_model]; d_model a multiple of 32.
+ *   logits  : NULL, or device fp32 [n_layers][5] (computed in fp32; bf16 operands).
+ *   actions : device int32 [n_layers], the argmax (lowest index on ties).
+ *   workspace: device, >= kvk_selector_workspace_bytes(...), 256-byte aligned.
+ * Errors: KVK_ERR_INVALID (sizes, NULL pointers, misalignment), KVK_ERR_BUFFER,
+ *         KVK_ERR_DEVICE. */
+int64_t kvk_selector_weight_elems(int32_t d_model, int32_t n_layers);
+kvk_status kvk_selector_workspace_bytes(int32_t d_model, int32_t n_layers, int32_t n_tokens, size_t* out_bytes);
+kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, const void* weights, const void* emb,
+                                int32_t n_tokens, float* logits, int32_t* actions, void* workspace,
+                                size_t ws_bytes, hipStream_t stream);
+
 /* One decode step of attention for layers [layer_begin, layer_end) (§2.1): layer l
  * uses its own query and the cache of anchor_of[l].  Layers in the range that
  * share an anchor are served by one read of that anchor's bytes.

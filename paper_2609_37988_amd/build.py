@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libkvk.so")
 OBJDIR = os.path.join(ROOT, "_build")
-SOURCES = ["table.cpp", "compress.hip", "decode.hip", "mla.hip", "snapkv.hip"]
+SOURCES = ["table.cpp", "compress.hip", "decode.hip", "mla.hip", "snapkv.hip", "selector.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

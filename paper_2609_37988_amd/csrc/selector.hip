@@ -1,0 +1,393 @@
+// The selector's forward pass (KV-Kaizen §2.3): a prompt's token embeddings ->
+// two bidirectional transformer blocks of width 256 -> time average -> one linear
+// head per layer -> argmax action per layer (the depth action of layer 0 excluded).
+// It runs once per prompt at prefill; the plan it yields is held for the whole
+// generation.  Weights are inputs (packed bf16, layout in include/kvk.h).
+//
+// Kernels (T = prompt length):
+//   sel_gemm_kernel<EPI>: C = A [T, K] . W^T, W [N, K] (bf16 operands on MFMA
+//       16x16x32, fp32 accumulation); one wave per 32 x 32 output tile; the epilogue
+//       adds the bias and, by EPI: stores fp32, adds into the fp32 residual stream,
+//       applies GELU and stores bf16, or splits q, k (bf16 rows) and v (bf16,
+//       transposed per head for the attention's value operand).
+//   sel_layernorm_kernel: one wave per row of 256, fp32 in, bf16 out.
+//   sel_attention_kernel: bidirectional attention, 4 heads of 64; a workgroup takes
+//       128 queries of one head (4 waves x two 16-query tiles) and walks the keys
+//       in tiles of 32 staged in LDS; S^T = K Q^T, online softmax (base 2) per
+//       query, O^T += V^T P^T with P^T taken straight from the S^T accumulators
+//       (the key order of the product's k-slots follows the accumulator layout).
+//   sel_pool_kernel / sel_heads_kernel: the time average (per-chunk partial sums,
+//       then their sum), the per-layer logits and the argmax.
+#include <hip/hip_runtime.h>
+
+#include "kvk_device.h"
+#include "kvk_internal.h"
+
+using namespace kvkd;
+
+namespace {
+
+constexpr int kW = 256, kHeads = 4, kDh = 64, kFfn = 1024, kActions = 5;
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ f4 mfma_bf(bf16x8 a, bf16x8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
+  return 0.5f * x * (1.0f + tanhf(u));
+}
+
+enum Epi { kStoreF32 = 0, kAddF32 = 1, kGeluBf16 = 2, kQkv = 3 };
+
+struct GemmArgs {
+  const uint16_t* a;   // [M][K] bf16
+  const uint16_t* w;   // [N][K] bf16
+  const uint16_t* bias;  // [N] bf16
+  float* out_f32;      // [M][N] (kStoreF32, kAddF32)
+  uint16_t* out_bf16;  // [M][N] (kGeluBf16), [M][512] q|k (kQkv)
+  uint16_t* vt;        // kQkv: [heads][64][vt_pitch] values, transposed
+  int32_t M, N, K, vt_pitch;
+};
+
+// One wave per 32 x 32 tile of C; lane (row i16, k-group kg) feeds 8 consecutive
+// k of its row of A and of its row of W per step.
+template <int EPI>
+__global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
+  const int lane = threadIdx.x & 63, i16 = lane & 15, kg = lane >> 4;
+  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int tiles_n = g.N / 32;
+  const int tm = wave / tiles_n, tn = wave % tiles_n;
+  if (tm * 32 >= g.M) return;
+  const int r0 = tm * 32, c0 = tn * 32;
+  f4 acc[2][2] = {};
+  for (int k0 = 0; k0 < g.K; k0 += 32) {
+    bf16x8 av[2], wv[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int r = r0 + 16 * i + i16;
+      if (r < g.M) av[i] = *reinterpret_cast<const bf16x8*>(g.a + (int64_t)r * g.K + k0 + 8 * kg);
+      else av[i] = bf16x8{};
+      wv[i] = *reinterpret_cast<const bf16x8*>(g.w + (int64_t)(c0 + 16 * i + i16) * g.K + k0 + 8 * kg);
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) acc[i][j] = mfma_bf(wv[j], av[i], acc[i][j]);  // C^T tile: rows n, cols m
+  }
+  // acc[i][j]: lane (m = r0 + 16 i + i16) holds n = c0 + 16 j + 4 kg + e
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int m = r0 + 16 * i + i16;
+    if (m >= g.M) continue;
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int n = c0 + 16 * j + 4 * kg + e;
+        const float v = acc[i][j][e] + bf16_to_f32(g.bias[n]);
+        if constexpr (EPI == kStoreF32) {
+          g.out_f32[(int64_t)m * g.N + n] = v;
+        } else if constexpr (EPI == kAddF32) {
+          g.out_f32[(int64_t)m * g.N + n] += v;
+        } else if constexpr (EPI == kGeluBf16) {
+          g.out_bf16[(int64_t)m * g.N + n] = f32_to_bf16_bits(gelu_tanh(v));
+        } else {
+          if (n < 2 * kW) g.out_bf16[(int64_t)m * (2 * kW) + n] = f32_to_bf16_bits(v);
+          else g.vt[(int64_t)(n - 2 * kW) * g.vt_pitch + m] = f32_to_bf16_bits(v);
+        }
+      }
+  }
+}
+
+// One wave per row of 256: LayerNorm (eps 1e-5, gain and bias) to bf16.
+__global__ __launch_bounds__(256) void sel_layernorm_kernel(const float* x, const uint16_t* gain,
+                                                            const uint16_t* bias, uint16_t* out, int M) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const f4 v = *reinterpret_cast<const f4*>(x + (int64_t)row * kW + 4 * lane);
+  float s = v[0] + v[1] + v[2] + v[3];
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+  const float mu = s * (1.0f / kW);
+  float q = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) q += (v[e] - mu) * (v[e] - mu);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) q += __shfl_xor(q, off);
+  const float rs = 1.0f / sqrtf(q * (1.0f / kW) + 1e-5f);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int c = 4 * lane + e;
+    out[(int64_t)row * kW + c] = f32_to_bf16_bits((v[e] - mu) * rs * bf16_to_f32(gain[c]) + bf16_to_f32(bias[c]));
+  }
+}
+
+// Bidirectional attention.  Workgroup: 128 queries (wave w: queries 32 w .. 32 w + 31
+// of the group, two 16-query tiles) of head h; keys in tiles of 32 through LDS.
+__global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, const uint16_t* vt, int vt_pitch,
+                                                            uint16_t* out, int T) {
+  __shared__ uint16_t ks[32][kDh + 8];   // key rows of the tile
+  __shared__ uint16_t vs[kDh][32 + 8];   // value columns (channel-major) of the tile
+  const int tid = threadIdx.x, lane = tid & 63, i16 = lane & 15, kg = lane >> 4, wv = tid >> 6;
+  const int h = blockIdx.y;
+  const int q_base = blockIdx.x * 128 + 32 * wv;
+  const float sc = 0.125f * kLog2e;  // 1/sqrt(64), base 2
+  // the query operand (B of S^T = K Q^T): lane (query i16, kg) holds channels 8 kg .. + 7 of each k-step
+  bf16x8 qb[2][2];
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    const int q = q_base + 16 * qt + i16;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      if (q < T) qb[qt][j] = *reinterpret_cast<const bf16x8*>(qk + (int64_t)q * (2 * kW) + h * kDh + 32 * j + 8 * kg);
+      else qb[qt][j] = bf16x8{};
+    }
+  }
+  f4 o[2][4] = {};
+  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.0f, 0.0f};
+  for (int k0 = 0; k0 < T; k0 += 32) {
+    __syncthreads();  // the previous tile is consumed
+    {  // stage: thread -> 8 bf16 of a key row, and 8 bf16 of a value column
+      const int r = tid >> 3, c8 = 8 * (tid & 7);
+      const int key = k0 + r;
+      uint4 kvv = make_uint4(0, 0, 0, 0);
+      if (key < T) kvv = *reinterpret_cast<const uint4*>(qk + (int64_t)key * (2 * kW) + kW + h * kDh + c8);
+      *reinterpret_cast<uint4*>(&ks[r][c8]) = kvv;
+      const int ch = tid >> 2, t8 = 8 * (tid & 3);
+      const uint16_t* vp = vt + (int64_t)(h * kDh + ch) * vt_pitch + k0 + t8;
+      uint4 vvv = make_uint4(0, 0, 0, 0);
+      if (k0 + t8 + 8 <= T) vvv = *reinterpret_cast<const uint4*>(vp);
+      else {  // past the prompt: zeros (their probabilities are 0, and 0 * garbage could be NaN)
+        uint32_t w4[4];
+        for (int e = 0; e < 4; ++e) {
+          const uint32_t a0 = k0 + t8 + 2 * e < T ? vp[2 * e] : 0u;
+          const uint32_t a1 = k0 + t8 + 2 * e + 1 < T ? vp[2 * e + 1] : 0u;
+          w4[e] = a0 | (a1 << 16);
+        }
+        vvv = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+      }
+      *reinterpret_cast<uint4*>(&vs[ch][t8]) = vvv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      // S^T tiles tau = 0, 1 (keys 16 tau ..): lane (query i16, kg) holds keys 16 tau + 4 kg + e
+      f4 s[2] = {};
+#pragma unroll
+      for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&ks[16 * tau + i16][32 * j + 8 * kg]);
+          s[tau] = mfma_bf(ka, qb[qt][j], s[tau]);
+        }
+      float x[8];
+#pragma unroll
+      for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * tau + e] = k0 + 16 * tau + 4 * kg + e < T ? s[tau][e] * sc : -INFINITY;
+      float mx = x[0];
+#pragma unroll
+      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, x[e]);
+      mx = rows_max(mx);
+      const float mnew = fmaxf(m[qt], mx);
+      const float alpha = __builtin_amdgcn_exp2f(m[qt] - mnew);
+      float ps = 0.0f;
+      bf16x8 pb;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = __builtin_amdgcn_exp2f(x[e] - mnew);
+        pb[e] = (__bf16)p;
+        ps += p;
+      }
+      l[qt] = l[qt] * alpha + rows_sum(ps);
+      m[qt] = mnew;
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) {
+        o[qt][ct] *= alpha;
+        // V^T operand: lane (channel i16, kg) holds the keys of its k-slots: 4 kg .. + 3, 16 + 4 kg .. + 3
+        const uint16_t* vr = &vs[16 * ct + i16][0];
+        const uint2 lo = *reinterpret_cast<const uint2*>(vr + 4 * kg);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16 + 4 * kg);
+        const bf16x8 va = bitcast<bf16x8>(make_uint4(lo.x, lo.y, hi.x, hi.y));
+        o[qt][ct] = mfma_bf(va, pb, o[qt][ct]);
+      }
+    }
+  }
+  // O^T tiles: lane (query i16, kg) holds channels 16 ct + 4 kg + e
+#pragma unroll
+  for (int qt = 0; qt < 2; ++qt) {
+    const int q = q_base + 16 * qt + i16;
+    if (q >= T) continue;
+    const float inv = 1.0f / l[qt];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        out[(int64_t)q * kW + h * kDh + 16 * ct + 4 * kg + e] = f32_to_bf16_bits(o[qt][ct][e] * inv);
+  }
+}
+
+// Partial column sums of x over chunks of 256 rows: part[chunk][c].
+__global__ __launch_bounds__(256) void sel_pool_kernel(const float* x, float* part, int T) {
+  const int c = threadIdx.x, chunk = blockIdx.x;
+  const int t1 = min(T, (chunk + 1) * 256);
+  float s = 0.0f;
+  for (int t = chunk * 256; t < t1; ++t) s += x[(int64_t)t * kW + c];
+  part[(int64_t)chunk * kW + c] = s;
+}
+
+// The feature (mean of the partial sums), the per-layer logits, the argmax (the
+// lowest action on ties; the depth action never at layer 0).  One workgroup.
+__global__ __launch_bounds__(256) void sel_heads_kernel(const float* part, int n_chunks, int T, const uint16_t* w_head,
+                                                        const uint16_t* b_head, int L, float* logits, int32_t* action) {
+  __shared__ float f[kW];
+  __shared__ float z[64 * kActions];
+  const int tid = threadIdx.x;
+  float s = 0.0f;
+  for (int k = 0; k < n_chunks; ++k) s += part[(int64_t)k * kW + tid];
+  f[tid] = s / (float)T;
+  __syncthreads();
+  for (int i = tid; i < L * kActions; i += 256) {
+    const int l = i / kActions, a = i % kActions;
+    float acc = bf16_to_f32(b_head[i]);
+    for (int c = 0; c < kW; ++c) acc += f[c] * bf16_to_f32(w_head[((int64_t)l * kW + c) * kActions + a]);
+    if (l == 0 && a == 0) acc = -INFINITY;
+    z[i] = acc;
+    if (logits) logits[i] = acc;
+  }
+  __syncthreads();
+  if (tid < L) {
+    int best = 0;
+    for (int a = 1; a < kActions; ++a)
+      if (z[tid * kActions + a] > z[tid * kActions + best]) best = a;
+    action[tid] = best;
+  }
+}
+
+// Packed weight offsets (bf16 elements).
+struct SelOffsets {
+  int64_t w_in, b_in, blk[2], w_head, b_head, total;
+};
+constexpr int64_t kBlockElems = 2 * kW + (int64_t)3 * kW * kW + 3 * kW + (int64_t)kW * kW + kW + 2 * kW +
+                                (int64_t)kFfn * kW + kFfn + (int64_t)kW * kFfn + kW;
+
+SelOffsets sel_offsets(int d_model, int L) {
+  SelOffsets o;
+  o.w_in = 0;
+  o.b_in = (int64_t)kW * d_model;
+  o.blk[0] = o.b_in + kW;
+  o.blk[1] = o.blk[0] + kBlockElems;
+  o.w_head = o.blk[1] + kBlockElems;
+  o.b_head = o.w_head + (int64_t)L * kW * kActions;
+  o.total = o.b_head + (int64_t)L * kActions;
+  return o;
+}
+
+struct SelWorkspace {
+  int64_t x, h, qk, vt, f1, part, total;  // byte offsets
+  int vt_pitch;
+};
+
+SelWorkspace sel_workspace(int T) {
+  SelWorkspace w;
+  const int Tp = (T + 31) / 32 * 32;
+  w.vt_pitch = Tp;
+  w.x = 0;                                              // fp32 [T][256] residual stream
+  w.h = kvk::round256(w.x + (int64_t)Tp * kW * 4);           // bf16 [T][256] normalised / attention output
+  w.qk = kvk::round256(w.h + (int64_t)Tp * kW * 2);          // bf16 [T][512]
+  w.vt = kvk::round256(w.qk + (int64_t)Tp * 2 * kW * 2);     // bf16 [256][Tp]
+  w.f1 = kvk::round256(w.vt + (int64_t)kW * Tp * 2);         // bf16 [T][1024]
+  w.part = kvk::round256(w.f1 + (int64_t)Tp * kFfn * 2);     // fp32 [chunks][256]
+  w.total = kvk::round256(w.part + (int64_t)((T + 255) / 256) * kW * 4);
+  return w;
+}
+
+}  // namespace
+
+using namespace kvk;
+
+extern "C" kvk_status kvk_selector_workspace_bytes(int32_t d_model, int32_t n_layers, int32_t n_tokens,
+                                                   size_t* out) {
+  if (!out) return fail(KVK_ERR_INVALID, "selector: NULL output");
+  if (d_model < 32 || d_model % 32 || n_layers < 1 || n_layers > KVK_MAX_LAYERS || n_tokens < 1)
+    return fail(KVK_ERR_INVALID, "selector: d_model %d (multiple of 32), n_layers %d, n_tokens %d", d_model,
+                n_layers, n_tokens);
+  *out = (size_t)sel_workspace(n_tokens).total;
+  return KVK_OK;
+}
+
+extern "C" int64_t kvk_selector_weight_elems(int32_t d_model, int32_t n_layers) {
+  return sel_offsets(d_model, n_layers).total;
+}
+
+extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, const void* weights,
+                                           const void* emb, int32_t n_tokens, float* logits, int32_t* actions,
+                                           void* workspace, size_t ws_bytes, hipStream_t stream) {
+  size_t need = 0;
+  kvk_status st = kvk_selector_workspace_bytes(d_model, n_layers, n_tokens, &need);
+  if (st != KVK_OK) return st;
+  if (!weights || !emb || !actions || !workspace) return fail(KVK_ERR_INVALID, "selector: NULL buffer");
+  if (need > ws_bytes) return fail(KVK_ERR_BUFFER, "selector: workspace %zu bytes < %zu needed", ws_bytes, need);
+  if ((reinterpret_cast<uintptr_t>(weights) & 15) || (reinterpret_cast<uintptr_t>(emb) & 15) ||
+      (reinterpret_cast<uintptr_t>(workspace) & 255) || (reinterpret_cast<uintptr_t>(logits) & 3) ||
+      (reinterpret_cast<uintptr_t>(actions) & 3))
+    return fail(KVK_ERR_INVALID, "selector: misaligned buffer (weights/emb 16 B, workspace 256 B)");
+  const SelOffsets O = sel_offsets(d_model, n_layers);
+  const SelWorkspace Wk = sel_workspace(n_tokens);
+  const uint16_t* wp = static_cast<const uint16_t*>(weights);
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  float* x = reinterpret_cast<float*>(ws + Wk.x);
+  uint16_t* hbuf = reinterpret_cast<uint16_t*>(ws + Wk.h);
+  uint16_t* qk = reinterpret_cast<uint16_t*>(ws + Wk.qk);
+  uint16_t* vt = reinterpret_cast<uint16_t*>(ws + Wk.vt);
+  uint16_t* f1 = reinterpret_cast<uint16_t*>(ws + Wk.f1);
+  float* part = reinterpret_cast<float*>(ws + Wk.part);
+  const int T = n_tokens;
+  auto gemm = [&](int epi, const uint16_t* a, int64_t w_off, int64_t b_off, int N, int K) {
+    GemmArgs g;
+    g.a = a;
+    g.w = wp + w_off;
+    g.bias = wp + b_off;
+    g.out_f32 = x;
+    g.out_bf16 = epi == kGeluBf16 ? f1 : qk;
+    g.vt = vt;
+    g.M = T;
+    g.N = N;
+    g.K = K;
+    g.vt_pitch = Wk.vt_pitch;
+    const int waves = (T + 31) / 32 * (N / 32);
+    const dim3 grid((unsigned)((waves + 3) / 4)), blk(256);
+    switch (epi) {
+      case kStoreF32: hipLaunchKernelGGL(sel_gemm_kernel<kStoreF32>, grid, blk, 0, stream, g); break;
+      case kAddF32: hipLaunchKernelGGL(sel_gemm_kernel<kAddF32>, grid, blk, 0, stream, g); break;
+      case kGeluBf16: hipLaunchKernelGGL(sel_gemm_kernel<kGeluBf16>, grid, blk, 0, stream, g); break;
+      default: hipLaunchKernelGGL(sel_gemm_kernel<kQkv>, grid, blk, 0, stream, g); break;
+    }
+  };
+  const dim3 rows((unsigned)((T + 3) / 4)), b256(256);
+  gemm(kStoreF32, static_cast<const uint16_t*>(emb), O.w_in, O.b_in, kW, d_model);
+  for (int bi = 0; bi < 2; ++bi) {
+    int64_t p = O.blk[bi];
+    const int64_t ln1_g = p, ln1_b = p + kW, w_qkv = p + 2 * kW, b_qkv = w_qkv + (int64_t)3 * kW * kW,
+                  w_o = b_qkv + 3 * kW, b_o = w_o + (int64_t)kW * kW, ln2_g = b_o + kW, ln2_b = ln2_g + kW,
+                  w_1 = ln2_b + kW, b_1 = w_1 + (int64_t)kFfn * kW, w_2 = b_1 + kFfn, b_2 = w_2 + (int64_t)kW * kFfn;
+    hipLaunchKernelGGL(sel_layernorm_kernel, rows, b256, 0, stream, x, wp + ln1_g, wp + ln1_b, hbuf, T);
+    gemm(kQkv, hbuf, w_qkv, b_qkv, 3 * kW, kW);
+    hipLaunchKernelGGL(sel_attention_kernel, dim3((unsigned)((T + 127) / 128), kHeads), b256, 0, stream, qk, vt,
+                       Wk.vt_pitch, hbuf, T);
+    gemm(kAddF32, hbuf, w_o, b_o, kW, kW);
+    hipLaunchKernelGGL(sel_layernorm_kernel, rows, b256, 0, stream, x, wp + ln2_g, wp + ln2_b, hbuf, T);
+    gemm(kGeluBf16, hbuf, w_1, b_1, kFfn, kW);
+    gemm(kAddF32, f1, w_2, b_2, kW, kFfn);
+  }
+  const int chunks = (T + 255) / 256;
+  hipLaunchKernelGGL(sel_pool_kernel, dim3((unsigned)chunks), b256, 0, stream, x, part, T);
+  hipLaunchKernelGGL(sel_heads_kernel, dim3(1), b256, 0, stream, part, chunks, T, wp + O.w_head, wp + O.b_head,
+                     n_layers, logits, actions);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "selector launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}

@@ -73,6 +73,9 @@ def load() -> ctypes.CDLL:
             "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
             "kvk_append_token": (I32, [P, I32, I32, P, P, I32, I32, P, P]),
             "kvk_snapkv_workspace_bytes": (I32, [P, I32, ctypes.POINTER(ctypes.c_size_t)]),
+            "kvk_selector_weight_elems": (I64, [I32, I32]),
+            "kvk_selector_workspace_bytes": (I32, [I32, I32, I32, ctypes.POINTER(ctypes.c_size_t)]),
+            "kvk_selector_forward": (I32, [I32, I32, P, P, I32, P, P, P, ctypes.c_size_t, P]),
             "kvk_snapkv_select": (I32, [P, I32, P, P, I32, I32, F, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_attention": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_splits": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P]),
@@ -97,6 +100,7 @@ def exported_symbols() -> List[str]:
     """Names of the C entry points the binding expects libkvk to export."""
     return ["kvk_layer_table", "kvk_layer_table_batched", "kvk_table_sequence_query", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
             "kvk_compress_layer", "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
+            "kvk_selector_weight_elems", "kvk_selector_workspace_bytes", "kvk_selector_forward",
             "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge",
             "kvk_read_bytes", "kvk_debug_dequantize",
             "kvk_realized_bits", "kvk_rho_range", "kvk_last_error", "kvk_version"]
@@ -350,6 +354,35 @@ def snapkv_select(t: Table, layer: int, k: torch.Tensor, q_obs: torch.Tensor, n_
     _check(load().kvk_snapkv_select(t.handle, layer, _ptr(k), _ptr(q_obs), _dtype_code(k), n_tokens, float(scale),
                                     _ptr(keep_out), _ptr(importance), _ptr(workspace), _nbytes(workspace),
                                     _stream(stream)))
+
+
+SELECTOR_ACTIONS = [(1, 16), (0, 16), (0, 8), (0, 4), (0, 2)]  # (inherit, bits) by action index
+
+
+def selector_weight_elems(d_model: int, n_layers: int) -> int:
+    return int(load().kvk_selector_weight_elems(d_model, n_layers))
+
+
+def selector_workspace_bytes(d_model: int, n_layers: int, n_tokens: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load().kvk_selector_workspace_bytes(d_model, n_layers, n_tokens, ctypes.byref(out)))
+    return out.value
+
+
+def selector_forward(d_model: int, n_layers: int, weights: torch.Tensor, emb: torch.Tensor,
+                     actions: torch.Tensor, workspace: torch.Tensor, logits: Optional[torch.Tensor] = None,
+                     stream=None):
+    """emb [n_tokens, d_model] bf16; weights packed bf16 (see kvk.h); actions int32
+    [n_layers]; logits (optional) fp32 [n_layers, 5]."""
+    _need(emb.dtype == torch.bfloat16 and emb.is_contiguous() and emb.dim() == 2 and emb.shape[1] == d_model,
+          "emb must be contiguous bf16 [n_tokens, d_model]")
+    _need(weights.dtype == torch.bfloat16 and weights.is_contiguous() and
+          weights.numel() == selector_weight_elems(d_model, n_layers), "weights must be the packed bf16 vector")
+    _need(actions.dtype == torch.int32 and actions.numel() == n_layers, "actions must be int32 [n_layers]")
+    if logits is not None:
+        _need(logits.dtype == torch.float32 and logits.numel() == n_layers * 5, "logits must be fp32 [n_layers, 5]")
+    _check(load().kvk_selector_forward(d_model, n_layers, _ptr(weights), _ptr(emb), emb.shape[0], _ptr(logits),
+                                       _ptr(actions), _ptr(workspace), _nbytes(workspace), _stream(stream)))
 
 
 def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_stored: int,
