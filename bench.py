@@ -91,6 +91,32 @@ def time_append(kvk, torch, table, n_layers, arena, n_stored, k_shape, v_shape, 
             "us_per_token": round(sum(us) / 32, 2)}
 
 
+def time_selector(kvk, torch, d_model, n_layers, dev, lengths=(2048, 8192, 32768)):
+    """The selector forward pass (prompt embeddings -> plan) at several prompt lengths,
+    synthetic weights of the model's embedding width: µs per prompt (median of 5)."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(99)
+    n_w = kvk.selector_weight_elems(d_model, n_layers)
+    weights = (torch.randn(n_w, generator=g, device=dev) * 0.02).to(torch.bfloat16)
+    actions = torch.empty(n_layers, dtype=torch.int32, device=dev)
+    out = {}
+    for T in lengths:
+        emb = torch.randn((T, d_model), generator=g, device=dev).to(torch.bfloat16)
+        ws = torch.empty(kvk.selector_workspace_bytes(d_model, n_layers, T), dtype=torch.uint8, device=dev)
+        kvk.selector_forward(d_model, n_layers, weights, emb, actions, ws)
+        times = []
+        for _ in range(5):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            kvk.selector_forward(d_model, n_layers, weights, emb, actions, ws)
+            e1.record()
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1) * 1e3)
+        out[str(T)] = round(sorted(times)[2], 1)
+        del emb, ws
+    return {"d_model": d_model, "layers": n_layers, "us_by_prompt_tokens": out}
+
+
 def kernel_source_hash(sources=GQA_SOURCES) -> str:
     """sha256 over the sources that determine a decode kernel and its splits."""
     import hashlib
@@ -471,6 +497,8 @@ def main():
                       (w.n_layers, w.batch, w.n_kv_heads, w.head_dim), (w.n_layers, w.batch, w.n_kv_heads, w.head_dim),
                       dev)
     log(f"append: {app}")
+    sel = time_selector(kvk, torch, w.n_q_heads * w.head_dim, w.n_layers, dev) if args.config == 2 else None
+    log(f"selector: {sel}")
 
     bits_mix = {}
     for p in ([w.plan] if plans is None else plans):
@@ -513,6 +541,7 @@ def main():
         "prefill_write": {"ms": round(w1_ms, 3), "bytes": w1_bytes,
                           "GB_per_s": round(w1_bytes / (w1_ms * 1e-3) / 1e9, 2)},
         "append": app,
+        "selector_forward": sel,
     }
     if w.keep_tokens:
         line["snapkv_select"] = {

@@ -13,7 +13,7 @@
 //   sel_layernorm_kernel: one wave per row of 256, fp32 in, bf16 out.
 //   sel_attention_kernel: bidirectional attention, 4 heads of 64; a workgroup takes
 //       128 queries of one head (4 waves x two 16-query tiles) and walks the keys
-//       in tiles of 32 staged in LDS; S^T = K Q^T, online softmax (base 2) per
+//       in tiles of 64 staged in LDS (consumed as two halves of 32); S^T = K Q^T, online softmax (base 2) per
 //       query, O^T += V^T P^T with P^T taken straight from the S^T accumulators
 //       (the key order of the product's k-slots follows the accumulator layout).
 //   sel_pool_kernel / sel_heads_kernel: the time average (per-chunk partial sums,
@@ -126,11 +126,13 @@ __global__ __launch_bounds__(256) void sel_layernorm_kernel(const float* x, cons
 }
 
 // Bidirectional attention.  Workgroup: 128 queries (wave w: queries 32 w .. 32 w + 31
-// of the group, two 16-query tiles) of head h; keys in tiles of 32 through LDS.
+// of the group, two 16-query tiles) of head h; keys in tiles of 64 through LDS, each
+// consumed as two halves of 32 whose key and value operands serve both query tiles.
 __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, const uint16_t* vt, int vt_pitch,
                                                             uint16_t* out, int T) {
-  __shared__ uint16_t ks[32][kDh + 8];   // key rows of the tile
-  __shared__ uint16_t vs[kDh][32 + 8];   // value columns (channel-major) of the tile
+  constexpr int KT = 64;
+  __shared__ uint16_t ks[KT][kDh + 8];   // key rows of the tile
+  __shared__ uint16_t vs[kDh][KT + 8];   // value columns (channel-major) of the tile
   const int tid = threadIdx.x, lane = tid & 63, i16 = lane & 15, kg = lane >> 4, wv = tid >> 6;
   const int h = blockIdx.y;
   const int q_base = blockIdx.x * 128 + 32 * wv;
@@ -148,19 +150,21 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
   }
   f4 o[2][4] = {};
   float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.0f, 0.0f};
-  for (int k0 = 0; k0 < T; k0 += 32) {
+  for (int k0 = 0; k0 < T; k0 += KT) {
     __syncthreads();  // the previous tile is consumed
-    {  // stage: thread -> 8 bf16 of a key row, and 8 bf16 of a value column
-      const int r = tid >> 3, c8 = 8 * (tid & 7);
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {  // stage: 8 bf16 of a key row, and 8 bf16 of a value column
+      const int r = (tid >> 3) + 32 * hh, c8 = 8 * (tid & 7);
       const int key = k0 + r;
       uint4 kvv = make_uint4(0, 0, 0, 0);
       if (key < T) kvv = *reinterpret_cast<const uint4*>(qk + (int64_t)key * (2 * kW) + kW + h * kDh + c8);
       *reinterpret_cast<uint4*>(&ks[r][c8]) = kvv;
-      const int ch = tid >> 2, t8 = 8 * (tid & 3);
+      const int ch = (tid >> 3) + 32 * hh, t8 = 8 * (tid & 7);
       const uint16_t* vp = vt + (int64_t)(h * kDh + ch) * vt_pitch + k0 + t8;
       uint4 vvv = make_uint4(0, 0, 0, 0);
-      if (k0 + t8 + 8 <= T) vvv = *reinterpret_cast<const uint4*>(vp);
-      else {  // past the prompt: zeros (their probabilities are 0, and 0 * garbage could be NaN)
+      if (k0 + t8 + 8 <= T) {
+        vvv = *reinterpret_cast<const uint4*>(vp);
+      } else {  // past the prompt: zeros (their probabilities are 0, and 0 * garbage could be NaN)
         uint32_t w4[4];
         for (int e = 0; e < 4; ++e) {
           const uint32_t a0 = k0 + t8 + 2 * e < T ? vp[2 * e] : 0u;
@@ -173,46 +177,65 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
     }
     __syncthreads();
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
-      // S^T tiles tau = 0, 1 (keys 16 tau ..): lane (query i16, kg) holds keys 16 tau + 4 kg + e
-      f4 s[2] = {};
+    for (int half = 0; half < 2; ++half) {
+      const int kb = 32 * half;
+      if (k0 + kb >= T) break;  // uniform
+      bf16x8 ka[2][2], va[4];
 #pragma unroll
       for (int tau = 0; tau < 2; ++tau)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(&ks[16 * tau + i16][32 * j + 8 * kg]);
-          s[tau] = mfma_bf(ka, qb[qt][j], s[tau]);
-        }
-      float x[8];
-#pragma unroll
-      for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) x[4 * tau + e] = k0 + 16 * tau + 4 * kg + e < T ? s[tau][e] * sc : -INFINITY;
-      float mx = x[0];
-#pragma unroll
-      for (int e = 1; e < 8; ++e) mx = fmaxf(mx, x[e]);
-      mx = rows_max(mx);
-      const float mnew = fmaxf(m[qt], mx);
-      const float alpha = __builtin_amdgcn_exp2f(m[qt] - mnew);
-      float ps = 0.0f;
-      bf16x8 pb;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(x[e] - mnew);
-        pb[e] = (__bf16)p;
-        ps += p;
-      }
-      l[qt] = l[qt] * alpha + rows_sum(ps);
-      m[qt] = mnew;
+        for (int j = 0; j < 2; ++j) ka[tau][j] = *reinterpret_cast<const bf16x8*>(&ks[kb + 16 * tau + i16][32 * j + 8 * kg]);
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
-        o[qt][ct] *= alpha;
         // V^T operand: lane (channel i16, kg) holds the keys of its k-slots: 4 kg .. + 3, 16 + 4 kg .. + 3
-        const uint16_t* vr = &vs[16 * ct + i16][0];
+        const uint16_t* vr = &vs[16 * ct + i16][kb];
         const uint2 lo = *reinterpret_cast<const uint2*>(vr + 4 * kg);
         const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16 + 4 * kg);
-        const bf16x8 va = bitcast<bf16x8>(make_uint4(lo.x, lo.y, hi.x, hi.y));
-        o[qt][ct] = mfma_bf(va, pb, o[qt][ct]);
+        va[ct] = bitcast<bf16x8>(make_uint4(lo.x, lo.y, hi.x, hi.y));
+      }
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        // S^T tiles tau = 0, 1: lane (query i16, kg) holds keys kb + 16 tau + 4 kg + e
+        f4 s[2] = {};
+#pragma unroll
+        for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+          for (int j = 0; j < 2; ++j) s[tau] = mfma_bf(ka[tau][j], qb[qt][j], s[tau]);
+        // raw scores; the scale enters the exponent (m holds scaled maxima)
+        float x[8];
+#pragma unroll
+        for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) x[4 * tau + e] = s[tau][e];
+        if (k0 + kb + 32 > T) {  // the last keys: mask those past the prompt
+#pragma unroll
+          for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (k0 + kb + 16 * tau + 4 * kg + e >= T) x[4 * tau + e] = -INFINITY;
+        }
+        float mx = x[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, x[e]);
+        mx = rows_max(mx) * sc;
+        const float mnew = fmaxf(m[qt], mx);
+        const float alpha = __builtin_amdgcn_exp2f(m[qt] - mnew);
+        float ps = 0.0f;
+        bf16x8 pb;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(x[e], sc, -mnew));
+          pb[e] = (__bf16)p;
+          ps += p;
+        }
+        l[qt] = l[qt] * alpha + rows_sum(ps);
+        m[qt] = mnew;
+        if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
+#pragma unroll
+          for (int ct = 0; ct < 4; ++ct) o[qt][ct] *= alpha;
+        }
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) o[qt][ct] = mfma_bf(va[ct], pb, o[qt][ct]);
       }
     }
   }
