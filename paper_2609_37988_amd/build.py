@@ -26,10 +26,16 @@ FLAGS = [
 ]
 
 
+# Per-source flags.  The selector's attention kernel rescales its product
+# accumulators on the VALU now and then; with the accumulators in AGPRs the compiler
+# copies them to VGPRs and back on every loop iteration, so its MFMAs write VGPRs.
+EXTRA = {"selector.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def _compile(src: str) -> str:
     obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
     lang = ["-x", "hip"] if src.endswith(".hip") else []
-    cmd = [HIPCC, *FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [HIPCC, *FLAGS, *EXTRA.get(src, []), *lang, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")

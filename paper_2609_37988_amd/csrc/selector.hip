@@ -13,9 +13,10 @@
 //   sel_layernorm_kernel: one wave per row of 256, fp32 in, bf16 out.
 //   sel_attention_kernel: bidirectional attention, 4 heads of 64; a workgroup takes
 //       128 queries of one head (4 waves x two 16-query tiles) and walks the keys
-//       in tiles of 64 staged in LDS (consumed as two halves of 32); S^T = K Q^T, online softmax (base 2) per
-//       query, O^T += V^T P^T with P^T taken straight from the S^T accumulators
-//       (the key order of the product's k-slots follows the accumulator layout).
+//       in tiles of 64, double-buffered in LDS; S^T = K Q^T, one online-softmax
+//       step (base 2) per query and tile, O^T += V^T P^T with P^T taken straight
+//       from the S^T accumulators (the key order of the product's k-slots follows
+//       the accumulator layout), the probability sums on MFMA as well.
 //   sel_pool_kernel / sel_heads_kernel: the time average (per-chunk partial sums,
 //       then their sum), the per-layer logits and the argmax.
 #include <hip/hip_runtime.h>
@@ -126,13 +127,21 @@ __global__ __launch_bounds__(256) void sel_layernorm_kernel(const float* x, cons
 }
 
 // Bidirectional attention.  Workgroup: 128 queries (wave w: queries 32 w .. 32 w + 31
-// of the group, two 16-query tiles) of head h; keys in tiles of 64 through LDS, each
-// consumed as two halves of 32 whose key and value operands serve both query tiles.
+// of the group, two 16-query tiles) of head h; keys in tiles of 64, double-buffered
+// in LDS: each thread's share of the next tile is loaded into registers while the
+// current tile is consumed and stored after it, so one barrier per tile suffices.
+// Per key tile, for both query tiles in turn, phase by phase (so that the MFMAs of one
+// tile overlap the VALU work of the other): S^T = K Q^T (8 MFMAs each), one online-
+// softmax step over the 64 keys, O^T += V^T P^T (8 MFMAs each) with P^T taken
+// straight from the S^T accumulators, and the probability sums by one more MFMA per
+// 32 keys with an all-ones left operand: every lane then holds its query's sum (no
+// cross-lane reduction), and the sums cover exactly the rounded probabilities that
+// enter the product.
 __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, const uint16_t* vt, int vt_pitch,
                                                             uint16_t* out, int T) {
   constexpr int KT = 64;
-  __shared__ uint16_t ks[KT][kDh + 8];   // key rows of the tile
-  __shared__ uint16_t vs[kDh][KT + 8];   // value columns (channel-major) of the tile
+  __shared__ uint16_t ks[2][KT][kDh + 8];  // key rows of the tile
+  __shared__ uint16_t vs[2][kDh][KT + 8];  // value columns (channel-major) of the tile
   const int tid = threadIdx.x, lane = tid & 63, i16 = lane & 15, kg = lane >> 4, wv = tid >> 6;
   const int h = blockIdx.y;
   const int q_base = blockIdx.x * 128 + 32 * wv;
@@ -148,103 +157,128 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
       else qb[qt][j] = bf16x8{};
     }
   }
-  f4 o[2][4] = {};
-  float m[2] = {-INFINITY, -INFINITY}, l[2] = {0.0f, 0.0f};
-  for (int k0 = 0; k0 < T; k0 += KT) {
-    __syncthreads();  // the previous tile is consumed
+  // Staging share of a thread: 8 bf16 of key row (tid >> 3) + 32 hh and 8 keys of
+  // value channel (tid >> 3) + 32 hh, both at offset 8 (tid & 7).
+  const int sr = tid >> 3, s8 = 8 * (tid & 7);
+  uint4 kreg[2], vreg[2];
+  auto fetch = [&](int k0) {
 #pragma unroll
-    for (int hh = 0; hh < 2; ++hh) {  // stage: 8 bf16 of a key row, and 8 bf16 of a value column
-      const int r = (tid >> 3) + 32 * hh, c8 = 8 * (tid & 7);
-      const int key = k0 + r;
-      uint4 kvv = make_uint4(0, 0, 0, 0);
-      if (key < T) kvv = *reinterpret_cast<const uint4*>(qk + (int64_t)key * (2 * kW) + kW + h * kDh + c8);
-      *reinterpret_cast<uint4*>(&ks[r][c8]) = kvv;
-      const int ch = (tid >> 3) + 32 * hh, t8 = 8 * (tid & 7);
-      const uint16_t* vp = vt + (int64_t)(h * kDh + ch) * vt_pitch + k0 + t8;
-      uint4 vvv = make_uint4(0, 0, 0, 0);
-      if (k0 + t8 + 8 <= T) {
-        vvv = *reinterpret_cast<const uint4*>(vp);
+    for (int hh = 0; hh < 2; ++hh) {
+      const int key = k0 + sr + 32 * hh;
+      kreg[hh] = key < T ? *reinterpret_cast<const uint4*>(qk + (int64_t)key * (2 * kW) + kW + h * kDh + s8)
+                         : make_uint4(0, 0, 0, 0);
+      const uint16_t* vp = vt + (int64_t)(h * kDh + sr + 32 * hh) * vt_pitch + k0 + s8;
+      if (k0 + s8 + 8 <= T) {
+        vreg[hh] = *reinterpret_cast<const uint4*>(vp);
       } else {  // past the prompt: zeros (their probabilities are 0, and 0 * garbage could be NaN)
         uint32_t w4[4];
         for (int e = 0; e < 4; ++e) {
-          const uint32_t a0 = k0 + t8 + 2 * e < T ? vp[2 * e] : 0u;
-          const uint32_t a1 = k0 + t8 + 2 * e + 1 < T ? vp[2 * e + 1] : 0u;
+          const uint32_t a0 = k0 + s8 + 2 * e < T ? vp[2 * e] : 0u;
+          const uint32_t a1 = k0 + s8 + 2 * e + 1 < T ? vp[2 * e + 1] : 0u;
           w4[e] = a0 | (a1 << 16);
         }
-        vvv = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+        vreg[hh] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
       }
-      *reinterpret_cast<uint4*>(&vs[ch][t8]) = vvv;
     }
-    __syncthreads();
+  };
+  auto stash = [&](int buf) {
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const int kb = 32 * half;
-      if (k0 + kb >= T) break;  // uniform
-      bf16x8 ka[2][2], va[4];
+    for (int hh = 0; hh < 2; ++hh) {
+      *reinterpret_cast<uint4*>(&ks[buf][sr + 32 * hh][s8]) = kreg[hh];
+      *reinterpret_cast<uint4*>(&vs[buf][sr + 32 * hh][s8]) = vreg[hh];
+    }
+  };
+  bf16x8 ones;
 #pragma unroll
-      for (int tau = 0; tau < 2; ++tau)
+  for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
+  f4 o[2][4] = {}, lsum[2] = {};
+  float m[2] = {-INFINITY, -INFINITY};
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  int buf = 0;
+  for (int k0 = 0; k0 < T; k0 += KT, buf ^= 1) {
+    const bool more = k0 + KT < T;  // uniform
+    if (more) fetch(k0 + KT);
+    // S^T tile tau (keys 16 tau .. + 15 of the tile): A = key rows; V^T operands of
+    // the halves: lane (channel i16, kg) holds the keys of its k-slots, 4 kg .. + 3
+    // and 16 + 4 kg .. + 3 of the half (the S^T accumulator order).
+    bf16x8 ka[4][2], va[2][4];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) ka[tau][j] = *reinterpret_cast<const bf16x8*>(&ks[kb + 16 * tau + i16][32 * j + 8 * kg]);
+    for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) ka[tau][j] = *reinterpret_cast<const bf16x8*>(&ks[buf][16 * tau + i16][32 * j + 8 * kg]);
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
       for (int ct = 0; ct < 4; ++ct) {
-        // V^T operand: lane (channel i16, kg) holds the keys of its k-slots: 4 kg .. + 3, 16 + 4 kg .. + 3
-        const uint16_t* vr = &vs[16 * ct + i16][kb];
+        const uint16_t* vr = &vs[buf][16 * ct + i16][32 * hf];
         const uint2 lo = *reinterpret_cast<const uint2*>(vr + 4 * kg);
         const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16 + 4 * kg);
-        va[ct] = bitcast<bf16x8>(make_uint4(lo.x, lo.y, hi.x, hi.y));
+        va[hf][ct] = bitcast<bf16x8>(make_uint4(lo.x, lo.y, hi.x, hi.y));
       }
+    // lane (query i16, kg) of s[qt][tau] holds the raw score of key 16 tau + 4 kg + e
+    f4 s[2][4] = {};
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+      for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) s[qt][tau] = mfma_bf(ka[tau][j], qb[qt][j], s[qt][tau]);
+    float alpha[2];
+    bf16x8 pb[2][2];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      float x[16];
+#pragma unroll
+      for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) x[4 * tau + e] = s[qt][tau][e];
+      if (!more) {  // the last tile: mask the keys past the prompt
+#pragma unroll
+        for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (k0 + 16 * tau + 4 * kg + e >= T) x[4 * tau + e] = -INFINITY;
+      }
+      float mx = x[0];
+#pragma unroll
+      for (int e = 1; e < 16; ++e) mx = fmaxf(mx, x[e]);
+      // the scale enters the exponent; m holds scaled maxima (finite: the tile holds a key)
+      const float mnew = fmaxf(m[qt], rows_max(mx) * sc);
+      alpha[qt] = __builtin_amdgcn_exp2f(m[qt] - mnew);
+      m[qt] = mnew;
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pb[qt][hf][e] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[8 * hf + e], sc, -mnew));
+    }
+    // rescale only when some query's running max moved (rare once it has settled)
+    if (__builtin_amdgcn_ballot_w64(alpha[0] != 1.0f || alpha[1] != 1.0f)) {
 #pragma unroll
       for (int qt = 0; qt < 2; ++qt) {
-        // S^T tiles tau = 0, 1: lane (query i16, kg) holds keys kb + 16 tau + 4 kg + e
-        f4 s[2] = {};
 #pragma unroll
-        for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-          for (int j = 0; j < 2; ++j) s[tau] = mfma_bf(ka[tau][j], qb[qt][j], s[tau]);
-        // raw scores; the scale enters the exponent (m holds scaled maxima)
-        float x[8];
-#pragma unroll
-        for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) x[4 * tau + e] = s[tau][e];
-        if (k0 + kb + 32 > T) {  // the last keys: mask those past the prompt
-#pragma unroll
-          for (int tau = 0; tau < 2; ++tau)
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              if (k0 + kb + 16 * tau + 4 * kg + e >= T) x[4 * tau + e] = -INFINITY;
-        }
-        float mx = x[0];
-#pragma unroll
-        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, x[e]);
-        mx = rows_max(mx) * sc;
-        const float mnew = fmaxf(m[qt], mx);
-        const float alpha = __builtin_amdgcn_exp2f(m[qt] - mnew);
-        float ps = 0.0f;
-        bf16x8 pb;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(x[e], sc, -mnew));
-          pb[e] = (__bf16)p;
-          ps += p;
-        }
-        l[qt] = l[qt] * alpha + rows_sum(ps);
-        m[qt] = mnew;
-        if (__builtin_amdgcn_ballot_w64(alpha != 1.0f)) {
-#pragma unroll
-          for (int ct = 0; ct < 4; ++ct) o[qt][ct] *= alpha;
-        }
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct) o[qt][ct] = mfma_bf(va[ct], pb, o[qt][ct]);
+        for (int ct = 0; ct < 4; ++ct) o[qt][ct] *= alpha[qt];
+        lsum[qt] *= alpha[qt];
       }
     }
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) o[qt][ct] = mfma_bf(va[hf][ct], pb[qt][hf], o[qt][ct]);
+        lsum[qt] = mfma_bf(ones, pb[qt][hf], lsum[qt]);
+      }
+    if (more) stash(buf ^ 1);  // that buffer was last read before the previous barrier
+    __syncthreads();
   }
   // O^T tiles: lane (query i16, kg) holds channels 16 ct + 4 kg + e
 #pragma unroll
   for (int qt = 0; qt < 2; ++qt) {
     const int q = q_base + 16 * qt + i16;
     if (q >= T) continue;
-    const float inv = 1.0f / l[qt];
+    const float inv = 1.0f / lsum[qt][0];
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
