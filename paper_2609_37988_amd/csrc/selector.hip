@@ -6,7 +6,8 @@
 //
 // Kernels (T = prompt length):
 //   sel_gemm_kernel<EPI>: C = A [T, K] . W^T, W [N, K] (bf16 operands on MFMA
-//       16x16x32, fp32 accumulation); one wave per 32 x 32 output tile; the epilogue
+//       16x16x32, fp32 accumulation); 64 x 256 output tiles per workgroup, the A and
+//       W rows of each k-step staged in LDS (double-buffered); the epilogue
 //       adds the bias and, by EPI: stores fp32, adds into the fp32 residual stream,
 //       applies GELU and stores bf16, or splits q, k (bf16 rows) and v (bf16,
 //       transposed per head for the attention's value operand).
@@ -18,7 +19,7 @@
 //       from the S^T accumulators (the key order of the product's k-slots follows
 //       the accumulator layout), the probability sums on MFMA as well.
 //   sel_pool_kernel / sel_heads_kernel: the time average (per-chunk partial sums,
-//       then their sum), the per-layer logits and the argmax.
+//       then their sum), the per-layer logits and the argmax (a workgroup per layer).
 #include <hip/hip_runtime.h>
 
 #include "kvk_device.h"
@@ -52,53 +53,91 @@ struct GemmArgs {
   int32_t M, N, K, vt_pitch;
 };
 
-// One wave per 32 x 32 tile of C; lane (row i16, k-group kg) feeds 8 consecutive
-// k of its row of A and of its row of W per step.
+// Workgroup tile: 64 rows of C x 256 columns (N % 256 == 0, K % 32 == 0), wave w
+// takes columns 64 w .. + 63 of all 64 rows (4 x 4 MFMA tiles).  Per k-step of 32 the
+// A rows and W rows of the tile are staged in LDS (double-buffered: the next step's
+// share of each thread is loaded into registers while the current step is consumed,
+// one barrier per step); lane (row i16, k-group kg) feeds 8 consecutive k.
 template <int EPI>
 __global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
-  const int lane = threadIdx.x & 63, i16 = lane & 15, kg = lane >> 4;
-  const int wave = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int tiles_n = g.N / 32;
-  const int tm = wave / tiles_n, tn = wave % tiles_n;
-  if (tm * 32 >= g.M) return;
-  const int r0 = tm * 32, c0 = tn * 32;
-  f4 acc[2][2] = {};
-  for (int k0 = 0; k0 < g.K; k0 += 32) {
-    bf16x8 av[2], wv[2];
+  constexpr int BM = 64, BN = 256, KP = 32 + 8;  // LDS row pitch (halfs)
+  __shared__ uint16_t as[2][BM][KP];
+  __shared__ uint16_t bs[2][BN][KP];
+  const int tid = threadIdx.x, lane = tid & 63, i16 = lane & 15, kg = lane >> 4, wv = tid >> 6;
+  const int r0 = blockIdx.x * BM, c0 = blockIdx.y * BN;
+  // staging share: A row tid / 4 and W rows tid / 4 + 64 r, 8 k at 8 (tid % 4)
+  const int sr = tid >> 2, sk = 8 * (tid & 3);
+  const bool a_ok = r0 + sr < g.M;
+  const uint16_t* ap = g.a + (int64_t)(a_ok ? r0 + sr : 0) * g.K + sk;
+  const uint16_t* wp = g.w + (int64_t)(c0 + sr) * g.K + sk;
+  const int64_t wstep = (int64_t)64 * g.K;
+  uint4 areg, w0, w1, w2, w3;
+  auto fetch = [&](int k0) {
+    areg = a_ok ? *reinterpret_cast<const uint4*>(ap + k0) : make_uint4(0, 0, 0, 0);
+    w0 = *reinterpret_cast<const uint4*>(wp + k0);
+    w1 = *reinterpret_cast<const uint4*>(wp + wstep + k0);
+    w2 = *reinterpret_cast<const uint4*>(wp + 2 * wstep + k0);
+    w3 = *reinterpret_cast<const uint4*>(wp + 3 * wstep + k0);
+  };
+  auto stash = [&](int buf) {
+    *reinterpret_cast<uint4*>(&as[buf][sr][sk]) = areg;
+    *reinterpret_cast<uint4*>(&bs[buf][sr][sk]) = w0;
+    *reinterpret_cast<uint4*>(&bs[buf][sr + 64][sk]) = w1;
+    *reinterpret_cast<uint4*>(&bs[buf][sr + 128][sk]) = w2;
+    *reinterpret_cast<uint4*>(&bs[buf][sr + 192][sk]) = w3;
+  };
+  f4 acc[4][4] = {};
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  int buf = 0;
+  for (int k0 = 0; k0 < g.K; k0 += 32, buf ^= 1) {
+    const bool more = k0 + 32 < g.K;  // uniform
+    if (more) fetch(k0 + 32);
+    bf16x8 av[4], wv8[4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int r = r0 + 16 * i + i16;
-      if (r < g.M) av[i] = *reinterpret_cast<const bf16x8*>(g.a + (int64_t)r * g.K + k0 + 8 * kg);
-      else av[i] = bf16x8{};
-      wv[i] = *reinterpret_cast<const bf16x8*>(g.w + (int64_t)(c0 + 16 * i + i16) * g.K + k0 + 8 * kg);
+    for (int i = 0; i < 4; ++i) {
+      av[i] = *reinterpret_cast<const bf16x8*>(&as[buf][16 * i + i16][8 * kg]);
+      wv8[i] = *reinterpret_cast<const bf16x8*>(&bs[buf][64 * wv + 16 * i + i16][8 * kg]);
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j) acc[i][j] = mfma_bf(wv[j], av[i], acc[i][j]);  // C^T tile: rows n, cols m
+      for (int j = 0; j < 4; ++j) acc[i][j] = mfma_bf(wv8[j], av[i], acc[i][j]);  // C^T tile: rows n, cols m
+    if (more) stash(buf ^ 1);  // that buffer was last read before the previous barrier
+    __syncthreads();
   }
-  // acc[i][j]: lane (m = r0 + 16 i + i16) holds n = c0 + 16 j + 4 kg + e
+  // acc[i][j]: lane (m = r0 + 16 i + i16) holds n = c0 + 64 wv + 16 j + 4 kg + e
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < 4; ++i) {
     const int m = r0 + 16 * i + i16;
     if (m >= g.M) continue;
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < 4; ++j) {
+      const int n0 = c0 + 64 * wv + 16 * j + 4 * kg;
+      f4 v = acc[i][j];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int n = c0 + 16 * j + 4 * kg + e;
-        const float v = acc[i][j][e] + bf16_to_f32(g.bias[n]);
-        if constexpr (EPI == kStoreF32) {
-          g.out_f32[(int64_t)m * g.N + n] = v;
-        } else if constexpr (EPI == kAddF32) {
-          g.out_f32[(int64_t)m * g.N + n] += v;
-        } else if constexpr (EPI == kGeluBf16) {
-          g.out_bf16[(int64_t)m * g.N + n] = f32_to_bf16_bits(gelu_tanh(v));
-        } else {
-          if (n < 2 * kW) g.out_bf16[(int64_t)m * (2 * kW) + n] = f32_to_bf16_bits(v);
-          else g.vt[(int64_t)(n - 2 * kW) * g.vt_pitch + m] = f32_to_bf16_bits(v);
-        }
+      for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(g.bias[n0 + e]);
+      if constexpr (EPI == kStoreF32) {
+        *reinterpret_cast<f4*>(g.out_f32 + (int64_t)m * g.N + n0) = v;
+      } else if constexpr (EPI == kAddF32) {
+        f4* px = reinterpret_cast<f4*>(g.out_f32 + (int64_t)m * g.N + n0);
+        *px = *px + v;
+      } else if constexpr (EPI == kGeluBf16) {
+        uint2 w2;
+        w2.x = (uint32_t)f32_to_bf16_bits(gelu_tanh(v[0])) | ((uint32_t)f32_to_bf16_bits(gelu_tanh(v[1])) << 16);
+        w2.y = (uint32_t)f32_to_bf16_bits(gelu_tanh(v[2])) | ((uint32_t)f32_to_bf16_bits(gelu_tanh(v[3])) << 16);
+        *reinterpret_cast<uint2*>(g.out_bf16 + (int64_t)m * g.N + n0) = w2;
+      } else if (n0 < 2 * kW) {  // q, k rows (the 4 columns never straddle 512)
+        uint2 w2;
+        w2.x = (uint32_t)f32_to_bf16_bits(v[0]) | ((uint32_t)f32_to_bf16_bits(v[1]) << 16);
+        w2.y = (uint32_t)f32_to_bf16_bits(v[2]) | ((uint32_t)f32_to_bf16_bits(v[3]) << 16);
+        *reinterpret_cast<uint2*>(g.out_bf16 + (int64_t)m * (2 * kW) + n0) = w2;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) g.vt[(int64_t)(n0 + e - 2 * kW) * g.vt_pitch + m] = f32_to_bf16_bits(v[e]);
       }
+    }
   }
 }
 
@@ -287,40 +326,59 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
   }
 }
 
-// Partial column sums of x over chunks of 256 rows: part[chunk][c].
+// Partial column sums of x over chunks of 256 rows: part[chunk][c].  Thread
+// (columns 4 (tid % 64) .. + 3, row group tid / 64) adds every fourth row of the
+// chunk; the four row groups meet in LDS.
 __global__ __launch_bounds__(256) void sel_pool_kernel(const float* x, float* part, int T) {
-  const int c = threadIdx.x, chunk = blockIdx.x;
-  const int t1 = min(T, (chunk + 1) * 256);
-  float s = 0.0f;
-  for (int t = chunk * 256; t < t1; ++t) s += x[(int64_t)t * kW + c];
-  part[(int64_t)chunk * kW + c] = s;
+  __shared__ float red[4][kW];
+  const int tid = threadIdx.x, c4 = tid & 63, rg = tid >> 6, chunk = blockIdx.x;
+  const int t0 = chunk * 256, t1 = min(T, t0 + 256);
+  f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+  for (int t = t0 + rg; t < t1; t += 4) acc += *reinterpret_cast<const f4*>(x + (int64_t)t * kW + 4 * c4);
+  *reinterpret_cast<f4*>(&red[rg][4 * c4]) = acc;
+  __syncthreads();
+  part[(int64_t)chunk * kW + tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
 }
 
-// The feature (mean of the partial sums), the per-layer logits, the argmax (the
-// lowest action on ties; the depth action never at layer 0).  One workgroup.
+// One workgroup per layer l: the feature (thread c: the mean over the partial sums of
+// channel c), the layer's 5 logits (products reduced over the 256 channels), and the
+// argmax (the lowest action on ties; the depth action never at layer 0).
 __global__ __launch_bounds__(256) void sel_heads_kernel(const float* part, int n_chunks, int T, const uint16_t* w_head,
-                                                        const uint16_t* b_head, int L, float* logits, int32_t* action) {
-  __shared__ float f[kW];
-  __shared__ float z[64 * kActions];
-  const int tid = threadIdx.x;
-  float s = 0.0f;
-  for (int k = 0; k < n_chunks; ++k) s += part[(int64_t)k * kW + tid];
-  f[tid] = s / (float)T;
-  __syncthreads();
-  for (int i = tid; i < L * kActions; i += 256) {
-    const int l = i / kActions, a = i % kActions;
-    float acc = bf16_to_f32(b_head[i]);
-    for (int c = 0; c < kW; ++c) acc += f[c] * bf16_to_f32(w_head[((int64_t)l * kW + c) * kActions + a]);
-    if (l == 0 && a == 0) acc = -INFINITY;
-    z[i] = acc;
-    if (logits) logits[i] = acc;
+                                                        const uint16_t* b_head, float* logits, int32_t* action) {
+  __shared__ float red[4][kActions];
+  const int c = threadIdx.x, lane = c & 63, wv = c >> 6, l = blockIdx.x;
+  float f4s[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // four independent chains over the chunks
+  int k = 0;
+  for (; k + 4 <= n_chunks; k += 4)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) f4s[u] += part[(int64_t)(k + u) * kW + c];
+  for (; k < n_chunks; ++k) f4s[0] += part[(int64_t)k * kW + c];
+  const float f = (f4s[0] + f4s[1] + f4s[2] + f4s[3]) / (float)T;
+  float z[kActions];
+#pragma unroll
+  for (int a = 0; a < kActions; ++a) {
+    z[a] = f * bf16_to_f32(w_head[((int64_t)l * kW + c) * kActions + a]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) z[a] += __shfl_xor(z[a], off);
   }
+  if (lane == 0)
+#pragma unroll
+    for (int a = 0; a < kActions; ++a) red[wv][a] = z[a];
   __syncthreads();
-  if (tid < L) {
+  if (c == 0) {
     int best = 0;
-    for (int a = 1; a < kActions; ++a)
-      if (z[tid * kActions + a] > z[tid * kActions + best]) best = a;
-    action[tid] = best;
+    float zb = 0.0f;
+    for (int a = 0; a < kActions; ++a) {
+      float v = red[0][a] + red[1][a] + red[2][a] + red[3][a] + bf16_to_f32(b_head[l * kActions + a]);
+      if (l == 0 && a == 0) v = -INFINITY;
+      if (logits) logits[l * kActions + a] = v;
+      if (a == 0 || v > zb) {
+        best = a;
+        zb = v;
+      }
+    }
+    action[l] = best;
   }
 }
 
@@ -415,8 +473,7 @@ extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, co
     g.N = N;
     g.K = K;
     g.vt_pitch = Wk.vt_pitch;
-    const int waves = (T + 31) / 32 * (N / 32);
-    const dim3 grid((unsigned)((waves + 3) / 4)), blk(256);
+    const dim3 grid((unsigned)((T + 63) / 64), (unsigned)(N / 256)), blk(256);
     switch (epi) {
       case kStoreF32: hipLaunchKernelGGL(sel_gemm_kernel<kStoreF32>, grid, blk, 0, stream, g); break;
       case kAddF32: hipLaunchKernelGGL(sel_gemm_kernel<kAddF32>, grid, blk, 0, stream, g); break;
@@ -442,8 +499,8 @@ extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, co
   }
   const int chunks = (T + 255) / 256;
   hipLaunchKernelGGL(sel_pool_kernel, dim3((unsigned)chunks), b256, 0, stream, x, part, T);
-  hipLaunchKernelGGL(sel_heads_kernel, dim3(1), b256, 0, stream, part, chunks, T, wp + O.w_head, wp + O.b_head,
-                     n_layers, logits, actions);
+  hipLaunchKernelGGL(sel_heads_kernel, dim3((unsigned)n_layers), b256, 0, stream, part, chunks, T, wp + O.w_head,
+                     wp + O.b_head, logits, actions);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "selector launch: %s", hipGetErrorString(e));
   return KVK_OK;

@@ -55,10 +55,10 @@ def _weights(seed, d_model, L):
     return ow, torch.cat([t.reshape(-1) for t in packed]).contiguous()
 
 
-@pytest.mark.parametrize("T", [100, 1000, 3000])
-def test_selector_matches_oracle(T):
-    d_model, L = 512, 48
-    say(f"case selector T={T}")
+@pytest.mark.parametrize("T,L", [(100, 48), (1000, 48), (3000, 48), (1, 64), (300, 7)])
+def test_selector_matches_oracle(T, L):
+    d_model = 512
+    say(f"case selector T={T} L={L}")
     ow, packed = _weights(1500 + T, d_model, L)
     assert packed.numel() == kvk.selector_weight_elems(d_model, L)
     rng = np.random.default_rng(1600 + T)
