@@ -22,6 +22,8 @@
 //       then their sum), the per-layer logits and the argmax (a workgroup per layer).
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kvk_device.h"
 #include "kvk_internal.h"
 
@@ -169,13 +171,15 @@ __global__ __launch_bounds__(256) void sel_layernorm_kernel(const float* x, cons
 // of the group, two 16-query tiles) of head h; keys in tiles of 64, double-buffered
 // in LDS: each thread's share of the next tile is loaded into registers while the
 // current tile is consumed and stored after it, so one barrier per tile suffices.
-// Per key tile, for both query tiles in turn, phase by phase (so that the MFMAs of one
-// tile overlap the VALU work of the other): S^T = K Q^T (8 MFMAs each), one online-
-// softmax step over the 64 keys, O^T += V^T P^T (8 MFMAs each) with P^T taken
-// straight from the S^T accumulators, and the probability sums by one more MFMA per
-// 32 keys with an all-ones left operand: every lane then holds its query's sum (no
-// cross-lane reduction), and the sums cover exactly the rounded probabilities that
-// enter the product.
+// Per key tile: S^T = K Q^T for both query tiles (8 MFMAs each), the tile's score
+// maxima, then per query tile the probabilities and O^T += V^T P^T (8 MFMAs) with P^T
+// taken straight from the S^T accumulators, and the probability sums by one more MFMA
+// per 32 keys with an all-ones left operand: every lane then holds its query's sum
+// (no cross-lane reduction), and the sums cover exactly the rounded probabilities
+// that enter the product.  The running max (base 2, scaled) moves only when a tile's
+// max exceeds it by more than 8, so probabilities stay below 2^8 (exact in the
+// normalised result; fp32 sums) and the rescaling of the accumulators is rare.  Only
+// the last key tile is masked.
 __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, const uint16_t* vt, int vt_pitch,
                                                             uint16_t* out, int T) {
   constexpr int KT = 64;
@@ -200,6 +204,14 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
   // value channel (tid >> 3) + 32 hh, both at offset 8 (tid & 7).
   const int sr = tid >> 3, s8 = 8 * (tid & 7);
   uint4 kreg[2], vreg[2];
+  // whole tile inside the prompt: no checks
+  auto fetch_full = [&](int k0) {
+#pragma unroll
+    for (int hh = 0; hh < 2; ++hh) {
+      kreg[hh] = *reinterpret_cast<const uint4*>(qk + (int64_t)(k0 + sr + 32 * hh) * (2 * kW) + kW + h * kDh + s8);
+      vreg[hh] = *reinterpret_cast<const uint4*>(vt + (int64_t)(h * kDh + sr + 32 * hh) * vt_pitch + k0 + s8);
+    }
+  };
   auto fetch = [&](int k0) {
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
@@ -232,13 +244,8 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
   for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
   f4 o[2][4] = {}, lsum[2] = {};
   float m[2] = {-INFINITY, -INFINITY};
-  fetch(0);
-  stash(0);
-  __syncthreads();
-  int buf = 0;
-  for (int k0 = 0; k0 < T; k0 += KT, buf ^= 1) {
-    const bool more = k0 + KT < T;  // uniform
-    if (more) fetch(k0 + KT);
+  auto tile = [&](int k0, int buf, auto last_tag) {
+    constexpr bool kLast = decltype(last_tag)::value;
     // S^T tile tau (keys 16 tau .. + 15 of the tile): A = key rows; V^T operands of
     // the halves: lane (channel i16, kg) holds the keys of its k-slots, 4 kg .. + 3
     // and 16 + 4 kg .. + 3 of the half (the S^T accumulator order).
@@ -264,54 +271,65 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
       for (int tau = 0; tau < 4; ++tau)
 #pragma unroll
         for (int j = 0; j < 2; ++j) s[qt][tau] = mfma_bf(ka[tau][j], qb[qt][j], s[qt][tau]);
-    float alpha[2];
-    bf16x8 pb[2][2];
+    float mt[2];
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt) {
-      float x[16];
-#pragma unroll
-      for (int tau = 0; tau < 4; ++tau)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) x[4 * tau + e] = s[qt][tau][e];
-      if (!more) {  // the last tile: mask the keys past the prompt
+      if constexpr (kLast) {  // mask the keys past the prompt
 #pragma unroll
         for (int tau = 0; tau < 4; ++tau)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (k0 + 16 * tau + 4 * kg + e >= T) x[4 * tau + e] = -INFINITY;
+            if (k0 + 16 * tau + 4 * kg + e >= T) s[qt][tau][e] = -INFINITY;
       }
-      float mx = x[0];
+      float mx = s[qt][0][0];
 #pragma unroll
-      for (int e = 1; e < 16; ++e) mx = fmaxf(mx, x[e]);
-      // the scale enters the exponent; m holds scaled maxima (finite: the tile holds a key)
-      const float mnew = fmaxf(m[qt], rows_max(mx) * sc);
-      alpha[qt] = __builtin_amdgcn_exp2f(m[qt] - mnew);
-      m[qt] = mnew;
+      for (int tau = 0; tau < 4; ++tau)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) mx = fmaxf(mx, s[qt][tau][e]);
+      mt[qt] = rows_max(mx) * sc;  // the scale enters the exponent
+    }
+    // move the running max (and rescale) only past a margin of 8; finite: the tile holds a key
+    if (__builtin_amdgcn_ballot_w64(mt[0] > m[0] + 8.0f || mt[1] > m[1] + 8.0f)) {
+#pragma unroll
+      for (int qt = 0; qt < 2; ++qt) {
+        const float mnew = fmaxf(m[qt], mt[qt]);
+        const float alpha = __builtin_amdgcn_exp2f(m[qt] - mnew);
+        m[qt] = mnew;
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct) o[qt][ct] *= alpha;
+        lsum[qt] *= alpha;
+      }
+    }
+    
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      bf16x8 pb[2];
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pb[qt][hf][e] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(x[8 * hf + e], sc, -mnew));
-    }
-    // rescale only when some query's running max moved (rare once it has settled)
-    if (__builtin_amdgcn_ballot_w64(alpha[0] != 1.0f || alpha[1] != 1.0f)) {
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
-#pragma unroll
-        for (int ct = 0; ct < 4; ++ct) o[qt][ct] *= alpha[qt];
-        lsum[qt] *= alpha[qt];
-      }
-    }
-#pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+        for (int e = 0; e < 8; ++e)
+          pb[hf][e] = (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[qt][2 * hf + (e >> 2)][e & 3], sc, -m[qt]));  // <= 2^8
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
 #pragma unroll
-        for (int ct = 0; ct < 4; ++ct) o[qt][ct] = mfma_bf(va[hf][ct], pb[qt][hf], o[qt][ct]);
-        lsum[qt] = mfma_bf(ones, pb[qt][hf], lsum[qt]);
+        for (int ct = 0; ct < 4; ++ct) o[qt][ct] = mfma_bf(va[hf][ct], pb[hf], o[qt][ct]);
+        lsum[qt] = mfma_bf(ones, pb[hf], lsum[qt]);
       }
-    if (more) stash(buf ^ 1);  // that buffer was last read before the previous barrier
+    }
+    
+  };
+  fetch(0);
+  stash(0);
+  __syncthreads();
+  int buf = 0, k0 = 0;
+  for (; k0 + KT < T; k0 += KT, buf ^= 1) {
+    if (k0 + 2 * KT <= T) fetch_full(k0 + KT);  // uniform
+    else fetch(k0 + KT);
+    tile(k0, buf, std::false_type{});
+    stash(buf ^ 1);  // that buffer was last read before the previous barrier
     __syncthreads();
   }
+  tile(k0, buf, std::true_type{});
   // O^T tiles: lane (query i16, kg) holds channels 16 ct + 4 kg + e
 #pragma unroll
   for (int qt = 0; qt < 2; ++qt) {
