@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--cpu-layers", type=int, default=0, help="layers in the CPU sample (0: auto)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
+    ap.add_argument("--selector-tokens", type=int, default=0,
+                    help="only time the selector forward pass at this many prompt tokens "
+                         "(workload 2's embedding width and layers)")
     return ap.parse_args()
 
 
@@ -387,6 +390,17 @@ def main():
         sys.exit(2)
     if args.config == 3:
         run_mla(args)
+        return
+    if args.selector_tokens > 0:
+        import torch
+
+        from paper_2609_37988_amd import kvk, synth
+
+        dev = torch.device("cuda:0")
+        torch.cuda.set_device(dev)
+        w = synth.workload(2)
+        sel = time_selector(kvk, torch, w.n_q_heads * w.head_dim, w.n_layers, dev, lengths=(args.selector_tokens,))
+        print(json.dumps({"selector_forward": sel}), flush=True)
         return
     import numpy as np
     import torch

@@ -22,6 +22,7 @@
 //       then their sum), the per-layer logits and the argmax (a workgroup per layer).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "kvk_device.h"
@@ -52,7 +53,9 @@ struct GemmArgs {
   float* out_f32;      // [M][N] (kStoreF32, kAddF32)
   uint16_t* out_bf16;  // [M][N] (kGeluBf16), [M][512] q|k (kQkv)
   uint16_t* vt;        // kQkv: [heads][64][vt_pitch] values, transposed
+  float* part;         // split-K: [gridDim.z][M][N] raw partial sums (no epilogue); else null
   int32_t M, N, K, vt_pitch;
+  int32_t k_len;       // k per split (a multiple of 32)
 };
 
 // Workgroup tile: 64 rows of C x 256 columns (N % 256 == 0, K % 32 == 0), wave w
@@ -89,12 +92,13 @@ __global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
     *reinterpret_cast<uint4*>(&bs[buf][sr + 192][sk]) = w3;
   };
   f4 acc[4][4] = {};
-  fetch(0);
+  const int kb = blockIdx.z * g.k_len, ke = min(g.K, kb + g.k_len);  // this split's k range
+  fetch(kb);
   stash(0);
   __syncthreads();
   int buf = 0;
-  for (int k0 = 0; k0 < g.K; k0 += 32, buf ^= 1) {
-    const bool more = k0 + 32 < g.K;  // uniform
+  for (int k0 = kb; k0 < ke; k0 += 32, buf ^= 1) {
+    const bool more = k0 + 32 < ke;  // uniform
     if (more) fetch(k0 + 32);
     bf16x8 av[4], wv8[4];
 #pragma unroll
@@ -117,6 +121,10 @@ __global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n0 = c0 + 64 * wv + 16 * j + 4 * kg;
+      if (g.part) {  // split-K: the reduce kernel applies the epilogue
+        *reinterpret_cast<f4*>(g.part + ((int64_t)blockIdx.z * g.M + m) * g.N + n0) = acc[i][j];
+        continue;
+      }
       f4 v = acc[i][j];
 #pragma unroll
       for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(g.bias[n0 + e]);
@@ -141,6 +149,23 @@ __global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
       }
     }
   }
+}
+
+// Split-K epilogue for the fp32 outputs (N = 256): out[m][n] (+)= sum over the splits
+// of part[s][m][n] + bias[n], in split order.  One thread per 4 columns.
+template <int EPI>
+__global__ __launch_bounds__(256) void sel_splitk_kernel(const float* part, int splits, const uint16_t* bias,
+                                                         float* out, int M) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;  // f4 index
+  if (i >= (int64_t)M * (kW / 4)) return;
+  const int n0 = 4 * (int)(i % (kW / 4));
+  f4 v = *reinterpret_cast<const f4*>(part + 4 * i);
+  for (int sp = 1; sp < splits; ++sp) v += *reinterpret_cast<const f4*>(part + (int64_t)sp * M * kW + 4 * i);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(bias[n0 + e]);
+  f4* po = reinterpret_cast<f4*>(out + 4 * i);
+  if constexpr (EPI == kAddF32) *po = *po + v;
+  else *po = v;
 }
 
 // One wave per row of 256: LayerNorm (eps 1e-5, gain and bias) to bf16.
@@ -420,9 +445,22 @@ SelOffsets sel_offsets(int d_model, int L) {
 }
 
 struct SelWorkspace {
-  int64_t x, h, qk, vt, f1, part, total;  // byte offsets
+  int64_t x, h, qk, vt, f1, part, splitk, total;  // byte offsets
   int vt_pitch;
 };
+
+// Split-K for the long-K GEMMs with 256 output columns (the input map, K = d_model,
+// and the second feed-forward matrix, K = 1024) when their 64-row tiles alone
+// would give few workgroups: enough splits for about 512 workgroups, at most 16,
+// each split at least 8 k-steps of 32.
+constexpr int kSplitMax = 16;
+int sel_splits(int T, int K) {
+  const int row_blocks = (T + 63) / 64;
+  int sp = std::min(std::min(kSplitMax, K / 256), (512 + row_blocks - 1) / row_blocks);
+  if (sp <= 1) return 1;
+  const int ksteps = K / 32, per = (ksteps + sp - 1) / sp;
+  return (ksteps + per - 1) / per;  // no empty split
+}
 
 SelWorkspace sel_workspace(int T) {
   SelWorkspace w;
@@ -434,7 +472,9 @@ SelWorkspace sel_workspace(int T) {
   w.vt = kvk::round256(w.qk + (int64_t)Tp * 2 * kW * 2);     // bf16 [256][Tp]
   w.f1 = kvk::round256(w.vt + (int64_t)kW * Tp * 2);         // bf16 [T][1024]
   w.part = kvk::round256(w.f1 + (int64_t)Tp * kFfn * 2);     // fp32 [chunks][256]
-  w.total = kvk::round256(w.part + (int64_t)((T + 255) / 256) * kW * 4);
+  w.splitk = kvk::round256(w.part + (int64_t)((T + 255) / 256) * kW * 4);  // fp32 [splits][T][256]
+  const int max_splits = std::min(kSplitMax, (512 + (T + 63) / 64 - 1) / ((T + 63) / 64));
+  w.total = kvk::round256(w.splitk + (int64_t)std::max(1, max_splits) * T * kW * 4);
   return w;
 }
 
@@ -491,12 +531,22 @@ extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, co
     g.N = N;
     g.K = K;
     g.vt_pitch = Wk.vt_pitch;
-    const dim3 grid((unsigned)((T + 63) / 64), (unsigned)(N / 256)), blk(256);
+    const int splits = (epi == kStoreF32 || epi == kAddF32) ? sel_splits(T, K) : 1;
+    g.k_len = (K / 32 + splits - 1) / splits * 32;
+    g.part = splits > 1 ? reinterpret_cast<float*>(ws + Wk.splitk) : nullptr;
+    const dim3 grid((unsigned)((T + 63) / 64), (unsigned)(N / 256), (unsigned)splits), blk(256);
     switch (epi) {
       case kStoreF32: hipLaunchKernelGGL(sel_gemm_kernel<kStoreF32>, grid, blk, 0, stream, g); break;
       case kAddF32: hipLaunchKernelGGL(sel_gemm_kernel<kAddF32>, grid, blk, 0, stream, g); break;
       case kGeluBf16: hipLaunchKernelGGL(sel_gemm_kernel<kGeluBf16>, grid, blk, 0, stream, g); break;
       default: hipLaunchKernelGGL(sel_gemm_kernel<kQkv>, grid, blk, 0, stream, g); break;
+    }
+    if (splits > 1) {
+      const dim3 rgrid((unsigned)(((int64_t)T * (kW / 4) + 255) / 256));
+      if (epi == kAddF32)
+        hipLaunchKernelGGL(sel_splitk_kernel<kAddF32>, rgrid, blk, 0, stream, g.part, splits, g.bias, x, T);
+      else
+        hipLaunchKernelGGL(sel_splitk_kernel<kStoreF32>, rgrid, blk, 0, stream, g.part, splits, g.bias, x, T);
     }
   };
   const dim3 rows((unsigned)((T + 3) / 4)), b256(256);
