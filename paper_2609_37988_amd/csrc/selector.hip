@@ -17,7 +17,9 @@
 //       in tiles of 64, double-buffered in LDS; S^T = K Q^T, one online-softmax
 //       step (base 2) per query and tile, O^T += V^T P^T with P^T taken straight
 //       from the S^T accumulators (the key order of the product's k-slots follows
-//       the accumulator layout), the probability sums on MFMA as well.
+//       the accumulator layout), the probability sums on MFMA as well; on short
+//       prompts the keys split across workgroups too, and sel_attn_merge_kernel
+//       combines the splits.
 //   sel_pool_kernel / sel_heads_kernel: the time average (per-chunk partial sums,
 //       then their sum), the per-layer logits and the argmax (a workgroup per layer).
 #include <hip/hip_runtime.h>
@@ -34,6 +36,7 @@ namespace {
 
 constexpr int kW = 256, kHeads = 4, kDh = 64, kFfn = 1024, kActions = 5;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kRec = kDh + 4;  // key-split record: 64 outputs, max, sum, 2 pad (16-byte rows)
 
 __device__ __forceinline__ f4 mfma_bf(bf16x8 a, bf16x8 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
@@ -206,13 +209,14 @@ __global__ __launch_bounds__(256) void sel_layernorm_kernel(const float* x, cons
 // normalised result; fp32 sums) and the rescaling of the accumulators is rare.  Only
 // the last key tile is masked.
 __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, const uint16_t* vt, int vt_pitch,
-                                                            uint16_t* out, int T) {
+                                                            uint16_t* out, int T, int key_len, float* part) {
   constexpr int KT = 64;
   __shared__ uint16_t ks[2][KT][kDh + 8];  // key rows of the tile
   __shared__ uint16_t vs[2][kDh][KT + 8];  // value columns (channel-major) of the tile
   const int tid = threadIdx.x, lane = tid & 63, i16 = lane & 15, kg = lane >> 4, wv = tid >> 6;
   const int h = blockIdx.y;
   const int q_base = blockIdx.x * 128 + 32 * wv;
+  const int kb = blockIdx.z * key_len, ke = min(T, kb + key_len);  // this workgroup's keys
   const float sc = 0.125f * kLog2e;  // 1/sqrt(64), base 2
   // the query operand (B of S^T = K Q^T): lane (query i16, kg) holds channels 8 kg .. + 7 of each k-step
   bf16x8 qb[2][2];
@@ -241,16 +245,16 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       const int key = k0 + sr + 32 * hh;
-      kreg[hh] = key < T ? *reinterpret_cast<const uint4*>(qk + (int64_t)key * (2 * kW) + kW + h * kDh + s8)
+      kreg[hh] = key < ke ? *reinterpret_cast<const uint4*>(qk + (int64_t)key * (2 * kW) + kW + h * kDh + s8)
                          : make_uint4(0, 0, 0, 0);
       const uint16_t* vp = vt + (int64_t)(h * kDh + sr + 32 * hh) * vt_pitch + k0 + s8;
-      if (k0 + s8 + 8 <= T) {
+      if (k0 + s8 + 8 <= ke) {
         vreg[hh] = *reinterpret_cast<const uint4*>(vp);
-      } else {  // past the prompt: zeros (their probabilities are 0, and 0 * garbage could be NaN)
+      } else {  // past the key range: zeros (their probabilities are 0, and 0 * garbage could be NaN)
         uint32_t w4[4];
         for (int e = 0; e < 4; ++e) {
-          const uint32_t a0 = k0 + s8 + 2 * e < T ? vp[2 * e] : 0u;
-          const uint32_t a1 = k0 + s8 + 2 * e + 1 < T ? vp[2 * e + 1] : 0u;
+          const uint32_t a0 = k0 + s8 + 2 * e < ke ? vp[2 * e] : 0u;
+          const uint32_t a1 = k0 + s8 + 2 * e + 1 < ke ? vp[2 * e + 1] : 0u;
           w4[e] = a0 | (a1 << 16);
         }
         vreg[hh] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
@@ -304,7 +308,7 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
         for (int tau = 0; tau < 4; ++tau)
 #pragma unroll
           for (int e = 0; e < 4; ++e)
-            if (k0 + 16 * tau + 4 * kg + e >= T) s[qt][tau][e] = -INFINITY;
+            if (k0 + 16 * tau + 4 * kg + e >= ke) s[qt][tau][e] = -INFINITY;
       }
       float mx = s[qt][0][0];
 #pragma unroll
@@ -341,14 +345,13 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
         lsum[qt] = mfma_bf(ones, pb[hf], lsum[qt]);
       }
     }
-    
   };
-  fetch(0);
+  fetch(kb);
   stash(0);
   __syncthreads();
-  int buf = 0, k0 = 0;
-  for (; k0 + KT < T; k0 += KT, buf ^= 1) {
-    if (k0 + 2 * KT <= T) fetch_full(k0 + KT);  // uniform
+  int buf = 0, k0 = kb;
+  for (; k0 + KT < ke; k0 += KT, buf ^= 1) {
+    if (k0 + 2 * KT <= ke) fetch_full(k0 + KT);  // uniform
     else fetch(k0 + KT);
     tile(k0, buf, std::false_type{});
     stash(buf ^ 1);  // that buffer was last read before the previous barrier
@@ -360,6 +363,16 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
   for (int qt = 0; qt < 2; ++qt) {
     const int q = q_base + 16 * qt + i16;
     if (q >= T) continue;
+    if (part) {  // a key split: unnormalised output, running max and sum for the merge
+      float* rec = part + (((int64_t)blockIdx.z * T + q) * kHeads + h) * kRec;
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct) *reinterpret_cast<f4*>(rec + 16 * ct + 4 * kg) = o[qt][ct];
+      if (kg == 0) {
+        rec[kDh] = m[qt];
+        rec[kDh + 1] = lsum[qt][0];
+      }
+      continue;
+    }
     const float inv = 1.0f / lsum[qt][0];
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct)
@@ -367,6 +380,32 @@ __global__ __launch_bounds__(256) void sel_attention_kernel(const uint16_t* qk, 
       for (int e = 0; e < 4; ++e)
         out[(int64_t)q * kW + h * kDh + 16 * ct + 4 * kg + e] = f32_to_bf16_bits(o[qt][ct][e] * inv);
   }
+}
+
+// Merge of the key splits: per (query, head), the splits' outputs weighted by
+// 2^(m_s - M) over the merged sum.  One thread per 4 channels.
+__global__ __launch_bounds__(256) void sel_attn_merge_kernel(const float* part, int splits, int T, uint16_t* out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)T * kHeads * (kDh / 4)) return;
+  const int c4 = (int)(i % (kDh / 4));
+  const int64_t qh = i / (kDh / 4);  // q * kHeads + h
+  const int64_t stride = (int64_t)T * kHeads * kRec;
+  const float* rec = part + qh * kRec;
+  float M = rec[kDh];
+  for (int sp = 1; sp < splits; ++sp) M = fmaxf(M, rec[sp * stride + kDh]);
+  f4 acc = {0.f, 0.f, 0.f, 0.f};
+  float L = 0.0f;
+  for (int sp = 0; sp < splits; ++sp) {
+    const float w = __builtin_amdgcn_exp2f(rec[sp * stride + kDh] - M);
+    acc += w * *reinterpret_cast<const f4*>(rec + sp * stride + 4 * c4);
+    L += w * rec[sp * stride + kDh + 1];
+  }
+  const float inv = 1.0f / L;
+  uint2 w2;
+  w2.x = (uint32_t)f32_to_bf16_bits(acc[0] * inv) | ((uint32_t)f32_to_bf16_bits(acc[1] * inv) << 16);
+  w2.y = (uint32_t)f32_to_bf16_bits(acc[2] * inv) | ((uint32_t)f32_to_bf16_bits(acc[3] * inv) << 16);
+  const int64_t q = qh / kHeads, h = qh % kHeads;
+  *reinterpret_cast<uint2*>(out + q * kW + h * kDh + 4 * c4) = w2;
 }
 
 // Partial column sums of x over chunks of 256 rows: part[chunk][c].  Thread
@@ -445,9 +484,23 @@ SelOffsets sel_offsets(int d_model, int L) {
 }
 
 struct SelWorkspace {
-  int64_t x, h, qk, vt, f1, part, splitk, total;  // byte offsets
+  int64_t x, h, qk, vt, f1, part, splitk, attn, total;  // byte offsets
   int vt_pitch;
 };
+
+// Key splits of the attention when its 128-query workgroups alone would be fewer
+// than about 512: each split at least 256 keys, a multiple of 64; no empty split.
+// Returns the split count; *key_len gets the keys per split.
+int sel_attn_splits(int T, int* key_len) {
+  const int wgs = (T + 127) / 128 * kHeads;
+  const int sp = std::min((512 + wgs - 1) / wgs, T / 256);
+  if (sp <= 1) {
+    *key_len = T;
+    return 1;
+  }
+  *key_len = ((T + sp - 1) / sp + 63) / 64 * 64;
+  return (T + *key_len - 1) / *key_len;
+}
 
 // Split-K for the long-K GEMMs with 256 output columns (the input map, K = d_model,
 // and the second feed-forward matrix, K = 1024) when their 64-row tiles alone
@@ -474,7 +527,10 @@ SelWorkspace sel_workspace(int T) {
   w.part = kvk::round256(w.f1 + (int64_t)Tp * kFfn * 2);     // fp32 [chunks][256]
   w.splitk = kvk::round256(w.part + (int64_t)((T + 255) / 256) * kW * 4);  // fp32 [splits][T][256]
   const int max_splits = std::min(kSplitMax, (512 + (T + 63) / 64 - 1) / ((T + 63) / 64));
-  w.total = kvk::round256(w.splitk + (int64_t)std::max(1, max_splits) * T * kW * 4);
+  w.attn = kvk::round256(w.splitk + (int64_t)std::max(1, max_splits) * T * kW * 4);  // fp32 [splits][T][4][kRec]
+  int key_len = 0;
+  const int attn_splits = sel_attn_splits(T, &key_len);
+  w.total = kvk::round256(w.attn + (attn_splits > 1 ? (int64_t)attn_splits * T * kHeads * kRec * 4 : 0));
   return w;
 }
 
@@ -558,8 +614,16 @@ extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, co
                   w_1 = ln2_b + kW, b_1 = w_1 + (int64_t)kFfn * kW, w_2 = b_1 + kFfn, b_2 = w_2 + (int64_t)kW * kFfn;
     hipLaunchKernelGGL(sel_layernorm_kernel, rows, b256, 0, stream, x, wp + ln1_g, wp + ln1_b, hbuf, T);
     gemm(kQkv, hbuf, w_qkv, b_qkv, 3 * kW, kW);
-    hipLaunchKernelGGL(sel_attention_kernel, dim3((unsigned)((T + 127) / 128), kHeads), b256, 0, stream, qk, vt,
-                       Wk.vt_pitch, hbuf, T);
+    {
+      int key_len = 0;
+      const int sp = sel_attn_splits(T, &key_len);
+      float* apart = sp > 1 ? reinterpret_cast<float*>(ws + Wk.attn) : nullptr;
+      hipLaunchKernelGGL(sel_attention_kernel, dim3((unsigned)((T + 127) / 128), kHeads, (unsigned)sp), b256, 0,
+                         stream, qk, vt, Wk.vt_pitch, hbuf, T, key_len, apart);
+      if (sp > 1)
+        hipLaunchKernelGGL(sel_attn_merge_kernel, dim3((unsigned)(((int64_t)T * kHeads * (kDh / 4) + 255) / 256)),
+                           b256, 0, stream, apart, sp, T, hbuf);
+    }
     gemm(kAddF32, hbuf, w_o, b_o, kW, kW);
     hipLaunchKernelGGL(sel_layernorm_kernel, rows, b256, 0, stream, x, wp + ln2_g, wp + ln2_b, hbuf, T);
     gemm(kGeluBf16, hbuf, w_1, b_1, kFfn, kW);
