@@ -19,7 +19,7 @@ import numpy as np
 
 from . import attention as att
 from . import layout, quant
-from .plan import (GROUP, KIVI32, Dims, anchor_of, arena_offsets, block_bytes, layer_bytes, stream_bytes,
+from .plan import (GROUP, GROUP64, KIVI32, Dims, anchor_of, arena_offsets, block_bytes, layer_bytes, stream_bytes,
                    tail_bytes)
 
 F32 = np.float32
@@ -34,6 +34,11 @@ def quantise_blocks(dims: Dims, bits: int, K: np.ndarray, V: np.ndarray) -> dict
         uv, vs, vz = quant.kivi_quantize(V.reshape(nb, 32, D // 32, 32), bits)  # token x 32 ch
         return {"uk": np.swapaxes(uk, 1, 2), "uv": uv.reshape(nb, 32, D),
                 "ks": ks, "kz": kz, "vs": vs, "vz": vz}
+    if dims.qscheme == GROUP64:  # keys and values alike: token x 64 consecutive channels
+        uk, ks, kz = quant.kivi_quantize(K.reshape(nb, 32, D // 64, 64), bits)
+        uv, vs, vz = quant.kivi_quantize(V.reshape(nb, 32, D // 64, 64), bits)
+        return {"uk": uk.reshape(nb, 32, D), "uv": uv.reshape(nb, 32, D),
+                "ks": ks, "kz": kz, "vs": vs, "vz": vz}
     uk, ks = quant.symrow_quantize(K, bits)  # one row = a token's D channels
     uv, vs = quant.symrow_quantize(V, bits)
     return {"uk": uk, "uv": uv, "ks": ks, "vs": vs}
@@ -46,6 +51,12 @@ def dequantise_blocks(dims: Dims, bits: int, f: dict):
     if dims.qscheme == KIVI32:
         kh = quant.kivi_dequantize(f["uk"], f["ks"][:, None, :], f["kz"][:, None, :])
         uv = f["uv"].reshape(nb, 32, D // 32, 32)
+        vh = quant.kivi_dequantize(uv, f["vs"][..., None], f["vz"][..., None]).reshape(nb, 32, D)
+        return kh, vh
+    if dims.qscheme == GROUP64:
+        uk = f["uk"].reshape(nb, 32, D // 64, 64)
+        uv = f["uv"].reshape(nb, 32, D // 64, 64)
+        kh = quant.kivi_dequantize(uk, f["ks"][..., None], f["kz"][..., None]).reshape(nb, 32, D)
         vh = quant.kivi_dequantize(uv, f["vs"][..., None], f["vz"][..., None]).reshape(nb, 32, D)
         return kh, vh
     kh = quant.symrow_dequantize(f["uk"], f["ks"][..., None], bits)

@@ -18,7 +18,7 @@ from functools import lru_cache
 
 import numpy as np
 
-from .plan import GROUP, KIVI32, SYMROW, Dims, block_bytes, stream_bytes, tail_bytes
+from .plan import GROUP, GROUP64, KIVI32, SYMROW, Dims, block_bytes, stream_bytes, tail_bytes
 
 
 def _lanes():
@@ -118,6 +118,33 @@ def kivi_vmeta_index(D: int):
     return idx
 
 
+def g64_kmeta_index(D: int):
+    """GROUP64 K-meta fp16 index for (w, token, group): ((tau*4 + kg)*NG*2 + g*2 + w)*4 + e
+    where token = 16 tau + 4 kg + e and NG = D/64.  Returns int64 [2, 32, NG]."""
+    NG = D // 64
+    idx = np.full((2, 32, NG), -1, dtype=np.int64)
+    for tau in range(2):
+        for kg in range(4):
+            for g in range(NG):
+                for w in range(2):
+                    for e in range(4):
+                        idx[w, 16 * tau + 4 * kg + e, g] = ((tau * 4 + kg) * NG * 2 + g * 2 + w) * 4 + e
+    return idx
+
+
+def g64_vmeta_index(D: int):
+    """GROUP64 V-meta fp16 index for (w, token, group): ((g*2 + w)*4 + kg)*8 + s where
+    token = 16 (s/4) + 4 kg + (s%4), g over the D/64 groups.  Returns int64 [2, 32, D/64]."""
+    idx = np.full((2, 32, D // 64), -1, dtype=np.int64)
+    for g in range(D // 64):
+        for w in range(2):
+            for kg in range(4):
+                for s in range(8):
+                    t = 16 * (s // 4) + 4 * kg + (s % 4)
+                    idx[w, t, g] = ((g * 2 + w) * 4 + kg) * 8 + s
+    return idx
+
+
 def _pack_bits(u: np.ndarray, addr: np.ndarray, bits: int, nbytes: int) -> np.ndarray:
     """Scatter codes u [n, 32, D] to bit addresses addr [32, D] of n regions of
     nbytes bytes each; returns uint8 [n, nbytes]."""
@@ -178,8 +205,9 @@ def unpack_bf16_blocks(raw: np.ndarray, D: int):
 
 def pack_quant_blocks(dims: Dims, bits: int, f: dict) -> np.ndarray:
     """Quantised blocks.  f holds 'uk', 'uv' int [n, 32, D] and, for KIVI32,
-    'ks', 'kz' fp16 [n, D], 'vs', 'vz' fp16 [n, 32, D/32]; for SYMROW, 'ks', 'vs'
-    bf16 bit patterns uint16 [n, 32]."""
+    'ks', 'kz' fp16 [n, D], 'vs', 'vz' fp16 [n, 32, D/32]; for GROUP64, 'ks', 'kz',
+    'vs', 'vz' fp16 [n, 32, D/64]; for SYMROW, 'ks', 'vs' bf16 bit patterns uint16
+    [n, 32]."""
     D = dims.head_dim
     n = f["uk"].shape[0]
     out = np.zeros((n, block_bytes(dims, bits)), dtype=np.uint8)
@@ -195,6 +223,12 @@ def pack_quant_blocks(dims: Dims, bits: int, f: dict) -> np.ndarray:
         vi = kivi_vmeta_index(D)
         _put_u16(out, mb + 4 * D + 2 * vi[0], f["vs"].view(np.uint16))
         _put_u16(out, mb + 4 * D + 2 * vi[1], f["vz"].view(np.uint16))
+    elif dims.qscheme == GROUP64:
+        ki, vi = g64_kmeta_index(D), g64_vmeta_index(D)
+        _put_u16(out, mb + 2 * ki[0], f["ks"].view(np.uint16))
+        _put_u16(out, mb + 2 * ki[1], f["kz"].view(np.uint16))
+        _put_u16(out, mb + 2 * D + 2 * vi[0], f["vs"].view(np.uint16))
+        _put_u16(out, mb + 2 * D + 2 * vi[1], f["vz"].view(np.uint16))
     else:
         t = np.arange(32)
         _put_u16(out, mb + 2 * t, f["ks"])
@@ -216,6 +250,12 @@ def unpack_quant_blocks(dims: Dims, bits: int, raw: np.ndarray) -> dict:
         vi = kivi_vmeta_index(D)
         f["vs"] = _get_u16(raw, mb + 4 * D + 2 * vi[0]).view(np.float16)
         f["vz"] = _get_u16(raw, mb + 4 * D + 2 * vi[1]).view(np.float16)
+    elif dims.qscheme == GROUP64:
+        ki, vi = g64_kmeta_index(D), g64_vmeta_index(D)
+        f["ks"] = _get_u16(raw, mb + 2 * ki[0]).view(np.float16)
+        f["kz"] = _get_u16(raw, mb + 2 * ki[1]).view(np.float16)
+        f["vs"] = _get_u16(raw, mb + 2 * D + 2 * vi[0]).view(np.float16)
+        f["vz"] = _get_u16(raw, mb + 2 * D + 2 * vi[1]).view(np.float16)
     else:
         t = np.arange(32)
         f["ks"] = _get_u16(raw, mb + 2 * t)
@@ -251,7 +291,8 @@ def split_stream(dims: Dims, bits: int, stream: np.ndarray, n_stored: int):
 
 
 __all__ = [
-    "k_slots", "v_slots", "code_bitaddr", "bf16_byteaddr", "kivi_vmeta_index",
+    "k_slots", "v_slots", "code_bitaddr", "bf16_byteaddr", "kivi_vmeta_index", "g64_kmeta_index",
+    "g64_vmeta_index",
     "pack_bf16_blocks", "unpack_bf16_blocks", "pack_quant_blocks", "unpack_quant_blocks",
     "assemble_stream", "split_stream", "SYMROW",
 ]

@@ -18,7 +18,7 @@ from typing import List, Optional, Sequence
 BITS = (2, 4, 8, 16)
 GROUP = 32
 GQA, MLA = 0, 1
-KIVI32, SYMROW = 0, 1
+KIVI32, SYMROW, GROUP64 = 0, 1, 2
 
 
 @dataclass(frozen=True)
@@ -74,6 +74,8 @@ def validate(dims: Dims, plan: Sequence[Action]) -> Optional[str]:
         return "plan length != n_layers"
     if plan[0].inherit:
         return "layer 0 must own a cache"
+    if dims.qscheme == GROUP64 and (dims.kind != GQA or dims.head_dim % 64):
+        return "GROUP64 needs a GQA table with head_dim a multiple of 64"
     for a in plan:
         if a.inherit:
             continue
@@ -183,6 +185,8 @@ def block_bytes(dims: Dims, bits: int, rank: int = 0) -> int:
         return 128 * D
     if dims.qscheme == KIVI32:
         return 8 * D * (bits + 1)
+    if dims.qscheme == GROUP64:
+        return 8 * D * bits + 4 * D  # codes + fp16 (scale, zero) per 64 channels of a token, K and V
     return 8 * D * bits + 128
 
 

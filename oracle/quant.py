@@ -2,7 +2,7 @@
 
 TEST INFRASTRUCTURE ONLY (see oracle/__init__.py).
 
-Two schemes:
+Three schemes:
   * SYMROW — the paper's own quantiser (App. B "Quantization", App. C.3):
     symmetric, one scale per stored vector set by its largest magnitude,
     q = 2^(b-1) - 1, s = max|x| / q, code = clip(round(x / s), -q, q),
@@ -12,6 +12,10 @@ Two schemes:
     scale and a zero point per group, all 2^b levels.  Groups: keys per channel
     over 32 consecutive stored tokens, values per token over 32 consecutive
     channels; scale and zero in fp16.
+  * GROUP64 — the same grouped asymmetric quantiser with per-token groups of 64
+    consecutive channels for keys and values alike (App. C.3's on-device grouped
+    cache: 4 + 32/64 = 4.5 bits per element at 4 bits, 3.56x); kivi_quantize over
+    such groups.
 
 Readings where the paper is silent (each is listed in the design doc): rounding is
 round-half-to-even; the scale is rounded to its storage type before codes are

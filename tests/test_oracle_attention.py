@@ -85,7 +85,7 @@ def test_bf16_layer_recovers_input_exactly(n):
         assert np.allclose(out[0, b], A.gqa_attention(q[0, b], K[b], V[b], 0.125), rtol=1e-13)
 
 
-@pytest.mark.parametrize("qs", [P.KIVI32, P.SYMROW])
+@pytest.mark.parametrize("qs", [P.KIVI32, P.SYMROW, P.GROUP64])
 @pytest.mark.parametrize("bits", [2, 4, 8])
 def test_cache_roundtrip_matches_direct_quantiser(qs, bits):
     """Compress -> bytes -> dequantise equals quantising the groups directly."""
@@ -101,6 +101,12 @@ def test_cache_roundtrip_matches_direct_quantiser(qs, bits):
             u, s, z = Q.kivi_quantize(kb.T, bits)
             assert np.array_equal(Kh[0, 0, 32 * blk:32 * blk + 32], Q.kivi_dequantize(u, s[:, None], z[:, None]).T)
             u, s, z = Q.kivi_quantize(vb.reshape(32, D // 32, 32), bits)
+            ref = Q.kivi_dequantize(u, s[..., None], z[..., None]).reshape(32, D)
+        elif qs == P.GROUP64:
+            u, s, z = Q.kivi_quantize(kb.reshape(32, D // 64, 64), bits)
+            assert np.array_equal(Kh[0, 0, 32 * blk:32 * blk + 32],
+                                  Q.kivi_dequantize(u, s[..., None], z[..., None]).reshape(32, D))
+            u, s, z = Q.kivi_quantize(vb.reshape(32, D // 64, 64), bits)
             ref = Q.kivi_dequantize(u, s[..., None], z[..., None]).reshape(32, D)
         else:
             u, s = Q.symrow_quantize(kb, bits)

@@ -154,7 +154,7 @@ def test_layout_examples_worked_by_hand():
         assert got == int(addr), (D, b, which, t, c)
 
 
-@pytest.mark.parametrize("qs", [P.KIVI32, P.SYMROW])
+@pytest.mark.parametrize("qs", [P.KIVI32, P.SYMROW, P.GROUP64])
 @pytest.mark.parametrize("D", [64, 128])
 @pytest.mark.parametrize("bits", [2, 4, 8])
 def test_pack_unpack_roundtrip_all_codes(qs, D, bits):
@@ -168,6 +168,8 @@ def test_pack_unpack_roundtrip_all_codes(qs, D, bits):
                  kz=rng.standard_normal((n, D)).astype(np.float16),
                  vs=rng.standard_normal((n, 32, D // 32)).astype(np.float16),
                  vz=rng.standard_normal((n, 32, D // 32)).astype(np.float16))
+    elif qs == P.GROUP64:
+        f.update({k: rng.standard_normal((n, 32, D // 64)).astype(np.float16) for k in ("ks", "kz", "vs", "vz")})
     else:
         f.update(ks=rng.integers(0, 2 ** 16, (n, 32)).astype(np.uint16),
                  vs=rng.integers(0, 2 ** 16, (n, 32)).astype(np.uint16))
