@@ -58,8 +58,12 @@ typedef enum { KVK_GQA = 0, KVK_MLA = 1 } kvk_kind;
  *    all 2^b levels.
  *  KVK_Q_SYMROW — the paper's own quantiser (App. B "Quantization", App. C.3):
  *    symmetric, one bf16 scale per 128-element token-head row (per token, per
- *    KV head, separately for K and V), codes in [-q, q] with q = 2^(b-1) - 1. */
-typedef enum { KVK_Q_KIVI32 = 0, KVK_Q_SYMROW = 1 } kvk_qscheme;
+ *    KV head, separately for K and V), codes in [-q, q] with q = 2^(b-1) - 1.
+ *  KVK_Q_GROUP64 — grouped asymmetric per token (App. C.3's on-device grouped
+ *    cache, 4 + 32/64 = 4.5 bits per element at 4 bits): keys and values alike,
+ *    one fp16 (scale, zero) pair per token per 64 consecutive channels.  GQA
+ *    tables only, head_dim a multiple of 64. */
+typedef enum { KVK_Q_KIVI32 = 0, KVK_Q_SYMROW = 1, KVK_Q_GROUP64 = 2 } kvk_qscheme;
 
 typedef enum { KVK_BF16 = 0, KVK_F32 = 1 } kvk_dtype;
 
@@ -170,12 +174,18 @@ typedef struct {
  *              16*(s/4) + 4*kg + (s%4).
  *   SYMROW meta (64 bytes each): K meta bf16 scale[32], V meta bf16 scale[32],
  *      natural token order.
- *   Block bytes: KIVI32 8*D*(b+1); SYMROW 8*D*b + 128.
+ *   GROUP64 meta (2*D bytes each), NG = D/64 channel groups g (channels
+ *      64g..64g+63), w = 0 scale / 1 zero:
+ *      K meta: fp16 at index ((tau*4 + kg)*NG*2 + g*2 + w)*4 + e for token
+ *              16*tau + 4*kg + e (the token order of a lane's score tile);
+ *      V meta: fp16 at index ((g*2 + w)*4 + kg)*8 + s for token
+ *              16*(s/4) + 4*kg + (s%4) (as KIVI32's V meta, over the NG groups).
+ *   Block bytes: KIVI32 8*D*(b+1); SYMROW 8*D*b + 128; GROUP64 8*D*b + 4*D.
  *
  * Codes (unsigned, b bits):
  *   KIVI32 (App. C.3 grouped asymmetric): for a group x_1..x_32 (a channel over a
- *   block's tokens for K, a token over 32 channels for V), in IEEE fp32
- *   arithmetic with round-to-nearest-even:
+ *   block's tokens for K, a token over 32 channels for V; GROUP64: a token over
+ *   64 channels, K and V), in IEEE fp32 arithmetic with round-to-nearest-even:
  *      mn = min x, mx = max x
  *      scale = fp16( (mx - mn) / (2^b - 1) ),  zero = fp16( mn )
  *      u = 0 if scale == 0 else clamp( rint( (x - zero) / scale ), 0, 2^b - 1 )
@@ -458,7 +468,8 @@ kvk_status kvk_debug_dequantize(const kvk_table* table, int32_t layer, int32_t n
 
 /* Storage accounting of App. C.3 (table of storage cost with quantisation
  * metadata): bits per cached element for `bits`-bit codes with 32 bits of
- * metadata per `group` elements (grouped scheme, KVK_Q_KIVI32) or one bf16 scale
+ * metadata per `group` elements (grouped schemes, KVK_Q_KIVI32 and KVK_Q_GROUP64, the
+ * latter with group 64 as stored) or one bf16 scale
  * per 128-element row (KVK_Q_SYMROW, group ignored), with `window` of the
  * `context` tokens kept in bf16.  Returns a negative value on invalid input. */
 double kvk_realized_bits(int32_t qscheme, int32_t bits, int32_t group, int64_t window,

@@ -38,7 +38,7 @@ struct CompressArgs {
   int32_t nb_cap;   // full-block capacity (tail block sits after it)
   int32_t D;
   int32_t bits;
-  int32_t kivi;
+  int32_t qs;       // kvk_qscheme
 };
 
 #pragma clang fp contract(off)
@@ -173,7 +173,7 @@ __device__ __forceinline__ float group_max(float x) {
 
 // Quantise the 32 tokens staged in LDS (Ks, Vs: fp32 rows of LD floats) into one
 // block of BITS-bit codes plus metadata at `out`.  Called by all 256 threads.
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, int QS>
 __device__ __forceinline__ void write_quant_block(const float* Ks, const float* Vs, float* kmeta, float* vmeta,
                                                   uint8_t* out, int tid) {
   constexpr int LD = D + 4;
@@ -181,7 +181,8 @@ __device__ __forceinline__ void write_quant_block(const float* Ks, const float* 
     constexpr float levels = (float)((1 << BITS) - 1);
 
     // ---- group metadata ----
-    if constexpr (KIVI) {
+    constexpr int NG64 = D / 64;  // GROUP64 channel groups
+    if constexpr (QS == kQsKivi) {
       {  // K: channel c over the block's 32 tokens, TPC threads per channel
         constexpr int TPC = 256 / D, TOK = 32 / TPC;
         const int c = tid / TPC, t0 = TOK * (tid % TPC);
@@ -217,6 +218,25 @@ __device__ __forceinline__ void write_quant_block(const float* Ks, const float* 
           vmeta[2 * (t * NG + g)] = (float)(_Float16)((mx - mn) / levels);
           vmeta[2 * (t * NG + g) + 1] = (float)(_Float16)mn;
         }
+      }
+    } else if constexpr (QS == kQsG64) {  // (token, 64 channels) of K then of V, TPG threads per group
+      constexpr int NGR = 2 * 32 * NG64, TPG = 256 / NGR, CH = 64 / TPG;
+      const int pr = tid / TPG, isv = pr >= 32 * NG64, r = pr % (32 * NG64), t = r / NG64, g = r % NG64;
+      const float* row = (isv ? &Vs[t * LD] : &Ks[t * LD]) + 64 * g + CH * (tid % TPG);
+      f4 x = *reinterpret_cast<const f4*>(row);
+      float mn = fminf(fminf(x[0], x[1]), fminf(x[2], x[3])), mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+#pragma unroll
+      for (int c = 4; c < CH; c += 4) {
+        x = *reinterpret_cast<const f4*>(row + c);
+        mn = fminf(mn, fminf(fminf(x[0], x[1]), fminf(x[2], x[3])));
+        mx = fmaxf(mx, fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])));
+      }
+      mn = group_min<TPG>(mn);
+      mx = group_max<TPG>(mx);
+      if (tid % TPG == 0) {
+        float* meta = isv ? vmeta : kmeta;
+        meta[2 * (t * NG64 + g)] = (float)(_Float16)((mx - mn) / levels);
+        meta[2 * (t * NG64 + g) + 1] = (float)(_Float16)mn;
       }
     } else {  // SYMROW: one scale per token row of K (rows 0..31) and V (rows 32..63), 4 threads per row
       constexpr int CH = D / 4;
@@ -271,14 +291,23 @@ __device__ __forceinline__ void write_quant_block(const float* Ks, const float* 
         if (!isv) {
           const int t = 16 * tau + i, c = 32 * x + 8 * kg + sl;
           const float xv = Ks[t * LD + c];
-          if constexpr (KIVI) u = kivi_code(xv, kmeta[c], kmeta[D + c], levels);
-          else u = sym_code(xv, kmeta[t], BITS);
+          if constexpr (QS == kQsKivi) {
+            u = kivi_code(xv, kmeta[c], kmeta[D + c], levels);
+          } else if constexpr (QS == kQsG64) {
+            const int gi = 2 * (t * NG64 + (c >> 6));
+            u = kivi_code(xv, kmeta[gi], kmeta[gi + 1], levels);
+          } else {
+            u = sym_code(xv, kmeta[t], BITS);
+          }
         } else {
           const int c = 16 * x + i, t = 16 * (sl >> 2) + 4 * kg + (sl & 3);
           const float xv = Vs[t * LD + c];
-          if constexpr (KIVI) {
+          if constexpr (QS == kQsKivi) {
             const int g = c >> 5;
             u = kivi_code(xv, vmeta[2 * (t * (D / 32) + g)], vmeta[2 * (t * (D / 32) + g) + 1], levels);
+          } else if constexpr (QS == kQsG64) {
+            const int gi = 2 * (t * NG64 + (c >> 6));
+            u = kivi_code(xv, vmeta[gi], vmeta[gi + 1], levels);
           } else {
             u = sym_code(xv, vmeta[t], BITS);
           }
@@ -290,7 +319,22 @@ __device__ __forceinline__ void write_quant_block(const float* Ks, const float* 
 
     // ---- metadata stores ----
     uint16_t* om = reinterpret_cast<uint16_t*>(out + 2 * cb);
-    if constexpr (KIVI) {
+    if constexpr (QS == kQsG64) {
+      for (int idx = tid; idx < 2 * D; idx += 256) {
+        float val;
+        if (idx < D) {  // K: ((tau*4 + kg)*NG*2 + g*2 + w)*4 + e, token 16 tau + 4 kg + e
+          const int e = idx & 3, w = (idx >> 2) & 1, g = (idx >> 3) % NG64, tk = (idx >> 3) / NG64;
+          const int t = 16 * (tk >> 2) + 4 * (tk & 3) + e;
+          val = kmeta[2 * (t * NG64 + g) + w];
+        } else {  // V: ((g*2 + w)*4 + kg)*8 + s, token 16 (s/4) + 4 kg + (s%4)
+          const int e = idx - D;
+          const int sl = e & 7, kg = (e >> 3) & 3, w = (e >> 5) & 1, g = e >> 6;
+          const int t = 16 * (sl >> 2) + 4 * kg + (sl & 3);
+          val = vmeta[2 * (t * NG64 + g) + w];
+        }
+        om[idx] = bitcast<uint16_t>((_Float16)val);  // exact: the value is an fp16
+      }
+    } else if constexpr (QS == kQsKivi) {
       for (int idx = tid; idx < 4 * D; idx += 256) {
         float val;
         if (idx < 2 * D) {
@@ -311,12 +355,12 @@ __device__ __forceinline__ void write_quant_block(const float* Ks, const float* 
 
 // One workgroup writes one 32-token block of one stream, with BITS-bit codes (or
 // bf16 at BITS = 16; a stream's tail block is always bf16).
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, int QS>
 __global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
   constexpr int LD = D + 4;  // padded LDS row (floats), rows 16-byte aligned
   __shared__ float Ks[32 * LD];
   __shared__ float Vs[32 * LD];
-  __shared__ float kmeta[2 * D];          // KIVI: scale, zero per channel; SYMROW: row scale
+  __shared__ float kmeta[2 * D];          // KIVI32: scale, zero per channel; GROUP64: per (token, group); SYMROW: row scale
   __shared__ float vmeta[2 * 32 * (D / 32)];
 
   const int tid = threadIdx.x;
@@ -336,7 +380,7 @@ __global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
     write_bf16_block<D, LD>(Ks, Vs, out, tid);
     return;
   }
-  if constexpr (BITS != 16) write_quant_block<D, BITS, KIVI>(Ks, Vs, kmeta, vmeta, out, tid);
+  if constexpr (BITS != 16) write_quant_block<D, BITS, QS>(Ks, Vs, kmeta, vmeta, out, tid);
 }
 
 // Decode-time append of one token to every anchor of a layer range.
@@ -382,7 +426,7 @@ __global__ __launch_bounds__(256) void tail_write_kernel(AppendArgs a) {
 // workgroup per (stream, anchor) quantises the tail's bf16 values plus the new
 // token (rounded to bf16) into full block pos / 32, exactly as the prefill write
 // quantises a block.  The tail is then empty (its stale slots are never read).
-template <int D, bool KIVI>
+template <int D, int QS>
 __global__ __launch_bounds__(256) void group_write_kernel(AppendArgs a) {
   constexpr int LD = D + 4;
   __shared__ float Ks[32 * LD];
@@ -404,9 +448,9 @@ __global__ __launch_bounds__(256) void group_write_kernel(AppendArgs a) {
   uint8_t* out = base + (int64_t)(a.pos >> 5) * it.block_bytes;
   switch (it.bits) {
     case 16: write_bf16_block<D, LD>(Ks, Vs, out, tid); break;
-    case 8: write_quant_block<D, 8, KIVI>(Ks, Vs, kmeta, vmeta, out, tid); break;
-    case 4: write_quant_block<D, 4, KIVI>(Ks, Vs, kmeta, vmeta, out, tid); break;
-    default: write_quant_block<D, 2, KIVI>(Ks, Vs, kmeta, vmeta, out, tid); break;
+    case 8: write_quant_block<D, 8, QS>(Ks, Vs, kmeta, vmeta, out, tid); break;
+    case 4: write_quant_block<D, 4, QS>(Ks, Vs, kmeta, vmeta, out, tid); break;
+    default: write_quant_block<D, 2, QS>(Ks, Vs, kmeta, vmeta, out, tid); break;
   }
 }
 
@@ -414,7 +458,7 @@ __global__ __launch_bounds__(256) void group_write_kernel(AppendArgs a) {
 template <int D>
 __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* region, int64_t stream_bytes,
                                                       int64_t block_bytes, int nb_cap, int n_stored,
-                                                      int n_streams, int bits, int kivi, float* kout,
+                                                      int n_streams, int bits, int qs, float* kout,
                                                       float* vout) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t total = (int64_t)n_streams * n_stored * D;
@@ -439,7 +483,13 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* region, int
     const uint32_t uk = (w[kb >> 5] >> (kb & 31)) & mask;
     const uint32_t uv = (w[vb >> 5] >> (vb & 31)) & mask;
     const uint16_t* meta = reinterpret_cast<const uint16_t*>(b + 8LL * D * bits);
-    if (kivi) {
+    if (qs == KVK_Q_GROUP64) {
+      const int g = c >> 6, ng = D / 64;
+      const int ki = (((t >> 4) * 4 + ((t >> 2) & 3)) * ng * 2 + g * 2) * 4 + (t & 3);
+      kv = fmaf((float)uk, f16_bits_to_f32(meta[ki]), f16_bits_to_f32(meta[ki + 4]));
+      vv = fmaf((float)uv, f16_bits_to_f32(meta[D + v_meta_index(t, g, 0)]),
+                f16_bits_to_f32(meta[D + v_meta_index(t, g, 1)]));
+    } else if (qs == KVK_Q_KIVI32) {
       kv = fmaf((float)uk, f16_bits_to_f32(meta[c]), f16_bits_to_f32(meta[D + c]));
       const int g = c >> 5;
       vv = fmaf((float)uv, f16_bits_to_f32(meta[2 * D + v_meta_index(t, g, 0)]),
@@ -507,21 +557,23 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
   a.nb_cap = t->nb_cap;
   a.D = d.head_dim;
   a.bits = t->bits[layer];
-  a.kivi = d.qscheme == KVK_Q_KIVI32;
+  a.qs = d.qscheme;
   const int64_t nstreams = (int64_t)d.batch * d.n_kv_heads;
   const int64_t grid = nstreams * (a.nbf + 1);
   if (grid > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "grid too large");
   const dim3 g3((unsigned)grid), b3(256);
 #define KVK_W1(DD, BB, KK) \
-  if (d.head_dim == DD && a.bits == BB && (BB == 16 || a.kivi == (KK ? 1 : 0))) { \
+  if (d.head_dim == DD && a.bits == BB && (BB == 16 || a.qs == KK)) { \
     hipLaunchKernelGGL((compress_kernel<DD, BB, KK>), g3, b3, 0, stream, a); \
     launched = true; \
   }
   bool launched = false;
-  KVK_W1(128, 16, true) else KVK_W1(128, 8, true) else KVK_W1(128, 4, true) else KVK_W1(128, 2, true)
-  else KVK_W1(128, 8, false) else KVK_W1(128, 4, false) else KVK_W1(128, 2, false)
-  else KVK_W1(64, 16, true) else KVK_W1(64, 8, true) else KVK_W1(64, 4, true) else KVK_W1(64, 2, true)
-  else KVK_W1(64, 8, false) else KVK_W1(64, 4, false) else KVK_W1(64, 2, false)
+  KVK_W1(128, 16, 0) else KVK_W1(128, 8, 0) else KVK_W1(128, 4, 0) else KVK_W1(128, 2, 0)
+  else KVK_W1(128, 8, 1) else KVK_W1(128, 4, 1) else KVK_W1(128, 2, 1)
+  else KVK_W1(128, 8, 2) else KVK_W1(128, 4, 2) else KVK_W1(128, 2, 2)
+  else KVK_W1(64, 16, 0) else KVK_W1(64, 8, 0) else KVK_W1(64, 4, 0) else KVK_W1(64, 2, 0)
+  else KVK_W1(64, 8, 1) else KVK_W1(64, 4, 1) else KVK_W1(64, 2, 1)
+  else KVK_W1(64, 8, 2) else KVK_W1(64, 4, 2) else KVK_W1(64, 2, 2)
 #undef KVK_W1
   if (!launched) return fail(KVK_ERR_UNSUPPORTED, "no write kernel for d_h %d, %d bits", d.head_dim, a.bits);
   hipError_t e = hipGetLastError();
@@ -587,7 +639,7 @@ static kvk_status append_gqa(const kvk_table* t, int32_t l0, int32_t l1, const v
     it.row = l - l0;
   }
   if (n == 0) return KVK_OK;
-  const bool kivi = d.qscheme == KVK_Q_KIVI32;
+  const int qs = d.qscheme;
   const dim3 b3(256);
   if (n_stored % KVK_GROUP != KVK_GROUP - 1) {
     const dim3 g3((unsigned)((a.n_streams * d.head_dim + 255) / 256), (unsigned)n);
@@ -596,11 +648,13 @@ static kvk_status append_gqa(const kvk_table* t, int32_t l0, int32_t l1, const v
   } else {
     const dim3 g3((unsigned)a.n_streams, (unsigned)n);
     if (d.head_dim == 128) {
-      if (kivi) hipLaunchKernelGGL((group_write_kernel<128, true>), g3, b3, 0, stream, a);
-      else hipLaunchKernelGGL((group_write_kernel<128, false>), g3, b3, 0, stream, a);
+      if (qs == KVK_Q_KIVI32) hipLaunchKernelGGL((group_write_kernel<128, kQsKivi>), g3, b3, 0, stream, a);
+      else if (qs == KVK_Q_GROUP64) hipLaunchKernelGGL((group_write_kernel<128, kQsG64>), g3, b3, 0, stream, a);
+      else hipLaunchKernelGGL((group_write_kernel<128, kQsSym>), g3, b3, 0, stream, a);
     } else {
-      if (kivi) hipLaunchKernelGGL((group_write_kernel<64, true>), g3, b3, 0, stream, a);
-      else hipLaunchKernelGGL((group_write_kernel<64, false>), g3, b3, 0, stream, a);
+      if (qs == KVK_Q_KIVI32) hipLaunchKernelGGL((group_write_kernel<64, kQsKivi>), g3, b3, 0, stream, a);
+      else if (qs == KVK_Q_GROUP64) hipLaunchKernelGGL((group_write_kernel<64, kQsG64>), g3, b3, 0, stream, a);
+      else hipLaunchKernelGGL((group_write_kernel<64, kQsSym>), g3, b3, 0, stream, a);
     }
   }
   const hipError_t e = hipGetLastError();
@@ -635,15 +689,15 @@ extern "C" kvk_status kvk_debug_dequantize(const kvk_table* t, int32_t layer, in
   const int64_t total = (int64_t)nstreams * n_stored * d.head_dim;
   const int64_t grid = (total + 255) / 256;
   if (grid > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "grid too large");
-  const int kivi = d.qscheme == KVK_Q_KIVI32;
+  const int qs = d.qscheme;
   if (d.head_dim == 128)
     hipLaunchKernelGGL(dequant_kernel<128>, dim3((unsigned)grid), dim3(256), 0, stream, region,
                        t->info.stream_bytes[a], t->block_bytes[a], t->nb_cap, n_stored, nstreams,
-                       t->bits[a], kivi, k_out, v_out);
+                       t->bits[a], qs, k_out, v_out);
   else
     hipLaunchKernelGGL(dequant_kernel<64>, dim3((unsigned)grid), dim3(256), 0, stream, region,
                        t->info.stream_bytes[a], t->block_bytes[a], t->nb_cap, n_stored, nstreams,
-                       t->bits[a], kivi, k_out, v_out);
+                       t->bits[a], qs, k_out, v_out);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "dequantise launch: %s", hipGetErrorString(e));
   return KVK_OK;

@@ -122,11 +122,11 @@ __device__ __forceinline__ bf16x8 to_bf16x8(const float* x) {
 // Per-lane raw bytes of one 32-token block, loaded ahead of use.
 // ---------------------------------------------------------------------------
 
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, int QS>
 struct Raw {
   static constexpr int KB = BITS == 16 ? D / 2 : D * BITS / 32;  // bytes per lane per K tile
   static constexpr int VB = BITS == 16 ? D : D * BITS / 16;      // bytes per lane of V
-  static constexpr int MB = BITS == 16 ? 0 : (KIVI ? D / 8 : 32);  // metadata bytes per lane
+  static constexpr int MB = BITS == 16 ? 0 : (QS == kQsKivi ? D / 8 : (QS == kQsG64 ? D / 16 : 32));  // metadata bytes per lane
   uint32_t k[2][KB / 4];
   uint32_t v[VB / 4];
   uint32_t m[MB > 0 ? MB / 4 : 1];
@@ -180,29 +180,30 @@ __device__ __forceinline__ void load_share(Rsrc rs, int lane, int soff, uint32_t
 // Loads of the block at byte offset `blk` (wave-uniform) of the stream (block
 // layout of include/kvk.h), in the parts that are consumed at different times:
 // key codes (score phase), value codes (value phase), metadata.
-template <int D, int BITS, bool KIVI, int POL>
-__device__ __forceinline__ void load_k(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane) {
-  using R = Raw<D, BITS, KIVI>;
+template <int D, int BITS, int QS, int POL>
+__device__ __forceinline__ void load_k(Raw<D, BITS, QS>& r, Rsrc rs, int blk, int lane) {
+  using R = Raw<D, BITS, QS>;
   constexpr int tile = BITS == 16 ? 32 * D : 2 * D * BITS;
 #pragma unroll
   for (int tau = 0; tau < 2; ++tau) load_share<R::KB / 4, POL>(rs, lane, blk + tau * tile, r.k[tau]);
 }
 
-template <int D, int BITS, bool KIVI, int POL>
-__device__ __forceinline__ void load_v(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane) {
-  using R = Raw<D, BITS, KIVI>;
+template <int D, int BITS, int QS, int POL>
+__device__ __forceinline__ void load_v(Raw<D, BITS, QS>& r, Rsrc rs, int blk, int lane) {
+  using R = Raw<D, BITS, QS>;
   constexpr int vbase = BITS == 16 ? 64 * D : 4 * D * BITS;
   load_share<R::VB / 4, POL>(rs, lane, blk + vbase, r.v);
 }
 
-// KIVI32: the lane's share of the 8D-byte metadata area.  SYMROW: part 0 the K
-// row scales (m[0..3]), part 1 the V row scales (m[4..7]) of the lane's tokens.
-template <int D, int BITS, bool KIVI, int POL>
-__device__ __forceinline__ void load_m(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane, int part) {
-  using R = Raw<D, BITS, KIVI>;
+// KIVI32 / GROUP64: the lane's share of the 8D- / 4D-byte metadata area.  SYMROW:
+// part 0 the K row scales (m[0..3]), part 1 the V row scales (m[4..7]) of the
+// lane's tokens.
+template <int D, int BITS, int QS, int POL>
+__device__ __forceinline__ void load_m(Raw<D, BITS, QS>& r, Rsrc rs, int blk, int lane, int part) {
+  using R = Raw<D, BITS, QS>;
   if constexpr (BITS != 16) {
     const int meta = blk + 8 * D * BITS;
-    if constexpr (KIVI) {
+    if constexpr (QS != kQsSym) {
       load_share<R::MB / 4, POL>(rs, lane, meta, r.m);
     } else {
       const int kg = lane >> 4;
@@ -213,12 +214,12 @@ __device__ __forceinline__ void load_m(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, 
   }
 }
 
-template <int D, int BITS, bool KIVI, int POL>
-__device__ __forceinline__ void load_raw(Raw<D, BITS, KIVI>& r, Rsrc rs, int blk, int lane) {
-  load_k<D, BITS, KIVI, POL>(r, rs, blk, lane);
-  load_v<D, BITS, KIVI, POL>(r, rs, blk, lane);
-  load_m<D, BITS, KIVI, POL>(r, rs, blk, lane, 0);
-  if constexpr (!KIVI) load_m<D, BITS, KIVI, POL>(r, rs, blk, lane, 1);
+template <int D, int BITS, int QS, int POL>
+__device__ __forceinline__ void load_raw(Raw<D, BITS, QS>& r, Rsrc rs, int blk, int lane) {
+  load_k<D, BITS, QS, POL>(r, rs, blk, lane);
+  load_v<D, BITS, QS, POL>(r, rs, blk, lane);
+  load_m<D, BITS, QS, POL>(r, rs, blk, lane, 0);
+  if constexpr (QS == kQsSym) load_m<D, BITS, QS, POL>(r, rs, blk, lane, 1);
 }
 
 // Unpack the 8 codes (one MFMA k-step) of chunk x from a lane's code words.
@@ -247,7 +248,8 @@ struct State {
   float l;                           // lane-partial running sum
 };
 
-// Extra accumulators rescaled with the output: KIVI32's value zero-point sums.
+// Extra accumulators rescaled with the output: the value zero-point sums of the
+// grouped schemes (one per channel group).
 template <int N>
 struct Extra {
   f4 zo[N];
@@ -291,9 +293,9 @@ __device__ __forceinline__ half8 to_half8(const float (&x)[8]) {
 // Each compute_* function consumes ring entry `r` and, with RELOAD, refills each
 // part of it from the block at byte offset `next` as soon as that part has been
 // read, so that the registers stay in flight for as long as possible.
-template <int D, bool K, bool RELOAD, int POL>
+template <int D, int QS, bool RELOAD, int POL>
 __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D / 32],
-                                             const bf16x8 (&qbl)[D / 32], Raw<D, 16, K>& r, Rsrc rs,
+                                             const bf16x8 (&qbl)[D / 32], Raw<D, 16, QS>& r, Rsrc rs,
                                              int next, bool valid, int lane) {
   constexpr int NJ = D / 32, NM = D / 16;
   const int kg = lane >> 4;
@@ -313,7 +315,7 @@ __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D 
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);  // the refill may not rise above the reads it replaces
-    load_k<D, 16, K, POL>(r, rs, next, lane);
+    load_k<D, 16, QS, POL>(r, rs, next, lane);
   }
   Extra<0> none;
   softmax_update<D, 0>(u, none, x);
@@ -333,7 +335,7 @@ __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D 
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_v<D, 16, K, POL>(r, rs, next, lane);
+    load_v<D, 16, QS, POL>(r, rs, next, lane);
   }
 }
 
@@ -342,16 +344,16 @@ __device__ __forceinline__ void compute_bf16(State<D>& u, const bf16x8 (&qbh)[D 
 // broadcast.
 template <int D, int BITS, bool RELOAD, int POL>
 __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, const half8 (&qh)[D / 32],
-                                             const half8 (&ql)[D / 32], Raw<D, BITS, true>& r, Rsrc rs,
+                                             const half8 (&ql)[D / 32], Raw<D, BITS, kQsKivi>& r, Rsrc rs,
                                              int next, bool valid, uint32_t* lds, int lane) {
-  using R = Raw<D, BITS, true>;
+  using R = Raw<D, BITS, kQsKivi>;
   constexpr int NJ = D / 32, NG = D / 32;
   const int kg = lane >> 4;
 #pragma unroll
   for (int i = 0; i < R::MB / 4; ++i) lds[lane * (R::MB / 4) + i] = r.m[i];
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_m<D, BITS, true, POL>(r, rs, next, lane, 0);
+    load_m<D, BITS, kQsKivi, POL>(r, rs, next, lane, 0);
   }
   const half8* kmeta = reinterpret_cast<const half8*>(lds);  // scale[D], zero[D], V meta[2D]
   // K: S = sum_c (q_c s_c) u_c + sum_c q_c z_c.  q' = q s as fp16 hi + lo (error-free
@@ -377,7 +379,7 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_k<D, BITS, true, POL>(r, rs, next, lane);
+    load_k<D, BITS, kQsKivi, POL>(r, rs, next, lane);
   }
   float x[8];
 #pragma unroll
@@ -417,14 +419,14 @@ __device__ __forceinline__ void compute_kivi(State<D>& u, Extra<D / 32>& ex, con
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_v<D, BITS, true, POL>(r, rs, next, lane);
+    load_v<D, BITS, kQsKivi, POL>(r, rs, next, lane);
   }
 }
 
 // SYMROW block: per-token scales factor out of both contractions.
 template <int D, int BITS, bool RELOAD, int POL>
 __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D / 32],
-                                               const half8 (&ql)[D / 32], Raw<D, BITS, false>& r,
+                                               const half8 (&ql)[D / 32], Raw<D, BITS, kQsSym>& r,
                                                Rsrc rs, int next, bool valid, int lane) {
   constexpr int NJ = D / 32, NM = D / 16;
   const float off = (float)(1 << (BITS - 1));
@@ -446,8 +448,8 @@ __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D 
   }
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_k<D, BITS, false, POL>(r, rs, next, lane);
-    load_m<D, BITS, false, POL>(r, rs, next, lane, 0);
+    load_k<D, BITS, kQsSym, POL>(r, rs, next, lane);
+    load_m<D, BITS, kQsSym, POL>(r, rs, next, lane, 0);
   }
   Extra<0> none;
   softmax_update<D, 0>(u, none, x);
@@ -463,13 +465,100 @@ __device__ __forceinline__ void compute_symrow(State<D>& u, const half8 (&qh)[D 
   const half8 p = to_half8(ps);
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_m<D, BITS, false, POL>(r, rs, next, lane, 1);
+    load_m<D, BITS, kQsSym, POL>(r, rs, next, lane, 1);
   }
 #pragma unroll
   for (int mt = 0; mt < NM; ++mt) u.o[mt] = mfma16(unpack_chunk<BITS>(r.v, mt, off), p, u.o[mt]);
   if constexpr (RELOAD) {
     __builtin_amdgcn_sched_barrier(0);
-    load_v<D, BITS, false, POL>(r, rs, next, lane);
+    load_v<D, BITS, kQsSym, POL>(r, rs, next, lane);
+  }
+}
+
+// GROUP64 block: per (token, 64-channel group) scale and zero for keys and values.
+// The metadata goes through the wave's LDS slot as for KIVI32.  Keys: the codes
+// enter the products raw, one accumulator per channel group, and
+//   S_t = sum_g s_tg (sum_{c in g} q_c u_tc) + z_tg Q_g,   Q_g = sum_{c in g} q_c
+// (Q_g per query row, computed once per unit).  Values: as KIVI32's, with groups of
+// 64 channels (four channel tiles per group).
+template <int D, int BITS, bool RELOAD, int POL>
+__device__ __forceinline__ void compute_g64(State<D>& u, Extra<D / 64>& ex, const half8 (&qh)[D / 32],
+                                            const half8 (&ql)[D / 32], const float (&qsum)[D / 64],
+                                            Raw<D, BITS, kQsG64>& r, Rsrc rs, int next, bool valid, uint32_t* lds,
+                                            int lane) {
+  using R = Raw<D, BITS, kQsG64>;
+  constexpr int NJ = D / 32, NG = D / 64;
+  const int kg = lane >> 4;
+#pragma unroll
+  for (int i = 0; i < R::MB / 4; ++i) lds[lane * (R::MB / 4) + i] = r.m[i];
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_m<D, BITS, kQsG64, POL>(r, rs, next, lane, 0);
+  }
+  const _Float16* meta = reinterpret_cast<const _Float16*>(lds);  // K meta [D halves], V meta [D halves]
+  f4 acc[2][NG];
+#pragma unroll
+  for (int tau = 0; tau < 2; ++tau)
+#pragma unroll
+    for (int g = 0; g < NG; ++g) acc[tau][g] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+#pragma unroll
+    for (int tau = 0; tau < 2; ++tau) {
+      const half8 kop = unpack_chunk<BITS>(r.k[tau], j, 0.0f);
+      acc[tau][j / 2] = mfma16(kop, qh[j], acc[tau][j / 2]);
+      acc[tau][j / 2] = mfma16(kop, ql[j], acc[tau][j / 2]);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // keep one k-step's operands live at a time
+  }
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_k<D, BITS, kQsG64, POL>(r, rs, next, lane);
+  }
+  float x[8];
+#pragma unroll
+  for (int tau = 0; tau < 2; ++tau) {
+    float sc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      // scales then zeros of tokens 16 tau + 4 kg + e, e = 0..3
+      const half8 sz = *reinterpret_cast<const half8*>(meta + ((tau * 4 + kg) * NG * 2 + g * 2) * 4);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sc[e] += (float)sz[e] * acc[tau][g][e] + (float)sz[4 + e] * qsum[g];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) x[4 * tau + e] = valid ? sc[e] : -INFINITY;
+  }
+  softmax_update<D, NG>(u, ex, x);
+  const half8 p = to_half8(x);
+  // V: o_c = sum_t (p_t s_tg) u_tc + sum_t p_t z_tg, g = c / 64 (raw codes at 2 and 4
+  // bits as for KIVI32).
+  const half8* vmeta = reinterpret_cast<const half8*>(meta + D);
+  const half8 pc = BITS == 8 ? p : p * raw_factors<BITS>();
+  const _Float16 m1024 = (_Float16)-1024.0f;
+  const half8 neg = {m1024, m1024, m1024, m1024, m1024, m1024, m1024, m1024};
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const half8 vs = vmeta[(g * 2 + 0) * 4 + kg];
+    const half8 vz = vmeta[(g * 2 + 1) * 4 + kg];
+    const half8 ps = pc * vs;
+    ex.zo[g] = mfma16(vz, p, ex.zo[g]);
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const int mt = 4 * g + h;
+      if constexpr (BITS == 8) {
+        u.o[mt] = mfma16(unpack_chunk<BITS>(r.v, mt, 0.0f), ps, u.o[mt]);
+      } else {
+        const uint32_t w0 = BITS == 4 ? r.v[mt] : r.v[mt >> 1] >> (8 * (mt & 1));
+        u.o[mt] = mfma16(neg, ps, u.o[mt]);
+        u.o[mt] = mfma16(raw_codes<BITS>(w0, 0u), ps, u.o[mt]);
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  if constexpr (RELOAD) {
+    __builtin_amdgcn_sched_barrier(0);
+    load_v<D, BITS, kQsG64, POL>(r, rs, next, lane);
   }
 }
 
@@ -543,12 +632,12 @@ __device__ __forceinline__ void load_query(const DecodeArgs& a, const DecodeItem
 // split partial (o[D], m, l) of every valid row.  Everything the unit keeps in
 // registers is local to this function, so that each precision gets its own
 // register allocation.
-template <int D, int BITS, bool KIVI, int POL>
+template <int D, int BITS, int QS, int POL>
 __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& it, int sidx, int split,
                                          int chunk, uint32_t* lds, int lane) {
   constexpr int NR = ring_depth<BITS>();
   constexpr int NM = D / 16;
-  constexpr int NX = (KIVI && BITS != 16) ? D / 32 : 0;
+  constexpr int NX = BITS == 16 ? 0 : (QS == kQsKivi ? D / 32 : (QS == kQsG64 ? D / 64 : 0));
   const int b = it.b0 + sidx / a.Hkv, kvh = sidx % a.Hkv;  // sidx: the item's own stream index
   const int i16 = lane & 15, kg = lane >> 4;
   const int row = 16 * chunk + i16;
@@ -565,14 +654,23 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
   for (int g = 0; g < NX; ++g) ex.zo[g] = f4{0.f, 0.f, 0.f, 0.f};
   const int bb = it.block_bytes;
   const Rsrc rs = stream_rsrc(stream, k1 * bb);  // loads past block k1-1 read zeros
-  Raw<D, BITS, KIVI> ring[NR];
+  Raw<D, BITS, QS> ring[NR];
 #pragma unroll
-  for (int i = 0; i < NR; ++i) load_raw<D, BITS, KIVI, POL>(ring[i], rs, (k0 + i) * bb, lane);
+  for (int i = 0; i < NR; ++i) load_raw<D, BITS, QS, POL>(ring[i], rs, (k0 + i) * bb, lane);
   // The query is issued after the ring so that both are waited for together.
   half8 qh[D / 32], ql[D / 32];
   load_query<D>(a, it, row, b, kvh, kg, qh, ql);
   bf16x8 qbh[D / 32], qbl[D / 32];
   if constexpr (BITS == 16) split_bf16<D>(qh, ql, qbh, qbl);
+  float qsum[D / 64] = {};  // GROUP64: the row's query sum over each 64-channel group
+  if constexpr (QS == kQsG64 && BITS != 16) {
+#pragma unroll
+    for (int j = 0; j < D / 32; ++j)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) qsum[j / 2] += (float)qh[j][e] + (float)ql[j][e];
+#pragma unroll
+    for (int g = 0; g < D / 64; ++g) qsum[g] = wave_sum_kg(qsum[g]);
+  }
 
   // Every reload is unconditional: ring entries past block k1-1 read zeros, and the
   // blocks they stand for (only in a stream's last split, since splits are a
@@ -582,8 +680,10 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
     for (int i = 0; i < NR; ++i) {
       const int next = (k + i + NR) * bb;
       const bool valid = k + i < k1;
-      if constexpr (BITS == 16) compute_bf16<D, KIVI, true, POL>(u, qbh, qbl, ring[i], rs, next, valid, lane);
-      else if constexpr (KIVI) compute_kivi<D, BITS, true, POL>(u, ex, qh, ql, ring[i], rs, next, valid, lds, lane);
+      if constexpr (BITS == 16) compute_bf16<D, QS, true, POL>(u, qbh, qbl, ring[i], rs, next, valid, lane);
+      else if constexpr (QS == kQsKivi) compute_kivi<D, BITS, true, POL>(u, ex, qh, ql, ring[i], rs, next, valid, lds, lane);
+      else if constexpr (QS == kQsG64)
+        compute_g64<D, BITS, true, POL>(u, ex, qh, ql, qsum, ring[i], rs, next, valid, lds, lane);
       else compute_symrow<D, BITS, true, POL>(u, qh, ql, ring[i], rs, next, valid, lane);
     }
   }
@@ -596,7 +696,7 @@ __device__ __forceinline__ void run_unit(const DecodeArgs& a, const DecodeItem& 
 #pragma unroll
     for (int mt = 0; mt < NM; ++mt) {
       f4 o = u.o[mt];
-      if constexpr (NX > 0) o += ex.zo[mt / 2];  // value zero-point sums of the channel group
+      if constexpr (NX > 0) o += ex.zo[mt / (NM / NX)];  // value zero-point sums of the channel group
       *reinterpret_cast<f4*>(pr + 16 * mt + 4 * kg) = o;
     }
     if (kg == 0) {
@@ -612,9 +712,9 @@ __device__ __forceinline__ const DecodeItem& item_at(const DecodeArgs& a, int i)
   else return a.items[i];
 }
 
-template <int D, bool KIVI, bool BATCHED>
+template <int D, int QS, bool BATCHED>
 __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
-  __shared__ uint32_t lds_meta[4][2 * D];  // per-wave KIVI32 metadata slot (8D bytes)
+  __shared__ uint32_t lds_meta[4][2 * D];  // per-wave metadata slot (KIVI32 8D bytes, GROUP64 4D)
   const int lane = threadIdx.x & 63;
   // Wave-uniform by construction; readfirstlane lets the compiler keep everything
   // derived from it (work item, stream address, buffer resource) in scalar registers.
@@ -639,17 +739,17 @@ __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
   // by several row chunks read it through the caches (the later reads hit).
   if (it.nchp == 1) {
     switch (it.bits) {
-      case 16: run_unit<D, 16, KIVI, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
-      case 8: run_unit<D, 8, KIVI, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
-      case 4: run_unit<D, 4, KIVI, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
-      default: run_unit<D, 2, KIVI, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
+      case 16: run_unit<D, 16, QS, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
+      case 8: run_unit<D, 8, QS, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
+      case 4: run_unit<D, 4, QS, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
+      default: run_unit<D, 2, QS, kStreamPolicy>(a, it, sidx, split, chunk, lds, lane); break;
     }
   } else {
     switch (it.bits) {
-      case 16: run_unit<D, 16, KIVI, 0>(a, it, sidx, split, chunk, lds, lane); break;
-      case 8: run_unit<D, 8, KIVI, 0>(a, it, sidx, split, chunk, lds, lane); break;
-      case 4: run_unit<D, 4, KIVI, 0>(a, it, sidx, split, chunk, lds, lane); break;
-      default: run_unit<D, 2, KIVI, 0>(a, it, sidx, split, chunk, lds, lane); break;
+      case 16: run_unit<D, 16, QS, 0>(a, it, sidx, split, chunk, lds, lane); break;
+      case 8: run_unit<D, 8, QS, 0>(a, it, sidx, split, chunk, lds, lane); break;
+      case 4: run_unit<D, 4, QS, 0>(a, it, sidx, split, chunk, lds, lane); break;
+      default: run_unit<D, 2, QS, 0>(a, it, sidx, split, chunk, lds, lane); break;
     }
   }
 }
@@ -757,7 +857,7 @@ namespace {
 struct DecodePlan {
   DecodeArgs d1;
   CombineArgs c1;
-  int kivi;
+  int qs;
   int head_dim;
   bool any_blocks;
   bool batched;
@@ -961,7 +1061,7 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
     ca.citems = reinterpret_cast<const CombItem*>(wsb + LL.citems);
     ca.map = reinterpret_cast<const int32_t*>(wsb + LL.map);
   }
-  P.kivi = d.qscheme == KVK_Q_KIVI32;
+  P.qs = d.qscheme;
   P.head_dim = D;
   P.any_blocks = nbf > 0 && waves > 0;
   return KVK_OK;
@@ -976,11 +1076,13 @@ kvk_status launch_d1(const DecodePlan& P, hipStream_t st) {
   const unsigned grid = (unsigned)((P.d1.total_waves + 3) / 4);
 #define KVK_D1(DD, KK, BB) hipLaunchKernelGGL((gqa_decode_kernel<DD, KK, BB>), dim3(grid), dim3(256), 0, st, P.d1)
   if (P.head_dim == 128) {
-    if (P.kivi) { if (P.batched) KVK_D1(128, true, true); else KVK_D1(128, true, false); }
-    else { if (P.batched) KVK_D1(128, false, true); else KVK_D1(128, false, false); }
+    if (P.qs == KVK_Q_KIVI32) { if (P.batched) KVK_D1(128, kQsKivi, true); else KVK_D1(128, kQsKivi, false); }
+    else if (P.qs == KVK_Q_GROUP64) { if (P.batched) KVK_D1(128, kQsG64, true); else KVK_D1(128, kQsG64, false); }
+    else { if (P.batched) KVK_D1(128, kQsSym, true); else KVK_D1(128, kQsSym, false); }
   } else {
-    if (P.kivi) { if (P.batched) KVK_D1(64, true, true); else KVK_D1(64, true, false); }
-    else { if (P.batched) KVK_D1(64, false, true); else KVK_D1(64, false, false); }
+    if (P.qs == KVK_Q_KIVI32) { if (P.batched) KVK_D1(64, kQsKivi, true); else KVK_D1(64, kQsKivi, false); }
+    else if (P.qs == KVK_Q_GROUP64) { if (P.batched) KVK_D1(64, kQsG64, true); else KVK_D1(64, kQsG64, false); }
+    else { if (P.batched) KVK_D1(64, kQsSym, true); else KVK_D1(64, kQsSym, false); }
   }
 #undef KVK_D1
   hipError_t e = hipGetLastError();

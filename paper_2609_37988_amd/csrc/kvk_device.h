@@ -8,6 +8,9 @@
 
 namespace kvkd {
 
+// Quantiser schemes (the values of kvk_qscheme), as template parameters.
+constexpr int kQsKivi = 0, kQsSym = 1, kQsG64 = 2;
+
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));

@@ -39,6 +39,7 @@ int64_t gqa_block_bytes(int32_t head_dim, int32_t bits, int32_t qscheme) {
   const int64_t D = head_dim;
   if (bits == 16) return 128 * D;                 // bf16 K and V, 32 tokens
   if (qscheme == KVK_Q_KIVI32) return 8 * D * (bits + 1);  // codes + fp16 (scale, zero)
+  if (qscheme == KVK_Q_GROUP64) return 8 * D * bits + 4 * D;  // codes + fp16 (scale, zero) per 64 ch, K and V
   return 8 * D * bits + 128;                      // codes + bf16 row scales
 }
 
@@ -191,8 +192,10 @@ extern "C" kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* pl
     if (d.head_dim != 64 && d.head_dim != 128)
       return fail(KVK_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", d.head_dim);
   }
-  if (d.qscheme != KVK_Q_KIVI32 && d.qscheme != KVK_Q_SYMROW)
+  if (d.qscheme != KVK_Q_KIVI32 && d.qscheme != KVK_Q_SYMROW && d.qscheme != KVK_Q_GROUP64)
     return fail(KVK_ERR_INVALID, "qscheme %d unknown", d.qscheme);
+  if (d.qscheme == KVK_Q_GROUP64 && d.kind != KVK_GQA)
+    return fail(KVK_ERR_UNSUPPORTED, "GROUP64 is built for GQA tables only");
   if (d.batch < 1 || d.max_tokens < 1)
     return fail(KVK_ERR_INVALID, "batch %d and max_tokens %d must be >= 1", d.batch, d.max_tokens);
   if (d.keep_tokens < 0 || d.keep_tokens > d.max_tokens)
@@ -411,7 +414,7 @@ extern "C" double kvk_realized_bits(int32_t qscheme, int32_t bits, int32_t group
   double per;
   if (qscheme == KVK_Q_SYMROW) {
     per = bits + 16.0 / 128.0;  // one bf16 scale per 128-element token-head row
-  } else if (qscheme == KVK_Q_KIVI32) {
+  } else if (qscheme == KVK_Q_KIVI32 || qscheme == KVK_Q_GROUP64) {
     if (group <= 0) return -1.0;
     per = bits + 32.0 / group;  // fp16 scale + fp16 zero per group
   } else {

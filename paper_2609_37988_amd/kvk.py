@@ -19,7 +19,7 @@ MAX_LAYERS = 64
 
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_DEVICE, ERR_BUFFER = 0, -1, -2, -3, -4
 GQA, MLA = 0, 1
-KIVI32, SYMROW = 0, 1
+KIVI32, SYMROW, GROUP64 = 0, 1, 2
 BF16, F32 = 0, 1
 
 

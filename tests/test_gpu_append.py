@@ -67,7 +67,7 @@ def _gqa_append_case(qs, bits_a, bits_b, D, dtype, n0, n1, seed):
     return case, streams
 
 
-@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW], ids=["kivi32", "symrow"])
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW, kvk.GROUP64], ids=["kivi32", "symrow", "group64"])
 @pytest.mark.parametrize("bits_a,bits_b", [(16, 2), (8, 4), (4, 16), (2, 8)])
 def test_gqa_append_matches_oracle_and_decodes(qs, bits_a, bits_b):
     """29 prefilled tokens, 70 appends (group boundaries at 32, 64 and 96), d_h 128."""

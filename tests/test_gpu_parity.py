@@ -68,7 +68,7 @@ def test_tiny_int8_workload():
     assert rel_err(out, ref) <= TOL
 
 
-@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW], ids=["kivi32", "symrow"])
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW, kvk.GROUP64], ids=["kivi32", "symrow", "group64"])
 @pytest.mark.parametrize("bits", [2, 4, 8, 16])
 @pytest.mark.parametrize("D", [64, 128])
 def test_single_layer_ragged(qs, bits, D):
@@ -100,7 +100,7 @@ def _stack_case(qs=kvk.KIVI32):
     return c, inputs, n
 
 
-@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW], ids=["kivi32", "symrow"])
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW, kvk.GROUP64], ids=["kivi32", "symrow", "group64"])
 def test_depth_stacking_and_invariants(qs):
     say(f"case depth-stacking qs={qs}")
     c, inputs, n = _stack_case(qs)

@@ -40,7 +40,7 @@ def _table_for(w):
 
 
 @pytest.mark.parametrize("cfg", [0, 1, 2, 4])
-@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW])
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW, kvk.GROUP64])
 def test_table_matches_oracle_accounting(cfg, qs):
     w = synth.workload(cfg)
     w.qscheme = qs
@@ -290,6 +290,8 @@ def test_mla_invalid_plans_and_dims():
     _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(nope=100), ok)
     _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(r=1024), kvk.make_plan([(0, 4, 1024), (1, 16, 0)]))
     kvk.layer_table(dims(r=1024), kvk.make_plan([(0, 4, 512), (0, 2, 128)]))
+    g64 = kvk.make_dims(kvk.MLA, 2, 32, 4, 128, 512, 64, 128, 128, qscheme=kvk.GROUP64, batch=1, max_tokens=64)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, g64, ok)  # the per-token 64-channel scheme is GQA-only
 
 
 def test_mla_entry_points_reject_bad_arguments_without_launching():
