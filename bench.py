@@ -44,7 +44,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=4)
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--variant", default=None)
-    ap.add_argument("--qscheme", default="kivi32", choices=["kivi32", "symrow"])
+    ap.add_argument("--qscheme", default="kivi32", choices=["kivi32", "symrow", "group64"],
+                    help="quantiser of the quantised layers (group64: GQA workloads only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--per-sequence", action="store_true",
                     help="workload 2 with a plan per sequence (each drawn like the shared one)")
@@ -61,6 +62,7 @@ def parse():
 # per workload, with the sources that determine that kernel and its launch shape.
 GQA_SOURCES = ["table.cpp", "decode.hip", "kvk_device.h", "kvk_internal.h"]
 MLA_SOURCES = ["table.cpp", "mla.hip", "kvk_device.h", "kvk_internal.h"]
+QS_NAMES = {0: "KIVI32", 1: "SYMROW", 2: "GROUP64"}
 TRAFFIC = {
     (2, None): ("gqa_decode_14b_mixed_traffic.json", GQA_SOURCES),
     (3, None): ("mla_decode_32l_bf16_traffic.json", MLA_SOURCES),
@@ -130,11 +132,11 @@ def kernel_source_hash(sources=GQA_SOURCES) -> str:
     return h.hexdigest()
 
 
-def recorded_traffic(config: int, variant=None):
+def recorded_traffic(config: int, variant=None, qscheme="kivi32"):
     """HBM bytes per launch of the roofline kernel from the committed counter record,
-    or None when there is no record for this workload or it was taken on different
-    kernel sources."""
-    if (config, variant) not in TRAFFIC:
+    or None when there is no record for this workload and quantiser (the records are
+    KIVI32's) or it was taken on different kernel sources."""
+    if qscheme != "kivi32" or (config, variant) not in TRAFFIC:
         return None
     name, sources = TRAFFIC[(config, variant)]
     try:
@@ -271,6 +273,9 @@ def run_mla(args):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     w = synth.mla_workload(args.variant)
+    if args.qscheme == "group64":
+        print("bench.py: the GROUP64 quantiser is built for GQA tables only", file=sys.stderr)
+        sys.exit(2)
     if args.qscheme == "symrow":
         w.qscheme = kvk.SYMROW
     n_tok = w.tokens
@@ -357,7 +362,7 @@ def run_mla(args):
         "config": {
             "workload": w.name, "layers": w.n_layers, "q_heads": w.n_q_heads, "latent_dim": w.latent_dim,
             "rope_dim": w.rope_dim, "batch": w.batch, "context": n_tok, "stored_tokens": n_stored,
-            "qscheme": "KIVI32" if w.qscheme == kvk.KIVI32 else "SYMROW", "anchors_by_rank": ranks,
+            "qscheme": QS_NAMES[w.qscheme], "anchors_by_rank": ranks,
             "bits": w.plan[0][1], "rho_eq2": round(info.rho, 3), "alg_bytes_per_step": alg,
             "up_projection_bytes_per_step": wbytes,
         },
@@ -412,6 +417,8 @@ def main():
     w = synth.workload(args.config, args.variant)
     if args.qscheme == "symrow":
         w.qscheme = kvk.SYMROW
+    elif args.qscheme == "group64":
+        w.qscheme = kvk.GROUP64
     n_tok = w.tokens
     n_stored = w.keep_tokens if w.keep_tokens else n_tok
     dims = kvk.make_dims(kvk.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, qscheme=w.qscheme,
@@ -538,7 +545,7 @@ def main():
             "workload": w.name + ("-per-sequence-plans" if plans else ""), "layers": w.n_layers,
             "q_heads": w.n_q_heads, "kv_heads": w.n_kv_heads,
             "head_dim": w.head_dim, "batch": w.batch, "context": n_tok, "stored_tokens": n_stored,
-            "qscheme": "KIVI32" if w.qscheme == kvk.KIVI32 else "SYMROW",
+            "qscheme": QS_NAMES[w.qscheme],
             "anchors_by_bits": bits_mix,
             "inheriting_layers": sum(e[0] for p in ([w.plan] if plans is None else plans) for e in p),
             "rho_eq2": round(info.rho, 3), "rho_realized": round(info.rho_realized, 3),
