@@ -17,6 +17,9 @@
 // arithmetic reduces to shifts and masks.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "kvk_device.h"
 #include "kvk_internal.h"
 
@@ -385,12 +388,17 @@ __global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
 
 // Decode-time append of one token to every anchor of a layer range.
 struct AppendItem {
-  int64_t region;        // byte offset of the anchor's region in the arena
+  int64_t region;        // byte offset of the anchor's region (of one sequence's streams) in the arena
   int32_t stream_bytes;
   int32_t block_bytes;
   int32_t bits;
   int32_t row;           // the anchor's row in the new-token input (layer - layer_begin)
+  int32_t s0;            // input stream (b * Hkv + kvh) of the item's first stream
+  int32_t pad;
 };
+
+// Items per launch: kernel arguments are limited to 4 KiB.
+constexpr int kAppendItems = 120;
 
 struct AppendArgs {
   const void* k;         // [rows][B][Hkv][D] new keys
@@ -399,10 +407,11 @@ struct AppendArgs {
   int32_t in_f32;
   int32_t pos;           // stored tokens before the call: the new token's position
   int32_t nb_cap;
-  int32_t n_streams;     // B * Hkv
+  int32_t n_streams;     // streams per item: B * Hkv, or Hkv under per-sequence plans
   int64_t row_stride;    // elements between the rows of consecutive layers in k and v
-  AppendItem items[KVK_MAX_LAYERS];
+  AppendItem items[kAppendItems];
 };
+static_assert(sizeof(AppendArgs) <= 4096, "kernel arguments");
 
 __device__ __forceinline__ uint16_t new_token_bf16(const void* p, int64_t e, int in_f32) {
   return in_f32 ? f32_to_bf16_bits(static_cast<const float*>(p)[e]) : static_cast<const uint16_t*>(p)[e];
@@ -417,7 +426,7 @@ __global__ __launch_bounds__(256) void tail_write_kernel(AppendArgs a) {
   const int sidx = idx / D, c = idx % D, t = a.pos & 31;
   const AppendItem& it = a.items[blockIdx.y];
   uint8_t* tailb = a.arena + it.region + (int64_t)sidx * it.stream_bytes + (int64_t)a.nb_cap * it.block_bytes;
-  const int64_t e = (int64_t)it.row * a.row_stride + (int64_t)sidx * D + c;
+  const int64_t e = (int64_t)it.row * a.row_stride + (int64_t)(it.s0 + sidx) * D + c;
   *reinterpret_cast<uint16_t*>(tailb + k_bf16_byte(D, t, c)) = new_token_bf16(a.k, e, a.in_f32);
   *reinterpret_cast<uint16_t*>(tailb + v_bf16_byte(D, t, c)) = new_token_bf16(a.v, e, a.in_f32);
 }
@@ -437,7 +446,7 @@ __global__ __launch_bounds__(256) void group_write_kernel(AppendArgs a) {
   const AppendItem& it = a.items[blockIdx.y];
   uint8_t* base = a.arena + it.region + (int64_t)sidx * it.stream_bytes;
   uint8_t* tailb = base + (int64_t)a.nb_cap * it.block_bytes;
-  const int64_t e0 = (int64_t)it.row * a.row_stride + (int64_t)sidx * D;
+  const int64_t e0 = (int64_t)it.row * a.row_stride + (int64_t)(it.s0 + sidx) * D;
   stage_bf16_block<D, LD>(tailb, Ks, Vs, tid);  // row 31 holds a stale slot until replaced
   __syncthreads();
   for (int c = tid; c < D; c += 256) {
@@ -582,8 +591,7 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
 }
 
 static kvk_status append_gqa(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
-                             int32_t in_dtype, int32_t n_stored, void* arena, int64_t row_stride,
-                             hipStream_t stream);
+                             int32_t in_dtype, int32_t n_stored, void* arena, hipStream_t stream);
 
 extern "C" kvk_status kvk_append_token(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
                                        int32_t in_dtype, int32_t n_stored, void* arena, hipStream_t stream) {
@@ -599,26 +607,33 @@ extern "C" kvk_status kvk_append_token(const kvk_table* t, int32_t l0, int32_t l
       (reinterpret_cast<uintptr_t>(v) & 15))
     return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
   if (d.kind == KVK_MLA) return mla_append_token(t, l0, l1, k, v, in_dtype, n_stored, arena, stream);
-  if (!t->seq.empty()) {  // per-sequence plans: each sequence's rows into its own arena
-    const int64_t elt = in_dtype == KVK_F32 ? 4 : 2;
-    const int64_t row = (int64_t)d.batch * d.n_kv_heads * d.head_dim;
-    for (int b = 0; b < d.batch; ++b) {
-      const int64_t off = (int64_t)b * d.n_kv_heads * d.head_dim * elt;
-      const kvk_status st = append_gqa(t->seq[b], l0, l1, static_cast<const uint8_t*>(k) + off,
-                                       static_cast<const uint8_t*>(v) + off, in_dtype, n_stored,
-                                       static_cast<uint8_t*>(arena) + t->seq_base[b], row, stream);
-      if (st != KVK_OK) return st;
-    }
-    return KVK_OK;
-  }
-  return append_gqa(t, l0, l1, k, v, in_dtype, n_stored, arena,
-                    (int64_t)d.batch * d.n_kv_heads * d.head_dim, stream);
+  return append_gqa(t, l0, l1, k, v, in_dtype, n_stored, arena, stream);
 }
 
+// One item per (anchor layer) of a shared plan, over all B * Hkv streams; under
+// per-sequence plans one per (sequence, anchor layer of its plan), over its Hkv
+// streams.  Launched in groups of up to kAppendItems items.
 static kvk_status append_gqa(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
-                             int32_t in_dtype, int32_t n_stored, void* arena, int64_t row_stride,
-                             hipStream_t stream) {
+                             int32_t in_dtype, int32_t n_stored, void* arena, hipStream_t stream) {
   const kvk_dims& d = t->d;
+  const bool per_seq = !t->seq.empty();
+  std::vector<AppendItem> items;
+  for (int b = 0; b < (per_seq ? d.batch : 1); ++b) {
+    const kvk_table* st = per_seq ? t->seq[b] : t;
+    const int64_t base = per_seq ? t->seq_base[b] : 0;
+    for (int l = l0; l < l1; ++l) {
+      if (st->plan[l].inherit) continue;  // an inheriting layer stores nothing (§2.1)
+      AppendItem it;
+      it.region = base + st->info.layer_offset[l];
+      it.stream_bytes = (int32_t)st->info.stream_bytes[l];
+      it.block_bytes = (int32_t)st->block_bytes[l];
+      it.bits = st->bits[l];
+      it.row = l - l0;
+      it.s0 = per_seq ? b * d.n_kv_heads : 0;
+      it.pad = 0;
+      items.push_back(it);
+    }
+  }
   AppendArgs a;
   a.k = k;
   a.v = v;
@@ -626,39 +641,32 @@ static kvk_status append_gqa(const kvk_table* t, int32_t l0, int32_t l1, const v
   a.in_f32 = in_dtype == KVK_F32;
   a.pos = n_stored;
   a.nb_cap = t->nb_cap;
-  a.n_streams = d.batch * d.n_kv_heads;
-  a.row_stride = row_stride;
-  int n = 0;
-  for (int l = l0; l < l1; ++l) {
-    if (t->plan[l].inherit) continue;  // an inheriting layer stores nothing (§2.1)
-    AppendItem& it = a.items[n++];
-    it.region = t->info.layer_offset[l];
-    it.stream_bytes = (int32_t)t->info.stream_bytes[l];
-    it.block_bytes = (int32_t)t->block_bytes[l];
-    it.bits = t->bits[l];
-    it.row = l - l0;
-  }
-  if (n == 0) return KVK_OK;
+  a.n_streams = per_seq ? d.n_kv_heads : d.batch * d.n_kv_heads;
+  a.row_stride = (int64_t)d.batch * d.n_kv_heads * d.head_dim;
   const int qs = d.qscheme;
   const dim3 b3(256);
-  if (n_stored % KVK_GROUP != KVK_GROUP - 1) {
-    const dim3 g3((unsigned)((a.n_streams * d.head_dim + 255) / 256), (unsigned)n);
-    if (d.head_dim == 128) hipLaunchKernelGGL(tail_write_kernel<128>, g3, b3, 0, stream, a);
-    else hipLaunchKernelGGL(tail_write_kernel<64>, g3, b3, 0, stream, a);
-  } else {
-    const dim3 g3((unsigned)a.n_streams, (unsigned)n);
-    if (d.head_dim == 128) {
-      if (qs == KVK_Q_KIVI32) hipLaunchKernelGGL((group_write_kernel<128, kQsKivi>), g3, b3, 0, stream, a);
-      else if (qs == KVK_Q_GROUP64) hipLaunchKernelGGL((group_write_kernel<128, kQsG64>), g3, b3, 0, stream, a);
-      else hipLaunchKernelGGL((group_write_kernel<128, kQsSym>), g3, b3, 0, stream, a);
+  for (size_t i0 = 0; i0 < items.size(); i0 += kAppendItems) {
+    const int n = (int)std::min<size_t>(kAppendItems, items.size() - i0);
+    std::copy(items.begin() + i0, items.begin() + i0 + n, a.items);
+    if (n_stored % KVK_GROUP != KVK_GROUP - 1) {
+      const dim3 g3((unsigned)((a.n_streams * d.head_dim + 255) / 256), (unsigned)n);
+      if (d.head_dim == 128) hipLaunchKernelGGL(tail_write_kernel<128>, g3, b3, 0, stream, a);
+      else hipLaunchKernelGGL(tail_write_kernel<64>, g3, b3, 0, stream, a);
     } else {
-      if (qs == KVK_Q_KIVI32) hipLaunchKernelGGL((group_write_kernel<64, kQsKivi>), g3, b3, 0, stream, a);
-      else if (qs == KVK_Q_GROUP64) hipLaunchKernelGGL((group_write_kernel<64, kQsG64>), g3, b3, 0, stream, a);
-      else hipLaunchKernelGGL((group_write_kernel<64, kQsSym>), g3, b3, 0, stream, a);
+      const dim3 g3((unsigned)a.n_streams, (unsigned)n);
+      if (d.head_dim == 128) {
+        if (qs == KVK_Q_KIVI32) hipLaunchKernelGGL((group_write_kernel<128, kQsKivi>), g3, b3, 0, stream, a);
+        else if (qs == KVK_Q_GROUP64) hipLaunchKernelGGL((group_write_kernel<128, kQsG64>), g3, b3, 0, stream, a);
+        else hipLaunchKernelGGL((group_write_kernel<128, kQsSym>), g3, b3, 0, stream, a);
+      } else {
+        if (qs == KVK_Q_KIVI32) hipLaunchKernelGGL((group_write_kernel<64, kQsKivi>), g3, b3, 0, stream, a);
+        else if (qs == KVK_Q_GROUP64) hipLaunchKernelGGL((group_write_kernel<64, kQsG64>), g3, b3, 0, stream, a);
+        else hipLaunchKernelGGL((group_write_kernel<64, kQsSym>), g3, b3, 0, stream, a);
+      }
     }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "append launch: %s", hipGetErrorString(e));
   }
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "append launch: %s", hipGetErrorString(e));
   return KVK_OK;
 }
 
