@@ -390,8 +390,7 @@ def main():
         calibrate_copy()
         return
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: this build has no multi-GPU path (asked for {args.gpus}); "
-              "the design for sharding is described in DESIGN.md.", file=sys.stderr)
+        print(f"bench.py measures one GPU: the library has no multi-GPU path (asked for {args.gpus} GPUs).", file=sys.stderr)
         sys.exit(2)
     if args.config == 3:
         run_mla(args)

@@ -17,7 +17,7 @@ Three schemes:
     cache: 4 + 32/64 = 4.5 bits per element at 4 bits, 3.56x); kivi_quantize over
     such groups.
 
-Readings where the paper is silent (each is listed in the design doc): rounding is
+Readings where the paper is silent: rounding is
 round-half-to-even; the scale is rounded to its storage type before codes are
 computed; the zero point is the fp16 of the group minimum; a group with a zero
 scale gets code 0 (so x_hat = zero, or 0 for SYMROW); the arithmetic is the fp32
