@@ -527,7 +527,7 @@ SelWorkspace sel_workspace(int T) {
   w.part = kvk::round256(w.f1 + (int64_t)Tp * kFfn * 2);     // fp32 [chunks][256]
   w.splitk = kvk::round256(w.part + (int64_t)((T + 255) / 256) * kW * 4);  // fp32 [splits][T][256]
   const int max_splits = std::min(kSplitMax, (512 + (T + 63) / 64 - 1) / ((T + 63) / 64));
-  w.attn = kvk::round256(w.splitk + (int64_t)std::max(1, max_splits) * T * kW * 4);  // fp32 [splits][T][4][kRec]
+  w.attn = kvk::round256(w.splitk + (max_splits > 1 ? (int64_t)max_splits * T * kW * 4 : 0));  // fp32 [splits][T][4][kRec]
   int key_len = 0;
   const int attn_splits = sel_attn_splits(T, &key_len);
   w.total = kvk::round256(w.attn + (attn_splits > 1 ? (int64_t)attn_splits * T * kHeads * kRec * 4 : 0));
