@@ -2,91 +2,150 @@
 
 TEST INFRASTRUCTURE ONLY (see oracle/__init__.py).
 
-§2.3: a selector maps the T input tokens to one action per layer.  A small shared
-sequence model ingests the backbone's own token embeddings through two bidirectional
-transformer blocks; its outputs are averaged over time; one linear head per layer
-maps that feature to logits over the action space; evaluation takes the plain
-argmax, with the depth action's logit forced to -inf where depth is not allowed
-(always at the first layer).  The evaluated selectors hold 2.6-3.7M parameters
-(§2.3); the paper reports about 3 ms per prompt on an H100 from 2k to 32k tokens
-(Fig. prefill).
+What it computes (§2.3 and App. B "Selector architecture"):
+  * the backbone's token embeddings [T, H] are mapped linearly to width 256;
+  * two bidirectional transformer blocks follow; each has
+      - an attention sublayer of 4 heads of width 64, with rotary position
+        embeddings applied to the queries and the keys,
+      - a SwiGLU feed-forward sublayer of inner width 1024,
+      - an RMSNorm before each sublayer and a residual connection around each;
+  * a final RMSNorm follows the second block;
+  * the output is averaged over the T tokens into z (256 wide);
+  * optionally the budget conditioning of App. B (FiLM) maps z to z * (1 + gamma) + beta
+    (the MLP producing gamma, beta from the target ratio is outside this function);
+  * each of the L layers has its own linear head (with bias) giving |A| logits;
+  * the depth action's logit is -inf at the first layer and at every layer when
+    depth is not in the selector's action space (§2.3); evaluation takes the argmax.
 
 Readings where the paper is silent (the library follows the same):
-  * width 256, 4 heads of 64, feed-forward 1024 with tanh-approximated GELU,
-    pre-normalisation (LayerNorm, eps 1e-5, with gain and bias) and residuals;
-  * the embeddings (width d_model) enter through a linear map to 256 with bias;
-    no positional encoding (the feature is a time average);
-  * attention is softmax(q k / 8) over every position (bidirectional);
-  * GQA action space: index 0 = inherit (depth), 1..4 = bf16, int8, int4, int2;
-  * every weight is an input (synthetic here; the paper's are trained).
-Everything is fp64 from the given values (bf16 weights and embeddings).
+  * RoPE: the position of token t is t (0 .. T-1); base 10000 (RoFormer's);
+    rotate-half pairing, channel i with channel i + 32 of a 64-wide head, at
+    frequency base^(-2i/64), i = 0 .. 31 (the convention of the Qwen2.5 family the
+    selector serves); applied to q and k after their projections, v untouched;
+  * attention scale 1/sqrt(64); softmax over every position (bidirectional);
+  * RMSNorm: x / sqrt(mean(x^2) + 1e-6) * g, a gain and no bias;
+  * SwiGLU: W_down (SiLU(W_gate n) * W_up n), SiLU(x) = x / (1 + e^-x);
+  * no bias in the trunk's linear maps (input map, q, k, v, o, gate, up, down);
+    the heads carry biases (App. B initialises them);
+  * action index order: 0 = inherit; 1 + 4 j + k = produce with kept width
+    r / 2^j and b = 16 / 2^k bits (j, k = 0 .. 3), so index 1 is the least
+    compressed action; a GQA selector (precision and depth) uses the first five.
+Weight matrices are [out][in].  Everything is fp64 from the given values.
 
-Pins (tests/test_oracle_selector.py): a block with zero weights is the identity
-(the residual path); attention over identical positions returns their value; the
-pooled feature is invariant to permuting the tokens; explicit loops on a tiny
-input for attention and LayerNorm; layer 0 never inherits; the argmax follows
-planted head biases.
+Pins (tests/test_oracle_selector.py): the parameter count of this weight set
+matches every count App. B prints (2.61 - 3.69M over six backbones, heads
+122k - 280k); RMSNorm and SwiGLU against explicit loops and torch's own
+rms_norm / silu; RoPE against complex rotation, norm preservation, the identity
+at position 0; attention with all positions at 0 against torch's
+scaled_dot_product_attention; shifting every position by a constant leaves the
+attention unchanged; identical tokens return their value; a block with zero
+weights is the identity; the feature depends on token order; layer 0 never
+inherits; a masked depth action is never chosen; planted biases steer the argmax;
+FiLM with zero scale and shift is the identity.
 """
 import numpy as np
 
 WIDTH = 256
 HEADS = 4
+HEAD_DIM = 64
 FFN = 1024
-N_ACTIONS = 5
-ACTIONS = [(1, 16), (0, 16), (0, 8), (0, 4), (0, 2)]  # (inherit, bits) by action index
+RMS_EPS = 1e-6
+ROPE_BASE = 10000.0
+
+# Composed action space (eq. (3)): index -> (inherit, rank divisor 2^j, bits)
+ACTIONS = [(1, 1, 16)] + [(0, 1 << j, 16 >> k) for j in range(4) for k in range(4)]
+N_ACTIONS_FULL = len(ACTIONS)        # 17
+N_ACTIONS_GQA = 5                    # inherit, 16, 8, 4, 2 bits at full width
+BLOCK_KEYS = ("g_attn", "w_q", "w_k", "w_v", "w_o", "g_ffn", "w_gate", "w_up", "w_down")
 
 
-def layer_norm(x, g, b, eps=1e-5):
+def rms_norm(x, g, eps=RMS_EPS):
     x = np.asarray(x, np.float64)
-    mu = x.mean(axis=-1, keepdims=True)
-    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
-    return (x - mu) / np.sqrt(var + eps) * g + b
+    return x / np.sqrt((x * x).mean(axis=-1, keepdims=True) + eps) * np.asarray(g, np.float64)
 
 
-def gelu(x):
-    return 0.5 * x * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (x + 0.044715 * x ** 3)))
+def silu(x):
+    return x / (1.0 + np.exp(-x))
 
 
-def attention(x, w_qkv, b_qkv, w_o, b_o):
-    """Bidirectional multi-head attention over x [T, 256]."""
-    T = x.shape[0]
-    qkv = x @ w_qkv + b_qkv  # [T, 768]
-    q, k, v = qkv[:, :WIDTH], qkv[:, WIDTH:2 * WIDTH], qkv[:, 2 * WIDTH:]
-    dh = WIDTH // HEADS
-    out = np.zeros((T, WIDTH))
+def rope_angles(positions):
+    """[T, 32] angles m * theta_i."""
+    i = np.arange(HEAD_DIM // 2, dtype=np.float64)
+    theta = ROPE_BASE ** (-2.0 * i / HEAD_DIM)
+    return np.asarray(positions, np.float64)[:, None] * theta[None, :]
+
+
+def rope(x, positions):
+    """Rotate-half RoPE of x [T, 64]: channels (i, i + 32) rotated by m * theta_i."""
+    a = rope_angles(positions)
+    c, s = np.cos(a), np.sin(a)
+    x1, x2 = x[:, :HEAD_DIM // 2], x[:, HEAD_DIM // 2:]
+    return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=1)
+
+
+def attention(n, p, positions):
+    """Bidirectional multi-head attention over the normalised rows n [T, 256]."""
+    q, k, v = n @ p["w_q"].T, n @ p["w_k"].T, n @ p["w_v"].T
+    out = np.zeros_like(q)
     for h in range(HEADS):
-        sl = slice(h * dh, (h + 1) * dh)
-        s = q[:, sl] @ k[:, sl].T / np.sqrt(dh)
+        sl = slice(h * HEAD_DIM, (h + 1) * HEAD_DIM)
+        qh, kh = rope(q[:, sl], positions), rope(k[:, sl], positions)
+        s = qh @ kh.T / np.sqrt(HEAD_DIM)
         s = s - s.max(axis=1, keepdims=True)
-        p = np.exp(s)
-        p /= p.sum(axis=1, keepdims=True)
-        out[:, sl] = p @ v[:, sl]
-    return out @ w_o + b_o
+        e = np.exp(s)
+        out[:, sl] = (e / e.sum(axis=1, keepdims=True)) @ v[:, sl]
+    return out @ p["w_o"].T
 
 
-def block(x, p):
-    """Pre-normalised transformer block; p holds ln1_g, ln1_b, w_qkv, b_qkv, w_o, b_o,
-    ln2_g, ln2_b, w_1, b_1, w_2, b_2 (weights [in, out])."""
-    h = x + attention(layer_norm(x, p["ln1_g"], p["ln1_b"]), p["w_qkv"], p["b_qkv"], p["w_o"], p["b_o"])
-    return h + gelu(layer_norm(h, p["ln2_g"], p["ln2_b"]) @ p["w_1"] + p["b_1"]) @ p["w_2"] + p["b_2"]
+def swiglu(n, p):
+    return (silu(n @ p["w_gate"].T) * (n @ p["w_up"].T)) @ p["w_down"].T
 
 
-def feature(emb, w):
-    """emb [T, d_model] -> the time-averaged feature [256]."""
-    x = np.asarray(emb, np.float64) @ w["w_in"] + w["b_in"]
+def block(x, p, positions):
+    """Pre-norm block: x + Attn(RMSNorm(x)), then + SwiGLU(RMSNorm(.))."""
+    h = x + attention(rms_norm(x, p["g_attn"]), p, positions)
+    return h + swiglu(rms_norm(h, p["g_ffn"]), p)
+
+
+def feature(emb, w, film=None, positions=None):
+    """emb [T, H] -> z [256]; film = (gamma, beta) or None."""
+    emb = np.asarray(emb, np.float64)
+    pos = np.arange(emb.shape[0]) if positions is None else positions
+    x = emb @ np.asarray(w["w_in"], np.float64).T
     for p in w["blocks"]:
-        x = block(x, p)
-    return x.mean(axis=0)
-
-
-def logits(emb, w):
-    """[n_layers, 5] logits; the depth action of layer 0 at -inf."""
-    f = feature(emb, w)
-    z = np.einsum("c,lca->la", f, np.asarray(w["w_head"], np.float64)) + w["b_head"]
-    z[0, 0] = -np.inf
+        x = block(x, p, pos)
+    z = rms_norm(x, w["g_final"]).mean(axis=0)
+    if film is not None:
+        gamma, beta = film
+        z = z * (1.0 + np.asarray(gamma, np.float64)) + np.asarray(beta, np.float64)
     return z
 
 
-def plan(emb, w):
-    """Per-layer (inherit, bits) by argmax (lowest index on ties)."""
-    return [ACTIONS[int(np.argmax(r))] for r in logits(emb, w)]
+def logits(emb, w, depth=True, film=None):
+    """[L, |A|] logits; the depth action (index 0) -inf at layer 0, or everywhere
+    when depth is not in the action space."""
+    z = feature(emb, w, film)
+    out = np.einsum("lac,c->la", np.asarray(w["w_head"], np.float64), z) + np.asarray(w["b_head"], np.float64)
+    out[0, 0] = -np.inf
+    if not depth:
+        out[:, 0] = -np.inf
+    return out
+
+
+def actions(emb, w, depth=True, film=None):
+    """Per-layer action index by argmax (the lowest index on ties)."""
+    return [int(np.argmax(r)) for r in logits(emb, w, depth, film)]
+
+
+def action_config(index):
+    """(inherit, rank divisor, bits) of a composed-space action index."""
+    return ACTIONS[index]
+
+
+def weight_shapes(d_model, n_layers, n_actions=N_ACTIONS_FULL):
+    """Shapes of every weight the functions above consume ([out][in] matrices)."""
+    blk = {"g_attn": (WIDTH,), "w_q": (WIDTH, WIDTH), "w_k": (WIDTH, WIDTH), "w_v": (WIDTH, WIDTH),
+           "w_o": (WIDTH, WIDTH), "g_ffn": (WIDTH,), "w_gate": (FFN, WIDTH), "w_up": (FFN, WIDTH),
+           "w_down": (WIDTH, FFN)}
+    return {"w_in": (WIDTH, d_model), "blocks": [dict(blk), dict(blk)], "g_final": (WIDTH,),
+            "w_head": (n_layers, n_actions, WIDTH), "b_head": (n_layers, n_actions)}
