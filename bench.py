@@ -98,28 +98,34 @@ def time_append(kvk, torch, table, n_layers, arena, n_stored, k_shape, v_shape, 
 
 def time_selector(kvk, torch, d_model, n_layers, dev, lengths=(2048, 8192, 32768)):
     """The selector forward pass (prompt embeddings -> plan) at several prompt lengths,
-    synthetic weights of the model's embedding width: µs per prompt (median of 5)."""
+    synthetic weights of the model's embedding width, the GQA action space (depth and
+    precision: 5 actions): µs per prompt, 4 warm-ups then the median of 12 (the
+    paper's timing protocol)."""
+    import numpy as np
     g = torch.Generator(device=dev)
     g.manual_seed(99)
-    n_w = kvk.selector_weight_elems(d_model, n_layers)
+    n_w = kvk.selector_weight_elems(d_model, n_layers, kvk.SELECTOR_ACTIONS_GQA)
     weights = (torch.randn(n_w, generator=g, device=dev) * 0.02).to(torch.bfloat16)
     actions = torch.empty(n_layers, dtype=torch.int32, device=dev)
     out = {}
     for T in lengths:
         emb = torch.randn((T, d_model), generator=g, device=dev).to(torch.bfloat16)
         ws = torch.empty(kvk.selector_workspace_bytes(d_model, n_layers, T), dtype=torch.uint8, device=dev)
-        kvk.selector_forward(d_model, n_layers, weights, emb, actions, ws)
+        for _ in range(4):
+            kvk.selector_forward(d_model, n_layers, weights, emb, actions, ws)
         times = []
-        for _ in range(5):
+        for _ in range(12):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
             e0.record()
             kvk.selector_forward(d_model, n_layers, weights, emb, actions, ws)
             e1.record()
             torch.cuda.synchronize()
             times.append(e0.elapsed_time(e1) * 1e3)
-        out[str(T)] = round(sorted(times)[2], 1)
+        out[str(T)] = round(float(np.median(times)), 1)
         del emb, ws
-    return {"d_model": d_model, "layers": n_layers, "us_by_prompt_tokens": out}
+    return {"d_model": d_model, "layers": n_layers, "actions": kvk.SELECTOR_ACTIONS_GQA,
+            "us_by_prompt_tokens": out}
 
 
 def kernel_source_hash(sources=GQA_SOURCES) -> str:

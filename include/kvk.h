@@ -367,35 +367,45 @@ kvk_status kvk_snapkv_select(const kvk_table* table, int32_t layer, const void* 
                              int32_t in_dtype, int32_t n_tokens, float scale, int32_t* keep_out,
                              float* importance, void* workspace, size_t ws_bytes, hipStream_t stream);
 
-/* The selector's forward pass (§2.3): the prompt's token embeddings (the backbone's
- * own) -> a linear map to width 256 -> two bidirectional transformer blocks ->
- * average over the prompt -> one linear head per layer -> the argmax action of
- * each layer, the depth action's logit at -inf for layer 0.  Run once per prompt
- * at prefill; the actions build the plan that is held for the whole generation.
- * Blocks: pre-normalised (LayerNorm with gain and bias, eps 1e-5), attention of
- * 4 heads of 64 over every position with scale 1/8, feed-forward 256 -> 1024 ->
- * 256 with the tanh form of GELU, residual additions; no positional encoding.
- * Actions: 0 inherit (depth), 1 bf16, 2 int8, 3 int4, 4 int2 (GQA plans).
- *   weights : device bf16, kvk_selector_weight_elems(d_model, n_layers) elements,
- *             packed in this order, each matrix [out][in] row-major:
- *             w_in [256][d_model], b_in [256]; then per block (two):
- *             ln1_gain [256], ln1_bias [256], w_qkv [768][256] (q, k, v rows;
- *             head h uses rows 64h .. 64h+63 of each), b_qkv [768], w_o [256][256],
- *             b_o [256], ln2_gain [256], ln2_bias [256], w_1 [1024][256],
- *             b_1 [1024], w_2 [256][1024], b_2 [256]; then w_head [n_layers][256][5]
- *             (layer l's head maps feature c to action a at [l][c][a]), b_head
- *             [n_layers][5].
- *   emb     : device bf16 [n_tokens][d_model]; d_model a multiple of 32.
- *   logits  : NULL, or device fp32 [n_layers][5] (computed in fp32; bf16 operands).
- *   actions : device int32 [n_layers], the argmax (lowest index on ties).
+/* The selector's forward pass (§2.3; App. B "Selector architecture"): the prompt's
+ * token embeddings (the backbone's own) -> a linear map to width 256 -> two
+ * bidirectional pre-norm transformer blocks -> a final RMSNorm -> the average over
+ * the prompt -> an optional budget scale and shift (App. B "Budget conditioning":
+ * z * (1 + gamma) + beta) -> one linear head per layer -> the argmax action of each
+ * layer.  Run once per prompt at prefill; the actions build the plan that is held
+ * for the whole generation.
+ * Block: x += W_o Attn(RMSNorm(x)), then x += W_down (SiLU(W_gate n) * W_up n) with
+ * n = RMSNorm(x); RMSNorm is x / sqrt(mean(x^2) + 1e-6) * gain; attention has 4
+ * heads of 64 over every position with scale 1/8 and rotary embeddings on q and k
+ * (token t at position t, base 10000, channel i of a head paired with i + 32 and
+ * turned by t * 10000^(-i/32)); the trunk's linear maps have no bias, the heads do.
+ * Actions (eq. (3)): index 0 = inherit (depth); 1 + 4 j + k = produce with kept
+ * width r / 2^j at 16 / 2^k bits (j, k = 0..3): 17 actions for the composed space;
+ * a GQA selector (precision and depth) uses the first 5 (inherit, bf16, int8, int4,
+ * int2).  The depth logit is -inf at layer 0, and at every layer when depth = 0.
+ *   d_model  : the embedding width, a multiple of 32; n_layers 1..64;
+ *   n_actions: 2..32 logits per layer;
+ *   weights  : device bf16, kvk_selector_weight_elems(d_model, n_layers, n_actions)
+ *              elements, packed in this order, each matrix [out][in] row-major:
+ *              w_in [256][d_model]; then per block (two): g_attn [256],
+ *              w_qkv [768][256] (q, k, v rows; head h uses rows 64h .. 64h+63 of
+ *              each), w_o [256][256], g_ffn [256], w_gate [1024][256],
+ *              w_up [1024][256], w_down [256][1024]; then g_final [256],
+ *              w_head [n_layers][n_actions][256], b_head [n_layers][n_actions].
+ *   emb      : device bf16 [n_tokens][d_model].
+ *   film     : NULL (no conditioning), or device fp32 [2][256]: gamma, then beta.
+ *   logits   : NULL, or device fp32 [n_layers][n_actions] (fp32; bf16 operands).
+ *   actions  : device int32 [n_layers], the argmax (lowest index on ties).
  *   workspace: device, >= kvk_selector_workspace_bytes(...), 256-byte aligned.
+ * kvk_selector_weight_elems returns -1 for sizes outside those ranges.
  * Errors: KVK_ERR_INVALID (sizes, NULL pointers, misalignment), KVK_ERR_BUFFER,
  *         KVK_ERR_DEVICE. */
-int64_t kvk_selector_weight_elems(int32_t d_model, int32_t n_layers);
+int64_t kvk_selector_weight_elems(int32_t d_model, int32_t n_layers, int32_t n_actions);
 kvk_status kvk_selector_workspace_bytes(int32_t d_model, int32_t n_layers, int32_t n_tokens, size_t* out_bytes);
-kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, const void* weights, const void* emb,
-                                int32_t n_tokens, float* logits, int32_t* actions, void* workspace,
-                                size_t ws_bytes, hipStream_t stream);
+kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, int32_t n_actions, int32_t depth,
+                                const void* weights, const void* emb, int32_t n_tokens, const float* film,
+                                float* logits, int32_t* actions, void* workspace, size_t ws_bytes,
+                                hipStream_t stream);
 
 /* One decode step of attention for layers [layer_begin, layer_end) (§2.1): layer l
  * uses its own query and the cache of anchor_of[l].  Layers in the range that

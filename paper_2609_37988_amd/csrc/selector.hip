@@ -1,17 +1,26 @@
-// The selector's forward pass (KV-Kaizen §2.3): a prompt's token embeddings ->
-// two bidirectional transformer blocks of width 256 -> time average -> one linear
-// head per layer -> argmax action per layer (the depth action of layer 0 excluded).
-// It runs once per prompt at prefill; the plan it yields is held for the whole
-// generation.  Weights are inputs (packed bf16, layout in include/kvk.h).
+// The selector's forward pass (KV-Kaizen §2.3, App. B "Selector architecture"): a
+// prompt's token embeddings -> a linear map to width 256 -> two bidirectional
+// pre-norm transformer blocks (RMSNorm, 4 heads of 64 with rotary embeddings on q
+// and k, RMSNorm, SwiGLU of inner width 1024; residuals around both sublayers) ->
+// a final RMSNorm -> time average -> optional budget scale and shift (FiLM) -> one
+// linear head per layer -> argmax action per layer (the depth action masked at the
+// first layer, or everywhere when depth is not in the action space).  It runs once
+// per prompt at prefill; the plan it yields is held for the whole generation.
+// Weights are inputs (packed bf16, layout in include/kvk.h).
 //
 // Kernels (T = prompt length):
+//   sel_rope_kernel: the rotation table cos/sin(t * theta_i), t < T, i < 32, formed
+//       in fp64 and stored fp32 (the angles reach 3e4 rad; an fp32 product would
+//       put errors of 1e-3 rad into them).
 //   sel_gemm_kernel<EPI>: C = A [T, K] . W^T, W [N, K] (bf16 operands on MFMA
 //       16x16x32, fp32 accumulation); 64 x 256 output tiles per workgroup, the A and
-//       W rows of each k-step staged in LDS (double-buffered); the epilogue
-//       adds the bias and, by EPI: stores fp32, adds into the fp32 residual stream,
-//       applies GELU and stores bf16, or splits q, k (bf16 rows) and v (bf16,
-//       transposed per head for the attention's value operand).
-//   sel_layernorm_kernel: one wave per row of 256, fp32 in, bf16 out.
+//       W rows of each k-step staged in LDS (double-buffered); by EPI the epilogue
+//       stores fp32, adds into the fp32 residual stream, forms SiLU(gate) * up to
+//       bf16 (the W rows of a tile are mapped so that a lane holds a gate column and
+//       its up column), or rotates q and k (a lane holds channel i and i + 32 of a
+//       head) and splits q, k (bf16 rows) and v (bf16, transposed per head for the
+//       attention's value operand).
+//   sel_rmsnorm_kernel: one wave per row of 256, fp32 in, bf16 out.
 //   sel_attention_kernel: bidirectional attention, 4 heads of 64; a workgroup takes
 //       128 queries of one head (4 waves x two 16-query tiles) and walks the keys
 //       in tiles of 64, double-buffered in LDS; S^T = K Q^T, one online-softmax
@@ -20,8 +29,9 @@
 //       the accumulator layout), the probability sums on MFMA as well; on short
 //       prompts the keys split across workgroups too, and sel_attn_merge_kernel
 //       combines the splits.
-//   sel_pool_kernel / sel_heads_kernel: the time average (per-chunk partial sums,
-//       then their sum), the per-layer logits and the argmax (a workgroup per layer).
+//   sel_pool_kernel / sel_heads_kernel: the final RMSNorm and the time average
+//       (per-chunk partial sums of the normalised rows, then their sum), the budget
+//       scale and shift, the per-layer logits and the argmax (a workgroup per layer).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -34,28 +44,39 @@ using namespace kvkd;
 
 namespace {
 
-constexpr int kW = 256, kHeads = 4, kDh = 64, kFfn = 1024, kActions = 5;
+constexpr int kW = 256, kHeads = 4, kDh = 64, kFfn = 1024, kMaxActions = 32;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kRmsEps = 1e-6f;
+constexpr double kRopeBase = 10000.0;
 constexpr int kRec = kDh + 4;  // key-split record: 64 outputs, max, sum, 2 pad (16-byte rows)
 
 __device__ __forceinline__ f4 mfma_bf(bf16x8 a, bf16x8 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
-__device__ __forceinline__ float gelu_tanh(float x) {
-  const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
-  return 0.5f * x * (1.0f + tanhf(u));
+__device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
+
+// cs[t][i] = (cos, sin)(t * base^(-i/32)), i < 32: the rotate-half pair (i, i + 32)
+// of every head turns by that angle at position t.
+__global__ __launch_bounds__(256) void sel_rope_kernel(float2* cs, int T) {
+  const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (k >= (int64_t)T * (kDh / 2)) return;
+  const int i = (int)(k % (kDh / 2));
+  const double theta = pow(kRopeBase, -(double)i / (kDh / 2));
+  double s, c;
+  sincos((double)(k / (kDh / 2)) * theta, &s, &c);
+  cs[k] = make_float2((float)c, (float)s);
 }
 
-enum Epi { kStoreF32 = 0, kAddF32 = 1, kGeluBf16 = 2, kQkv = 3 };
+enum Epi { kStoreF32 = 0, kAddF32 = 1, kSwiGlu = 2, kQkv = 3 };
 
 struct GemmArgs {
   const uint16_t* a;   // [M][K] bf16
-  const uint16_t* w;   // [N][K] bf16
-  const uint16_t* bias;  // [N] bf16
+  const uint16_t* w;   // [N][K] bf16 (kSwiGlu: gate rows [1024][K], then up rows)
   float* out_f32;      // [M][N] (kStoreF32, kAddF32)
-  uint16_t* out_bf16;  // [M][N] (kGeluBf16), [M][512] q|k (kQkv)
+  uint16_t* out_bf16;  // [M][1024] (kSwiGlu), [M][512] q|k (kQkv)
   uint16_t* vt;        // kQkv: [heads][64][vt_pitch] values, transposed
+  const float2* rope;  // kQkv: [M][32] cos, sin
   float* part;         // split-K: [gridDim.z][M][N] raw partial sums (no epilogue); else null
   int32_t M, N, K, vt_pitch;
   int32_t k_len;       // k per split (a multiple of 32)
@@ -66,6 +87,9 @@ struct GemmArgs {
 // A rows and W rows of the tile are staged in LDS (double-buffered: the next step's
 // share of each thread is loaded into registers while the current step is consumed,
 // one barrier per step); lane (row i16, k-group kg) feeds 8 consecutive k.
+// kSwiGlu: tile y covers hidden columns 128 y .. + 127; wave w's MFMA tiles j = 0, 1
+// read gate rows 128 y + 32 w + 16 j + i and tiles j = 2, 3 the up rows of the same
+// hidden columns, so acc[i][j] and acc[i][j + 2] of a lane hold a gate and its up.
 template <int EPI>
 __global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
   constexpr int BM = 64, BN = 256, KP = 32 + 8;  // LDS row pitch (halfs)
@@ -73,12 +97,20 @@ __global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
   __shared__ uint16_t bs[2][BN][KP];
   const int tid = threadIdx.x, lane = tid & 63, i16 = lane & 15, kg = lane >> 4, wv = tid >> 6;
   const int r0 = blockIdx.x * BM, c0 = blockIdx.y * BN;
-  // staging share: A row tid / 4 and W rows tid / 4 + 64 r, 8 k at 8 (tid % 4)
+  // staging share: A row tid / 4 and LDS W rows tid / 4 + 64 r, 8 k at 8 (tid % 4)
   const int sr = tid >> 2, sk = 8 * (tid & 3);
   const bool a_ok = r0 + sr < g.M;
   const uint16_t* ap = g.a + (int64_t)(a_ok ? r0 + sr : 0) * g.K + sk;
-  const uint16_t* wp = g.w + (int64_t)(c0 + sr) * g.K + sk;
-  const int64_t wstep = (int64_t)64 * g.K;
+  int64_t wrow0, wrstep;  // W row of LDS row sr + 64 r: wrow0 + r * wrstep
+  if constexpr (EPI == kSwiGlu) {
+    wrow0 = (sr < 32 ? 0 : kFfn - 32) + blockIdx.y * 128 + sr;
+    wrstep = 32;
+  } else {
+    wrow0 = c0 + sr;
+    wrstep = 64;
+  }
+  const uint16_t* wp = g.w + wrow0 * g.K + sk;
+  const int64_t wstep = wrstep * g.K;
   uint4 areg, w0, w1, w2, w3;
   auto fetch = [&](int k0) {
     areg = a_ok ? *reinterpret_cast<const uint4*>(ap + k0) : make_uint4(0, 0, 0, 0);
@@ -116,11 +148,37 @@ __global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
     if (more) stash(buf ^ 1);  // that buffer was last read before the previous barrier
     __syncthreads();
   }
-  // acc[i][j]: lane (m = r0 + 16 i + i16) holds n = c0 + 64 wv + 16 j + 4 kg + e
+  // acc[i][j]: lane (m = r0 + 16 i + i16) holds LDS column 64 wv + 16 j + 4 kg + e
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = r0 + 16 * i + i16;
     if (m >= g.M) continue;
+    if constexpr (EPI == kSwiGlu) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int hc = blockIdx.y * 128 + 32 * wv + 16 * j + 4 * kg;  // hidden column
+        uint2 w2;
+        w2.x = (uint32_t)f32_to_bf16_bits(silu(acc[i][j][0]) * acc[i][j + 2][0]) |
+               ((uint32_t)f32_to_bf16_bits(silu(acc[i][j][1]) * acc[i][j + 2][1]) << 16);
+        w2.y = (uint32_t)f32_to_bf16_bits(silu(acc[i][j][2]) * acc[i][j + 2][2]) |
+               ((uint32_t)f32_to_bf16_bits(silu(acc[i][j][3]) * acc[i][j + 2][3]) << 16);
+        *reinterpret_cast<uint2*>(g.out_bf16 + (int64_t)m * kFfn + hc) = w2;
+      }
+      continue;
+    }
+    if constexpr (EPI == kQkv) {
+      if (c0 < 2 * kW) {  // q or k of head wv: rotate pairs (c, c + 32), c = 16 j + 4 kg + e
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float2 r = g.rope[(int64_t)m * (kDh / 2) + 16 * j + 4 * kg + e];
+            const float x1 = acc[i][j][e], x2 = acc[i][j + 2][e];
+            acc[i][j][e] = x1 * r.x - x2 * r.y;
+            acc[i][j + 2][e] = x2 * r.x + x1 * r.y;
+          }
+      }
+    }
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int n0 = c0 + 64 * wv + 16 * j + 4 * kg;
@@ -128,19 +186,12 @@ __global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
         *reinterpret_cast<f4*>(g.part + ((int64_t)blockIdx.z * g.M + m) * g.N + n0) = acc[i][j];
         continue;
       }
-      f4 v = acc[i][j];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(g.bias[n0 + e]);
+      const f4 v = acc[i][j];
       if constexpr (EPI == kStoreF32) {
         *reinterpret_cast<f4*>(g.out_f32 + (int64_t)m * g.N + n0) = v;
       } else if constexpr (EPI == kAddF32) {
         f4* px = reinterpret_cast<f4*>(g.out_f32 + (int64_t)m * g.N + n0);
         *px = *px + v;
-      } else if constexpr (EPI == kGeluBf16) {
-        uint2 w2;
-        w2.x = (uint32_t)f32_to_bf16_bits(gelu_tanh(v[0])) | ((uint32_t)f32_to_bf16_bits(gelu_tanh(v[1])) << 16);
-        w2.y = (uint32_t)f32_to_bf16_bits(gelu_tanh(v[2])) | ((uint32_t)f32_to_bf16_bits(gelu_tanh(v[3])) << 16);
-        *reinterpret_cast<uint2*>(g.out_bf16 + (int64_t)m * g.N + n0) = w2;
       } else if (n0 < 2 * kW) {  // q, k rows (the 4 columns never straddle 512)
         uint2 w2;
         w2.x = (uint32_t)f32_to_bf16_bits(v[0]) | ((uint32_t)f32_to_bf16_bits(v[1]) << 16);
@@ -155,44 +206,40 @@ __global__ __launch_bounds__(256) void sel_gemm_kernel(GemmArgs g) {
 }
 
 // Split-K epilogue for the fp32 outputs (N = 256): out[m][n] (+)= sum over the splits
-// of part[s][m][n] + bias[n], in split order.  One thread per 4 columns.
+// of part[s][m][n], in split order.  One thread per 4 columns.
 template <int EPI>
-__global__ __launch_bounds__(256) void sel_splitk_kernel(const float* part, int splits, const uint16_t* bias,
-                                                         float* out, int M) {
+__global__ __launch_bounds__(256) void sel_splitk_kernel(const float* part, int splits, float* out, int M) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;  // f4 index
   if (i >= (int64_t)M * (kW / 4)) return;
-  const int n0 = 4 * (int)(i % (kW / 4));
   f4 v = *reinterpret_cast<const f4*>(part + 4 * i);
   for (int sp = 1; sp < splits; ++sp) v += *reinterpret_cast<const f4*>(part + (int64_t)sp * M * kW + 4 * i);
-#pragma unroll
-  for (int e = 0; e < 4; ++e) v[e] += bf16_to_f32(bias[n0 + e]);
   f4* po = reinterpret_cast<f4*>(out + 4 * i);
   if constexpr (EPI == kAddF32) *po = *po + v;
   else *po = v;
 }
 
-// One wave per row of 256: LayerNorm (eps 1e-5, gain and bias) to bf16.
-__global__ __launch_bounds__(256) void sel_layernorm_kernel(const float* x, const uint16_t* gain,
-                                                            const uint16_t* bias, uint16_t* out, int M) {
+__device__ __forceinline__ float wave_sum(float s) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
+  return s;
+}
+
+// One wave per row of 256: RMSNorm (eps 1e-6, gain) to bf16.
+__global__ __launch_bounds__(256) void sel_rmsnorm_kernel(const float* x, const uint16_t* gain, uint16_t* out,
+                                                          int M) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= M) return;
   const f4 v = *reinterpret_cast<const f4*>(x + (int64_t)row * kW + 4 * lane);
-  float s = v[0] + v[1] + v[2] + v[3];
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off);
-  const float mu = s * (1.0f / kW);
-  float q = 0.0f;
-#pragma unroll
-  for (int e = 0; e < 4; ++e) q += (v[e] - mu) * (v[e] - mu);
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) q += __shfl_xor(q, off);
-  const float rs = 1.0f / sqrtf(q * (1.0f / kW) + 1e-5f);
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int c = 4 * lane + e;
-    out[(int64_t)row * kW + c] = f32_to_bf16_bits((v[e] - mu) * rs * bf16_to_f32(gain[c]) + bf16_to_f32(bias[c]));
-  }
+  const float ms = wave_sum(v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3]) * (1.0f / kW);
+  const float rs = 1.0f / sqrtf(ms + kRmsEps);
+  uint2 w2;
+  const int c = 4 * lane;
+  w2.x = (uint32_t)f32_to_bf16_bits(v[0] * rs * bf16_to_f32(gain[c])) |
+         ((uint32_t)f32_to_bf16_bits(v[1] * rs * bf16_to_f32(gain[c + 1])) << 16);
+  w2.y = (uint32_t)f32_to_bf16_bits(v[2] * rs * bf16_to_f32(gain[c + 2])) |
+         ((uint32_t)f32_to_bf16_bits(v[3] * rs * bf16_to_f32(gain[c + 3])) << 16);
+  *reinterpret_cast<uint2*>(out + (int64_t)row * kW + c) = w2;
 }
 
 // Bidirectional attention.  Workgroup: 128 queries (wave w: queries 32 w .. 32 w + 31
@@ -408,27 +455,35 @@ __global__ __launch_bounds__(256) void sel_attn_merge_kernel(const float* part, 
   *reinterpret_cast<uint2*>(out + q * kW + h * kDh + 4 * c4) = w2;
 }
 
-// Partial column sums of x over chunks of 256 rows: part[chunk][c].  Thread
-// (columns 4 (tid % 64) .. + 3, row group tid / 64) adds every fourth row of the
-// chunk; the four row groups meet in LDS.
+// Partial column sums of the RMS-normalised rows over chunks of 256 rows:
+// part[chunk][c] = sum_t x[t][c] / rms(x[t]) (the final gain is applied to the
+// mean).  Wave rg takes every fourth row of the chunk, lane c4 columns 4 c4 .. + 3;
+// the four waves meet in LDS.
 __global__ __launch_bounds__(256) void sel_pool_kernel(const float* x, float* part, int T) {
   __shared__ float red[4][kW];
   const int tid = threadIdx.x, c4 = tid & 63, rg = tid >> 6, chunk = blockIdx.x;
   const int t0 = chunk * 256, t1 = min(T, t0 + 256);
   f4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-  for (int t = t0 + rg; t < t1; t += 4) acc += *reinterpret_cast<const f4*>(x + (int64_t)t * kW + 4 * c4);
+#pragma unroll 4
+  for (int t = t0 + rg; t < t1; t += 4) {
+    const f4 v = *reinterpret_cast<const f4*>(x + (int64_t)t * kW + 4 * c4);
+    const float ms = wave_sum(v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3]) * (1.0f / kW);
+    acc += v * (1.0f / sqrtf(ms + kRmsEps));
+  }
   *reinterpret_cast<f4*>(&red[rg][4 * c4]) = acc;
   __syncthreads();
   part[(int64_t)chunk * kW + tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
 }
 
 // One workgroup per layer l: the feature (thread c: the mean over the partial sums of
-// channel c), the layer's 5 logits (products reduced over the 256 channels), and the
-// argmax (the lowest action on ties; the depth action never at layer 0).
-__global__ __launch_bounds__(256) void sel_heads_kernel(const float* part, int n_chunks, int T, const uint16_t* w_head,
-                                                        const uint16_t* b_head, float* logits, int32_t* action) {
-  __shared__ float red[4][kActions];
+// channel c times the final gain, then the budget scale and shift), the layer's
+// logits (products reduced over the 256 channels), and the argmax (the lowest
+// action on ties; the depth action, index 0, never at layer 0 nor without depth).
+__global__ __launch_bounds__(256) void sel_heads_kernel(const float* part, int n_chunks, int T, const uint16_t* g_final,
+                                                        const float* film, const uint16_t* w_head,
+                                                        const uint16_t* b_head, int n_actions, int depth,
+                                                        float* logits, int32_t* action) {
+  __shared__ float red[4][kMaxActions];
   const int c = threadIdx.x, lane = c & 63, wv = c >> 6, l = blockIdx.x;
   float f4s[4] = {0.0f, 0.0f, 0.0f, 0.0f};  // four independent chains over the chunks
   int k = 0;
@@ -436,25 +491,20 @@ __global__ __launch_bounds__(256) void sel_heads_kernel(const float* part, int n
 #pragma unroll
     for (int u = 0; u < 4; ++u) f4s[u] += part[(int64_t)(k + u) * kW + c];
   for (; k < n_chunks; ++k) f4s[0] += part[(int64_t)k * kW + c];
-  const float f = (f4s[0] + f4s[1] + f4s[2] + f4s[3]) / (float)T;
-  float z[kActions];
-#pragma unroll
-  for (int a = 0; a < kActions; ++a) {
-    z[a] = f * bf16_to_f32(w_head[((int64_t)l * kW + c) * kActions + a]);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) z[a] += __shfl_xor(z[a], off);
+  float f = (f4s[0] + f4s[1] + f4s[2] + f4s[3]) / (float)T * bf16_to_f32(g_final[c]);
+  if (film) f = fmaf(f, film[c], f) + film[kW + c];
+  for (int a = 0; a < n_actions; ++a) {
+    const float z = wave_sum(f * bf16_to_f32(w_head[((int64_t)l * n_actions + a) * kW + c]));
+    if (lane == 0) red[wv][a] = z;
   }
-  if (lane == 0)
-#pragma unroll
-    for (int a = 0; a < kActions; ++a) red[wv][a] = z[a];
   __syncthreads();
   if (c == 0) {
     int best = 0;
-    float zb = 0.0f;
-    for (int a = 0; a < kActions; ++a) {
-      float v = red[0][a] + red[1][a] + red[2][a] + red[3][a] + bf16_to_f32(b_head[l * kActions + a]);
-      if (l == 0 && a == 0) v = -INFINITY;
-      if (logits) logits[l * kActions + a] = v;
+    float zb = -INFINITY;
+    for (int a = 0; a < n_actions; ++a) {
+      float v = red[0][a] + red[1][a] + red[2][a] + red[3][a] + bf16_to_f32(b_head[l * n_actions + a]);
+      if (a == 0 && (l == 0 || !depth)) v = -INFINITY;
+      if (logits) logits[l * n_actions + a] = v;
       if (a == 0 || v > zb) {
         best = a;
         zb = v;
@@ -466,25 +516,26 @@ __global__ __launch_bounds__(256) void sel_heads_kernel(const float* part, int n
 
 // Packed weight offsets (bf16 elements).
 struct SelOffsets {
-  int64_t w_in, b_in, blk[2], w_head, b_head, total;
+  int64_t w_in, blk[2], g_final, w_head, b_head, total;
 };
-constexpr int64_t kBlockElems = 2 * kW + (int64_t)3 * kW * kW + 3 * kW + (int64_t)kW * kW + kW + 2 * kW +
-                                (int64_t)kFfn * kW + kFfn + (int64_t)kW * kFfn + kW;
+// per block: g_attn, w_qkv [768][256], w_o [256][256], g_ffn, w_gate|w_up [2048][256], w_down [256][1024]
+constexpr int64_t kBlockElems = kW + (int64_t)3 * kW * kW + (int64_t)kW * kW + kW + (int64_t)2 * kFfn * kW +
+                                (int64_t)kW * kFfn;
 
-SelOffsets sel_offsets(int d_model, int L) {
+SelOffsets sel_offsets(int d_model, int L, int A) {
   SelOffsets o;
   o.w_in = 0;
-  o.b_in = (int64_t)kW * d_model;
-  o.blk[0] = o.b_in + kW;
+  o.blk[0] = (int64_t)kW * d_model;
   o.blk[1] = o.blk[0] + kBlockElems;
-  o.w_head = o.blk[1] + kBlockElems;
-  o.b_head = o.w_head + (int64_t)L * kW * kActions;
-  o.total = o.b_head + (int64_t)L * kActions;
+  o.g_final = o.blk[1] + kBlockElems;
+  o.w_head = o.g_final + kW;
+  o.b_head = o.w_head + (int64_t)L * A * kW;
+  o.total = o.b_head + (int64_t)L * A;
   return o;
 }
 
 struct SelWorkspace {
-  int64_t x, h, qk, vt, f1, part, splitk, attn, total;  // byte offsets
+  int64_t x, h, qk, vt, f1, rope, part, splitk, attn, total;  // byte offsets
   int vt_pitch;
 };
 
@@ -503,9 +554,9 @@ int sel_attn_splits(int T, int* key_len) {
 }
 
 // Split-K for the long-K GEMMs with 256 output columns (the input map, K = d_model,
-// and the second feed-forward matrix, K = 1024) when their 64-row tiles alone
-// would give few workgroups: enough splits for about 512 workgroups, at most 16,
-// each split at least 8 k-steps of 32.
+// and the down projection, K = 1024) when their 64-row tiles alone would give few
+// workgroups: enough splits for about 512 workgroups, at most 16, each split at
+// least 8 k-steps of 32.
 constexpr int kSplitMax = 16;
 int sel_splits(int T, int K) {
   const int row_blocks = (T + 63) / 64;
@@ -519,12 +570,13 @@ SelWorkspace sel_workspace(int T) {
   SelWorkspace w;
   const int Tp = (T + 31) / 32 * 32;
   w.vt_pitch = Tp;
-  w.x = 0;                                              // fp32 [T][256] residual stream
+  w.x = 0;                                                   // fp32 [T][256] residual stream
   w.h = kvk::round256(w.x + (int64_t)Tp * kW * 4);           // bf16 [T][256] normalised / attention output
-  w.qk = kvk::round256(w.h + (int64_t)Tp * kW * 2);          // bf16 [T][512]
+  w.qk = kvk::round256(w.h + (int64_t)Tp * kW * 2);          // bf16 [T][512] rotated q | k
   w.vt = kvk::round256(w.qk + (int64_t)Tp * 2 * kW * 2);     // bf16 [256][Tp]
-  w.f1 = kvk::round256(w.vt + (int64_t)kW * Tp * 2);         // bf16 [T][1024]
-  w.part = kvk::round256(w.f1 + (int64_t)Tp * kFfn * 2);     // fp32 [chunks][256]
+  w.f1 = kvk::round256(w.vt + (int64_t)kW * Tp * 2);         // bf16 [T][1024] SiLU(gate) * up
+  w.rope = kvk::round256(w.f1 + (int64_t)Tp * kFfn * 2);     // fp32 [T][32] (cos, sin)
+  w.part = kvk::round256(w.rope + (int64_t)Tp * (kDh / 2) * 8);  // fp32 [chunks][256]
   w.splitk = kvk::round256(w.part + (int64_t)((T + 255) / 256) * kW * 4);  // fp32 [splits][T][256]
   const int max_splits = std::min(kSplitMax, (512 + (T + 63) / 64 - 1) / ((T + 63) / 64));
   w.attn = kvk::round256(w.splitk + (max_splits > 1 ? (int64_t)max_splits * T * kW * 4 : 0));  // fp32 [splits][T][4][kRec]
@@ -548,23 +600,30 @@ extern "C" kvk_status kvk_selector_workspace_bytes(int32_t d_model, int32_t n_la
   return KVK_OK;
 }
 
-extern "C" int64_t kvk_selector_weight_elems(int32_t d_model, int32_t n_layers) {
-  return sel_offsets(d_model, n_layers).total;
+extern "C" int64_t kvk_selector_weight_elems(int32_t d_model, int32_t n_layers, int32_t n_actions) {
+  if (d_model < 32 || d_model % 32 || n_layers < 1 || n_layers > KVK_MAX_LAYERS || n_actions < 2 ||
+      n_actions > kMaxActions)
+    return -1;
+  return sel_offsets(d_model, n_layers, n_actions).total;
 }
 
-extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, const void* weights,
-                                           const void* emb, int32_t n_tokens, float* logits, int32_t* actions,
+extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, int32_t n_actions, int32_t depth,
+                                           const void* weights, const void* emb, int32_t n_tokens,
+                                           const float* film, float* logits, int32_t* actions,
                                            void* workspace, size_t ws_bytes, hipStream_t stream) {
   size_t need = 0;
   kvk_status st = kvk_selector_workspace_bytes(d_model, n_layers, n_tokens, &need);
   if (st != KVK_OK) return st;
+  if (n_actions < 2 || n_actions > kMaxActions)
+    return fail(KVK_ERR_INVALID, "selector: n_actions %d outside 2..%d", n_actions, kMaxActions);
+  if (depth != 0 && depth != 1) return fail(KVK_ERR_INVALID, "selector: depth flag %d (0 or 1)", depth);
   if (!weights || !emb || !actions || !workspace) return fail(KVK_ERR_INVALID, "selector: NULL buffer");
   if (need > ws_bytes) return fail(KVK_ERR_BUFFER, "selector: workspace %zu bytes < %zu needed", ws_bytes, need);
   if ((reinterpret_cast<uintptr_t>(weights) & 15) || (reinterpret_cast<uintptr_t>(emb) & 15) ||
       (reinterpret_cast<uintptr_t>(workspace) & 255) || (reinterpret_cast<uintptr_t>(logits) & 3) ||
-      (reinterpret_cast<uintptr_t>(actions) & 3))
+      (reinterpret_cast<uintptr_t>(actions) & 3) || (reinterpret_cast<uintptr_t>(film) & 3))
     return fail(KVK_ERR_INVALID, "selector: misaligned buffer (weights/emb 16 B, workspace 256 B)");
-  const SelOffsets O = sel_offsets(d_model, n_layers);
+  const SelOffsets O = sel_offsets(d_model, n_layers, n_actions);
   const SelWorkspace Wk = sel_workspace(n_tokens);
   const uint16_t* wp = static_cast<const uint16_t*>(weights);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
@@ -573,16 +632,17 @@ extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, co
   uint16_t* qk = reinterpret_cast<uint16_t*>(ws + Wk.qk);
   uint16_t* vt = reinterpret_cast<uint16_t*>(ws + Wk.vt);
   uint16_t* f1 = reinterpret_cast<uint16_t*>(ws + Wk.f1);
+  float2* rope = reinterpret_cast<float2*>(ws + Wk.rope);
   float* part = reinterpret_cast<float*>(ws + Wk.part);
   const int T = n_tokens;
-  auto gemm = [&](int epi, const uint16_t* a, int64_t w_off, int64_t b_off, int N, int K) {
+  auto gemm = [&](int epi, const uint16_t* a, int64_t w_off, int N, int K) {
     GemmArgs g;
     g.a = a;
     g.w = wp + w_off;
-    g.bias = wp + b_off;
     g.out_f32 = x;
-    g.out_bf16 = epi == kGeluBf16 ? f1 : qk;
+    g.out_bf16 = epi == kSwiGlu ? f1 : qk;
     g.vt = vt;
+    g.rope = rope;
     g.M = T;
     g.N = N;
     g.K = K;
@@ -594,26 +654,27 @@ extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, co
     switch (epi) {
       case kStoreF32: hipLaunchKernelGGL(sel_gemm_kernel<kStoreF32>, grid, blk, 0, stream, g); break;
       case kAddF32: hipLaunchKernelGGL(sel_gemm_kernel<kAddF32>, grid, blk, 0, stream, g); break;
-      case kGeluBf16: hipLaunchKernelGGL(sel_gemm_kernel<kGeluBf16>, grid, blk, 0, stream, g); break;
+      case kSwiGlu: hipLaunchKernelGGL(sel_gemm_kernel<kSwiGlu>, grid, blk, 0, stream, g); break;
       default: hipLaunchKernelGGL(sel_gemm_kernel<kQkv>, grid, blk, 0, stream, g); break;
     }
     if (splits > 1) {
       const dim3 rgrid((unsigned)(((int64_t)T * (kW / 4) + 255) / 256));
       if (epi == kAddF32)
-        hipLaunchKernelGGL(sel_splitk_kernel<kAddF32>, rgrid, blk, 0, stream, g.part, splits, g.bias, x, T);
+        hipLaunchKernelGGL(sel_splitk_kernel<kAddF32>, rgrid, blk, 0, stream, g.part, splits, x, T);
       else
-        hipLaunchKernelGGL(sel_splitk_kernel<kStoreF32>, rgrid, blk, 0, stream, g.part, splits, g.bias, x, T);
+        hipLaunchKernelGGL(sel_splitk_kernel<kStoreF32>, rgrid, blk, 0, stream, g.part, splits, x, T);
     }
   };
   const dim3 rows((unsigned)((T + 3) / 4)), b256(256);
-  gemm(kStoreF32, static_cast<const uint16_t*>(emb), O.w_in, O.b_in, kW, d_model);
+  hipLaunchKernelGGL(sel_rope_kernel, dim3((unsigned)(((int64_t)T * (kDh / 2) + 255) / 256)), b256, 0, stream,
+                     rope, T);
+  gemm(kStoreF32, static_cast<const uint16_t*>(emb), O.w_in, kW, d_model);
   for (int bi = 0; bi < 2; ++bi) {
-    int64_t p = O.blk[bi];
-    const int64_t ln1_g = p, ln1_b = p + kW, w_qkv = p + 2 * kW, b_qkv = w_qkv + (int64_t)3 * kW * kW,
-                  w_o = b_qkv + 3 * kW, b_o = w_o + (int64_t)kW * kW, ln2_g = b_o + kW, ln2_b = ln2_g + kW,
-                  w_1 = ln2_b + kW, b_1 = w_1 + (int64_t)kFfn * kW, w_2 = b_1 + kFfn, b_2 = w_2 + (int64_t)kW * kFfn;
-    hipLaunchKernelGGL(sel_layernorm_kernel, rows, b256, 0, stream, x, wp + ln1_g, wp + ln1_b, hbuf, T);
-    gemm(kQkv, hbuf, w_qkv, b_qkv, 3 * kW, kW);
+    const int64_t p = O.blk[bi];
+    const int64_t g_attn = p, w_qkv = p + kW, w_o = w_qkv + (int64_t)3 * kW * kW, g_ffn = w_o + (int64_t)kW * kW,
+                  w_gu = g_ffn + kW, w_down = w_gu + (int64_t)2 * kFfn * kW;
+    hipLaunchKernelGGL(sel_rmsnorm_kernel, rows, b256, 0, stream, x, wp + g_attn, hbuf, T);
+    gemm(kQkv, hbuf, w_qkv, 3 * kW, kW);
     {
       int key_len = 0;
       const int sp = sel_attn_splits(T, &key_len);
@@ -624,15 +685,15 @@ extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, co
         hipLaunchKernelGGL(sel_attn_merge_kernel, dim3((unsigned)(((int64_t)T * kHeads * (kDh / 4) + 255) / 256)),
                            b256, 0, stream, apart, sp, T, hbuf);
     }
-    gemm(kAddF32, hbuf, w_o, b_o, kW, kW);
-    hipLaunchKernelGGL(sel_layernorm_kernel, rows, b256, 0, stream, x, wp + ln2_g, wp + ln2_b, hbuf, T);
-    gemm(kGeluBf16, hbuf, w_1, b_1, kFfn, kW);
-    gemm(kAddF32, f1, w_2, b_2, kW, kFfn);
+    gemm(kAddF32, hbuf, w_o, kW, kW);
+    hipLaunchKernelGGL(sel_rmsnorm_kernel, rows, b256, 0, stream, x, wp + g_ffn, hbuf, T);
+    gemm(kSwiGlu, hbuf, w_gu, 2 * kFfn, kW);
+    gemm(kAddF32, f1, w_down, kW, kFfn);
   }
   const int chunks = (T + 255) / 256;
   hipLaunchKernelGGL(sel_pool_kernel, dim3((unsigned)chunks), b256, 0, stream, x, part, T);
-  hipLaunchKernelGGL(sel_heads_kernel, dim3((unsigned)n_layers), b256, 0, stream, part, chunks, T, wp + O.w_head,
-                     wp + O.b_head, logits, actions);
+  hipLaunchKernelGGL(sel_heads_kernel, dim3((unsigned)n_layers), b256, 0, stream, part, chunks, T, wp + O.g_final,
+                     film, wp + O.w_head, wp + O.b_head, n_actions, depth, logits, actions);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "selector launch: %s", hipGetErrorString(e));
   return KVK_OK;

@@ -73,9 +73,9 @@ def load() -> ctypes.CDLL:
             "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
             "kvk_append_token": (I32, [P, I32, I32, P, P, I32, I32, P, P]),
             "kvk_snapkv_workspace_bytes": (I32, [P, I32, ctypes.POINTER(ctypes.c_size_t)]),
-            "kvk_selector_weight_elems": (I64, [I32, I32]),
+            "kvk_selector_weight_elems": (I64, [I32, I32, I32]),
             "kvk_selector_workspace_bytes": (I32, [I32, I32, I32, ctypes.POINTER(ctypes.c_size_t)]),
-            "kvk_selector_forward": (I32, [I32, I32, P, P, I32, P, P, P, ctypes.c_size_t, P]),
+            "kvk_selector_forward": (I32, [I32, I32, I32, I32, P, P, I32, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_snapkv_select": (I32, [P, I32, P, P, I32, I32, F, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_attention": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_splits": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P]),
@@ -356,11 +356,16 @@ def snapkv_select(t: Table, layer: int, k: torch.Tensor, q_obs: torch.Tensor, n_
                                     _stream(stream)))
 
 
-SELECTOR_ACTIONS = [(1, 16), (0, 16), (0, 8), (0, 4), (0, 2)]  # (inherit, bits) by action index
+# Composed action space (eq. (3)): index 0 = inherit, 1 + 4 j + k = produce with
+# kept width r / 2^j at 16 / 2^k bits; a GQA selector uses the first five.
+SELECTOR_ACTIONS = [(1, 1, 16)] + [(0, 1 << j, 16 >> k) for j in range(4) for k in range(4)]
+SELECTOR_ACTIONS_GQA = 5
 
 
-def selector_weight_elems(d_model: int, n_layers: int) -> int:
-    return int(load().kvk_selector_weight_elems(d_model, n_layers))
+def selector_weight_elems(d_model: int, n_layers: int, n_actions: int = SELECTOR_ACTIONS_GQA) -> int:
+    n = int(load().kvk_selector_weight_elems(d_model, n_layers, n_actions))
+    _need(n > 0, f"selector sizes d_model {d_model}, n_layers {n_layers}, n_actions {n_actions}")
+    return n
 
 
 def selector_workspace_bytes(d_model: int, n_layers: int, n_tokens: int) -> int:
@@ -371,18 +376,26 @@ def selector_workspace_bytes(d_model: int, n_layers: int, n_tokens: int) -> int:
 
 def selector_forward(d_model: int, n_layers: int, weights: torch.Tensor, emb: torch.Tensor,
                      actions: torch.Tensor, workspace: torch.Tensor, logits: Optional[torch.Tensor] = None,
-                     stream=None):
+                     n_actions: int = SELECTOR_ACTIONS_GQA, depth: bool = True,
+                     film: Optional[torch.Tensor] = None, stream=None):
     """emb [n_tokens, d_model] bf16; weights packed bf16 (see kvk.h); actions int32
-    [n_layers]; logits (optional) fp32 [n_layers, 5]."""
+    [n_layers]; logits (optional) fp32 [n_layers, n_actions]; film (optional) fp32
+    [2, 256]: the budget scale gamma and shift beta applied to the pooled feature."""
     _need(emb.dtype == torch.bfloat16 and emb.is_contiguous() and emb.dim() == 2 and emb.shape[1] == d_model,
           "emb must be contiguous bf16 [n_tokens, d_model]")
     _need(weights.dtype == torch.bfloat16 and weights.is_contiguous() and
-          weights.numel() == selector_weight_elems(d_model, n_layers), "weights must be the packed bf16 vector")
+          weights.numel() == selector_weight_elems(d_model, n_layers, n_actions),
+          "weights must be the packed bf16 vector")
     _need(actions.dtype == torch.int32 and actions.numel() == n_layers, "actions must be int32 [n_layers]")
     if logits is not None:
-        _need(logits.dtype == torch.float32 and logits.numel() == n_layers * 5, "logits must be fp32 [n_layers, 5]")
-    _check(load().kvk_selector_forward(d_model, n_layers, _ptr(weights), _ptr(emb), emb.shape[0], _ptr(logits),
-                                       _ptr(actions), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+        _need(logits.dtype == torch.float32 and logits.is_contiguous() and logits.numel() == n_layers * n_actions,
+              "logits must be fp32 [n_layers, n_actions]")
+    if film is not None:
+        _need(film.dtype == torch.float32 and film.is_contiguous() and film.numel() == 2 * 256,
+              "film must be fp32 [2, 256]")
+    _check(load().kvk_selector_forward(d_model, n_layers, n_actions, 1 if depth else 0, _ptr(weights), _ptr(emb),
+                                       emb.shape[0], _ptr(film), _ptr(logits), _ptr(actions), _ptr(workspace),
+                                       _nbytes(workspace), _stream(stream)))
 
 
 def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_stored: int,
