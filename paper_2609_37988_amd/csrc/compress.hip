@@ -536,6 +536,7 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
   if ((reinterpret_cast<uintptr_t>(arena) & 15) || (reinterpret_cast<uintptr_t>(k) & 15) ||
       (reinterpret_cast<uintptr_t>(v) & 15))
     return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
+  if (kvk_status st = check_gpu_buffers({k, v, keep_idx, arena}, "kvk_compress_layer")) return st;
   if (d.kind == KVK_MLA)
     return mla_compress_layer(t, layer, k, v, in_dtype, n_tokens, keep_idx, arena, stream);
   if (!t->seq.empty()) {  // per-sequence plans: each sequence's own table and arena
@@ -606,6 +607,11 @@ extern "C" kvk_status kvk_append_token(const kvk_table* t, int32_t l0, int32_t l
   if ((reinterpret_cast<uintptr_t>(arena) & 15) || (reinterpret_cast<uintptr_t>(k) & 15) ||
       (reinterpret_cast<uintptr_t>(v) & 15))
     return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
+  bool stores = false;  // an anchor in the range (of some sequence's plan)
+  for (size_t i = 0; i < (t->seq.empty() ? 1 : t->seq.size()); ++i)
+    for (int l = l0; l < l1; ++l) stores |= !(t->seq.empty() ? t : t->seq[i])->plan[l].inherit;
+  if (!stores) return KVK_OK;  // only inheritors: nothing is stored
+  if (kvk_status st = check_gpu_buffers({k, v, arena}, "kvk_append_token")) return st;
   if (d.kind == KVK_MLA) return mla_append_token(t, l0, l1, k, v, in_dtype, n_stored, arena, stream);
   return append_gqa(t, l0, l1, k, v, in_dtype, n_stored, arena, stream);
 }
@@ -680,6 +686,7 @@ extern "C" kvk_status kvk_debug_dequantize(const kvk_table* t, int32_t layer, in
   if (n_stored < 0 || n_stored > t->cap)
     return fail(KVK_ERR_INVALID, "n_stored %d outside 0..%d", n_stored, t->cap);
   if (n_stored == 0) return KVK_OK;
+  if (kvk_status st = check_gpu_buffers({arena, k_out, v_out}, "kvk_debug_dequantize")) return st;
   if (d.kind == KVK_MLA) return mla_debug_dequantize(t, layer, n_stored, arena, k_out, v_out, stream);
   if (!t->seq.empty()) {
     const int64_t per = (int64_t)d.n_kv_heads * n_stored * d.head_dim;

@@ -953,9 +953,11 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   const int64_t split_target = gqa_split_target(t, l0, l1);
   // One work item per distinct anchor read by the range (§2.1 depth sharing): per
   // anchor for all sequences, or per (sequence, anchor) under per-sequence plans.
-  std::vector<DecodeItem> items;
+  SmallVec<DecodeItem, kMaxItems> items;
   const int ngroups = batched ? d.batch : 1;
-  std::vector<int32_t> l_item((size_t)ngroups * nl), l_slot((size_t)ngroups * nl);
+  SmallVec<int32_t, kMaxItems> l_item, l_slot;
+  l_item.resize((size_t)ngroups * nl);
+  l_slot.resize((size_t)ngroups * nl);
   int64_t ws_floats = 0;
   auto add_group = [&](const kvk_table* s, int g, int b0, int nb, int64_t base) {
     int item_of_anchor[KVK_MAX_LAYERS];
@@ -998,11 +1000,15 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   // unpacking makes them compute-bound) first, so that the launch ends on short
   // waves.  Item indices follow the new order; wave_begin stays increasing.
   auto cost_rank = [](int bits) { return bits == 2 ? 0 : (bits == 4 ? 1 : (bits == 8 ? 2 : 3)); };
-  std::vector<int> order(n_it), new_index(n_it);
-  for (int k = 0; k < n_it; ++k) order[k] = k;
-  std::stable_sort(order.begin(), order.end(),
-                   [&](int x, int y) { return cost_rank(items[x].bits) < cost_rank(items[y].bits); });
-  std::vector<DecodeItem> sorted(n_it);
+  SmallVec<int, kMaxItems> order, new_index;
+  order.resize(n_it);
+  new_index.resize(n_it);
+  int n_ord = 0;
+  for (int r = 0; r < 4; ++r)  // a stable counting sort by rank
+    for (int k = 0; k < n_it; ++k)
+      if (cost_rank(items[k].bits) == r) order[n_ord++] = k;
+  SmallVec<DecodeItem, kMaxItems> sorted;
+  sorted.resize(n_it);
   int64_t waves = 0;
   for (int k = 0; k < n_it; ++k) {
     DecodeItem it = items[order[k]];
@@ -1064,7 +1070,7 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   P.qs = d.qscheme;
   P.head_dim = D;
   P.any_blocks = nbf > 0 && waves > 0;
-  return KVK_OK;
+  return check_gpu_buffers({q, arena, out, workspace}, "decode");
 }
 
 kvk_status launch_d1(const DecodePlan& P, hipStream_t st) {
@@ -1125,7 +1131,7 @@ kvk_status mla_check(const kvk_table* t, int32_t l0, int32_t l1, const void* q, 
   mla_workspace(t, l0, l1, &ws);
   if ((size_t)ws.total > ws_bytes)
     return fail(KVK_ERR_BUFFER, "workspace %zu bytes < %lld needed", ws_bytes, (long long)ws.total);
-  return KVK_OK;
+  return check_gpu_buffers({q, w_uk, w_uv, arena, out, workspace}, "decode");
 }
 
 }  // namespace

@@ -3,6 +3,7 @@
 
 #include <cstdarg>
 #include <cstdint>
+#include <initializer_list>
 #include <string>
 #include <vector>
 
@@ -34,6 +35,43 @@ void set_error(const char* fmt, ...);
 kvk_status fail(kvk_status st, const char* fmt, ...);
 
 inline int64_t round256(int64_t n) { return (n + 255) / 256 * 256; }
+
+// Every buffer a kernel dereferences must be memory the HIP runtime maps for the GPU
+// (a device allocation, or pinned or managed host memory): a pageable host pointer
+// would fault the GPU.  Checked before any launch; NULL entries (optional buffers)
+// are skipped.  `what` names the entry point in the error message.
+kvk_status check_gpu_buffers(std::initializer_list<const void*> ptrs, const char* what);
+
+// A list whose first N elements live inside the object (no heap allocation while
+// it holds at most N: the one-plan decode path, bounded by the layer count) and
+// which moves to the heap beyond that (per-sequence plans).  T trivially copyable.
+template <class T, int N>
+struct SmallVec {
+  T local[N];
+  std::vector<T> big;
+  T* p = local;
+  size_t n = 0;
+  void resize(size_t m) {
+    if (m > (size_t)N) {
+      big.resize(m);
+      p = big.data();
+    }
+    n = m;
+  }
+  void push_back(const T& v) {
+    if (n < (size_t)N && big.empty()) {
+      local[n++] = v;
+      return;
+    }
+    if (big.empty()) big.assign(local, local + n);
+    big.push_back(v);
+    p = big.data();
+    ++n;
+  }
+  T& operator[](size_t i) { return p[i]; }
+  const T& operator[](size_t i) const { return p[i]; }
+  size_t size() const { return n; }
+};
 
 // Bytes of one 32-token block of a GQA stream with `bits`-bit codes.
 int64_t gqa_block_bytes(int32_t head_dim, int32_t bits, int32_t qscheme);

@@ -623,6 +623,8 @@ extern "C" kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, in
       (reinterpret_cast<uintptr_t>(workspace) & 255) || (reinterpret_cast<uintptr_t>(logits) & 3) ||
       (reinterpret_cast<uintptr_t>(actions) & 3) || (reinterpret_cast<uintptr_t>(film) & 3))
     return fail(KVK_ERR_INVALID, "selector: misaligned buffer (weights/emb 16 B, workspace 256 B)");
+  if (kvk_status st2 = check_gpu_buffers({weights, emb, film, logits, actions, workspace}, "kvk_selector_forward"))
+    return st2;
   const SelOffsets O = sel_offsets(d_model, n_layers, n_actions);
   const SelWorkspace Wk = sel_workspace(n_tokens);
   const uint16_t* wp = static_cast<const uint16_t*>(weights);

@@ -401,6 +401,8 @@ extern "C" kvk_status kvk_snapkv_select(const kvk_table* t, int32_t layer, const
   const SnapSizes s = snap_sizes(t, n_tokens);
   const int64_t bh = (int64_t)d.batch * d.n_kv_heads;
   if (bh > 65535 || s.P > 0x7fffffff) return fail(KVK_ERR_UNSUPPORTED, "snapkv: grid too large");
+  if (kvk_status st2 = check_gpu_buffers({k, q_obs, keep_out, importance_out, workspace}, "kvk_snapkv_select"))
+    return st2;
   SnapArgs a;
   a.k = static_cast<const uint16_t*>(k);
   a.q = static_cast<const uint16_t*>(q_obs);

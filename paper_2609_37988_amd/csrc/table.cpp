@@ -4,7 +4,8 @@
 // each action's cost in bits per token, eq. (2) the plan's compression ratio
 // against the bf16 GQA cache, eq. (3) the action set; §2.1 defines anchors (a
 // layer owns a cache or inherits from the nearest anchor before it).  The
-// storage accounting follows App. C.3.  Nothing in this file touches a device.
+// storage accounting follows App. C.3.  Nothing in this file launches work on a
+// device; it only asks the HIP runtime whether a buffer is GPU memory.
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -35,6 +36,20 @@ kvk_status fail(kvk_status st, const char* fmt, ...) {
   return st;
 }
 
+kvk_status check_gpu_buffers(std::initializer_list<const void*> ptrs, const char* what) {
+  int i = 0;
+  for (const void* p : ptrs) {
+    ++i;
+    if (!p) continue;
+    hipPointerAttribute_t a;
+    const hipError_t e = hipPointerGetAttributes(&a, p);
+    if (e != hipSuccess) (void)hipGetLastError();  // the query's error is not the caller's
+    if (e != hipSuccess || a.type == hipMemoryTypeUnregistered)
+      return fail(KVK_ERR_INVALID, "%s: buffer argument %d (%p) is not GPU-accessible memory", what, i, p);
+  }
+  return KVK_OK;
+}
+
 int64_t gqa_block_bytes(int32_t head_dim, int32_t bits, int32_t qscheme) {
   const int64_t D = head_dim;
   if (bits == 16) return 128 * D;                 // bf16 K and V, 32 tokens
@@ -53,8 +68,9 @@ int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1) {
   // table counts every sequence's distinct anchors.
   constexpr int64_t kSplitWaves = 4096;
   int64_t total = 0;
-  const std::vector<kvk_table*> one(1, const_cast<kvk_table*>(t));
-  for (const kvk_table* s : t->seq.empty() ? one : t->seq) {
+  const size_t n_seq = t->seq.empty() ? 1 : t->seq.size();
+  for (size_t i = 0; i < n_seq; ++i) {
+    const kvk_table* s = t->seq.empty() ? t : t->seq[i];
     bool seen[KVK_MAX_LAYERS] = {};
     for (int l = l0; l < l1; ++l) {
       const int32_t a = s->info.anchor_of[l];

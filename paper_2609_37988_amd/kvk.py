@@ -120,8 +120,11 @@ def _check(st: int):
 
 
 def _ptr(t: Optional[torch.Tensor]):
+    """The device address of a GPU tensor (every buffer the library's kernels read or
+    write); a tensor in host memory is refused here, before the call."""
     if t is None:
         return None
+    _need(t.is_cuda, "buffers must be GPU tensors (got a tensor on the host)")
     return ctypes.c_void_p(t.data_ptr())
 
 

@@ -358,3 +358,27 @@ def test_batched_table_rejects_bad_input():
     u = kvk.layer_table(d, kvk.make_plan([(0, 4), (1, 16)]))
     with pytest.raises(kvk.KvkError):
         kvk.table_sequence_query(u, 0)
+
+
+def test_host_buffers_are_refused_before_any_launch():
+    """A kernel given a pageable host address would fault the GPU: the binding refuses
+    host tensors, and the C entry points refuse buffers the HIP runtime does not map
+    for the GPU (checked after the size checks, before any launch)."""
+    import numpy as np
+    import torch
+    d = kvk.make_dims(kvk.GQA, 1, 4, 1, 64, batch=1, max_tokens=64)
+    t = kvk.layer_table(d, kvk.make_plan([(0, 8)]))
+    k = torch.zeros(1, 1, 64, 64, dtype=torch.bfloat16)
+    arena = torch.zeros(kvk.table_query(t).arena_bytes, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="GPU tensors"):
+        kvk.compress_layer(t, 0, k, k, 64, None, arena)
+    host = np.zeros(1 << 16, dtype=np.uint8)
+    base = host.ctypes.data + (-host.ctypes.data) % 256  # aligned host addresses
+    P = ctypes.c_void_p
+    hk, ha = P(base), P(base + 16384)
+    _raw(kvk.ERR_INVALID, "kvk_compress_layer", t.handle, 0, hk, hk, kvk.BF16, 64, None, ha, None)
+    assert "GPU-accessible" in kvk.last_error()
+    _raw(kvk.ERR_INVALID, "kvk_decode_attention", t.handle, 0, 1, hk, kvk.BF16, 64, 0.1, None, None, ha, ha,
+         P(base + 32768), 1 << 14, None)
+    assert "GPU-accessible" in kvk.last_error()
+    _raw(kvk.ERR_INVALID, "kvk_append_token", t.handle, 0, 1, hk, hk, kvk.BF16, 10, ha, None)
