@@ -463,6 +463,27 @@ kvk_status kvk_decode_merge(const kvk_table* table, int32_t layer_begin, int32_t
                             const void* workspace, size_t workspace_bytes, float* out,
                             hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): kvk_decode_attention with
+ * no workspace argument.  The split partials (and, for MLA tables, the absorbed
+ * queries) go to a static device array of KVK_NOALLOC_SCRATCH_BYTES that the
+ * library holds on each GPU it runs on, from the first call on that GPU until the
+ * process ends.  The call allocates nothing (no hipMalloc, no host heap on this
+ * path) and runs the same kernels, so its output equals kvk_decode_attention's.
+ * Arguments as for kvk_decode_attention; the GPU is the stream's (the current
+ * device for the null stream).
+ * Every call on one GPU shares that GPU's scratch: calls that overlap on one GPU
+ * (on different streams, or from different threads) race.
+ * Errors: those of kvk_decode_attention; KVK_ERR_UNSUPPORTED for a per-sequence
+ * table, or when the layer range needs more than KVK_NOALLOC_SCRATCH_BYTES of
+ * scratch (kvk_workspace_bytes of the range; decode fewer layers per call), before
+ * any launch. */
+#define KVK_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+kvk_status kvk_decode_attention_noalloc(const kvk_table* table, int32_t layer_begin, int32_t layer_end,
+                                        const void* q, int32_t q_dtype, int32_t n_stored, float scale,
+                                        const void* w_uk, const void* w_uv, const void* arena, float* out,
+                                        hipStream_t stream);
+
 /* Algorithmic bytes one decode call over [layer_begin, layer_end) reads from the
  * arena with n_stored tokens per stream: each distinct anchor's full blocks and
  * bf16 tail tokens, counted once (split partials, queries, MLA up-projection

@@ -27,6 +27,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "kvk_device.h"
@@ -1198,6 +1199,71 @@ extern "C" kvk_status kvk_decode_merge(const kvk_table* t, int32_t l0, int32_t l
                           const_cast<void*>(workspace), ws_bytes, P);
   if (st != KVK_OK) return st;
   return launch_c1(P, stream);
+}
+
+// ---------------------------------------------------------------------------
+// The allocation-free decode entry point: kvk_decode_attention with the split
+// partials (and, for MLA tables, the absorbed queries) in a file-scope device array
+// instead of a caller workspace.  Each GPU holds its own copy of the array (from the
+// first call on it until the process ends); its address on a device is looked up
+// once, with that device current, and kept.  Nothing in the scratch needs clearing:
+// every partial the merge reads is written by the split phase of the same call.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) uint8_t scratch[KVK_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+kvk_status scratch_on(hipStream_t stream, void** out) {
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+  int dev = cur;
+  if (stream) {
+    e = hipStreamGetDevice(stream, &dev);
+    if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "hipStreamGetDevice: %s", hipGetErrorString(e));
+  }
+  if (dev < 0 || dev >= kMaxDevices) return fail(KVK_ERR_UNSUPPORTED, "device %d beyond %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess)
+      return fail(KVK_ERR_DEVICE, "hipSetDevice(%d): %s", dev, hipGetErrorString(e));
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !p)
+      return fail(KVK_ERR_DEVICE, "scratch address on device %d: %s", dev, hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return KVK_OK;
+}
+
+}  // namespace
+
+extern "C" kvk_status kvk_decode_attention_noalloc(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
+                                                   int32_t q_dtype, int32_t n_stored, float scale,
+                                                   const void* w_uk, const void* w_uv, const void* arena,
+                                                   float* out, hipStream_t stream) {
+  if (!t) return fail(KVK_ERR_INVALID, "decode: NULL table");
+  if (!t->seq.empty())
+    return fail(KVK_ERR_UNSUPPORTED, "the allocation-free decode takes one-plan tables only");
+  size_t need = 0;
+  kvk_status st = kvk_workspace_bytes(t, l0, l1, &need);
+  if (st != KVK_OK) return st;
+  if (need > (size_t)KVK_NOALLOC_SCRATCH_BYTES)
+    return fail(KVK_ERR_UNSUPPORTED,
+                "layers [%d, %d) need %zu bytes of scratch; the static scratch holds %zu: decode fewer "
+                "layers per call",
+                l0, l1, need, (size_t)KVK_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  st = scratch_on(stream, &ws);
+  if (st != KVK_OK) return st;
+  return kvk_decode_attention(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, ws,
+                              (size_t)KVK_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 extern "C" kvk_status kvk_read_bytes(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored,

@@ -79,6 +79,7 @@ def load() -> ctypes.CDLL:
             "kvk_snapkv_select": (I32, [P, I32, P, P, I32, I32, F, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_attention": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_splits": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P]),
+            "kvk_decode_attention_noalloc": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P]),
             "kvk_decode_merge": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P, P]),
             "kvk_read_bytes": (I32, [P, I32, I32, I32, ctypes.POINTER(ctypes.c_int64)]),
             "kvk_debug_dequantize": (I32, [P, I32, I32, P, P, P, P]),
@@ -101,7 +102,7 @@ def exported_symbols() -> List[str]:
     return ["kvk_layer_table", "kvk_layer_table_batched", "kvk_table_sequence_query", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
             "kvk_compress_layer", "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
             "kvk_selector_weight_elems", "kvk_selector_workspace_bytes", "kvk_selector_forward",
-            "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge",
+            "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge", "kvk_decode_attention_noalloc",
             "kvk_read_bytes", "kvk_debug_dequantize",
             "kvk_realized_bits", "kvk_rho_range", "kvk_last_error", "kvk_version"]
 
@@ -420,6 +421,28 @@ def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor
         t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
         _ptr(w_uk), _ptr(w_uv), _ptr(arena), _ptr(out), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # KVK_NOALLOC_SCRATCH_BYTES
+
+
+def decode_attention_noalloc(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_stored: int,
+                             scale: float, arena: torch.Tensor, out: torch.Tensor,
+                             w_uk: Optional[torch.Tensor] = None, w_uv: Optional[torch.Tensor] = None,
+                             stream=None):
+    """decode_attention without a workspace: the library's static device scratch
+    holds the split partials (calls that overlap on one GPU race)."""
+    d = t.dims
+    nl = layer_end - layer_begin
+    _need(q.is_contiguous() and out.is_contiguous() and out.dtype == torch.float32,
+          "q must be contiguous; out contiguous fp32")
+    _need(q.numel() == nl * d.batch * d.n_q_heads * _q_width(d), "q size must be layers*B*Hq*width")
+    _need(out.numel() == nl * d.batch * d.n_q_heads * _out_width(d), "out size must be layers*B*Hq*width")
+    _check_weights(t, nl, w_uk, w_uv)
+    _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
+    _check(load().kvk_decode_attention_noalloc(
+        t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
+        _ptr(w_uk), _ptr(w_uv), _ptr(arena), _ptr(out), _stream(stream)))
 
 
 def decode_splits(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor, n_stored: int,
