@@ -730,8 +730,18 @@ __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
   }
   const DecodeItem& it = item_at<BATCHED>(a, lo);
   const int local = wave - it.wave_begin;
-  const int chunk = local % it.nchp;
-  const int unit = local / it.nchp;
+  int chunk, unit;
+  if (it.nchp <= 4) {  // a unit's chunk waves share one workgroup
+    chunk = local % it.nchp;
+    unit = local / it.nchp;
+  } else {
+    // nchp = 4 k: a unit's waves fill k workgroups, which sit 8 apart in launch
+    // order so that they land on one XCD and share the stream through its L2:
+    // local workgroup j of a group of 8 units holds part j / 8 of unit j % 8.
+    const int k = it.nchp >> 2, wl = local >> 2, j = wl % (8 * k);
+    unit = wl / (8 * k) * 8 + j % 8;
+    chunk = (j / 8) * 4 + (local & 3);
+  }
   if (unit >= it.nb * a.Hkv * it.nsplit || 16 * chunk >= it.geff) return;  // alignment padding
   const int split = unit % it.nsplit;
   const int sidx = unit / it.nsplit;  // (b - b0) * Hkv + kvh
@@ -978,7 +988,7 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
         it.split_blocks = split_blocks_for(it.bits, d.qscheme, D, nbf, split_target);
         it.nsplit = n_splits(nbf, it.split_blocks);
         const int nch = (it.geff + 15) / 16;
-        it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : 4);
+        it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : (nch + 3) / 4 * 4);
         it.b0 = b0;
         it.nb = nb;
         it.ws_off = (int32_t)ws_floats;
@@ -1015,7 +1025,9 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
     DecodeItem it = items[order[k]];
     waves = (waves + 3) / 4 * 4;  // a chunk group never straddles a workgroup
     it.wave_begin = (int32_t)waves;
-    waves += (int64_t)it.nb * d.n_kv_heads * it.nsplit * it.nchp;
+    int64_t units = (int64_t)it.nb * d.n_kv_heads * it.nsplit;
+    if (it.nchp > 4) units = (units + 7) / 8 * 8;  // whole groups of 8 units (see the kernel)
+    waves += units * it.nchp;
     sorted[k] = it;
     new_index[order[k]] = k;
   }

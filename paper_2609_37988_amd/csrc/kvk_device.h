@@ -39,13 +39,23 @@ __device__ __forceinline__ half2v h2s(float a) { return h2(a, a); }
 // fp16 1024 + n has the integer n (n < 1024) in its low mantissa bits.
 constexpr uint32_t kMagic = 0x64006400u;
 
-// (a & b) | c in one v_and_or_b32.  The operands are register operands: the gfx9
-// VOP3 encoding takes no 32-bit literal, so constant masks would otherwise split
-// the operation into a separate AND and OR.
+// x in a VGPR, opaque to constant folding.  The asm is empty (no instruction): it
+// only stops the compiler from folding a constant mask into a 32-bit literal,
+// which the gfx9 VOP3 encoding cannot take (and_or would then become two VOP2
+// instructions).  The compiler itself materialises the value (a v_mov it sees)
+// and can hoist it out of loops.
+__device__ __forceinline__ uint32_t in_vgpr(uint32_t x) {
+  asm("" : "+v"(x));
+  return x;
+}
+
+// (a & b) | c in one v_and_or_b32, selected by the compiler from C with the masks
+// in registers.  Not inline assembly: the compiler's hazard checks do not look
+// inside an asm statement, so an asm v_and_or_b32 that overwrote the accumulator
+// input of an MFMA still in flight got no wait states and corrupted that product
+// (seen in the 4-bit decode at d_h 64).
 __device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t b, uint32_t c) {
-  uint32_t r;
-  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
+  return (a & in_vgpr(b)) | in_vgpr(c);
 }
 
 // b = 4: one 32-bit chunk, slot s at bit 16*(s%2) + 4*(s/2).  Returns the 8 codes

@@ -230,7 +230,6 @@ extern "C" kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* pl
     const kvk_status st = validate_mla(d, plan);
     if (st != KVK_OK) return st;
   }
-  const int32_t G = mla ? 1 : d.n_q_heads / d.n_kv_heads;
   const int64_t streams = mla ? (int64_t)d.batch : (int64_t)d.batch * d.n_kv_heads;
 
   kvk_table* t = new (std::nothrow) kvk_table();
@@ -246,7 +245,6 @@ extern "C" kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* pl
   inf.c0_bits_per_token = (double)d.n_layers * width * 16.0;  // eq. (2)
   int64_t offset = 0;
   int32_t last = -1;
-  int32_t max_readers = 0, run = 0;
   double total_cost = 0.0;
   int64_t stored_alg = 0;
   for (int l = 0; l < d.n_layers; ++l) {
@@ -254,7 +252,6 @@ extern "C" kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* pl
     inf.layer_offset[l] = -1;
     if (!a.inherit) {
       last = l;
-      run = 0;
       t->bits[l] = a.bits;
       // Scalars one stream stores per token: GQA K and V of one head; MLA c[:d] and k^R.
       const int32_t per_tok = mla ? a.rank + d.rope_dim : 2 * d.head_dim;
@@ -278,20 +275,12 @@ extern "C" kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* pl
       t->rank[l] = 0;
       inf.layer_cost_bits[l] = 0.0;
     }
-    ++run;
-    if (run > max_readers) max_readers = run;
     inf.anchor_of[l] = last;
     total_cost += inf.layer_cost_bits[l];
   }
   for (int l = d.n_layers - 1, nxt = d.n_layers; l >= 0; --l) {
     t->next_anchor[l] = nxt;
     if (!plan[l].inherit) nxt = l;
-  }
-  if (!mla && (int64_t)G * max_readers > 64) {
-    delete t;
-    return fail(KVK_ERR_UNSUPPORTED,
-                "an anchor serves %d layers x %d query heads per KV head = %d > 64 query rows",
-                max_readers, G, max_readers * G);
   }
   inf.arena_bytes = offset;
   inf.cost_bits_per_token = total_cost;

@@ -79,18 +79,22 @@ def plan_grouped(seed: int, group_sizes, anchor_bits):
 
 def workload(cfg: int, variant: Optional[str] = None) -> Workload:
     """The five decode workloads.  cfg 0: tiny single layer; 1: Qwen2.5-7B-shaped
-    all-int4 (variant 'bf16': all bf16); 2: Qwen2.5-14B-shaped mixed plan with
-    depth sharing; 4: 14B-shaped, 128k context, half the positions evicted, an
+    all-int4 (variants 'bf16', 'int8', 'int2': every layer at that precision); 2: Qwen2.5-14B-shaped mixed plan with
+    depth sharing (variant 'one-anchor-<bits>': layer 0's cache serves all 48); 4: 14B-shaped, 128k context, half the positions evicted, an
     int2/int4 plan in pairs and triples."""
     if cfg == 0:
         return Workload("tiny-gqa-int8", 1, 4, 1, 64, 1, 256, in_dtype=torch.float32,
                         q_dtype=torch.float32, key_outliers=False, scale=1.0 / 8.0,
                         plan=plan_uniform(1, 8), seed=1000)
     if cfg == 1:
-        bits = 16 if variant == "bf16" else 4
-        return Workload("qwen2.5-7b-shape-int4" if bits == 4 else "qwen2.5-7b-shape-bf16",
-                        28, 28, 4, 128, 8, 8192, plan=plan_uniform(28, bits), seed=1001)
+        bits = {"bf16": 16, "int8": 8, "int2": 2}.get(variant, 4)
+        name = "bf16" if bits == 16 else f"int{bits}"
+        return Workload(f"qwen2.5-7b-shape-{name}", 28, 28, 4, 128, 8, 8192, plan=plan_uniform(28, bits), seed=1001)
     if cfg == 2:
+        if variant and variant.startswith("one-anchor-"):  # depth's extreme: one cache for all 48 layers
+            bits = int(variant.split("-")[-1])
+            return Workload(f"qwen2.5-14b-shape-one-anchor-b{bits}", 48, 40, 8, 128, 32, 8192,
+                            plan=[(0, bits)] + [(1, 16)] * 47, seed=1002)
         return Workload("qwen2.5-14b-shape-mixed", 48, 40, 8, 128, 32, 8192,
                         plan=plan_mixed(1002, 48, 16), seed=1002)
     if cfg == 4:

@@ -39,8 +39,9 @@ class Case:
     def decode(self, q, n_stored, scale, l0=0, l1=None):
         l1 = self.dims.n_layers if l1 is None else l1
         d = self.dims
-        out = torch.empty((l1 - l0, d.batch, d.n_q_heads, d.head_dim), dtype=torch.float32, device=DEV)
-        ws = torch.empty(max(kvk.workspace_bytes(self.table, l0, l1), 256), dtype=torch.uint8, device=DEV)
+        # NaN-filled output and workspace: a read of anything the kernels did not write shows
+        out = torch.full((l1 - l0, d.batch, d.n_q_heads, d.head_dim), float("nan"), dtype=torch.float32, device=DEV)
+        ws = torch.full((max(kvk.workspace_bytes(self.table, l0, l1), 256),), 0xFF, dtype=torch.uint8, device=DEV)
         kvk.decode_attention(self.table, l0, l1, q.contiguous(), n_stored, scale, self.arena, out, ws)
         return out
 

@@ -55,8 +55,8 @@ class MlaCase:
     def decode(self, q, wk, wv, n, scale, l0=0, l1=None):
         l1 = self.dims.n_layers if l1 is None else l1
         d = self.dims
-        out = torch.empty((l1 - l0, d.batch, d.n_q_heads, d.v_dim), dtype=torch.float32, device=DEV)
-        ws = torch.empty(max(kvk.workspace_bytes(self.table, l0, l1), 256), dtype=torch.uint8, device=DEV)
+        out = torch.full((l1 - l0, d.batch, d.n_q_heads, d.v_dim), float("nan"), dtype=torch.float32, device=DEV)
+        ws = torch.full((max(kvk.workspace_bytes(self.table, l0, l1), 256),), 0xFF, dtype=torch.uint8, device=DEV)
         kvk.decode_attention(self.table, l0, l1, q.to(DEV).contiguous(), n, scale, self.arena, out, ws,
                              w_uk=kvk.mla_weights_for_library(wk.to(DEV)), w_uv=wv.to(DEV).contiguous())
         return out

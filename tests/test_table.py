@@ -134,9 +134,11 @@ def test_invalid_plans_and_dims():
     _expect(kvk.ERR_INVALID, kvk.layer_table,
             kvk.make_dims(kvk.GQA, 3, 8, 2, 128, max_tokens=8, keep_tokens=9), ok_plan)
     _expect(kvk.ERR_INVALID, kvk.layer_table, kvk.make_dims(kvk.GQA, 0, 8, 2, 128, max_tokens=8), ok_plan)
-    # 17 layers sharing one anchor with 4 query heads per KV head: 68 rows > 64
-    d17 = kvk.make_dims(kvk.GQA, 17, 8, 2, 128, max_tokens=8)
-    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, d17, kvk.make_plan([(0, 4)] + [(1, 16)] * 16))
+    # every eq. (3) plan is accepted, including one anchor serving all layers
+    # (App. C.1's depth extreme): 64 layers x 8 query heads per KV head = 512 rows
+    d64 = kvk.make_dims(kvk.GQA, 64, 64, 8, 128, max_tokens=64)
+    one = kvk.table_query(kvk.layer_table(d64, kvk.make_plan([(0, 2)] + [(1, 16)] * 63)))
+    assert one.n_anchors == 1 and all(a == 0 for a in one.anchor_of[:64])
 
 
 def _raw(status, name, *args):
