@@ -79,10 +79,7 @@ int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1) {
       total += (int64_t)s->d.batch * s->d.n_kv_heads * s->nb_cap * s->block_bytes[a];
     }
   }
-  int64_t target = total / kSplitWaves;
-  if (target < (1LL << 20)) target = 1LL << 20;
-  if (target > (16LL << 20)) target = 16LL << 20;
-  return target;
+  return total / kSplitWaves;  // clamped per precision by split_blocks_for
 }
 
 int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes) {
@@ -92,9 +89,14 @@ int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_
   // its end.
   const int64_t bb = gqa_block_bytes(head_dim, bits, qscheme);
   const int64_t nr = ring_depth_for(bits);
-  // The 2- and 4-bit paths are bound by their unpacking, not by the stream: longer
-  // splits do not pay there (14B eviction stack: 1 MiB 1.14 ms, 1.1 MiB 1.17 ms).
-  int64_t target = (bits <= 4 ? (1LL << 20) : target_bytes) / bb;
+  // The 8- and 16-bit paths stream: splits between 1 and 16 MiB.  The 2- and 4-bit
+  // paths are bound by their unpacking, not by the stream, so longer splits do not
+  // pay there (14B eviction stack: 1 MiB 1.14 ms, 1.1 MiB 1.17 ms); their splits are
+  // at most 1 MiB and shorter when the launch would otherwise hold fewer waves than
+  // about two per wave slot (7B shape, 28 layers x 32 streams: 1 MiB splits gave the
+  // int2 stack 896 waves for 2048 slots), down to 128 KiB.
+  const int64_t lo = bits <= 4 ? (128LL << 10) : (1LL << 20), hi = bits <= 4 ? (1LL << 20) : (16LL << 20);
+  int64_t target = (target_bytes < lo ? lo : (target_bytes > hi ? hi : target_bytes)) / bb;
   if (target < nr) target = nr;
   const int64_t nb = n_blocks > 0 ? n_blocks : 1;
   const int64_t nsplit = (nb + target - 1) / target;
