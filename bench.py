@@ -488,6 +488,7 @@ def main():
     qs = [synth.queries(w, w.n_layers, device=dev, seed_offset=i) for i in range(2)]
     out = torch.empty((w.n_layers, w.batch, w.n_q_heads, w.head_dim), dtype=torch.float32, device=dev)
     ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=dev)
+    kvk.decode_setup(table, 0, w.n_layers, ws)  # per-sequence plans: the work list, once
     scale = w.softmax_scale()
     alg = kvk.read_bytes(table, 0, w.n_layers, n_stored)
 

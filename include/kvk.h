@@ -255,8 +255,8 @@ kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* plan, kvk_tab
  * sequence by its own plan (a sequence whose layer inherits writes nothing there);
  * one kvk_decode_attention call decodes the whole batch in one launch, each
  * sequence reading its own anchors once (its work list, one item per sequence and
- * anchor, is copied to the head of the workspace on the stream; kvk_decode_merge
- * reads the list that kvk_decode_splits left there); kvk_read_bytes sums the
+ * anchor, sits at the head of the workspace, written there once per workspace and
+ * layer range by kvk_decode_setup; decode calls then copy nothing); kvk_read_bytes sums the
  * sequences.  kvk_table_query reports the batch (arena_bytes, workspace_bytes,
  * n_anchors over all sequences, rho of the mean plan); its per-layer fields are
  * empty (anchor_of and layer_offset -1): use kvk_table_sequence_query.
@@ -406,6 +406,26 @@ kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, int32_t n_act
                                 const void* weights, const void* emb, int32_t n_tokens, const float* film,
                                 float* logits, int32_t* actions, void* workspace, size_t ws_bytes,
                                 hipStream_t stream);
+
+/* Set-up for decoding layers [layer_begin, layer_end) with `workspace` (§2.3: a
+ * plan is chosen once per prompt and held for every decode step, so this runs once
+ * per table, layer range and workspace, not per step).  Per-sequence tables
+ * (kvk_layer_table_batched): writes the decode work list (one item per sequence and
+ * anchor of its plan, laid out for the capacity, so valid for every n_stored) to the
+ * head of `workspace` (kvk_workspace_bytes of the range) and waits for the copy (it
+ * synchronises `stream`; do not call it inside graph capture).  The table records
+ * the workspace; kvk_decode_attention, kvk_decode_splits and kvk_decode_merge on a
+ * per-sequence table then require a prior set-up of the same workspace and layer
+ * range (else KVK_ERR_INVALID), copy nothing and never synchronise.  The workspace
+ * must keep its list (and stay allocated) while it is used for decoding: a set-up
+ * of another range on the same workspace replaces the record; a list that does not
+ * match the call's (a workspace overwritten since) makes the kernels write NaN
+ * outputs and read nothing through it.  One-plan tables: a no-op (their work list
+ * travels in the kernel arguments).
+ * Errors: KVK_ERR_INVALID (range, NULL), KVK_ERR_BUFFER (workspace too small),
+ *         KVK_ERR_DEVICE (the copy). */
+kvk_status kvk_decode_setup(const kvk_table* table, int32_t layer_begin, int32_t layer_end, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream);
 
 /* One decode step of attention for layers [layer_begin, layer_end) (§2.1): layer l
  * uses its own query and the cache of anchor_of[l].  Layers in the range that

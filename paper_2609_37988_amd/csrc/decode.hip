@@ -69,6 +69,8 @@ struct DecodeArgs {
   int32_t n_items;
   float scale_log2;  // softmax scale * log2(e)
   const DecodeItem* items_dev;  // per-sequence plans: the work list in device memory
+  const uint64_t* list_hdr;     // per-sequence plans: its header (magic, hash)
+  uint64_t list_hash;           // the hash this call's list must carry
   DecodeItem items[kMaxItems];  // one plan: the work list in the arguments
 };
 static_assert(sizeof(DecodeArgs) <= 4096, "kernel arguments");
@@ -76,8 +78,14 @@ static_assert(sizeof(DecodeArgs) <= 4096, "kernel arguments");
 // Combine-side fields of a work item (device memory, per-sequence plans).
 struct CombItem {
   int64_t tail;  // byte offset of stream 0's tail block of the item
-  int32_t ws_off, nsplit, geff, stream_bytes, b0, pad;
+  int32_t ws_off, nsplit, geff, stream_bytes, b0, split_blocks;
 };
+
+// Header of a per-sequence work list in the workspace: a magic word and the hash
+// of the list that follows.  A kernel whose arguments expect another hash (a
+// workspace never set up, or set up for another table or layer range) touches
+// nothing through the list.
+constexpr uint64_t kListMagic = 0x4b564b4c49535431ull;  // "KVKLIST1"
 
 struct CombineArgs {
   float* out;
@@ -100,6 +108,9 @@ struct CombineArgs {
   int32_t item_geff[kMaxItems];
   const CombItem* citems;  // per-sequence plans: per item, and per (layer, sequence)
   const int32_t* map;      // the item and the first query slot of the row group
+  const uint64_t* list_hdr;
+  uint64_t list_hash;
+  int32_t nbf;             // full blocks stored per stream (per-sequence plans: live splits)
 };
 
 __device__ __forceinline__ f4 mfma16(half8 a, half8 b, f4 c) {
@@ -722,6 +733,8 @@ __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
   const int wslot = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wave = blockIdx.x * 4 + wslot;
   if (wave >= a.total_waves) return;
+  if constexpr (BATCHED)
+    if (a.list_hdr[0] != kListMagic || a.list_hdr[1] != a.list_hash) return;  // not this call's list
   int lo = 0, hi = a.n_items - 1;  // last item with wave_begin <= wave
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -745,6 +758,9 @@ __global__ __launch_bounds__(256, 2) void gqa_decode_kernel(DecodeArgs a) {
   if (unit >= it.nb * a.Hkv * it.nsplit || 16 * chunk >= it.geff) return;  // alignment padding
   const int split = unit % it.nsplit;
   const int sidx = unit / it.nsplit;  // (b - b0) * Hkv + kvh
+  // Per-sequence lists are laid out for the capacity: a split past the stored
+  // blocks holds nothing at this n_stored (the merge reads only the live ones).
+  if (BATCHED && split * it.split_blocks >= a.nbf) return;
   uint32_t* lds = lds_meta[wslot];
   // A stream read by one wave is streamed non-temporally; the waves of a stream read
   // by several row chunks read it through the caches (the later reads hit).
@@ -778,19 +794,26 @@ __global__ __launch_bounds__(256) void gqa_combine_kernel(CombineArgs a) {
   const int b = rem / a.Hq, h = rem % a.Hq;
   int item, slot, nsplit, geff, ws_off, b0, sbytes;
   int64_t tail_off;
+  int nlive;  // splits holding stored blocks (their partials are written)
   if constexpr (BATCHED) {
+    if (a.list_hdr[0] != kListMagic || a.list_hdr[1] != a.list_hash) {  // not this call's list
+      for (int e = lane; e < D; e += 64) a.out[(int64_t)row * D + e] = __builtin_nanf("");
+      return;
+    }
     const int32_t* m = a.map + ((int64_t)li * a.B + b) * 2;
     item = m[0];
     slot = m[1] + h % a.G;
     const CombItem& ci = a.citems[item];
     nsplit = ci.nsplit, geff = ci.geff, ws_off = ci.ws_off, b0 = ci.b0, sbytes = ci.stream_bytes;
     tail_off = ci.tail;
+    nlive = min(nsplit, (a.nbf + ci.split_blocks - 1) / ci.split_blocks);
   } else {
     item = a.layer_item[li];
     slot = a.layer_slot0[li] + h % a.G;
     nsplit = a.item_nsplit[item], geff = a.item_geff[item], ws_off = a.item_ws_off[item], b0 = 0;
     sbytes = a.item_stream_bytes[item];
     tail_off = a.item_tail[item];
+    nlive = nsplit;
   }
   const int kvh = h / a.G;
   const int sidx = (b - b0) * a.Hkv + kvh;  // the item's own stream index
@@ -823,7 +846,7 @@ __global__ __launch_bounds__(256) void gqa_combine_kernel(CombineArgs a) {
     st = acc * a.scale_log2;
   }
   float mstar = st;
-  for (int s = lane; s < nsplit; s += 64) mstar = fmaxf(mstar, base[s * stride + D]);
+  for (int s = lane; s < nlive; s += 64) mstar = fmaxf(mstar, base[s * stride + D]);
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) mstar = fmaxf(mstar, __shfl_xor(mstar, off));
   constexpr int PER = D / 64;
@@ -831,7 +854,7 @@ __global__ __launch_bounds__(256) void gqa_combine_kernel(CombineArgs a) {
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.0f;
   float lsum = 0.0f;
-  for (int s = 0; s < nsplit; ++s) {
+  for (int s = 0; s < nlive; ++s) {
     const float* p = base + s * stride;
     const float ms = p[D];
     const float w = (ms == -INFINITY) ? 0.0f : exp2f(ms - mstar);
@@ -863,8 +886,10 @@ namespace {
 
 // Everything one decode call launches: the D1 arguments (all anchors of the
 // range in one launch) and the C1 arguments.  Under per-sequence plans the work
-// list (one item per sequence and anchor: more than the arguments hold) goes to the
-// head of the workspace, copied there before D1 on the same stream.
+// list (one item per sequence and anchor: more than the arguments hold) lives at
+// the head of the workspace, written there once by kvk_decode_setup; it is laid out
+// for the capacity, so it does not depend on n_stored, and each call only checks
+// that the setup of this table, layer range and workspace happened.
 struct DecodePlan {
   DecodeArgs d1;
   CombineArgs c1;
@@ -873,8 +898,10 @@ struct DecodePlan {
   bool any_blocks;
   bool batched;
   std::vector<uint8_t> list;  // the host image of the work list (per-sequence plans)
-  void* list_dev;
+  uint64_t hash;              // its hash (FNV-1a over the list after the header)
 };
+
+enum PrepareMode { kForDecode, kForSetup };
 
 int64_t batched_items(const kvk_table* t, int32_t l0, int32_t l1) {
   int64_t n = 0;
@@ -890,26 +917,40 @@ int64_t batched_items(const kvk_table* t, int32_t l0, int32_t l1) {
 }
 
 struct ListLayout {
-  int64_t items, citems, map, total;  // byte offsets of the sections, and the size
+  int64_t hdr, items, citems, map, total;  // byte offsets of the sections, and the size
 };
 
 ListLayout list_layout(const kvk_table* t, int32_t l0, int32_t l1) {
   const int64_t n = batched_items(t, l0, l1);
   ListLayout L;
-  L.items = 0;
-  L.citems = round256(n * (int64_t)sizeof(DecodeItem));
+  L.hdr = 0;
+  L.items = 256;
+  L.citems = L.items + round256(n * (int64_t)sizeof(DecodeItem));
   L.map = L.citems + round256(n * (int64_t)sizeof(CombItem));
   L.total = L.map + round256((int64_t)(l1 - l0) * t->d.batch * 2 * (int64_t)sizeof(int32_t));
   return L;
 }
 
+uint64_t fnv1a(const uint8_t* p, size_t n) {
+  uint64_t h = 0xcbf29ce484222325ull;
+  for (size_t i = 0; i < n; ++i) h = (h ^ p[i]) * 0x100000001b3ull;
+  return h;
+}
+
+// kForSetup builds the per-sequence work list only (q, arena, out unused).
 kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
                    int32_t n_stored, float scale, const void* w_uk, const void* w_uv, const void* arena,
-                   float* out, void* workspace, size_t ws_bytes, DecodePlan& P) {
+                   float* out, void* workspace, size_t ws_bytes, DecodePlan& P, PrepareMode mode = kForDecode) {
   if (!t) return fail(KVK_ERR_INVALID, "decode: NULL table");
   const kvk_dims& d = t->d;
   if (l0 < 0 || l1 > d.n_layers || l0 >= l1)
     return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, d.n_layers);
+  if (mode == kForSetup) {
+    q = arena = out = static_cast<float*>(workspace);
+    q_dtype = KVK_BF16;
+    n_stored = t->cap;
+    scale = 1.0f;
+  }
   if (!q || !arena || !out || !workspace) return fail(KVK_ERR_INVALID, "NULL buffer");
   if (w_uk || w_uv) return fail(KVK_ERR_INVALID, "w_uk / w_uv must be NULL for a GQA table");
   if (q_dtype != KVK_BF16 && q_dtype != KVK_F32) return fail(KVK_ERR_INVALID, "q_dtype %d", q_dtype);
@@ -925,6 +966,7 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   const int32_t nbf = n_stored / KVK_GROUP, ntail = n_stored % KVK_GROUP;
   const int32_t nl = l1 - l0;
   const bool batched = !t->seq.empty();
+  const int32_t nbf_split = batched ? t->nb_cap : nbf;  // per-sequence lists: laid out for the capacity
   P.batched = batched;
   const ListLayout LL = batched ? list_layout(t, l0, l1) : ListLayout{0, 0, 0, 0};
   float* ws = reinterpret_cast<float*>(static_cast<uint8_t*>(workspace) + LL.total);  // the partials
@@ -944,6 +986,9 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   a.scale_log2 = scale * kLog2e;
   a.n_items = 0;
   a.items_dev = nullptr;
+  a.list_hdr = nullptr;
+  a.list_hash = 0;
+  P.hash = 0;
   ca.out = out;
   ca.ws = ws;
   ca.arena = static_cast<const uint8_t*>(arena);
@@ -959,6 +1004,9 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
   ca.n_layers = nl;
   ca.n_rows = nl * d.batch * d.n_q_heads;
   ca.citems = nullptr;
+  ca.list_hdr = nullptr;
+  ca.list_hash = 0;
+  ca.nbf = nbf;
   ca.map = nullptr;
 
   const int64_t split_target = gqa_split_target(t, l0, l1);
@@ -985,8 +1033,8 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
         it.bits = s->bits[anc];
         it.q_layer0 = rb - l0;
         it.geff = G * (re - rb);
-        it.split_blocks = split_blocks_for(it.bits, d.qscheme, D, nbf, split_target);
-        it.nsplit = n_splits(nbf, it.split_blocks);
+        it.split_blocks = split_blocks_for(it.bits, d.qscheme, D, nbf_split, split_target);
+        it.nsplit = n_splits(nbf_split, it.split_blocks);
         const int nch = (it.geff + 15) / 16;
         it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : (nch + 3) / 4 * 4);
         it.b0 = b0;
@@ -1067,18 +1115,37 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
       ci[k].geff = it.geff;
       ci[k].stream_bytes = it.stream_bytes;
       ci[k].b0 = it.b0;
-      ci[k].pad = 0;
+      ci[k].split_blocks = it.split_blocks;
     }
     for (int l = 0; l < nl; ++l)
       for (int b = 0; b < d.batch; ++b) {
         map[((int64_t)l * d.batch + b) * 2] = new_index[l_item[(size_t)b * nl + l]];
         map[((int64_t)l * d.batch + b) * 2 + 1] = l_slot[(size_t)b * nl + l];
       }
-    P.list_dev = workspace;
+    P.hash = fnv1a(P.list.data() + LL.items, (size_t)(LL.total - LL.items));
+    uint64_t* hdr = reinterpret_cast<uint64_t*>(P.list.data() + LL.hdr);
+    hdr[0] = kListMagic;
+    hdr[1] = P.hash;
     uint8_t* wsb = static_cast<uint8_t*>(workspace);
     a.items_dev = reinterpret_cast<const DecodeItem*>(wsb + LL.items);
+    a.list_hdr = reinterpret_cast<const uint64_t*>(wsb + LL.hdr);
+    a.list_hash = P.hash;
     ca.citems = reinterpret_cast<const CombItem*>(wsb + LL.citems);
     ca.map = reinterpret_cast<const int32_t*>(wsb + LL.map);
+    ca.list_hdr = a.list_hdr;
+    ca.list_hash = P.hash;
+    ca.nbf = nbf;
+    if (mode == kForDecode) {
+      bool ready = false;
+      {
+        std::lock_guard<std::mutex> lock(t->setup_mu);
+        for (const kvk_table::DecodeSetup& s : t->setups)
+          ready |= s.workspace == workspace && s.l0 == l0 && s.l1 == l1 && s.hash == P.hash;
+      }
+      if (!ready)
+        return fail(KVK_ERR_INVALID,
+                    "per-sequence plans: call kvk_decode_setup for layers [%d, %d) on this workspace first", l0, l1);
+    }
   }
   P.qs = d.qscheme;
   P.head_dim = D;
@@ -1087,10 +1154,6 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
 }
 
 kvk_status launch_d1(const DecodePlan& P, hipStream_t st) {
-  if (P.batched) {  // the work list D1 and C1 read (C1 reads what D1's call copied)
-    const hipError_t e = hipMemcpyAsync(P.list_dev, P.list.data(), P.list.size(), hipMemcpyHostToDevice, st);
-    if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "work list copy: %s", hipGetErrorString(e));
-  }
   if (!P.any_blocks) return KVK_OK;
   const unsigned grid = (unsigned)((P.d1.total_waves + 3) / 4);
 #define KVK_D1(DD, KK, BB) hipLaunchKernelGGL((gqa_decode_kernel<DD, KK, BB>), dim3(grid), dim3(256), 0, st, P.d1)
@@ -1211,6 +1274,32 @@ extern "C" kvk_status kvk_decode_merge(const kvk_table* t, int32_t l0, int32_t l
                           const_cast<void*>(workspace), ws_bytes, P);
   if (st != KVK_OK) return st;
   return launch_c1(P, stream);
+}
+
+extern "C" kvk_status kvk_decode_setup(const kvk_table* t, int32_t l0, int32_t l1, void* workspace,
+                                       size_t ws_bytes, hipStream_t stream) {
+  if (!t) return fail(KVK_ERR_INVALID, "kvk_decode_setup: NULL table");
+  if (l0 < 0 || l1 > t->d.n_layers || l0 >= l1)
+    return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, t->d.n_layers);
+  if (!workspace) return fail(KVK_ERR_INVALID, "kvk_decode_setup: NULL workspace");
+  if (t->seq.empty()) return KVK_OK;  // one plan: the work list travels in the kernel arguments
+  DecodePlan P;
+  kvk_status st = prepare(t, l0, l1, nullptr, KVK_BF16, 0, 1.0f, nullptr, nullptr, nullptr, nullptr, workspace,
+                          ws_bytes, P, kForSetup);
+  if (st != KVK_OK) return st;
+  {  // the workspace's earlier list (if any) is overwritten now
+    std::lock_guard<std::mutex> lock(t->setup_mu);
+    auto& v = t->setups;
+    for (size_t i = 0; i < v.size();)
+      if (v[i].workspace == workspace) v.erase(v.begin() + i);
+      else ++i;
+  }
+  hipError_t e = hipMemcpyAsync(workspace, P.list.data(), P.list.size(), hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);  // the host image is freed on return
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "work list copy: %s", hipGetErrorString(e));
+  std::lock_guard<std::mutex> lock(t->setup_mu);
+  t->setups.push_back({workspace, l0, l1, P.hash});
+  return KVK_OK;
 }
 
 // ---------------------------------------------------------------------------

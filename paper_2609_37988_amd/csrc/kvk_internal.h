@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <initializer_list>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -23,6 +24,16 @@ struct kvk_table {
   // at byte seq_base[b] of the batch's arena.  Empty for a table with one plan.
   std::vector<kvk_table*> seq;
   std::vector<int64_t> seq_base;
+  // Per-sequence plans: the workspaces kvk_decode_setup has written a decode work list
+  // to (workspace address, layer range, hash of the list).  The only mutable part of a
+  // table; guarded by setup_mu.
+  struct DecodeSetup {
+    const void* workspace;
+    int32_t l0, l1;
+    uint64_t hash;
+  };
+  mutable std::mutex setup_mu;
+  mutable std::vector<DecodeSetup> setups;
   ~kvk_table() {
     for (kvk_table* s : seq) delete s;
   }

@@ -80,6 +80,7 @@ def load() -> ctypes.CDLL:
             "kvk_decode_attention": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_splits": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P]),
             "kvk_decode_attention_noalloc": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, P]),
+            "kvk_decode_setup": (I32, [P, I32, I32, P, ctypes.c_size_t, P]),
             "kvk_decode_merge": (I32, [P, I32, I32, P, I32, I32, F, P, P, P, P, ctypes.c_size_t, P, P]),
             "kvk_read_bytes": (I32, [P, I32, I32, I32, ctypes.POINTER(ctypes.c_int64)]),
             "kvk_debug_dequantize": (I32, [P, I32, I32, P, P, P, P]),
@@ -102,7 +103,7 @@ def exported_symbols() -> List[str]:
     return ["kvk_layer_table", "kvk_layer_table_batched", "kvk_table_sequence_query", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
             "kvk_compress_layer", "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
             "kvk_selector_weight_elems", "kvk_selector_workspace_bytes", "kvk_selector_forward",
-            "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge", "kvk_decode_attention_noalloc",
+            "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge", "kvk_decode_attention_noalloc", "kvk_decode_setup",
             "kvk_read_bytes", "kvk_debug_dequantize",
             "kvk_realized_bits", "kvk_rho_range", "kvk_last_error", "kvk_version"]
 
@@ -421,6 +422,13 @@ def decode_attention(t: Table, layer_begin: int, layer_end: int, q: torch.Tensor
         t.handle, layer_begin, layer_end, _ptr(q), _dtype_code(q), n_stored, float(scale),
         _ptr(w_uk), _ptr(w_uv), _ptr(arena), _ptr(out), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
+
+
+def decode_setup(t: Table, layer_begin: int, layer_end: int, workspace: torch.Tensor, stream=None):
+    """Once per (table, layer range, workspace) before decoding a per-sequence table:
+    writes the work list to the head of the workspace (synchronises the stream)."""
+    _check(load().kvk_decode_setup(t.handle, layer_begin, layer_end, _ptr(workspace), _nbytes(workspace),
+                                   _stream(stream)))
 
 
 NOALLOC_SCRATCH_BYTES = 64 << 20  # KVK_NOALLOC_SCRATCH_BYTES

@@ -384,3 +384,21 @@ def test_host_buffers_are_refused_before_any_launch():
          P(base + 32768), 1 << 14, None)
     assert "GPU-accessible" in kvk.last_error()
     _raw(kvk.ERR_INVALID, "kvk_append_token", t.handle, 0, 1, hk, hk, kvk.BF16, 10, ha, None)
+
+
+def test_per_sequence_decode_needs_its_setup():
+    """A per-sequence table's decode reads its work list from the workspace that
+    kvk_decode_setup wrote: without that set-up the call fails before any launch
+    (and copies nothing)."""
+    d = kvk.make_dims(kvk.GQA, 2, 4, 1, 64, batch=2, max_tokens=64)
+    t = kvk.layer_table_batched(d, [kvk.make_plan([(0, 16), (1, 16)]), kvk.make_plan([(0, 4), (0, 8)])])
+    f, P = ctypes.c_void_p(1 << 20), ctypes.c_void_p
+    _raw(kvk.ERR_INVALID, "kvk_decode_attention", t.handle, 0, 2, f, kvk.BF16, 64, 0.1, None, None, f, f,
+         P(1 << 21), 1 << 20, None)
+    assert "kvk_decode_setup" in kvk.last_error()
+    _raw(kvk.ERR_INVALID, "kvk_decode_splits", t.handle, 0, 2, f, kvk.BF16, 64, 0.1, None, None, f,
+         P(1 << 21), 1 << 20, None)
+    _raw(kvk.ERR_INVALID, "kvk_decode_setup", t.handle, 0, 3, P(1 << 21), 1 << 20, None)  # range
+    _raw(kvk.ERR_BUFFER, "kvk_decode_setup", t.handle, 0, 2, P(1 << 21), 16, None)         # workspace size
+    one = kvk.layer_table(d, kvk.make_plan([(0, 16), (1, 16)]))
+    _raw(kvk.OK, "kvk_decode_setup", one.handle, 0, 2, P(1 << 21), 16, None)  # one plan: nothing to write
