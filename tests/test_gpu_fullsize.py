@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 
 
-def _run_workload(w, n_samples, seed):
+def _run_workload(w, n_samples, seed, cover_bits=False):
     n_tok = w.tokens
     n_stored = w.keep_tokens if w.keep_tokens else n_tok
     dims = kvk.make_dims(kvk.GQA, w.n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, qscheme=w.qscheme,
@@ -47,8 +47,13 @@ def _run_workload(w, n_samples, seed):
     G = w.n_q_heads // w.n_kv_heads
     rng = np.random.default_rng(seed)
     got_rows, ref_rows = [], []
-    for _ in range(n_samples):
-        l = int(rng.integers(w.n_layers))
+    picks = []
+    if cover_bits:  # one reading layer of an anchor of every bit-width in the plan first
+        for bits in sorted({w.plan[info.anchor_of[l]][1] for l in range(w.n_layers)}):
+            ls = [l for l in range(w.n_layers) if w.plan[info.anchor_of[l]][1] == bits]
+            picks.append(ls[int(rng.integers(len(ls)))])
+    picks += [int(rng.integers(w.n_layers)) for _ in range(max(0, n_samples - len(picks)))]
+    for l in picks:
         b = int(rng.integers(w.batch))
         h = int(rng.integers(w.n_kv_heads))
         a = info.anchor_of[l]
@@ -90,6 +95,35 @@ def test_qwen14b_shaped_mixed_stack():
     w = synth.workload(2)
     say(f"case {w.name}")
     _run_workload(w, 8, 12)
+
+
+@pytest.mark.parametrize("qs", [kvk.SYMROW, kvk.GROUP64], ids=["symrow", "group64"])
+def test_qwen14b_shaped_mixed_stack_other_quantisers(qs):
+    """The benchmark workload with the paper's own quantiser (SYMROW: one bf16 scale per
+    stored row, App. B / App. C.3) and with the grouped per-token one (GROUP64): every
+    bit-width of the plan sampled, stream bytes bit-exact, rows within tolerance."""
+    w = synth.workload(2)
+    w.qscheme = qs
+    say(f"case {w.name} qscheme {qs}")
+    _run_workload(w, 8, 15 + qs, cover_bits=True)
+
+
+@pytest.mark.parametrize("qs", [kvk.SYMROW, kvk.GROUP64], ids=["symrow", "group64"])
+def test_qwen7b_shaped_int4_other_quantisers(qs):
+    """28 layers of int4 (Qwen2.5-7B shape) with SYMROW and GROUP64 (App. C.3's 3.56x)."""
+    w = synth.workload(1)
+    w.qscheme = qs
+    say(f"case {w.name} qscheme {qs}")
+    _run_workload(w, 6, 21 + qs)
+
+
+def test_qwen14b_shaped_one_anchor_for_all_layers():
+    """Depth's extreme at full size (App. C.1): layer 0's int4 cache read by all 48
+    layers (240 query rows per KV head: 16 chunk waves in 4 workgroups per split),
+    batch 32, context 8192, in the launch shape the benchmark times."""
+    w = synth.workload(2, "one-anchor-4")
+    say(f"case {w.name}")
+    _run_workload(w, 6, 17)
 
 
 def test_qwen14b_shaped_128k_eviction():
