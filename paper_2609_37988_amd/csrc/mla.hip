@@ -578,11 +578,14 @@ struct MlaRaw {
   uint32_t m[MW > 0 ? MW : 1];
 };
 
+// POL: the cache policy of the loads, non-temporal when one workgroup reads the
+// stream, cached when the workgroups of several reader layers read it (the later
+// readers then find the lines in L2; non-temporal lines are not kept for them).
 // Lane (i = lane % 16, g = lane / 16) of wave part kh holds, at its k-step ks, the
 // 8 channels 32 (kh NKW + ks) + 8 g .. + 7 of block row t (its tile's row i): the
 // MFMA A-operand layout, which the block's lane-ordered slots follow, so every load
 // of a k-step reads one contiguous run of the block.
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, bool KIVI, int POL>
 __device__ __forceinline__ void mla_issue(MlaRaw<D, BITS, KIVI>& r, Rsrc rs, int soff, int t, int g, int kh) {
   constexpr int W = D + kRope, NKW = Geo<D>::NKW;
   const int j0 = kh * NKW;
@@ -591,7 +594,7 @@ __device__ __forceinline__ void mla_issue(MlaRaw<D, BITS, KIVI>& r, Rsrc rs, int
     const int v = 16 * (kq * 64 + i + 16 * g);
 #pragma unroll
     for (int ks = 0; ks < NKW; ++ks) {
-      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, v + 1024 * ks, soff, kStreamPolicy);
+      const u4v x = __builtin_amdgcn_raw_buffer_load_b128(rs, v + 1024 * ks, soff, POL);
       r.c[ks][0] = x[0]; r.c[ks][1] = x[1]; r.c[ks][2] = x[2]; r.c[ks][3] = x[3];
     }
   } else {
@@ -600,24 +603,24 @@ __device__ __forceinline__ void mla_issue(MlaRaw<D, BITS, KIVI>& r, Rsrc rs, int
       const int v = 8 * (kq * 64 + i + 16 * g);
 #pragma unroll
       for (int ks = 0; ks < NKW; ++ks) {
-        const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, v + 512 * ks, soff, kStreamPolicy);
+        const u2v x = __builtin_amdgcn_raw_buffer_load_b64(rs, v + 512 * ks, soff, POL);
         r.c[ks][0] = x[0]; r.c[ks][1] = x[1];
       }
     } else if constexpr (BITS == 4) {
       const int v = 4 * (kq * 64 + i + 16 * g);
 #pragma unroll
-      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 256 * ks, soff, kStreamPolicy);
+      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 256 * ks, soff, POL);
     } else {
       const int v = 4 * ((kq * 16 + i) * 2 + (g >> 1));
 #pragma unroll
-      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 128 * ks, soff, kStreamPolicy);
+      for (int ks = 0; ks < NKW; ++ks) r.c[ks][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 128 * ks, soff, POL);
     }
     if constexpr (KIVI) {
       const int v = cb + 4 * (kq * 16 + i);
 #pragma unroll
-      for (int ks = 0; ks < NKW; ++ks) r.m[ks] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 64 * ks, soff, kStreamPolicy);
+      for (int ks = 0; ks < NKW; ++ks) r.m[ks] = __builtin_amdgcn_raw_buffer_load_b32(rs, v + 64 * ks, soff, POL);
     } else {
-      r.m[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, cb + 4 * t, soff, kStreamPolicy);
+      r.m[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, cb + 4 * t, soff, POL);
     }
   }
 }
@@ -788,7 +791,7 @@ __device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, MlaLds& L, int nva
   }
 }
 
-template <int D, int BITS, bool KIVI>
+template <int D, int BITS, bool KIVI, int POL>
 __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& it, int rl, int hc,
                                         int b, int u, MlaLds& L) {
   using G = Geo<D>;
@@ -806,7 +809,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
 
   MlaRaw<D, BITS, KIVI> ring[NR];
 #pragma unroll
-  for (int i = 0; i < NR; ++i) mla_issue<D, BITS, KIVI>(ring[i], rs, (k0 + G::NBI * i + tblk) * bb, trow, g, kh);
+  for (int i = 0; i < NR; ++i) mla_issue<D, BITS, KIVI, POL>(ring[i], rs, (k0 + G::NBI * i + tblk) * bb, trow, g, kh);
 
   // absorbed query of the 32 heads over this wave's channel part, fp16
   half8 qreg[G::NKW][2];
@@ -839,7 +842,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
       const int nvalid = max(0, min(G::TT, 32 * (k1 - kb)));  // uniform
       __syncthreads();                                 // the tile, scores and p are free
       mla_phase_a<D, BITS, KIVI>(ring[i], qreg, L, wv, tt, kh, lane);
-      mla_issue<D, BITS, KIVI>(ring[i], rs, (kb + G::NBI * NR + tblk) * bb, trow, g, kh);
+      mla_issue<D, BITS, KIVI, POL>(ring[i], rs, (kb + G::NBI * NR + tblk) * bb, trow, g, kh);
       __syncthreads();
       if (nvalid > 0) mla_phase_bc<D>(st, L, nvalid, tid);
     }
@@ -847,7 +850,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
   if (u == it.units - 1 && a.ntail > 0) {  // the bf16 tail block as one more iteration
     MlaRaw<D, 16, false> tr;
     const Rsrc rt = buffer_rsrc(stream + (int64_t)a.nb_cap * bb, tblk == 0 ? 64 * G::W : 0);
-    mla_issue<D, 16, false>(tr, rt, 0, trow, g, kh);
+    mla_issue<D, 16, false, POL>(tr, rt, 0, trow, g, kh);
     __syncthreads();
     mla_phase_a<D, 16, false>(tr, qreg, L, wv, tt, kh, lane);
     __syncthreads();
@@ -876,7 +879,9 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
   }
 }
 
-template <bool KIVI>
+// POL: the loads' cache policy for every item of the launch (see mla_issue); the host
+// launches single-reader and multi-reader items separately.
+template <bool KIVI, int POL>
 __global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(MlaDecodeArgs a) {
   __shared__ MlaLds L;
   const int wg = blockIdx.x;
@@ -899,10 +904,10 @@ __global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(Mla
   if (unit >= a.B * it.units) return;
   const int b = unit / it.units, u = unit - b * it.units;
   const int rl = row / it.nhc, hc = row - rl * it.nhc;
-#define KVK_MLA_CASE(DD, BB)                                        \
-  if (it.d == DD && it.bits == BB) {                                \
-    run_mla<DD, BB, KIVI>(a, it, rl, hc, b, u, L);                  \
-    return;                                                         \
+#define KVK_MLA_CASE(DD, BB)                            \
+  if (it.d == DD && it.bits == BB) {                    \
+    run_mla<DD, BB, KIVI, POL>(a, it, rl, hc, b, u, L); \
+    return;                                             \
   }
 #define KVK_MLA_D(DD) KVK_MLA_CASE(DD, 16) KVK_MLA_CASE(DD, 8) KVK_MLA_CASE(DD, 4) KVK_MLA_CASE(DD, 2)
   KVK_MLA_D(512)
@@ -1124,24 +1129,34 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     // and needs no partials, so nothing is launched here.
     return KVK_OK;
   }
-  MlaDecodeArgs a;
-  a.arena = static_cast<const uint8_t*>(arena);
-  a.ws = wsb;
-  a.B = d.batch;
-  a.Hq = d.n_q_heads;
-  a.nbf = nbf;
-  a.ntail = ntail;
-  a.nb_cap = t->nb_cap;
-  a.n_items = 0;
-  int64_t wgs = 0;
-  auto flush = [&]() -> kvk_status {
+  // Two launches: items whose stream one workgroup reads (non-temporal loads) and
+  // items read by the workgroups of several reader layers or head chunks (cached).
+  MlaDecodeArgs args[2];
+  int64_t wgs_of[2] = {0, 0};
+  for (MlaDecodeArgs& a : args) {
+    a.arena = static_cast<const uint8_t*>(arena);
+    a.ws = wsb;
+    a.B = d.batch;
+    a.Hq = d.n_q_heads;
+    a.nbf = nbf;
+    a.ntail = ntail;
+    a.nb_cap = t->nb_cap;
+    a.n_items = 0;
+  }
+  auto flush = [&](int k) -> kvk_status {
+    MlaDecodeArgs& a = args[k];
+    int64_t& wgs = wgs_of[k];
     if (a.n_items == 0) return KVK_OK;
     if (wgs > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "too many MLA decode workgroups");
     a.n_wg = (int32_t)wgs;
-    if (d.qscheme == KVK_Q_KIVI32)
-      hipLaunchKernelGGL(mla_decode_kernel<true>, dim3((unsigned)wgs), dim3(64 * kWaves), 0, stream, a);
-    else
-      hipLaunchKernelGGL(mla_decode_kernel<false>, dim3((unsigned)wgs), dim3(64 * kWaves), 0, stream, a);
+    const dim3 grid((unsigned)wgs), blk(64 * kWaves);
+    if (d.qscheme == KVK_Q_KIVI32) {
+      if (k == 0) hipLaunchKernelGGL((mla_decode_kernel<true, kStreamPolicy>), grid, blk, 0, stream, a);
+      else hipLaunchKernelGGL((mla_decode_kernel<true, 0>), grid, blk, 0, stream, a);
+    } else {
+      if (k == 0) hipLaunchKernelGGL((mla_decode_kernel<false, kStreamPolicy>), grid, blk, 0, stream, a);
+      else hipLaunchKernelGGL((mla_decode_kernel<false, 0>), grid, blk, 0, stream, a);
+    }
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA decode launch: %s", hipGetErrorString(err));
     a.n_items = 0;
@@ -1152,8 +1167,11 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
   for (int l = l0; l < l1;) {
     const int anc = t->info.anchor_of[l];
     const int re = t->next_anchor[anc] < l1 ? t->next_anchor[anc] : l1;  // readers [l, re)
+    const int k = (re - l) * nhc > 1 ? 1 : 0;
+    MlaDecodeArgs& a = args[k];
+    int64_t& wgs = wgs_of[k];
     if (a.n_items == kMaxItems) {
-      const kvk_status st = flush();
+      const kvk_status st = flush(k);
       if (st != KVK_OK) return st;
     }
     MlaItem& it = a.items[a.n_items++];
@@ -1176,7 +1194,8 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     wgs += (units + 7) / 8 * 8 * it.nreaders * nhc;
     l = re;
   }
-  return flush();
+  const kvk_status st = flush(0);
+  return st != KVK_OK ? st : flush(1);
 }
 
 kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored, const void* w_uv,

@@ -148,13 +148,31 @@ def plan_ranks(seed: int, n_layers: int, latent_dim: int, bits: int, n_inherit: 
     return [(1, 16, 0) if l in inh else (0, bits, int(rng.choice(ranks))) for l in range(n_layers)]
 
 
+def plan_ranks_grouped(seed: int, n_layers: int, latent_dim: int, bits: int, sizes=(2, 3, 4)):
+    """Depth groups on the rank axis: consecutive groups of 2-4 layers (sizes drawn
+    uniformly, the last group cut to fit), each an anchor whose kept width is drawn
+    from {r, r/2, r/4, r/8} followed by inheritors."""
+    rng = np.random.default_rng(seed)
+    ranks = [latent_dim, latent_dim // 2, latent_dim // 4, latent_dim // 8]
+    plan = []
+    while len(plan) < n_layers:
+        g = min(int(rng.choice(sizes)), n_layers - len(plan))
+        plan.append((0, bits, int(rng.choice(ranks))))
+        plan.extend([(1, 16, 0)] * (g - 1))
+    return plan
+
+
 def mla_workload(variant: Optional[str] = None) -> MlaWorkload:
     """The MLA-style decode workload: 32 layers, 32 query heads, latent 512 + 64,
     batch 16, context 16384, per-layer kept width drawn from {512, 256, 128, 64};
-    variant None: bf16 cache, 'int4': KIVI32 4-bit latent and positional key."""
-    bits = 4 if variant == "int4" else 16
-    return MlaWorkload("mla-32l-r512-bf16" if bits == 16 else "mla-32l-r512-int4", 32, 32, 512, 16,
-                       16384, plan_ranks(1003, 32, 512, bits))
+    variant None: bf16 cache, 'int4': KIVI32 4-bit latent and positional key;
+    'depth' / 'int4-depth': the same with the layers in depth groups of 2-4 (one
+    anchor each, its kept width drawn as above)."""
+    bits = 4 if variant in ("int4", "int4-depth") else 16
+    name = "mla-32l-r512-" + ("bf16" if bits == 16 else "int4")
+    if variant in ("depth", "int4-depth"):
+        return MlaWorkload(name + "-depth", 32, 32, 512, 16, 16384, plan_ranks_grouped(1005, 32, 512, bits))
+    return MlaWorkload(name, 32, 32, 512, 16, 16384, plan_ranks(1003, 32, 512, bits))
 
 
 def mla_layer(w: MlaWorkload, layer: int, device="cpu", batch: Optional[int] = None,

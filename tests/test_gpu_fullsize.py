@@ -133,7 +133,7 @@ def test_qwen14b_shaped_128k_eviction():
     _run_workload(w, 4, 14)
 
 
-@pytest.mark.parametrize("variant", [None, "int4"], ids=["bf16", "int4"])
+@pytest.mark.parametrize("variant", [None, "int4", "depth", "int4-depth"], ids=["bf16", "int4", "depth", "int4-depth"])
 def test_mla_shaped_stack(variant):
     """The MLA-style stack at full size: 32 layers, 32 heads, latent 512 + 64 kept to
     per-layer widths, batch 16, context 16384, one decode call over all layers;
@@ -164,16 +164,20 @@ def test_mla_shaped_stack(variant):
                  max_tokens=n)
     rng = np.random.default_rng(13)
     got_rows, ref_rows = [], []
-    for _ in range(4):
-        l, b = int(rng.integers(w.n_layers)), int(rng.integers(w.batch))
-        _, bits, d = w.plan[l]
-        say(f"  sample layer {l} (d {d}, {bits} bits) b {b}")
-        c, r = synth.mla_layer(w, l, device=DEV)
+    readers = [l for l in range(w.n_layers) if w.plan[l][0]]  # inheriting layers (depth variants)
+    picks = [readers[int(rng.integers(len(readers)))] for _ in range(2)] if readers else []
+    picks += [int(rng.integers(w.n_layers)) for _ in range(4 - len(picks))]
+    for l in picks:
+        b = int(rng.integers(w.batch))
+        a = info.anchor_of[l]
+        _, bits, d = w.plan[a]
+        say(f"  sample layer {l} (anchor {a}: d {d}, {bits} bits) b {b}")
+        c, r = synth.mla_layer(w, a, device=DEV)
         cs, rs = c[b].float().cpu().numpy(), r[b].float().cpu().numpy()
         del c, r
         ref_stream = OM.compress_stream(od, bits, d, cs, rs)
-        sb = info.stream_bytes[l]
-        off = info.layer_offset[l] + b * sb
+        sb = info.stream_bytes[a]
+        off = info.layer_offset[a] + b * sb
         assert np.array_equal(arena[off:off + sb].cpu().numpy(), ref_stream), f"stream bytes differ: {(l, b)}"
         C, R = OM.dequant_stream(od, bits, d, ref_stream, n)
         qb = q[l, b].float().cpu().numpy().astype(np.float64)
