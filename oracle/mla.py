@@ -29,8 +29,16 @@ its text as explicit (token, channel) -> address maps: inside a block, bytes are
 ordered by slots of 8 channels of one token, slot S = (T NK + K) 64 + i + 16 g for
 token 16 T + i and channels 32 K + 8 g .. + 7.
 
+Low-rank projection on write (§2.1 "Rank", App. C.2): the latent of a layer is the
+down-projection of the token's hidden state, of which a layer keeping width d
+computes and stores only the first d coordinates (project_latent); it is held in
+bf16 and then written as any latent input.
+
 Pins (tests/test_oracle_mla.py): absorbed == reconstructed; prefix mask ==
-truncation; a full-rank MLA whose up-projections select disjoint latent slices is
+truncation; the projection: an identity map returns the hidden state's first d
+coordinates, keeping d is the prefix of keeping r, brute-force sums on a tiny
+input, single rounding to bf16 with ties to even, and the projected write equals
+the latent-input write of the projected latent; a full-rank MLA whose up-projections select disjoint latent slices is
 multi-head attention over those slices (checked against the GQA oracle); T = 1
 gives W_UV c_0; q = 0 gives W_UV of the mean latent; the layout maps are
 bijections; the quantiser closed forms; block sizes against eq. (1) plus the
@@ -295,6 +303,39 @@ def compress_layer(dims: Dims, bits: int, d: int, C: np.ndarray, R: np.ndarray,
             c, r = c[idx], r[idx]
         out[b * sb:(b + 1) * sb] = compress_stream(dims, bits, d, c, r)
     return out
+
+
+# ---------------------------------------------------------------------------
+# Low-rank projection on write (§2.1 "Rank", App. C.2)
+# ---------------------------------------------------------------------------
+
+def round_bf16_exact(x) -> np.ndarray:
+    """fp64 values rounded once to bf16 (nearest, ties to even), returned as fp64.
+    Values stay well inside the bf16 normal range here."""
+    x = np.ascontiguousarray(np.asarray(x, np.float64))
+    b = x.view(np.uint64)
+    lsb = (b >> np.uint64(45)) & np.uint64(1)  # last kept mantissa bit (7 of 52 kept)
+    r = ((b + np.uint64((1 << 44) - 1) + lsb) >> np.uint64(45)) << np.uint64(45)
+    return r.view(np.float64)
+
+
+def project_latent(X, W_DKV, d: int) -> np.ndarray:
+    """The latent a layer keeping width d stores for tokens X [n, H]: the first d
+    coordinates of the down-projection, c[:d] = W_DKV[:d, :] x per token (App. C.2:
+    a deployed kernel computes only those), exact in fp64 and rounded once to bf16
+    (the latent is held in bf16 before the cache write quantises it).  W_DKV
+    [r, H]: row i maps a token's hidden state to latent coordinate i."""
+    c = np.asarray(X, np.float64) @ np.asarray(W_DKV, np.float64)[:d].T
+    return round_bf16_exact(c)
+
+
+def compress_layer_projected(dims: Dims, bits: int, d: int, X: np.ndarray, W_DKV: np.ndarray, R: np.ndarray,
+                             keep=None) -> np.ndarray:
+    """X [B, n, H] hidden states, R [B, n, d_R] positional keys -> the layer's region:
+    the latent of every token projected to its first d coordinates, then written
+    exactly as a latent input is (truncation, quantiser, layout)."""
+    C = np.stack([project_latent(X[b], W_DKV, d) for b in range(X.shape[0])])
+    return compress_layer(dims, bits, d, C, R, keep)
 
 
 def compress_arena(dims: Dims, plan, Cs, Rs, keeps=None) -> np.ndarray:

@@ -342,3 +342,58 @@ def test_decode_step_depth_and_eviction():
         ref = M.attention_reconstructed(q[2, b, :, :16], q[2, b, :, 16:], Cs[2][b][idx, :32],
                                         Rs[2][b][idx], WK[2], WV[2], 0.1)
         assert np.allclose(out[2, b], ref, rtol=1e-12, atol=1e-14)
+
+
+# --- low-rank projection on write ------------------------------------------------
+
+def test_projection_identity_returns_the_prefix():
+    rng = np.random.default_rng(900)
+    H, r = 96, 64
+    X = Q.round_bf16(rng.standard_normal((10, H)).astype(np.float32)).astype(np.float64)
+    W = np.zeros((r, H))
+    W[:, :r] = np.eye(r)
+    for d in (8, 32, 64):
+        assert np.array_equal(M.project_latent(X, W, d), X[:, :d])
+
+
+def test_projection_keeping_d_is_the_prefix_of_keeping_r():
+    rng = np.random.default_rng(901)
+    X, W = rng.standard_normal((7, 40)), rng.standard_normal((32, 40))
+    full = M.project_latent(X, W, 32)
+    for d in (4, 8, 16):
+        assert np.array_equal(M.project_latent(X, W, d), full[:, :d])
+
+
+def test_projection_brute_force_and_rounding():
+    rng = np.random.default_rng(902)
+    X, W = rng.standard_normal((3, 5)), rng.standard_normal((4, 5))
+    got = M.project_latent(X, W, 4)
+    for t in range(3):
+        for i in range(4):
+            exact = sum(W[i, k] * X[t, k] for k in range(5))
+            # the nearest bf16 (8 significant bits): neighbours 2^(e-7) apart
+            e = np.floor(np.log2(abs(exact)))
+            ulp = 2.0 ** (e - 7)
+            lo = np.floor(exact / ulp) * ulp
+            cand = [lo, lo + ulp]
+            assert got[t, i] in cand and abs(got[t, i] - exact) <= ulp / 2 + 1e-300
+    # ties go to the even neighbour: 1 + 2^-8 -> 1, 1 + 3 * 2^-8 -> 1 + 2^-6
+    one = np.ones((1, 1))
+    assert M.project_latent(one, np.array([[1 + 2.0 ** -8]]), 1)[0, 0] == 1.0
+    assert M.project_latent(one, np.array([[1 + 3 * 2.0 ** -8]]), 1)[0, 0] == 1 + 2.0 ** -6
+    assert M.project_latent(one, np.array([[1 + 2.0 ** -8 + 2.0 ** -30]]), 1)[0, 0] == 1 + 2.0 ** -7
+
+
+@pytest.mark.parametrize("bits", [16, 8, 4, 2])
+@pytest.mark.parametrize("qs", [P.KIVI32, P.SYMROW])
+def test_projected_write_is_the_latent_write_of_the_projection(bits, qs):
+    rng = np.random.default_rng(903 + bits)
+    B, n, H, r, d = 2, 70, 64, 64, 32
+    dims = P.Dims(P.MLA, 1, 8, 1, 64, latent_dim=r, rope_dim=64, nope_dim=64, v_dim=64, qscheme=qs,
+                   batch=B, max_tokens=96)
+    X = rng.standard_normal((B, n, H))
+    W = rng.standard_normal((r, H)) / 8.0
+    R = Q.round_bf16(rng.standard_normal((B, n, 64)).astype(np.float32))
+    C = np.stack([M.project_latent(X[b], W, d) for b in range(B)])
+    assert np.array_equal(M.compress_layer_projected(dims, bits, d, X, W, R),
+                          M.compress_layer(dims, bits, d, C, R))
