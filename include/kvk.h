@@ -304,6 +304,28 @@ kvk_status kvk_compress_layer(const kvk_table* table, int32_t layer, const void*
                               int32_t in_dtype, int32_t n_tokens, const int32_t* keep_idx,
                               void* arena, hipStream_t stream);
 
+/* Prefill write with the down-projection (§2.1 "Rank", App. C.2), MLA tables: each
+ * stored token's latent is computed from its hidden state on the matrix cores, only
+ * its first d coordinates (the layer's kept width; a deployed kernel writes only
+ * those): c[:d] = W_DKV[:d, :] x, bf16 operands, fp32 accumulation, rounded to bf16.
+ * [c[:d] ; k^R] is then stored exactly as kvk_compress_layer stores a latent input
+ * (eviction gather, quantiser, block layout).
+ *   x         : device bf16 [B][n_tokens][d_model], the hidden states; d_model a
+ *               positive multiple of 32.
+ *   w_dkv     : device bf16 [r][d_model]; row i maps a hidden state to latent
+ *               coordinate i (rows 0 .. d-1 are read).
+ *   k_rope    : device bf16 [B][n_tokens][64], the positional keys after RoPE.
+ *   keep_idx  : as for kvk_compress_layer.
+ *   latent_out: NULL, or device bf16 [B][n_stored][d]: the bf16 latent the write
+ *               stored (test support).
+ * An inheriting layer is a no-op returning KVK_OK.  All buffers 16-byte aligned.
+ * Errors: KVK_ERR_INVALID (GQA table, sizes, NULL, misalignment, host memory),
+ *         KVK_ERR_UNSUPPORTED (per-sequence tables, kept width above 512),
+ *         KVK_ERR_DEVICE. */
+kvk_status kvk_compress_layer_project(const kvk_table* table, int32_t layer, const void* x, const void* w_dkv,
+                                      int32_t d_model, const void* k_rope, int32_t n_tokens,
+                                      const int32_t* keep_idx, void* arena, void* latent_out, hipStream_t stream);
+
 /* Decode-time append of one generated token to every anchor layer in
  * [layer_begin, layer_end).  The plan chosen at prefill holds for the whole
  * generation (§2.3), so each anchor keeps its configuration: the new token enters

@@ -594,6 +594,36 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
 static kvk_status append_gqa(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
                              int32_t in_dtype, int32_t n_stored, void* arena, hipStream_t stream);
 
+extern "C" kvk_status kvk_compress_layer_project(const kvk_table* t, int32_t layer, const void* x,
+                                                 const void* w_dkv, int32_t d_model, const void* k_rope,
+                                                 int32_t n_tokens, const int32_t* keep_idx, void* arena,
+                                                 void* latent_out, hipStream_t stream) {
+  if (!t) return fail(KVK_ERR_INVALID, "kvk_compress_layer_project: NULL table");
+  const kvk_dims& d = t->d;
+  if (d.kind != KVK_MLA) return fail(KVK_ERR_INVALID, "kvk_compress_layer_project: an MLA table is required");
+  if (!t->seq.empty()) return fail(KVK_ERR_UNSUPPORTED, "kvk_compress_layer_project: per-sequence tables");
+  if (layer < 0 || layer >= d.n_layers) return fail(KVK_ERR_INVALID, "layer %d out of range", layer);
+  if (t->plan[layer].inherit) return KVK_OK;  // an inheriting layer writes nothing (§2.1)
+  if (!x || !w_dkv || !k_rope || !arena) return fail(KVK_ERR_INVALID, "kvk_compress_layer_project: NULL buffer");
+  if (d_model < 32 || d_model % 32)
+    return fail(KVK_ERR_INVALID, "d_model %d: a positive multiple of 32", d_model);
+  if (n_tokens < 1 || n_tokens > d.max_tokens)
+    return fail(KVK_ERR_INVALID, "n_tokens %d outside 1..max_tokens (%d)", n_tokens, d.max_tokens);
+  const bool evict = d.keep_tokens > 0;
+  if (evict && !keep_idx) return fail(KVK_ERR_INVALID, "the table evicts: keep_idx is required");
+  if (!evict && keep_idx) return fail(KVK_ERR_INVALID, "the table does not evict: keep_idx must be NULL");
+  if (evict && n_tokens < d.keep_tokens)
+    return fail(KVK_ERR_INVALID, "n_tokens %d < keep_tokens %d", n_tokens, d.keep_tokens);
+  if ((reinterpret_cast<uintptr_t>(arena) & 15) || (reinterpret_cast<uintptr_t>(x) & 15) ||
+      (reinterpret_cast<uintptr_t>(w_dkv) & 15) || (reinterpret_cast<uintptr_t>(k_rope) & 15) ||
+      (reinterpret_cast<uintptr_t>(latent_out) & 15))
+    return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
+  if (kvk_status st = check_gpu_buffers({x, w_dkv, k_rope, keep_idx, arena, latent_out}, "kvk_compress_layer_project"))
+    return st;
+  return mla_compress_layer_project(t, layer, x, w_dkv, d_model, k_rope, n_tokens, keep_idx, arena, latent_out,
+                                    stream);
+}
+
 extern "C" kvk_status kvk_append_token(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
                                        int32_t in_dtype, int32_t n_stored, void* arena, hipStream_t stream) {
   if (!t) return fail(KVK_ERR_INVALID, "kvk_append_token: NULL table");

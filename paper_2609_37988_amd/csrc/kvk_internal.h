@@ -165,6 +165,9 @@ struct MlaWorkspace {
 };
 void mla_workspace(const kvk_table* t, int32_t l0, int32_t l1, MlaWorkspace* ws);
 
+kvk_status mla_compress_layer_project(const kvk_table* t, int32_t layer, const void* x, const void* w_dkv,
+                                      int32_t d_model, const void* rope, int32_t n_tokens,
+                                      const int32_t* keep_idx, void* arena, void* latent_out, hipStream_t stream);
 kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* latent,
                               const void* rope, int32_t in_dtype, int32_t n_tokens,
                               const int32_t* keep_idx, void* arena, hipStream_t stream);

@@ -262,6 +262,160 @@ __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
   mla_write_block<BITS, KIVI>(src, out, a.d, tail, amax);
 }
 
+// ---------------------------------------------------------------------------
+// W2 with the down-projection (§2.1 "Rank", App. C.2): the latent's first d
+// coordinates c[:d] = W_DKV[:d, :] x of each stored token on MFMA, rounded to bf16,
+// then written by the block writer exactly as a latent input is.
+// ---------------------------------------------------------------------------
+
+struct MlaProjectArgs {
+  const uint16_t* x;     // [B][n_tokens][H] bf16 hidden states
+  const uint16_t* w;     // [r][H] bf16 W_DKV (row i -> latent coordinate i)
+  const uint16_t* rope;  // [B][n_tokens][64] bf16 positional keys (after RoPE)
+  const int32_t* keep;   // [B][n_stored] or null
+  uint8_t* region;
+  uint16_t* latent_out;  // [B][n_stored][d] bf16, or null
+  int64_t stream_bytes;
+  int64_t block_bytes;
+  int32_t n_tokens;
+  int32_t n_stored;
+  int32_t nbf;
+  int32_t nb_cap;
+  int32_t H;
+  int32_t d;
+};
+
+__device__ __forceinline__ int mla_stored_pos(const int32_t* keep, int b, int n_stored, int n_tokens, int pos) {
+  if (!keep) return pos;
+  const int p = keep[(int64_t)b * n_stored + pos];
+  return p < 0 ? 0 : (p >= n_tokens ? n_tokens - 1 : p);
+}
+
+// The block writer's source for a projected block: the bf16 latent rows in LDS
+// (pitch LP halfs) and the positional keys from the input.
+struct ProjectedRows {
+  const MlaProjectArgs& a;
+  const uint16_t* lat;
+  int LP, b, tok0, ntok;
+  __device__ __forceinline__ void load8(int t, int c0, float (&x)[8]) const {
+    if (t >= ntok) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+      return;
+    }
+    u4v w;
+    if (c0 < a.d) {
+      w = *reinterpret_cast<const u4v*>(lat + t * LP + c0);
+    } else {
+      const int pos = mla_stored_pos(a.keep, b, a.n_stored, a.n_tokens, tok0 + t);
+      w = *reinterpret_cast<const u4v*>(a.rope + ((int64_t)b * a.n_tokens + pos) * kRope + (c0 - a.d));
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[2 * e] = __uint_as_float(w[e] << 16);
+      x[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  }
+};
+
+// One workgroup per (32-token block, sequence).  K loop over the model width in
+// steps of 32.  The block's 32 hidden-state rows, which every wave uses, are staged
+// in LDS (double-buffered: a thread loads its share of the next step into registers
+// while the current one is consumed, one barrier per step).  The rows of W_DKV are
+// each used by one wave only, so each wave loads its own straight into registers,
+// one step ahead.  Wave w computes the 16-channel tiles w, w + 4, ... for both
+// 16-token tiles (A = W_DKV rows, B = hidden rows: a lane's accumulator holds 4
+// consecutive channels of one token).
+template <int D, int BITS, bool KIVI>
+__global__ __launch_bounds__(256) void mla_project_kernel(MlaProjectArgs a) {
+  constexpr int KP = 32 + 8;                 // staging row pitch (halfs)
+  constexpr int NT = D / 16;                 // channel tiles
+  constexpr int NTW = (NT + 3) / 4;          // per wave
+  constexpr int LP = D + 8;                  // latent tile pitch (halfs)
+  __shared__ __attribute__((aligned(16))) uint16_t xs[2 * 32 * KP];
+  __shared__ __attribute__((aligned(16))) uint16_t lat[32 * LP];
+  __shared__ uint32_t amax[2][32];
+  const int blk = blockIdx.x, b = blockIdx.y;
+  const bool tail = blk == a.nbf;
+  const int tok0 = 32 * blk;
+  const int ntok = tail ? a.n_stored - tok0 : 32;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, i16 = lane & 15, kg = lane >> 4;
+  // staging share (threads < 128): hidden row tid / 4, 8 k at 8 (tid % 4)
+  const int xr = (tid >> 2) & 31, xk = 8 * (tid & 3);
+  const bool x_ok = tid < 128 && xr < ntok;
+  // (a thread with no row reads stored token 0's keep entry: the tail block of a
+  // whole number of groups has no rows at all)
+  const uint16_t* xp =
+      a.x + ((int64_t)b * a.n_tokens + mla_stored_pos(a.keep, b, a.n_stored, a.n_tokens, x_ok ? tok0 + xr : 0)) *
+                a.H + xk;
+  const uint16_t* wp[NTW];  // the wave's W_DKV rows: tile wv + 4 j, row i16, k at 8 kg
+#pragma unroll
+  for (int j = 0; j < NTW; ++j) wp[j] = a.w + (int64_t)(16 * min(wv + 4 * j, NT - 1) + i16) * a.H + 8 * kg;
+  u4v xreg;
+  bf16x8 wcur[NTW], wnext[NTW];
+  auto fetch_w = [&](int k0, bf16x8 (&dst)[NTW]) {
+#pragma unroll
+    for (int j = 0; j < NTW; ++j)
+      if (NT % 4 == 0 || wv + 4 * j < NT) dst[j] = *reinterpret_cast<const bf16x8*>(wp[j] + k0);
+  };
+  f4 acc[2][NTW];
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) acc[m][j] = f4{0.f, 0.f, 0.f, 0.f};
+  if (ntok > 0) {
+    xreg = x_ok ? *reinterpret_cast<const u4v*>(xp) : u4v{0u, 0u, 0u, 0u};
+    fetch_w(0, wcur);
+    if (tid < 128) *reinterpret_cast<u4v*>(xs + xr * KP + xk) = xreg;
+    __syncthreads();
+    int buf = 0;
+    for (int k0 = 0; k0 < a.H; k0 += 32, buf ^= 1) {
+      const bool more = k0 + 32 < a.H;  // uniform
+      if (more) {
+        xreg = x_ok ? *reinterpret_cast<const u4v*>(xp + k0 + 32) : u4v{0u, 0u, 0u, 0u};
+        fetch_w(k0 + 32, wnext);
+      }
+      bf16x8 xb[2];
+#pragma unroll
+      for (int m = 0; m < 2; ++m) xb[m] = *reinterpret_cast<const bf16x8*>(xs + (buf * 32 + 16 * m + i16) * KP + 8 * kg);
+#pragma unroll
+      for (int j = 0; j < NTW; ++j)
+        if (NT % 4 == 0 || wv + 4 * j < NT)
+#pragma unroll
+          for (int m = 0; m < 2; ++m) acc[m][j] = mfmab(wcur[j], xb[m], acc[m][j]);
+      if (more) {
+        if (tid < 128) *reinterpret_cast<u4v*>(xs + ((buf ^ 1) * 32 + xr) * KP + xk) = xreg;  // read before the last barrier
+#pragma unroll
+        for (int j = 0; j < NTW; ++j) wcur[j] = wnext[j];
+      }
+      __syncthreads();
+    }
+  }
+  // the latent tile, bf16: lane (token 16 m + i16, kg) holds channels 16 ct + 4 kg .. + 3
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    const int t = 16 * m + i16;
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) {
+      const int ct = wv + 4 * j;
+      if (NT % 4 == 0 || ct < NT) {
+        const int c = 16 * ct + 4 * kg;
+        u2v w2;
+        w2[0] = (uint32_t)f32_to_bf16_bits(acc[m][j][0]) | ((uint32_t)f32_to_bf16_bits(acc[m][j][1]) << 16);
+        w2[1] = (uint32_t)f32_to_bf16_bits(acc[m][j][2]) | ((uint32_t)f32_to_bf16_bits(acc[m][j][3]) << 16);
+        *reinterpret_cast<u2v*>(lat + t * LP + c) = w2;
+        if (a.latent_out && t < ntok)
+          *reinterpret_cast<u2v*>(a.latent_out + ((int64_t)b * a.n_stored + tok0 + t) * a.d + c) = w2;
+      }
+    }
+  }
+  __syncthreads();
+  const ProjectedRows src{a, lat, LP, b, tok0, ntok};
+  uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
+                 (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
+  mla_write_block<BITS, KIVI>(src, out, D, tail, amax);
+}
+
 // Decode-time append of one token to every MLA anchor of a layer range.
 struct MlaAppendItem {
   int64_t region;
@@ -1074,6 +1228,46 @@ kvk_status mla_append_token(const kvk_table* t, int32_t l0, int32_t l1, const vo
   else hipLaunchKernelGGL(mla_append_kernel<false>, g3, b3, 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA append launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+kvk_status mla_compress_layer_project(const kvk_table* t, int32_t layer, const void* x, const void* w_dkv,
+                                      int32_t d_model, const void* rope, int32_t n_tokens,
+                                      const int32_t* keep_idx, void* arena, void* latent_out, hipStream_t stream) {
+  const kvk_dims& d = t->d;
+  MlaProjectArgs a;
+  a.x = static_cast<const uint16_t*>(x);
+  a.w = static_cast<const uint16_t*>(w_dkv);
+  a.rope = static_cast<const uint16_t*>(rope);
+  a.keep = keep_idx;
+  a.region = static_cast<uint8_t*>(arena) + t->info.layer_offset[layer];
+  a.latent_out = static_cast<uint16_t*>(latent_out);
+  a.stream_bytes = t->info.stream_bytes[layer];
+  a.block_bytes = t->block_bytes[layer];
+  a.n_tokens = n_tokens;
+  a.n_stored = d.keep_tokens > 0 ? d.keep_tokens : n_tokens;
+  a.nbf = a.n_stored / KVK_GROUP;
+  a.nb_cap = t->nb_cap;
+  a.H = d_model;
+  a.d = t->rank[layer];
+  const int bits = t->bits[layer];
+  const bool kivi = d.qscheme == KVK_Q_KIVI32;
+  const dim3 g3((unsigned)(a.nbf + 1), (unsigned)d.batch), b3(256);
+#define KVK_PROJ(DD)                                                                                          \
+  if (a.d == DD) {                                                                                            \
+    if (bits == 16) hipLaunchKernelGGL((mla_project_kernel<DD, 16, true>), g3, b3, 0, stream, a);              \
+    else if (kivi && bits == 8) hipLaunchKernelGGL((mla_project_kernel<DD, 8, true>), g3, b3, 0, stream, a);  \
+    else if (kivi && bits == 4) hipLaunchKernelGGL((mla_project_kernel<DD, 4, true>), g3, b3, 0, stream, a);  \
+    else if (kivi) hipLaunchKernelGGL((mla_project_kernel<DD, 2, true>), g3, b3, 0, stream, a);               \
+    else if (bits == 8) hipLaunchKernelGGL((mla_project_kernel<DD, 8, false>), g3, b3, 0, stream, a);         \
+    else if (bits == 4) hipLaunchKernelGGL((mla_project_kernel<DD, 4, false>), g3, b3, 0, stream, a);         \
+    else hipLaunchKernelGGL((mla_project_kernel<DD, 2, false>), g3, b3, 0, stream, a);                        \
+  }
+  KVK_PROJ(512) else KVK_PROJ(256) else KVK_PROJ(128) else KVK_PROJ(64) else KVK_PROJ(32)
+  else return fail(KVK_ERR_UNSUPPORTED, "projected write: kept width %d", a.d);
+#undef KVK_PROJ
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA projected write launch: %s", hipGetErrorString(e));
   return KVK_OK;
 }
 

@@ -71,6 +71,7 @@ def load() -> ctypes.CDLL:
             "kvk_layer_table_batched": (I32, [P, P, ctypes.POINTER(P)]),
             "kvk_table_sequence_query": (I32, [P, I32, P]),
             "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
+            "kvk_compress_layer_project": (I32, [P, I32, P, P, I32, P, I32, P, P, P, P]),
             "kvk_append_token": (I32, [P, I32, I32, P, P, I32, I32, P, P]),
             "kvk_snapkv_workspace_bytes": (I32, [P, I32, ctypes.POINTER(ctypes.c_size_t)]),
             "kvk_selector_weight_elems": (I64, [I32, I32, I32]),
@@ -101,7 +102,7 @@ def load() -> ctypes.CDLL:
 def exported_symbols() -> List[str]:
     """Names of the C entry points the binding expects libkvk to export."""
     return ["kvk_layer_table", "kvk_layer_table_batched", "kvk_table_sequence_query", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
-            "kvk_compress_layer", "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
+            "kvk_compress_layer", "kvk_compress_layer_project", "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
             "kvk_selector_weight_elems", "kvk_selector_workspace_bytes", "kvk_selector_forward",
             "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge", "kvk_decode_attention_noalloc", "kvk_decode_setup",
             "kvk_read_bytes", "kvk_debug_dequantize",
@@ -311,6 +312,31 @@ def compress_layer(t: Table, layer: int, k: torch.Tensor, v: torch.Tensor, n_tok
     _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
     _check(load().kvk_compress_layer(t.handle, layer, _ptr(k), _ptr(v), _dtype_code(k), n_tokens,
                                      _ptr(keep_idx), _ptr(arena), _stream(stream)))
+
+
+def compress_layer_project(t: Table, layer: int, x: torch.Tensor, w_dkv: torch.Tensor, k_rope: torch.Tensor,
+                           n_tokens: int, keep_idx: Optional[torch.Tensor], arena: torch.Tensor,
+                           latent_out: Optional[torch.Tensor] = None, stream=None):
+    """MLA prefill write from hidden states: x [B, n_tokens, d_model] bf16, w_dkv
+    [r, d_model] bf16, k_rope [B, n_tokens, 64] bf16; latent_out (optional) bf16
+    [B, n_stored, d] receives the projected latent."""
+    d = t.dims
+    _need(d.kind == MLA, "an MLA table is required")
+    _need(x.dtype == torch.bfloat16 and x.is_contiguous() and x.dim() == 3 and x.shape[0] == d.batch and
+          x.shape[1] == n_tokens, "x must be contiguous bf16 [B, n_tokens, d_model]")
+    _need(w_dkv.dtype == torch.bfloat16 and w_dkv.is_contiguous() and w_dkv.shape == (d.latent_dim, x.shape[2]),
+          "w_dkv must be contiguous bf16 [r, d_model]")
+    _need(k_rope.dtype == torch.bfloat16 and k_rope.is_contiguous() and
+          k_rope.numel() == d.batch * n_tokens * d.rope_dim, "k_rope must be contiguous bf16 [B, n_tokens, 64]")
+    if keep_idx is not None:
+        _need(keep_idx.dtype == torch.int32 and keep_idx.is_contiguous() and
+              keep_idx.numel() == d.batch * d.keep_tokens, "keep_idx must be int32 [B, keep_tokens]")
+    if latent_out is not None:
+        _need(latent_out.dtype == torch.bfloat16 and latent_out.is_contiguous(), "latent_out must be contiguous bf16")
+    _need(_nbytes(arena) >= table_query(t).arena_bytes, "arena smaller than arena_bytes")
+    _check(load().kvk_compress_layer_project(t.handle, layer, _ptr(x), _ptr(w_dkv), x.shape[2], _ptr(k_rope),
+                                             n_tokens, _ptr(keep_idx), _ptr(arena), _ptr(latent_out),
+                                             _stream(stream)))
 
 
 def append_token(t: Table, layer_begin: int, layer_end: int, k: torch.Tensor, v: torch.Tensor,
