@@ -114,25 +114,29 @@ def test_project_short_and_inheritor():
     assert torch.equal(c.arena, before)
 
 
-def test_project_full_size_sample():
-    """DeepSeek-V2-Lite-shaped write at the Qwen2.5-7B model width (3584) over 4k
-    tokens, d 512, 4 bits, B 1: the latent of a sampled set of tokens against the
-    exact projection, the stored bytes against the oracle's write of the kernel's
-    latent."""
-    say("case project full-size H=3584 n=4096 d=512 int4")
-    B, n, H, r, d = 1, 4096, 3584, 512, 512
-    c = MlaCase(1, 32, r, B, n, [(0, 4, d)])
-    X = synth.latent_random(501, B, n, H)
-    W = synth.weights_random(502, 1, 1, r, H)[0, 0].contiguous()
-    R = synth.latent_random(503, B, n, 64)
+@pytest.mark.parametrize("qs,d", [(kvk.KIVI32, 512), (kvk.SYMROW, 256)], ids=["kivi32-512", "symrow-256"])
+def test_project_full_size_sample(qs, d):
+    """The 32-layer latent stack's layer write at full size: B 16, 16384 tokens, r 512,
+    model width 2048 (DeepSeek-V2-Lite's), int4.  Sampled: the latent of 96 tokens
+    against the exact projection, and two whole sequences' streams against the
+    oracle's write of the kernel's latent."""
+    say(f"case project full-size B=16 n=16384 H=2048 d={d} qs={qs} int4")
+    B, n, H, r = 16, 16384, 2048, 512
+    c = MlaCase(1, 32, r, B, n, [(0, 4, d)], qscheme=qs)
+    X = synth.latent_random(501, B, n, H, device=DEV)
+    W = synth.weights_random(502, 1, 1, r, H, device=DEV)[0, 0].contiguous()
+    R = synth.latent_random(503, B, n, 64, device=DEV)
     lat = torch.empty((B, n, d), dtype=torch.bfloat16, device=DEV)
-    kvk.compress_layer_project(c.table, 0, X.to(DEV), W.to(DEV), R.to(DEV), n, None, c.arena, lat)
-    got = _np(lat)
-    rows = np.random.default_rng(7).choice(n, 96, replace=False)
-    _check_latent(got[0, rows], _np(X)[0, rows], _np(W), d)
-    ref = OM.compress_layer(c.odims, 4, d, got, _np(R))
-    off, nb = c.info.layer_offset[0], c.info.layer_bytes[0]
-    assert np.array_equal(c.arena[off:off + nb].cpu().numpy(), ref), "arena bytes differ"
+    kvk.compress_layer_project(c.table, 0, X, W, R, n, None, c.arena, lat)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(7)
+    bs, ts = rng.integers(B, size=96), rng.integers(n, size=96)
+    _check_latent(_np(lat[bs, ts]), _np(X[bs, ts]), _np(W), d)
+    off, sb = c.info.layer_offset[0], c.info.stream_bytes[0]
+    for b in (0, int(rng.integers(1, B))):
+        ref = OM.compress_stream(c.odims, 4, d, _np(lat[b]), _np(R[b]))
+        got = c.arena[off + b * sb:off + (b + 1) * sb].cpu().numpy()
+        assert np.array_equal(got, ref), f"stream {b} bytes differ"
 
 
 def test_project_refusals():
