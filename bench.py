@@ -18,8 +18,11 @@ sample of the same workload.
 
 With --config 3 the workload is the MLA-style stack instead (32 layers, 32 heads,
 latent 512 + 64 kept to a per-layer width drawn from {512, 256, 128, 64}, batch 16,
-context 16384; --variant int4 for a KIVI32 4-bit latent): a step is the absorbed
-query (A1), the latent decode (D2) and the merge with the W_UV up-projection (C2).
+context 16384; --variant int4 for a KIVI32 4-bit latent; --variant 14b / 14b-int4
+for Qwen2.5-14B's latent shape: 48 layers, 40 heads, latent 1024 + 64, batch 32,
+context 8192): a step is the absorbed query (A1), the latent decode (D2) and the
+merge with the W_UV up-projection (C2).  The MLA line also times the prefill write
+with the down-projection from hidden states of the model width.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
 """
@@ -390,6 +393,8 @@ def run_mla(args):
     app = time_append(kvk, torch, table, w.n_layers, arena, n_stored, (w.n_layers, w.batch, w.latent_dim),
                       (w.n_layers, w.batch, w.rope_dim), dev)
     log(f"append: {app}")
+    proj = time_projected_write(kvk, torch, w, table, arena, n_tok, dev)
+    log(f"projected write: {proj}")
     ranks = {}
     for e in w.plan:
         if not e[0]:
@@ -423,8 +428,41 @@ def run_mla(args):
                           "GB_per_s": round(w2_bytes / (w2_ms * 1e-3) / 1e9, 2)},
         "median_of_12_us_per_step": med12,
         "append": app,
+        "prefill_write_projected": proj,
     }
     print(json.dumps(line), flush=True)
+
+
+def time_projected_write(kvk, torch, w, table, arena, n_tok, dev):
+    """The prefill write with the down-projection (kvk_compress_layer_project) of the
+    widest anchor, from hidden states of the model width: median of 5 after 2 warmups.
+    Runs after the decode timing (it rewrites that layer's region)."""
+    from paper_2609_37988_amd import synth
+    anchors = [l for l in range(w.n_layers) if not w.plan[l][0]]
+    l = max(anchors, key=lambda a: w.plan[a][2])
+    d, bits = w.plan[l][2], w.plan[l][1]
+    x = synth.latent_random(91, w.batch, n_tok, w.d_model, device=dev)
+    wd = synth.weights_random(92, 1, 1, w.latent_dim, w.d_model, device=dev)[0, 0].contiguous()
+    r = synth.latent_random(93, w.batch, n_tok, w.rope_dim, device=dev)
+    for _ in range(2):
+        kvk.compress_layer_project(table, l, x, wd, r, n_tok, None, arena)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        kvk.compress_layer_project(table, l, x, wd, r, n_tok, None, arena)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms = sorted(ts)[2]
+    flops = 2.0 * w.batch * n_tok * w.d_model * d
+    del x, wd, r
+    torch.cuda.empty_cache()
+    return {"layer": l, "d": d, "bits": bits, "d_model": w.d_model, "tokens": w.batch * n_tok,
+            "us": round(ms * 1e3, 1), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
+            "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
+            "x_read_GB_per_s": round(w.batch * n_tok * w.d_model * 2 / (ms * 1e-3) / 1e9, 1)}
 
 
 def main():

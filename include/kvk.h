@@ -81,12 +81,12 @@ typedef struct {
 typedef struct {
   int32_t kind;        /* kvk_kind */
   int32_t n_layers;    /* L, 1..KVK_MAX_LAYERS */
-  int32_t n_q_heads;   /* Hq; MLA: a multiple of 32, at most 256 */
+  int32_t n_q_heads;   /* Hq; MLA: a multiple of 8, at most 256 */
   int32_t n_kv_heads;  /* GQA: Hkv; Hq % Hkv == 0; Hq/Hkv * (readers of one anchor) <= 64.
                           MLA: KV heads of the bf16 GQA model the ratio eq. (2) is
                           quoted against (C0 = L * 2 * Hkv * d_h * 16); >= 1 */
   int32_t head_dim;    /* GQA: d_h in {64, 128}.  MLA: d_h of that reference model, >= 1 */
-  int32_t latent_dim;  /* MLA r: a multiple of 256, at most 512 (unused for GQA, pass 0) */
+  int32_t latent_dim;  /* MLA r: a multiple of 256; kept widths at most 1024 (unused for GQA, pass 0) */
   int32_t rope_dim;    /* MLA d_R: 64 (unused for GQA, pass 0) */
   int32_t nope_dim;    /* MLA per-head no-RoPE query/key width: a multiple of 32, <= 256 */
   int32_t v_dim;       /* MLA per-head value width: a multiple of 16, <= 256 */
@@ -320,7 +320,7 @@ kvk_status kvk_compress_layer(const kvk_table* table, int32_t layer, const void*
  *               stored (test support).
  * An inheriting layer is a no-op returning KVK_OK.  All buffers 16-byte aligned.
  * Errors: KVK_ERR_INVALID (GQA table, sizes, NULL, misalignment, host memory),
- *         KVK_ERR_UNSUPPORTED (per-sequence tables, kept width above 512),
+ *         KVK_ERR_UNSUPPORTED (per-sequence tables),
  *         KVK_ERR_DEVICE. */
 kvk_status kvk_compress_layer_project(const kvk_table* table, int32_t layer, const void* x, const void* w_dkv,
                                       int32_t d_model, const void* k_rope, int32_t n_tokens,

@@ -132,12 +132,17 @@ constexpr int mla_ring_depth(int W, int bits, int kivi) {
   const int nkw = W / 32 / mla_ksplit(W);                        // k-steps per wave
   const int regs = bits == 16 ? 4 * nkw : (bits == 8 ? 2 * nkw : nkw) + (bits == 16 ? 0 : (kivi ? nkw : 1));
   const long wg_bytes = 4L * 16 * (W / mla_ksplit(W)) * bits / 8;  // codes of one iteration
-  const int cap = W > 192 ? 40 : 64;
+  const int cap = W > 576 ? 80 : (W > 192 ? 40 : 64);  // width 1024: one wave per SIMD, more registers
   const int by_regs = regs > cap ? 1 : cap / regs;
   const int by_bytes = (int)((32768 + wg_bytes - 1) / wg_bytes);
   const int nr = by_regs < by_bytes ? by_regs : by_bytes;
   return nr < 1 ? 1 : nr;
 }
+
+// Query heads of an MLA decode rounded up to whole 32-head chunks (the workgroup's
+// two 16-head tiles): the absorbed queries and split partials are laid out for
+// this many; the padding heads carry zero queries and are never written out.
+constexpr int32_t mla_heads_padded(int32_t hq) { return (hq + 31) / 32 * 32; }
 
 // Most splits of one MLA stream (the merge holds one weight per split in LDS).
 constexpr int kMlaMaxUnits = 128;

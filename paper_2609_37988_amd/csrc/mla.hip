@@ -29,6 +29,8 @@
 // writer that takes its rows from the input or from the stream's bf16 tail.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "kvk_device.h"
 #include "kvk_internal.h"
 
@@ -38,7 +40,6 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kRope = 64;
-constexpr int kMaxW = 512 + kRope;  // widest stored row
 constexpr int kMaxItems = 32;       // anchors per decode launch (kernel-argument size)
 
 typedef __amdgpu_buffer_rsrc_t Rsrc;
@@ -561,10 +562,10 @@ struct MlaAbsorbArgs {
   const void* q;          // [nl][B][Hq][nope + 64]
   const uint16_t* w_ukt;  // [nl][Hq][r][nope] bf16: W_UK[h] transposed (latent-major)
   uint8_t* ws;
-  int64_t q_off[KVK_MAX_LAYERS];  // per relative layer: fp16 [B][Hq][d + 64]
+  int64_t q_off[KVK_MAX_LAYERS];  // per relative layer: fp16 [B][Hp][d + 64]
   int32_t d_of[KVK_MAX_LAYERS];
   int32_t q_f32;
-  int32_t B, Hq, nope, r;
+  int32_t B, Hq, Hp, nope, r;  // Hp: Hq rounded up to whole 32-head chunks
   float scale_log2;
 };
 
@@ -581,10 +582,17 @@ __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
   const int qw = a.nope + kRope;
   const int nks = a.nope / 32;
   _Float16* qa = reinterpret_cast<_Float16*>(a.ws + a.q_off[li]);
+  if (h >= a.Hq) {  // a padding head: zero query (finite scores, never written out)
+    for (int e = tid; e < a.B * W; e += 256) {
+      const int b = e / W, c = e - b * W;
+      qa[((int64_t)b * a.Hp + h) * W + c] = (_Float16)0.0f;
+    }
+    return;
+  }
   for (int e = tid; e < a.B * kRope; e += 256) {
     const int b = e / kRope, j = e - b * kRope;
     const float x = load_in(a.q, a.q_f32, (((int64_t)li * a.B + b) * a.Hq + h) * qw + a.nope + j);
-    qa[((int64_t)b * a.Hq + h) * W + d + j] = (_Float16)(x * a.scale_log2);
+    qa[((int64_t)b * a.Hp + h) * W + d + j] = (_Float16)(x * a.scale_log2);
   }
   const uint16_t* wt = a.w_ukt + ((int64_t)li * a.Hq + h) * a.r * a.nope;
   for (int b0 = 0; b0 < a.B; b0 += 16) {
@@ -623,7 +631,7 @@ __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
         }
       }
       if (bq < a.B) {  // D[chan c + 4g + e][seq i16]
-        _Float16* dst = qa + ((int64_t)bq * a.Hq + h) * W + c + 4 * g;
+        _Float16* dst = qa + ((int64_t)bq * a.Hp + h) * W + c + 4 * g;
 #pragma unroll
         for (int e = 0; e < 4; ++e) dst[e] = (_Float16)(acc[e] * a.scale_log2);
       }
@@ -659,7 +667,7 @@ struct MlaDecodeArgs {
   MlaItem items[kMaxItems];
   int32_t n_items;
   int32_t n_wg;
-  int32_t B, Hq;
+  int32_t B, Hq;         // Hq: the padded head count (whole 32-head chunks)
   int32_t nbf;          // full blocks per stream
   int32_t ntail;        // tail tokens
   int32_t nb_cap;
@@ -686,13 +694,19 @@ struct Geo {
 };
 
 constexpr int kMaxTT = 16 * kWaves;                   // tokens per iteration at KS = 1
-constexpr int kTileHalfs = kMaxTT * (256 + kRope + 16);  // the largest TT * PH over the widths
+constexpr int kTileHalfs = kMaxTT * (256 + kRope + 16);  // the largest TT * PH over widths up to 512
+constexpr int kWideTileHalfs = Geo<1024>::TT * Geo<1024>::PH;  // kept width 1024
 constexpr int kSP = 20;                               // score rows: 16 tokens + pad (floats)
 constexpr int kPP = kMaxTT + 8;                       // probability rows: TT + pad (halfs)
+// Kept width 1024 holds the absorbed query of the workgroup's 32 heads in LDS
+// (rows of W + 8 halfs: 16 consecutive rows start 16 distinct 4-bank windows apart).
+constexpr int kWideQP = Geo<1024>::W + 8;
 
 // Vector-typed so that 16-byte accesses compile to single b128 LDS instructions.
+template <int TILE_HALFS, int Q_HALFS>
 struct MlaLds {
-  half8 tile[kTileHalfs / 8];   // fp16 latent rows of the iteration (swizzled)
+  half8 tile[TILE_HALFS / 8];   // fp16 latent rows of the iteration (swizzled)
+  half8 q[Q_HALFS > 0 ? Q_HALFS / 8 : 1];  // absorbed query [head][channel] (width 1024 only)
   f4 s[kWaves * 32 * kSP / 4];  // per wave: scores (partial over its channels) [head][token]
   half8 p[32 * kPP / 8];        // probabilities [head][k-slot]
   float alpha[32];
@@ -830,11 +844,25 @@ struct MlaState {
   float m, l;
 };
 
+// The absorbed query fragments of a wave (B operand of the scores: lane (head
+// 16 ht + i16, k-group g) holds channels 32 ks + 8 g .. + 7 of its channel part),
+// in registers (kept widths up to 512) ...
+template <int D>
+struct QRegs {
+  half8 v[Geo<D>::NKW][2];
+  __device__ __forceinline__ half8 get(int ks, int ht) const { return v[ks][ht]; }
+};
+// ... or read from the LDS copy (kept width 1024).
+struct QLds {
+  const half8* row[2];  // the lane's first fragment for head tiles 0 and 1
+  __device__ __forceinline__ half8 get(int ks, int ht) const { return row[ht][4 * ks]; }
+};
+
 // Phase A of an iteration for one wave: values of its 16 tokens x channel part into
 // the tile, and its partial scores S^T[token, head] over those channels.
-template <int D, int BITS, bool KIVI>
-__device__ __forceinline__ void mla_phase_a(const MlaRaw<D, BITS, KIVI>& r, const half8 (&qreg)[Geo<D>::NKW][2],
-                                            MlaLds& L, int wv, int tt, int kh, int lane) {
+template <int D, int BITS, bool KIVI, class LDS, class Q>
+__device__ __forceinline__ void mla_phase_a(const MlaRaw<D, BITS, KIVI>& r, const Q& qreg, LDS& L, int wv, int tt,
+                                            int kh, int lane) {
   using G = Geo<D>;
   const int g = lane >> 4, i16 = lane & 15;
   const int row = 16 * tt + i16;
@@ -844,8 +872,8 @@ __device__ __forceinline__ void mla_phase_a(const MlaRaw<D, BITS, KIVI>& r, cons
     const half8 x = mla_values<D, BITS, KIVI>(r, ks, g, kh);
     const int c0 = 32 * (kh * G::NKW + ks) + 8 * g;
     L.tile[tile_at<G::PH>(row, c0) >> 3] = x;
-    acc[0] = mfma16(x, qreg[ks][0], acc[0]);
-    acc[1] = mfma16(x, qreg[ks][1], acc[1]);
+    acc[0] = mfma16(x, qreg.get(ks, 0), acc[0]);
+    acc[1] = mfma16(x, qreg.get(ks, 1), acc[1]);
   }
 #pragma unroll
   for (int ht = 0; ht < 2; ++ht)
@@ -854,8 +882,8 @@ __device__ __forceinline__ void mla_phase_a(const MlaRaw<D, BITS, KIVI>& r, cons
 
 // Phases B (online softmax over the iteration's tokens; the first nvalid count)
 // and C (probabilities x latent), after phase A and a barrier.
-template <int D>
-__device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, MlaLds& L, int nvalid, int tid) {
+template <int D, class LDS>
+__device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, LDS& L, int nvalid, int tid) {
   using G = Geo<D>;
   constexpr int TPB = 2 * kWaves;      // softmax threads per head
   constexpr int TPT = G::TT / TPB;     // tokens per softmax thread
@@ -945,9 +973,9 @@ __device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, MlaLds& L, int nva
   }
 }
 
-template <int D, int BITS, bool KIVI, int POL>
+template <int D, int BITS, bool KIVI, int POL, class LDS>
 __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& it, int rl, int hc,
-                                        int b, int u, MlaLds& L) {
+                                        int b, int u, LDS& L) {
   using G = Geo<D>;
   constexpr int NR = kvk::mla_ring_depth(G::W, BITS, KIVI ? 1 : 0);
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, i16 = lane & 15;
@@ -966,22 +994,32 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
   for (int i = 0; i < NR; ++i) mla_issue<D, BITS, KIVI, POL>(ring[i], rs, (k0 + G::NBI * i + tblk) * bb, trow, g, kh);
 
   // absorbed query of the 32 heads over this wave's channel part, fp16
-  half8 qreg[G::NKW][2];
-  {
-    const _Float16* qb = reinterpret_cast<const _Float16*>(a.ws + it.q_off0 + (int64_t)rl * it.q_stride) +
-                         ((int64_t)b * a.Hq + 32 * hc) * G::W + 32 * kh * G::NKW + 8 * g;
+  const _Float16* qsrc = reinterpret_cast<const _Float16*>(a.ws + it.q_off0 + (int64_t)rl * it.q_stride) +
+                         ((int64_t)b * a.Hq + 32 * hc) * G::W;
+  using QT = typename std::conditional<(D > 512), QLds, QRegs<D>>::type;
+  QT qreg;
+  if constexpr (D > 512) {
+    // the whole [32][W] block into LDS; the loop's first barrier orders it before use
+    for (int e = tid; e < 32 * (G::W / 8); e += 64 * kWaves) {
+      const int h = e / (G::W / 8), c8 = e - h * (G::W / 8);
+      L.q[(h * kWideQP >> 3) + c8] = *reinterpret_cast<const half8*>(qsrc + (int64_t)h * G::W + 8 * c8);
+    }
+#pragma unroll
+    for (int ht = 0; ht < 2; ++ht) qreg.row[ht] = L.q + (((16 * ht + i16) * kWideQP + 32 * kh * G::NKW + 8 * g) >> 3);
+  } else {
+    const _Float16* qb = qsrc + 32 * kh * G::NKW + 8 * g;
 #pragma unroll
     for (int ht = 0; ht < 2; ++ht)
 #pragma unroll
       for (int ks = 0; ks < G::NKW; ++ks)
-        qreg[ks][ht] = *reinterpret_cast<const half8*>(qb + (int64_t)(16 * ht + i16) * G::W + 32 * ks);
+        qreg.v[ks][ht] = *reinterpret_cast<const half8*>(qb + (int64_t)(16 * ht + i16) * G::W + 32 * ks);
     // Consume the query here: its first use is then outside the loop, so the loop
     // waits only for the ring entry it uses (a first use inside the loop would make
     // every iteration wait for every load in flight).
 #pragma unroll
     for (int ht = 0; ht < 2; ++ht)
 #pragma unroll
-      for (int ks = 0; ks < G::NKW; ++ks) asm volatile("" ::"v"(qreg[ks][ht]));
+      for (int ks = 0; ks < G::NKW; ++ks) asm volatile("" ::"v"(qreg.v[ks][ht]));
   }
   MlaState<D> st;
   st.m = -INFINITY;
@@ -1033,13 +1071,13 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
   }
 }
 
-// POL: the loads' cache policy for every item of the launch (see mla_issue); the host
-// launches single-reader and multi-reader items separately.
-template <bool KIVI, int POL>
-__global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(MlaDecodeArgs a) {
-  __shared__ MlaLds L;
-  const int wg = blockIdx.x;
-  if (wg >= a.n_wg) return;
+// The item, reader row, head chunk, sequence and split of workgroup wg; false for
+// the padding workgroups of an item.  Workgroups of one (sequence, split) for the
+// different readers and head chunks sit 8 apart, so that they run on one XCD at
+// about the same time and share the stream through its L2.
+__device__ __forceinline__ bool mla_locate(const MlaDecodeArgs& a, int wg, int& item, int& rl, int& hc, int& b,
+                                           int& u) {
+  if (wg >= a.n_wg) return false;
   int lo = 0, hi = a.n_items - 1;  // last item with wg_begin <= wg
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
@@ -1047,17 +1085,29 @@ __global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(Mla
     else hi = mid - 1;
   }
   const MlaItem& it = a.items[lo];
-  // Workgroups of one (sequence, split) for the different readers and head chunks
-  // sit 8 apart, so that they run on one XCD at about the same time and share the
-  // stream through its L2.
   const int R = it.nreaders * it.nhc;
   const int local = wg - it.wg_begin;
   const int grp = local / (8 * R), rem = local - grp * 8 * R;
   const int row = rem >> 3;
   const int unit = 8 * grp + (rem & 7);
-  if (unit >= a.B * it.units) return;
-  const int b = unit / it.units, u = unit - b * it.units;
-  const int rl = row / it.nhc, hc = row - rl * it.nhc;
+  if (unit >= a.B * it.units) return false;
+  item = lo;
+  b = unit / it.units;
+  u = unit - b * it.units;
+  rl = row / it.nhc;
+  hc = row - rl * it.nhc;
+  return true;
+}
+
+// POL: the loads' cache policy for every item of the launch (see mla_issue); the host
+// launches single-reader and multi-reader items separately.  Kept widths up to 512:
+// two workgroups per CU.
+template <bool KIVI, int POL>
+__global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(MlaDecodeArgs a) {
+  __shared__ MlaLds<kTileHalfs, 0> L;
+  int item, rl, hc, b, u;
+  if (!mla_locate(a, blockIdx.x, item, rl, hc, b, u)) return;
+  const MlaItem& it = a.items[item];
 #define KVK_MLA_CASE(DD, BB)                            \
   if (it.d == DD && it.bits == BB) {                    \
     run_mla<DD, BB, KIVI, POL>(a, it, rl, hc, b, u, L); \
@@ -1069,6 +1119,19 @@ __global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(Mla
   KVK_MLA_D(128)
   KVK_MLA_D(64)
   KVK_MLA_D(32)
+}
+
+// Kept width 1024 (1088 stored channels): the product accumulators take 128
+// registers and the iteration's tile 70 KiB of LDS, so one workgroup per CU; the
+// absorbed query (136 registers per lane if held there) is read from a 70 KiB LDS
+// copy instead.
+template <bool KIVI, int POL>
+__global__ __launch_bounds__(64 * kWaves, 1) void mla_decode_wide_kernel(MlaDecodeArgs a) {
+  __shared__ MlaLds<kWideTileHalfs, 32 * kWideQP> L;
+  int item, rl, hc, b, u;
+  if (!mla_locate(a, blockIdx.x, item, rl, hc, b, u)) return;
+  const MlaItem& it = a.items[item];
+  KVK_MLA_D(1024)
 #undef KVK_MLA_D
 #undef KVK_MLA_CASE
 }
@@ -1085,14 +1148,15 @@ struct MlaCombineArgs {
   int32_t d_of[KVK_MAX_LAYERS];
   int32_t units[KVK_MAX_LAYERS];
   int32_t units_cap[KVK_MAX_LAYERS];
-  int32_t B, Hq, v, r;
+  int32_t B, Hq, Hp, v, r;  // Hp: heads per split partial record (padded)
 };
 
 // One workgroup per (layer, head): for 16 sequences at a time, merge the split
 // partials by log-sum-exp into o_lat (LDS, bf16 hi + lo), then multiply by
 // W_UV[h] on the matrix cores (M = value channels, K = d, N = sequences).
+template <int DMAX>
 __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
-  constexpr int PO = 512 + 8;  // LDS row pitch (bf16)
+  constexpr int PO = DMAX + 8;  // LDS row pitch (bf16)
   constexpr int kMaxU = kvk::kMlaMaxUnits;  // split weights held in LDS per sequence
   __shared__ uint16_t oh[16 * PO], ol[16 * PO];
   __shared__ float wgt[16 * kMaxU];
@@ -1100,7 +1164,7 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
   const int d = a.d_of[li], U = a.units[li], UC = a.units_cap[li];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
   const float* part = reinterpret_cast<const float*>(a.ws + a.part_off[li]);
-  const int64_t rec = (int64_t)a.Hq * (d + 2);
+  const int64_t rec = (int64_t)a.Hp * (d + 2);
   const uint16_t* wv_h = a.w_uv + ((int64_t)li * a.Hq + h) * a.v * a.r;
   for (int b0 = 0; b0 < a.B; b0 += 16) {
     const int nb = min(16, a.B - b0);
@@ -1115,7 +1179,7 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
       m = max16(m);
       float l = 0.0f;
       if (bi < nb && m > -INFINITY)
-        for (int u = p; u < U; u += 16) l += __builtin_amdgcn_exp2f(p0[u * rec + h] - m) * p0[u * rec + a.Hq + h];
+        for (int u = p; u < U; u += 16) l += __builtin_amdgcn_exp2f(p0[u * rec + h] - m) * p0[u * rec + a.Hp + h];
       l = sum16(l);
       const float inv = l > 0.0f ? 1.0f / l : 0.0f;
       for (int u = p; u < min(U, kMaxU); u += 16)
@@ -1126,7 +1190,7 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
       const int bi = e / (d / 4), c = 4 * (e - bi * (d / 4));
       f4 x = {0.f, 0.f, 0.f, 0.f};
       if (bi < nb) {
-        const float* o0 = part + (int64_t)(b0 + bi) * UC * rec + 2 * a.Hq + (int64_t)h * d + c;
+        const float* o0 = part + (int64_t)(b0 + bi) * UC * rec + 2 * a.Hp + (int64_t)h * d + c;
 #pragma unroll 4
         for (int u = 0; u < U; ++u) x += wgt[bi * kMaxU + u] * *reinterpret_cast<const f4*>(o0 + u * rec);
       }
@@ -1139,21 +1203,24 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
     }
     __syncthreads();
     for (int jt = wv; jt < a.v / 16; jt += 4) {
-      // A operands of the whole row tile first (independent loads), then the products
+      // A operands of 16 k-steps of the row tile first (independent loads), then the products
       const uint16_t* wrow = wv_h + (int64_t)(16 * jt + i16) * a.r + 8 * g;
       const int nks = d / 32;
-      u4v wa[16];
-#pragma unroll
-      for (int ks = 0; ks < 16; ++ks)
-        if (ks < nks) wa[ks] = *reinterpret_cast<const u4v*>(wrow + 32 * ks);
       f4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int k0 = 0; k0 < nks; k0 += 16) {
+        u4v wa[16];
 #pragma unroll
-      for (int ks = 0; ks < 16; ++ks) {
-        if (ks < nks) {
-          const bf16x8 bh = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&oh[i16 * PO + 32 * ks + 8 * g]));
-          const bf16x8 bl = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&ol[i16 * PO + 32 * ks + 8 * g]));
-          acc = mfmab(bitcast<bf16x8>(wa[ks]), bh, acc);
-          acc = mfmab(bitcast<bf16x8>(wa[ks]), bl, acc);
+        for (int ks = 0; ks < 16; ++ks)
+          if (k0 + ks < nks) wa[ks] = *reinterpret_cast<const u4v*>(wrow + 32 * (k0 + ks));
+#pragma unroll
+        for (int ks = 0; ks < 16; ++ks) {
+          if (k0 + ks < nks) {
+            const int c = 32 * (k0 + ks) + 8 * g;
+            const bf16x8 bh = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&oh[i16 * PO + c]));
+            const bf16x8 bl = bitcast<bf16x8>(*reinterpret_cast<const u4v*>(&ol[i16 * PO + c]));
+            acc = mfmab(bitcast<bf16x8>(wa[ks]), bh, acc);
+            acc = mfmab(bitcast<bf16x8>(wa[ks]), bl, acc);
+          }
         }
       }
       if (i16 < nb)  // D[value channel 16 jt + 4g + e][sequence b0 + i16]
@@ -1263,7 +1330,7 @@ kvk_status mla_compress_layer_project(const kvk_table* t, int32_t layer, const v
     else if (bits == 4) hipLaunchKernelGGL((mla_project_kernel<DD, 4, false>), g3, b3, 0, stream, a);         \
     else hipLaunchKernelGGL((mla_project_kernel<DD, 2, false>), g3, b3, 0, stream, a);                        \
   }
-  KVK_PROJ(512) else KVK_PROJ(256) else KVK_PROJ(128) else KVK_PROJ(64) else KVK_PROJ(32)
+  KVK_PROJ(1024) else KVK_PROJ(512) else KVK_PROJ(256) else KVK_PROJ(128) else KVK_PROJ(64) else KVK_PROJ(32)
   else return fail(KVK_ERR_UNSUPPORTED, "projected write: kept width %d", a.d);
 #undef KVK_PROJ
   const hipError_t e = hipGetLastError();
@@ -1304,6 +1371,7 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
   aa.q_f32 = q_dtype == KVK_F32;
   aa.B = d.batch;
   aa.Hq = d.n_q_heads;
+  aa.Hp = mla_heads_padded(d.n_q_heads);
   aa.nope = d.nope_dim;
   aa.r = d.latent_dim;
   aa.scale_log2 = scale * kLog2e;
@@ -1311,7 +1379,7 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     aa.q_off[l - l0] = ws.q_off[l];
     aa.d_of[l - l0] = t->rank[t->info.anchor_of[l]];
   }
-  hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)(l1 - l0), (unsigned)d.n_q_heads), dim3(256), 0,
+  hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)(l1 - l0), (unsigned)aa.Hp), dim3(256), 0,
                      stream, aa);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA absorb launch: %s", hipGetErrorString(e));
@@ -1323,15 +1391,17 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     // and needs no partials, so nothing is launched here.
     return KVK_OK;
   }
-  // Two launches: items whose stream one workgroup reads (non-temporal loads) and
-  // items read by the workgroups of several reader layers or head chunks (cached).
-  MlaDecodeArgs args[2];
-  int64_t wgs_of[2] = {0, 0};
+  // Up to four launches: items whose stream one workgroup reads (non-temporal loads)
+  // and items read by the workgroups of several reader layers or head chunks
+  // (cached), each for kept widths up to 512 and for 1024 (its own kernel).
+  // Launch k + 2 w: policy k, width class w.
+  MlaDecodeArgs args[4];
+  int64_t wgs_of[4] = {0, 0, 0, 0};
   for (MlaDecodeArgs& a : args) {
     a.arena = static_cast<const uint8_t*>(arena);
     a.ws = wsb;
     a.B = d.batch;
-    a.Hq = d.n_q_heads;
+    a.Hq = mla_heads_padded(d.n_q_heads);
     a.nbf = nbf;
     a.ntail = ntail;
     a.nb_cap = t->nb_cap;
@@ -1344,12 +1414,16 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     if (wgs > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "too many MLA decode workgroups");
     a.n_wg = (int32_t)wgs;
     const dim3 grid((unsigned)wgs), blk(64 * kWaves);
-    if (d.qscheme == KVK_Q_KIVI32) {
-      if (k == 0) hipLaunchKernelGGL((mla_decode_kernel<true, kStreamPolicy>), grid, blk, 0, stream, a);
-      else hipLaunchKernelGGL((mla_decode_kernel<true, 0>), grid, blk, 0, stream, a);
-    } else {
-      if (k == 0) hipLaunchKernelGGL((mla_decode_kernel<false, kStreamPolicy>), grid, blk, 0, stream, a);
-      else hipLaunchKernelGGL((mla_decode_kernel<false, 0>), grid, blk, 0, stream, a);
+    const bool kivi = d.qscheme == KVK_Q_KIVI32;
+    switch (k + 4 * (kivi ? 1 : 0)) {
+      case 0: hipLaunchKernelGGL((mla_decode_kernel<false, kStreamPolicy>), grid, blk, 0, stream, a); break;
+      case 1: hipLaunchKernelGGL((mla_decode_kernel<false, 0>), grid, blk, 0, stream, a); break;
+      case 2: hipLaunchKernelGGL((mla_decode_wide_kernel<false, kStreamPolicy>), grid, blk, 0, stream, a); break;
+      case 3: hipLaunchKernelGGL((mla_decode_wide_kernel<false, 0>), grid, blk, 0, stream, a); break;
+      case 4: hipLaunchKernelGGL((mla_decode_kernel<true, kStreamPolicy>), grid, blk, 0, stream, a); break;
+      case 5: hipLaunchKernelGGL((mla_decode_kernel<true, 0>), grid, blk, 0, stream, a); break;
+      case 6: hipLaunchKernelGGL((mla_decode_wide_kernel<true, kStreamPolicy>), grid, blk, 0, stream, a); break;
+      default: hipLaunchKernelGGL((mla_decode_wide_kernel<true, 0>), grid, blk, 0, stream, a); break;
     }
     const hipError_t err = hipGetLastError();
     if (err != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA decode launch: %s", hipGetErrorString(err));
@@ -1357,11 +1431,11 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     wgs = 0;
     return KVK_OK;
   };
-  const int nhc = d.n_q_heads / 32;
+  const int nhc = mla_heads_padded(d.n_q_heads) / 32;
   for (int l = l0; l < l1;) {
     const int anc = t->info.anchor_of[l];
     const int re = t->next_anchor[anc] < l1 ? t->next_anchor[anc] : l1;  // readers [l, re)
-    const int k = (re - l) * nhc > 1 ? 1 : 0;
+    const int k = ((re - l) * nhc > 1 ? 1 : 0) + (t->rank[anc] > 512 ? 2 : 0);
     MlaDecodeArgs& a = args[k];
     int64_t& wgs = wgs_of[k];
     if (a.n_items == kMaxItems) {
@@ -1388,8 +1462,11 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     wgs += (units + 7) / 8 * 8 * it.nreaders * nhc;
     l = re;
   }
-  const kvk_status st = flush(0);
-  return st != KVK_OK ? st : flush(1);
+  for (int k = 0; k < 4; ++k) {
+    const kvk_status st = flush(k);
+    if (st != KVK_OK) return st;
+  }
+  return KVK_OK;
 }
 
 kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored, const void* w_uv,
@@ -1403,17 +1480,21 @@ kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t 
   c.out = out;
   c.B = d.batch;
   c.Hq = d.n_q_heads;
+  c.Hp = mla_heads_padded(d.n_q_heads);
   c.v = d.v_dim;
   c.r = d.latent_dim;
+  int dmax = 0;
   for (int l = l0; l < l1; ++l) {
     const int anc = t->info.anchor_of[l];
     c.part_off[l - l0] = ws.part_off[l];
     c.d_of[l - l0] = t->rank[anc];
     c.units[l - l0] = n_stored > 0 ? mla_units(t, anc, n_stored) : 0;  // none: o = 0
     c.units_cap[l - l0] = ws.units_cap[l];
+    dmax = t->rank[anc] > dmax ? t->rank[anc] : dmax;
   }
-  hipLaunchKernelGGL(mla_combine_kernel, dim3((unsigned)(l1 - l0), (unsigned)d.n_q_heads), dim3(256), 0,
-                     stream, c);
+  const dim3 grid((unsigned)(l1 - l0), (unsigned)d.n_q_heads);
+  if (dmax > 512) hipLaunchKernelGGL(mla_combine_kernel<1024>, grid, dim3(256), 0, stream, c);
+  else hipLaunchKernelGGL(mla_combine_kernel<512>, grid, dim3(256), 0, stream, c);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA combine launch: %s", hipGetErrorString(e));
   return KVK_OK;

@@ -148,13 +148,13 @@ void mla_workspace(const kvk_table* t, int32_t l0, int32_t l1, MlaWorkspace* ws)
   for (int l = l0; l < l1; ++l) {
     const int32_t a = t->info.anchor_of[l];
     ws->q_off[l] = off;
-    off += round256((int64_t)d.batch * d.n_q_heads * (t->rank[a] + d.rope_dim) * 2);
+    off += round256((int64_t)d.batch * mla_heads_padded(d.n_q_heads) * (t->rank[a] + d.rope_dim) * 2);
   }
   for (int l = l0; l < l1; ++l) {
     const int32_t a = t->info.anchor_of[l];
     ws->units_cap[l] = mla_units(t, a, t->cap);
     ws->part_off[l] = off;
-    off += round256((int64_t)d.batch * ws->units_cap[l] * d.n_q_heads * (t->rank[a] + 2) * 4);
+    off += round256((int64_t)d.batch * ws->units_cap[l] * mla_heads_padded(d.n_q_heads) * (t->rank[a] + 2) * 4);
   }
   ws->total = off;
 }
@@ -164,8 +164,8 @@ void mla_workspace(const kvk_table* t, int32_t l0, int32_t l1, MlaWorkspace* ws)
 using namespace kvk;
 
 static kvk_status validate_mla(const kvk_dims& d, const kvk_action* plan) {
-  if (d.n_q_heads < 32 || d.n_q_heads % 32 != 0 || d.n_q_heads > 256)
-    return fail(KVK_ERR_UNSUPPORTED, "MLA n_q_heads %d must be a multiple of 32 up to 256",
+  if (d.n_q_heads < 8 || d.n_q_heads % 8 != 0 || d.n_q_heads > 256)
+    return fail(KVK_ERR_UNSUPPORTED, "MLA n_q_heads %d must be a multiple of 8 up to 256",
                 d.n_q_heads);
   if (d.n_kv_heads < 1 || d.head_dim < 1)
     return fail(KVK_ERR_INVALID, "MLA n_kv_heads/head_dim (the bf16 GQA reference of eq. (2)) must be >= 1");
@@ -185,8 +185,8 @@ static kvk_status validate_mla(const kvk_dims& d, const kvk_action* plan) {
     if (a.rank != r && a.rank != r / 2 && a.rank != r / 4 && a.rank != r / 8)
       return fail(KVK_ERR_INVALID, "layer %d: rank %d not in {r/8, r/4, r/2, r} with r = %d", l,
                   a.rank, r);
-    if (a.rank > 512)
-      return fail(KVK_ERR_UNSUPPORTED, "layer %d: kept width %d above 512 is not provided", l, a.rank);
+    if (a.rank > 1024)
+      return fail(KVK_ERR_UNSUPPORTED, "layer %d: kept width %d above 1024 is not provided", l, a.rank);
   }
   return KVK_OK;
 }

@@ -129,6 +129,7 @@ class MlaWorkload:
     qscheme: int = KIVI32
     ref_kv_heads: int = 4    # the bf16 GQA model eq. (2) is quoted against
     ref_head_dim: int = 128
+    d_model: int = 2048      # hidden-state width the down-projection W_DKV reads
     in_dtype: torch.dtype = torch.bfloat16
     q_dtype: torch.dtype = torch.bfloat16
     seed: int = 1003
@@ -167,7 +168,15 @@ def mla_workload(variant: Optional[str] = None) -> MlaWorkload:
     batch 16, context 16384, per-layer kept width drawn from {512, 256, 128, 64};
     variant None: bf16 cache, 'int4': KIVI32 4-bit latent and positional key;
     'depth' / 'int4-depth': the same with the layers in depth groups of 2-4 (one
-    anchor each, its kept width drawn as above)."""
+    anchor each, its kept width drawn as above).  '14b' / '14b-int4': Qwen2.5-14B's
+    latent shape (48 layers, 40 query heads, latent 1024 + 64, the bf16 GQA model
+    it is quoted against 8 KV heads of 128, model width 5120), batch 32, context
+    8192, kept widths drawn from {1024, 512, 256, 128}.  The 32-layer stack's model
+    width (for the projected write) is DeepSeek-V2-Lite's, 2048."""
+    if variant in ("14b", "14b-int4"):
+        bits = 4 if variant == "14b-int4" else 16
+        return MlaWorkload("mla-48l-r1024-" + ("bf16" if bits == 16 else "int4"), 48, 40, 1024, 32, 8192,
+                           plan_ranks(1007, 48, 1024, bits), ref_kv_heads=8, d_model=5120, seed=1007)
     bits = 4 if variant in ("int4", "int4-depth") else 16
     name = "mla-32l-r512-" + ("bf16" if bits == 16 else "int4")
     if variant in ("depth", "int4-depth"):

@@ -133,12 +133,15 @@ def test_qwen14b_shaped_128k_eviction():
     _run_workload(w, 4, 14)
 
 
-@pytest.mark.parametrize("variant", [None, "int4", "depth", "int4-depth"], ids=["bf16", "int4", "depth", "int4-depth"])
+@pytest.mark.parametrize("variant", [None, "int4", "depth", "int4-depth", "14b", "14b-int4"],
+                         ids=["bf16", "int4", "depth", "int4-depth", "14b-bf16", "14b-int4"])
 def test_mla_shaped_stack(variant):
-    """The MLA-style stack at full size: 32 layers, 32 heads, latent 512 + 64 kept to
-    per-layer widths, batch 16, context 16384, one decode call over all layers;
-    sampled (layer, sequence) streams bit-exact and their 32 output heads within
-    tolerance (oracle in the absorbed form, pinned equal to the reconstruction)."""
+    """The MLA-style stacks at full size (32 layers, 32 heads, latent 512 + 64,
+    batch 16, context 16384; and Qwen2.5-14B's latent shape: 48 layers, 40 heads,
+    latent 1024 + 64, batch 32, context 8192), kept to per-layer widths, one decode
+    call over all layers; sampled (layer, sequence) streams bit-exact and their
+    output heads within tolerance (oracle in the absorbed form, pinned equal to the
+    reconstruction).  A layer reading a full-width anchor is always sampled."""
     from oracle import mla as OM
     w = synth.mla_workload(variant)
     say(f"case {w.name}")
@@ -166,6 +169,9 @@ def test_mla_shaped_stack(variant):
     got_rows, ref_rows = [], []
     readers = [l for l in range(w.n_layers) if w.plan[l][0]]  # inheriting layers (depth variants)
     picks = [readers[int(rng.integers(len(readers)))] for _ in range(2)] if readers else []
+    full = [l for l in range(w.n_layers) if w.plan[info.anchor_of[l]][2] == w.latent_dim]
+    if full:
+        picks.append(full[int(rng.integers(len(full)))])
     picks += [int(rng.integers(w.n_layers)) for _ in range(4 - len(picks))]
     for l in picks:
         b = int(rng.integers(w.batch))

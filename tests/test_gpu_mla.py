@@ -218,3 +218,63 @@ def test_fp32_inputs_and_symrow_stack():
     wv = synth.weights_random(76, 3, 64, 128, 256)
     out = _np(c.decode(q, wk, wv, n, SCALE))
     assert rel_err(out, c.oracle_out(q, wk, wv, n, SCALE)) <= TOL
+
+
+@pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW], ids=["kivi32", "symrow"])
+@pytest.mark.parametrize("bits", [16, 8, 4, 2])
+def test_width_1024_qwen14b_heads(qs, bits):
+    """Qwen2.5-14B's latent shape: 40 query heads (two 32-head chunks inside, the
+    second padded), r 1024; a kept-width-1024 anchor read by two layers beside 512
+    and 128 anchors, 200 tokens (6 blocks + an 8-token tail); per-layer calls equal
+    the stacked call."""
+    say(f"case mla width-1024 Hq 40 qs={qs} bits={bits}")
+    plan = [(0, bits, 1024), (1, 16, 0), (0, 4, 512), (0, bits, 128)]
+    n, Hq, r = 200, 40, 1024
+    c = MlaCase(4, Hq, r, 2, 224, plan, qscheme=qs)
+    for l in (0, 2, 3):
+        c.compress(l, synth.latent_random(500 + l + bits, 2, n, r), synth.latent_random(600 + l, 2, n, 64), n)
+        c.check_layer(l, n)
+    q = synth.q_random(7 + bits, 4, 2, Hq, 192)
+    wk = synth.weights_random(8, 4, Hq, 128, r)
+    wv = synth.weights_random(9, 4, Hq, 128, r)
+    out = c.decode(q, wk, wv, n, SCALE)
+    err = rel_err(_np(out), c.oracle_out(q, wk, wv, n, SCALE))
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
+    for l in range(4):
+        one = c.decode(q[l:l + 1], wk[l:l + 1], wv[l:l + 1], n, SCALE, l, l + 1)
+        assert torch.equal(one[0], out[l]), f"layer {l}"
+
+
+@pytest.mark.parametrize("bits,n", [(4, 4000), (16, 7777), (2, 33)])
+def test_width_1024_single_reader_splits(bits, n):
+    """One reader of a kept-width-1024 stream (32 heads: the non-temporal launch),
+    several splits of the stream and a ragged tail (33: one block and one token)."""
+    say(f"case mla width-1024 single reader bits={bits} n={n}")
+    r = 1024
+    c = MlaCase(1, 32, r, 1, (n + 31) // 32 * 32, [(0, bits, r)])
+    c.compress(0, synth.latent_random(700 + bits, 1, n, r), synth.latent_random(701, 1, n, 64), n)
+    c.check_layer(0, n)
+    q = synth.q_random(702, 1, 1, 32, 192)
+    wk = synth.weights_random(703, 1, 32, 128, r)
+    wv = synth.weights_random(704, 1, 32, 128, r)
+    err = rel_err(_np(c.decode(q, wk, wv, n, SCALE)), c.oracle_out(q, wk, wv, n, SCALE))
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("Hq", [8, 16, 40, 72])
+def test_head_counts_padded_to_chunks(Hq):
+    """Query-head counts that are not whole 32-head chunks (padded inside) at r 512,
+    two layers (an anchor at 512 and one at 64 bits 4), 90 tokens."""
+    say(f"case mla Hq {Hq}")
+    n = 90
+    c = MlaCase(2, Hq, 512, 3, 96, [(0, 16, 512), (0, 4, 64)])
+    for l in range(2):
+        c.compress(l, synth.latent_random(800 + l, 3, n, 512), synth.latent_random(810 + l, 3, n, 64), n)
+    q = synth.q_random(820, 2, 3, Hq, 192)
+    wk = synth.weights_random(821, 2, Hq, 128, 512)
+    wv = synth.weights_random(822, 2, Hq, 128, 512)
+    err = rel_err(_np(c.decode(q, wk, wv, n, SCALE)), c.oracle_out(q, wk, wv, n, SCALE))
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL

@@ -127,8 +127,15 @@ def test_invalid_plans_and_dims():
     _expect(kvk.ERR_INVALID, kvk.layer_table, good, kvk.make_plan([(1, 16), (0, 4), (0, 4)]))
     _expect(kvk.ERR_INVALID, kvk.layer_table, good, kvk.make_plan([(0, 3), (0, 4), (0, 4)]))
     _expect(kvk.ERR_INVALID, kvk.layer_table, good, kvk.make_plan([(0, 4, 256), (0, 4), (0, 4)]))
-    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, kvk.make_dims(kvk.MLA, 3, 8, 2, 128, 512, 64, 128, 128,
-                                                                batch=1, max_tokens=8), ok_plan)
+    mla_plan = kvk.make_plan([(0, 4, 512), (1, 16, 0), (0, 2, 128)])
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, kvk.make_dims(kvk.MLA, 3, 12, 2, 128, 512, 64, 128, 128,
+                                                                batch=1, max_tokens=8), mla_plan)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, kvk.make_dims(kvk.MLA, 3, 32, 2, 128, 2048, 64, 128, 128,
+                                                                batch=1, max_tokens=8),
+            kvk.make_plan([(0, 4, 2048), (1, 16, 0), (0, 2, 256)]))
+    # Qwen2.5-14B's heads (40 query heads) at its full latent width 1024 + 64
+    kvk.layer_table(kvk.make_dims(kvk.MLA, 3, 40, 8, 128, 1024, 64, 128, 128, batch=1, max_tokens=8),
+                    kvk.make_plan([(0, 4, 1024), (1, 16, 0), (0, 2, 128)]))
     _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, kvk.make_dims(kvk.GQA, 3, 8, 2, 96, max_tokens=8), ok_plan)
     _expect(kvk.ERR_INVALID, kvk.layer_table, kvk.make_dims(kvk.GQA, 3, 6, 4, 128, max_tokens=8), ok_plan)
     _expect(kvk.ERR_INVALID, kvk.layer_table,
@@ -288,9 +295,12 @@ def test_mla_invalid_plans_and_dims():
     _expect(kvk.ERR_INVALID, kvk.layer_table, dims(r=300), ok)
     _expect(kvk.ERR_INVALID, kvk.layer_table, dims(Hkv=0), ok)
     _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(rope=32), ok)
-    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(Hq=16), ok)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(Hq=20), ok)
+    kvk.layer_table(dims(Hq=16), ok)
+    kvk.layer_table(dims(Hq=40), ok)
     _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(nope=100), ok)
-    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(r=1024), kvk.make_plan([(0, 4, 1024), (1, 16, 0)]))
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, dims(r=2048), kvk.make_plan([(0, 4, 2048), (1, 16, 0)]))
+    kvk.layer_table(dims(r=1024), kvk.make_plan([(0, 4, 1024), (1, 16, 0)]))
     kvk.layer_table(dims(r=1024), kvk.make_plan([(0, 4, 512), (0, 2, 128)]))
     g64 = kvk.make_dims(kvk.MLA, 2, 32, 4, 128, 512, 64, 128, 128, qscheme=kvk.GROUP64, batch=1, max_tokens=64)
     _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, g64, ok)  # the per-token 64-channel scheme is GQA-only
