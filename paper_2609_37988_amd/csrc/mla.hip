@@ -155,15 +155,16 @@ struct PrefillRows {
 // exactly slot (T NK + K) 64 + i + 16 g, so loads and stores need no staging.
 // KIVI32 groups (32 channels of one token) are the 4 lanes i, i + 16, i + 32, i + 48;
 // SYMROW scales (one per token and vector) come from a first pass through LDS.
-// Called by all 256 threads; as_bf16 writes the bf16 block instead.
+// Called by every thread of the workgroup (tid = threadIdx.x, nw waves); as_bf16
+// writes the bf16 block instead.
 template <int BITS, bool KIVI, class Src>
 __device__ __forceinline__ void mla_write_block(const Src& src, uint8_t* out, int d, bool as_bf16,
-                                                uint32_t (&amax)[2][32]) {
+                                                uint32_t (&amax)[2][32], int tid, int nw) {
 #pragma clang fp contract(off)
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, i = lane & 15, g = lane >> 4;
+  const int lane = tid & 63, wv = tid >> 6, i = lane & 15, g = lane >> 4;
   const int W = d + kRope, NK = W / 32;
   if (BITS == 16 || as_bf16) {  // bf16 block: 16 bytes (8 channels) per slot
-    for (int task = wv; task < 2 * NK; task += 4) {
+    for (int task = wv; task < 2 * NK; task += nw) {
       const int T = task / NK, K = task - T * NK;
       float x[8];
       src.load8(16 * T + i, 32 * K + 8 * g, x);
@@ -182,7 +183,7 @@ __device__ __forceinline__ void mla_write_block(const Src& src, uint8_t* out, in
     if constexpr (!KIVI) {
       if (tid < 64) amax[tid >> 5][tid & 31] = 0u;
       __syncthreads();
-      for (int task = wv; task < 2 * NK; task += 4) {
+      for (int task = wv; task < 2 * NK; task += nw) {
         const int T = task / NK, K = task - T * NK;
         float x[8];
         src.load8(16 * T + i, 32 * K + 8 * g, x);
@@ -194,7 +195,7 @@ __device__ __forceinline__ void mla_write_block(const Src& src, uint8_t* out, in
       }
       __syncthreads();
     }
-    for (int task = wv; task < 2 * NK; task += 4) {
+    for (int task = wv; task < 2 * NK; task += nw) {
       const int T = task / NK, K = task - T * NK, t = 16 * T + i;
       float x[8];
       src.load8(t, 32 * K + 8 * g, x);
@@ -260,7 +261,7 @@ __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
   const PrefillRows src{a, b, tok0, tail ? a.n_stored - tok0 : 32};
   uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
                  (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
-  mla_write_block<BITS, KIVI>(src, out, a.d, tail, amax);
+  mla_write_block<BITS, KIVI>(src, out, a.d, tail, amax, threadIdx.x, 4);
 }
 
 // ---------------------------------------------------------------------------
@@ -319,102 +320,145 @@ struct ProjectedRows {
   }
 };
 
-// One workgroup per (32-token block, sequence).  K loop over the model width in
-// steps of 32.  The block's 32 hidden-state rows, which every wave uses, are staged
-// in LDS (double-buffered: a thread loads its share of the next step into registers
-// while the current one is consumed, one barrier per step).  The rows of W_DKV are
-// each used by one wave only, so each wave loads its own straight into registers,
-// one step ahead.  Wave w computes the 16-channel tiles w, w + 4, ... for both
-// 16-token tiles (A = W_DKV rows, B = hidden rows: a lane's accumulator holds 4
-// consecutive channels of one token).
+// Geometry of the projected write for kept width D: TOK stored tokens per 8-wave
+// workgroup (whole 32-token blocks); the waves split into WC channel groups x WT
+// token groups, wave (wc, wt) owning CTW 16-channel tiles x TTW 16-token tiles of
+// the latent tile.  Each k-step (32 of the model width) stages the W_DKV rows and
+// the hidden-state rows in LDS (NBUF buffers, filled through registers one step
+// ahead); the finished latent tile then takes the LDS as bf16 rows of pitch LP.
+template <int D>
+struct ProjGeo {
+  static constexpr int TOK = D > 512 ? 64 : 128;
+  static constexpr int NBLK = TOK / 32;
+  static constexpr int CT = D / 16, TT = TOK / 16;
+  static constexpr int WC = CT < 8 ? CT : 8, WT = 8 / WC;
+  static constexpr int CTW = CT / WC, TTW = TT / WT;
+  static constexpr int KP = 32 + 8;                   // staging row pitch (halfs): 16 rows, 16 bank windows
+  static constexpr int NBUF = D > 512 ? 1 : 2;        // width 1024: one 85 KiB buffer
+  static constexpr int NW = (4 * D + 511) / 512;      // 16-byte W_DKV chunks a thread stages per k-step
+  static constexpr int LP = D + 8;                    // latent tile pitch (halfs)
+  static constexpr int STAGE = NBUF * (D + TOK) * KP;
+  static constexpr int LDS_HALFS = STAGE > TOK * LP ? STAGE : TOK * LP;
+  static_assert(CT % WC == 0 && TT % WT == 0 && 4 * TOK <= 512, "tiles must split evenly over the waves");
+};
+
+// One 512-thread workgroup per (TOK stored tokens, sequence): the latent tile
+// C[token][channel] = sum_k X[token][k] W[channel][k] on MFMA (A = W_DKV rows,
+// B = hidden rows: a lane's accumulator holds 4 consecutive channels of one token),
+// rounded to bf16 into LDS, then the tile's blocks (and the stream's tail block)
+// written by the block writer with all 8 waves.
 template <int D, int BITS, bool KIVI>
-__global__ __launch_bounds__(256) void mla_project_kernel(MlaProjectArgs a) {
-  constexpr int KP = 32 + 8;                 // staging row pitch (halfs)
-  constexpr int NT = D / 16;                 // channel tiles
-  constexpr int NTW = (NT + 3) / 4;          // per wave
-  constexpr int LP = D + 8;                  // latent tile pitch (halfs)
-  __shared__ __attribute__((aligned(16))) uint16_t xs[2 * 32 * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t lat[32 * LP];
+__global__ __launch_bounds__(512) void mla_project_kernel(MlaProjectArgs a) {
+  using P = ProjGeo<D>;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[P::LDS_HALFS];
   __shared__ uint32_t amax[2][32];
-  const int blk = blockIdx.x, b = blockIdx.y;
-  const bool tail = blk == a.nbf;
-  const int tok0 = 32 * blk;
-  const int ntok = tail ? a.n_stored - tok0 : 32;
+  const int wg = blockIdx.x, b = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, i16 = lane & 15, kg = lane >> 4;
-  // staging share (threads < 128): hidden row tid / 4, 8 k at 8 (tid % 4)
-  const int xr = (tid >> 2) & 31, xk = 8 * (tid & 3);
-  const bool x_ok = tid < 128 && xr < ntok;
-  // (a thread with no row reads stored token 0's keep entry: the tail block of a
-  // whole number of groups has no rows at all)
-  const uint16_t* xp =
-      a.x + ((int64_t)b * a.n_tokens + mla_stored_pos(a.keep, b, a.n_stored, a.n_tokens, x_ok ? tok0 + xr : 0)) *
-                a.H + xk;
-  const uint16_t* wp[NTW];  // the wave's W_DKV rows: tile wv + 4 j, row i16, k at 8 kg
+  const int wc = wv % P::WC, wt = wv / P::WC;
+  const int row0 = P::TOK * wg;                         // first stored token of the tile
+  const int nrow = min(P::TOK, a.n_stored - row0);      // may be <= 0 (the tail slot only)
+  constexpr int BUF = (D + P::TOK) * P::KP;             // halfs per staging buffer: W rows, then hidden rows
+  // W_DKV staging: chunk c = tid + 512 n < 4 D is row c / 4, k 8 (c % 4)
+  const uint16_t* wsrc = a.w + (int64_t)(tid >> 2) * a.H + 8 * (tid & 3);
+  const int64_t wstep = (int64_t)128 * a.H;             // 512 chunks = 128 rows further
+  // hidden-row staging: thread tid < 4 TOK moves row tid / 4, k 8 (tid % 4)
+  const int xr = tid >> 2, xk = 8 * (tid & 3);
+  const bool x_stager = tid < 4 * P::TOK, x_ok = x_stager && xr < nrow;
+  const uint16_t* xsrc = a.x + ((int64_t)b * a.n_tokens +
+                                mla_stored_pos(a.keep, b, a.n_stored, a.n_tokens, x_ok ? row0 + xr : 0)) * a.H + xk;
+  u4v wr[P::NW];
+  auto fetch_w = [&](int k0) {
 #pragma unroll
-  for (int j = 0; j < NTW; ++j) wp[j] = a.w + (int64_t)(16 * min(wv + 4 * j, NT - 1) + i16) * a.H + 8 * kg;
-  u4v xreg;
-  bf16x8 wcur[NTW], wnext[NTW];
-  auto fetch_w = [&](int k0, bf16x8 (&dst)[NTW]) {
-#pragma unroll
-    for (int j = 0; j < NTW; ++j)
-      if (NT % 4 == 0 || wv + 4 * j < NT) dst[j] = *reinterpret_cast<const bf16x8*>(wp[j] + k0);
+    for (int n = 0; n < P::NW; ++n)
+      if (tid + 512 * n < 4 * D) wr[n] = *reinterpret_cast<const u4v*>(wsrc + n * wstep + k0);
   };
-  f4 acc[2][NTW];
+  auto store_w = [&](uint16_t* buf) {
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+    for (int n = 0; n < P::NW; ++n)
+      if (tid + 512 * n < 4 * D)
+        *reinterpret_cast<u4v*>(buf + (xr + 128 * n) * P::KP + xk) = wr[n];
+  };
+  auto fetch_x = [&](u4v& r, int k0) {
+    r = x_ok ? *reinterpret_cast<const u4v*>(xsrc + k0) : u4v{0u, 0u, 0u, 0u};
+  };
+  auto store_x = [&](const u4v& r, uint16_t* buf) {
+    if (x_stager) *reinterpret_cast<u4v*>(buf + (D + xr) * P::KP + xk) = r;
+  };
+  f4 acc[P::CTW][P::TTW];
 #pragma unroll
-    for (int j = 0; j < NTW; ++j) acc[m][j] = f4{0.f, 0.f, 0.f, 0.f};
-  if (ntok > 0) {
-    xreg = x_ok ? *reinterpret_cast<const u4v*>(xp) : u4v{0u, 0u, 0u, 0u};
-    fetch_w(0, wcur);
-    if (tid < 128) *reinterpret_cast<u4v*>(xs + xr * KP + xk) = xreg;
-    __syncthreads();
-    int buf = 0;
-    for (int k0 = 0; k0 < a.H; k0 += 32, buf ^= 1) {
-      const bool more = k0 + 32 < a.H;  // uniform
-      if (more) {
-        xreg = x_ok ? *reinterpret_cast<const u4v*>(xp + k0 + 32) : u4v{0u, 0u, 0u, 0u};
-        fetch_w(k0 + 32, wnext);
-      }
-      bf16x8 xb[2];
+  for (int j = 0; j < P::CTW; ++j)
 #pragma unroll
-      for (int m = 0; m < 2; ++m) xb[m] = *reinterpret_cast<const bf16x8*>(xs + (buf * 32 + 16 * m + i16) * KP + 8 * kg);
+    for (int m = 0; m < P::TTW; ++m) acc[j][m] = f4{0.f, 0.f, 0.f, 0.f};
+  // the products of one k-step from a staging buffer
+  auto step = [&](const uint16_t* base) {
+    bf16x8 xb[P::TTW];
 #pragma unroll
-      for (int j = 0; j < NTW; ++j)
-        if (NT % 4 == 0 || wv + 4 * j < NT)
+    for (int m = 0; m < P::TTW; ++m)
+      xb[m] = *reinterpret_cast<const bf16x8*>(base + (D + 16 * (wt * P::TTW + m) + i16) * P::KP + 8 * kg);
 #pragma unroll
-          for (int m = 0; m < 2; ++m) acc[m][j] = mfmab(wcur[j], xb[m], acc[m][j]);
-      if (more) {
-        if (tid < 128) *reinterpret_cast<u4v*>(xs + ((buf ^ 1) * 32 + xr) * KP + xk) = xreg;  // read before the last barrier
+    for (int j = 0; j < P::CTW; ++j) {
+      const bf16x8 wa = *reinterpret_cast<const bf16x8*>(base + (16 * (wc * P::CTW + j) + i16) * P::KP + 8 * kg);
 #pragma unroll
-        for (int j = 0; j < NTW; ++j) wcur[j] = wnext[j];
+      for (int m = 0; m < P::TTW; ++m) acc[j][m] = mfmab(wa, xb[m], acc[j][m]);
+    }
+  };
+  const int nks = a.H / 32;
+  u4v xr0;
+  fetch_w(0);
+  fetch_x(xr0, 0);
+  store_w(lds);
+  store_x(xr0, lds);
+  __syncthreads();
+  for (int ks = 0; ks < nks; ++ks) {
+    const int buf = P::NBUF == 2 ? (ks & 1) : 0;
+    const bool more = ks + 1 < nks;  // uniform
+    if (more) {
+      fetch_w(32 * (ks + 1));
+      fetch_x(xr0, 32 * (ks + 1));
+    }
+    step(lds + buf * BUF);
+    if constexpr (P::NBUF == 2) {
+      if (more) {  // the other buffer was last read before the previous barrier
+        store_w(lds + (buf ^ 1) * BUF);
+        store_x(xr0, lds + (buf ^ 1) * BUF);
       }
       __syncthreads();
+    } else {
+      __syncthreads();  // every wave is done with the buffer
+      if (more) {
+        store_w(lds);
+        store_x(xr0, lds);
+        __syncthreads();
+      }
     }
   }
-  // the latent tile, bf16: lane (token 16 m + i16, kg) holds channels 16 ct + 4 kg .. + 3
+  // the latent tile, bf16, over the staging buffers (all reads of them are done)
 #pragma unroll
-  for (int m = 0; m < 2; ++m) {
-    const int t = 16 * m + i16;
+  for (int j = 0; j < P::CTW; ++j) {
+    const int c = 16 * (wc * P::CTW + j) + 4 * kg;
 #pragma unroll
-    for (int j = 0; j < NTW; ++j) {
-      const int ct = wv + 4 * j;
-      if (NT % 4 == 0 || ct < NT) {
-        const int c = 16 * ct + 4 * kg;
-        u2v w2;
-        w2[0] = (uint32_t)f32_to_bf16_bits(acc[m][j][0]) | ((uint32_t)f32_to_bf16_bits(acc[m][j][1]) << 16);
-        w2[1] = (uint32_t)f32_to_bf16_bits(acc[m][j][2]) | ((uint32_t)f32_to_bf16_bits(acc[m][j][3]) << 16);
-        *reinterpret_cast<u2v*>(lat + t * LP + c) = w2;
-        if (a.latent_out && t < ntok)
-          *reinterpret_cast<u2v*>(a.latent_out + ((int64_t)b * a.n_stored + tok0 + t) * a.d + c) = w2;
-      }
+    for (int m = 0; m < P::TTW; ++m) {
+      const int t = 16 * (wt * P::TTW + m) + i16;
+      u2v w2;
+      w2[0] = (uint32_t)f32_to_bf16_bits(acc[j][m][0]) | ((uint32_t)f32_to_bf16_bits(acc[j][m][1]) << 16);
+      w2[1] = (uint32_t)f32_to_bf16_bits(acc[j][m][2]) | ((uint32_t)f32_to_bf16_bits(acc[j][m][3]) << 16);
+      *reinterpret_cast<u2v*>(lds + t * P::LP + c) = w2;
+      if (a.latent_out && t < nrow)
+        *reinterpret_cast<u2v*>(a.latent_out + ((int64_t)b * a.n_stored + row0 + t) * a.d + c) = w2;
     }
   }
   __syncthreads();
-  const ProjectedRows src{a, lat, LP, b, tok0, ntok};
-  uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
-                 (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
-  mla_write_block<BITS, KIVI>(src, out, D, tail, amax);
+  // block slots 0 .. nbf - 1 are full blocks, slot nbf the stream's bf16 tail block
+  for (int k = 0; k < P::NBLK; ++k) {
+    const int slot = P::NBLK * wg + k;  // uniform
+    if (slot > a.nbf) break;
+    const bool tail = slot == a.nbf;
+    const ProjectedRows src_rows{a, lds + 32 * k * P::LP, P::LP, b, 32 * slot, tail ? a.n_stored - 32 * slot : 32};
+    uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
+                   (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)slot * a.block_bytes);
+    mla_write_block<BITS, KIVI>(src_rows, out, D, tail, amax, tid, 8);
+    if constexpr (!KIVI) __syncthreads();  // amax is reused by the next block
+  }
 }
 
 // Decode-time append of one token to every MLA anchor of a layer range.
@@ -503,10 +547,10 @@ __global__ __launch_bounds__(256) void mla_append_kernel(MlaAppendArgs a) {
   const TailRows src{a, it, tail, b, NK};
   uint8_t* out = base + (int64_t)(a.pos >> 5) * it.block_bytes;
   switch (it.bits) {
-    case 16: mla_write_block<16, KIVI>(src, out, it.d, true, amax); break;
-    case 8: mla_write_block<8, KIVI>(src, out, it.d, false, amax); break;
-    case 4: mla_write_block<4, KIVI>(src, out, it.d, false, amax); break;
-    default: mla_write_block<2, KIVI>(src, out, it.d, false, amax); break;
+    case 16: mla_write_block<16, KIVI>(src, out, it.d, true, amax, threadIdx.x, 4); break;
+    case 8: mla_write_block<8, KIVI>(src, out, it.d, false, amax, threadIdx.x, 4); break;
+    case 4: mla_write_block<4, KIVI>(src, out, it.d, false, amax, threadIdx.x, 4); break;
+    default: mla_write_block<2, KIVI>(src, out, it.d, false, amax, threadIdx.x, 4); break;
   }
 }
 
@@ -1319,7 +1363,8 @@ kvk_status mla_compress_layer_project(const kvk_table* t, int32_t layer, const v
   a.d = t->rank[layer];
   const int bits = t->bits[layer];
   const bool kivi = d.qscheme == KVK_Q_KIVI32;
-  const dim3 g3((unsigned)(a.nbf + 1), (unsigned)d.batch), b3(256);
+  const int tok = a.d > 512 ? ProjGeo<1024>::TOK : ProjGeo<512>::TOK;  // stored tokens per workgroup
+  const dim3 g3((unsigned)((a.nbf + 1 + tok / 32 - 1) / (tok / 32)), (unsigned)d.batch), b3(512);
 #define KVK_PROJ(DD)                                                                                          \
   if (a.d == DD) {                                                                                            \
     if (bits == 16) hipLaunchKernelGGL((mla_project_kernel<DD, 16, true>), g3, b3, 0, stream, a);              \
