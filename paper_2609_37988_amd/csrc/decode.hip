@@ -1033,10 +1033,9 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
         it.bits = s->bits[anc];
         it.q_layer0 = rb - l0;
         it.geff = G * (re - rb);
-        it.split_blocks = split_blocks_for(it.bits, d.qscheme, D, nbf_split, split_target);
+        it.split_blocks = gqa_item_split_blocks(s, anc, l0, l1, nbf_split, split_target);
         it.nsplit = n_splits(nbf_split, it.split_blocks);
-        const int nch = (it.geff + 15) / 16;
-        it.nchp = nch == 1 ? 1 : (nch == 2 ? 2 : (nch + 3) / 4 * 4);
+        it.nchp = gqa_chunk_waves((it.geff + 15) / 16);
         it.b0 = b0;
         it.nb = nb;
         it.ws_off = (int32_t)ws_floats;

@@ -98,7 +98,18 @@ inline int32_t ring_depth_for(int32_t bits) { return gqa_ring_depth(bits); }
 // Blocks processed per split of the decode kernel for a `bits`-bit anchor whose
 // streams hold n_blocks full blocks.  The split count never exceeds the one at a
 // larger n_blocks, so workspace sized at capacity covers every n_stored.
-int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes);
+// `waves` D1 waves read each split (an item's chunk waves), so its target and its
+// bounds are that many times the per-wave ones.
+int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes,
+                         int32_t waves);
+// D1 waves per (stream, split) of an item whose anchor's readers give nch 16-row
+// query chunks: 1, 2, or a multiple of 4 (up to 4 share a workgroup, more fill
+// several).
+constexpr int32_t gqa_chunk_waves(int32_t nch) { return nch == 1 ? 1 : (nch == 2 ? 2 : (nch + 3) / 4 * 4); }
+// Full blocks per split of the D1 item of `anchor` read by the layers of [l0, l1)
+// in table s (split_blocks_for with the item's chunk waves in one workgroup).
+int32_t gqa_item_split_blocks(const kvk_table* s, int32_t anchor, int32_t l0, int32_t l1, int32_t n_blocks,
+                              int64_t target_bytes);
 // Bytes per D1 split for a decode over layers [l0, l1) of a GQA table (see table.cpp).
 int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1);
 

@@ -82,11 +82,17 @@ int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1) {
   return total / kSplitWaves;  // clamped per precision by split_blocks_for
 }
 
-int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes) {
+int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes,
+                         int32_t waves) {
   // target_bytes of cache per wave (gqa_split_target); the stream's blocks are
   // divided evenly so that no split is a short remainder, in a multiple of the
   // decode kernel's prefetch depth so that only a stream's last split runs past
-  // its end.
+  // its end.  A split read by `waves` chunk waves (an anchor with many reader rows)
+  // is that many times as long: the launch's wave count is what the target sizes,
+  // and every split re-reads the item's queries and writes partials for all its
+  // rows (one anchor read by 48 layers at 14B: 240 rows, 61 KiB of queries and
+  // 127 KiB of partials per split and stream; 357 MB of partials per step with
+  // per-wave splits, 97 MB with 4x longer ones).
   const int64_t bb = gqa_block_bytes(head_dim, bits, qscheme);
   const int64_t nr = ring_depth_for(bits);
   // The 8- and 16-bit paths stream: splits between 1 and 16 MiB.  The 2- and 4-bit
@@ -95,7 +101,9 @@ int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_
   // at most 1 MiB and shorter when the launch would otherwise hold fewer waves than
   // about two per wave slot (7B shape, 28 layers x 32 streams: 1 MiB splits gave the
   // int2 stack 896 waves for 2048 slots), down to 128 KiB.
-  const int64_t lo = bits <= 4 ? (128LL << 10) : (1LL << 20), hi = bits <= 4 ? (1LL << 20) : (16LL << 20);
+  const int64_t w = waves > 1 ? waves : 1;
+  const int64_t lo = w * (bits <= 4 ? (128LL << 10) : (1LL << 20)), hi = w * (bits <= 4 ? (1LL << 20) : (16LL << 20));
+  target_bytes *= w;
   int64_t target = (target_bytes < lo ? lo : (target_bytes > hi ? hi : target_bytes)) / bb;
   if (target < nr) target = nr;
   const int64_t nb = n_blocks > 0 ? n_blocks : 1;
@@ -103,6 +111,21 @@ int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_
   int64_t per = (nb + nsplit - 1) / nsplit;
   per = (per + nr - 1) / nr * nr;
   return (int32_t)per;
+}
+
+int32_t gqa_item_split_blocks(const kvk_table* s, int32_t anchor, int32_t l0, int32_t l1, int32_t n_blocks,
+                              int64_t target_bytes) {
+  const int32_t G = s->d.n_q_heads / s->d.n_kv_heads;
+  const int32_t rb = anchor > l0 ? anchor : l0;
+  const int32_t re = s->next_anchor[anchor] < l1 ? s->next_anchor[anchor] : l1;
+  const int32_t nch = (G * (re - rb) + 15) / 16;
+  // Only the chunk waves of one workgroup (up to 4) lengthen the split: the several
+  // workgroups of a larger unit drift apart over a long split and then read it from
+  // HBM again (one int4 anchor for 48 layers at 14B, 16 chunk waves: FETCH 1.38x the
+  // cache bytes with per-wave splits, 1.19x with 4x longer ones, 1.41x with 8x, 1.69x
+  // with 16x).
+  const int32_t w = gqa_chunk_waves(nch);
+  return split_blocks_for(s->bits[anchor], s->d.qscheme, s->d.head_dim, n_blocks, target_bytes, w < 4 ? w : 4);
 }
 
 int64_t mla_block_bytes(int32_t W, int32_t bits, int32_t qscheme) {
@@ -126,7 +149,15 @@ int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_block
                      mla_iter_blocks(W);  // blocks per pass of the ring
   // bf16 streams are bound by HBM and take twice as long splits (fewer workgroup
   // starts: MLA stack 0.96 -> 0.93 ms); the dequantising paths keep the shorter ones.
-  int64_t target = (t->bits[anchor] == 16 ? 2 : 1) * (int64_t)KVK_MLA_SPLIT_UNITS / (W + 192);
+  // A bf16 anchor read by several layers (one workgroup per reader, sharing the
+  // stream through L2) takes half the dequantising length instead: over longer
+  // splits the readers drift apart and fetch the stream again (depth-grouped MLA
+  // stack: 1.37x the cache bytes fetched at the long length, 1.19x at a quarter of
+  // it, 705 -> 692 us; the int4 form is unchanged by the length, 1.16-1.17x, the
+  // readers' absorbed queries).
+  const bool shared = t->next_anchor[anchor] - anchor > 1;
+  int64_t target = (int64_t)KVK_MLA_SPLIT_UNITS / (W + 192);
+  if (t->bits[anchor] == 16) target = shared ? target / 2 : 2 * target;
   if (target < nr) target = nr;
   const int64_t nb = n_blocks > 0 ? n_blocks : 1;
   if (target * kMlaMaxUnits < nb) target = (nb + kMlaMaxUnits - 1) / kMlaMaxUnits;  // merge limit
@@ -408,7 +439,7 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
   size_t floats = 0;
   for (int l = l0; l < l1; ++l) {
     const int32_t a = t->info.anchor_of[l];
-    const int32_t sb = split_blocks_for(t->bits[a], d.qscheme, d.head_dim, nblk, target);
+    const int32_t sb = gqa_item_split_blocks(t, a, l0, l1, nblk, target);
     floats += (size_t)d.batch * d.n_kv_heads * G * n_splits(nblk, sb) * (d.head_dim + 4);
   }
   *out = (size_t)round256((int64_t)(floats * sizeof(float)));
