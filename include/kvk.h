@@ -326,6 +326,28 @@ kvk_status kvk_compress_layer_project(const kvk_table* table, int32_t layer, con
                                       int32_t d_model, const void* k_rope, int32_t n_tokens,
                                       const int32_t* keep_idx, void* arena, void* latent_out, hipStream_t stream);
 
+/* W_UK in the layout the query absorption reads (App. C.2: the content-key
+ * projection folds into the query, q~ = W_UK[h]^T q_nope, so the library reads
+ * W_UK[h] latent-major).  Transposes every (layer, head) matrix on the device.
+ *   w_uk : device bf16 [n_layers][n_heads][nope_dim][latent_dim], the model's layout
+ *          (row i of W_UK[h] maps the latent to content-key channel i).
+ *   out  : device bf16 [n_layers][n_heads][latent_dim][nope_dim]; must not alias w_uk.
+ * nope_dim and latent_dim multiples of 32; both buffers 16-byte aligned.  Asynchronous
+ * on `stream`.  Errors: KVK_ERR_INVALID (sizes, NULL, aliasing, misalignment, host
+ * memory), KVK_ERR_DEVICE. */
+kvk_status kvk_mla_arrange_w_uk(const void* w_uk, int32_t n_layers, int32_t n_heads, int32_t nope_dim,
+                                int32_t latent_dim, void* out, hipStream_t stream);
+
+/* Attach an MLA table's up-projections for all its layers (App. C.2): w_uk as
+ * kvk_mla_arrange_w_uk writes it, [n_layers][Hq][r][nope_dim], and w_uv
+ * [n_layers][Hq][v_dim][r], both device bf16, 16-byte aligned.  Decode calls that
+ * pass NULL for both weights then use these from their first layer on.  The
+ * buffers stay owned by the caller and must outlive their use; NULL for both
+ * detaches.  Not to be called while a decode call on the table runs on another
+ * thread.  Errors: KVK_ERR_INVALID (GQA table, one weight NULL, misalignment, host
+ * memory). */
+kvk_status kvk_set_mla_weights(kvk_table* table, const void* w_uk, const void* w_uv);
+
 /* Decode-time append of one generated token to every anchor layer in
  * [layer_begin, layer_end).  The plan chosen at prefill holds for the whole
  * generation (§2.3), so each anchor keeps its configuration: the new token enters
@@ -462,9 +484,11 @@ kvk_status kvk_decode_setup(const kvk_table* table, int32_t layer_begin, int32_t
  *   w_uk     : device bf16 [nl][Hq][r][nope_dim]: layer l's W_UK, the map from the
  *              latent to head h's content key (k = W_UK[h] c), stored transposed
  *              (latent-major: element (i, c) of W_UK[h] at [h][c][i]), the layout the
- *              query absorption reads contiguously; callers arrange it once when
- *              they load the weights.
+ *              query absorption reads contiguously (kvk_mla_arrange_w_uk makes it
+ *              from the model's layout once, at weight load).
  *   w_uv     : device bf16 [nl][Hq][v_dim][r]: layer l's W_UV (v = W_UV[h] c).
+ *   Both NULL: the weights attached by kvk_set_mla_weights, from layer_begin on
+ *              (KVK_ERR_INVALID if none are attached); pass both or neither.
  *   out      : device fp32 [nl][B][Hq][v_dim].
  *   Head h of layer l attends with query [q_nope ; q_rope] to keys
  *   [W_UK[h] c_t ; k^R_t] and values W_UV[h] c_t, where c_t is the stored latent

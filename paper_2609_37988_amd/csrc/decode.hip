@@ -1185,6 +1185,15 @@ kvk_status launch_c1(const DecodePlan& P, hipStream_t st) {
   return KVK_OK;
 }
 
+// An MLA decode call that passes neither weight uses the table's attached ones
+// (kvk_set_mla_weights), from the range's first layer on.
+void mla_attached_weights(const kvk_table* t, int32_t l0, const void*& w_uk, const void*& w_uv) {
+  const kvk_dims& d = t->d;
+  if (d.kind != KVK_MLA || w_uk || w_uv || !t->mla_w_uk || l0 < 0 || l0 >= d.n_layers) return;
+  w_uk = static_cast<const uint8_t*>(t->mla_w_uk) + (int64_t)l0 * d.n_q_heads * d.latent_dim * d.nope_dim * 2;
+  w_uv = static_cast<const uint8_t*>(t->mla_w_uv) + (int64_t)l0 * d.n_q_heads * d.v_dim * d.latent_dim * 2;
+}
+
 // Argument checks shared by the MLA decode entry points.
 kvk_status mla_check(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
                      int32_t n_stored, float scale, const void* w_uk, const void* w_uv,
@@ -1223,6 +1232,7 @@ extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32
                                            float* out, void* workspace, size_t ws_bytes,
                                            hipStream_t stream) {
   if (t && t->d.kind == KVK_MLA) {
+    mla_attached_weights(t, l0, w_uk, w_uv);
     kvk_status st = mla_check(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
                               ws_bytes);
     if (st != KVK_OK) return st;
@@ -1244,6 +1254,7 @@ extern "C" kvk_status kvk_decode_splits(const kvk_table* t, int32_t l0, int32_t 
                                         const void* w_uk, const void* w_uv, const void* arena,
                                         void* workspace, size_t ws_bytes, hipStream_t stream) {
   if (t && t->d.kind == KVK_MLA) {
+    mla_attached_weights(t, l0, w_uk, w_uv);
     const kvk_status st = mla_check(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, workspace,
                                     workspace, ws_bytes);
     if (st != KVK_OK) return st;
@@ -1263,6 +1274,7 @@ extern "C" kvk_status kvk_decode_merge(const kvk_table* t, int32_t l0, int32_t l
                                        const void* workspace, size_t ws_bytes, float* out,
                                        hipStream_t stream) {
   if (t && t->d.kind == KVK_MLA) {
+    mla_attached_weights(t, l0, w_uk, w_uv);
     const kvk_status st = mla_check(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out,
                                     workspace, ws_bytes);
     if (st != KVK_OK) return st;

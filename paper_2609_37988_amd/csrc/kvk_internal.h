@@ -34,6 +34,10 @@ struct kvk_table {
   };
   mutable std::mutex setup_mu;
   mutable std::vector<DecodeSetup> setups;
+  // MLA: the all-layer W_UK (latent-major) and W_UV attached by kvk_set_mla_weights
+  // (caller-owned device memory), used by decode calls that pass no weights.
+  const void* mla_w_uk = nullptr;
+  const void* mla_w_uv = nullptr;
   ~kvk_table() {
     for (kvk_table* s : seq) delete s;
   }

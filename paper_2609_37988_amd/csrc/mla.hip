@@ -1273,6 +1273,28 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
   }
 }
 
+// W_UK from the model's layout ([nl][Hq][nope][r]) to the latent-major one the
+// absorption reads ([nl][Hq][r][nope]): one 32 x 32 tile per workgroup through LDS
+// (rows of 33 halfs), 8-byte accesses coalesced on both sides.
+__global__ __launch_bounds__(256) void mla_arrange_w_uk_kernel(const uint16_t* in, uint16_t* out, int nope, int r) {
+  __shared__ uint16_t tile[32][33];
+  const int c0 = 32 * blockIdx.x, i0 = 32 * blockIdx.y;  // latent column, nope row of the tile
+  const int64_t m = blockIdx.z;                          // (layer, head)
+  const uint16_t* src = in + m * nope * r;
+  uint16_t* dst = out + m * r * nope;
+  const int tid = threadIdx.x, row = tid >> 3, col = 4 * (tid & 7);
+  const u2v v = *reinterpret_cast<const u2v*>(src + (int64_t)(i0 + row) * r + c0 + col);
+  tile[row][col] = (uint16_t)(v[0] & 0xFFFFu);
+  tile[row][col + 1] = (uint16_t)(v[0] >> 16);
+  tile[row][col + 2] = (uint16_t)(v[1] & 0xFFFFu);
+  tile[row][col + 3] = (uint16_t)(v[1] >> 16);
+  __syncthreads();
+  u2v w;
+  w[0] = (uint32_t)tile[col][row] | ((uint32_t)tile[col + 1][row] << 16);
+  w[1] = (uint32_t)tile[col + 2][row] | ((uint32_t)tile[col + 3][row] << 16);
+  *reinterpret_cast<u2v*>(dst + (int64_t)(c0 + row) * nope + i0 + col) = w;
+}
+
 }  // namespace
 
 namespace kvk {
@@ -1546,3 +1568,24 @@ kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t 
 }
 
 }  // namespace kvk
+
+// Absorption-ready W_UK (App. C.2): the transpose of every (layer, head) matrix.
+extern "C" kvk_status kvk_mla_arrange_w_uk(const void* w_uk, int32_t n_layers, int32_t n_heads, int32_t nope_dim,
+                                           int32_t latent_dim, void* out, hipStream_t stream) {
+  if (!w_uk || !out) return kvk::fail(KVK_ERR_INVALID, "kvk_mla_arrange_w_uk: NULL buffer");
+  if (n_layers < 1 || n_layers > KVK_MAX_LAYERS || n_heads < 1 || n_heads > 256)
+    return kvk::fail(KVK_ERR_INVALID, "kvk_mla_arrange_w_uk: %d layers x %d heads", n_layers, n_heads);
+  if (nope_dim < 32 || nope_dim % 32 || latent_dim < 32 || latent_dim % 32)
+    return kvk::fail(KVK_ERR_INVALID, "kvk_mla_arrange_w_uk: nope_dim %d and latent_dim %d must be multiples of 32",
+                     nope_dim, latent_dim);
+  if ((reinterpret_cast<uintptr_t>(w_uk) & 15) || (reinterpret_cast<uintptr_t>(out) & 15))
+    return kvk::fail(KVK_ERR_INVALID, "kvk_mla_arrange_w_uk: misaligned buffer (16 bytes required)");
+  if (w_uk == out) return kvk::fail(KVK_ERR_INVALID, "kvk_mla_arrange_w_uk: the output may not alias the input");
+  if (kvk_status st = kvk::check_gpu_buffers({w_uk, out}, "kvk_mla_arrange_w_uk")) return st;
+  const dim3 grid((unsigned)(latent_dim / 32), (unsigned)(nope_dim / 32), (unsigned)(n_layers * n_heads));
+  hipLaunchKernelGGL(mla_arrange_w_uk_kernel, grid, dim3(256), 0, stream, static_cast<const uint16_t*>(w_uk),
+                     static_cast<uint16_t*>(out), nope_dim, latent_dim);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return kvk::fail(KVK_ERR_DEVICE, "W_UK arrange launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}

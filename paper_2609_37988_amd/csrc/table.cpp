@@ -446,6 +446,19 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
   return KVK_OK;
 }
 
+extern "C" kvk_status kvk_set_mla_weights(kvk_table* t, const void* w_uk, const void* w_uv) {
+  if (!t) return fail(KVK_ERR_INVALID, "kvk_set_mla_weights: NULL table");
+  if (t->d.kind != KVK_MLA) return fail(KVK_ERR_INVALID, "kvk_set_mla_weights: an MLA table is required");
+  if (!w_uk != !w_uv) return fail(KVK_ERR_INVALID, "kvk_set_mla_weights: pass both weights or neither");
+  if ((reinterpret_cast<uintptr_t>(w_uk) & 15) || (reinterpret_cast<uintptr_t>(w_uv) & 15))
+    return fail(KVK_ERR_INVALID, "kvk_set_mla_weights: misaligned weights (16 bytes required)");
+  if (w_uk)
+    if (kvk_status st = check_gpu_buffers({w_uk, w_uv}, "kvk_set_mla_weights")) return st;
+  t->mla_w_uk = w_uk;
+  t->mla_w_uv = w_uv;
+  return KVK_OK;
+}
+
 extern "C" double kvk_realized_bits(int32_t qscheme, int32_t bits, int32_t group, int64_t window,
                                     int64_t context) {
   if (!is_bits(bits) || context <= 0 || window < 0 || window > context) return -1.0;

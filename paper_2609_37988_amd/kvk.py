@@ -72,6 +72,8 @@ def load() -> ctypes.CDLL:
             "kvk_table_sequence_query": (I32, [P, I32, P]),
             "kvk_compress_layer": (I32, [P, I32, P, P, I32, I32, P, P, P]),
             "kvk_compress_layer_project": (I32, [P, I32, P, P, I32, P, I32, P, P, P, P]),
+            "kvk_mla_arrange_w_uk": (I32, [P, I32, I32, I32, I32, P, P]),
+            "kvk_set_mla_weights": (I32, [P, P, P]),
             "kvk_append_token": (I32, [P, I32, I32, P, P, I32, I32, P, P]),
             "kvk_snapkv_workspace_bytes": (I32, [P, I32, ctypes.POINTER(ctypes.c_size_t)]),
             "kvk_selector_weight_elems": (I64, [I32, I32, I32]),
@@ -102,7 +104,8 @@ def load() -> ctypes.CDLL:
 def exported_symbols() -> List[str]:
     """Names of the C entry points the binding expects libkvk to export."""
     return ["kvk_layer_table", "kvk_layer_table_batched", "kvk_table_sequence_query", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
-            "kvk_compress_layer", "kvk_compress_layer_project", "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
+            "kvk_compress_layer", "kvk_compress_layer_project", "kvk_mla_arrange_w_uk", "kvk_set_mla_weights",
+            "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
             "kvk_selector_weight_elems", "kvk_selector_workspace_bytes", "kvk_selector_forward",
             "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge", "kvk_decode_attention_noalloc", "kvk_decode_setup",
             "kvk_read_bytes", "kvk_debug_dequantize",
@@ -162,6 +165,7 @@ class Table:
         self._h = handle
         self.dims = dims
         self.plan = list(plan)
+        self.mla_weights = None  # (w_uk, w_uv) attached by set_mla_weights
 
     @property
     def handle(self):
@@ -270,10 +274,32 @@ def _out_width(d: Dims) -> int:
     return d.v_dim if d.kind == MLA else d.head_dim
 
 
-def mla_weights_for_library(w_uk: torch.Tensor) -> torch.Tensor:
+def mla_weights_for_library(w_uk: torch.Tensor, stream=None) -> torch.Tensor:
     """W_UK [layers, Hq, nope, r] in the model's layout -> the latent-major layout the
-    library reads ([layers, Hq, r, nope], contiguous); done once at weight load."""
-    return w_uk.transpose(-1, -2).contiguous()
+    library reads ([layers, Hq, r, nope]), by kvk_mla_arrange_w_uk; done once at
+    weight load."""
+    _need(w_uk.dtype == torch.bfloat16 and w_uk.is_contiguous() and w_uk.dim() == 4,
+          "w_uk must be contiguous bf16 [layers, Hq, nope, r]")
+    L, H, nope, r = w_uk.shape
+    out = torch.empty((L, H, r, nope), dtype=torch.bfloat16, device=w_uk.device)
+    _check(load().kvk_mla_arrange_w_uk(_ptr(w_uk), L, H, nope, r, _ptr(out), _stream(stream)))
+    return out
+
+
+def set_mla_weights(t: Table, w_uk: Optional[torch.Tensor], w_uv: Optional[torch.Tensor]):
+    """Attach all-layer weights to an MLA table (w_uk as mla_weights_for_library
+    returns it, w_uv [layers, Hq, v, r]); None for both detaches.  The table keeps
+    references so the tensors outlive their use."""
+    d = t.dims
+    if w_uk is not None or w_uv is not None:
+        _need(w_uk is not None and w_uv is not None, "pass both weights or neither")
+        _need(w_uk.dtype == torch.bfloat16 and w_uv.dtype == torch.bfloat16 and w_uk.is_contiguous()
+              and w_uv.is_contiguous(), "w_uk / w_uv must be contiguous bf16")
+        _need(w_uk.numel() == d.n_layers * d.n_q_heads * d.latent_dim * d.nope_dim and
+              w_uv.numel() == d.n_layers * d.n_q_heads * d.v_dim * d.latent_dim,
+              "attached weights cover every layer of the table")
+    _check(load().kvk_set_mla_weights(t.handle, _ptr(w_uk), _ptr(w_uv)))
+    t.mla_weights = None if w_uk is None else (w_uk, w_uv)
 
 
 def _check_weights(t: Table, nl: int, w_uk, w_uv):
@@ -281,6 +307,8 @@ def _check_weights(t: Table, nl: int, w_uk, w_uv):
     if d.kind != MLA:
         _need(w_uk is None and w_uv is None, "w_uk / w_uv are for MLA tables only")
         return
+    if w_uk is None and w_uv is None and t.mla_weights is not None:
+        return  # the weights attached to the table
     _need(w_uk is not None and w_uv is not None, "an MLA table needs w_uk and w_uv")
     _need(w_uk.dtype == torch.bfloat16 and w_uv.dtype == torch.bfloat16 and w_uk.is_contiguous()
           and w_uv.is_contiguous(), "w_uk / w_uv must be contiguous bf16")

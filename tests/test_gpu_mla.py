@@ -278,3 +278,45 @@ def test_head_counts_padded_to_chunks(Hq):
     err = rel_err(_np(c.decode(q, wk, wv, n, SCALE)), c.oracle_out(q, wk, wv, n, SCALE))
     say(f"  max|diff| / max|out| = {err:.2e}")
     assert err <= TOL
+
+
+def test_arrange_w_uk_is_the_transpose():
+    """kvk_mla_arrange_w_uk writes every (layer, head) matrix transposed, bit for bit
+    (Qwen2.5-14B's latent shape: 40 heads, nope 128, r 1024)."""
+    say("case mla arrange W_UK")
+    w = synth.weights_random(31, 3, 40, 128, 1024).to(DEV)
+    got = kvk.mla_weights_for_library(w)
+    assert torch.equal(got, w.transpose(-1, -2).contiguous())
+
+
+def test_attached_weights_decode_like_passed_ones():
+    """Weights attached to the table (kvk_set_mla_weights) give the same outputs, bit
+    for bit, as the same weights passed per call: the whole range, a sub-range whose
+    first layer is not 0, and the allocation-free entry; detaching them makes a call
+    without weights fail."""
+    say("case mla attached weights")
+    plan = [(0, 16, 512), (1, 16, 0), (0, 4, 256), (0, 8, 128)]
+    n = 120
+    c = MlaCase(4, 32, 512, 2, 128, plan)
+    for l in (0, 2, 3):
+        c.compress(l, synth.latent_random(900 + l, 2, n, 512), synth.latent_random(910 + l, 2, n, 64), n)
+    q = synth.q_random(920, 4, 2, 32, 192)
+    wk = synth.weights_random(921, 4, 32, 128, 512).to(DEV)
+    wv = synth.weights_random(922, 4, 32, 128, 512).to(DEV)
+    ref = c.decode(q, wk, wv, n, SCALE)
+    ref_sub = c.decode(q[2:4], wk[2:4], wv[2:4], n, SCALE, 2, 4)
+    wk_lib = kvk.mla_weights_for_library(wk)
+    kvk.set_mla_weights(c.table, wk_lib, wv.contiguous())
+    d = c.dims
+    for l0, l1, want in ((0, 4, ref), (2, 4, ref_sub)):
+        out = torch.full((l1 - l0, d.batch, d.n_q_heads, d.v_dim), float("nan"), dtype=torch.float32, device=DEV)
+        ws = torch.full((kvk.workspace_bytes(c.table, l0, l1),), 0xFF, dtype=torch.uint8, device=DEV)
+        kvk.decode_attention(c.table, l0, l1, q[l0:l1].to(DEV).contiguous(), n, SCALE, c.arena, out, ws)
+        assert torch.equal(out, want), (l0, l1)
+    out = torch.full_like(ref, float("nan"))
+    kvk.decode_attention_noalloc(c.table, 0, 4, q.to(DEV).contiguous(), n, SCALE, c.arena, out)
+    assert torch.equal(out, ref)
+    kvk.set_mla_weights(c.table, None, None)
+    ws = torch.empty((kvk.workspace_bytes(c.table, 0, 4),), dtype=torch.uint8, device=DEV)
+    with pytest.raises(ValueError):  # refused by the binding; the library's own refusal is a CPU test
+        kvk.decode_attention(c.table, 0, 4, q.to(DEV).contiguous(), n, SCALE, c.arena, out, ws)

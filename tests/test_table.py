@@ -412,3 +412,25 @@ def test_per_sequence_decode_needs_its_setup():
     _raw(kvk.ERR_BUFFER, "kvk_decode_setup", t.handle, 0, 2, P(1 << 21), 16, None)         # workspace size
     one = kvk.layer_table(d, kvk.make_plan([(0, 16), (1, 16)]))
     _raw(kvk.OK, "kvk_decode_setup", one.handle, 0, 2, P(1 << 21), 16, None)  # one plan: nothing to write
+
+
+def test_mla_weight_entry_points_reject_bad_arguments():
+    """kvk_set_mla_weights and kvk_mla_arrange_w_uk validate before touching memory;
+    an MLA decode that passes no weights needs attached ones."""
+    import ctypes
+    Pv = ctypes.c_void_p
+    f = Pv(256)
+    I = kvk.ERR_INVALID
+    g = kvk.layer_table(kvk.make_dims(kvk.GQA, 2, 8, 2, 128, max_tokens=64), kvk.make_plan([(0, 4), (1, 16)]))
+    _raw(I, "kvk_set_mla_weights", g.handle, f, f)                     # GQA table
+    m = kvk.layer_table(kvk.make_dims(kvk.MLA, 2, 32, 4, 128, 256, 64, 128, 128, batch=1, max_tokens=64),
+                        kvk.make_plan([(0, 8, 128), (1, 16, 0)]))
+    _raw(I, "kvk_set_mla_weights", m.handle, f, None)                  # one of the two
+    _raw(I, "kvk_set_mla_weights", m.handle, Pv(264), f)               # misaligned
+    _raw(kvk.OK, "kvk_set_mla_weights", m.handle, None, None)          # detaching is always allowed
+    need = kvk.workspace_bytes(m, 0, 2)
+    _raw(I, "kvk_decode_attention", m.handle, 0, 2, f, kvk.BF16, 64, 0.1, None, None, f, f, f, need, None)
+    _raw(I, "kvk_mla_arrange_w_uk", None, 2, 32, 128, 256, f, None)     # NULL input
+    _raw(I, "kvk_mla_arrange_w_uk", f, 2, 32, 100, 256, Pv(512), None)  # nope not a multiple of 32
+    _raw(I, "kvk_mla_arrange_w_uk", f, 0, 32, 128, 256, Pv(512), None)  # no layers
+    _raw(I, "kvk_mla_arrange_w_uk", f, 2, 32, 128, 256, f, None)        # output aliases the input
