@@ -51,7 +51,7 @@ def parse():
                     help="quantiser of the quantised layers (group64: GQA workloads only)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--per-sequence", action="store_true",
-                    help="workload 2 with a plan per sequence (each drawn like the shared one)")
+                    help="workloads 2 and 3 with a plan per sequence (each drawn like the shared one)")
     ap.add_argument("--cpu-layers", type=int, default=0, help="layers in the CPU sample (0: auto)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of known size (counter calibration)")
@@ -326,7 +326,13 @@ def run_mla(args):
     dims = kvk.make_dims(kvk.MLA, w.n_layers, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, w.latent_dim,
                          w.rope_dim, w.nope_dim, w.v_dim, qscheme=w.qscheme, batch=w.batch,
                          max_tokens=n_tok, keep_tokens=w.keep_tokens)
-    table = kvk.layer_table(dims, kvk.make_plan(w.plan))
+    plans = None
+    if args.per_sequence:  # each sequence its own kept widths (drawn like the shared plan)
+        plans = synth.mla_plans_per_sequence(w)
+        table = kvk.layer_table_batched(dims, [kvk.make_plan(p) for p in plans])
+        w.name += "-per-sequence"
+    else:
+        table = kvk.layer_table(dims, kvk.make_plan(w.plan))
     info = kvk.table_query(table)
     log(f"workload {w.name}: arena {info.arena_bytes / 1e9:.2f} GB, rho eq.(2) {info.rho:.2f}, "
         f"anchors {info.n_anchors}")
@@ -343,8 +349,13 @@ def run_mla(args):
         e1.record()
         torch.cuda.synchronize()
         w2_ms += e0.elapsed_time(e1)
-        rank = w.plan[l][2]
-        w2_bytes += w.batch * n_tok * (rank + w.rope_dim) * c.element_size() + info.layer_bytes[l]
+        if plans is None:
+            w2_bytes += w.batch * n_tok * (w.plan[l][2] + w.rope_dim) * c.element_size() + info.layer_bytes[l]
+        else:
+            for b, p in enumerate(plans):
+                if not p[l][0]:
+                    w2_bytes += n_tok * (p[l][2] + w.rope_dim) * c.element_size() + \
+                        kvk.table_sequence_query(table, b).layer_bytes[l]
         del c, r
     torch.cuda.empty_cache()
     log(f"prefill write: {w2_ms:.1f} ms over {info.n_anchors} anchors")
@@ -378,27 +389,32 @@ def run_mla(args):
     sp_gbs = alg / (sp_avg * 1e-3) / 1e9
     med12 = median_of_12(torch, lambda i: kvk.decode_attention(table, 0, w.n_layers, qs[i % 2], n_stored, scale,
                                                                arena, out, ws, w_uk=wk, w_uv=wv))
-    wbytes = sum(w.n_q_heads * (w.nope_dim + w.v_dim) * w.plan[info.anchor_of[l]][2] * 2
-                 for l in range(w.n_layers))
+    # the kept width each (sequence, layer) reads: its plan's anchor's
+    seq_plans = plans if plans is not None else [w.plan] * w.batch
+    seq_infos = [kvk.table_sequence_query(table, b) for b in range(w.batch)] if plans is not None else [info] * w.batch
+    kept = [[p[si.anchor_of[l]][2] for l in range(w.n_layers)] for p, si in zip(seq_plans, seq_infos)]
+    # up-projection bytes: once per layer with one plan, once per sequence and layer with one per sequence
+    wbytes = sum(w.n_q_heads * (w.nope_dim + w.v_dim) * d * 2
+                 for kb in (kept if plans is not None else kept[:1]) for d in kb)
     # matrix-core work of D2 per step: scores over the W = d + d_R stored channels and
     # the probability-by-latent product over d, per (token, head), 2 flops per MAC
-    d2_flops = sum(2 * w.batch * n_stored * w.n_q_heads *
-                   (2 * w.plan[info.anchor_of[l]][2] + w.rope_dim) for l in range(w.n_layers))
+    d2_flops = sum(2 * n_stored * w.n_q_heads * (2 * d + w.rope_dim) for kb in kept for d in kb)
     log(f"step {ms_step * 1e3:.1f} us, {gbs:.1f} GB/s ({100 * gbs / HBM_PEAK_GBS:.1f}% of HBM); "
         f"A1+D2 {sp_avg * 1e3:.1f} us ({sp_gbs:.1f} GB/s)")
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and plans is None:
         cpu = cpu_baseline_mla(w, table, n_stored, scale, min(args.cpu_layers or 32, w.n_layers))
         log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
     app = time_append(kvk, torch, table, w.n_layers, arena, n_stored, (w.n_layers, w.batch, w.latent_dim),
                       (w.n_layers, w.batch, w.rope_dim), dev)
     log(f"append: {app}")
-    proj = time_projected_write(kvk, torch, w, table, arena, n_tok, dev)
+    proj = time_projected_write(kvk, torch, w, table, arena, n_tok, dev) if plans is None else None
     log(f"projected write: {proj}")
     ranks = {}
-    for e in w.plan:
-        if not e[0]:
-            ranks[str(e[2])] = ranks.get(str(e[2]), 0) + 1
+    for p in (seq_plans if plans is not None else [w.plan]):
+        for e in p:
+            if not e[0]:
+                ranks[str(e[2])] = ranks.get(str(e[2]), 0) + 1
     line = {
         "metric": METRIC, "value": round(gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "us_per_step": round(ms_step * 1e3, 2),

@@ -246,21 +246,24 @@ kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* plan, kvk_tab
 /* A batch whose sequences carry their own plans (§2.3: the selector maps each
  * input sequence to its own configuration; eq. (4) takes the realized cost per
  * sequence).  plans: host [batch][n_layers] actions, sequence b's plan at
- * plans + b * n_layers, each validated as by kvk_layer_table.  GQA only; batch
- * 1..KVK_MAX_BATCH_PLANS.  Sequence b is stored exactly as a one-sequence table
+ * plans + b * n_layers, each validated as by kvk_layer_table (for MLA the plans
+ * may differ in kept width too, §2.2 eq. (3)); batch 1..KVK_MAX_BATCH_PLANS.  Sequence b is stored exactly as a one-sequence table
  * (dims with batch 1) of plans[b] would store it, at byte base_b of the arena:
  * base_0 = 0, base_{b+1} = base_b + that table's arena_bytes rounded up to 256.
  * Every other entry point accepts the table: kvk_compress_layer, kvk_append_token
  * and kvk_debug_dequantize take the batch's tensors as for one plan and serve each
  * sequence by its own plan (a sequence whose layer inherits writes nothing there);
- * one kvk_decode_attention call decodes the whole batch in one launch, each
+ * GQA: one kvk_decode_attention call decodes the whole batch in one launch, each
  * sequence reading its own anchors once (its work list, one item per sequence and
  * anchor, sits at the head of the workspace, written there once per workspace and
- * layer range by kvk_decode_setup; decode calls then copy nothing); kvk_read_bytes sums the
- * sequences.  kvk_table_query reports the batch (arena_bytes, workspace_bytes,
+ * layer range by kvk_decode_setup; decode calls then copy nothing).  MLA: the call
+ * decodes sequence by sequence (A1 + D2 and C2 of each sequence's own table, its
+ * query and output rows read and written in place), each sequence in its own part
+ * of the workspace; no set-up is needed; kvk_compress_layer_project takes the
+ * table with latent_out NULL.  kvk_read_bytes sums the sequences.  kvk_table_query reports the batch (arena_bytes, workspace_bytes,
  * n_anchors over all sequences, rho of the mean plan); its per-layer fields are
  * empty (anchor_of and layer_offset -1): use kvk_table_sequence_query.
- * Errors: KVK_ERR_INVALID, KVK_ERR_UNSUPPORTED (MLA). */
+ * Errors: KVK_ERR_INVALID, and those of kvk_layer_table for a sequence's plan. */
 kvk_status kvk_layer_table_batched(const kvk_dims* dims, const kvk_action* plans, kvk_table** out);
 
 /* Per-sequence plans: the accounting of sequence b as its one-sequence table
@@ -317,11 +320,12 @@ kvk_status kvk_compress_layer(const kvk_table* table, int32_t layer, const void*
  *   k_rope    : device bf16 [B][n_tokens][64], the positional keys after RoPE.
  *   keep_idx  : as for kvk_compress_layer.
  *   latent_out: NULL, or device bf16 [B][n_stored][d]: the bf16 latent the write
- *               stored (test support).
- * An inheriting layer is a no-op returning KVK_OK.  All buffers 16-byte aligned.
- * Errors: KVK_ERR_INVALID (GQA table, sizes, NULL, misalignment, host memory),
- *         KVK_ERR_UNSUPPORTED (per-sequence tables),
- *         KVK_ERR_DEVICE. */
+ *               stored (test support; NULL for per-sequence tables, whose
+ *               sequences may keep different widths).
+ * An inheriting layer is a no-op returning KVK_OK (per sequence under
+ * per-sequence plans).  All buffers 16-byte aligned.
+ * Errors: KVK_ERR_INVALID (GQA table, sizes, NULL, misalignment, host memory,
+ *         latent_out with per-sequence plans), KVK_ERR_DEVICE. */
 kvk_status kvk_compress_layer_project(const kvk_table* table, int32_t layer, const void* x, const void* w_dkv,
                                       int32_t d_model, const void* k_rope, int32_t n_tokens,
                                       const int32_t* keep_idx, void* arena, void* latent_out, hipStream_t stream);
@@ -464,8 +468,9 @@ kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, int32_t n_act
  * must keep its list (and stay allocated) while it is used for decoding: a set-up
  * of another range on the same workspace replaces the record; a list that does not
  * match the call's (a workspace overwritten since) makes the kernels write NaN
- * outputs and read nothing through it.  One-plan tables: a no-op (their work list
- * travels in the kernel arguments).
+ * outputs and read nothing through it.  One-plan tables and MLA tables: a no-op
+ * (a one-plan work list travels in the kernel arguments; MLA decodes a
+ * per-sequence batch sequence by sequence).
  * Errors: KVK_ERR_INVALID (range, NULL), KVK_ERR_BUFFER (workspace too small),
  *         KVK_ERR_DEVICE (the copy). */
 kvk_status kvk_decode_setup(const kvk_table* table, int32_t layer_begin, int32_t layer_end, void* workspace,
@@ -559,7 +564,9 @@ kvk_status kvk_read_bytes(const kvk_table* table, int32_t layer_begin, int32_t l
 
 /* Test support: dequantise the cache read by `layer` (its anchor's) into fp32,
  * using the rules above bit for bit.  GQA: k_out, v_out [B][Hkv][n_stored][d_h].
- * MLA: k_out = the stored latent [B][n_stored][d], v_out = k^R [B][n_stored][d_R]. */
+ * MLA: k_out = the stored latent [B][n_stored][d], v_out = k^R [B][n_stored][d_R];
+ * under per-sequence plans sequence b's latent starts at b * n_stored * r, in rows of
+ * its own anchor's kept width d_b. */
 kvk_status kvk_debug_dequantize(const kvk_table* table, int32_t layer, int32_t n_stored,
                                 const void* arena, float* k_out, float* v_out, hipStream_t stream);
 

@@ -537,21 +537,24 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
       (reinterpret_cast<uintptr_t>(v) & 15))
     return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
   if (kvk_status st = check_gpu_buffers({k, v, keep_idx, arena}, "kvk_compress_layer")) return st;
-  if (d.kind == KVK_MLA)
-    return mla_compress_layer(t, layer, k, v, in_dtype, n_tokens, keep_idx, arena, stream);
   if (!t->seq.empty()) {  // per-sequence plans: each sequence's own table and arena
     const int64_t elt = in_dtype == KVK_F32 ? 4 : 2;
-    const int64_t in_seq = (int64_t)d.n_kv_heads * n_tokens * d.head_dim * elt;
-    const int64_t keep_seq = (int64_t)d.n_kv_heads * d.keep_tokens;
+    const bool mla = d.kind == KVK_MLA;
+    // GQA: K and V [B][Hkv][n][d_h]; MLA: latent [B][n][r] and positional key [B][n][d_R]
+    const int64_t k_seq = mla ? (int64_t)n_tokens * d.latent_dim * elt : (int64_t)d.n_kv_heads * n_tokens * d.head_dim * elt;
+    const int64_t v_seq = mla ? (int64_t)n_tokens * d.rope_dim * elt : k_seq;
+    const int64_t keep_seq = mla ? (int64_t)d.keep_tokens : (int64_t)d.n_kv_heads * d.keep_tokens;
     for (int b = 0; b < d.batch; ++b) {
       const kvk_status st = kvk_compress_layer(
-          t->seq[b], layer, static_cast<const uint8_t*>(k) + b * in_seq, static_cast<const uint8_t*>(v) + b * in_seq,
+          t->seq[b], layer, static_cast<const uint8_t*>(k) + b * k_seq, static_cast<const uint8_t*>(v) + b * v_seq,
           in_dtype, n_tokens, keep_idx ? keep_idx + b * keep_seq : nullptr,
           static_cast<uint8_t*>(arena) + t->seq_base[b], stream);
       if (st != KVK_OK) return st;
     }
     return KVK_OK;
   }
+  if (d.kind == KVK_MLA)
+    return mla_compress_layer(t, layer, k, v, in_dtype, n_tokens, keep_idx, arena, stream);
 
   CompressArgs a;
   a.k = k;
@@ -601,9 +604,11 @@ extern "C" kvk_status kvk_compress_layer_project(const kvk_table* t, int32_t lay
   if (!t) return fail(KVK_ERR_INVALID, "kvk_compress_layer_project: NULL table");
   const kvk_dims& d = t->d;
   if (d.kind != KVK_MLA) return fail(KVK_ERR_INVALID, "kvk_compress_layer_project: an MLA table is required");
-  if (!t->seq.empty()) return fail(KVK_ERR_UNSUPPORTED, "kvk_compress_layer_project: per-sequence tables");
   if (layer < 0 || layer >= d.n_layers) return fail(KVK_ERR_INVALID, "layer %d out of range", layer);
-  if (t->plan[layer].inherit) return KVK_OK;  // an inheriting layer writes nothing (§2.1)
+  const bool per_seq = !t->seq.empty();
+  if (per_seq && latent_out)
+    return fail(KVK_ERR_INVALID, "kvk_compress_layer_project: latent_out must be NULL for per-sequence tables");
+  if (!per_seq && t->plan[layer].inherit) return KVK_OK;  // an inheriting layer writes nothing (§2.1)
   if (!x || !w_dkv || !k_rope || !arena) return fail(KVK_ERR_INVALID, "kvk_compress_layer_project: NULL buffer");
   if (d_model < 32 || d_model % 32)
     return fail(KVK_ERR_INVALID, "d_model %d: a positive multiple of 32", d_model);
@@ -620,6 +625,19 @@ extern "C" kvk_status kvk_compress_layer_project(const kvk_table* t, int32_t lay
     return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
   if (kvk_status st = check_gpu_buffers({x, w_dkv, k_rope, keep_idx, arena, latent_out}, "kvk_compress_layer_project"))
     return st;
+  if (per_seq) {  // each sequence's own table and arena
+    for (int b = 0; b < d.batch; ++b) {
+      const kvk_table* s = t->seq[b];
+      if (s->plan[layer].inherit) continue;
+      const kvk_status st = mla_compress_layer_project(
+          s, layer, static_cast<const uint16_t*>(x) + (int64_t)b * n_tokens * d_model, w_dkv, d_model,
+          static_cast<const uint16_t*>(k_rope) + (int64_t)b * n_tokens * d.rope_dim, n_tokens,
+          keep_idx ? keep_idx + (int64_t)b * d.keep_tokens : nullptr, static_cast<uint8_t*>(arena) + t->seq_base[b],
+          nullptr, stream);
+      if (st != KVK_OK) return st;
+    }
+    return KVK_OK;
+  }
   return mla_compress_layer_project(t, layer, x, w_dkv, d_model, k_rope, n_tokens, keep_idx, arena, latent_out,
                                     stream);
 }
@@ -717,6 +735,18 @@ extern "C" kvk_status kvk_debug_dequantize(const kvk_table* t, int32_t layer, in
     return fail(KVK_ERR_INVALID, "n_stored %d outside 0..%d", n_stored, t->cap);
   if (n_stored == 0) return KVK_OK;
   if (kvk_status st = check_gpu_buffers({arena, k_out, v_out}, "kvk_debug_dequantize")) return st;
+  if (d.kind == KVK_MLA && !t->seq.empty()) {
+    // sequence b's values at b n_stored r (latent, rows of its own kept width) and
+    // b n_stored d_R (positional key)
+    for (int b = 0; b < d.batch; ++b) {
+      const kvk_status st = mla_debug_dequantize(t->seq[b], layer, n_stored,
+                                                 static_cast<const uint8_t*>(arena) + t->seq_base[b],
+                                                 k_out + (int64_t)b * n_stored * d.latent_dim,
+                                                 v_out + (int64_t)b * n_stored * d.rope_dim, stream);
+      if (st != KVK_OK) return st;
+    }
+    return KVK_OK;
+  }
   if (d.kind == KVK_MLA) return mla_debug_dequantize(t, layer, n_stored, arena, k_out, v_out, stream);
   if (!t->seq.empty()) {
     const int64_t per = (int64_t)d.n_kv_heads * n_stored * d.head_dim;

@@ -1211,11 +1211,42 @@ kvk_status mla_check(const kvk_table* t, int32_t l0, int32_t l1, const void* q, 
       (reinterpret_cast<uintptr_t>(out) & 15) || (reinterpret_cast<uintptr_t>(w_uk) & 15) ||
       (reinterpret_cast<uintptr_t>(w_uv) & 15) || (reinterpret_cast<uintptr_t>(workspace) & 255))
     return fail(KVK_ERR_INVALID, "misaligned buffer (q/w_uk/w_uv/arena/out 16 B, workspace 256 B)");
-  MlaWorkspace ws;
-  mla_workspace(t, l0, l1, &ws);
-  if ((size_t)ws.total > ws_bytes)
-    return fail(KVK_ERR_BUFFER, "workspace %zu bytes < %lld needed", ws_bytes, (long long)ws.total);
+  size_t need = 0;
+  if (kvk_status st = kvk_workspace_bytes(t, l0, l1, &need)) return st;
+  if (need > ws_bytes) return fail(KVK_ERR_BUFFER, "workspace %zu bytes < %zu needed", ws_bytes, need);
   return check_gpu_buffers({q, w_uk, w_uv, arena, out, workspace}, "decode");
+}
+
+// MLA under per-sequence plans: each sequence decodes with its own one-sequence table
+// (A1 + D2 and / or C2), its query and output rows read and written in place with
+// the batch's layer strides, in its own part of the workspace (the parts in
+// sequence order, as kvk_workspace_bytes sizes them).
+kvk_status mla_decode_per_sequence(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
+                                   int32_t n_stored, float scale, const void* w_uk, const void* w_uv,
+                                   const void* arena, float* out, const void* workspace, hipStream_t stream,
+                                   bool splits, bool merge) {
+  const kvk_dims& d = t->d;
+  const int64_t qw = d.nope_dim + d.rope_dim, elt = q_dtype == KVK_F32 ? 4 : 2;
+  const int64_t q_ls = (int64_t)d.batch * d.n_q_heads * qw, o_ls = (int64_t)d.batch * d.n_q_heads * d.v_dim;
+  uint8_t* ws = static_cast<uint8_t*>(const_cast<void*>(workspace));
+  for (int b = 0; b < d.batch; ++b) {
+    const kvk_table* s = t->seq[b];
+    const void* ab = static_cast<const uint8_t*>(arena) + t->seq_base[b];
+    if (splits) {
+      const void* qb = static_cast<const uint8_t*>(q) + (int64_t)b * d.n_q_heads * qw * elt;
+      if (kvk_status st = mla_decode_splits(s, l0, l1, qb, q_dtype, n_stored, scale, w_uk, ab, ws, stream, q_ls))
+        return st;
+    }
+    if (merge) {
+      if (kvk_status st = mla_decode_merge(s, l0, l1, n_stored, w_uv, ws, out + (int64_t)b * d.n_q_heads * d.v_dim,
+                                           stream, o_ls))
+        return st;
+    }
+    MlaWorkspace w;
+    mla_workspace(s, l0, l1, &w);
+    ws += w.total;
+  }
+  return KVK_OK;
 }
 
 }  // namespace
@@ -1236,6 +1267,9 @@ extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32
     kvk_status st = mla_check(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
                               ws_bytes);
     if (st != KVK_OK) return st;
+    if (!t->seq.empty())
+      return mla_decode_per_sequence(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
+                                     stream, true, true);
     st = mla_decode_splits(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, arena, workspace, stream);
     if (st != KVK_OK) return st;
     return mla_decode_merge(t, l0, l1, n_stored, w_uv, workspace, out, stream);
@@ -1258,6 +1292,9 @@ extern "C" kvk_status kvk_decode_splits(const kvk_table* t, int32_t l0, int32_t 
     const kvk_status st = mla_check(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, workspace,
                                     workspace, ws_bytes);
     if (st != KVK_OK) return st;
+    if (!t->seq.empty())
+      return mla_decode_per_sequence(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, nullptr,
+                                     workspace, stream, true, false);
     return mla_decode_splits(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, arena, workspace, stream);
   }
   DecodePlan P;
@@ -1278,6 +1315,9 @@ extern "C" kvk_status kvk_decode_merge(const kvk_table* t, int32_t l0, int32_t l
     const kvk_status st = mla_check(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out,
                                     workspace, ws_bytes);
     if (st != KVK_OK) return st;
+    if (!t->seq.empty())
+      return mla_decode_per_sequence(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
+                                     stream, false, true);
     return mla_decode_merge(t, l0, l1, n_stored, w_uv, workspace, out, stream);
   }
   DecodePlan P;
@@ -1293,7 +1333,9 @@ extern "C" kvk_status kvk_decode_setup(const kvk_table* t, int32_t l0, int32_t l
   if (l0 < 0 || l1 > t->d.n_layers || l0 >= l1)
     return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, t->d.n_layers);
   if (!workspace) return fail(KVK_ERR_INVALID, "kvk_decode_setup: NULL workspace");
-  if (t->seq.empty()) return KVK_OK;  // one plan: the work list travels in the kernel arguments
+  // one plan: the work list travels in the kernel arguments; MLA decodes a
+  // per-sequence batch sequence by sequence, with no work list
+  if (t->seq.empty() || t->d.kind == KVK_MLA) return KVK_OK;
   DecodePlan P;
   kvk_status st = prepare(t, l0, l1, nullptr, KVK_BF16, 0, 1.0f, nullptr, nullptr, nullptr, nullptr, workspace,
                           ws_bytes, P, kForSetup);

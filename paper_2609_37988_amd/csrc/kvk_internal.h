@@ -194,12 +194,15 @@ kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* lat
 kvk_status mla_append_token(const kvk_table* t, int32_t l0, int32_t l1, const void* latent,
                             const void* rope, int32_t in_dtype, int32_t n_stored, void* arena,
                             hipStream_t stream);
+// q_lstride / out_lstride: elements between consecutive layers of q / out (0: the
+// table's own [B][Hq][...] per layer; a sequence of a per-sequence batch passes the
+// batch's, with q and out at its first row).
 kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const void* q,
                              int32_t q_dtype, int32_t n_stored, float scale, const void* w_uk,
-                             const void* arena, void* workspace, hipStream_t stream);
+                             const void* arena, void* workspace, hipStream_t stream, int64_t q_lstride = 0);
 kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored,
                             const void* w_uv, const void* workspace, float* out,
-                            hipStream_t stream);
+                            hipStream_t stream, int64_t out_lstride = 0);
 kvk_status mla_debug_dequantize(const kvk_table* t, int32_t layer, int32_t n_stored,
                                 const void* arena, float* c_out, float* r_out, hipStream_t stream);
 

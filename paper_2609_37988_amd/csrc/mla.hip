@@ -29,7 +29,9 @@
 // writer that takes its rows from the input or from the stream's bf16 tail.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <type_traits>
+#include <vector>
 
 #include "kvk_device.h"
 #include "kvk_internal.h"
@@ -469,6 +471,7 @@ struct MlaAppendItem {
   int32_t bits;
   int32_t row;  // the anchor's row in the new-token input (layer - layer_begin)
   int32_t d;    // kept latent width
+  int32_t seq;  // per-sequence plans: the one sequence (stream 0 of its region); -1: all
 };
 
 struct MlaAppendArgs {
@@ -527,10 +530,10 @@ struct TailRows {
 template <bool KIVI>
 __global__ __launch_bounds__(256) void mla_append_kernel(MlaAppendArgs a) {
   __shared__ uint32_t amax[2][32];
-  const int b = blockIdx.x;
   const MlaAppendItem& it = a.items[blockIdx.y];
+  const int b = it.seq >= 0 ? it.seq : blockIdx.x;  // the input row's sequence
   const int W = it.d + kRope, NK = W / 32, t = a.pos & 31;
-  uint8_t* base = a.arena + it.region + (int64_t)b * it.stream_bytes;
+  uint8_t* base = a.arena + it.region + (it.seq >= 0 ? 0 : (int64_t)b * it.stream_bytes);
   uint8_t* tail = base + (int64_t)a.nb_cap * it.block_bytes;
   if (t != 31) {
     for (int ch = threadIdx.x; ch < W / 8; ch += 256) {
@@ -610,6 +613,7 @@ struct MlaAbsorbArgs {
   int32_t d_of[KVK_MAX_LAYERS];
   int32_t q_f32;
   int32_t B, Hq, Hp, nope, r;  // Hp: Hq rounded up to whole 32-head chunks
+  int64_t q_lstride;           // elements between consecutive layers' queries
   float scale_log2;
 };
 
@@ -635,7 +639,7 @@ __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
   }
   for (int e = tid; e < a.B * kRope; e += 256) {
     const int b = e / kRope, j = e - b * kRope;
-    const float x = load_in(a.q, a.q_f32, (((int64_t)li * a.B + b) * a.Hq + h) * qw + a.nope + j);
+    const float x = load_in(a.q, a.q_f32, li * a.q_lstride + ((int64_t)b * a.Hq + h) * qw + a.nope + j);
     qa[((int64_t)b * a.Hp + h) * W + d + j] = (_Float16)(x * a.scale_log2);
   }
   const uint16_t* wt = a.w_ukt + ((int64_t)li * a.Hq + h) * a.r * a.nope;
@@ -643,7 +647,7 @@ __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
     __syncthreads();
     for (int e = tid; e < 16 * a.nope; e += 256) {
       const int bi = e / a.nope, i = e - bi * a.nope;
-      qs[bi * PQ + i] = b0 + bi < a.B ? load_in(a.q, a.q_f32, (((int64_t)li * a.B + b0 + bi) * a.Hq + h) * qw + i) : 0.0f;
+      qs[bi * PQ + i] = b0 + bi < a.B ? load_in(a.q, a.q_f32, li * a.q_lstride + ((int64_t)(b0 + bi) * a.Hq + h) * qw + i) : 0.0f;
     }
     __syncthreads();
     bf16x8 bh[8], bl[8];  // nope <= 256
@@ -1193,6 +1197,7 @@ struct MlaCombineArgs {
   int32_t units[KVK_MAX_LAYERS];
   int32_t units_cap[KVK_MAX_LAYERS];
   int32_t B, Hq, Hp, v, r;  // Hp: heads per split partial record (padded)
+  int64_t out_lstride;       // elements between consecutive layers' outputs
 };
 
 // One workgroup per (layer, head): for 16 sequences at a time, merge the split
@@ -1268,7 +1273,7 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
         }
       }
       if (i16 < nb)  // D[value channel 16 jt + 4g + e][sequence b0 + i16]
-        *reinterpret_cast<f4*>(a.out + (((int64_t)li * a.B + b0 + i16) * a.Hq + h) * a.v + 16 * jt + 4 * g) = acc;
+        *reinterpret_cast<f4*>(a.out + li * a.out_lstride + ((int64_t)(b0 + i16) * a.Hq + h) * a.v + 16 * jt + 4 * g) = acc;
     }
   }
 }
@@ -1344,23 +1349,34 @@ kvk_status mla_append_token(const kvk_table* t, int32_t l0, int32_t l1, const vo
   a.nb_cap = t->nb_cap;
   a.B = d.batch;
   a.r = d.latent_dim;
-  int n = 0;
-  for (int l = l0; l < l1; ++l) {
-    if (t->plan[l].inherit) continue;
-    MlaAppendItem& it = a.items[n++];
-    it.region = t->info.layer_offset[l];
-    it.stream_bytes = (int32_t)t->info.stream_bytes[l];
-    it.block_bytes = (int32_t)t->block_bytes[l];
-    it.bits = t->bits[l];
-    it.row = l - l0;
-    it.d = t->rank[l];
+  // one item per anchor (over all sequences), or per (sequence, anchor of its plan)
+  const bool per_seq = !t->seq.empty();
+  std::vector<MlaAppendItem> items;
+  for (int b = 0; b < (per_seq ? d.batch : 1); ++b) {
+    const kvk_table* st = per_seq ? t->seq[b] : t;
+    for (int l = l0; l < l1; ++l) {
+      if (st->plan[l].inherit) continue;  // an inheriting layer stores nothing (§2.1)
+      MlaAppendItem it;
+      it.region = (per_seq ? t->seq_base[b] : 0) + st->info.layer_offset[l];
+      it.stream_bytes = (int32_t)st->info.stream_bytes[l];
+      it.block_bytes = (int32_t)st->block_bytes[l];
+      it.bits = st->bits[l];
+      it.row = l - l0;
+      it.d = st->rank[l];
+      it.seq = per_seq ? b : -1;
+      items.push_back(it);
+    }
   }
-  if (n == 0) return KVK_OK;
-  const dim3 g3((unsigned)d.batch, (unsigned)n), b3(256);
-  if (d.qscheme == KVK_Q_KIVI32) hipLaunchKernelGGL(mla_append_kernel<true>, g3, b3, 0, stream, a);
-  else hipLaunchKernelGGL(mla_append_kernel<false>, g3, b3, 0, stream, a);
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA append launch: %s", hipGetErrorString(e));
+  const dim3 b3(256);
+  for (size_t i0 = 0; i0 < items.size(); i0 += KVK_MAX_LAYERS) {
+    const int n = (int)std::min<size_t>(KVK_MAX_LAYERS, items.size() - i0);
+    std::copy(items.begin() + i0, items.begin() + i0 + n, a.items);
+    const dim3 g3(per_seq ? 1u : (unsigned)d.batch, (unsigned)n);
+    if (d.qscheme == KVK_Q_KIVI32) hipLaunchKernelGGL(mla_append_kernel<true>, g3, b3, 0, stream, a);
+    else hipLaunchKernelGGL(mla_append_kernel<false>, g3, b3, 0, stream, a);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA append launch: %s", hipGetErrorString(e));
+  }
   return KVK_OK;
 }
 
@@ -1424,7 +1440,7 @@ kvk_status mla_debug_dequantize(const kvk_table* t, int32_t layer, int32_t n_sto
 
 kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
                              int32_t n_stored, float scale, const void* w_uk, const void* arena,
-                             void* workspace, hipStream_t stream) {
+                             void* workspace, hipStream_t stream, int64_t q_lstride) {
   const kvk_dims& d = t->d;
   MlaWorkspace ws;
   mla_workspace(t, l0, l1, &ws);
@@ -1439,6 +1455,7 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
   aa.B = d.batch;
   aa.Hq = d.n_q_heads;
   aa.Hp = mla_heads_padded(d.n_q_heads);
+  aa.q_lstride = q_lstride > 0 ? q_lstride : (int64_t)d.batch * d.n_q_heads * (d.nope_dim + d.rope_dim);
   aa.nope = d.nope_dim;
   aa.r = d.latent_dim;
   aa.scale_log2 = scale * kLog2e;
@@ -1537,7 +1554,7 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
 }
 
 kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored, const void* w_uv,
-                            const void* workspace, float* out, hipStream_t stream) {
+                            const void* workspace, float* out, hipStream_t stream, int64_t out_lstride) {
   const kvk_dims& d = t->d;
   MlaWorkspace ws;
   mla_workspace(t, l0, l1, &ws);
@@ -1548,6 +1565,7 @@ kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t 
   c.B = d.batch;
   c.Hq = d.n_q_heads;
   c.Hp = mla_heads_padded(d.n_q_heads);
+  c.out_lstride = out_lstride > 0 ? out_lstride : (int64_t)d.batch * d.n_q_heads * d.v_dim;
   c.v = d.v_dim;
   c.r = d.latent_dim;
   int dmax = 0;

@@ -344,7 +344,6 @@ extern "C" kvk_status kvk_layer_table_batched(const kvk_dims* dims, const kvk_ac
   if (!dims || !plans || !out) return fail(KVK_ERR_INVALID, "kvk_layer_table_batched: NULL argument");
   *out = nullptr;
   const kvk_dims& d = *dims;
-  if (d.kind != KVK_GQA) return fail(KVK_ERR_UNSUPPORTED, "per-sequence plans: GQA tables only");
   if (d.batch < 1 || d.batch > KVK_MAX_BATCH_PLANS)
     return fail(KVK_ERR_INVALID, "batch %d outside 1..%d for per-sequence plans", d.batch, KVK_MAX_BATCH_PLANS);
   if (d.n_layers < 1 || d.n_layers > KVK_MAX_LAYERS)
@@ -413,16 +412,17 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
   if (l0 < 0 || l1 > t->d.n_layers || l0 >= l1)
     return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, t->d.n_layers);
   const kvk_dims& d = t->d;
-  if (d.kind == KVK_MLA) {
+  if (d.kind == KVK_MLA && t->seq.empty()) {
     MlaWorkspace ws;
     mla_workspace(t, l0, l1, &ws);
     *out = (size_t)ws.total;
     return KVK_OK;
   }
   if (!t->seq.empty()) {
-    // the device-side work list, then every sequence's split partials (each sized
-    // with its own, smaller, split target: the batch's longer splits need no more)
-    size_t total = (size_t)gqa_batched_list_bytes(t, l0, l1);
+    // GQA: the device-side work list, then every sequence's split partials (each
+    // sized with its own, smaller, split target: the batch's longer splits need no
+    // more).  MLA: every sequence's own workspace, one after the other.
+    size_t total = d.kind == KVK_MLA ? 0 : (size_t)gqa_batched_list_bytes(t, l0, l1);
     for (const kvk_table* s : t->seq) {
       size_t one = 0;
       const kvk_status st = kvk_workspace_bytes(s, l0, l1, &one);

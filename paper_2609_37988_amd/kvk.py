@@ -166,6 +166,7 @@ class Table:
         self.dims = dims
         self.plan = list(plan)
         self.mla_weights = None  # (w_uk, w_uv) attached by set_mla_weights
+        self.plans = None        # per-sequence plans (layer_table_batched)
 
     @property
     def handle(self):
@@ -553,10 +554,14 @@ def read_bytes(t: Table, layer_begin: int, layer_end: int, n_stored: int) -> int
 def debug_dequantize(t: Table, layer: int, n_stored: int, arena: torch.Tensor, k_out: torch.Tensor,
                      v_out: torch.Tensor, stream=None):
     """GQA: k_out, v_out fp32 [B, Hkv, n_stored, d_h].  MLA: k_out = latent fp32
-    [B, n_stored, d] (the anchor's kept width), v_out = k^R fp32 [B, n_stored, d_R]."""
+    [B, n_stored, d] (the anchor's kept width), v_out = k^R fp32 [B, n_stored, d_R];
+    under per-sequence plans sequence b's latent starts at b * n_stored * r, in rows
+    of its own anchor's kept width."""
     d = t.dims
     n = max(n_stored, 0)
-    if d.kind == MLA:
+    if d.kind == MLA and getattr(t, "plans", None) is not None:
+        nk, nv = d.batch * n * d.latent_dim, d.batch * n * d.rope_dim
+    elif d.kind == MLA:
         a = table_query(t).anchor_of[layer]
         nk, nv = d.batch * n * t.plan[a].rank, d.batch * n * d.rope_dim
     else:

@@ -110,6 +110,14 @@ def plans_per_sequence(w: Workload, n_inherit: int = 16):
     return [plan_mixed(w.seed * 1000 + b, w.n_layers, n_inherit) for b in range(w.batch)]
 
 
+def mla_plans_per_sequence(w: "MlaWorkload"):
+    """One plan per sequence of an MLA workload, each drawn like the shared plan
+    (its own seed): every anchor's kept width from {r, r/2, r/4, r/8}, the shared
+    plan's bit-width."""
+    bits = w.plan[0][1]
+    return [plan_ranks(w.seed * 1000 + b, w.n_layers, w.latent_dim, bits) for b in range(w.batch)]
+
+
 @dataclass
 class MlaWorkload:
     """An MLA-style stack (§2.1 rank axis): one latent of width r per token shared by

@@ -362,8 +362,9 @@ def test_batched_table_rejects_bad_input():
     with pytest.raises(kvk.KvkError):
         kvk.layer_table_batched(d, [kvk.make_plan([(0, 4), (1, 16)]), kvk.make_plan([(0, 3), (1, 16)])])
     m = kvk.make_dims(kvk.MLA, 2, 32, 4, 128, 256, 64, 128, 128, batch=2, max_tokens=64)
-    with pytest.raises(kvk.KvkError):
-        kvk.layer_table_batched(m, [kvk.make_plan([(0, 8, 128), (1, 16, 0)])] * 2)
+    with pytest.raises(kvk.KvkError):  # a kept width outside {r/8 .. r} in one sequence's plan
+        kvk.layer_table_batched(m, [kvk.make_plan([(0, 8, 128), (1, 16, 0)]), kvk.make_plan([(0, 8, 100), (1, 16, 0)])])
+    kvk.layer_table_batched(m, [kvk.make_plan([(0, 8, 128), (1, 16, 0)]), kvk.make_plan([(0, 2, 32), (0, 16, 256)])])
     t = kvk.layer_table_batched(d, [kvk.make_plan([(0, 4), (1, 16)]), kvk.make_plan([(0, 8), (0, 2)])])
     with pytest.raises(kvk.KvkError):
         kvk.table_sequence_query(t, 2)
@@ -434,3 +435,31 @@ def test_mla_weight_entry_points_reject_bad_arguments():
     _raw(I, "kvk_mla_arrange_w_uk", f, 2, 32, 100, 256, Pv(512), None)  # nope not a multiple of 32
     _raw(I, "kvk_mla_arrange_w_uk", f, 0, 32, 128, 256, Pv(512), None)  # no layers
     _raw(I, "kvk_mla_arrange_w_uk", f, 2, 32, 128, 256, f, None)        # output aliases the input
+
+
+def test_batched_mla_table_accounting_matches_oracle():
+    """Per-sequence MLA plans (kept widths, bit-widths and depth differing per
+    sequence): bases, per-layer offsets and read bytes as the oracle's one-sequence
+    tables give them; the workspace holds every sequence's own MLA workspace."""
+    from oracle import plan as OP
+    plans = [[(0, 4, 512), (1, 16, 0), (0, 8, 128)], [(0, 16, 64), (0, 2, 256), (1, 16, 0)],
+             [(0, 8, 256), (0, 8, 256), (0, 4, 512)]]
+    d = kvk.make_dims(kvk.MLA, 3, 32, 4, 128, 512, 64, 128, 128, batch=3, max_tokens=300)
+    t = kvk.layer_table_batched(d, [kvk.make_plan(p) for p in plans])
+    od = OP.Dims(OP.MLA, 3, 32, 4, 128, latent_dim=512, rope_dim=64, nope_dim=128, v_dim=128, batch=3,
+                 max_tokens=300)
+    oplans = [[OP.Action(bool(a), b, r) for a, b, r in p] for p in plans]
+    bases, total = OP.batched_arena_bases(od, oplans)
+    info = kvk.table_query(t)
+    assert info.arena_bytes == total and info.n_anchors == 7
+    sd = OP.sequence_dims(od)
+    one_ws = 0
+    for b in range(3):
+        si = kvk.table_sequence_query(t, b)
+        offs, _ = OP.arena_offsets(sd, oplans[b])
+        assert si.layer_offset == [o + bases[b] if o >= 0 else -1 for o in offs]
+        one = kvk.layer_table(kvk.make_dims(kvk.MLA, 3, 32, 4, 128, 512, 64, 128, 128, batch=1, max_tokens=300),
+                              kvk.make_plan(plans[b]))
+        one_ws += kvk.workspace_bytes(one, 0, 3)
+    assert kvk.workspace_bytes(t, 0, 3) == one_ws
+    assert kvk.read_bytes(t, 0, 3, 250) == OP.read_bytes_batched(od, oplans, 0, 3, 250)
