@@ -72,3 +72,44 @@ def keep_list(q_obs: np.ndarray, K: np.ndarray, scale: float, keep: int, window:
     """[Hkv, keep] kept positions of one sequence."""
     imp = importance(q_obs, K, scale, window)
     return np.stack([select(imp[h], keep, window) for h in range(imp.shape[0])])
+
+
+# ---------------------------------------------------------------------------
+# MLA layers (§2.1 "Rank", App. C.2): the latent is shared by every head, so a
+# sequence keeps one list of positions for all heads.  Head h's key at position t is
+# [W_UK[h] c_t ; k^R_t] (the latent at its full width r, before the layer keeps
+# its first d coordinates); its window queries are [q_nope ; q_rope].  The
+# importance of a position sums the causal softmax probabilities over the 32
+# window queries of every query head; the selection rule is the one above.
+# ---------------------------------------------------------------------------
+
+def importance_mla(q_obs: np.ndarray, C: np.ndarray, R: np.ndarray, W_UK: np.ndarray, scale: float,
+                   window: int = WINDOW) -> np.ndarray:
+    """q_obs [Hq, W, nope + d_R] (each head's window queries: no-RoPE part, then the
+    RoPE part), C [n, r] latent, R [n, d_R] positional keys, W_UK [Hq, nope, r] ->
+    importance [n] (fp64), the keys reconstructed per head."""
+    q = np.asarray(q_obs, dtype=np.float64)
+    C = np.asarray(C, dtype=np.float64)
+    R = np.asarray(R, dtype=np.float64)
+    Wk = np.asarray(W_UK, dtype=np.float64)
+    Hq, W, qw = q.shape
+    n, dR = R.shape
+    nope = qw - dR
+    assert W == window and n >= W and Wk.shape[:2] == (Hq, nope)
+    pos = n - W + np.arange(W)
+    visible = np.arange(n)[None, :] <= pos[:, None]
+    imp = np.zeros(n)
+    for h in range(Hq):
+        K = np.concatenate([C @ Wk[h].T, R], axis=1)  # [n, nope + d_R]: head h's keys
+        s = scale * (q[h] @ K.T)                      # [W, n]
+        s = np.where(visible, s, -np.inf)
+        s = s - s.max(axis=1, keepdims=True)
+        p = np.exp(s)
+        p /= p.sum(axis=1, keepdims=True)
+        imp += p.sum(axis=0)
+    return imp
+
+
+def keep_list_mla(q_obs, C, R, W_UK, scale: float, keep: int, window: int = WINDOW) -> np.ndarray:
+    """[keep] kept positions of one sequence of an MLA layer."""
+    return select(importance_mla(q_obs, C, R, W_UK, scale, window), keep, window)

@@ -102,3 +102,67 @@ def test_keep_list_is_sorted_unique_and_holds_window():
     for h in range(2):
         assert np.all(np.diff(kl[h]) > 0)
         assert set(range(200 - W, 200)) <= set(kl[h].tolist())
+
+
+# --- MLA layers: one keep list per sequence, the heads sharing the latent ---------
+
+def _mla_inputs(seed, Hq=3, n=60, r=12, nope=4, dR=2):
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal((Hq, W, nope + dR)), rng.standard_normal((n, r)), rng.standard_normal((n, dR)),
+            rng.standard_normal((Hq, nope, r)) / np.sqrt(r))
+
+
+def test_mla_importance_matches_explicit_loops():
+    q, C, R, Wk = _mla_inputs(11, Hq=2, n=36, r=6, nope=3, dR=2)
+    scale, n = 0.6, C.shape[0]
+    want = np.zeros(n)
+    for h in range(2):
+        for w in range(W):
+            last = n - W + w
+            sc = []
+            for t in range(last + 1):
+                key = [sum(Wk[h, i, c] * C[t, c] for c in range(6)) for i in range(3)] + [R[t, 0], R[t, 1]]
+                sc.append(scale * sum(q[h, w, j] * key[j] for j in range(5)))
+            m = max(sc)
+            e = [np.exp(x - m) for x in sc]
+            z = sum(e)
+            for t in range(last + 1):
+                want[t] += e[t] / z
+    assert np.allclose(S.importance_mla(q, C, R, Wk, scale), want, rtol=1e-12, atol=1e-14)
+
+
+def test_mla_importance_reduces_to_multi_head_attention():
+    """W_UK[h] reading a slice of the latent of its own: head h's keys are that slice
+    and the positional keys, so the MLA importance is the sum over heads of the
+    (pinned) per-KV-head importance with one query head per KV head."""
+    Hq, n, nope, dR = 3, 50, 4, 2
+    rng = np.random.default_rng(12)
+    q = rng.standard_normal((Hq, W, nope + dR))
+    C = rng.standard_normal((n, Hq * nope))
+    R = rng.standard_normal((n, dR))
+    Wk = np.zeros((Hq, nope, Hq * nope))
+    for h in range(Hq):
+        Wk[h, :, h * nope:(h + 1) * nope] = np.eye(nope)
+    K = np.stack([np.concatenate([C[:, h * nope:(h + 1) * nope], R], axis=1) for h in range(Hq)])
+    want = S.importance(q, K, 0.45).sum(axis=0)
+    assert np.allclose(S.importance_mla(q, C, R, Wk, 0.45), want, rtol=1e-12)
+
+
+def test_mla_importance_positional_part_alone():
+    """No-RoPE queries of zero: only the shared positional keys score, as one KV head
+    read by all query heads."""
+    q, C, R, Wk = _mla_inputs(13)
+    q[:, :, :4] = 0.0
+    want = S.importance(q[:, :, 4:], R[None], 0.8)[0]
+    assert np.allclose(S.importance_mla(q, C, R, Wk, 0.8), want, rtol=1e-12)
+
+
+def test_mla_importance_mass_and_scale_zero():
+    q, C, R, Wk = _mla_inputs(14, Hq=4, n=70)
+    assert np.isclose(S.importance_mla(q, C, R, Wk, 0.3).sum(), 4 * W, rtol=1e-12)
+    imp0 = S.importance_mla(q, C, R, Wk, 0.0)
+    n = 70
+    closed = 4 * sum(1.0 / (n - W + w + 1) for w in range(W))
+    assert np.allclose(imp0[:n - W], closed, rtol=1e-12)
+    kl = S.keep_list_mla(q, C, R, Wk, 0.3, 40)
+    assert kl.shape == (40,) and np.all(np.diff(kl) > 0) and np.array_equal(kl[-W:], np.arange(n - W, n))
