@@ -410,6 +410,8 @@ def run_mla(args):
     log(f"append: {app}")
     proj = time_projected_write(kvk, torch, w, table, arena, n_tok, dev) if plans is None else None
     log(f"projected write: {proj}")
+    snap = time_snapkv_mla(kvk, torch, w, dev) if plans is None else None
+    log(f"snapkv (MLA): {snap}")
     ranks = {}
     for p in (seq_plans if plans is not None else [w.plan]):
         for e in p:
@@ -445,6 +447,7 @@ def run_mla(args):
         "median_of_12_us_per_step": med12,
         "append": app,
         "prefill_write_projected": proj,
+        "snapkv_select_mla": snap,
     }
     print(json.dumps(line), flush=True)
 
@@ -479,6 +482,46 @@ def time_projected_write(kvk, torch, w, table, arena, n_tok, dev):
             "us": round(ms * 1e3, 1), "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1),
             "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
             "x_read_GB_per_s": round(w.batch * n_tok * w.d_model * 2 / (ms * 1e-3) / 1e9, 1)}
+
+
+def time_snapkv_mla(kvk, torch, w, dev):
+    """The query-aware keep list of one MLA anchor (kvk_snapkv_select_mla) at the
+    stack's shape, keeping half of the positions: median of 5 after 2 warmups.  Bytes:
+    the latent and positional keys read by both score passes; matrix-core work: the
+    window rows' scores (32 queries x every head) against the full-width latent, twice."""
+    from paper_2609_37988_amd import synth
+    n = w.tokens
+    dims = kvk.make_dims(kvk.MLA, 1, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, w.latent_dim, w.rope_dim,
+                         w.nope_dim, w.v_dim, qscheme=w.qscheme, batch=w.batch, max_tokens=n, keep_tokens=n // 2)
+    t = kvk.layer_table(dims, kvk.make_plan([(0, 16, w.latent_dim)]))
+    c = synth.latent_random(95, w.batch, n, w.latent_dim, device=dev)
+    r = synth.latent_random(96, w.batch, n, w.rope_dim, device=dev)
+    q = synth.q_random(97, w.batch, 32, w.n_q_heads, w.nope_dim + w.rope_dim, device=dev)
+    wk = kvk.mla_weights_for_library(synth.weights_random(98, 1, w.n_q_heads, w.nope_dim, w.latent_dim,
+                                                          device=dev))[0]
+    keep = torch.empty((w.batch, n // 2), dtype=torch.int32, device=dev)
+    ws = torch.empty(kvk.snapkv_workspace_bytes(t, n), dtype=torch.uint8, device=dev)
+    scale = w.softmax_scale()
+    for _ in range(2):
+        kvk.snapkv_select_mla(t, 0, c, r, q, n, scale, keep, ws, w_uk=wk)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        kvk.snapkv_select_mla(t, 0, c, r, q, n, scale, keep, ws, w_uk=wk)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms = sorted(ts)[2]
+    width = w.latent_dim + w.rope_dim
+    nbytes = 2 * w.batch * n * width * 2
+    flops = 2 * 2.0 * w.batch * n * 32 * w.n_q_heads * width
+    del c, r, q, wk, ws
+    torch.cuda.empty_cache()
+    return {"batch": w.batch, "tokens": n, "keep": n // 2, "q_heads": w.n_q_heads, "latent_dim": w.latent_dim,
+            "us": round(ms * 1e3, 1), "key_reads_GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "TFLOP/s": round(flops / (ms * 1e-3) / 1e12, 1)}
 
 
 def main():

@@ -407,10 +407,38 @@ kvk_status kvk_append_token(const kvk_table* table, int32_t layer_begin, int32_t
  * exact for the importances it computes (fp32).  An inheriting layer returns
  * KVK_OK and writes nothing.
  * Errors: KVK_ERR_INVALID (table without eviction or keep_tokens < 32, sizes, NULL
- *         pointers, misalignment), KVK_ERR_UNSUPPORTED (MLA table, dtype other than
+ *         pointers, misalignment), KVK_ERR_UNSUPPORTED (MLA table: kvk_snapkv_select_mla; dtype other than
  *         bf16, more than 8 query heads per KV head, d_h other than 64 or 128),
  *         KVK_ERR_BUFFER (workspace), KVK_ERR_DEVICE. */
 kvk_status kvk_snapkv_workspace_bytes(const kvk_table* table, int32_t n_tokens, size_t* out_bytes);
+
+/* The query-aware keep list of one MLA anchor layer (§3.4, App. F.3 as above; the
+ * rank axis of §2.1 and App. C.2): the latent is shared by every head, so a
+ * sequence keeps one list of positions.  Head h's key at position t is
+ * [W_UK[h] c_t ; k^R_t] with the latent at its full width r (the layer then stores
+ * the first d coordinates of the kept tokens); a position's importance sums the
+ * causal softmax probabilities of the 32 window queries of every query head; the
+ * selection rule is kvk_snapkv_select's.  Computed in the absorbed form: the window
+ * queries are absorbed (q~ = W_UK[h]^T q_nope, fp16) and scored against the latent
+ * on the matrix cores (fp16 products, fp32 accumulation).
+ *   latent    : device bf16 [B][n_tokens][r] (the tensor kvk_compress_layer takes).
+ *   k_rope    : device bf16 [B][n_tokens][64], the positional keys after RoPE.
+ *   q_obs     : device bf16 [B][32][Hq][nope_dim + 64], the window queries (per head
+ *               the no-RoPE part, then the RoPE part).
+ *   w_uk      : device bf16 [Hq][r][nope_dim], this layer's W_UK as
+ *               kvk_mla_arrange_w_uk writes it; NULL: the attached weights' layer.
+ *   keep_out  : device int32 [B][keep_tokens], increasing.
+ *   importance: NULL, or device fp32 [B][n_tokens].
+ *   workspace : device, >= kvk_snapkv_workspace_bytes(table, n_tokens), 256-byte aligned.
+ * latent_dim 256, 512, 768 or 1024.  An inheriting layer (one-plan tables) returns
+ * KVK_OK and writes nothing; per-sequence tables score every sequence.
+ * Errors: KVK_ERR_INVALID (GQA table, no eviction or keep_tokens < 32, sizes, NULL,
+ *         no weights, misalignment), KVK_ERR_UNSUPPORTED (latent_dim),
+ *         KVK_ERR_BUFFER (workspace), KVK_ERR_DEVICE. */
+kvk_status kvk_snapkv_select_mla(const kvk_table* table, int32_t layer, const void* latent, const void* k_rope,
+                                 const void* q_obs, const void* w_uk, int32_t n_tokens, float scale,
+                                 int32_t* keep_out, float* importance, void* workspace, size_t ws_bytes,
+                                 hipStream_t stream);
 kvk_status kvk_snapkv_select(const kvk_table* table, int32_t layer, const void* k, const void* q_obs,
                              int32_t in_dtype, int32_t n_tokens, float scale, int32_t* keep_out,
                              float* importance, void* workspace, size_t ws_bytes, hipStream_t stream);

@@ -203,6 +203,11 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
 kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored,
                             const void* w_uv, const void* workspace, float* out,
                             hipStream_t stream, int64_t out_lstride = 0);
+// The absorbed queries of `rows` query rows [rows][Hq][nope + d_R] (bf16) at the full
+// latent width: out fp16 [rows][Hp][r + d_R], prescaled by scale log2 e (the decode's
+// absorption with the window positions of the query-aware keep list as rows).
+kvk_status mla_absorb_rows(const kvk_table* t, const void* q, int32_t rows, const void* w_uk, void* out,
+                           float scale, hipStream_t stream);
 kvk_status mla_debug_dequantize(const kvk_table* t, int32_t layer, int32_t n_stored,
                                 const void* arena, float* c_out, float* r_out, hipStream_t stream);
 

@@ -1553,6 +1553,29 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
   return KVK_OK;
 }
 
+kvk_status mla_absorb_rows(const kvk_table* t, const void* q, int32_t rows, const void* w_uk, void* out,
+                           float scale, hipStream_t stream) {
+  const kvk_dims& d = t->d;
+  MlaAbsorbArgs aa;
+  aa.q = q;
+  aa.w_ukt = static_cast<const uint16_t*>(w_uk);
+  aa.ws = static_cast<uint8_t*>(out);
+  aa.q_f32 = 0;
+  aa.B = rows;
+  aa.Hq = d.n_q_heads;
+  aa.Hp = mla_heads_padded(d.n_q_heads);
+  aa.nope = d.nope_dim;
+  aa.r = d.latent_dim;
+  aa.q_lstride = (int64_t)rows * d.n_q_heads * (d.nope_dim + d.rope_dim);
+  aa.scale_log2 = scale * kLog2e;
+  aa.q_off[0] = 0;
+  aa.d_of[0] = d.latent_dim;  // the full width
+  hipLaunchKernelGGL(mla_absorb_kernel, dim3(1u, (unsigned)aa.Hp), dim3(256), 0, stream, aa);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA absorb launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
 kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t n_stored, const void* w_uv,
                             const void* workspace, float* out, hipStream_t stream, int64_t out_lstride) {
   const kvk_dims& d = t->d;

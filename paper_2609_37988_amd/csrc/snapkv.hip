@@ -313,6 +313,159 @@ __global__ __launch_bounds__(1024) void snap_topk_kernel(SnapArgs a) {
   for (int i = tid; i < kWin; i += 1024) out[k + i] = np + i;
 }
 
+// ---------------------------------------------------------------------------
+// MLA layers (one keep list per sequence: the heads share the latent).  Rows of a
+// sequence are (window slot w, head h), row index w Hp + h over the padded head
+// count Hp; the absorbed window queries q~ = W_UK[h]^T q_nope (full latent width
+// r, prescaled by scale log2 e, fp16) and the RoPE part, [B][32][Hp][r + d_R], come
+// from the absorption kernel.  Head h's score of position t is then
+// q~ . c_t + q_rope . k^R_t; padding heads (h >= Hq) take no part.
+// ---------------------------------------------------------------------------
+
+constexpr int kMlaChunk = 256;  // tokens per workgroup in the MLA score passes
+
+struct SnapMlaArgs {
+  const uint16_t* lat;   // [B][n][r] bf16 latent (full width)
+  const uint16_t* rope;  // [B][n][64] bf16 positional keys
+  const _Float16* q;     // [B][32][Hp][r + 64] absorbed window queries
+  float* part;           // [B][RB][P][64] x (max, sum)
+  float* stats;          // [B][32 Hp] x (M, 1/L)
+  float* ipart;          // [B][RB][n] importance of each 64-row block
+  float* imp;            // [B][n]
+  int32_t n, P, RB, Hq, Hp, r;
+};
+
+__device__ __forceinline__ f4 mfma_f16(half8 a, half8 b, f4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// One workgroup per (256-token chunk, 64-row block, sequence); wave w holds the
+// fp16 fragments of rows 16 w .. + 15 of the block (B operand) for the whole chunk.
+// Per 32 tokens the chunk's latent and positional keys are staged in LDS as fp16
+// rows (pitch W + 8 halfs: 16 consecutive rows start 16 distinct 4-bank windows
+// apart) and each wave scores both 16-token tiles (A operand from LDS): lane
+// (i16, kg) gets tokens 4 kg .. + 3 of its row i16.
+// PASS 0: per row the chunk's max and sum of 2^(s - max).  PASS 1: per token the sum
+// over the block's rows of 2^(s - M) / L.
+template <int NK, int PASS>
+__global__ __launch_bounds__(256) void snap_mla_scores_kernel(SnapMlaArgs a) {
+  constexpr int W = 32 * NK, PT = W + 8;
+  __shared__ __attribute__((aligned(16))) _Float16 tile[32 * PT];
+  __shared__ float red[4][32];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, i16 = lane & 15, kg = lane >> 4;
+  const int p = blockIdx.x, rb = blockIdx.y, b = blockIdx.z;
+  const int row = 64 * rb + 16 * wv + i16;  // w Hp + h
+  const int w = row / a.Hp, h = row - w * a.Hp;
+  const bool valid = h < a.Hq;
+  const int lastvis = a.n - kWin + w;  // the row's window query sees t <= lastvis
+  half8 qf[NK];
+  {
+    const _Float16* qr = a.q + ((int64_t)b * kWin * a.Hp + row) * W + 8 * kg;
+#pragma unroll
+    for (int j = 0; j < NK; ++j) qf[j] = *reinterpret_cast<const half8*>(qr + 32 * j);
+  }
+  float m = -INFINITY, l = 0.0f, sM = 0.0f, sL = 0.0f;
+  if constexpr (PASS == 1) {
+    if (valid) {
+      sM = a.stats[((int64_t)b * kWin * a.Hp + row) * 2];
+      sL = a.stats[((int64_t)b * kWin * a.Hp + row) * 2 + 1];
+    }
+  }
+  const int t0 = p * kMlaChunk, t1 = min(a.n, t0 + kMlaChunk);
+  for (int tb = t0; tb < t1; tb += 32) {
+    __syncthreads();  // the tile (and red) are free
+    for (int c = tid; c < 32 * (W / 8); c += 256) {
+      const int tr = c / (W / 8), c8 = 8 * (c - tr * (W / 8));
+      const int t = tb + tr;
+      u4v v = {0u, 0u, 0u, 0u};
+      if (t < t1)
+        v = c8 < a.r ? *reinterpret_cast<const u4v*>(a.lat + ((int64_t)b * a.n + t) * a.r + c8)
+                     : *reinterpret_cast<const u4v*>(a.rope + ((int64_t)b * a.n + t) * 64 + (c8 - a.r));
+      half8 x;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        x[2 * e] = (_Float16)__uint_as_float(v[e] << 16);
+        x[2 * e + 1] = (_Float16)__uint_as_float(v[e] & 0xFFFF0000u);
+      }
+      *reinterpret_cast<half8*>(tile + tr * PT + c8) = x;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      f4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < NK; ++j)
+        acc = mfma_f16(*reinterpret_cast<const half8*>(tile + (16 * tt + i16) * PT + 32 * j + 8 * kg), qf[j], acc);
+      float x[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int t = tb + 16 * tt + 4 * kg + e;
+        const bool vis = valid && t < t1 && t <= lastvis;
+        if constexpr (PASS == 0) {
+          if (vis) {
+            if (acc[e] > m) {
+              l *= __builtin_amdgcn_exp2f(m - acc[e]);
+              m = acc[e];
+            }
+            l += __builtin_amdgcn_exp2f(acc[e] - m);
+          }
+        } else {
+          x[e] = vis ? __builtin_amdgcn_exp2f(acc[e] - sM) * sL : 0.0f;
+        }
+      }
+      if constexpr (PASS == 1) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float sum = sum16(x[e]);  // over the wave's 16 rows
+          if (i16 == 0) red[wv][16 * tt + 4 * kg + e] = sum;
+        }
+      }
+    }
+    if constexpr (PASS == 1) {
+      __syncthreads();
+      if (tid < 32 && tb + tid < t1)
+        a.ipart[((int64_t)b * a.RB + rb) * a.n + tb + tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
+    }
+  }
+  if constexpr (PASS == 0) {  // the row's four token groups (lanes i16 + 16 kg)
+    const float M = rows_max(m);
+    const float L = rows_sum(M == -INFINITY ? 0.0f : l * __builtin_amdgcn_exp2f(m - M));
+    if (kg == 0) {
+      float* out = a.part + (((int64_t)b * a.RB + rb) * a.P + p) * 128 + 2 * (16 * wv + i16);
+      out[0] = M;
+      out[1] = L;
+    }
+  }
+}
+
+// Per (sequence, row): the chunks' (max, sum) merged into (M, 1/L).
+__global__ __launch_bounds__(256) void snap_mla_merge_kernel(SnapMlaArgs a) {
+  const int b = blockIdx.y, row = blockIdx.x * 256 + threadIdx.x;
+  if (row >= kWin * a.Hp) return;
+  const int rb = row >> 6, rr = row & 63;
+  const float* pp = a.part + ((int64_t)b * a.RB + rb) * a.P * 128 + 2 * rr;
+  float M = -INFINITY;
+  for (int p = 0; p < a.P; ++p) M = fmaxf(M, pp[(int64_t)p * 128]);
+  float L = 0.0f;
+  for (int p = 0; p < a.P; ++p) {
+    const float mp = pp[(int64_t)p * 128];
+    if (mp != -INFINITY) L += pp[(int64_t)p * 128 + 1] * __builtin_amdgcn_exp2f(mp - M);
+  }
+  float* st = a.stats + ((int64_t)b * kWin * a.Hp + row) * 2;
+  st[0] = M;
+  st[1] = L > 0.0f ? 1.0f / L : 0.0f;  // a padding head's row has no mass
+}
+
+// importance[b][t] = the row blocks' partial sums, added in block order.
+__global__ __launch_bounds__(256) void snap_mla_reduce_kernel(SnapMlaArgs a) {
+  const int b = blockIdx.y, t = blockIdx.x * 256 + threadIdx.x;
+  if (t >= a.n) return;
+  const float* ip = a.ipart + (int64_t)b * a.RB * a.n + t;
+  float s = 0.0f;
+  for (int rb = 0; rb < a.RB; ++rb) s += ip[(int64_t)rb * a.n];
+  a.imp[(int64_t)b * a.n + t] = s;
+}
+
 }  // namespace
 
 using namespace kvk;
@@ -350,10 +503,49 @@ void launch_scores(int D, int G, dim3 gs, size_t lds, hipStream_t stream, const 
 #undef KVK_SNAP
 }
 
+struct SnapMlaSizes {
+  int64_t q, part, stats, ipart, imp;  // bytes
+  int32_t P, RB, Hp;
+};
+
+SnapMlaSizes snap_mla_sizes(const kvk_table* t, int32_t n_tokens) {
+  const kvk_dims& d = t->d;
+  SnapMlaSizes s;
+  s.Hp = mla_heads_padded(d.n_q_heads);
+  s.P = (n_tokens + kMlaChunk - 1) / kMlaChunk;
+  s.RB = kWin * s.Hp / 64;
+  s.q = round256((int64_t)d.batch * kWin * s.Hp * (d.latent_dim + d.rope_dim) * 2);
+  s.part = round256((int64_t)d.batch * s.RB * s.P * 128 * 4);
+  s.stats = round256((int64_t)d.batch * kWin * s.Hp * 2 * 4);
+  s.ipart = round256((int64_t)d.batch * s.RB * n_tokens * 4);
+  s.imp = round256((int64_t)d.batch * n_tokens * 4);
+  return s;
+}
+
+kvk_status snap_check_common(const kvk_table* t, int32_t n_tokens) {
+  const kvk_dims& d = t->d;
+  if (d.keep_tokens < kWin)
+    return fail(KVK_ERR_INVALID, "snapkv: the table must evict with keep_tokens >= %d (has %d)", kWin,
+                d.keep_tokens);
+  if (n_tokens < d.keep_tokens || n_tokens > d.max_tokens)
+    return fail(KVK_ERR_INVALID, "snapkv: n_tokens %d outside keep_tokens..max_tokens (%d..%d)", n_tokens,
+                d.keep_tokens, d.max_tokens);
+  return KVK_OK;
+}
+
+kvk_status snap_mla_check(const kvk_table* t, int32_t n_tokens) {
+  if (!t) return fail(KVK_ERR_INVALID, "snapkv: NULL table");
+  const kvk_dims& d = t->d;
+  if (d.kind != KVK_MLA) return fail(KVK_ERR_INVALID, "kvk_snapkv_select_mla: an MLA table is required");
+  if (d.latent_dim != 256 && d.latent_dim != 512 && d.latent_dim != 768 && d.latent_dim != 1024)
+    return fail(KVK_ERR_UNSUPPORTED, "kvk_snapkv_select_mla: latent_dim %d (256, 512, 768 or 1024)", d.latent_dim);
+  return snap_check_common(t, n_tokens);
+}
+
 kvk_status snap_check(const kvk_table* t, int32_t n_tokens) {
   if (!t) return fail(KVK_ERR_INVALID, "snapkv: NULL table");
   const kvk_dims& d = t->d;
-  if (d.kind != KVK_GQA) return fail(KVK_ERR_UNSUPPORTED, "snapkv: GQA tables only");
+  if (d.kind != KVK_GQA) return fail(KVK_ERR_UNSUPPORTED, "kvk_snapkv_select: GQA tables (MLA: kvk_snapkv_select_mla)");
   if (d.keep_tokens < kWin)
     return fail(KVK_ERR_INVALID, "snapkv: the table must evict with keep_tokens >= %d (has %d)", kWin,
                 d.keep_tokens);
@@ -369,6 +561,14 @@ kvk_status snap_check(const kvk_table* t, int32_t n_tokens) {
 }  // namespace
 
 extern "C" kvk_status kvk_snapkv_workspace_bytes(const kvk_table* t, int32_t n_tokens, size_t* out) {
+  if (t && t->d.kind == KVK_MLA) {
+    const kvk_status st = snap_mla_check(t, n_tokens);
+    if (st != KVK_OK) return st;
+    if (!out) return fail(KVK_ERR_INVALID, "snapkv: NULL output");
+    const SnapMlaSizes s = snap_mla_sizes(t, n_tokens);
+    *out = (size_t)(s.q + s.part + s.stats + s.ipart + s.imp);
+    return KVK_OK;
+  }
   const kvk_status st = snap_check(t, n_tokens);
   if (st != KVK_OK) return st;
   if (!out) return fail(KVK_ERR_INVALID, "snapkv: NULL output");
@@ -427,5 +627,77 @@ extern "C" kvk_status kvk_snapkv_select(const kvk_table* t, int32_t layer, const
   hipLaunchKernelGGL(snap_topk_kernel, dim3((unsigned)bh), dim3(1024), 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "snapkv launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+extern "C" kvk_status kvk_snapkv_select_mla(const kvk_table* t, int32_t layer, const void* latent,
+                                            const void* k_rope, const void* q_obs, const void* w_uk,
+                                            int32_t n_tokens, float scale, int32_t* keep_out,
+                                            float* importance_out, void* workspace, size_t ws_bytes,
+                                            hipStream_t stream) {
+  kvk_status st = snap_mla_check(t, n_tokens);
+  if (st != KVK_OK) return st;
+  const kvk_dims& d = t->d;
+  if (layer < 0 || layer >= d.n_layers) return fail(KVK_ERR_INVALID, "layer %d out of range", layer);
+  if (t->seq.empty() && t->plan[layer].inherit) return KVK_OK;  // nothing stored to select from
+  if (!w_uk && t->mla_w_uk)
+    w_uk = static_cast<const uint8_t*>(t->mla_w_uk) + (int64_t)layer * d.n_q_heads * d.latent_dim * d.nope_dim * 2;
+  if (!latent || !k_rope || !q_obs || !w_uk || !keep_out || !workspace)
+    return fail(KVK_ERR_INVALID, "kvk_snapkv_select_mla: NULL buffer (w_uk: passed or attached)");
+  if (!(scale == scale)) return fail(KVK_ERR_INVALID, "snapkv: scale is NaN");
+  if ((reinterpret_cast<uintptr_t>(latent) & 15) || (reinterpret_cast<uintptr_t>(k_rope) & 15) ||
+      (reinterpret_cast<uintptr_t>(q_obs) & 15) || (reinterpret_cast<uintptr_t>(w_uk) & 15) ||
+      (reinterpret_cast<uintptr_t>(keep_out) & 3) || (reinterpret_cast<uintptr_t>(importance_out) & 3) ||
+      (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return fail(KVK_ERR_INVALID, "snapkv: misaligned buffer (inputs 16 B, keep/importance 4 B, workspace 256 B)");
+  size_t need = 0;
+  kvk_snapkv_workspace_bytes(t, n_tokens, &need);
+  if (need > ws_bytes) return fail(KVK_ERR_BUFFER, "snapkv: workspace %zu bytes < %zu needed", ws_bytes, need);
+  const SnapMlaSizes s = snap_mla_sizes(t, n_tokens);
+  if (d.batch > 65535 || s.P > 65535 || s.RB > 65535) return fail(KVK_ERR_UNSUPPORTED, "snapkv: grid too large");
+  if (kvk_status st2 = check_gpu_buffers({latent, k_rope, q_obs, w_uk, keep_out, importance_out, workspace},
+                                         "kvk_snapkv_select_mla"))
+    return st2;
+  uint8_t* wsb = static_cast<uint8_t*>(workspace);
+  // the absorbed window queries: the B x 32 window positions as rows of the absorption
+  st = mla_absorb_rows(t, q_obs, d.batch * kWin, w_uk, wsb, scale, stream);
+  if (st != KVK_OK) return st;
+  SnapMlaArgs a;
+  a.lat = static_cast<const uint16_t*>(latent);
+  a.rope = static_cast<const uint16_t*>(k_rope);
+  a.q = reinterpret_cast<const _Float16*>(wsb);
+  a.part = reinterpret_cast<float*>(wsb + s.q);
+  a.stats = reinterpret_cast<float*>(wsb + s.q + s.part);
+  a.ipart = reinterpret_cast<float*>(wsb + s.q + s.part + s.stats);
+  a.imp = importance_out ? importance_out : reinterpret_cast<float*>(wsb + s.q + s.part + s.stats + s.ipart);
+  a.n = n_tokens;
+  a.P = s.P;
+  a.RB = s.RB;
+  a.Hq = d.n_q_heads;
+  a.Hp = s.Hp;
+  a.r = d.latent_dim;
+  const dim3 gs((unsigned)s.P, (unsigned)s.RB, (unsigned)d.batch), b256(256);
+  const dim3 gm((unsigned)((kWin * s.Hp + 255) / 256), (unsigned)d.batch);
+  const dim3 gr((unsigned)((n_tokens + 255) / 256), (unsigned)d.batch);
+#define KVK_SNAP_MLA(PASS)                                                                                  \
+  switch (d.latent_dim) {                                                                                   \
+    case 256: hipLaunchKernelGGL((snap_mla_scores_kernel<10, PASS>), gs, b256, 0, stream, a); break;        \
+    case 512: hipLaunchKernelGGL((snap_mla_scores_kernel<18, PASS>), gs, b256, 0, stream, a); break;        \
+    case 768: hipLaunchKernelGGL((snap_mla_scores_kernel<26, PASS>), gs, b256, 0, stream, a); break;        \
+    default: hipLaunchKernelGGL((snap_mla_scores_kernel<34, PASS>), gs, b256, 0, stream, a); break;         \
+  }
+  KVK_SNAP_MLA(0)
+  hipLaunchKernelGGL(snap_mla_merge_kernel, gm, b256, 0, stream, a);
+  KVK_SNAP_MLA(1)
+#undef KVK_SNAP_MLA
+  hipLaunchKernelGGL(snap_mla_reduce_kernel, gr, b256, 0, stream, a);
+  SnapArgs k{};  // the selection, one stream per sequence
+  k.imp = a.imp;
+  k.keep = keep_out;
+  k.n = n_tokens;
+  k.keep_n = d.keep_tokens;
+  hipLaunchKernelGGL(snap_topk_kernel, dim3((unsigned)d.batch), dim3(1024), 0, stream, k);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "snapkv (MLA) launch: %s", hipGetErrorString(e));
   return KVK_OK;
 }

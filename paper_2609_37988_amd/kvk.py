@@ -74,6 +74,7 @@ def load() -> ctypes.CDLL:
             "kvk_compress_layer_project": (I32, [P, I32, P, P, I32, P, I32, P, P, P, P]),
             "kvk_mla_arrange_w_uk": (I32, [P, I32, I32, I32, I32, P, P]),
             "kvk_set_mla_weights": (I32, [P, P, P]),
+            "kvk_snapkv_select_mla": (I32, [P, I32, P, P, P, P, I32, F, P, P, P, ctypes.c_size_t, P]),
             "kvk_append_token": (I32, [P, I32, I32, P, P, I32, I32, P, P]),
             "kvk_snapkv_workspace_bytes": (I32, [P, I32, ctypes.POINTER(ctypes.c_size_t)]),
             "kvk_selector_weight_elems": (I64, [I32, I32, I32]),
@@ -105,6 +106,7 @@ def exported_symbols() -> List[str]:
     """Names of the C entry points the binding expects libkvk to export."""
     return ["kvk_layer_table", "kvk_layer_table_batched", "kvk_table_sequence_query", "kvk_table_query", "kvk_table_destroy", "kvk_workspace_bytes",
             "kvk_compress_layer", "kvk_compress_layer_project", "kvk_mla_arrange_w_uk", "kvk_set_mla_weights",
+            "kvk_snapkv_select_mla",
             "kvk_append_token", "kvk_snapkv_workspace_bytes", "kvk_snapkv_select",
             "kvk_selector_weight_elems", "kvk_selector_workspace_bytes", "kvk_selector_forward",
             "kvk_decode_attention", "kvk_decode_splits", "kvk_decode_merge", "kvk_decode_attention_noalloc", "kvk_decode_setup",
@@ -414,6 +416,36 @@ def snapkv_select(t: Table, layer: int, k: torch.Tensor, q_obs: torch.Tensor, n_
     _check(load().kvk_snapkv_select(t.handle, layer, _ptr(k), _ptr(q_obs), _dtype_code(k), n_tokens, float(scale),
                                     _ptr(keep_out), _ptr(importance), _ptr(workspace), _nbytes(workspace),
                                     _stream(stream)))
+
+
+def snapkv_select_mla(t: Table, layer: int, latent: torch.Tensor, k_rope: torch.Tensor, q_obs: torch.Tensor,
+                      n_tokens: int, scale: float, keep_out: torch.Tensor, workspace: torch.Tensor,
+                      w_uk: Optional[torch.Tensor] = None, importance: Optional[torch.Tensor] = None, stream=None):
+    """MLA keep list of one anchor layer at prefill, one list per sequence.  latent
+    [B, n_tokens, r], k_rope [B, n_tokens, 64], q_obs [B, 32, Hq, nope + 64] bf16;
+    w_uk [Hq, r, nope] (this layer's, as mla_weights_for_library arranges it) or None
+    for the attached weights; keep_out int32 [B, keep_tokens]; importance (optional)
+    fp32 [B, n_tokens]."""
+    d = t.dims
+    _need(d.kind == MLA, "an MLA table is required")
+    _need(latent.dtype == k_rope.dtype == q_obs.dtype == torch.bfloat16 and latent.is_contiguous() and
+          k_rope.is_contiguous() and q_obs.is_contiguous(), "latent, k_rope and q_obs must be contiguous bf16")
+    _need(latent.numel() == d.batch * n_tokens * d.latent_dim and k_rope.numel() == d.batch * n_tokens * d.rope_dim,
+          "latent must be B*n_tokens*r and k_rope B*n_tokens*64")
+    _need(q_obs.numel() == d.batch * 32 * d.n_q_heads * (d.nope_dim + d.rope_dim), "q_obs must be B*32*Hq*(nope+64)")
+    if w_uk is not None:
+        _need(w_uk.dtype == torch.bfloat16 and w_uk.is_contiguous() and
+              w_uk.numel() == d.n_q_heads * d.latent_dim * d.nope_dim, "w_uk must be bf16 [Hq, r, nope]")
+    else:
+        _need(t.mla_weights is not None, "pass w_uk or attach the weights (set_mla_weights)")
+    _need(keep_out.dtype == torch.int32 and keep_out.is_contiguous() and keep_out.numel() == d.batch * d.keep_tokens,
+          "keep_out must be int32 B*keep_tokens")
+    if importance is not None:
+        _need(importance.dtype == torch.float32 and importance.is_contiguous() and
+              importance.numel() == d.batch * n_tokens, "importance must be fp32 B*n_tokens")
+    _check(load().kvk_snapkv_select_mla(t.handle, layer, _ptr(latent), _ptr(k_rope), _ptr(q_obs), _ptr(w_uk),
+                                        n_tokens, float(scale), _ptr(keep_out), _ptr(importance), _ptr(workspace),
+                                        _nbytes(workspace), _stream(stream)))
 
 
 # Composed action space (eq. (3)): index 0 = inherit, 1 + 4 j + k = produce with
