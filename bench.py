@@ -366,6 +366,7 @@ def run_mla(args):
     wk = kvk.mla_weights_for_library(wk)  # arranged once, as at weight load
     out = torch.empty((w.n_layers, w.batch, w.n_q_heads, w.v_dim), dtype=torch.float32, device=dev)
     ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=dev)
+    kvk.decode_setup(table, 0, w.n_layers, ws)  # per-sequence plans: the work list, once
     scale = w.softmax_scale()
     alg = kvk.read_bytes(table, 0, w.n_layers, n_stored)
     for i in range(args.warmup):

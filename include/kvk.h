@@ -256,11 +256,13 @@ kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* plan, kvk_tab
  * GQA: one kvk_decode_attention call decodes the whole batch in one launch, each
  * sequence reading its own anchors once (its work list, one item per sequence and
  * anchor, sits at the head of the workspace, written there once per workspace and
- * layer range by kvk_decode_setup; decode calls then copy nothing).  MLA: the call
- * decodes sequence by sequence (A1 + D2 and C2 of each sequence's own table, its
- * query and output rows read and written in place), each sequence in its own part
- * of the workspace; no set-up is needed; kvk_compress_layer_project takes the
- * table with latent_out NULL.  kvk_read_bytes sums the sequences.  kvk_table_query reports the batch (arena_bytes, workspace_bytes,
+ * layer range by kvk_decode_setup; decode calls then copy nothing).  MLA: likewise
+ * one launch per phase for the batch (A1 over every (layer, sequence) at its own
+ * kept width, D2 over every (sequence, anchor), C2 over every (layer, sequence)),
+ * from the work list kvk_decode_setup writes; sequence b's absorbed queries and
+ * partials sit in its own part of the workspace, after the list, as its one-sequence
+ * table lays them out, so each sequence's output equals that table's bit for bit;
+ * kvk_compress_layer_project takes the table with latent_out NULL.  kvk_read_bytes sums the sequences.  kvk_table_query reports the batch (arena_bytes, workspace_bytes,
  * n_anchors over all sequences, rho of the mean plan); its per-layer fields are
  * empty (anchor_of and layer_offset -1): use kvk_table_sequence_query.
  * Errors: KVK_ERR_INVALID, and those of kvk_layer_table for a sequence's plan. */
@@ -496,9 +498,11 @@ kvk_status kvk_selector_forward(int32_t d_model, int32_t n_layers, int32_t n_act
  * must keep its list (and stay allocated) while it is used for decoding: a set-up
  * of another range on the same workspace replaces the record; a list that does not
  * match the call's (a workspace overwritten since) makes the kernels write NaN
- * outputs and read nothing through it.  One-plan tables and MLA tables: a no-op
- * (a one-plan work list travels in the kernel arguments; MLA decodes a
- * per-sequence batch sequence by sequence).
+ * outputs and read nothing through it.  MLA per-sequence tables: the list holds a
+ * row per (layer, sequence) (kept width, where its absorbed queries and split
+ * partials sit, its anchor's split rule) and an item per (sequence, anchor) for each
+ * decode launch; the splits of a call follow from its n_stored in the kernels.
+ * One-plan tables: a no-op (the work list travels in the kernel arguments).
  * Errors: KVK_ERR_INVALID (range, NULL), KVK_ERR_BUFFER (workspace too small),
  *         KVK_ERR_DEVICE (the copy). */
 kvk_status kvk_decode_setup(const kvk_table* table, int32_t layer_begin, int32_t layer_end, void* workspace,

@@ -1217,38 +1217,6 @@ kvk_status mla_check(const kvk_table* t, int32_t l0, int32_t l1, const void* q, 
   return check_gpu_buffers({q, w_uk, w_uv, arena, out, workspace}, "decode");
 }
 
-// MLA under per-sequence plans: each sequence decodes with its own one-sequence table
-// (A1 + D2 and / or C2), its query and output rows read and written in place with
-// the batch's layer strides, in its own part of the workspace (the parts in
-// sequence order, as kvk_workspace_bytes sizes them).
-kvk_status mla_decode_per_sequence(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
-                                   int32_t n_stored, float scale, const void* w_uk, const void* w_uv,
-                                   const void* arena, float* out, const void* workspace, hipStream_t stream,
-                                   bool splits, bool merge) {
-  const kvk_dims& d = t->d;
-  const int64_t qw = d.nope_dim + d.rope_dim, elt = q_dtype == KVK_F32 ? 4 : 2;
-  const int64_t q_ls = (int64_t)d.batch * d.n_q_heads * qw, o_ls = (int64_t)d.batch * d.n_q_heads * d.v_dim;
-  uint8_t* ws = static_cast<uint8_t*>(const_cast<void*>(workspace));
-  for (int b = 0; b < d.batch; ++b) {
-    const kvk_table* s = t->seq[b];
-    const void* ab = static_cast<const uint8_t*>(arena) + t->seq_base[b];
-    if (splits) {
-      const void* qb = static_cast<const uint8_t*>(q) + (int64_t)b * d.n_q_heads * qw * elt;
-      if (kvk_status st = mla_decode_splits(s, l0, l1, qb, q_dtype, n_stored, scale, w_uk, ab, ws, stream, q_ls))
-        return st;
-    }
-    if (merge) {
-      if (kvk_status st = mla_decode_merge(s, l0, l1, n_stored, w_uv, ws, out + (int64_t)b * d.n_q_heads * d.v_dim,
-                                           stream, o_ls))
-        return st;
-    }
-    MlaWorkspace w;
-    mla_workspace(s, l0, l1, &w);
-    ws += w.total;
-  }
-  return KVK_OK;
-}
-
 }  // namespace
 
 namespace kvk {
@@ -1268,8 +1236,8 @@ extern "C" kvk_status kvk_decode_attention(const kvk_table* t, int32_t l0, int32
                               ws_bytes);
     if (st != KVK_OK) return st;
     if (!t->seq.empty())
-      return mla_decode_per_sequence(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
-                                     stream, true, true);
+      return mla_decode_batched(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
+                                stream, true, true);
     st = mla_decode_splits(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, arena, workspace, stream);
     if (st != KVK_OK) return st;
     return mla_decode_merge(t, l0, l1, n_stored, w_uv, workspace, out, stream);
@@ -1293,8 +1261,8 @@ extern "C" kvk_status kvk_decode_splits(const kvk_table* t, int32_t l0, int32_t 
                                     workspace, ws_bytes);
     if (st != KVK_OK) return st;
     if (!t->seq.empty())
-      return mla_decode_per_sequence(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, nullptr,
-                                     workspace, stream, true, false);
+      return mla_decode_batched(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, nullptr, workspace,
+                                stream, true, false);
     return mla_decode_splits(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, arena, workspace, stream);
   }
   DecodePlan P;
@@ -1316,8 +1284,8 @@ extern "C" kvk_status kvk_decode_merge(const kvk_table* t, int32_t l0, int32_t l
                                     workspace, ws_bytes);
     if (st != KVK_OK) return st;
     if (!t->seq.empty())
-      return mla_decode_per_sequence(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out, workspace,
-                                     stream, false, true);
+      return mla_decode_batched(t, l0, l1, q, q_dtype, n_stored, scale, w_uk, w_uv, arena, out,
+                                const_cast<void*>(workspace), stream, false, true);
     return mla_decode_merge(t, l0, l1, n_stored, w_uv, workspace, out, stream);
   }
   DecodePlan P;
@@ -1333,13 +1301,23 @@ extern "C" kvk_status kvk_decode_setup(const kvk_table* t, int32_t l0, int32_t l
   if (l0 < 0 || l1 > t->d.n_layers || l0 >= l1)
     return fail(KVK_ERR_INVALID, "layer range [%d, %d) invalid for %d layers", l0, l1, t->d.n_layers);
   if (!workspace) return fail(KVK_ERR_INVALID, "kvk_decode_setup: NULL workspace");
-  // one plan: the work list travels in the kernel arguments; MLA decodes a
-  // per-sequence batch sequence by sequence, with no work list
-  if (t->seq.empty() || t->d.kind == KVK_MLA) return KVK_OK;
+  // one plan: the work list travels in the kernel arguments
+  if (t->seq.empty()) return KVK_OK;
   DecodePlan P;
-  kvk_status st = prepare(t, l0, l1, nullptr, KVK_BF16, 0, 1.0f, nullptr, nullptr, nullptr, nullptr, workspace,
-                          ws_bytes, P, kForSetup);
-  if (st != KVK_OK) return st;
+  if (t->d.kind == KVK_MLA) {
+    MlaSeqList L;
+    if (kvk_status st = mla_seq_list(t, l0, l1, L, true)) return st;
+    size_t need = 0;
+    if (kvk_status st = kvk_workspace_bytes(t, l0, l1, &need)) return st;
+    if (need > ws_bytes) return fail(KVK_ERR_BUFFER, "workspace %zu bytes < %zu needed", ws_bytes, need);
+    if (kvk_status st = check_gpu_buffers({workspace}, "kvk_decode_setup")) return st;
+    P.list.swap(L.img);
+    P.hash = L.hash;
+  } else {
+    kvk_status st = prepare(t, l0, l1, nullptr, KVK_BF16, 0, 1.0f, nullptr, nullptr, nullptr, nullptr, workspace,
+                            ws_bytes, P, kForSetup);
+    if (st != KVK_OK) return st;
+  }
   {  // the workspace's earlier list (if any) is overwritten now
     std::lock_guard<std::mutex> lock(t->setup_mu);
     auto& v = t->setups;

@@ -100,12 +100,13 @@ constexpr int gqa_ring_depth(int bits) { return bits == 16 ? 2 : (bits == 8 ? 2 
 inline int32_t ring_depth_for(int32_t bits) { return gqa_ring_depth(bits); }
 
 // Blocks processed per split of the decode kernel for a `bits`-bit anchor whose
-// streams hold n_blocks full blocks.  The split count never exceeds the one at a
-// larger n_blocks, so workspace sized at capacity covers every n_stored.
-// `waves` D1 waves read each split (an item's chunk waves), so its target and its
-// bounds are that many times the per-wave ones.
+// streams hold n_blocks full blocks.  *count_bound (if given) receives a bound of the
+// split count of every length up to n_blocks, so that a workspace sized with it at
+// the capacity covers every n_stored (the count itself is not monotone in the
+// length).  `waves` D1 waves read each split (an item's chunk waves), so its target
+// and its bounds are that many times the per-wave ones.
 int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes,
-                         int32_t waves);
+                         int32_t waves, int32_t* count_bound = nullptr);
 // D1 waves per (stream, split) of an item whose anchor's readers give nch 16-row
 // query chunks: 1, 2, or a multiple of 4 (up to 4 share a workgroup, more fill
 // several).
@@ -113,7 +114,7 @@ constexpr int32_t gqa_chunk_waves(int32_t nch) { return nch == 1 ? 1 : (nch == 2
 // Full blocks per split of the D1 item of `anchor` read by the layers of [l0, l1)
 // in table s (split_blocks_for with the item's chunk waves in one workgroup).
 int32_t gqa_item_split_blocks(const kvk_table* s, int32_t anchor, int32_t l0, int32_t l1, int32_t n_blocks,
-                              int64_t target_bytes);
+                              int64_t target_bytes, int32_t* count_bound = nullptr);
 // Bytes per D1 split for a decode over layers [l0, l1) of a GQA table (see table.cpp).
 int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1);
 
@@ -168,6 +169,33 @@ constexpr int kMlaMaxUnits = 128;
 // only a stream's last split prefetches past its end); the split count is
 // monotone in n_blocks.
 int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_blocks);
+// The anchor's split rule in two numbers (mla_split_rule: the target length in
+// blocks and the ring pass nr), from which mla_split_len gives the split length for
+// any n_blocks; the host and the kernels (which know n_blocks only at decode time
+// under per-sequence plans) share it.
+void mla_split_rule(const kvk_table* t, int32_t anchor, int32_t* target, int32_t* nr);
+constexpr int32_t mla_split_len(int32_t target, int32_t nr, int32_t n_blocks) {
+  const int32_t nb = n_blocks > 0 ? n_blocks : 1;
+  if ((int64_t)target * kMlaMaxUnits < nb) target = (nb + kMlaMaxUnits - 1) / kMlaMaxUnits;  // merge limit
+  const int32_t nsplit = (nb + target - 1) / target;
+  const int32_t per = (nb + nsplit - 1) / nsplit;
+  return (per + nr - 1) / nr * nr;
+}
+// At least the splits of every length up to n_blocks_cap full blocks (the partial
+// records a workspace sized at the capacity holds).  The split count itself is not
+// monotone in the length (rounding a split up to whole ring passes can save one: at
+// target 128 blocks and ring pass 6, 2898 blocks take 23 splits and 2899 take 22), but
+// it never exceeds the count before that rounding, ceil(n / target), which is.
+constexpr int32_t mla_units_bound(int32_t target, int32_t n_blocks_cap) {
+  const int32_t nb = n_blocks_cap > 0 ? n_blocks_cap : 1;
+  return (int64_t)target * kMlaMaxUnits < nb ? kMlaMaxUnits : (nb + target - 1) / target;
+}
+// Splits of a stream holding n_stored tokens (n_blocks full ones) with split length
+// `split`: the full blocks in balanced splits, the tail in the last; at least one
+// unit when anything is stored, none otherwise.
+constexpr int32_t mla_units_len(int32_t n_blocks, int32_t n_stored, int32_t split) {
+  return n_stored <= 0 ? 0 : (n_blocks > 0 ? (n_blocks + split - 1) / split : 1);
+}
 
 // Work units (splits) of one MLA stream holding n_stored tokens: the full blocks
 // in balanced splits, the tail tokens in the last one; at least one unit.
@@ -208,6 +236,27 @@ kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t 
 // absorption with the window positions of the query-aware keep list as rows).
 kvk_status mla_absorb_rows(const kvk_table* t, const void* q, int32_t rows, const void* w_uk, void* out,
                            float scale, hipStream_t stream);
+// Per-sequence MLA tables: the work list at the head of the workspace (image when
+// `image`; sizes and offsets always).
+struct MlaSeqList {
+  MlaSeqList();
+  ~MlaSeqList();
+  std::vector<uint8_t> img;
+  int64_t rows_off = 0, items_off[4] = {0, 0, 0, 0}, bytes = 0;
+  int32_t n_items[4] = {0, 0, 0, 0};
+  int64_t n_wg[4] = {0, 0, 0, 0};
+  int32_t dmax = 0;
+  uint64_t hash = 0;
+};
+kvk_status mla_seq_list(const kvk_table* t, int32_t l0, int32_t l1, MlaSeqList& L, bool image);
+// One decode of a per-sequence MLA table (A1 + D2 with `splits`, C2 with `merge`):
+// one launch per phase for the batch, from the list kvk_decode_setup wrote.
+kvk_status mla_decode_batched(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
+                              int32_t n_stored, float scale, const void* w_uk, const void* w_uv,
+                              const void* arena, float* out, void* workspace, hipStream_t stream, bool splits,
+                              bool merge);
+// FNV-1a over n bytes (the work lists' hashes).
+uint64_t fnv1a64(const uint8_t* p, size_t n);
 kvk_status mla_debug_dequantize(const kvk_table* t, int32_t layer, int32_t n_stored,
                                 const void* arena, float* c_out, float* r_out, hipStream_t stream);
 

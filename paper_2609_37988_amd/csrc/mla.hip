@@ -30,6 +30,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstring>
 #include <type_traits>
 #include <vector>
 
@@ -601,6 +602,26 @@ __global__ __launch_bounds__(256) void mla_dequant_kernel(const uint8_t* region,
   else rout[bt * kRope + (c - d)] = x;
 }
 
+// A per-sequence table's work list sits at the head of the workspace: this header,
+// then its rows and items, hashed, so that a kernel reading a list that is not its
+// call's returns without touching memory through it.
+constexpr uint64_t kMlaListMagic = 0x4b564b4d4c413031ull;  // "KVKMLA01"
+
+// One (layer of the range, sequence) of a per-sequence table: where its absorbed
+// queries and split partials sit in the workspace, its kept width and split rule.
+struct MlaSeqRow {
+  int64_t q_off;         // fp16 [Hp][d + 64]
+  int64_t part_off;      // fp32 [units_cap][Hp][d + 2]
+  int32_t d;
+  int32_t units_cap;
+  int32_t split_target, split_nr;
+};
+static_assert(sizeof(MlaSeqRow) == 32, "MlaSeqRow without padding");
+
+__device__ __forceinline__ bool mla_list_ok(const uint64_t* hdr, uint64_t hash) {
+  return !hdr || (hdr[0] == kMlaListMagic && hdr[1] == hash);
+}
+
 // ---------------------------------------------------------------------------
 // A1: absorbed queries, q~ = W_UK[h][:, :d]^T q_nope (scaled into the exp2 domain)
 // ---------------------------------------------------------------------------
@@ -611,39 +632,65 @@ struct MlaAbsorbArgs {
   uint8_t* ws;
   int64_t q_off[KVK_MAX_LAYERS];  // per relative layer: fp16 [B][Hp][d + 64]
   int32_t d_of[KVK_MAX_LAYERS];
+  const MlaSeqRow* rows;  // per-sequence tables: per (relative layer, sequence) (else NULL)
+  const uint64_t* list_hdr;
+  uint64_t list_hash;
   int32_t q_f32;
   int32_t B, Hq, Hp, nope, r;  // Hp: Hq rounded up to whole 32-head chunks
   int64_t q_lstride;           // elements between consecutive layers' queries
   float scale_log2;
 };
 
+// Where sequence b's absorbed queries of relative layer li go, and their kept width:
+// one plan, [B][Hp][d + 64] at q_off[li]; per-sequence plans, [Hp][d_b + 64] at the
+// sequence's row.
+__device__ __forceinline__ _Float16* absorb_dst(const MlaAbsorbArgs& a, int li, int b, int& d) {
+  if (a.rows) {
+    const MlaSeqRow& rw = a.rows[(int64_t)li * a.B + b];
+    d = rw.d;
+    return reinterpret_cast<_Float16*>(a.ws + rw.q_off);
+  }
+  d = a.d_of[li];
+  return reinterpret_cast<_Float16*>(a.ws + a.q_off[li]) + (int64_t)b * a.Hp * (d + kRope);
+}
+
 // One workgroup per (layer, head).  The queries of 16 sequences are staged once in
 // LDS and split into bf16 hi + lo B operands (K = nope); wave w then runs the
 // 16-channel tiles w, w + 4, ... of the latent: A = rows of W_UK[h]^T (latent
-// channel x nope, contiguous in the latent-major layout).
+// channel x nope, contiguous in the latent-major layout), up to the widest kept width
+// of the 16 (per-sequence plans: each sequence keeps the channels below its own).
 __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
   constexpr int PQ = 256 + 8;  // LDS row pitch of the queries (floats)
   __shared__ float qs[16 * PQ];
+  if (!mla_list_ok(a.list_hdr, a.list_hash)) return;  // not this call's list
   const int li = blockIdx.x, h = blockIdx.y;
-  const int d = a.d_of[li], W = d + kRope;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
   const int qw = a.nope + kRope;
   const int nks = a.nope / 32;
-  _Float16* qa = reinterpret_cast<_Float16*>(a.ws + a.q_off[li]);
   if (h >= a.Hq) {  // a padding head: zero query (finite scores, never written out)
-    for (int e = tid; e < a.B * W; e += 256) {
-      const int b = e / W, c = e - b * W;
-      qa[((int64_t)b * a.Hp + h) * W + c] = (_Float16)0.0f;
+    for (int b = 0; b < a.B; ++b) {
+      int d;
+      _Float16* qa = absorb_dst(a, li, b, d);
+      for (int c = tid; c < d + kRope; c += 256) qa[(int64_t)h * (d + kRope) + c] = (_Float16)0.0f;
     }
     return;
   }
-  for (int e = tid; e < a.B * kRope; e += 256) {
-    const int b = e / kRope, j = e - b * kRope;
-    const float x = load_in(a.q, a.q_f32, li * a.q_lstride + ((int64_t)b * a.Hq + h) * qw + a.nope + j);
-    qa[((int64_t)b * a.Hp + h) * W + d + j] = (_Float16)(x * a.scale_log2);
+  for (int b = 0; b < a.B; ++b) {
+    int d;
+    _Float16* qa = absorb_dst(a, li, b, d);
+    if (tid < kRope) {
+      const float x = load_in(a.q, a.q_f32, li * a.q_lstride + ((int64_t)b * a.Hq + h) * qw + a.nope + tid);
+      qa[(int64_t)h * (d + kRope) + d + tid] = (_Float16)(x * a.scale_log2);
+    }
   }
   const uint16_t* wt = a.w_ukt + ((int64_t)li * a.Hq + h) * a.r * a.nope;
   for (int b0 = 0; b0 < a.B; b0 += 16) {
+    int d = 0;  // the widest kept width of the 16 sequences
+    for (int bi = 0; bi < 16 && b0 + bi < a.B; ++bi) {
+      int db;
+      absorb_dst(a, li, b0 + bi, db);
+      d = db > d ? db : d;
+    }
     __syncthreads();
     for (int e = tid; e < 16 * a.nope; e += 256) {
       const int bi = e / a.nope, i = e - bi * a.nope;
@@ -679,9 +726,13 @@ __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
         }
       }
       if (bq < a.B) {  // D[chan c + 4g + e][seq i16]
-        _Float16* dst = qa + ((int64_t)bq * a.Hp + h) * W + c + 4 * g;
+        int db;
+        _Float16* qa = absorb_dst(a, li, bq, db);
+        if (c < db) {  // kept widths are multiples of 32: the tile is wholly in or out
+          _Float16* dst = qa + (int64_t)h * (db + kRope) + c + 4 * g;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) dst[e] = (_Float16)(acc[e] * a.scale_log2);
+          for (int e = 0; e < 4; ++e) dst[e] = (_Float16)(acc[e] * a.scale_log2);
+        }
       }
     }
   }
@@ -703,16 +754,26 @@ struct MlaItem {
   int32_t bits;
   int32_t nreaders;     // reader layers (consecutive)
   int32_t nhc;          // 32-head chunks per layer
-  int32_t units;        // splits per stream
+  int32_t units;        // splits per stream the item's workgroups are laid out for
   int32_t units_cap;    // partial records per stream
   int32_t split_blocks;
   int32_t wg_begin;
+  int32_t nseq;         // sequences (streams) of the item
+  // Per-sequence items (written once, before the stored length is known): the split
+  // rule (mla_split_len), from which the kernel takes the split length and the
+  // splits of the call; split_nr = 0: split_blocks and units hold them.
+  int32_t split_target, split_nr;
+  int32_t reserved;     // (zero: the struct has no padding, and lists hash byte for byte)
 };
+static_assert(sizeof(MlaItem) == 96, "MlaItem without padding");
 
 struct MlaDecodeArgs {
   const uint8_t* arena;
   uint8_t* ws;
   MlaItem items[kMaxItems];
+  const MlaItem* items_dev;  // per-sequence tables: the items in the workspace (else NULL)
+  const uint64_t* list_hdr;  // ... and the list's header, with the hash it must carry
+  uint64_t list_hash;
   int32_t n_items;
   int32_t n_wg;
   int32_t B, Hq;         // Hq: the padded head count (whole 32-head chunks)
@@ -720,6 +781,8 @@ struct MlaDecodeArgs {
   int32_t ntail;        // tail tokens
   int32_t nb_cap;
 };
+static_assert(sizeof(MlaDecodeArgs) <= 4096, "kernel arguments");
+
 
 constexpr int kWaves = 4;  // waves per D2 workgroup (two workgroups share a CU)
 
@@ -1021,16 +1084,17 @@ __device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, LDS& L, int nvalid
   }
 }
 
+// sb, units: the split length and the splits of the stream in this call.
 template <int D, int BITS, bool KIVI, int POL, class LDS>
 __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& it, int rl, int hc,
-                                        int b, int u, LDS& L) {
+                                        int b, int u, int sb, int units, LDS& L) {
   using G = Geo<D>;
   constexpr int NR = kvk::mla_ring_depth(G::W, BITS, KIVI ? 1 : 0);
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, i16 = lane & 15;
   const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int tt = wv / G::KS, kh = wv % G::KS;
-  const int k0 = u * it.split_blocks;
-  const int k1 = min(a.nbf, k0 + it.split_blocks);
+  const int k0 = u * sb;
+  const int k1 = min(a.nbf, k0 + sb);
   const int bb = it.block_bytes;
   const uint8_t* stream = a.arena + it.region + (int64_t)b * it.stream_bytes;
   const Rsrc rs = buffer_rsrc(stream, k1 > 0 ? k1 * bb : 0);  // loads past block k1-1 read zeros
@@ -1087,7 +1151,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
       if (nvalid > 0) mla_phase_bc<D>(st, L, nvalid, tid);
     }
   }
-  if (u == it.units - 1 && a.ntail > 0) {  // the bf16 tail block as one more iteration
+  if (u == units - 1 && a.ntail > 0) {  // the bf16 tail block as one more iteration
     MlaRaw<D, 16, false> tr;
     const Rsrc rt = buffer_rsrc(stream + (int64_t)a.nb_cap * bb, tblk == 0 ? 64 * G::W : 0);
     mla_issue<D, 16, false, POL>(tr, rt, 0, trow, g, kh);
@@ -1119,29 +1183,60 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
   }
 }
 
-// The item, reader row, head chunk, sequence and split of workgroup wg; false for
-// the padding workgroups of an item.  Workgroups of one (sequence, split) for the
-// different readers and head chunks sit 8 apart, so that they run on one XCD at
-// about the same time and share the stream through its L2.
+// The items of a launch: in the kernel arguments, or (DEV, per-sequence tables) in
+// the workspace, read there through the constant address space (nothing writes
+// them during the launch), so that the wave-uniform loads go to scalar registers.
+// (The host pass of this file parses these functions but never runs them.)
+#if defined(__HIP_DEVICE_COMPILE__)
+typedef const __attribute__((address_space(4))) MlaItem ConstMlaItem;
+#else
+typedef const MlaItem ConstMlaItem;
+#endif
+
+template <bool DEV>
+__device__ __forceinline__ int mla_item_wg_begin(const MlaDecodeArgs& a, int i) {
+  if constexpr (DEV) return ((ConstMlaItem*)a.items_dev)[i].wg_begin;
+  else return a.items[i].wg_begin;
+}
+
+__device__ __forceinline__ MlaItem mla_item_dev(const MlaDecodeArgs& a, int i) {
+  return ((ConstMlaItem*)a.items_dev)[i];
+}
+
+// The item, reader row, head chunk, sequence, split, split length and splits of
+// the stream for workgroup wg; false for the padding workgroups of an item (and for
+// splits past the stored blocks of a per-sequence item, whose workgroups are laid
+// out for the capacity).  Workgroups of one (sequence, split) for the different
+// readers and head chunks sit 8 apart, so that they run on one XCD at about the
+// same time and share the stream through its L2.
+template <bool DEV>
 __device__ __forceinline__ bool mla_locate(const MlaDecodeArgs& a, int wg, int& item, int& rl, int& hc, int& b,
-                                           int& u) {
+                                           int& u, int& sb, int& units) {
   if (wg >= a.n_wg) return false;
   int lo = 0, hi = a.n_items - 1;  // last item with wg_begin <= wg
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (a.items[mid].wg_begin <= wg) lo = mid;
+    if (mla_item_wg_begin<DEV>(a, mid) <= wg) lo = mid;
     else hi = mid - 1;
   }
-  const MlaItem& it = a.items[lo];
+  const MlaItem& it = DEV ? mla_item_dev(a, lo) : a.items[lo];
   const int R = it.nreaders * it.nhc;
   const int local = wg - it.wg_begin;
   const int grp = local / (8 * R), rem = local - grp * 8 * R;
   const int row = rem >> 3;
   const int unit = 8 * grp + (rem & 7);
-  if (unit >= a.B * it.units) return false;
-  item = lo;
+  if (unit >= it.nseq * it.units) return false;
   b = unit / it.units;
   u = unit - b * it.units;
+  if (it.split_nr > 0) {
+    sb = kvk::mla_split_len(it.split_target, it.split_nr, a.nbf);
+    units = kvk::mla_units_len(a.nbf, 32 * a.nbf + a.ntail, sb);
+  } else {
+    sb = it.split_blocks;
+    units = it.units;
+  }
+  if (u >= units) return false;
+  item = lo;
   rl = row / it.nhc;
   hc = row - rl * it.nhc;
   return true;
@@ -1150,36 +1245,51 @@ __device__ __forceinline__ bool mla_locate(const MlaDecodeArgs& a, int wg, int& 
 // POL: the loads' cache policy for every item of the launch (see mla_issue); the host
 // launches single-reader and multi-reader items separately.  Kept widths up to 512:
 // two workgroups per CU.
-template <bool KIVI, int POL>
+template <bool KIVI, int POL, bool DEV>
 __global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(MlaDecodeArgs a) {
   __shared__ MlaLds<kTileHalfs, 0> L;
-  int item, rl, hc, b, u;
-  if (!mla_locate(a, blockIdx.x, item, rl, hc, b, u)) return;
-  const MlaItem& it = a.items[item];
-#define KVK_MLA_CASE(DD, BB)                            \
-  if (it.d == DD && it.bits == BB) {                    \
-    run_mla<DD, BB, KIVI, POL>(a, it, rl, hc, b, u, L); \
-    return;                                             \
+  if (!mla_list_ok(a.list_hdr, a.list_hash)) return;  // not this call's list
+  int item, rl, hc, b, u, sb, units;
+  if (!mla_locate<DEV>(a, blockIdx.x, item, rl, hc, b, u, sb, units)) return;
+#define KVK_MLA_CASE(DD, BB)                                        \
+  if (it.d == DD && it.bits == BB) {                                \
+    run_mla<DD, BB, KIVI, POL>(a, it, rl, hc, b, u, sb, units, L); \
+    return;                                                         \
   }
 #define KVK_MLA_D(DD) KVK_MLA_CASE(DD, 16) KVK_MLA_CASE(DD, 8) KVK_MLA_CASE(DD, 4) KVK_MLA_CASE(DD, 2)
-  KVK_MLA_D(512)
-  KVK_MLA_D(256)
-  KVK_MLA_D(128)
-  KVK_MLA_D(64)
+#define KVK_MLA_NARROW \
+  KVK_MLA_D(512)       \
+  KVK_MLA_D(256)       \
+  KVK_MLA_D(128)       \
+  KVK_MLA_D(64)        \
   KVK_MLA_D(32)
+  if constexpr (DEV) {
+    const MlaItem it = mla_item_dev(a, item);
+    KVK_MLA_NARROW
+  } else {
+    const MlaItem& it = a.items[item];
+    KVK_MLA_NARROW
+  }
+#undef KVK_MLA_NARROW
 }
 
 // Kept width 1024 (1088 stored channels): the product accumulators take 128
 // registers and the iteration's tile 70 KiB of LDS, so one workgroup per CU; the
 // absorbed query (136 registers per lane if held there) is read from a 70 KiB LDS
 // copy instead.
-template <bool KIVI, int POL>
+template <bool KIVI, int POL, bool DEV>
 __global__ __launch_bounds__(64 * kWaves, 1) void mla_decode_wide_kernel(MlaDecodeArgs a) {
   __shared__ MlaLds<kWideTileHalfs, 32 * kWideQP> L;
-  int item, rl, hc, b, u;
-  if (!mla_locate(a, blockIdx.x, item, rl, hc, b, u)) return;
-  const MlaItem& it = a.items[item];
-  KVK_MLA_D(1024)
+  if (!mla_list_ok(a.list_hdr, a.list_hash)) return;  // not this call's list
+  int item, rl, hc, b, u, sb, units;
+  if (!mla_locate<DEV>(a, blockIdx.x, item, rl, hc, b, u, sb, units)) return;
+  if constexpr (DEV) {
+    const MlaItem it = mla_item_dev(a, item);
+    KVK_MLA_D(1024)
+  } else {
+    const MlaItem& it = a.items[item];
+    KVK_MLA_D(1024)
+  }
 #undef KVK_MLA_D
 #undef KVK_MLA_CASE
 }
@@ -1196,13 +1306,36 @@ struct MlaCombineArgs {
   int32_t d_of[KVK_MAX_LAYERS];
   int32_t units[KVK_MAX_LAYERS];
   int32_t units_cap[KVK_MAX_LAYERS];
+  const MlaSeqRow* rows;  // per-sequence tables: per (relative layer, sequence) (else NULL)
+  const uint64_t* list_hdr;
+  uint64_t list_hash;
+  int32_t nbf, n_stored;  // per-sequence tables: the splits follow from these
   int32_t B, Hq, Hp, v, r;  // Hp: heads per split partial record (padded)
   int64_t out_lstride;       // elements between consecutive layers' outputs
 };
 
+// Sequence b's split partials of relative layer li (fp32 records of Hp (d + 2)), with
+// its kept width d, splits U and partial records per sequence UC.
+__device__ __forceinline__ const float* combine_src(const MlaCombineArgs& a, int li, int b, int& d, int& U,
+                                                    int& UC) {
+  if (a.rows) {
+    const MlaSeqRow& rw = a.rows[(int64_t)li * a.B + b];
+    d = rw.d;
+    UC = rw.units_cap;
+    U = kvk::mla_units_len(a.nbf, a.n_stored, kvk::mla_split_len(rw.split_target, rw.split_nr, a.nbf));
+    return reinterpret_cast<const float*>(a.ws + rw.part_off);
+  }
+  d = a.d_of[li];
+  U = a.units[li];
+  UC = a.units_cap[li];
+  return reinterpret_cast<const float*>(a.ws + a.part_off[li]) + (int64_t)b * UC * a.Hp * (d + 2);
+}
+
 // One workgroup per (layer, head): for 16 sequences at a time, merge the split
 // partials by log-sum-exp into o_lat (LDS, bf16 hi + lo), then multiply by
-// W_UV[h] on the matrix cores (M = value channels, K = d, N = sequences).
+// W_UV[h] on the matrix cores (M = value channels, K = d, N = sequences).  Under
+// per-sequence plans K is the widest kept width of the 16, each sequence's o_lat
+// zero past its own (the products past it add exact zeros).
 template <int DMAX>
 __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
   constexpr int PO = DMAX + 8;  // LDS row pitch (bf16)
@@ -1210,18 +1343,30 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
   __shared__ uint16_t oh[16 * PO], ol[16 * PO];
   __shared__ float wgt[16 * kMaxU];
   const int li = blockIdx.x, h = blockIdx.y;
-  const int d = a.d_of[li], U = a.units[li], UC = a.units_cap[li];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
-  const float* part = reinterpret_cast<const float*>(a.ws + a.part_off[li]);
-  const int64_t rec = (int64_t)a.Hp * (d + 2);
+  if (!mla_list_ok(a.list_hdr, a.list_hash)) {  // not this call's list: NaN outputs
+    for (int e = tid; e < a.B * a.v; e += 256) {
+      const int b = e / a.v, j = e - b * a.v;
+      a.out[li * a.out_lstride + ((int64_t)b * a.Hq + h) * a.v + j] = __builtin_nanf("");
+    }
+    return;
+  }
   const uint16_t* wv_h = a.w_uv + ((int64_t)li * a.Hq + h) * a.v * a.r;
   for (int b0 = 0; b0 < a.B; b0 += 16) {
     const int nb = min(16, a.B - b0);
+    int d = 0;  // the widest kept width of the 16 sequences
+    for (int bi = 0; bi < nb; ++bi) {
+      int db, U, UC;
+      combine_src(a, li, b0 + bi, db, U, UC);
+      d = db > d ? db : d;
+    }
     __syncthreads();
     // split weights w_u = 2^(m_u - m*) / sum_u 2^(m_u - m*) l_u, one sequence per 16 threads
     {
       const int bi = tid >> 4, p = tid & 15;
-      const float* p0 = part + (int64_t)(b0 + bi) * UC * rec;
+      int db = 0, U = 0, UC = 0;
+      const float* p0 = bi < nb ? combine_src(a, li, b0 + bi, db, U, UC) : nullptr;
+      const int64_t rec = (int64_t)a.Hp * (db + 2);
       float m = -INFINITY;
       if (bi < nb)
         for (int u = p; u < U; u += 16) m = fmaxf(m, p0[u * rec + h]);
@@ -1239,9 +1384,14 @@ __global__ __launch_bounds__(256) void mla_combine_kernel(MlaCombineArgs a) {
       const int bi = e / (d / 4), c = 4 * (e - bi * (d / 4));
       f4 x = {0.f, 0.f, 0.f, 0.f};
       if (bi < nb) {
-        const float* o0 = part + (int64_t)(b0 + bi) * UC * rec + 2 * a.Hp + (int64_t)h * d + c;
+        int db, U, UC;
+        const float* p0 = combine_src(a, li, b0 + bi, db, U, UC);
+        const int64_t rec = (int64_t)a.Hp * (db + 2);
+        if (c < db) {
+          const float* o0 = p0 + 2 * a.Hp + (int64_t)h * db + c;
 #pragma unroll 4
-        for (int u = 0; u < U; ++u) x += wgt[bi * kMaxU + u] * *reinterpret_cast<const f4*>(o0 + u * rec);
+          for (int u = 0; u < U; ++u) x += wgt[bi * kMaxU + u] * *reinterpret_cast<const f4*>(o0 + u * rec);
+        }
       }
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
@@ -1438,6 +1588,30 @@ kvk_status mla_debug_dequantize(const kvk_table* t, int32_t layer, int32_t n_sto
   return KVK_OK;
 }
 
+// D2 launch class k: bit 0 the cached load policy (items whose stream several
+// workgroups read), bit 1 the width-1024 kernel; a.n_wg workgroups.
+kvk_status launch_mla_d2(const MlaDecodeArgs& a, int k, bool kivi, hipStream_t stream) {
+  const dim3 grid((unsigned)a.n_wg), blk(64 * kWaves);
+  const bool dev = a.items_dev != nullptr;
+#define KVK_D2(KERNEL, KV, PO)                                                                          \
+  if (dev) hipLaunchKernelGGL((KERNEL<KV, PO, true>), grid, blk, 0, stream, a);                        \
+  else hipLaunchKernelGGL((KERNEL<KV, PO, false>), grid, blk, 0, stream, a);
+  switch (k + 4 * (kivi ? 1 : 0)) {
+    case 0: KVK_D2(mla_decode_kernel, false, kStreamPolicy) break;
+    case 1: KVK_D2(mla_decode_kernel, false, 0) break;
+    case 2: KVK_D2(mla_decode_wide_kernel, false, kStreamPolicy) break;
+    case 3: KVK_D2(mla_decode_wide_kernel, false, 0) break;
+    case 4: KVK_D2(mla_decode_kernel, true, kStreamPolicy) break;
+    case 5: KVK_D2(mla_decode_kernel, true, 0) break;
+    case 6: KVK_D2(mla_decode_wide_kernel, true, kStreamPolicy) break;
+    default: KVK_D2(mla_decode_wide_kernel, true, 0) break;
+  }
+#undef KVK_D2
+  const hipError_t err = hipGetLastError();
+  if (err != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA decode launch: %s", hipGetErrorString(err));
+  return KVK_OK;
+}
+
 kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
                              int32_t n_stored, float scale, const void* w_uk, const void* arena,
                              void* workspace, hipStream_t stream, int64_t q_lstride) {
@@ -1463,6 +1637,9 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     aa.q_off[l - l0] = ws.q_off[l];
     aa.d_of[l - l0] = t->rank[t->info.anchor_of[l]];
   }
+  aa.rows = nullptr;
+  aa.list_hdr = nullptr;
+  aa.list_hash = 0;
   hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)(l1 - l0), (unsigned)aa.Hp), dim3(256), 0,
                      stream, aa);
   hipError_t e = hipGetLastError();
@@ -1484,6 +1661,9 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
   for (MlaDecodeArgs& a : args) {
     a.arena = static_cast<const uint8_t*>(arena);
     a.ws = wsb;
+    a.items_dev = nullptr;
+    a.list_hdr = nullptr;
+    a.list_hash = 0;
     a.B = d.batch;
     a.Hq = mla_heads_padded(d.n_q_heads);
     a.nbf = nbf;
@@ -1497,23 +1677,10 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     if (a.n_items == 0) return KVK_OK;
     if (wgs > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "too many MLA decode workgroups");
     a.n_wg = (int32_t)wgs;
-    const dim3 grid((unsigned)wgs), blk(64 * kWaves);
-    const bool kivi = d.qscheme == KVK_Q_KIVI32;
-    switch (k + 4 * (kivi ? 1 : 0)) {
-      case 0: hipLaunchKernelGGL((mla_decode_kernel<false, kStreamPolicy>), grid, blk, 0, stream, a); break;
-      case 1: hipLaunchKernelGGL((mla_decode_kernel<false, 0>), grid, blk, 0, stream, a); break;
-      case 2: hipLaunchKernelGGL((mla_decode_wide_kernel<false, kStreamPolicy>), grid, blk, 0, stream, a); break;
-      case 3: hipLaunchKernelGGL((mla_decode_wide_kernel<false, 0>), grid, blk, 0, stream, a); break;
-      case 4: hipLaunchKernelGGL((mla_decode_kernel<true, kStreamPolicy>), grid, blk, 0, stream, a); break;
-      case 5: hipLaunchKernelGGL((mla_decode_kernel<true, 0>), grid, blk, 0, stream, a); break;
-      case 6: hipLaunchKernelGGL((mla_decode_wide_kernel<true, kStreamPolicy>), grid, blk, 0, stream, a); break;
-      default: hipLaunchKernelGGL((mla_decode_wide_kernel<true, 0>), grid, blk, 0, stream, a); break;
-    }
-    const hipError_t err = hipGetLastError();
-    if (err != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA decode launch: %s", hipGetErrorString(err));
+    const kvk_status st = launch_mla_d2(a, k, d.qscheme == KVK_Q_KIVI32, stream);
     a.n_items = 0;
     wgs = 0;
-    return KVK_OK;
+    return st;
   };
   const int nhc = mla_heads_padded(d.n_q_heads) / 32;
   for (int l = l0; l < l1;) {
@@ -1542,6 +1709,10 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     it.units = mla_units(t, anc, n_stored);
     it.units_cap = ws.units_cap[l];
     it.wg_begin = (int32_t)wgs;
+    it.nseq = d.batch;
+    it.split_target = 0;
+    it.split_nr = 0;
+    it.reserved = 0;
     const int64_t units = (int64_t)d.batch * it.units;
     wgs += (units + 7) / 8 * 8 * it.nreaders * nhc;
     l = re;
@@ -1570,6 +1741,9 @@ kvk_status mla_absorb_rows(const kvk_table* t, const void* q, int32_t rows, cons
   aa.scale_log2 = scale * kLog2e;
   aa.q_off[0] = 0;
   aa.d_of[0] = d.latent_dim;  // the full width
+  aa.rows = nullptr;
+  aa.list_hdr = nullptr;
+  aa.list_hash = 0;
   hipLaunchKernelGGL(mla_absorb_kernel, dim3(1u, (unsigned)aa.Hp), dim3(256), 0, stream, aa);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA absorb launch: %s", hipGetErrorString(e));
@@ -1591,6 +1765,11 @@ kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t 
   c.out_lstride = out_lstride > 0 ? out_lstride : (int64_t)d.batch * d.n_q_heads * d.v_dim;
   c.v = d.v_dim;
   c.r = d.latent_dim;
+  c.rows = nullptr;
+  c.list_hdr = nullptr;
+  c.list_hash = 0;
+  c.nbf = 0;
+  c.n_stored = 0;
   int dmax = 0;
   for (int l = l0; l < l1; ++l) {
     const int anc = t->info.anchor_of[l];
@@ -1605,6 +1784,218 @@ kvk_status mla_decode_merge(const kvk_table* t, int32_t l0, int32_t l1, int32_t 
   else hipLaunchKernelGGL(mla_combine_kernel<512>, grid, dim3(256), 0, stream, c);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA combine launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Per-sequence plans (§2.3, eq. (3) with the rank axis): one launch per phase for the
+// whole batch.  The work list (a row per (layer, sequence), an item per (sequence,
+// anchor) in each D2 launch class) is written once per workspace and layer range by
+// kvk_decode_setup; every decode call rebuilds it on the host only to check that the
+// workspace holds it (its hash) and to size the launches.  The splits follow from
+// the stored length in the kernels (each row and item carries its anchor's split
+// rule), so the list does not depend on it.  Sequence b's absorbed queries and
+// partials sit in its own part of the workspace, laid out as its one-sequence table
+// lays them out, the parts one after the other after the list.
+// ---------------------------------------------------------------------------
+
+MlaSeqList::MlaSeqList() = default;
+MlaSeqList::~MlaSeqList() = default;
+
+kvk_status mla_seq_list(const kvk_table* t, int32_t l0, int32_t l1, MlaSeqList& L, bool image) {
+  const kvk_dims& d = t->d;
+  const int32_t nl = l1 - l0, B = d.batch;
+  const int nhc = mla_heads_padded(d.n_q_heads) / 32;
+  // items per launch class
+  int32_t n_k[4] = {0, 0, 0, 0};
+  for (int b = 0; b < B; ++b) {
+    const kvk_table* s = t->seq[b];
+    for (int l = l0; l < l1;) {
+      const int anc = s->info.anchor_of[l];
+      const int re = s->next_anchor[anc] < l1 ? s->next_anchor[anc] : l1;
+      ++n_k[((re - l) * nhc > 1 ? 1 : 0) + (s->rank[anc] > 512 ? 2 : 0)];
+      l = re;
+    }
+  }
+  int64_t off = 256;
+  L.rows_off = off;
+  off += round256((int64_t)nl * B * (int64_t)sizeof(MlaSeqRow));
+  for (int k = 0; k < 4; ++k) {
+    L.items_off[k] = off;
+    L.n_items[k] = n_k[k];
+    L.n_wg[k] = 0;
+    off += round256((int64_t)n_k[k] * (int64_t)sizeof(MlaItem));
+  }
+  L.bytes = off;
+  L.dmax = 0;
+  if (!image) return KVK_OK;
+  L.img.assign((size_t)L.bytes, 0);
+  MlaSeqRow* rows = reinterpret_cast<MlaSeqRow*>(L.img.data() + L.rows_off);
+  std::vector<MlaItem> items[4];
+  int64_t base = L.bytes;  // sequence b's part of the workspace
+  for (int b = 0; b < B; ++b) {
+    const kvk_table* s = t->seq[b];
+    MlaWorkspace w;
+    mla_workspace(s, l0, l1, &w);
+    for (int l = l0; l < l1; ++l) {
+      const int anc = s->info.anchor_of[l];
+      MlaSeqRow& r = rows[(int64_t)(l - l0) * B + b];
+      r.q_off = base + w.q_off[l];
+      r.part_off = base + w.part_off[l];
+      r.d = s->rank[anc];
+      r.units_cap = w.units_cap[l];
+      mla_split_rule(s, anc, &r.split_target, &r.split_nr);
+      L.dmax = r.d > L.dmax ? r.d : L.dmax;
+    }
+    for (int l = l0; l < l1;) {
+      const int anc = s->info.anchor_of[l];
+      const int re = s->next_anchor[anc] < l1 ? s->next_anchor[anc] : l1;  // readers [l, re)
+      const int k = ((re - l) * nhc > 1 ? 1 : 0) + (s->rank[anc] > 512 ? 2 : 0);
+      MlaItem it;
+      std::memset(&it, 0, sizeof(it));  // the list is hashed byte for byte: padding too
+      it.region = t->seq_base[b] + s->info.layer_offset[anc];
+      it.q_off0 = base + w.q_off[l];
+      it.q_stride = re - l > 1 ? w.q_off[l + 1] - w.q_off[l] : 0;
+      it.part_off0 = base + w.part_off[l];
+      it.part_stride = re - l > 1 ? w.part_off[l + 1] - w.part_off[l] : 0;
+      it.stream_bytes = (int32_t)s->info.stream_bytes[anc];
+      it.block_bytes = (int32_t)s->block_bytes[anc];
+      it.d = s->rank[anc];
+      it.bits = s->bits[anc];
+      it.nreaders = re - l;
+      it.nhc = nhc;
+      it.units = w.units_cap[l];  // workgroups laid out for the capacity
+      it.units_cap = w.units_cap[l];
+      it.split_blocks = 0;
+      it.wg_begin = 0;
+      it.nseq = 1;
+      mla_split_rule(s, anc, &it.split_target, &it.split_nr);
+      items[k].push_back(it);
+      l = re;
+    }
+    base += w.total;
+  }
+  // Launch order: the items of one (kept width, bit-width) together, so that the
+  // workgroups sharing a CU mostly run the same specialisation of the kernel (each is
+  // large; a CU that alternates between them keeps reloading instructions).
+  // Workgroup ids go round the 8 XCDs.  An item one workgroup row reads takes its
+  // units' workgroups back to back.  An item several rows (readers, head chunks) read
+  // keeps the 8-unit groups whose rows sit 8 apart (one XCD per unit); a
+  // one-sequence item has fewer than 8 units, so its first workgroup is moved on (by
+  // workgroups that exit at once) to the XCD after the previous item's last unit,
+  // instead of every such item starting on the same XCD.
+  for (int k = 0; k < 4; ++k) {
+    std::stable_sort(items[k].begin(), items[k].end(), [](const MlaItem& x, const MlaItem& y) {
+      return x.d != y.d ? x.d > y.d : x.bits > y.bits;
+    });
+    MlaItem* dst = reinterpret_cast<MlaItem*>(L.img.data() + L.items_off[k]);
+    int64_t placed = 0;  // units placed so far
+    for (size_t i = 0; i < items[k].size(); ++i) {
+      MlaItem& it = items[k][i];
+      const int64_t R = (int64_t)it.nreaders * nhc;
+      if (R == 1) {
+        it.wg_begin = (int32_t)L.n_wg[k];
+        L.n_wg[k] += it.units;
+      } else {
+        L.n_wg[k] += ((placed - L.n_wg[k]) % 8 + 8) % 8;
+        it.wg_begin = (int32_t)L.n_wg[k];
+        L.n_wg[k] += (int64_t)(it.units + 7) / 8 * 8 * R;
+      }
+      placed += it.units;
+      std::memcpy(dst + i, &it, sizeof(MlaItem));
+    }
+  }
+  for (int k = 0; k < 4; ++k)
+    if (L.n_wg[k] > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "too many MLA decode workgroups");
+  L.hash = fnv1a64(L.img.data() + 256, L.img.size() - 256);
+  uint64_t* hdr = reinterpret_cast<uint64_t*>(L.img.data());
+  hdr[0] = kMlaListMagic;
+  hdr[1] = L.hash;
+  return KVK_OK;
+}
+
+kvk_status mla_decode_batched(const kvk_table* t, int32_t l0, int32_t l1, const void* q, int32_t q_dtype,
+                              int32_t n_stored, float scale, const void* w_uk, const void* w_uv,
+                              const void* arena, float* out, void* workspace, hipStream_t stream, bool splits,
+                              bool merge) {
+  const kvk_dims& d = t->d;
+  MlaSeqList L;
+  if (kvk_status st = mla_seq_list(t, l0, l1, L, true)) return st;
+  {
+    bool ready = false;
+    std::lock_guard<std::mutex> lock(t->setup_mu);
+    for (const kvk_table::DecodeSetup& su : t->setups)
+      ready |= su.workspace == workspace && su.l0 == l0 && su.l1 == l1 && su.hash == L.hash;
+    if (!ready)
+      return fail(KVK_ERR_INVALID,
+                  "per-sequence plans: call kvk_decode_setup for layers [%d, %d) on this workspace first", l0, l1);
+  }
+  uint8_t* wsb = static_cast<uint8_t*>(workspace);
+  const uint64_t* hdr = reinterpret_cast<const uint64_t*>(wsb);
+  const int32_t nl = l1 - l0, nbf = n_stored / KVK_GROUP, ntail = n_stored % KVK_GROUP;
+  const int32_t Hp = mla_heads_padded(d.n_q_heads);
+  const int64_t qw = d.nope_dim + d.rope_dim;
+  if (splits) {
+    MlaAbsorbArgs aa;
+    aa.q = q;
+    aa.w_ukt = static_cast<const uint16_t*>(w_uk);
+    aa.ws = wsb;
+    aa.rows = reinterpret_cast<const MlaSeqRow*>(wsb + L.rows_off);
+    aa.list_hdr = hdr;
+    aa.list_hash = L.hash;
+    aa.q_f32 = q_dtype == KVK_F32;
+    aa.B = d.batch;
+    aa.Hq = d.n_q_heads;
+    aa.Hp = Hp;
+    aa.nope = d.nope_dim;
+    aa.r = d.latent_dim;
+    aa.q_lstride = (int64_t)d.batch * d.n_q_heads * qw;
+    aa.scale_log2 = scale * kLog2e;
+    hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)nl, (unsigned)Hp), dim3(256), 0, stream, aa);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA absorb launch: %s", hipGetErrorString(e));
+    if (n_stored > 0) {  // none stored: the merge needs no partials
+      for (int k = 0; k < 4; ++k) {
+        if (L.n_items[k] == 0) continue;
+        MlaDecodeArgs a;
+        a.arena = static_cast<const uint8_t*>(arena);
+        a.ws = wsb;
+        a.items_dev = reinterpret_cast<const MlaItem*>(wsb + L.items_off[k]);
+        a.list_hdr = hdr;
+        a.list_hash = L.hash;
+        a.n_items = L.n_items[k];
+        a.n_wg = (int32_t)L.n_wg[k];
+        a.B = d.batch;
+        a.Hq = Hp;
+        a.nbf = nbf;
+        a.ntail = ntail;
+        a.nb_cap = t->nb_cap;
+        if (kvk_status st = launch_mla_d2(a, k, d.qscheme == KVK_Q_KIVI32, stream)) return st;
+      }
+    }
+  }
+  if (merge) {
+    MlaCombineArgs c;
+    c.ws = wsb;
+    c.w_uv = static_cast<const uint16_t*>(w_uv);
+    c.out = out;
+    c.rows = reinterpret_cast<const MlaSeqRow*>(wsb + L.rows_off);
+    c.list_hdr = hdr;
+    c.list_hash = L.hash;
+    c.nbf = nbf;
+    c.n_stored = n_stored;
+    c.B = d.batch;
+    c.Hq = d.n_q_heads;
+    c.Hp = Hp;
+    c.v = d.v_dim;
+    c.r = d.latent_dim;
+    c.out_lstride = (int64_t)d.batch * d.n_q_heads * d.v_dim;
+    const dim3 grid((unsigned)nl, (unsigned)d.n_q_heads);
+    if (L.dmax > 512) hipLaunchKernelGGL(mla_combine_kernel<1024>, grid, dim3(256), 0, stream, c);
+    else hipLaunchKernelGGL(mla_combine_kernel<512>, grid, dim3(256), 0, stream, c);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA combine launch: %s", hipGetErrorString(e));
+  }
   return KVK_OK;
 }
 

@@ -83,7 +83,7 @@ int64_t gqa_split_target(const kvk_table* t, int32_t l0, int32_t l1) {
 }
 
 int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_t n_blocks, int64_t target_bytes,
-                         int32_t waves) {
+                         int32_t waves, int32_t* count_bound) {
   // target_bytes of cache per wave (gqa_split_target); the stream's blocks are
   // divided evenly so that no split is a short remainder, in a multiple of the
   // decode kernel's prefetch depth so that only a stream's last split runs past
@@ -110,11 +110,15 @@ int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_
   const int64_t nsplit = (nb + target - 1) / target;
   int64_t per = (nb + nsplit - 1) / nsplit;
   per = (per + nr - 1) / nr * nr;
+  // The split count ceil(nb / per) is at most nsplit, which grows with nb (the count
+  // itself need not: rounding per up can save a split), so nsplit bounds the count of
+  // every length up to n_blocks.
+  if (count_bound) *count_bound = (int32_t)nsplit;
   return (int32_t)per;
 }
 
 int32_t gqa_item_split_blocks(const kvk_table* s, int32_t anchor, int32_t l0, int32_t l1, int32_t n_blocks,
-                              int64_t target_bytes) {
+                              int64_t target_bytes, int32_t* count_bound) {
   const int32_t G = s->d.n_q_heads / s->d.n_kv_heads;
   const int32_t rb = anchor > l0 ? anchor : l0;
   const int32_t re = s->next_anchor[anchor] < l1 ? s->next_anchor[anchor] : l1;
@@ -125,7 +129,8 @@ int32_t gqa_item_split_blocks(const kvk_table* s, int32_t anchor, int32_t l0, in
   // cache bytes with per-wave splits, 1.19x with 4x longer ones, 1.41x with 8x, 1.69x
   // with 16x).
   const int32_t w = gqa_chunk_waves(nch);
-  return split_blocks_for(s->bits[anchor], s->d.qscheme, s->d.head_dim, n_blocks, target_bytes, w < 4 ? w : 4);
+  return split_blocks_for(s->bits[anchor], s->d.qscheme, s->d.head_dim, n_blocks, target_bytes, w < 4 ? w : 4,
+                          count_bound);
 }
 
 int64_t mla_block_bytes(int32_t W, int32_t bits, int32_t qscheme) {
@@ -134,7 +139,7 @@ int64_t mla_block_bytes(int32_t W, int32_t bits, int32_t qscheme) {
   return 4LL * W * bits + 128;                              // codes + two bf16 scales / token
 }
 
-int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_blocks) {
+void mla_split_rule(const kvk_table* t, int32_t anchor, int32_t* target_out, int32_t* nr_out) {
   // A workgroup's time per block grows with the stored width W (scores over W
   // channels, the latent product over d) on top of a fixed part (softmax,
   // barriers): about W + 192 units.  Splits hold about 73728 units (96 blocks at
@@ -159,12 +164,20 @@ int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_block
   int64_t target = (int64_t)KVK_MLA_SPLIT_UNITS / (W + 192);
   if (t->bits[anchor] == 16) target = shared ? target / 2 : 2 * target;
   if (target < nr) target = nr;
-  const int64_t nb = n_blocks > 0 ? n_blocks : 1;
-  if (target * kMlaMaxUnits < nb) target = (nb + kMlaMaxUnits - 1) / kMlaMaxUnits;  // merge limit
-  const int64_t nsplit = (nb + target - 1) / target;
-  int64_t per = (nb + nsplit - 1) / nsplit;
-  per = (per + nr - 1) / nr * nr;
-  return (int32_t)per;
+  *target_out = (int32_t)target;
+  *nr_out = (int32_t)nr;
+}
+
+int32_t mla_split_blocks_for(const kvk_table* t, int32_t anchor, int32_t n_blocks) {
+  int32_t target = 0, nr = 1;
+  mla_split_rule(t, anchor, &target, &nr);
+  return mla_split_len(target, nr, n_blocks);
+}
+
+uint64_t fnv1a64(const uint8_t* p, size_t n) {
+  uint64_t h = 0xcbf29ce484222325ull;
+  for (size_t i = 0; i < n; ++i) h = (h ^ p[i]) * 0x100000001b3ull;
+  return h;
 }
 
 int32_t mla_units(const kvk_table* t, int32_t anchor, int32_t n_stored) {
@@ -183,7 +196,9 @@ void mla_workspace(const kvk_table* t, int32_t l0, int32_t l1, MlaWorkspace* ws)
   }
   for (int l = l0; l < l1; ++l) {
     const int32_t a = t->info.anchor_of[l];
-    ws->units_cap[l] = mla_units(t, a, t->cap);
+    int32_t target = 0, nr = 1;
+    mla_split_rule(t, a, &target, &nr);
+    ws->units_cap[l] = mla_units_bound(target, t->nb_cap);  // every n_stored <= cap
     ws->part_off[l] = off;
     off += round256((int64_t)d.batch * ws->units_cap[l] * mla_heads_padded(d.n_q_heads) * (t->rank[a] + 2) * 4);
   }
@@ -419,10 +434,17 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
     return KVK_OK;
   }
   if (!t->seq.empty()) {
-    // GQA: the device-side work list, then every sequence's split partials (each
+    // The device-side work list, then GQA: every sequence's split partials (each
     // sized with its own, smaller, split target: the batch's longer splits need no
-    // more).  MLA: every sequence's own workspace, one after the other.
-    size_t total = d.kind == KVK_MLA ? 0 : (size_t)gqa_batched_list_bytes(t, l0, l1);
+    // more); MLA: every sequence's own workspace, one after the other.
+    size_t total;
+    if (d.kind == KVK_MLA) {
+      MlaSeqList L;
+      if (kvk_status st = mla_seq_list(t, l0, l1, L, false)) return st;
+      total = (size_t)L.bytes;
+    } else {
+      total = (size_t)gqa_batched_list_bytes(t, l0, l1);
+    }
     for (const kvk_table* s : t->seq) {
       size_t one = 0;
       const kvk_status st = kvk_workspace_bytes(s, l0, l1, &one);
@@ -439,8 +461,9 @@ extern "C" kvk_status kvk_workspace_bytes(const kvk_table* t, int32_t l0, int32_
   size_t floats = 0;
   for (int l = l0; l < l1; ++l) {
     const int32_t a = t->info.anchor_of[l];
-    const int32_t sb = gqa_item_split_blocks(t, a, l0, l1, nblk, target);
-    floats += (size_t)d.batch * d.n_kv_heads * G * n_splits(nblk, sb) * (d.head_dim + 4);
+    int32_t bound = 0;  // the splits of every n_stored up to the capacity
+    gqa_item_split_blocks(t, a, l0, l1, nblk, target, &bound);
+    floats += (size_t)d.batch * d.n_kv_heads * G * bound * (d.head_dim + 4);
   }
   *out = (size_t)round256((int64_t)(floats * sizeof(float)));
   return KVK_OK;

@@ -43,6 +43,7 @@ def _decode(t, q, wk, wv, n):
     d = t.dims
     out = torch.full((L, d.batch, HQ, 128), float("nan"), dtype=torch.float32, device=DEV)
     ws = torch.full((kvk.workspace_bytes(t, 0, L),), 0xFF, dtype=torch.uint8, device=DEV)
+    kvk.decode_setup(t, 0, L, ws)  # the per-sequence work list (a no-op for one plan)
     kvk.decode_attention(t, 0, L, q.to(DEV).contiguous(), n, SCALE, _arena(t), out, ws,
                          w_uk=kvk.mla_weights_for_library(wk.to(DEV)), w_uv=wv.to(DEV).contiguous())
     return out
@@ -163,3 +164,106 @@ def test_per_sequence_mla_projected_write():
                 continue
             nb = info1.layer_bytes[l]
             assert np.array_equal(got[base[l]:base[l] + nb], a1[info1.layer_offset[l]:info1.layer_offset[l] + nb].cpu().numpy())
+
+
+def _one_table_decode(plan, inp_b, q_b, wk, wv, n, cap, qs=kvk.KIVI32):
+    """Decode of one sequence through a one-sequence table of its plan."""
+    one = kvk.layer_table(kvk.make_dims(kvk.MLA, len(plan), HQ, 4, 128, R, 64, 128, 128, qscheme=qs, batch=1,
+                                        max_tokens=cap), kvk.make_plan(plan))
+    a1 = _new(one)
+    for l, (c, r) in enumerate(inp_b):
+        kvk.compress_layer(one, l, c.to(DEV), r.to(DEV), n, None, a1)
+    nl = len(plan)
+    out = torch.full((nl, 1, HQ, 128), float("nan"), dtype=torch.float32, device=DEV)
+    ws = torch.full((kvk.workspace_bytes(one, 0, nl),), 0xFF, dtype=torch.uint8, device=DEV)
+    kvk.decode_attention(one, 0, nl, q_b.to(DEV).contiguous(), n, SCALE, a1, out, ws,
+                         w_uk=kvk.mla_weights_for_library(wk.to(DEV)), w_uv=wv.to(DEV).contiguous())
+    return out
+
+
+def test_per_sequence_mla_batched_launch_many_items():
+    """8 sequences x 6 layers (every kept width and bit-width, depth groups of up to 3),
+    5000 of 8192 tokens stored: the list is laid out for the capacity (3 splits of the
+    4-bit width-512 streams) and the call runs 2; the split phase and the merge called
+    separately; every sequence bit for bit its one-sequence table's decode, two of them
+    against the oracle."""
+    say("case batched mla many items")
+    nl, B8, n, cap = 6, 8, 5000, 8192
+    rng = np.random.default_rng(77)
+    widths, bits = [512, 256, 128, 64], [16, 8, 4, 2]
+    plans = []
+    for b in range(B8):
+        p, l = [], 0
+        while l < nl:
+            g = int(rng.integers(1, 4)) if l > 0 else 1
+            p.append((0, int(rng.choice(bits)), int(rng.choice(widths))))
+            p += [(1, 16, 0)] * (min(g, nl - l) - 1)
+            l += min(g, nl - l)
+        plans.append(p)
+    plans[0][0] = (0, 4, 512)  # a 4-bit full-width anchor (several splits)
+    d = kvk.make_dims(kvk.MLA, nl, HQ, 4, 128, R, 64, 128, 128, batch=B8, max_tokens=cap)
+    t = kvk.layer_table_batched(d, [kvk.make_plan(p) for p in plans])
+    arena = _new(t)
+    inp = [(synth.latent_random(900 + l, B8, n, R), synth.latent_random(950 + l, B8, n, 64)) for l in range(nl)]
+    for l in range(nl):
+        kvk.compress_layer(t, l, inp[l][0].to(DEV), inp[l][1].to(DEV), n, None, arena)
+    q = synth.q_random(901, nl, B8, HQ, 192)
+    wk = synth.weights_random(902, nl, HQ, 128, R)
+    wv = synth.weights_random(903, nl, HQ, 128, R)
+    wk_lib, wv_d = kvk.mla_weights_for_library(wk.to(DEV)), wv.to(DEV).contiguous()
+    ws = torch.full((kvk.workspace_bytes(t, 0, nl),), 0xFF, dtype=torch.uint8, device=DEV)
+    kvk.decode_setup(t, 0, nl, ws)
+    out = torch.full((nl, B8, HQ, 128), float("nan"), dtype=torch.float32, device=DEV)
+    kvk.decode_attention(t, 0, nl, q.to(DEV), n, SCALE, arena, out, ws, w_uk=wk_lib, w_uv=wv_d)
+    out2 = torch.full_like(out, float("nan"))
+    kvk.decode_splits(t, 0, nl, q.to(DEV), n, SCALE, arena, ws, w_uk=wk_lib, w_uv=wv_d)
+    kvk.decode_merge(t, 0, nl, q.to(DEV), n, SCALE, arena, ws, out2, w_uk=wk_lib, w_uv=wv_d)
+    assert torch.equal(out, out2)
+    for b in range(B8):
+        ref = _one_table_decode(plans[b], [(inp[l][0][b:b + 1].contiguous(), inp[l][1][b:b + 1].contiguous())
+                                           for l in range(nl)], q[:, b:b + 1], wk, wv, n, cap)
+        assert torch.equal(ref[:, 0], out[:, b]), f"sequence {b} differs from its one-sequence table"
+    od = OP.Dims(OP.MLA, nl, HQ, 4, 128, latent_dim=R, rope_dim=64, nope_dim=128, v_dim=128, batch=B8,
+                 max_tokens=cap)
+    sd = OP.sequence_dims(od)
+    oplans = [[OP.Action(bool(a), bb, r) for a, bb, r in p] for p in plans]
+    bases, _ = OP.batched_arena_bases(od, oplans)
+    got_arena = arena.cpu().numpy()
+    for b in (0, 5):
+        offs, total = OP.arena_offsets(sd, oplans[b])
+        want = OM.decode_step(sd, oplans[b], got_arena[bases[b]:bases[b] + total], _np(q[:, b:b + 1]).astype(np.float64),
+                              _np(wk).astype(np.float64), _np(wv).astype(np.float64), n, SCALE)
+        err = rel_err(_np(out[:, b:b + 1]), want)
+        say(f"  sequence {b}: max|diff| / max|out| = {err:.2e}")
+        assert err <= TOL
+
+
+def test_per_sequence_mla_needs_setup_and_its_list():
+    """A per-sequence MLA decode needs kvk_decode_setup of the same workspace and layer
+    range; a workspace whose list was overwritten since makes the kernels return NaN
+    outputs and read nothing through it."""
+    say("case batched mla setup")
+    n = 100
+    t = kvk.layer_table_batched(_dims(B, 128), [kvk.make_plan(p) for p in PLANS])
+    arena = _new(t)
+    inp = _inputs(n, seed=300)
+    for l in range(L):
+        kvk.compress_layer(t, l, inp[l][0].to(DEV), inp[l][1].to(DEV), n, None, arena)
+    q = synth.q_random(301, L, B, HQ, 192).to(DEV)
+    wk = kvk.mla_weights_for_library(synth.weights_random(302, L, HQ, 128, R).to(DEV))
+    wv = synth.weights_random(303, L, HQ, 128, R).to(DEV).contiguous()
+    ws = torch.zeros(kvk.workspace_bytes(t, 0, L), dtype=torch.uint8, device=DEV)
+    out = torch.zeros((L, B, HQ, 128), dtype=torch.float32, device=DEV)
+    with pytest.raises(kvk.KvkError, match="kvk_decode_setup"):
+        kvk.decode_attention(t, 0, L, q, n, SCALE, arena, out, ws, w_uk=wk, w_uv=wv)
+    kvk.decode_setup(t, 1, L, ws)
+    with pytest.raises(kvk.KvkError, match="kvk_decode_setup"):
+        kvk.decode_attention(t, 0, L, q, n, SCALE, arena, out, ws, w_uk=wk, w_uv=wv)
+    kvk.decode_setup(t, 0, L, ws)
+    kvk.decode_attention(t, 0, L, q, n, SCALE, arena, out, ws, w_uk=wk, w_uv=wv)
+    torch.cuda.synchronize()
+    assert torch.isfinite(out).all()
+    ws[:256].zero_()  # the list's header overwritten
+    kvk.decode_attention(t, 0, L, q, n, SCALE, arena, out, ws, w_uk=wk, w_uv=wv)
+    torch.cuda.synchronize()
+    assert torch.isnan(out).all()

@@ -320,3 +320,27 @@ def test_attached_weights_decode_like_passed_ones():
     ws = torch.empty((kvk.workspace_bytes(c.table, 0, 4),), dtype=torch.uint8, device=DEV)
     with pytest.raises(ValueError):  # refused by the binding; the library's own refusal is a CPU test
         kvk.decode_attention(c.table, 0, 4, q.to(DEV).contiguous(), n, SCALE, c.arena, out, ws)
+
+
+def test_partial_records_cover_every_stored_length():
+    """The split count is not monotone in the stored length (a bf16 width-32 anchor
+    read by two layers, 128-block splits in whole passes of 6: 23 splits at 2898
+    blocks, 22 at 2899), so the partial records are sized for every length up to the
+    capacity: 2898 blocks stored in a table of capacity 2899 decode exactly as in a
+    table of capacity 2898 (bit for bit: the same splits, the same merge)."""
+    say("case mla partial records bound")
+    n = 2898 * 32
+    plan = [(0, 16, 32), (1, 16, 0)]
+    C = synth.latent_random(2200, 1, n, 256)
+    R = synth.latent_random(2201, 1, n, 64)
+    q = synth.q_random(2202, 2, 1, 32, 192)
+    wk = synth.weights_random(2203, 2, 32, 128, 256)
+    wv = synth.weights_random(2204, 2, 32, 128, 256)
+    outs = []
+    for cap in (2899 * 32, n):
+        c = MlaCase(2, 32, 256, 1, cap, plan)
+        c.compress(0, C, R, n)
+        outs.append(c.decode(q, wk, wv, n, SCALE))
+        del c
+    assert torch.isfinite(outs[0]).all()
+    assert torch.equal(outs[0], outs[1])

@@ -192,3 +192,23 @@ def test_many_splits(bits, n):
     out = _np(c.decode(q.cuda(), n, 0.088))
     ref = _oracle_out(c, {0: (_np(k), _np(v))}, q, n, 0.088)
     assert rel_err(out, ref) <= TOL
+
+
+def test_workspace_covers_every_stored_length():
+    """The split count is not monotone in the stored length (rounding a split up to
+    whole ring passes can save one: a 4-bit stream with 25-block splits takes 8 splits
+    at 190 blocks and 7 at 193), so the workspace sized at the capacity (193 blocks)
+    holds the partials of every shorter length: 190 blocks + 5 tail tokens decode
+    without a workspace error and match the oracle."""
+    say("case workspace bound gqa")
+    cap, n = 193 * 32, 190 * 32 + 5
+    c = Case(1, 4, 1, 128, 1, cap, [(0, 4)])
+    k, v = synth.kv_random(2100, 1, 1, n, 128)
+    c.compress(0, k.cuda(), v.cuda(), n)
+    q = synth.q_random(2101, 1, 1, 4, 128)
+    scale = 1.0 / np.sqrt(128.0)
+    out = _np(c.decode(q.cuda(), n, scale))
+    ref = _oracle_out(c, {0: (_np(k), _np(v))}, q, n, scale)
+    err = rel_err(out, ref)
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL

@@ -440,7 +440,8 @@ def test_mla_weight_entry_points_reject_bad_arguments():
 def test_batched_mla_table_accounting_matches_oracle():
     """Per-sequence MLA plans (kept widths, bit-widths and depth differing per
     sequence): bases, per-layer offsets and read bytes as the oracle's one-sequence
-    tables give them; the workspace holds every sequence's own MLA workspace."""
+    tables give them; the workspace holds the work list and every sequence's own MLA
+    workspace."""
     from oracle import plan as OP
     plans = [[(0, 4, 512), (1, 16, 0), (0, 8, 128)], [(0, 16, 64), (0, 2, 256), (1, 16, 0)],
              [(0, 8, 256), (0, 8, 256), (0, 4, 512)]]
@@ -461,5 +462,6 @@ def test_batched_mla_table_accounting_matches_oracle():
         one = kvk.layer_table(kvk.make_dims(kvk.MLA, 3, 32, 4, 128, 512, 64, 128, 128, batch=1, max_tokens=300),
                               kvk.make_plan(plans[b]))
         one_ws += kvk.workspace_bytes(one, 0, 3)
-    assert kvk.workspace_bytes(t, 0, 3) == one_ws
+    # the work list (rows and items, a few KiB) at the head, then every sequence's own
+    assert one_ws < kvk.workspace_bytes(t, 0, 3) <= one_ws + (16 << 10)
     assert kvk.read_bytes(t, 0, 3, 250) == OP.read_bytes_batched(od, oplans, 0, 3, 250)
