@@ -654,86 +654,87 @@ __device__ __forceinline__ _Float16* absorb_dst(const MlaAbsorbArgs& a, int li, 
   return reinterpret_cast<_Float16*>(a.ws + a.q_off[li]) + (int64_t)b * a.Hp * (d + kRope);
 }
 
-// One workgroup per (layer, head).  The queries of 16 sequences are staged once in
-// LDS and split into bf16 hi + lo B operands (K = nope); wave w then runs the
-// 16-channel tiles w, w + 4, ... of the latent: A = rows of W_UK[h]^T (latent
-// channel x nope, contiguous in the latent-major layout), up to the widest kept width
-// of the 16 (per-sequence plans: each sequence keeps the channels below its own).
+// One workgroup per (layer, head, 16 sequences).  The 16 queries are staged in LDS
+// and split into bf16 hi + lo B operands (K = nope); wave w then runs the 16-channel
+// tiles w, w + 4, ... of the latent: A = rows of W_UK[h]^T (latent channel x nope,
+// contiguous in the latent-major layout), up to the widest kept width of the 16
+// (per-sequence plans: each sequence keeps the channels below its own).
 __global__ __launch_bounds__(256) void mla_absorb_kernel(MlaAbsorbArgs a) {
   constexpr int PQ = 256 + 8;  // LDS row pitch of the queries (floats)
   __shared__ float qs[16 * PQ];
   if (!mla_list_ok(a.list_hdr, a.list_hash)) return;  // not this call's list
-  const int li = blockIdx.x, h = blockIdx.y;
+  const int li = blockIdx.x, h = blockIdx.y, b0 = 16 * blockIdx.z;
+  const int nb = min(16, a.B - b0);
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, g = lane >> 4, i16 = lane & 15;
   const int qw = a.nope + kRope;
   const int nks = a.nope / 32;
   if (h >= a.Hq) {  // a padding head: zero query (finite scores, never written out)
-    for (int b = 0; b < a.B; ++b) {
+    const int wmax = a.r + kRope;
+    for (int e = tid; e < nb * wmax; e += 256) {
+      const int bi = e / wmax, c = e - bi * wmax;
       int d;
-      _Float16* qa = absorb_dst(a, li, b, d);
-      for (int c = tid; c < d + kRope; c += 256) qa[(int64_t)h * (d + kRope) + c] = (_Float16)0.0f;
+      _Float16* qa = absorb_dst(a, li, b0 + bi, d);
+      if (c < d + kRope) qa[(int64_t)h * (d + kRope) + c] = (_Float16)0.0f;
     }
     return;
   }
-  for (int b = 0; b < a.B; ++b) {
+  for (int e = tid; e < nb * kRope; e += 256) {  // the RoPE part, scaled
+    const int bi = e / kRope, j = e - bi * kRope;
     int d;
-    _Float16* qa = absorb_dst(a, li, b, d);
-    if (tid < kRope) {
-      const float x = load_in(a.q, a.q_f32, li * a.q_lstride + ((int64_t)b * a.Hq + h) * qw + a.nope + tid);
-      qa[(int64_t)h * (d + kRope) + d + tid] = (_Float16)(x * a.scale_log2);
-    }
+    _Float16* qa = absorb_dst(a, li, b0 + bi, d);
+    const float x = load_in(a.q, a.q_f32, li * a.q_lstride + ((int64_t)(b0 + bi) * a.Hq + h) * qw + a.nope + j);
+    qa[(int64_t)h * (d + kRope) + d + j] = (_Float16)(x * a.scale_log2);
   }
   const uint16_t* wt = a.w_ukt + ((int64_t)li * a.Hq + h) * a.r * a.nope;
-  for (int b0 = 0; b0 < a.B; b0 += 16) {
-    int d = 0;  // the widest kept width of the 16 sequences
-    for (int bi = 0; bi < 16 && b0 + bi < a.B; ++bi) {
+  int d = 0;  // the widest kept width of the 16 sequences
+#pragma unroll
+  for (int bi = 0; bi < 16; ++bi) {
+    if (bi < nb) {
       int db;
       absorb_dst(a, li, b0 + bi, db);
       d = db > d ? db : d;
     }
-    __syncthreads();
-    for (int e = tid; e < 16 * a.nope; e += 256) {
-      const int bi = e / a.nope, i = e - bi * a.nope;
-      qs[bi * PQ + i] = b0 + bi < a.B ? load_in(a.q, a.q_f32, li * a.q_lstride + ((int64_t)(b0 + bi) * a.Hq + h) * qw + i) : 0.0f;
+  }
+  for (int e = tid; e < 16 * a.nope; e += 256) {
+    const int bi = e / a.nope, i = e - bi * a.nope;
+    qs[bi * PQ + i] = bi < nb ? load_in(a.q, a.q_f32, li * a.q_lstride + ((int64_t)(b0 + bi) * a.Hq + h) * qw + i) : 0.0f;
+  }
+  __syncthreads();
+  bf16x8 bh[8], bl[8];  // nope <= 256
+#pragma unroll
+  for (int ks = 0; ks < 8; ++ks) {
+    if (ks < nks) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float x = qs[i16 * PQ + 32 * ks + 8 * g + j];
+        const uint16_t hb = bf16_bits_rne(x);
+        bh[ks][j] = bitcast<__bf16>(hb);
+        bl[ks][j] = bitcast<__bf16>(bf16_bits_rne(x - bf16_to_f32(hb)));
+      }
     }
-    __syncthreads();
-    bf16x8 bh[8], bl[8];  // nope <= 256
+  }
+  const int bq = b0 + i16;
+  int dq = 0;
+  _Float16* qa = i16 < nb ? absorb_dst(a, li, bq, dq) : nullptr;
+  for (int c = 16 * wv; c < d; c += 64) {
+    const uint16_t* wrow = wt + (int64_t)(c + i16) * a.nope + 8 * g;
+    u4v wa[8];
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks)
+      if (ks < nks) wa[ks] = *reinterpret_cast<const u4v*>(wrow + 32 * ks);
+    f4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       if (ks < nks) {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float x = qs[i16 * PQ + 32 * ks + 8 * g + j];
-          const uint16_t hb = bf16_bits_rne(x);
-          bh[ks][j] = bitcast<__bf16>(hb);
-          bl[ks][j] = bitcast<__bf16>(bf16_bits_rne(x - bf16_to_f32(hb)));
-        }
+        acc = mfmab(bitcast<bf16x8>(wa[ks]), bh[ks], acc);
+        acc = mfmab(bitcast<bf16x8>(wa[ks]), bl[ks], acc);
       }
     }
-    const int bq = b0 + i16;
-    for (int c = 16 * wv; c < d; c += 64) {
-      const uint16_t* wrow = wt + (int64_t)(c + i16) * a.nope + 8 * g;
-      u4v wa[8];
+    // D[chan c + 4g + e][seq i16]; kept widths are multiples of 32: a tile is wholly in or out
+    if (i16 < nb && c < dq) {
+      _Float16* dst = qa + (int64_t)h * (dq + kRope) + c + 4 * g;
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks)
-        if (ks < nks) wa[ks] = *reinterpret_cast<const u4v*>(wrow + 32 * ks);
-      f4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
-        if (ks < nks) {
-          acc = mfmab(bitcast<bf16x8>(wa[ks]), bh[ks], acc);
-          acc = mfmab(bitcast<bf16x8>(wa[ks]), bl[ks], acc);
-        }
-      }
-      if (bq < a.B) {  // D[chan c + 4g + e][seq i16]
-        int db;
-        _Float16* qa = absorb_dst(a, li, bq, db);
-        if (c < db) {  // kept widths are multiples of 32: the tile is wholly in or out
-          _Float16* dst = qa + (int64_t)h * (db + kRope) + c + 4 * g;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) dst[e] = (_Float16)(acc[e] * a.scale_log2);
-        }
-      }
+      for (int e = 0; e < 4; ++e) dst[e] = (_Float16)(acc[e] * a.scale_log2);
     }
   }
 }
@@ -1640,8 +1641,8 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
   aa.rows = nullptr;
   aa.list_hdr = nullptr;
   aa.list_hash = 0;
-  hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)(l1 - l0), (unsigned)aa.Hp), dim3(256), 0,
-                     stream, aa);
+  hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)(l1 - l0), (unsigned)aa.Hp, (unsigned)((d.batch + 15) / 16)),
+                     dim3(256), 0, stream, aa);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA absorb launch: %s", hipGetErrorString(e));
 
@@ -1744,7 +1745,7 @@ kvk_status mla_absorb_rows(const kvk_table* t, const void* q, int32_t rows, cons
   aa.rows = nullptr;
   aa.list_hdr = nullptr;
   aa.list_hash = 0;
-  hipLaunchKernelGGL(mla_absorb_kernel, dim3(1u, (unsigned)aa.Hp), dim3(256), 0, stream, aa);
+  hipLaunchKernelGGL(mla_absorb_kernel, dim3(1u, (unsigned)aa.Hp, (unsigned)((rows + 15) / 16)), dim3(256), 0, stream, aa);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA absorb launch: %s", hipGetErrorString(e));
   return KVK_OK;
@@ -1951,7 +1952,8 @@ kvk_status mla_decode_batched(const kvk_table* t, int32_t l0, int32_t l1, const 
     aa.r = d.latent_dim;
     aa.q_lstride = (int64_t)d.batch * d.n_q_heads * qw;
     aa.scale_log2 = scale * kLog2e;
-    hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)nl, (unsigned)Hp), dim3(256), 0, stream, aa);
+    hipLaunchKernelGGL(mla_absorb_kernel, dim3((unsigned)nl, (unsigned)Hp, (unsigned)((d.batch + 15) / 16)), dim3(256), 0,
+                       stream, aa);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA absorb launch: %s", hipGetErrorString(e));
     if (n_stored > 0) {  // none stored: the merge needs no partials

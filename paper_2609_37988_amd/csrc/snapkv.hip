@@ -323,117 +323,171 @@ __global__ __launch_bounds__(1024) void snap_topk_kernel(SnapArgs a) {
 // ---------------------------------------------------------------------------
 
 constexpr int kMlaChunk = 256;  // tokens per workgroup in the MLA score passes
+// The MLA score passes' workgroups: 8 waves, each holding the query fragments of
+// two 16-row tiles up to r = 512 (one above, whose fragments take 136 registers), so
+// that the chunk's latent, converted to fp16 once per workgroup, serves 256 (128)
+// rows, and each LDS read of it feeds two score products.
+constexpr int kMlaWaves = 8;
+constexpr int snap_mla_row_tiles(int r) { return r <= 512 ? 2 : 1; }
 
 struct SnapMlaArgs {
   const uint16_t* lat;   // [B][n][r] bf16 latent (full width)
   const uint16_t* rope;  // [B][n][64] bf16 positional keys
   const _Float16* q;     // [B][32][Hp][r + 64] absorbed window queries
-  float* part;           // [B][RB][P][64] x (max, sum)
+  float* part;           // [B][RB][P][rpb] x (max, sum)
   float* stats;          // [B][32 Hp] x (M, 1/L)
-  float* ipart;          // [B][RB][n] importance of each 64-row block
+  float* ipart;          // [B][RB][n] importance of each row block
   float* imp;            // [B][n]
   int32_t n, P, RB, Hq, Hp, r;
+  int32_t rpb;           // rows per block (16 per wave)
 };
 
 __device__ __forceinline__ f4 mfma_f16(half8 a, half8 b, f4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
-// One workgroup per (256-token chunk, 64-row block, sequence); wave w holds the
-// fp16 fragments of rows 16 w .. + 15 of the block (B operand) for the whole chunk.
-// Per 32 tokens the chunk's latent and positional keys are staged in LDS as fp16
-// rows (pitch W + 8 halfs: 16 consecutive rows start 16 distinct 4-bank windows
-// apart) and each wave scores both 16-token tiles (A operand from LDS): lane
-// (i16, kg) gets tokens 4 kg .. + 3 of its row i16.
+// One workgroup per (256-token chunk, row block, sequence); wave w holds the fp16
+// fragments of its RT 16-row tiles (rows 16 (RT w + t) .. + 15 of the block, B
+// operands) for the whole chunk.  Per 32 tokens the chunk's latent and positional
+// keys are staged in LDS as fp16 rows (pitch W + 8 halfs: 16 consecutive rows start
+// 16 distinct 4-bank windows apart; the next step's are loaded meanwhile) and each
+// wave scores both 16-token tiles, every A operand read from LDS once for its RT row
+// tiles: lane (i16, kg) gets tokens 4 kg .. + 3 of row i16 of each tile.  (Reading
+// the tile is what bounds the passes: each wave reads all of it, so more rows per
+// wave means fewer reads per score.)
 // PASS 0: per row the chunk's max and sum of 2^(s - max).  PASS 1: per token the sum
 // over the block's rows of 2^(s - M) / L.
-template <int NK, int PASS>
-__global__ __launch_bounds__(256) void snap_mla_scores_kernel(SnapMlaArgs a) {
-  constexpr int W = 32 * NK, PT = W + 8;
+template <int NK, int PASS, int WV, int RT>
+__global__ __launch_bounds__(64 * WV) void snap_mla_scores_kernel(SnapMlaArgs a) {
+  constexpr int W = 32 * NK, PT = W + 8, NT = 64 * WV;
   __shared__ __attribute__((aligned(16))) _Float16 tile[32 * PT];
-  __shared__ float red[4][32];
+  __shared__ float red[WV][32];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, i16 = lane & 15, kg = lane >> 4;
   const int p = blockIdx.x, rb = blockIdx.y, b = blockIdx.z;
-  const int row = 64 * rb + 16 * wv + i16;  // w Hp + h
-  const int w = row / a.Hp, h = row - w * a.Hp;
-  const bool valid = h < a.Hq;
-  const int lastvis = a.n - kWin + w;  // the row's window query sees t <= lastvis
-  half8 qf[NK];
-  {
+  int lastvis[RT];  // the row's window query sees t <= lastvis
+  bool valid[RT];
+  half8 qf[RT][NK];
+  float m[RT], l[RT], sM[RT], sL[RT];
+#pragma unroll
+  for (int r = 0; r < RT; ++r) {
+    const int row = 16 * RT * WV * rb + 16 * (RT * wv + r) + i16;  // w Hp + h
+    const int w = row / a.Hp, h = row - w * a.Hp;
+    valid[r] = h < a.Hq;
+    lastvis[r] = a.n - kWin + w;
     const _Float16* qr = a.q + ((int64_t)b * kWin * a.Hp + row) * W + 8 * kg;
 #pragma unroll
-    for (int j = 0; j < NK; ++j) qf[j] = *reinterpret_cast<const half8*>(qr + 32 * j);
-  }
-  float m = -INFINITY, l = 0.0f, sM = 0.0f, sL = 0.0f;
-  if constexpr (PASS == 1) {
-    if (valid) {
-      sM = a.stats[((int64_t)b * kWin * a.Hp + row) * 2];
-      sL = a.stats[((int64_t)b * kWin * a.Hp + row) * 2 + 1];
+    for (int j = 0; j < NK; ++j) qf[r][j] = *reinterpret_cast<const half8*>(qr + 32 * j);
+    m[r] = -INFINITY;
+    l[r] = sM[r] = sL[r] = 0.0f;
+    if constexpr (PASS == 1) {
+      if (valid[r]) {
+        sM[r] = a.stats[((int64_t)b * kWin * a.Hp + row) * 2];
+        sL[r] = a.stats[((int64_t)b * kWin * a.Hp + row) * 2 + 1];
+      }
     }
   }
   const int t0 = p * kMlaChunk, t1 = min(a.n, t0 + kMlaChunk);
-  for (int tb = t0; tb < t1; tb += 32) {
-    __syncthreads();  // the tile (and red) are free
-    for (int c = tid; c < 32 * (W / 8); c += 256) {
+  // Each thread moves CPT 8-channel pieces of a 32-token step; the next step's are
+  // loaded while the current one is scored (register double buffering).
+  constexpr int NC = 32 * (W / 8), CPT = (NC + NT - 1) / NT;
+  u4v pre[CPT];
+  auto fetch = [&](int tb) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + i * NT;
       const int tr = c / (W / 8), c8 = 8 * (c - tr * (W / 8));
       const int t = tb + tr;
-      u4v v = {0u, 0u, 0u, 0u};
-      if (t < t1)
-        v = c8 < a.r ? *reinterpret_cast<const u4v*>(a.lat + ((int64_t)b * a.n + t) * a.r + c8)
-                     : *reinterpret_cast<const u4v*>(a.rope + ((int64_t)b * a.n + t) * 64 + (c8 - a.r));
-      half8 x;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        x[2 * e] = (_Float16)__uint_as_float(v[e] << 16);
-        x[2 * e + 1] = (_Float16)__uint_as_float(v[e] & 0xFFFF0000u);
-      }
-      *reinterpret_cast<half8*>(tile + tr * PT + c8) = x;
+      pre[i] = u4v{0u, 0u, 0u, 0u};
+      if (c < NC && t < t1)
+        pre[i] = c8 < a.r ? *reinterpret_cast<const u4v*>(a.lat + ((int64_t)b * a.n + t) * a.r + c8)
+                          : *reinterpret_cast<const u4v*>(a.rope + ((int64_t)b * a.n + t) * 64 + (c8 - a.r));
     }
-    __syncthreads();
+  };
+  fetch(t0);
+  for (int tb = t0; tb < t1; tb += 32) {
+    __syncthreads();  // the tile (and red) are free
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      f4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < NK; ++j)
-        acc = mfma_f16(*reinterpret_cast<const half8*>(tile + (16 * tt + i16) * PT + 32 * j + 8 * kg), qf[j], acc);
-      float x[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int t = tb + 16 * tt + 4 * kg + e;
-        const bool vis = valid && t < t1 && t <= lastvis;
-        if constexpr (PASS == 0) {
-          if (vis) {
-            if (acc[e] > m) {
-              l *= __builtin_amdgcn_exp2f(m - acc[e]);
-              m = acc[e];
-            }
-            l += __builtin_amdgcn_exp2f(acc[e] - m);
-          }
-        } else {
-          x[e] = vis ? __builtin_amdgcn_exp2f(acc[e] - sM) * sL : 0.0f;
-        }
-      }
-      if constexpr (PASS == 1) {
+    for (int i = 0; i < CPT; ++i) {
+      const int c = tid + i * NT;
+      if (c < NC) {
+        const int tr = c / (W / 8), c8 = 8 * (c - tr * (W / 8));
+        half8 x;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const float sum = sum16(x[e]);  // over the wave's 16 rows
-          if (i16 == 0) red[wv][16 * tt + 4 * kg + e] = sum;
+          x[2 * e] = (_Float16)__uint_as_float(pre[i][e] << 16);
+          x[2 * e + 1] = (_Float16)__uint_as_float(pre[i][e] & 0xFFFF0000u);
         }
+        *reinterpret_cast<half8*>(tile + tr * PT + c8) = x;
       }
     }
-    if constexpr (PASS == 1) {
+    if (tb + 32 < t1) fetch(tb + 32);
+    __syncthreads();
+    float x[RT][2][4];  // scores (PASS 0, masked) or probabilities (PASS 1)
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      f4 acc[RT];
+#pragma unroll
+      for (int r = 0; r < RT; ++r) acc[r] = f4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < NK; ++j) {
+        const half8 av = *reinterpret_cast<const half8*>(tile + (16 * tt + i16) * PT + 32 * j + 8 * kg);
+#pragma unroll
+        for (int r = 0; r < RT; ++r) acc[r] = mfma_f16(av, qf[r][j], acc[r]);
+      }
+#pragma unroll
+      for (int r = 0; r < RT; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int t = tb + 16 * tt + 4 * kg + e;
+          const bool vis = valid[r] && t < t1 && t <= lastvis[r];
+          if constexpr (PASS == 0) x[r][tt][e] = vis ? acc[r][e] : -INFINITY;
+          else x[r][tt][e] = vis ? __builtin_amdgcn_exp2f(acc[r][e] - sM[r]) * sL[r] : 0.0f;
+        }
+    }
+    if constexpr (PASS == 0) {  // online max and sum over the step's 8 tokens of each row
+#pragma unroll
+      for (int r = 0; r < RT; ++r) {
+        float mx = x[r][0][0];
+#pragma unroll
+        for (int k = 1; k < 8; ++k) mx = fmaxf(mx, x[r][k >> 2][k & 3]);
+        if (mx > m[r]) {
+          l[r] *= __builtin_amdgcn_exp2f(m[r] - mx);
+          m[r] = mx;
+        }
+        if (m[r] != -INFINITY) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k) l[r] += __builtin_amdgcn_exp2f(x[r][k >> 2][k & 3] - m[r]);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float sum = 0.0f;  // over the wave's rows, tile by tile
+#pragma unroll
+          for (int r = 0; r < RT; ++r) sum += sum16(x[r][tt][e]);
+          if (i16 == 0) red[wv][16 * tt + 4 * kg + e] = sum;
+        }
       __syncthreads();
-      if (tid < 32 && tb + tid < t1)
-        a.ipart[((int64_t)b * a.RB + rb) * a.n + tb + tid] = red[0][tid] + red[1][tid] + red[2][tid] + red[3][tid];
+      if (tid < 32 && tb + tid < t1) {
+        float sum = 0.0f;  // the waves' sums in wave order
+#pragma unroll
+        for (int v = 0; v < WV; ++v) sum += red[v][tid];
+        a.ipart[((int64_t)b * a.RB + rb) * a.n + tb + tid] = sum;
+      }
     }
   }
   if constexpr (PASS == 0) {  // the row's four token groups (lanes i16 + 16 kg)
-    const float M = rows_max(m);
-    const float L = rows_sum(M == -INFINITY ? 0.0f : l * __builtin_amdgcn_exp2f(m - M));
-    if (kg == 0) {
-      float* out = a.part + (((int64_t)b * a.RB + rb) * a.P + p) * 128 + 2 * (16 * wv + i16);
-      out[0] = M;
-      out[1] = L;
+#pragma unroll
+    for (int r = 0; r < RT; ++r) {
+      const float M = rows_max(m[r]);
+      const float L = rows_sum(M == -INFINITY ? 0.0f : l[r] * __builtin_amdgcn_exp2f(m[r] - M));
+      if (kg == 0) {
+        float* out = a.part + (((int64_t)b * a.RB + rb) * a.P + p) * (2 * a.rpb) + 2 * (16 * (RT * wv + r) + i16);
+        out[0] = M;
+        out[1] = L;
+      }
     }
   }
 }
@@ -442,14 +496,15 @@ __global__ __launch_bounds__(256) void snap_mla_scores_kernel(SnapMlaArgs a) {
 __global__ __launch_bounds__(256) void snap_mla_merge_kernel(SnapMlaArgs a) {
   const int b = blockIdx.y, row = blockIdx.x * 256 + threadIdx.x;
   if (row >= kWin * a.Hp) return;
-  const int rb = row >> 6, rr = row & 63;
-  const float* pp = a.part + ((int64_t)b * a.RB + rb) * a.P * 128 + 2 * rr;
+  const int rb = row / a.rpb, rr = row - rb * a.rpb;
+  const int64_t ps = 2 * a.rpb;  // floats per (row block, chunk)
+  const float* pp = a.part + ((int64_t)b * a.RB + rb) * a.P * ps + 2 * rr;
   float M = -INFINITY;
-  for (int p = 0; p < a.P; ++p) M = fmaxf(M, pp[(int64_t)p * 128]);
+  for (int p = 0; p < a.P; ++p) M = fmaxf(M, pp[(int64_t)p * ps]);
   float L = 0.0f;
   for (int p = 0; p < a.P; ++p) {
-    const float mp = pp[(int64_t)p * 128];
-    if (mp != -INFINITY) L += pp[(int64_t)p * 128 + 1] * __builtin_amdgcn_exp2f(mp - M);
+    const float mp = pp[(int64_t)p * ps];
+    if (mp != -INFINITY) L += pp[(int64_t)p * ps + 1] * __builtin_amdgcn_exp2f(mp - M);
   }
   float* st = a.stats + ((int64_t)b * kWin * a.Hp + row) * 2;
   st[0] = M;
@@ -505,7 +560,7 @@ void launch_scores(int D, int G, dim3 gs, size_t lds, hipStream_t stream, const 
 
 struct SnapMlaSizes {
   int64_t q, part, stats, ipart, imp;  // bytes
-  int32_t P, RB, Hp;
+  int32_t P, RB, Hp, rpb;
 };
 
 SnapMlaSizes snap_mla_sizes(const kvk_table* t, int32_t n_tokens) {
@@ -513,9 +568,10 @@ SnapMlaSizes snap_mla_sizes(const kvk_table* t, int32_t n_tokens) {
   SnapMlaSizes s;
   s.Hp = mla_heads_padded(d.n_q_heads);
   s.P = (n_tokens + kMlaChunk - 1) / kMlaChunk;
-  s.RB = kWin * s.Hp / 64;
+  s.rpb = 16 * kMlaWaves * snap_mla_row_tiles(d.latent_dim);
+  s.RB = kWin * s.Hp / s.rpb;  // 32 Hp is a multiple of 1024
   s.q = round256((int64_t)d.batch * kWin * s.Hp * (d.latent_dim + d.rope_dim) * 2);
-  s.part = round256((int64_t)d.batch * s.RB * s.P * 128 * 4);
+  s.part = round256((int64_t)d.batch * s.RB * s.P * 2 * s.rpb * 4);
   s.stats = round256((int64_t)d.batch * kWin * s.Hp * 2 * 4);
   s.ipart = round256((int64_t)d.batch * s.RB * n_tokens * 4);
   s.imp = round256((int64_t)d.batch * n_tokens * 4);
@@ -673,18 +729,19 @@ extern "C" kvk_status kvk_snapkv_select_mla(const kvk_table* t, int32_t layer, c
   a.n = n_tokens;
   a.P = s.P;
   a.RB = s.RB;
+  a.rpb = s.rpb;
   a.Hq = d.n_q_heads;
   a.Hp = s.Hp;
   a.r = d.latent_dim;
-  const dim3 gs((unsigned)s.P, (unsigned)s.RB, (unsigned)d.batch), b256(256);
+  const dim3 gs((unsigned)s.P, (unsigned)s.RB, (unsigned)d.batch), b256(256), bw(64 * kMlaWaves);
   const dim3 gm((unsigned)((kWin * s.Hp + 255) / 256), (unsigned)d.batch);
   const dim3 gr((unsigned)((n_tokens + 255) / 256), (unsigned)d.batch);
 #define KVK_SNAP_MLA(PASS)                                                                                  \
   switch (d.latent_dim) {                                                                                   \
-    case 256: hipLaunchKernelGGL((snap_mla_scores_kernel<10, PASS>), gs, b256, 0, stream, a); break;        \
-    case 512: hipLaunchKernelGGL((snap_mla_scores_kernel<18, PASS>), gs, b256, 0, stream, a); break;        \
-    case 768: hipLaunchKernelGGL((snap_mla_scores_kernel<26, PASS>), gs, b256, 0, stream, a); break;        \
-    default: hipLaunchKernelGGL((snap_mla_scores_kernel<34, PASS>), gs, b256, 0, stream, a); break;         \
+    case 256: hipLaunchKernelGGL((snap_mla_scores_kernel<10, PASS, kMlaWaves, 2>), gs, bw, 0, stream, a); break; \
+    case 512: hipLaunchKernelGGL((snap_mla_scores_kernel<18, PASS, kMlaWaves, 2>), gs, bw, 0, stream, a); break; \
+    case 768: hipLaunchKernelGGL((snap_mla_scores_kernel<26, PASS, kMlaWaves, 1>), gs, bw, 0, stream, a); break; \
+    default: hipLaunchKernelGGL((snap_mla_scores_kernel<34, PASS, kMlaWaves, 1>), gs, bw, 0, stream, a); break;  \
   }
   KVK_SNAP_MLA(0)
   hipLaunchKernelGGL(snap_mla_merge_kernel, gm, b256, 0, stream, a);
