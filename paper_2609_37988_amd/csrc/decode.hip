@@ -1304,8 +1304,9 @@ extern "C" kvk_status kvk_decode_setup(const kvk_table* t, int32_t l0, int32_t l
   // one plan: the work list travels in the kernel arguments
   if (t->seq.empty()) return KVK_OK;
   DecodePlan P;
+  MlaSeqList mla;
   if (t->d.kind == KVK_MLA) {
-    MlaSeqList L;
+    MlaSeqList& L = mla;
     if (kvk_status st = mla_seq_list(t, l0, l1, L, true)) return st;
     size_t need = 0;
     if (kvk_status st = kvk_workspace_bytes(t, l0, l1, &need)) return st;
@@ -1328,8 +1329,22 @@ extern "C" kvk_status kvk_decode_setup(const kvk_table* t, int32_t l0, int32_t l
   hipError_t e = hipMemcpyAsync(workspace, P.list.data(), P.list.size(), hipMemcpyHostToDevice, stream);
   if (e == hipSuccess) e = hipStreamSynchronize(stream);  // the host image is freed on return
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "work list copy: %s", hipGetErrorString(e));
+  kvk_table::DecodeSetup rec;
+  rec.workspace = workspace;
+  rec.l0 = l0;
+  rec.l1 = l1;
+  rec.hash = P.hash;
+  if (t->d.kind == KVK_MLA) {
+    rec.rows_off = mla.rows_off;
+    rec.dmax = mla.dmax;
+    for (int k = 0; k < 4; ++k) {
+      rec.items_off[k] = mla.items_off[k];
+      rec.n_items[k] = mla.n_items[k];
+      rec.n_wg[k] = mla.n_wg[k];
+    }
+  }
   std::lock_guard<std::mutex> lock(t->setup_mu);
-  t->setups.push_back({workspace, l0, l1, P.hash});
+  t->setups.push_back(rec);
   return KVK_OK;
 }
 

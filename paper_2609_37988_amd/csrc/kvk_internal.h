@@ -31,6 +31,11 @@ struct kvk_table {
     const void* workspace;
     int32_t l0, l1;
     uint64_t hash;
+    // MLA: the list's launch sizes, so that decode calls need not rebuild it
+    int64_t rows_off = 0, items_off[4] = {0, 0, 0, 0};
+    int32_t n_items[4] = {0, 0, 0, 0};
+    int64_t n_wg[4] = {0, 0, 0, 0};
+    int32_t dmax = 0;
   };
   mutable std::mutex setup_mu;
   mutable std::vector<DecodeSetup> setups;

@@ -1920,13 +1920,17 @@ kvk_status mla_decode_batched(const kvk_table* t, int32_t l0, int32_t l1, const 
                               const void* arena, float* out, void* workspace, hipStream_t stream, bool splits,
                               bool merge) {
   const kvk_dims& d = t->d;
-  MlaSeqList L;
-  if (kvk_status st = mla_seq_list(t, l0, l1, L, true)) return st;
+  // The list depends on the table and the layer range only: its set-up recorded
+  // where it sits and the launch sizes (the kernels check its hash in the workspace).
+  kvk_table::DecodeSetup L;
   {
     bool ready = false;
     std::lock_guard<std::mutex> lock(t->setup_mu);
     for (const kvk_table::DecodeSetup& su : t->setups)
-      ready |= su.workspace == workspace && su.l0 == l0 && su.l1 == l1 && su.hash == L.hash;
+      if (su.workspace == workspace && su.l0 == l0 && su.l1 == l1) {
+        L = su;
+        ready = true;
+      }
     if (!ready)
       return fail(KVK_ERR_INVALID,
                   "per-sequence plans: call kvk_decode_setup for layers [%d, %d) on this workspace first", l0, l1);
