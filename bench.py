@@ -402,10 +402,6 @@ def run_mla(args):
     d2_flops = sum(2 * n_stored * w.n_q_heads * (2 * d + w.rope_dim) for kb in kept for d in kb)
     log(f"step {ms_step * 1e3:.1f} us, {gbs:.1f} GB/s ({100 * gbs / HBM_PEAK_GBS:.1f}% of HBM); "
         f"A1+D2 {sp_avg * 1e3:.1f} us ({sp_gbs:.1f} GB/s)")
-    cpu = None
-    if not args.no_cpu_baseline and plans is None:
-        cpu = cpu_baseline_mla(w, table, n_stored, scale, min(args.cpu_layers or 32, w.n_layers))
-        log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
     app = time_append(kvk, torch, table, w.n_layers, arena, n_stored, (w.n_layers, w.batch, w.latent_dim),
                       (w.n_layers, w.batch, w.rope_dim), dev)
     log(f"append: {app}")
@@ -413,6 +409,10 @@ def run_mla(args):
     log(f"projected write: {proj}")
     snap = time_snapkv_mla(kvk, torch, w, dev) if plans is None else None
     log(f"snapkv (MLA): {snap}")
+    cpu = None  # last: its host thread pool would delay the launch-bound timings above
+    if not args.no_cpu_baseline and plans is None:
+        cpu = cpu_baseline_mla(w, table, n_stored, scale, min(args.cpu_layers or 32, w.n_layers))
+        log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
     ranks = {}
     for p in (seq_plans if plans is not None else [w.plan]):
         for e in p:
@@ -653,17 +653,19 @@ def main():
                                                                arena, out, ws))
     log(f"paper's protocol (4 warm-ups, median of 12 synchronised steps): {med12} us")
 
-    cpu = None
-    if not args.no_cpu_baseline and plans is None:
-        nl = args.cpu_layers or (w.n_layers if args.config in (1, 2) else 4)
-        cpu = cpu_baseline(w, table, n_stored, scale, nl, n_batch=2 if args.config in (1, 2) else 1)
-        log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
     app = time_append(kvk, torch, table, w.n_layers, arena, n_stored,
                       (w.n_layers, w.batch, w.n_kv_heads, w.head_dim), (w.n_layers, w.batch, w.n_kv_heads, w.head_dim),
                       dev)
     log(f"append: {app}")
     sel = time_selector(kvk, torch, w.n_q_heads * w.head_dim, w.n_layers, dev) if args.config == 2 else None
     log(f"selector: {sel}")
+    # The CPU baseline runs last: its host thread pool, busy for seconds, would
+    # otherwise delay the launches of the launch-bound timings above.
+    cpu = None
+    if not args.no_cpu_baseline and plans is None:
+        nl = args.cpu_layers or (w.n_layers if args.config in (1, 2) else 4)
+        cpu = cpu_baseline(w, table, n_stored, scale, nl, n_batch=2 if args.config in (1, 2) else 1)
+        log(f"cpu baseline: {cpu['value']} GB/s over {cpu['seconds']} s")
 
     bits_mix = {}
     for p in ([w.plan] if plans is None else plans):
