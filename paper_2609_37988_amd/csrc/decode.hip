@@ -1054,10 +1054,14 @@ kvk_status prepare(const kvk_table* t, int32_t l0, int32_t l1, const void* q, in
     for (int b = 0; b < d.batch; ++b) add_group(t->seq[b], b, b, 1, t->seq_base[b]);
   const int n_it = (int)items.size();
 
-  // Launch order: the waves that take longest per split (the low-bit items, whose
-  // unpacking makes them compute-bound) first, so that the launch ends on short
-  // waves.  Item indices follow the new order; wave_begin stays increasing.
-  auto cost_rank = [](int bits) { return bits == 2 ? 0 : (bits == 4 ? 1 : (bits == 8 ? 2 : 3)); };
+  // Launch order by precision: bf16, 2-bit, 8-bit, 4-bit.  The bf16 items (the
+  // longest waves, bound by HBM) fill the GPU first; the 2-bit items (bound by their
+  // unpacking) then run beside them rather than alone at the start or the end of the
+  // launch.  Measured on the 14B mixed stack over all 24 orders (D1, one process):
+  // this one 3258 us, 2/4/8/16 3346-3427 us, 16/8/4/2 3430 us, round-robin
+  // interleaving of the items 3316-3380 us.  Item indices follow the new order;
+  // wave_begin stays increasing.
+  auto cost_rank = [](int bits) { return bits == 16 ? 0 : (bits == 2 ? 1 : (bits == 8 ? 2 : 3)); };
   SmallVec<int, kMaxItems> order, new_index;
   order.resize(n_it);
   new_index.resize(n_it);
