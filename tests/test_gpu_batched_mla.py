@@ -267,3 +267,54 @@ def test_per_sequence_mla_needs_setup_and_its_list():
     kvk.decode_attention(t, 0, L, q, n, SCALE, arena, out, ws, w_uk=wk, w_uv=wv)
     torch.cuda.synchronize()
     assert torch.isnan(out).all()
+
+
+def test_per_sequence_mla_14b_latent_shape():
+    """Qwen2.5-14B's latent shape (40 heads padded to two 32-head chunks, r 1024 + 64):
+    per-sequence plans with width-1024 anchors (the wide kernel reading its items from
+    the workspace), depth and every bit-width; every sequence bit for bit its
+    one-sequence table's decode, one against the oracle."""
+    say("case batched mla 14b latent")
+    nl, B3, n, cap, hq, r = 3, 3, 150, 160, 40, 1024
+    plans = [[(0, 16, 1024), (1, 16, 0), (0, 4, 256)],
+             [(0, 8, 512), (0, 4, 1024), (1, 16, 0)],
+             [(0, 2, 1024), (0, 16, 128), (0, 8, 1024)]]
+    d = kvk.make_dims(kvk.MLA, nl, hq, 8, 128, r, 64, 128, 128, batch=B3, max_tokens=cap)
+    t = kvk.layer_table_batched(d, [kvk.make_plan(p) for p in plans])
+    arena = _new(t)
+    inp = [(synth.latent_random(1300 + l, B3, n, r), synth.latent_random(1350 + l, B3, n, 64)) for l in range(nl)]
+    for l in range(nl):
+        kvk.compress_layer(t, l, inp[l][0].to(DEV), inp[l][1].to(DEV), n, None, arena)
+    q = synth.q_random(1301, nl, B3, hq, 192)
+    wk = synth.weights_random(1302, nl, hq, 128, r)
+    wv = synth.weights_random(1303, nl, hq, 128, r)
+    ws = torch.full((kvk.workspace_bytes(t, 0, nl),), 0xFF, dtype=torch.uint8, device=DEV)
+    kvk.decode_setup(t, 0, nl, ws)
+    out = torch.full((nl, B3, hq, 128), float("nan"), dtype=torch.float32, device=DEV)
+    kvk.decode_attention(t, 0, nl, q.to(DEV), n, SCALE, arena, out, ws,
+                         w_uk=kvk.mla_weights_for_library(wk.to(DEV)), w_uv=wv.to(DEV).contiguous())
+    for b in range(B3):
+        one = kvk.layer_table(kvk.make_dims(kvk.MLA, nl, hq, 8, 128, r, 64, 128, 128, batch=1, max_tokens=cap),
+                              kvk.make_plan(plans[b]))
+        a1 = _new(one)
+        for l in range(nl):
+            kvk.compress_layer(one, l, inp[l][0][b:b + 1].contiguous().to(DEV), inp[l][1][b:b + 1].contiguous().to(DEV),
+                               n, None, a1)
+        o1 = torch.full((nl, 1, hq, 128), float("nan"), dtype=torch.float32, device=DEV)
+        w1 = torch.full((kvk.workspace_bytes(one, 0, nl),), 0xFF, dtype=torch.uint8, device=DEV)
+        kvk.decode_attention(one, 0, nl, q[:, b:b + 1].contiguous().to(DEV), n, SCALE, a1, o1, w1,
+                             w_uk=kvk.mla_weights_for_library(wk.to(DEV)), w_uv=wv.to(DEV).contiguous())
+        assert torch.equal(o1[:, 0], out[:, b]), f"sequence {b} differs from its one-sequence table"
+    od = OP.Dims(OP.MLA, nl, hq, 8, 128, latent_dim=r, rope_dim=64, nope_dim=128, v_dim=128, batch=B3,
+                 max_tokens=cap)
+    sd = OP.sequence_dims(od)
+    oplans = [[OP.Action(bool(a), bb, rr) for a, bb, rr in p] for p in plans]
+    bases, _ = OP.batched_arena_bases(od, oplans)
+    got = arena.cpu().numpy()
+    b = 2
+    offs, total = OP.arena_offsets(sd, oplans[b])
+    want = OM.decode_step(sd, oplans[b], got[bases[b]:bases[b] + total], _np(q[:, b:b + 1]).astype(np.float64),
+                          _np(wk).astype(np.float64), _np(wv).astype(np.float64), n, SCALE)
+    err = rel_err(_np(out[:, b:b + 1]), want)
+    say(f"  sequence {b}: max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
