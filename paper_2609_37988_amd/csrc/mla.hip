@@ -1676,6 +1676,19 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     MlaDecodeArgs& a = args[k];
     int64_t& wgs = wgs_of[k];
     if (a.n_items == 0) return KVK_OK;
+    // Launch order: the widest kept width first (then the most bits), as the
+    // per-sequence lists order their items.  Measured on the 32-layer latent stack
+    // (A1 + D2): int4 648 / 605 -> 587 / 568 us, bf16 916 / 884 -> 883 us against
+    // layer order; the narrowest first gave about the same.
+    std::stable_sort(a.items, a.items + a.n_items, [](const MlaItem& x, const MlaItem& y) {
+      return x.d != y.d ? x.d > y.d : x.bits > y.bits;
+    });
+    wgs = 0;
+    for (int i = 0; i < a.n_items; ++i) {
+      MlaItem& it = a.items[i];
+      it.wg_begin = (int32_t)wgs;
+      wgs += ((int64_t)it.nseq * it.units + 7) / 8 * 8 * it.nreaders * it.nhc;
+    }
     if (wgs > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "too many MLA decode workgroups");
     a.n_wg = (int32_t)wgs;
     const kvk_status st = launch_mla_d2(a, k, d.qscheme == KVK_Q_KIVI32, stream);
