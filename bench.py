@@ -24,6 +24,13 @@ context 8192): a step is the absorbed query (A1), the latent decode (D2) and the
 merge with the W_UV up-projection (C2).  The MLA line also times the prefill write
 with the down-projection from hidden states of the model width.
 
+Before its W warm-up steps the decode runs untimed for about 0.25 s (settle()):
+after the prefill write, or an idle second, the GPU's clocks take tens of
+milliseconds to settle (14B mixed stack: the first 14 steps after the write at
+3360-3385 us, then 3260 us; after 1 s idle 3650 us falling to 3260 within 8
+steps), so that W warm-ups alone would time part of that ramp instead of the
+steady decode.  Every timed step still does the whole step's work.
+
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
 """
 import argparse
@@ -170,6 +177,22 @@ def calibrate_copy():
         dst.copy_(src)
     torch.cuda.synchronize()
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "copies": 3}), flush=True)
+
+
+def settle(torch, step, ms=250.0, max_steps=400):
+    """Run step(i) untimed until about `ms` of wall time has passed (synchronising
+    every 8 steps) so that the GPU's clocks have settled before the warm-up steps."""
+    t0 = time.perf_counter()
+    i = 0
+    while i < max_steps:
+        step(i)
+        i += 1
+        if i % 8 == 0:
+            torch.cuda.synchronize()
+            if (time.perf_counter() - t0) * 1e3 >= ms:
+                break
+    torch.cuda.synchronize()
+    return i
 
 
 def log(*a):
@@ -369,6 +392,8 @@ def run_mla(args):
     kvk.decode_setup(table, 0, w.n_layers, ws)  # per-sequence plans: the work list, once
     scale = w.softmax_scale()
     alg = kvk.read_bytes(table, 0, w.n_layers, n_stored)
+    settle(torch, lambda i: kvk.decode_attention(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, out, ws,
+                                                 w_uk=wk, w_uv=wv))
     for i in range(args.warmup):
         kvk.decode_attention(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, out, ws, w_uk=wk, w_uv=wv)
     torch.cuda.synchronize()
@@ -627,6 +652,7 @@ def main():
     scale = w.softmax_scale()
     alg = kvk.read_bytes(table, 0, w.n_layers, n_stored)
 
+    settle(torch, lambda i: kvk.decode_attention(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, out, ws))
     for i in range(args.warmup):
         kvk.decode_attention(table, 0, w.n_layers, qs[i % 2], n_stored, scale, arena, out, ws)
     torch.cuda.synchronize()
