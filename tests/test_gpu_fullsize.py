@@ -301,3 +301,50 @@ def test_snapkv_at_128k():
             assert np.all(np.abs(ref[diff] - theta) <= 1e-4 * top)
     del k, ws, imp
     torch.cuda.empty_cache()
+
+
+def test_mla_per_sequence_plans_full_size():
+    """The benchmark's per-sequence MLA workload (16 sequences of 16384 tokens, each its
+    own 32-layer plan of kept widths, 512 anchors) in the one batched launch per phase:
+    two sampled sequences decode bit for bit as their one-sequence tables do."""
+    w = synth.mla_workload(None)
+    plans = synth.mla_plans_per_sequence(w)
+    say(f"case {w.name} per-sequence plans")
+    n = w.tokens
+    dims = kvk.make_dims(kvk.MLA, w.n_layers, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, w.latent_dim,
+                         w.rope_dim, w.nope_dim, w.v_dim, qscheme=w.qscheme, batch=w.batch, max_tokens=n)
+    table = kvk.layer_table_batched(dims, [kvk.make_plan(p) for p in plans])
+    arena = torch.empty(kvk.table_query(table).arena_bytes, dtype=torch.uint8, device=DEV)
+    for l in range(w.n_layers):
+        c, r = synth.mla_layer(w, l, device=DEV)
+        kvk.compress_layer(table, l, c, r, n, None, arena)
+        del c, r
+    q = synth.mla_queries(w, w.n_layers, device=DEV)
+    wk, wv = synth.mla_weights(w, w.n_layers, device=DEV)
+    wk = kvk.mla_weights_for_library(wk)
+    out = torch.full((w.n_layers, w.batch, w.n_q_heads, w.v_dim), float("nan"), dtype=torch.float32, device=DEV)
+    ws = torch.empty(kvk.workspace_bytes(table, 0, w.n_layers), dtype=torch.uint8, device=DEV)
+    kvk.decode_setup(table, 0, w.n_layers, ws)
+    kvk.decode_attention(table, 0, w.n_layers, q, n, w.softmax_scale(), arena, out, ws, w_uk=wk, w_uv=wv)
+    torch.cuda.synchronize()
+    del arena, ws
+    torch.cuda.empty_cache()
+    one_dims = kvk.make_dims(kvk.MLA, w.n_layers, w.n_q_heads, w.ref_kv_heads, w.ref_head_dim, w.latent_dim,
+                             w.rope_dim, w.nope_dim, w.v_dim, qscheme=w.qscheme, batch=1, max_tokens=n)
+    for b in (0, 9):
+        one = kvk.layer_table(one_dims, kvk.make_plan(plans[b]))
+        a1 = torch.empty(kvk.table_query(one).arena_bytes, dtype=torch.uint8, device=DEV)
+        for l in range(w.n_layers):
+            c, r = synth.mla_layer(w, l, device=DEV)
+            kvk.compress_layer(one, l, c[b:b + 1].contiguous(), r[b:b + 1].contiguous(), n, None, a1)
+            del c, r
+        o1 = torch.full((w.n_layers, 1, w.n_q_heads, w.v_dim), float("nan"), dtype=torch.float32, device=DEV)
+        w1 = torch.empty(kvk.workspace_bytes(one, 0, w.n_layers), dtype=torch.uint8, device=DEV)
+        kvk.decode_attention(one, 0, w.n_layers, q[:, b:b + 1].contiguous(), n, w.softmax_scale(), a1, o1, w1,
+                             w_uk=wk, w_uv=wv)
+        torch.cuda.synchronize()
+        assert torch.isfinite(o1).all()
+        assert torch.equal(o1[:, 0], out[:, b]), f"sequence {b} differs from its one-sequence table"
+        say(f"  sequence {b}: bit for bit")
+        del a1, w1
+        torch.cuda.empty_cache()
