@@ -101,9 +101,17 @@ int32_t split_blocks_for(int32_t bits, int32_t qscheme, int32_t head_dim, int32_
   // at most 1 MiB and shorter when the launch would otherwise hold fewer waves than
   // about two per wave slot (7B shape, 28 layers x 32 streams: 1 MiB splits gave the
   // int2 stack 896 waves for 2048 slots), down to 128 KiB.
+  // The launch's bytes per wave (target_bytes) aim at about 4096 waves; per precision
+  // that becomes about 512 for bf16 (streaming waves saturate HBM well before the
+  // wave slots are full, and every split costs a start and a partial: the 7B-shaped
+  // bf16 stack read whole streams, 896 waves, at 88 % of HBM against 81 % with 4
+  // splits per stream), 2048 for the 2- and 4-bit items (one round of the wave slots:
+  // the 7B int4 stack 62 % -> 64 %) and 4096 for int8 (3 splits per stream on the 7B
+  // stack, 79 %, beat 1 and 2).  The 14B mixed and the 128k eviction stacks split as
+  // before (their targets sit at the clamps).
   const int64_t w = waves > 1 ? waves : 1;
   const int64_t lo = w * (bits <= 4 ? (128LL << 10) : (1LL << 20)), hi = w * (bits <= 4 ? (1LL << 20) : (16LL << 20));
-  target_bytes *= w;
+  target_bytes *= w * (bits == 16 ? 8 : (bits <= 4 ? 2 : 1));
   int64_t target = (target_bytes < lo ? lo : (target_bytes > hi ? hi : target_bytes)) / bb;
   if (target < nr) target = nr;
   const int64_t nb = n_blocks > 0 ? n_blocks : 1;
