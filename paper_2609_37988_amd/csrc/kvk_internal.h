@@ -160,10 +160,13 @@ constexpr int mla_ring_depth(int W, int bits, int kivi) {
   return nr < 1 ? 1 : nr;
 }
 
-// Query heads of an MLA decode rounded up to whole 32-head chunks (the workgroup's
-// two 16-head tiles): the absorbed queries and split partials are laid out for
-// this many; the padding heads carry zero queries and are never written out.
-constexpr int32_t mla_heads_padded(int32_t hq) { return (hq + 31) / 32 * 32; }
+// Query heads of an MLA decode rounded up to whole 16-head tiles (an MFMA's N): the
+// absorbed queries and split partials are laid out for this many; the padding heads
+// carry zero queries and are never written out.  A decode workgroup takes a chunk
+// of two tiles, the last chunk one tile when the padded count is an odd number of
+// tiles (40 heads: 32 + 16, not 64).
+constexpr int32_t mla_heads_padded(int32_t hq) { return (hq + 15) / 16 * 16; }
+constexpr int32_t mla_head_chunks(int32_t hq) { return (mla_heads_padded(hq) + 31) / 32; }
 
 // Most splits of one MLA stream (the merge holds one weight per split in LDS).
 constexpr int kMlaMaxUnits = 128;

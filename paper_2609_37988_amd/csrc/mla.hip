@@ -15,11 +15,13 @@
 // and the latent is read once per decode step for all heads: a dense contraction
 // of the heads against the tokens, which is what the matrix cores are for.
 //
-// D2 work unit: one workgroup of 4 waves per (anchor, reader layer and 32-head
-// chunk, sequence, split).  Per 32-token block the workgroup stages the block in
-// LDS as fp16 (dequantised, or converted from bf16), then
-//   S^T[token, head] = C[token, :] . q~[head, :]   wave w: tokens 16 (w/2).., heads 16 (w%2)..
-//   online softmax over the block                  256 threads: 8 per head
+// D2 work unit: one workgroup of 4 waves per (anchor, reader layer and head chunk,
+// sequence, split); a chunk is two 16-head tiles (32 heads), the last one of a
+// layer one tile when the padded head count is odd in tiles.  Per 32-token block
+// the workgroup stages the block in LDS as fp16 (dequantised, or converted from
+// bf16), then, per head tile of the chunk,
+//   S^T[token, head] = C[token, :] . q~[head, :]   wave w: token tile w / KS, channel part w % KS
+//   online softmax over the block                  8 threads per head
 //   O^T[chan, head] += C^T[chan, token] P^T[token, head]   wave w: channel tiles w, w+4, ...
 // Register ring: the next blocks' raw bytes are loaded while the current block
 // is computed.  The absorbed query and the probabilities enter the MFMAs as
@@ -636,7 +638,7 @@ struct MlaAbsorbArgs {
   const uint64_t* list_hdr;
   uint64_t list_hash;
   int32_t q_f32;
-  int32_t B, Hq, Hp, nope, r;  // Hp: Hq rounded up to whole 32-head chunks
+  int32_t B, Hq, Hp, nope, r;  // Hp: Hq rounded up to whole 16-head tiles
   int64_t q_lstride;           // elements between consecutive layers' queries
   float scale_log2;
 };
@@ -754,7 +756,7 @@ struct MlaItem {
   int32_t d;
   int32_t bits;
   int32_t nreaders;     // reader layers (consecutive)
-  int32_t nhc;          // 32-head chunks per layer
+  int32_t nhc;          // head chunks per layer (32 heads; the last may hold 16)
   int32_t units;        // splits per stream the item's workgroups are laid out for
   int32_t units_cap;    // partial records per stream
   int32_t split_blocks;
@@ -777,7 +779,7 @@ struct MlaDecodeArgs {
   uint64_t list_hash;
   int32_t n_items;
   int32_t n_wg;
-  int32_t B, Hq;         // Hq: the padded head count (whole 32-head chunks)
+  int32_t B, Hq;         // Hq: the padded head count (whole 16-head tiles)
   int32_t nbf;          // full blocks per stream
   int32_t ntail;        // tail tokens
   int32_t nb_cap;
@@ -949,7 +951,7 @@ __device__ __forceinline__ half8 mla_values(const MlaRaw<D, BITS, KIVI>& r, int 
 }
 
 // Running state of a unit: the product accumulators of the wave's channel tiles
-// and, in the softmax threads (16 per head), the head's running max and sum.
+// and, in the softmax threads (8 per head), the head's running max and sum.
 template <int D>
 struct MlaState {
   f4 o[Geo<D>::NCTW][2];
@@ -971,8 +973,9 @@ struct QLds {
 };
 
 // Phase A of an iteration for one wave: values of its 16 tokens x channel part into
-// the tile, and its partial scores S^T[token, head] over those channels.
-template <int D, int BITS, bool KIVI, class LDS, class Q>
+// the tile, and its partial scores S^T[token, head] over those channels for the
+// chunk's HT head tiles.
+template <int D, int BITS, bool KIVI, int HT, class LDS, class Q>
 __device__ __forceinline__ void mla_phase_a(const MlaRaw<D, BITS, KIVI>& r, const Q& qreg, LDS& L, int wv, int tt,
                                             int kh, int lane) {
   using G = Geo<D>;
@@ -985,23 +988,26 @@ __device__ __forceinline__ void mla_phase_a(const MlaRaw<D, BITS, KIVI>& r, cons
     const int c0 = 32 * (kh * G::NKW + ks) + 8 * g;
     L.tile[tile_at<G::PH>(row, c0) >> 3] = x;
     acc[0] = mfma16(x, qreg.get(ks, 0), acc[0]);
-    acc[1] = mfma16(x, qreg.get(ks, 1), acc[1]);
+    if constexpr (HT == 2) acc[1] = mfma16(x, qreg.get(ks, 1), acc[1]);
   }
 #pragma unroll
-  for (int ht = 0; ht < 2; ++ht)
+  for (int ht = 0; ht < HT; ++ht)
     L.s[((wv * 32 + 16 * ht + i16) * kSP + 4 * g) >> 2] = acc[ht];
 }
 
 // Phases B (online softmax over the iteration's tokens; the first nvalid count)
-// and C (probabilities x latent), after phase A and a barrier.
-template <int D, class LDS>
+// and C (probabilities x latent), after phase A and a barrier, for the chunk's HT
+// head tiles (with one tile, the softmax threads of heads 16..31 sit idle: whole
+// waves, so the branch is uniform).
+template <int D, int HT, class LDS>
 __device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, LDS& L, int nvalid, int tid) {
   using G = Geo<D>;
   constexpr int TPB = 2 * kWaves;      // softmax threads per head
   constexpr int TPT = G::TT / TPB;     // tokens per softmax thread
   static_assert(TPT % 4 == 0, "softmax threads read whole f4 score groups");
   const int lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6), g = lane >> 4, i16 = lane & 15;
-  {
+  static_assert(HT == 2 || 16 * TPB % 64 == 0, "one head tile's softmax threads fill whole waves");
+  if (HT == 2 || tid < 16 * TPB) {
     const int h = tid / TPB, p = tid % TPB;
     float x[TPT];
 #pragma unroll
@@ -1043,20 +1049,22 @@ __device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, LDS& L, int nvalid
   }
   __syncthreads();
   {
-    float al[2];
-    half8 pb[G::TT / 32][2];  // the probabilities, read once for all channel tiles
+    float al[HT];
+    half8 pb[G::TT / 32][HT];  // the probabilities, read once for all channel tiles
 #pragma unroll
-    for (int ht = 0; ht < 2; ++ht) {
+    for (int ht = 0; ht < HT; ++ht) {
       al[ht] = L.alpha[16 * ht + i16];
 #pragma unroll
       for (int kk = 0; kk < G::TT / 32; ++kk) pb[kk][ht] = L.p[((16 * ht + i16) * kPP + 32 * kk + 8 * g) >> 3];
     }
     // Rescale only when some head's running max moved (rare once it has settled).
-    if (__builtin_amdgcn_ballot_w64(al[0] != 1.0f || al[1] != 1.0f)) {
+    bool moved = al[0] != 1.0f;
+    if constexpr (HT == 2) moved = moved || al[HT - 1] != 1.0f;
+    if (__builtin_amdgcn_ballot_w64(moved)) {
 #pragma unroll
       for (int i = 0; i < G::NCTW; ++i)
 #pragma unroll
-        for (int ht = 0; ht < 2; ++ht) st.o[i][ht] *= al[ht];
+        for (int ht = 0; ht < HT; ++ht) st.o[i][ht] *= al[ht];
     }
     // A operand: lane (channel i16, k-group g) holds tokens 32 kk + 8 g .. + 7.  The
     // swizzle only touches bit 3 of the channel, so tile ct sits 16 kWaves (ct - wv)
@@ -1078,15 +1086,16 @@ __device__ __forceinline__ void mla_phase_bc(MlaState<D>& st, LDS& L, int nvalid
           const short4v hi = ds_read_tr4(abase[kk][1] + 16 * kWaves * i);
           const half8 av = bitcast<half8>(__builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 #pragma unroll
-          for (int ht = 0; ht < 2; ++ht) st.o[i][ht] = mfma16(av, pb[kk][ht], st.o[i][ht]);
+          for (int ht = 0; ht < HT; ++ht) st.o[i][ht] = mfma16(av, pb[kk][ht], st.o[i][ht]);
         }
       }
     }
   }
 }
 
-// sb, units: the split length and the splits of the stream in this call.
-template <int D, int BITS, bool KIVI, int POL, class LDS>
+// sb, units: the split length and the splits of the stream in this call; HT: the
+// head tiles of chunk hc (2, or 1 for a last chunk of 16 heads).
+template <int D, int BITS, bool KIVI, int POL, int HT, class LDS>
 __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& it, int rl, int hc,
                                         int b, int u, int sb, int units, LDS& L) {
   using G = Geo<D>;
@@ -1112,8 +1121,8 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
   using QT = typename std::conditional<(D > 512), QLds, QRegs<D>>::type;
   QT qreg;
   if constexpr (D > 512) {
-    // the whole [32][W] block into LDS; the loop's first barrier orders it before use
-    for (int e = tid; e < 32 * (G::W / 8); e += 64 * kWaves) {
+    // the chunk's [16 HT][W] block into LDS; the loop's first barrier orders it before use
+    for (int e = tid; e < 16 * HT * (G::W / 8); e += 64 * kWaves) {
       const int h = e / (G::W / 8), c8 = e - h * (G::W / 8);
       L.q[(h * kWideQP >> 3) + c8] = *reinterpret_cast<const half8*>(qsrc + (int64_t)h * G::W + 8 * c8);
     }
@@ -1122,7 +1131,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
   } else {
     const _Float16* qb = qsrc + 32 * kh * G::NKW + 8 * g;
 #pragma unroll
-    for (int ht = 0; ht < 2; ++ht)
+    for (int ht = 0; ht < HT; ++ht)
 #pragma unroll
       for (int ks = 0; ks < G::NKW; ++ks)
         qreg.v[ks][ht] = *reinterpret_cast<const half8*>(qb + (int64_t)(16 * ht + i16) * G::W + 32 * ks);
@@ -1130,7 +1139,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
     // waits only for the ring entry it uses (a first use inside the loop would make
     // every iteration wait for every load in flight).
 #pragma unroll
-    for (int ht = 0; ht < 2; ++ht)
+    for (int ht = 0; ht < HT; ++ht)
 #pragma unroll
       for (int ks = 0; ks < G::NKW; ++ks) asm volatile("" ::"v"(qreg.v[ks][ht]));
   }
@@ -1146,10 +1155,10 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
       const int kb = k + G::NBI * i;                   // first block of the iteration
       const int nvalid = max(0, min(G::TT, 32 * (k1 - kb)));  // uniform
       __syncthreads();                                 // the tile, scores and p are free
-      mla_phase_a<D, BITS, KIVI>(ring[i], qreg, L, wv, tt, kh, lane);
+      mla_phase_a<D, BITS, KIVI, HT>(ring[i], qreg, L, wv, tt, kh, lane);
       mla_issue<D, BITS, KIVI, POL>(ring[i], rs, (kb + G::NBI * NR + tblk) * bb, trow, g, kh);
       __syncthreads();
-      if (nvalid > 0) mla_phase_bc<D>(st, L, nvalid, tid);
+      if (nvalid > 0) mla_phase_bc<D, HT>(st, L, nvalid, tid);
     }
   }
   if (u == units - 1 && a.ntail > 0) {  // the bf16 tail block as one more iteration
@@ -1157,15 +1166,15 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
     const Rsrc rt = buffer_rsrc(stream + (int64_t)a.nb_cap * bb, tblk == 0 ? 64 * G::W : 0);
     mla_issue<D, 16, false, POL>(tr, rt, 0, trow, g, kh);
     __syncthreads();
-    mla_phase_a<D, 16, false>(tr, qreg, L, wv, tt, kh, lane);
+    mla_phase_a<D, 16, false, HT>(tr, qreg, L, wv, tt, kh, lane);
     __syncthreads();
-    mla_phase_bc<D>(st, L, a.ntail, tid);
+    mla_phase_bc<D, HT>(st, L, a.ntail, tid);
   }
 
   // split partial: m[Hq], l[Hq], o[Hq][D] of this (reader, sequence, split)
   float* rec = reinterpret_cast<float*>(a.ws + it.part_off0 + (int64_t)rl * it.part_stride) +
                ((int64_t)b * it.units_cap + u) * a.Hq * (D + 2);
-  if (tid % (2 * kWaves) == 0) {
+  if (tid % (2 * kWaves) == 0 && tid / (2 * kWaves) < 16 * HT) {
     const int h = 32 * hc + tid / (2 * kWaves);
     rec[h] = st.m;
     rec[a.Hq + h] = st.l;
@@ -1176,7 +1185,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
     const int ct = wv + kWaves * i;
     if (ct < G::NCT) {
 #pragma unroll
-      for (int ht = 0; ht < 2; ++ht) {
+      for (int ht = 0; ht < HT; ++ht) {
         const int h = 32 * hc + 16 * ht + i16;
         *reinterpret_cast<f4*>(orec + (int64_t)h * D + 16 * ct + 4 * g) = st.o[i][ht];
       }
@@ -1202,6 +1211,15 @@ __device__ __forceinline__ int mla_item_wg_begin(const MlaDecodeArgs& a, int i) 
 
 __device__ __forceinline__ MlaItem mla_item_dev(const MlaDecodeArgs& a, int i) {
   return ((ConstMlaItem*)a.items_dev)[i];
+}
+
+// A kernel's by-value argument, read in place in the kernel-argument segment (a
+// lone struct argument starts at its offset 0) through the constant address space:
+// pointers into it that the inlined code selects between then never make the
+// compiler copy the 3 KiB struct to private memory first.
+template <class T>
+__device__ __forceinline__ const T& kernel_args() {
+  return *(const T*)__builtin_amdgcn_kernarg_segment_ptr();
 }
 
 // The item, reader row, head chunk, sequence, split, split length and splits of
@@ -1247,15 +1265,18 @@ __device__ __forceinline__ bool mla_locate(const MlaDecodeArgs& a, int wg, int& 
 // launches single-reader and multi-reader items separately.  Kept widths up to 512:
 // two workgroups per CU.
 template <bool KIVI, int POL, bool DEV>
-__global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(MlaDecodeArgs a) {
+__global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(MlaDecodeArgs) {
   __shared__ MlaLds<kTileHalfs, 0> L;
+  const MlaDecodeArgs& a = kernel_args<MlaDecodeArgs>();
   if (!mla_list_ok(a.list_hdr, a.list_hash)) return;  // not this call's list
   int item, rl, hc, b, u, sb, units;
   if (!mla_locate<DEV>(a, blockIdx.x, item, rl, hc, b, u, sb, units)) return;
-#define KVK_MLA_CASE(DD, BB)                                        \
-  if (it.d == DD && it.bits == BB) {                                \
-    run_mla<DD, BB, KIVI, POL>(a, it, rl, hc, b, u, sb, units, L); \
-    return;                                                         \
+  const bool two = 32 * hc + 32 <= a.Hq;  // a whole chunk, or the last 16 heads
+#define KVK_MLA_CASE(DD, BB)                                                   \
+  if (it.d == DD && it.bits == BB) {                                           \
+    if (two) run_mla<DD, BB, KIVI, POL, 2>(a, it, rl, hc, b, u, sb, units, L); \
+    else run_mla<DD, BB, KIVI, POL, 1>(a, it, rl, hc, b, u, sb, units, L);     \
+    return;                                                                    \
   }
 #define KVK_MLA_D(DD) KVK_MLA_CASE(DD, 16) KVK_MLA_CASE(DD, 8) KVK_MLA_CASE(DD, 4) KVK_MLA_CASE(DD, 2)
 #define KVK_MLA_NARROW \
@@ -1279,11 +1300,13 @@ __global__ __launch_bounds__(64 * kWaves, 8 / kWaves) void mla_decode_kernel(Mla
 // absorbed query (136 registers per lane if held there) is read from a 70 KiB LDS
 // copy instead.
 template <bool KIVI, int POL, bool DEV>
-__global__ __launch_bounds__(64 * kWaves, 1) void mla_decode_wide_kernel(MlaDecodeArgs a) {
+__global__ __launch_bounds__(64 * kWaves, 1) void mla_decode_wide_kernel(MlaDecodeArgs) {
   __shared__ MlaLds<kWideTileHalfs, 32 * kWideQP> L;
+  const MlaDecodeArgs& a = kernel_args<MlaDecodeArgs>();
   if (!mla_list_ok(a.list_hdr, a.list_hash)) return;  // not this call's list
   int item, rl, hc, b, u, sb, units;
   if (!mla_locate<DEV>(a, blockIdx.x, item, rl, hc, b, u, sb, units)) return;
+  const bool two = 32 * hc + 32 <= a.Hq;
   if constexpr (DEV) {
     const MlaItem it = mla_item_dev(a, item);
     KVK_MLA_D(1024)
@@ -1696,7 +1719,7 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     wgs = 0;
     return st;
   };
-  const int nhc = mla_heads_padded(d.n_q_heads) / 32;
+  const int nhc = mla_head_chunks(d.n_q_heads);
   for (int l = l0; l < l1;) {
     const int anc = t->info.anchor_of[l];
     const int re = t->next_anchor[anc] < l1 ? t->next_anchor[anc] : l1;  // readers [l, re)
@@ -1819,7 +1842,7 @@ MlaSeqList::~MlaSeqList() = default;
 kvk_status mla_seq_list(const kvk_table* t, int32_t l0, int32_t l1, MlaSeqList& L, bool image) {
   const kvk_dims& d = t->d;
   const int32_t nl = l1 - l0, B = d.batch;
-  const int nhc = mla_heads_padded(d.n_q_heads) / 32;
+  const int nhc = mla_head_chunks(d.n_q_heads);
   // items per launch class
   int32_t n_k[4] = {0, 0, 0, 0};
   for (int b = 0; b < B; ++b) {
