@@ -15,11 +15,13 @@
 //       (online, rescaled only when the max moves).
 //   snap_merge_kernel: per row, the chunks' (max, sum) merged into (M, 1/L).
 //   snap_scores_kernel<D, 1>: S again, p = 2^(s - M) / L summed over the rows.
-//   snap_topk_kernel: one 1024-thread workgroup per (b, h): radix select (12-, 10-
-//       and 9-bit digits of the fp32 pattern, importance >= 0) of the threshold,
+//   topk_*_kernel: radix select (12-, 10- and 9-bit digits of the fp32 pattern,
+//       importance >= 0) of the threshold over slices of each stream's positions,
 //       then an in-order pass that writes the kept positions already sorted.
 // The keys are read twice from HBM; the queries sit in LDS.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 
 #include "kvk_device.h"
 #include "kvk_internal.h"
@@ -220,65 +222,144 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t ballot, int lane) {
   return (uint32_t)__popcll(ballot & ((1ull << lane) - 1ull));
 }
 
-// One workgroup per (b, h): the keep - 32 largest prefix importances (ties to the
-// lower position) and the window, in increasing order.  The threshold is found by
-// radix select over the fp32 pattern (importance >= 0, so patterns order as values):
-// digits of 12, 10 and 9 bits below the sign, one LDS histogram per digit.  Then
-// each wave takes a contiguous sixteenth of the positions, counts what it keeps,
-// and after one exchange of counts writes its positions in order (ballots give the
-// ranks inside each 64-position step).
-__global__ __launch_bounds__(1024) void snap_topk_kernel(SnapArgs a) {
-  __shared__ uint32_t hist[4096];
-  __shared__ uint32_t wsum[16], wgt[16], weq[16];
-  __shared__ uint32_t sh_prefix, sh_remaining;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int bh = blockIdx.x;
-  const int np = a.n - kWin, k = a.keep_n - kWin;
-  const uint32_t* key = reinterpret_cast<const uint32_t*>(a.imp + (int64_t)bh * a.n);
-  int32_t* out = a.keep + (int64_t)bh * a.keep_n;
-  if (k > 0) {
-    uint32_t prefix = 0, mask = 0, remaining = (uint32_t)k;
-    for (int dg = 0; dg < 3; ++dg) {
-      const int sh = dg == 0 ? 19 : (dg == 1 ? 9 : 0);
-      const int nb = dg == 0 ? 4096 : (dg == 1 ? 1024 : 512);
-      for (int i = tid; i < nb; i += 1024) hist[i] = 0u;
-      __syncthreads();
-      for (int i = tid; i < np; i += 1024) {
-        const uint32_t u = key[i];
-        if ((u & mask) == prefix) atomicAdd(&hist[(u >> sh) & (uint32_t)(nb - 1)], 1u);
-      }
-      __syncthreads();
-      // digits in descending order, four per thread; the thread whose range holds
-      // the remaining-th largest element fixes the digit
-      const int top = nb - 1 - 4 * tid;
-      uint32_t c4 = 0;
-      if (top >= 0)
-        for (int j = 0; j < 4; ++j) c4 += hist[top - j];
-      uint32_t tot;
-      const uint32_t above = block_exclusive_scan(c4, wsum, tot);
-      if (top >= 0 && above < remaining && above + c4 >= remaining) {
-        uint32_t cum = above;
-        for (int j = 0; j < 4; ++j) {
-          const uint32_t c = hist[top - j];
-          if (cum + c >= remaining) {
-            sh_prefix = prefix | ((uint32_t)(top - j) << sh);
-            sh_remaining = remaining - cum;
-            break;
-          }
-          cum += c;
-        }
-      }
-      __syncthreads();
-      prefix = sh_prefix;
-      remaining = sh_remaining;
-      mask |= (uint32_t)(nb - 1) << sh;
-      __syncthreads();
+// Selection per stream (a (b, h) pair, or a sequence of an MLA layer): the keep - 32
+// largest prefix importances (ties to the lower position) and the window, in
+// increasing order.  The threshold is found by radix select over the fp32 pattern
+// (importance >= 0, so patterns order as values): digits of 12, 10 and 9 bits below
+// the sign.  The positions of a stream are cut into slices, one 1024-thread
+// workgroup each, so that a launch spreads over the GPU: per digit one launch builds
+// the histogram (in LDS per slice, then added into the stream's histogram in the
+// workspace) and one picks the digit; then the slices count what they keep and write
+// their positions at their offsets (each wave a contiguous sixteenth of its slice,
+// ballots giving the ranks inside each 64-position step).
+struct TopkArgs {
+  const uint32_t* key;  // [S][n] fp32 patterns of the importances
+  int32_t* keep;        // [S][keep_n]
+  uint32_t* hist;       // [S][4096] digit histograms (zero between digits)
+  uint32_t* state;      // [S][4]: prefix, mask, remaining
+  uint32_t* cnt;        // [S][P][2]: positions above and at the threshold per slice
+  int32_t n, keep_n, P, slice;
+};
+
+constexpr int kTopkBins = 4096;
+
+template <int DG>
+struct Digit {
+  static constexpr int SH = DG == 0 ? 19 : (DG == 1 ? 9 : 0);         // lowest bit
+  static constexpr int NB = DG == 0 ? 4096 : (DG == 1 ? 1024 : 512);  // bins
+};
+
+// The stream's histogram cleared and its state set: no prefix yet, keep - 32 to find.
+__global__ __launch_bounds__(256) void topk_init_kernel(TopkArgs a) {
+  const int s = blockIdx.x;
+  for (int i = threadIdx.x; i < kTopkBins; i += 256) a.hist[(int64_t)s * kTopkBins + i] = 0u;
+  if (threadIdx.x < 4) a.state[4 * s + threadIdx.x] = threadIdx.x == 2 ? (uint32_t)(a.keep_n - kWin) : 0u;
+}
+
+// Histogram of digit DG over one slice, for the keys that carry the prefix so far.
+template <int DG>
+__global__ __launch_bounds__(1024) void topk_hist_kernel(TopkArgs a) {
+  constexpr int SH = Digit<DG>::SH, NB = Digit<DG>::NB;
+  __shared__ uint32_t h[NB];
+  const int s = blockIdx.y, tid = threadIdx.x;
+  const int np = a.n - kWin;
+  const uint32_t prefix = a.state[4 * s], mask = a.state[4 * s + 1];
+  for (int i = tid; i < NB; i += 1024) h[i] = 0u;
+  __syncthreads();
+  const uint32_t* key = a.key + (int64_t)s * a.n;
+  const int i0 = blockIdx.x * a.slice, i1 = min(np, i0 + a.slice);
+  for (int i = i0 + tid; i < i1; i += 1024) {
+    const uint32_t u = key[i];
+    if ((u & mask) == prefix) atomicAdd(&h[(u >> SH) & (uint32_t)(NB - 1)], 1u);
+  }
+  __syncthreads();
+  uint32_t* g = a.hist + (int64_t)s * kTopkBins;
+  for (int i = tid; i < NB; i += 1024)
+    if (h[i] != 0u) atomicAdd(&g[i], h[i]);
+}
+
+// Digit DG of the threshold: over the digits in descending order, four per thread,
+// the thread whose range holds the remaining-th largest key fixes it.  The
+// histogram is cleared behind (each bin by the thread that read it).
+template <int DG>
+__global__ __launch_bounds__(1024) void topk_pick_kernel(TopkArgs a) {
+  constexpr int SH = Digit<DG>::SH, NB = Digit<DG>::NB;
+  __shared__ uint32_t wsum[16];
+  const int s = blockIdx.x, tid = threadIdx.x;
+  uint32_t* g = a.hist + (int64_t)s * kTopkBins;
+  uint32_t* st = a.state + 4 * s;
+  const uint32_t prefix = st[0], mask = st[1], remaining = st[2];
+  const int top = NB - 1 - 4 * tid;
+  uint32_t c[4] = {0u, 0u, 0u, 0u}, c4 = 0u;
+  if (top >= 0)
+    for (int j = 0; j < 4; ++j) {
+      c[j] = g[top - j];
+      c4 += c[j];
     }
-    // prefix = the threshold pattern: keep every larger key and the first
-    // `remaining` keys equal to it, in position order
-    const int seg = (np + 15) / 16;
-    const int r0 = min(np, wv * seg), r1 = min(np, r0 + seg);
-    uint32_t n_gt = 0, n_eq = 0;
+  uint32_t tot;
+  const uint32_t above = block_exclusive_scan(c4, wsum, tot);
+  if (top >= 0 && above < remaining && above + c4 >= remaining) {
+    uint32_t cum = above;
+    for (int j = 0; j < 4; ++j) {
+      if (cum + c[j] >= remaining) {
+        st[0] = prefix | ((uint32_t)(top - j) << SH);
+        st[1] = mask | ((uint32_t)(NB - 1) << SH);
+        st[2] = remaining - cum;
+        break;
+      }
+      cum += c[j];
+    }
+  }
+  if (top >= 0)
+    for (int j = 0; j < 4; ++j) g[top - j] = 0u;
+}
+
+// Per slice: the positions above the threshold pattern and at it.
+__global__ __launch_bounds__(1024) void topk_count_kernel(TopkArgs a) {
+  __shared__ uint32_t wsum[16];
+  const int s = blockIdx.y, tid = threadIdx.x;
+  const int np = a.n - kWin;
+  const uint32_t prefix = a.state[4 * s];
+  const uint32_t* key = a.key + (int64_t)s * a.n;
+  const int i0 = blockIdx.x * a.slice, i1 = min(np, i0 + a.slice);
+  uint32_t n_gt = 0u, n_eq = 0u;
+  for (int i = i0 + tid; i < i1; i += 1024) {
+    const uint32_t u = key[i];
+    n_gt += u > prefix ? 1u : 0u;
+    n_eq += u == prefix ? 1u : 0u;
+  }
+  uint32_t tot_gt, tot_eq;
+  block_exclusive_scan(n_gt, wsum, tot_gt);
+  block_exclusive_scan(n_eq, wsum, tot_eq);
+  if (tid == 0) {
+    uint32_t* c = a.cnt + ((int64_t)s * a.P + blockIdx.x) * 2;
+    c[0] = tot_gt;
+    c[1] = tot_eq;
+  }
+}
+
+// The slice's kept positions at its offset: every position above the threshold
+// pattern, and those at it while fewer than `remaining` came before (position order).
+// Slice 0 also writes the window.  select: false when nothing is selected (keep =
+// the window).
+__global__ __launch_bounds__(1024) void topk_write_kernel(TopkArgs a, int select) {
+  __shared__ uint32_t wgt[16], weq[16];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int s = blockIdx.y;
+  const int np = a.n - kWin, k = a.keep_n - kWin;
+  int32_t* out = a.keep + (int64_t)s * a.keep_n;
+  if (select) {
+    const uint32_t prefix = a.state[4 * s], remaining = a.state[4 * s + 2];
+    const uint32_t* key = a.key + (int64_t)s * a.n;
+    uint32_t gt_slices = 0u, eq_slices = 0u;  // the slices before this one
+    for (int j = 0; j < (int)blockIdx.x; ++j) {
+      gt_slices += a.cnt[((int64_t)s * a.P + j) * 2];
+      eq_slices += a.cnt[((int64_t)s * a.P + j) * 2 + 1];
+    }
+    const int i0 = blockIdx.x * a.slice, i1 = min(np, i0 + a.slice);
+    const int seg = (i1 - i0 + 15) / 16;
+    const int r0 = min(i1, i0 + wv * seg), r1 = min(i1, r0 + seg);
+    uint32_t n_gt = 0u, n_eq = 0u;
     for (int base = r0; base < r1; base += 64) {
       const int i = base + lane;
       const uint32_t u = i < r1 ? key[i] : 0u;
@@ -290,7 +371,7 @@ __global__ __launch_bounds__(1024) void snap_topk_kernel(SnapArgs a) {
       weq[wv] = n_eq;
     }
     __syncthreads();
-    uint32_t gt_before = 0, eq_before = 0;
+    uint32_t gt_before = gt_slices, eq_before = eq_slices;
     for (int w = 0; w < wv; ++w) {
       gt_before += wgt[w];
       eq_before += weq[w];
@@ -310,7 +391,8 @@ __global__ __launch_bounds__(1024) void snap_topk_kernel(SnapArgs a) {
       eq_seen += (uint32_t)__popcll(beq);
     }
   }
-  for (int i = tid; i < kWin; i += 1024) out[k + i] = np + i;
+  if (blockIdx.x == 0)
+    for (int i = tid; i < kWin; i += 1024) out[k + i] = np + i;
 }
 
 // ---------------------------------------------------------------------------
@@ -532,6 +614,56 @@ struct SnapSizes {
   int32_t P, R;
 };
 
+// The selection's slices and scratch for S streams of n positions: slices of at least
+// 4096 positions, as many as keep about 512 workgroups busy.
+struct TopkSizes {
+  int32_t P, slice;
+  int64_t hist, state, cnt;  // bytes
+};
+
+TopkSizes topk_sizes(int64_t S, int32_t n_tokens) {
+  TopkSizes z;
+  const int32_t np = n_tokens - kWin > 0 ? n_tokens - kWin : 0;
+  const int64_t by_size = (np + 4095) / 4096, by_count = (512 + S - 1) / S;
+  z.P = (int32_t)std::max<int64_t>(1, std::min(by_size, by_count));
+  z.slice = ((np + z.P - 1) / z.P + 63) / 64 * 64;
+  if (z.slice == 0) z.slice = 64;
+  z.hist = round256(S * kTopkBins * 4);
+  z.state = round256(S * 4 * 4);
+  z.cnt = round256(S * z.P * 2 * 4);
+  return z;
+}
+
+// The selection over S streams of importances (keys) into keep lists; scratch: the
+// topk_sizes bytes at `w`.
+void launch_topk(const float* imp, int32_t* keep, int64_t S, int32_t n_tokens, int32_t keep_n, uint8_t* w,
+                 hipStream_t stream) {
+  const TopkSizes z = topk_sizes(S, n_tokens);
+  TopkArgs t;
+  t.key = reinterpret_cast<const uint32_t*>(imp);
+  t.keep = keep;
+  t.hist = reinterpret_cast<uint32_t*>(w);
+  t.state = reinterpret_cast<uint32_t*>(w + z.hist);
+  t.cnt = reinterpret_cast<uint32_t*>(w + z.hist + z.state);
+  t.n = n_tokens;
+  t.keep_n = keep_n;
+  t.P = z.P;
+  t.slice = z.slice;
+  const dim3 gs((unsigned)z.P, (unsigned)S), b1024(1024);
+  const bool select = keep_n - kWin > 0;
+  if (select) {
+    hipLaunchKernelGGL(topk_init_kernel, dim3((unsigned)S), dim3(256), 0, stream, t);
+    hipLaunchKernelGGL(topk_hist_kernel<0>, gs, b1024, 0, stream, t);
+    hipLaunchKernelGGL(topk_pick_kernel<0>, dim3((unsigned)S), b1024, 0, stream, t);
+    hipLaunchKernelGGL(topk_hist_kernel<1>, gs, b1024, 0, stream, t);
+    hipLaunchKernelGGL(topk_pick_kernel<1>, dim3((unsigned)S), b1024, 0, stream, t);
+    hipLaunchKernelGGL(topk_hist_kernel<2>, gs, b1024, 0, stream, t);
+    hipLaunchKernelGGL(topk_pick_kernel<2>, dim3((unsigned)S), b1024, 0, stream, t);
+    hipLaunchKernelGGL(topk_count_kernel, gs, b1024, 0, stream, t);
+  }
+  hipLaunchKernelGGL(topk_write_kernel, gs, b1024, 0, stream, t, select ? 1 : 0);
+}
+
 SnapSizes snap_sizes(const kvk_table* t, int32_t n_tokens) {
   const kvk_dims& d = t->d;
   SnapSizes s;
@@ -569,7 +701,7 @@ SnapMlaSizes snap_mla_sizes(const kvk_table* t, int32_t n_tokens) {
   s.Hp = mla_heads_padded(d.n_q_heads);
   s.P = (n_tokens + kMlaChunk - 1) / kMlaChunk;
   s.rpb = 16 * kMlaWaves * snap_mla_row_tiles(d.latent_dim);
-  s.RB = kWin * s.Hp / s.rpb;  // 32 Hp is a multiple of 1024
+  s.RB = kWin * s.Hp / s.rpb;  // 32 Hp is a multiple of 512
   s.q = round256((int64_t)d.batch * kWin * s.Hp * (d.latent_dim + d.rope_dim) * 2);
   s.part = round256((int64_t)d.batch * s.RB * s.P * 2 * s.rpb * 4);
   s.stats = round256((int64_t)d.batch * kWin * s.Hp * 2 * 4);
@@ -622,14 +754,16 @@ extern "C" kvk_status kvk_snapkv_workspace_bytes(const kvk_table* t, int32_t n_t
     if (st != KVK_OK) return st;
     if (!out) return fail(KVK_ERR_INVALID, "snapkv: NULL output");
     const SnapMlaSizes s = snap_mla_sizes(t, n_tokens);
-    *out = (size_t)(s.q + s.part + s.stats + s.ipart + s.imp);
+    const TopkSizes z = topk_sizes(t->d.batch, n_tokens);
+    *out = (size_t)(s.q + s.part + s.stats + s.ipart + s.imp + z.hist + z.state + z.cnt);
     return KVK_OK;
   }
   const kvk_status st = snap_check(t, n_tokens);
   if (st != KVK_OK) return st;
   if (!out) return fail(KVK_ERR_INVALID, "snapkv: NULL output");
   const SnapSizes s = snap_sizes(t, n_tokens);
-  *out = (size_t)(round256(s.part * 4) + round256(s.stats * 4) + round256(s.imp * 4));
+  const TopkSizes z = topk_sizes((int64_t)t->d.batch * t->d.n_kv_heads, n_tokens);
+  *out = (size_t)(round256(s.part * 4) + round256(s.stats * 4) + round256(s.imp * 4) + z.hist + z.state + z.cnt);
   return KVK_OK;
 }
 
@@ -680,7 +814,8 @@ extern "C" kvk_status kvk_snapkv_select(const kvk_table* t, int32_t layer, const
   launch_scores<0>(d.head_dim, G, gs, lds_q, stream, a);
   hipLaunchKernelGGL(snap_merge_kernel, dim3((unsigned)bh), b256, 0, stream, a);
   launch_scores<1>(d.head_dim, G, gs, lds_q, stream, a);
-  hipLaunchKernelGGL(snap_topk_kernel, dim3((unsigned)bh), dim3(1024), 0, stream, a);
+  launch_topk(a.imp, keep_out, bh, n_tokens, d.keep_tokens,
+              w + round256(s.part * 4) + round256(s.stats * 4) + round256(s.imp * 4), stream);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "snapkv launch: %s", hipGetErrorString(e));
   return KVK_OK;
@@ -748,12 +883,9 @@ extern "C" kvk_status kvk_snapkv_select_mla(const kvk_table* t, int32_t layer, c
   KVK_SNAP_MLA(1)
 #undef KVK_SNAP_MLA
   hipLaunchKernelGGL(snap_mla_reduce_kernel, gr, b256, 0, stream, a);
-  SnapArgs k{};  // the selection, one stream per sequence
-  k.imp = a.imp;
-  k.keep = keep_out;
-  k.n = n_tokens;
-  k.keep_n = d.keep_tokens;
-  hipLaunchKernelGGL(snap_topk_kernel, dim3((unsigned)d.batch), dim3(1024), 0, stream, k);
+  // the selection, one stream per sequence
+  launch_topk(a.imp, keep_out, d.batch, n_tokens, d.keep_tokens, wsb + s.q + s.part + s.stats + s.ipart + s.imp,
+              stream);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "snapkv (MLA) launch: %s", hipGetErrorString(e));
   return KVK_OK;
