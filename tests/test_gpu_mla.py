@@ -223,10 +223,10 @@ def test_fp32_inputs_and_symrow_stack():
 @pytest.mark.parametrize("qs", [kvk.KIVI32, kvk.SYMROW], ids=["kivi32", "symrow"])
 @pytest.mark.parametrize("bits", [16, 8, 4, 2])
 def test_width_1024_qwen14b_heads(qs, bits):
-    """Qwen2.5-14B's latent shape: 40 query heads (two 32-head chunks inside, the
-    second padded), r 1024; a kept-width-1024 anchor read by two layers beside 512
-    and 128 anchors, 200 tokens (6 blocks + an 8-token tail); per-layer calls equal
-    the stacked call."""
+    """Qwen2.5-14B's latent shape: 40 query heads (a 32-head chunk and a one-tile
+    chunk of 16, 8 of them padding), r 1024; a kept-width-1024 anchor read by two
+    layers beside 512 and 128 anchors, 200 tokens (6 blocks + an 8-token tail);
+    per-layer calls equal the stacked call."""
     say(f"case mla width-1024 Hq 40 qs={qs} bits={bits}")
     plan = [(0, bits, 1024), (1, 16, 0), (0, 4, 512), (0, bits, 128)]
     n, Hq, r = 200, 40, 1024
@@ -265,8 +265,9 @@ def test_width_1024_single_reader_splits(bits, n):
 
 @pytest.mark.parametrize("Hq", [8, 16, 40, 72])
 def test_head_counts_padded_to_chunks(Hq):
-    """Query-head counts that are not whole 32-head chunks (padded inside) at r 512,
-    two layers (an anchor at 512 and one at 64 bits 4), 90 tokens."""
+    """Query-head counts that are not whole 32-head chunks, padded to 16-head tiles
+    inside (8 and 16: one one-tile chunk; 40: 32 + 16; 72: 32 + 32 + 16) at r 512, two
+    layers (an anchor at 512 and one at 64 bits 4), 90 tokens."""
     say(f"case mla Hq {Hq}")
     n = 90
     c = MlaCase(2, Hq, 512, 3, 96, [(0, 16, 512), (0, 4, 64)])
