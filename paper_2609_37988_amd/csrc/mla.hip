@@ -812,7 +812,7 @@ constexpr int kTileHalfs = kMaxTT * (256 + kRope + 16);  // the largest TT * PH 
 constexpr int kWideTileHalfs = Geo<1024>::TT * Geo<1024>::PH;  // kept width 1024
 constexpr int kSP = 20;                               // score rows: 16 tokens + pad (floats)
 constexpr int kPP = kMaxTT + 8;                       // probability rows: TT + pad (halfs)
-// Kept width 1024 holds the absorbed query of the workgroup's 32 heads in LDS
+// Kept width 1024 holds the absorbed query of the workgroup's (up to) 32 heads in LDS
 // (rows of W + 8 halfs: 16 consecutive rows start 16 distinct 4-bank windows apart).
 constexpr int kWideQP = Geo<1024>::W + 8;
 
@@ -1115,7 +1115,7 @@ __device__ __forceinline__ void run_mla(const MlaDecodeArgs& a, const MlaItem& i
 #pragma unroll
   for (int i = 0; i < NR; ++i) mla_issue<D, BITS, KIVI, POL>(ring[i], rs, (k0 + G::NBI * i + tblk) * bb, trow, g, kh);
 
-  // absorbed query of the 32 heads over this wave's channel part, fp16
+  // absorbed query of the chunk's heads over this wave's channel part, fp16
   const _Float16* qsrc = reinterpret_cast<const _Float16*>(a.ws + it.q_off0 + (int64_t)rl * it.q_stride) +
                          ((int64_t)b * a.Hq + 32 * hc) * G::W;
   using QT = typename std::conditional<(D > 512), QLds, QRegs<D>>::type;
