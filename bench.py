@@ -179,6 +179,35 @@ def calibrate_copy():
     print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "copies": 3}), flush=True)
 
 
+def hbm_context(torch, dev, n=4 << 30):
+    """Context for the roofline, not a target: the rates of torch's own device copy
+    (reads and writes n bytes) and of a sum over n bytes (reads them), the median of
+    10 after 3 warm-ups, on the same GPU in the same process."""
+    src = torch.empty(n // 4, dtype=torch.float32, device=dev).fill_(1.0)
+    dst = torch.empty_like(src)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(10):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        return sorted(ts)[len(ts) // 2]
+
+    t_copy = timed(lambda: dst.copy_(src))
+    t_sum = timed(lambda: src.sum())
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"copy_GB_per_s": round(2 * n / t_copy / 1e9, 1), "sum_read_GB_per_s": round(n / t_sum / 1e9, 1),
+            "bytes": n, "kernels": "torch copy_ and sum, not this library's"}
+
+
 def settle(torch, step, ms=250.0, max_steps=400):
     """Run step(i) untimed until about `ms` of wall time has passed (synchronising
     every 8 steps) so that the GPU's clocks have settled before the warm-up steps."""
@@ -434,6 +463,8 @@ def run_mla(args):
     log(f"projected write: {proj}")
     snap = time_snapkv_mla(kvk, torch, w, dev) if plans is None else None
     log(f"snapkv (MLA): {snap}")
+    ctx = hbm_context(torch, dev)
+    log(f"HBM context: {ctx}")
     cpu = None  # last: its host thread pool would delay the launch-bound timings above
     if not args.no_cpu_baseline and plans is None:
         cpu = cpu_baseline_mla(w, table, n_stored, scale, min(args.cpu_layers or 32, w.n_layers))
@@ -468,6 +499,7 @@ def run_mla(args):
                  "peak": MFMA_F16_PEAK_TFLOPS, "unit": "TFLOP/s",
                  "frac": round(d2_flops / (sp_avg * 1e-3) / 1e12 / MFMA_F16_PEAK_TFLOPS, 4)},
         "cpu_baseline": cpu,
+        "hbm_context": ctx,
         "prefill_write": {"ms": round(w2_ms, 3), "bytes": w2_bytes,
                           "GB_per_s": round(w2_bytes / (w2_ms * 1e-3) / 1e9, 2)},
         "median_of_12_us_per_step": med12,
@@ -685,6 +717,8 @@ def main():
     log(f"append: {app}")
     sel = time_selector(kvk, torch, w.n_q_heads * w.head_dim, w.n_layers, dev) if args.config == 2 else None
     log(f"selector: {sel}")
+    ctx = hbm_context(torch, dev)
+    log(f"HBM context: {ctx}")
     # The CPU baseline runs last: its host thread pool, busy for seconds, would
     # otherwise delay the launches of the launch-bound timings above.
     cpu = None
@@ -736,6 +770,7 @@ def main():
         "append": app,
         "selector_forward": sel,
         "median_of_12_us_per_step": med12,
+        "hbm_context": ctx,
     }
     if w.keep_tokens:
         line["snapkv_select"] = {
