@@ -45,7 +45,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kRope = 64;
-constexpr int kMaxItems = 32;       // anchors per decode launch (kernel-argument size)
+constexpr int kMaxItems = 41;       // anchors per decode launch (kernel arguments <= 4 KiB)
 
 typedef __amdgpu_buffer_rsrc_t Rsrc;
 
@@ -1720,13 +1720,26 @@ kvk_status mla_decode_splits(const kvk_table* t, int32_t l0, int32_t l1, const v
     return st;
   };
   const int nhc = mla_head_chunks(d.n_q_heads);
+  // A class with more items than one launch's arguments hold runs as launches of
+  // equal item counts (a short last launch would run alone, far from filling the GPU).
+  int n_class[4] = {0, 0, 0, 0}, per_launch[4];
+  for (int l = l0; l < l1;) {
+    const int anc = t->info.anchor_of[l];
+    const int re = t->next_anchor[anc] < l1 ? t->next_anchor[anc] : l1;
+    ++n_class[((re - l) * nhc > 1 ? 1 : 0) + (t->rank[anc] > 512 ? 2 : 0)];
+    l = re;
+  }
+  for (int k = 0; k < 4; ++k) {
+    const int nl = (n_class[k] + kMaxItems - 1) / kMaxItems;
+    per_launch[k] = nl > 0 ? (n_class[k] + nl - 1) / nl : kMaxItems;
+  }
   for (int l = l0; l < l1;) {
     const int anc = t->info.anchor_of[l];
     const int re = t->next_anchor[anc] < l1 ? t->next_anchor[anc] : l1;  // readers [l, re)
     const int k = ((re - l) * nhc > 1 ? 1 : 0) + (t->rank[anc] > 512 ? 2 : 0);
     MlaDecodeArgs& a = args[k];
     int64_t& wgs = wgs_of[k];
-    if (a.n_items == kMaxItems) {
+    if (a.n_items == per_launch[k]) {
       const kvk_status st = flush(k);
       if (st != KVK_OK) return st;
     }

@@ -281,6 +281,30 @@ def test_head_counts_padded_to_chunks(Hq):
     assert err <= TOL
 
 
+def test_more_anchors_than_one_launch_holds():
+    """48 single-reader anchors in one launch class, more than the 41 items one
+    launch's arguments hold (two launches of 24): kept widths 32-256 and every
+    bit-width, 70 tokens, against the oracle; per-layer calls equal the stacked call
+    on both sides of the launch boundary."""
+    say("case mla 48 anchors in one class")
+    L, r, n = 48, 256, 70
+    widths, bitss = [256, 128, 64, 32], [16, 8, 4, 2]
+    plan = [(0, bitss[l % 4], widths[(l // 4) % 4]) for l in range(L)]
+    c = MlaCase(L, 32, r, 1, 96, plan)
+    for l in range(L):
+        c.compress(l, synth.latent_random(900 + l, 1, n, r), synth.latent_random(1000 + l, 1, n, 64), n)
+    q = synth.q_random(1100, L, 1, 32, 192)
+    wk = synth.weights_random(1101, L, 32, 128, r)
+    wv = synth.weights_random(1102, L, 32, 128, r)
+    out = c.decode(q, wk, wv, n, SCALE)
+    err = rel_err(_np(out), c.oracle_out(q, wk, wv, n, SCALE))
+    say(f"  max|diff| / max|out| = {err:.2e}")
+    assert err <= TOL
+    for l in (0, 23, 24, 47):
+        one = c.decode(q[l:l + 1], wk[l:l + 1], wv[l:l + 1], n, SCALE, l, l + 1)
+        assert torch.equal(one[0], out[l]), f"layer {l}"
+
+
 def test_arrange_w_uk_is_the_transpose():
     """kvk_mla_arrange_w_uk writes every (layer, head) matrix transposed, bit for bit
     (Qwen2.5-14B's latent shape: 40 heads, nope 128, r 1024)."""
