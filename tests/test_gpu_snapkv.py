@@ -97,6 +97,18 @@ def test_snapkv_ties_keep_lowest_positions():
         assert abs(imp_gpu[0, h].sum() - 5 * W) <= 1e-3
 
 
+def test_snapkv_ties_across_selection_slices():
+    """Zero keys over 9000 positions: the selection runs on three slices of each
+    stream, and the lowest keep - 32 = 4000 prefix positions (equal importances,
+    the threshold tie running across the first slice boundary) are kept in order."""
+    say("case snapkv ties across slices")
+    n, keep = 9000, 4032
+    case, k, q, scale, keep_gpu, imp_gpu, kn, qn = _run(1, 10, 2, 128, n, keep, 960, zero_keys=True)
+    want = np.concatenate([np.arange(keep - W), np.arange(n - W, n)])
+    for h in range(2):
+        assert np.array_equal(keep_gpu[0, h], want)
+
+
 def test_snapkv_keep_list_drives_the_eviction_write():
     """The selected positions go to kvk_compress_layer as keep_idx; decode over the
     evicted int4 cache matches the oracle's attention over the same positions."""
