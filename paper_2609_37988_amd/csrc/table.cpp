@@ -296,6 +296,21 @@ extern "C" kvk_status kvk_layer_table(const kvk_dims* dims, const kvk_action* pl
     const kvk_status st = validate_mla(d, plan);
     if (st != KVK_OK) return st;
   }
+  // The decode kernels address a stream through a 32-bit byte range (buffer
+  // resources and work-item fields), so every stream stays below 2 GiB.
+  {
+    const int64_t cap = d.keep_tokens > 0 ? d.keep_tokens : d.max_tokens;
+    for (int l = 0; l < d.n_layers; ++l) {
+      const kvk_action& a = plan[l];
+      if (a.inherit) continue;
+      const int32_t per_tok = mla ? a.rank + d.rope_dim : 2 * d.head_dim;
+      const int64_t bb = mla ? mla_block_bytes(per_tok, a.bits, d.qscheme) : gqa_block_bytes(d.head_dim, a.bits, d.qscheme);
+      const int64_t sb = round256(cap / KVK_GROUP * bb + 64LL * per_tok);
+      if (sb > 0x7fffffffLL)
+        return fail(KVK_ERR_UNSUPPORTED, "layer %d: a stream of %lld bytes at %lld stored tokens; streams are limited to 2 GiB",
+                    l, (long long)sb, (long long)cap);
+    }
+  }
   const int64_t streams = mla ? (int64_t)d.batch : (int64_t)d.batch * d.n_kv_heads;
 
   kvk_table* t = new (std::nothrow) kvk_table();

@@ -137,6 +137,14 @@ def test_invalid_plans_and_dims():
     kvk.layer_table(kvk.make_dims(kvk.MLA, 3, 40, 8, 128, 1024, 64, 128, 128, batch=1, max_tokens=8),
                     kvk.make_plan([(0, 4, 1024), (1, 16, 0), (0, 2, 128)]))
     _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, kvk.make_dims(kvk.GQA, 3, 8, 2, 96, max_tokens=8), ok_plan)
+    # streams above 2 GiB (bf16 K and V of d_h 128: 512 bytes per token; a width-1024
+    # bf16 latent: 2176) are refused; just below the limit they are accepted
+    big_gqa = kvk.make_plan([(0, 16), (1, 16), (0, 2)])
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table, kvk.make_dims(kvk.GQA, 3, 8, 2, 128, max_tokens=5_000_000), big_gqa)
+    kvk.layer_table(kvk.make_dims(kvk.GQA, 3, 8, 2, 128, max_tokens=4_000_000), big_gqa)
+    _expect(kvk.ERR_UNSUPPORTED, kvk.layer_table,
+            kvk.make_dims(kvk.MLA, 3, 40, 8, 128, 1024, 64, 128, 128, batch=1, max_tokens=1_000_000),
+            kvk.make_plan([(0, 16, 1024), (1, 16, 0), (0, 2, 128)]))
     _expect(kvk.ERR_INVALID, kvk.layer_table, kvk.make_dims(kvk.GQA, 3, 6, 4, 128, max_tokens=8), ok_plan)
     _expect(kvk.ERR_INVALID, kvk.layer_table,
             kvk.make_dims(kvk.GQA, 3, 8, 2, 128, max_tokens=8, keep_tokens=9), ok_plan)
