@@ -27,6 +27,10 @@ using namespace kvkd;
 
 namespace {
 
+// Sequences of a per-sequence batch one write launch serves (those whose plan gives
+// the layer the same bit-width), and each one's region.
+constexpr int kWriteSeqs = 64;
+
 struct CompressArgs {
   const void* k;
   const void* v;
@@ -42,6 +46,12 @@ struct CompressArgs {
   int32_t D;
   int32_t bits;
   int32_t qs;       // kvk_qscheme
+  // Per-sequence batches (n_seq > 0): the launch's streams are the Hkv streams of
+  // sequences seq_of[0 .. n_seq), whose regions start seq_region[j] bytes after
+  // `region`; the inputs stay indexed by the batch's sequence.  n_seq = 0: one table.
+  int32_t n_seq, Hkv;
+  int32_t seq_of[kWriteSeqs];
+  int64_t seq_region[kWriteSeqs];
 };
 
 #pragma clang fp contract(off)
@@ -368,17 +378,23 @@ __global__ __launch_bounds__(256) void compress_kernel(CompressArgs a) {
 
   const int tid = threadIdx.x;
   const int nblk = a.nbf + 1;
-  const int stream = blockIdx.x / nblk;
+  const int stream = blockIdx.x / nblk;  // of the launch
   const int blk = blockIdx.x % nblk;
   const bool tail = blk == a.nbf;
   const int tok0 = blk * 32;
   const int ntok = tail ? a.n_stored - tok0 : 32;  // valid tokens of this block
+  int in_stream = stream;                          // of the inputs
+  uint8_t* sbase = a.region + (int64_t)stream * a.stream_bytes;
+  if (a.n_seq > 0) {
+    const int j = stream / a.Hkv, h = stream - j * a.Hkv;
+    in_stream = a.seq_of[j] * a.Hkv + h;
+    sbase = a.region + a.seq_region[j] + (int64_t)h * a.stream_bytes;
+  }
 
-  stage_block<D, LD>(a, stream, tok0, ntok, Ks, Vs, tid);
+  stage_block<D, LD>(a, in_stream, tok0, ntok, Ks, Vs, tid);
   __syncthreads();
 
-  uint8_t* out = a.region + (int64_t)stream * a.stream_bytes +
-                 (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
+  uint8_t* out = sbase + (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
   if (BITS == 16 || tail) {
     write_bf16_block<D, LD>(Ks, Vs, out, tid);
     return;
@@ -517,6 +533,30 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* region, int
 
 using namespace kvk;
 
+// One W1 launch over `nstreams` streams of the arguments' layout.
+static kvk_status launch_w1(const CompressArgs& a, int64_t nstreams, hipStream_t stream) {
+  const int64_t grid = nstreams * (a.nbf + 1);
+  if (grid > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "grid too large");
+  const dim3 g3((unsigned)grid), b3(256);
+#define KVK_W1(DD, BB, KK) \
+  if (a.D == DD && a.bits == BB && (BB == 16 || a.qs == KK)) { \
+    hipLaunchKernelGGL((compress_kernel<DD, BB, KK>), g3, b3, 0, stream, a); \
+    launched = true; \
+  }
+  bool launched = false;
+  KVK_W1(128, 16, 0) else KVK_W1(128, 8, 0) else KVK_W1(128, 4, 0) else KVK_W1(128, 2, 0)
+  else KVK_W1(128, 8, 1) else KVK_W1(128, 4, 1) else KVK_W1(128, 2, 1)
+  else KVK_W1(128, 8, 2) else KVK_W1(128, 4, 2) else KVK_W1(128, 2, 2)
+  else KVK_W1(64, 16, 0) else KVK_W1(64, 8, 0) else KVK_W1(64, 4, 0) else KVK_W1(64, 2, 0)
+  else KVK_W1(64, 8, 1) else KVK_W1(64, 4, 1) else KVK_W1(64, 2, 1)
+  else KVK_W1(64, 8, 2) else KVK_W1(64, 4, 2) else KVK_W1(64, 2, 2)
+#undef KVK_W1
+  if (!launched) return fail(KVK_ERR_UNSUPPORTED, "no write kernel for d_h %d, %d bits", a.D, a.bits);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "compress launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
 extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, const void* k, const void* v,
                                          int32_t in_dtype, int32_t n_tokens, const int32_t* keep_idx,
                                          void* arena, hipStream_t stream) {
@@ -544,6 +584,45 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
     const int64_t k_seq = mla ? (int64_t)n_tokens * d.latent_dim * elt : (int64_t)d.n_kv_heads * n_tokens * d.head_dim * elt;
     const int64_t v_seq = mla ? (int64_t)n_tokens * d.rope_dim * elt : k_seq;
     const int64_t keep_seq = mla ? (int64_t)d.keep_tokens : (int64_t)d.n_kv_heads * d.keep_tokens;
+    if (!mla) {
+      // One launch per bit-width for the sequences whose plans store the layer at it
+      // (each sequence still written exactly as its one-sequence table writes it).
+      for (const int bits : {16, 8, 4, 2}) {
+        CompressArgs a;
+        a.k = k;
+        a.v = v;
+        a.keep = keep_idx;
+        a.region = static_cast<uint8_t*>(arena);
+        a.in_f32 = in_dtype == KVK_F32;
+        a.n_tokens = n_tokens;
+        a.n_stored = evict ? d.keep_tokens : n_tokens;
+        a.nbf = a.n_stored / KVK_GROUP;
+        a.nb_cap = t->nb_cap;
+        a.D = d.head_dim;
+        a.bits = bits;
+        a.qs = d.qscheme;
+        a.Hkv = d.n_kv_heads;
+        a.n_seq = 0;
+        for (int b = 0; b < d.batch; ++b) {
+          const kvk_table* s = t->seq[b];
+          if (s->plan[layer].inherit || s->bits[layer] != bits) continue;
+          a.block_bytes = s->block_bytes[layer];      // equal for every sequence at this bit-width
+          a.stream_bytes = s->info.stream_bytes[layer];
+          a.seq_of[a.n_seq] = b;
+          a.seq_region[a.n_seq] = t->seq_base[b] + s->info.layer_offset[layer];
+          if (++a.n_seq == kWriteSeqs) {
+            const kvk_status st = launch_w1(a, (int64_t)a.n_seq * d.n_kv_heads, stream);
+            if (st != KVK_OK) return st;
+            a.n_seq = 0;
+          }
+        }
+        if (a.n_seq > 0) {
+          const kvk_status st = launch_w1(a, (int64_t)a.n_seq * d.n_kv_heads, stream);
+          if (st != KVK_OK) return st;
+        }
+      }
+      return KVK_OK;
+    }
     for (int b = 0; b < d.batch; ++b) {
       const kvk_status st = kvk_compress_layer(
           t->seq[b], layer, static_cast<const uint8_t*>(k) + b * k_seq, static_cast<const uint8_t*>(v) + b * v_seq,
@@ -571,27 +650,9 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
   a.D = d.head_dim;
   a.bits = t->bits[layer];
   a.qs = d.qscheme;
-  const int64_t nstreams = (int64_t)d.batch * d.n_kv_heads;
-  const int64_t grid = nstreams * (a.nbf + 1);
-  if (grid > 0x7fffffffLL) return fail(KVK_ERR_UNSUPPORTED, "grid too large");
-  const dim3 g3((unsigned)grid), b3(256);
-#define KVK_W1(DD, BB, KK) \
-  if (d.head_dim == DD && a.bits == BB && (BB == 16 || a.qs == KK)) { \
-    hipLaunchKernelGGL((compress_kernel<DD, BB, KK>), g3, b3, 0, stream, a); \
-    launched = true; \
-  }
-  bool launched = false;
-  KVK_W1(128, 16, 0) else KVK_W1(128, 8, 0) else KVK_W1(128, 4, 0) else KVK_W1(128, 2, 0)
-  else KVK_W1(128, 8, 1) else KVK_W1(128, 4, 1) else KVK_W1(128, 2, 1)
-  else KVK_W1(128, 8, 2) else KVK_W1(128, 4, 2) else KVK_W1(128, 2, 2)
-  else KVK_W1(64, 16, 0) else KVK_W1(64, 8, 0) else KVK_W1(64, 4, 0) else KVK_W1(64, 2, 0)
-  else KVK_W1(64, 8, 1) else KVK_W1(64, 4, 1) else KVK_W1(64, 2, 1)
-  else KVK_W1(64, 8, 2) else KVK_W1(64, 4, 2) else KVK_W1(64, 2, 2)
-#undef KVK_W1
-  if (!launched) return fail(KVK_ERR_UNSUPPORTED, "no write kernel for d_h %d, %d bits", d.head_dim, a.bits);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "compress launch: %s", hipGetErrorString(e));
-  return KVK_OK;
+  a.n_seq = 0;
+  a.Hkv = d.n_kv_heads;
+  return launch_w1(a, (int64_t)d.batch * d.n_kv_heads, stream);
 }
 
 static kvk_status append_gqa(const kvk_table* t, int32_t l0, int32_t l1, const void* k, const void* v,
