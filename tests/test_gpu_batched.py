@@ -120,6 +120,22 @@ def test_batched_plans_match_oracle(qs):
             assert np.array_equal(kd[b].cpu().numpy(), Kr[0]) and np.array_equal(vd[b].cpu().numpy(), Vr[0])
 
 
+def test_write_of_more_sequences_than_one_launch_serves():
+    """70 sequences with their own plans (layer 0 int4 in every plan: 70 sequences of
+    one bit-width, more than the 64 one write launch serves; layer 1 int2 or bf16 by
+    sequence), ragged length 90: every stream bit-exact against the oracle's write."""
+    say("case batched write, 70 sequences")
+    n, D = 90, 64
+    plans = [[(0, 4), (0, 2 if b % 2 == 0 else 16)] for b in range(70)]
+    c = BatchCase(plans, 2, 1, D, 96)
+    Ks, Vs = _inputs(c, n, 1300)
+    for l in range(c.L):
+        kvk.compress_layer(c.table, l, Ks[l].to(DEV), Vs[l].to(DEV), n, None, c.arena)
+    oarena = OC.compress_arena_batched(c.od, c.oplans, [K.float().numpy() for K in Ks],
+                                       [V.float().numpy() for V in Vs])
+    c.check_streams(oarena, n)
+
+
 def test_equal_plans_agree_with_one_plan():
     """All sequences on the same plan: the per-sequence batch decodes like the table
     with that one plan (within the tolerance; its splits differ)."""
