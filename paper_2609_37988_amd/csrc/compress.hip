@@ -578,13 +578,9 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
     return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
   if (kvk_status st = check_gpu_buffers({k, v, keep_idx, arena}, "kvk_compress_layer")) return st;
   if (!t->seq.empty()) {  // per-sequence plans: each sequence's own table and arena
-    const int64_t elt = in_dtype == KVK_F32 ? 4 : 2;
-    const bool mla = d.kind == KVK_MLA;
-    // GQA: K and V [B][Hkv][n][d_h]; MLA: latent [B][n][r] and positional key [B][n][d_R]
-    const int64_t k_seq = mla ? (int64_t)n_tokens * d.latent_dim * elt : (int64_t)d.n_kv_heads * n_tokens * d.head_dim * elt;
-    const int64_t v_seq = mla ? (int64_t)n_tokens * d.rope_dim * elt : k_seq;
-    const int64_t keep_seq = mla ? (int64_t)d.keep_tokens : (int64_t)d.n_kv_heads * d.keep_tokens;
-    if (!mla) {
+    // The inputs stay indexed by the batch's sequence (GQA: K and V [B][Hkv][n][d_h];
+    // MLA: latent [B][n][r] and positional key [B][n][d_R]).
+    if (d.kind != KVK_MLA) {
       // One launch per bit-width for the sequences whose plans store the layer at it
       // (each sequence still written exactly as its one-sequence table writes it).
       for (const int bits : {16, 8, 4, 2}) {
@@ -623,14 +619,7 @@ extern "C" kvk_status kvk_compress_layer(const kvk_table* t, int32_t layer, cons
       }
       return KVK_OK;
     }
-    for (int b = 0; b < d.batch; ++b) {
-      const kvk_status st = kvk_compress_layer(
-          t->seq[b], layer, static_cast<const uint8_t*>(k) + b * k_seq, static_cast<const uint8_t*>(v) + b * v_seq,
-          in_dtype, n_tokens, keep_idx ? keep_idx + b * keep_seq : nullptr,
-          static_cast<uint8_t*>(arena) + t->seq_base[b], stream);
-      if (st != KVK_OK) return st;
-    }
-    return KVK_OK;
+    return mla_compress_layer_batched(t, layer, k, v, in_dtype, n_tokens, keep_idx, arena, stream);
   }
   if (d.kind == KVK_MLA)
     return mla_compress_layer(t, layer, k, v, in_dtype, n_tokens, keep_idx, arena, stream);

@@ -227,6 +227,11 @@ kvk_status mla_compress_layer_project(const kvk_table* t, int32_t layer, const v
 kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* latent,
                               const void* rope, int32_t in_dtype, int32_t n_tokens,
                               const int32_t* keep_idx, void* arena, hipStream_t stream);
+// The write of one layer of a per-sequence MLA table: one launch per (kept width,
+// bit-width) over the sequences whose plans store the layer so.
+kvk_status mla_compress_layer_batched(const kvk_table* t, int32_t layer, const void* latent, const void* rope,
+                                      int32_t in_dtype, int32_t n_tokens, const int32_t* keep_idx, void* arena,
+                                      hipStream_t stream);
 kvk_status mla_append_token(const kvk_table* t, int32_t l0, int32_t l1, const void* latent,
                             const void* rope, int32_t in_dtype, int32_t n_stored, void* arena,
                             hipStream_t stream);

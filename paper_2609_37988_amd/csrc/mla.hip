@@ -75,6 +75,8 @@ __device__ __forceinline__ uint16_t bf16_bits_rne(float x) { return f32_to_bf16_
 // W2: prefill write of one MLA layer
 // ---------------------------------------------------------------------------
 
+constexpr int kMlaWriteSeqs = 64;  // sequences of a per-sequence batch per write launch
+
 struct MlaCompressArgs {
   const void* latent;  // [B][n_tokens][r]
   const void* rope;    // [B][n_tokens][64]
@@ -91,6 +93,12 @@ struct MlaCompressArgs {
   int32_t d;
   int32_t bits;
   int32_t kivi;
+  // Per-sequence batches (n_seq > 0): launch row j writes sequence seq_of[j] (its
+  // inputs indexed by the batch's sequence) into the stream seq_region[j] bytes after
+  // `region`.  n_seq = 0: row b is sequence b of one table.
+  int32_t n_seq;
+  int32_t seq_of[kMlaWriteSeqs];
+  int64_t seq_region[kMlaWriteSeqs];
 };
 
 __device__ __forceinline__ uint32_t kivi_code(float x, float s, float z, float levels) {
@@ -260,11 +268,12 @@ __device__ __forceinline__ void mla_write_block(const Src& src, uint8_t* out, in
 template <int BITS, bool KIVI>
 __global__ __launch_bounds__(256) void mla_compress_kernel(MlaCompressArgs a) {
   __shared__ uint32_t amax[2][32];  // SYMROW: max |x| bits of (c[:d] | k^R, token)
-  const int blk = blockIdx.x, b = blockIdx.y;
+  const int blk = blockIdx.x, j = blockIdx.y;
+  const int b = a.n_seq > 0 ? a.seq_of[j] : j;
   const bool tail = blk == a.nbf;
   const int tok0 = 32 * blk;
   const PrefillRows src{a, b, tok0, tail ? a.n_stored - tok0 : 32};
-  uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
+  uint8_t* out = a.region + (a.n_seq > 0 ? a.seq_region[j] : (int64_t)j * a.stream_bytes) +
                  (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)blk * a.block_bytes);
   mla_write_block<BITS, KIVI>(src, out, a.d, tail, amax, threadIdx.x, 4);
 }
@@ -1478,6 +1487,8 @@ __global__ __launch_bounds__(256) void mla_arrange_w_uk_kernel(const uint16_t* i
 
 namespace kvk {
 
+static kvk_status launch_w2(const MlaCompressArgs& a, int32_t rows, hipStream_t stream);
+
 kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* latent, const void* rope,
                               int32_t in_dtype, int32_t n_tokens, const int32_t* keep_idx, void* arena,
                               hipStream_t stream) {
@@ -1498,7 +1509,13 @@ kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* lat
   a.d = t->rank[layer];
   a.bits = t->bits[layer];
   a.kivi = d.qscheme == KVK_Q_KIVI32;
-  const dim3 g3((unsigned)(a.nbf + 1), (unsigned)d.batch), b3(256);
+  a.n_seq = 0;
+  return launch_w2(a, d.batch, stream);
+}
+
+// One W2 launch: blocks x `rows` (sequences of one table, or the batch rows of a.seq_of).
+static kvk_status launch_w2(const MlaCompressArgs& a, int32_t rows, hipStream_t stream) {
+  const dim3 g3((unsigned)(a.nbf + 1), (unsigned)rows), b3(256);
   if (a.bits == 16) hipLaunchKernelGGL((mla_compress_kernel<16, true>), g3, b3, 0, stream, a);
   else if (a.kivi && a.bits == 8) hipLaunchKernelGGL((mla_compress_kernel<8, true>), g3, b3, 0, stream, a);
   else if (a.kivi && a.bits == 4) hipLaunchKernelGGL((mla_compress_kernel<4, true>), g3, b3, 0, stream, a);
@@ -1508,6 +1525,53 @@ kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* lat
   else hipLaunchKernelGGL((mla_compress_kernel<2, false>), g3, b3, 0, stream, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(KVK_ERR_DEVICE, "MLA compress launch: %s", hipGetErrorString(e));
+  return KVK_OK;
+}
+
+kvk_status mla_compress_layer_batched(const kvk_table* t, int32_t layer, const void* latent, const void* rope,
+                                      int32_t in_dtype, int32_t n_tokens, const int32_t* keep_idx, void* arena,
+                                      hipStream_t stream) {
+  const kvk_dims& d = t->d;
+  // One launch per (kept width, bit-width) for the sequences whose plans store the
+  // layer so; each sequence is written exactly as its one-sequence table writes it.
+  std::vector<char> done(d.batch, 0);
+  for (int b0 = 0; b0 < d.batch; ++b0) {
+    const kvk_table* s0 = t->seq[b0];
+    if (done[b0] || s0->plan[layer].inherit) continue;
+    MlaCompressArgs a;
+    a.latent = latent;
+    a.rope = rope;
+    a.keep = keep_idx;
+    a.region = static_cast<uint8_t*>(arena);
+    a.stream_bytes = s0->info.stream_bytes[layer];
+    a.block_bytes = s0->block_bytes[layer];
+    a.in_f32 = in_dtype == KVK_F32;
+    a.n_tokens = n_tokens;
+    a.n_stored = d.keep_tokens > 0 ? d.keep_tokens : n_tokens;
+    a.nbf = a.n_stored / KVK_GROUP;
+    a.nb_cap = t->nb_cap;
+    a.r = d.latent_dim;
+    a.d = s0->rank[layer];
+    a.bits = s0->bits[layer];
+    a.kivi = d.qscheme == KVK_Q_KIVI32;
+    a.n_seq = 0;
+    for (int b = b0; b < d.batch; ++b) {
+      const kvk_table* s = t->seq[b];
+      if (done[b] || s->plan[layer].inherit || s->rank[layer] != a.d || s->bits[layer] != a.bits) continue;
+      done[b] = 1;
+      a.seq_of[a.n_seq] = b;
+      a.seq_region[a.n_seq] = t->seq_base[b] + s->info.layer_offset[layer];
+      if (++a.n_seq == kMlaWriteSeqs) {
+        const kvk_status st = launch_w2(a, a.n_seq, stream);
+        if (st != KVK_OK) return st;
+        a.n_seq = 0;
+      }
+    }
+    if (a.n_seq > 0) {
+      const kvk_status st = launch_w2(a, a.n_seq, stream);
+      if (st != KVK_OK) return st;
+    }
+  }
   return KVK_OK;
 }
 
