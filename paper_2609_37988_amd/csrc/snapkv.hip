@@ -13,7 +13,7 @@
 //   snap_scores_kernel<D, 0>: S = Q K^T on MFMA (bf16 in, fp32 out) over a
 //       2048-token chunk per workgroup; per row the chunk's max and sum of 2^(s-max)
 //       (online, rescaled only when the max moves).
-//   snap_merge_kernel: per row, the chunks' (max, sum) merged into (M, 1/L).
+//   snap_merge_kernel: per row (one wave), the chunks' (max, sum) merged into (M, 1/L).
 //   snap_scores_kernel<D, 1>: S again, p = 2^(s - M) / L summed over the rows.
 //   topk_*_kernel: radix select (12-, 10- and 9-bit digits of the fp32 pattern,
 //       importance >= 0) of the threshold over slices of each stream's positions,
@@ -179,20 +179,37 @@ __global__ __launch_bounds__(256) void snap_scores_kernel(SnapArgs a) {
 }
 
 // Per (b, h) and row: merge the chunks' (max, sum) into (M, 1/L).
+__device__ __forceinline__ float wave_max64(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+  return x;
+}
+__device__ __forceinline__ float wave_sum64(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+// One wave per (stream, row): lane p merges chunks p, p + 64, ..., then the wave
+// reduces (a reduction order fixed by the lane count, so results repeat exactly).
 __global__ __launch_bounds__(256) void snap_merge_kernel(SnapArgs a) {
-  const int bh = blockIdx.x, r = threadIdx.x;
+  const int bh = blockIdx.y, r = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (r >= a.R) return;
   const float* pp = a.part + (int64_t)bh * a.P * a.R * 2;
   float M = -INFINITY;
-  for (int p = 0; p < a.P; ++p) M = fmaxf(M, pp[((int64_t)p * a.R + r) * 2]);
+  for (int p = lane; p < a.P; p += 64) M = fmaxf(M, pp[((int64_t)p * a.R + r) * 2]);
+  M = wave_max64(M);
   float L = 0.0f;
-  for (int p = 0; p < a.P; ++p) {
+  for (int p = lane; p < a.P; p += 64) {
     const float mp = pp[((int64_t)p * a.R + r) * 2];
     if (mp != -INFINITY) L += pp[((int64_t)p * a.R + r) * 2 + 1] * __builtin_amdgcn_exp2f(mp - M);
   }
-  float* st = a.stats + ((int64_t)bh * a.R + r) * 2;
-  st[0] = M;
-  st[1] = 1.0f / L;  // every row sees position 0, so L >= 1
+  L = wave_sum64(L);
+  if (lane == 0) {
+    float* st = a.stats + ((int64_t)bh * a.R + r) * 2;
+    st[0] = M;
+    st[1] = 1.0f / L;  // every row sees position 0, so L >= 1
+  }
 }
 
 // Exclusive prefix sum over the 1024 threads of a workgroup (16 waves); total out.
@@ -575,22 +592,27 @@ __global__ __launch_bounds__(64 * WV) void snap_mla_scores_kernel(SnapMlaArgs a)
 }
 
 // Per (sequence, row): the chunks' (max, sum) merged into (M, 1/L).
+// One wave per (sequence, row), as snap_merge_kernel.
 __global__ __launch_bounds__(256) void snap_mla_merge_kernel(SnapMlaArgs a) {
-  const int b = blockIdx.y, row = blockIdx.x * 256 + threadIdx.x;
+  const int b = blockIdx.y, row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   if (row >= kWin * a.Hp) return;
   const int rb = row / a.rpb, rr = row - rb * a.rpb;
   const int64_t ps = 2 * a.rpb;  // floats per (row block, chunk)
   const float* pp = a.part + ((int64_t)b * a.RB + rb) * a.P * ps + 2 * rr;
   float M = -INFINITY;
-  for (int p = 0; p < a.P; ++p) M = fmaxf(M, pp[(int64_t)p * ps]);
+  for (int p = lane; p < a.P; p += 64) M = fmaxf(M, pp[(int64_t)p * ps]);
+  M = wave_max64(M);
   float L = 0.0f;
-  for (int p = 0; p < a.P; ++p) {
+  for (int p = lane; p < a.P; p += 64) {
     const float mp = pp[(int64_t)p * ps];
     if (mp != -INFINITY) L += pp[(int64_t)p * ps + 1] * __builtin_amdgcn_exp2f(mp - M);
   }
-  float* st = a.stats + ((int64_t)b * kWin * a.Hp + row) * 2;
-  st[0] = M;
-  st[1] = L > 0.0f ? 1.0f / L : 0.0f;  // a padding head's row has no mass
+  L = wave_sum64(L);
+  if (lane == 0) {
+    float* st = a.stats + ((int64_t)b * kWin * a.Hp + row) * 2;
+    st[0] = M;
+    st[1] = L > 0.0f ? 1.0f / L : 0.0f;  // a padding head's row has no mass
+  }
 }
 
 // importance[b][t] = the row blocks' partial sums, added in block order.
@@ -812,7 +834,7 @@ extern "C" kvk_status kvk_snapkv_select(const kvk_table* t, int32_t layer, const
   const size_t lds_q = (size_t)s.R * (d.head_dim + 8) * sizeof(uint16_t);  // the window queries
   const int G = d.n_q_heads / d.n_kv_heads;
   launch_scores<0>(d.head_dim, G, gs, lds_q, stream, a);
-  hipLaunchKernelGGL(snap_merge_kernel, dim3((unsigned)bh), b256, 0, stream, a);
+  hipLaunchKernelGGL(snap_merge_kernel, dim3((unsigned)((s.R + 3) / 4), (unsigned)bh), b256, 0, stream, a);
   launch_scores<1>(d.head_dim, G, gs, lds_q, stream, a);
   launch_topk(a.imp, keep_out, bh, n_tokens, d.keep_tokens,
               w + round256(s.part * 4) + round256(s.stats * 4) + round256(s.imp * 4), stream);
@@ -869,7 +891,7 @@ extern "C" kvk_status kvk_snapkv_select_mla(const kvk_table* t, int32_t layer, c
   a.Hp = s.Hp;
   a.r = d.latent_dim;
   const dim3 gs((unsigned)s.P, (unsigned)s.RB, (unsigned)d.batch), b256(256), bw(64 * kMlaWaves);
-  const dim3 gm((unsigned)((kWin * s.Hp + 255) / 256), (unsigned)d.batch);
+  const dim3 gm((unsigned)((kWin * s.Hp + 3) / 4), (unsigned)d.batch);  // a wave per row
   const dim3 gr((unsigned)((n_tokens + 255) / 256), (unsigned)d.batch);
 #define KVK_SNAP_MLA(PASS)                                                                                  \
   switch (d.latent_dim) {                                                                                   \
