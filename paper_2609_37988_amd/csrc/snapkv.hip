@@ -252,35 +252,82 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t ballot, int lane) {
 struct TopkArgs {
   const uint32_t* key;  // [S][n] fp32 patterns of the importances
   int32_t* keep;        // [S][keep_n]
-  uint32_t* hist;       // [S][4096] digit histograms (zero between digits)
-  uint32_t* state;      // [S][4]: prefix, mask, remaining
+  uint32_t* hist;       // [S][kTopkBins]: the histograms of digits 0, 1, 2
+  uint32_t* state;      // [S][4][4]: (prefix, mask, remaining) before digit 0, 1, 2 and after 2
   uint32_t* cnt;        // [S][P][2]: positions above and at the threshold per slice
   int32_t n, keep_n, P, slice;
 };
-
-constexpr int kTopkBins = 4096;
 
 template <int DG>
 struct Digit {
   static constexpr int SH = DG == 0 ? 19 : (DG == 1 ? 9 : 0);         // lowest bit
   static constexpr int NB = DG == 0 ? 4096 : (DG == 1 ? 1024 : 512);  // bins
+  static constexpr int OFF = DG == 0 ? 0 : (DG == 1 ? 4096 : 5120);   // in the stream's histograms
 };
+constexpr int kTopkBins = 4096 + 1024 + 512;
 
-// The stream's histogram cleared and its state set: no prefix yet, keep - 32 to find.
+// The stream's histograms cleared and its state set: no prefix yet, keep - 32 to find.
 __global__ __launch_bounds__(256) void topk_init_kernel(TopkArgs a) {
   const int s = blockIdx.x;
   for (int i = threadIdx.x; i < kTopkBins; i += 256) a.hist[(int64_t)s * kTopkBins + i] = 0u;
-  if (threadIdx.x < 4) a.state[4 * s + threadIdx.x] = threadIdx.x == 2 ? (uint32_t)(a.keep_n - kWin) : 0u;
+  if (threadIdx.x < 4) a.state[16 * s + threadIdx.x] = threadIdx.x == 2 ? (uint32_t)(a.keep_n - kWin) : 0u;
 }
 
-// Histogram of digit DG over one slice, for the keys that carry the prefix so far.
+// Digit DG of the threshold, from the state before it and the finished histogram of
+// the digit: over the digits in descending order, four per thread, the thread whose
+// range holds the remaining-th largest key fixes it.  Every workgroup of a launch
+// computes it alike; the state after the digit comes back in st (shared), and the
+// first slice's workgroup stores it for the launches that follow.
+template <int DG>
+__device__ __forceinline__ void topk_pick(const TopkArgs& a, int s, int tid, uint32_t* wsum, uint32_t* st) {
+  constexpr int SH = Digit<DG>::SH, NB = Digit<DG>::NB;
+  const uint32_t* g = a.hist + (int64_t)s * kTopkBins + Digit<DG>::OFF;
+  const uint32_t* prev = a.state + 16 * s + 4 * DG;
+  const uint32_t prefix = prev[0], mask = prev[1], remaining = prev[2];
+  if (tid == 0) {  // unchanged unless a thread owns the digit (one always does)
+    st[0] = prefix;
+    st[1] = mask | ((uint32_t)(NB - 1) << SH);
+    st[2] = remaining;
+  }
+  const int top = NB - 1 - 4 * tid;
+  uint32_t c[4] = {0u, 0u, 0u, 0u}, c4 = 0u;
+  if (top >= 0)
+    for (int j = 0; j < 4; ++j) {
+      c[j] = g[top - j];
+      c4 += c[j];
+    }
+  uint32_t tot;
+  const uint32_t above = block_exclusive_scan(c4, wsum, tot);  // (its barriers order st's first write)
+  if (top >= 0 && above < remaining && above + c4 >= remaining) {
+    uint32_t cum = above;
+    for (int j = 0; j < 4; ++j) {
+      if (cum + c[j] >= remaining) {
+        st[0] = prefix | ((uint32_t)(top - j) << SH);
+        st[2] = remaining - cum;
+        break;
+      }
+      cum += c[j];
+    }
+  }
+  __syncthreads();
+  if (blockIdx.x == 0 && tid < 3) a.state[16 * s + 4 * (DG + 1) + tid] = st[tid];
+}
+
+// Histogram of digit DG over one slice, for the keys that carry the prefix so far
+// (for DG > 0 fixed here first from the previous digit's histogram).
 template <int DG>
 __global__ __launch_bounds__(1024) void topk_hist_kernel(TopkArgs a) {
   constexpr int SH = Digit<DG>::SH, NB = Digit<DG>::NB;
   __shared__ uint32_t h[NB];
+  __shared__ uint32_t wsum[16], st[4];
   const int s = blockIdx.y, tid = threadIdx.x;
   const int np = a.n - kWin;
-  const uint32_t prefix = a.state[4 * s], mask = a.state[4 * s + 1];
+  uint32_t prefix = 0u, mask = 0u;
+  if constexpr (DG > 0) {
+    topk_pick<DG - 1>(a, s, tid, wsum, st);
+    prefix = st[0];
+    mask = st[1];
+  }
   for (int i = tid; i < NB; i += 1024) h[i] = 0u;
   __syncthreads();
   const uint32_t* key = a.key + (int64_t)s * a.n;
@@ -290,53 +337,19 @@ __global__ __launch_bounds__(1024) void topk_hist_kernel(TopkArgs a) {
     if ((u & mask) == prefix) atomicAdd(&h[(u >> SH) & (uint32_t)(NB - 1)], 1u);
   }
   __syncthreads();
-  uint32_t* g = a.hist + (int64_t)s * kTopkBins;
+  uint32_t* g = a.hist + (int64_t)s * kTopkBins + Digit<DG>::OFF;
   for (int i = tid; i < NB; i += 1024)
     if (h[i] != 0u) atomicAdd(&g[i], h[i]);
 }
 
-// Digit DG of the threshold: over the digits in descending order, four per thread,
-// the thread whose range holds the remaining-th largest key fixes it.  The
-// histogram is cleared behind (each bin by the thread that read it).
-template <int DG>
-__global__ __launch_bounds__(1024) void topk_pick_kernel(TopkArgs a) {
-  constexpr int SH = Digit<DG>::SH, NB = Digit<DG>::NB;
-  __shared__ uint32_t wsum[16];
-  const int s = blockIdx.x, tid = threadIdx.x;
-  uint32_t* g = a.hist + (int64_t)s * kTopkBins;
-  uint32_t* st = a.state + 4 * s;
-  const uint32_t prefix = st[0], mask = st[1], remaining = st[2];
-  const int top = NB - 1 - 4 * tid;
-  uint32_t c[4] = {0u, 0u, 0u, 0u}, c4 = 0u;
-  if (top >= 0)
-    for (int j = 0; j < 4; ++j) {
-      c[j] = g[top - j];
-      c4 += c[j];
-    }
-  uint32_t tot;
-  const uint32_t above = block_exclusive_scan(c4, wsum, tot);
-  if (top >= 0 && above < remaining && above + c4 >= remaining) {
-    uint32_t cum = above;
-    for (int j = 0; j < 4; ++j) {
-      if (cum + c[j] >= remaining) {
-        st[0] = prefix | ((uint32_t)(top - j) << SH);
-        st[1] = mask | ((uint32_t)(NB - 1) << SH);
-        st[2] = remaining - cum;
-        break;
-      }
-      cum += c[j];
-    }
-  }
-  if (top >= 0)
-    for (int j = 0; j < 4; ++j) g[top - j] = 0u;
-}
-
-// Per slice: the positions above the threshold pattern and at it.
+// Per slice: the last digit fixed (the threshold pattern and how many keys at it
+// are kept), then the positions above the pattern and at it.
 __global__ __launch_bounds__(1024) void topk_count_kernel(TopkArgs a) {
-  __shared__ uint32_t wsum[16];
+  __shared__ uint32_t wsum[16], st[4];
   const int s = blockIdx.y, tid = threadIdx.x;
   const int np = a.n - kWin;
-  const uint32_t prefix = a.state[4 * s];
+  topk_pick<2>(a, s, tid, wsum, st);
+  const uint32_t prefix = st[0];
   const uint32_t* key = a.key + (int64_t)s * a.n;
   const int i0 = blockIdx.x * a.slice, i1 = min(np, i0 + a.slice);
   uint32_t n_gt = 0u, n_eq = 0u;
@@ -366,7 +379,7 @@ __global__ __launch_bounds__(1024) void topk_write_kernel(TopkArgs a, int select
   const int np = a.n - kWin, k = a.keep_n - kWin;
   int32_t* out = a.keep + (int64_t)s * a.keep_n;
   if (select) {
-    const uint32_t prefix = a.state[4 * s], remaining = a.state[4 * s + 2];
+    const uint32_t prefix = a.state[16 * s + 12], remaining = a.state[16 * s + 14];  // after digit 2
     const uint32_t* key = a.key + (int64_t)s * a.n;
     uint32_t gt_slices = 0u, eq_slices = 0u;  // the slices before this one
     for (int j = 0; j < (int)blockIdx.x; ++j) {
@@ -651,7 +664,7 @@ TopkSizes topk_sizes(int64_t S, int32_t n_tokens) {
   z.slice = ((np + z.P - 1) / z.P + 63) / 64 * 64;
   if (z.slice == 0) z.slice = 64;
   z.hist = round256(S * kTopkBins * 4);
-  z.state = round256(S * 4 * 4);
+  z.state = round256(S * 16 * 4);
   z.cnt = round256(S * z.P * 2 * 4);
   return z;
 }
@@ -676,12 +689,9 @@ void launch_topk(const float* imp, int32_t* keep, int64_t S, int32_t n_tokens, i
   if (select) {
     hipLaunchKernelGGL(topk_init_kernel, dim3((unsigned)S), dim3(256), 0, stream, t);
     hipLaunchKernelGGL(topk_hist_kernel<0>, gs, b1024, 0, stream, t);
-    hipLaunchKernelGGL(topk_pick_kernel<0>, dim3((unsigned)S), b1024, 0, stream, t);
-    hipLaunchKernelGGL(topk_hist_kernel<1>, gs, b1024, 0, stream, t);
-    hipLaunchKernelGGL(topk_pick_kernel<1>, dim3((unsigned)S), b1024, 0, stream, t);
-    hipLaunchKernelGGL(topk_hist_kernel<2>, gs, b1024, 0, stream, t);
-    hipLaunchKernelGGL(topk_pick_kernel<2>, dim3((unsigned)S), b1024, 0, stream, t);
-    hipLaunchKernelGGL(topk_count_kernel, gs, b1024, 0, stream, t);
+    hipLaunchKernelGGL(topk_hist_kernel<1>, gs, b1024, 0, stream, t);  // digit 0 fixed first
+    hipLaunchKernelGGL(topk_hist_kernel<2>, gs, b1024, 0, stream, t);  // digit 1 fixed first
+    hipLaunchKernelGGL(topk_count_kernel, gs, b1024, 0, stream, t);    // digit 2 fixed first
   }
   hipLaunchKernelGGL(topk_write_kernel, gs, b1024, 0, stream, t, select ? 1 : 0);
 }
