@@ -459,7 +459,7 @@ def run_mla(args):
     app = time_append(kvk, torch, table, w.n_layers, arena, n_stored, (w.n_layers, w.batch, w.latent_dim),
                       (w.n_layers, w.batch, w.rope_dim), dev)
     log(f"append: {app}")
-    proj = time_projected_write(kvk, torch, w, table, arena, n_tok, dev) if plans is None else None
+    proj = time_projected_write(kvk, torch, w, table, arena, n_tok, dev, plans)
     log(f"projected write: {proj}")
     snap = time_snapkv_mla(kvk, torch, w, dev) if plans is None else None
     log(f"snapkv (MLA): {snap}")
@@ -510,14 +510,21 @@ def run_mla(args):
     print(json.dumps(line), flush=True)
 
 
-def time_projected_write(kvk, torch, w, table, arena, n_tok, dev):
+def time_projected_write(kvk, torch, w, table, arena, n_tok, dev, plans=None):
     """The prefill write with the down-projection (kvk_compress_layer_project) of the
     widest anchor, from hidden states of the model width: median of 5 after 2 warmups.
-    Runs after the decode timing (it rewrites that layer's region)."""
+    With one plan per sequence: layer 0, which every plan stores, each sequence at its
+    own kept width.  Runs after the decode timing (it rewrites that layer's region)."""
     from paper_2609_37988_amd import synth
-    anchors = [l for l in range(w.n_layers) if not w.plan[l][0]]
-    l = max(anchors, key=lambda a: w.plan[a][2])
-    d, bits = w.plan[l][2], w.plan[l][1]
+    if plans is None:
+        anchors = [l for l in range(w.n_layers) if not w.plan[l][0]]
+        l = max(anchors, key=lambda a: w.plan[a][2])
+        d, bits = w.plan[l][2], w.plan[l][1]
+        widths = [d] * w.batch
+    else:
+        l = 0
+        widths = [p[l][2] for p in plans]
+        d, bits = sorted(set(widths)), sorted({p[l][1] for p in plans})
     x = synth.latent_random(91, w.batch, n_tok, w.d_model, device=dev)
     wd = synth.weights_random(92, 1, 1, w.latent_dim, w.d_model, device=dev)[0, 0].contiguous()
     r = synth.latent_random(93, w.batch, n_tok, w.rope_dim, device=dev)
@@ -533,7 +540,7 @@ def time_projected_write(kvk, torch, w, table, arena, n_tok, dev):
         torch.cuda.synchronize()
         ts.append(e0.elapsed_time(e1))
     ms = sorted(ts)[2]
-    flops = 2.0 * w.batch * n_tok * w.d_model * d
+    flops = 2.0 * n_tok * w.d_model * sum(widths)
     del x, wd, r
     torch.cuda.empty_cache()
     return {"layer": l, "d": d, "bits": bits, "d_model": w.d_model, "tokens": w.batch * n_tok,

@@ -675,19 +675,8 @@ extern "C" kvk_status kvk_compress_layer_project(const kvk_table* t, int32_t lay
     return fail(KVK_ERR_INVALID, "misaligned buffer (16-byte alignment required)");
   if (kvk_status st = check_gpu_buffers({x, w_dkv, k_rope, keep_idx, arena, latent_out}, "kvk_compress_layer_project"))
     return st;
-  if (per_seq) {  // each sequence's own table and arena
-    for (int b = 0; b < d.batch; ++b) {
-      const kvk_table* s = t->seq[b];
-      if (s->plan[layer].inherit) continue;
-      const kvk_status st = mla_compress_layer_project(
-          s, layer, static_cast<const uint16_t*>(x) + (int64_t)b * n_tokens * d_model, w_dkv, d_model,
-          static_cast<const uint16_t*>(k_rope) + (int64_t)b * n_tokens * d.rope_dim, n_tokens,
-          keep_idx ? keep_idx + (int64_t)b * d.keep_tokens : nullptr, static_cast<uint8_t*>(arena) + t->seq_base[b],
-          nullptr, stream);
-      if (st != KVK_OK) return st;
-    }
-    return KVK_OK;
-  }
+  if (per_seq)  // each sequence's own table and arena, the inputs indexed by the batch's sequence
+    return mla_compress_layer_project_batched(t, layer, x, w_dkv, d_model, k_rope, n_tokens, keep_idx, arena, stream);
   return mla_compress_layer_project(t, layer, x, w_dkv, d_model, k_rope, n_tokens, keep_idx, arena, latent_out,
                                     stream);
 }

@@ -227,6 +227,11 @@ kvk_status mla_compress_layer_project(const kvk_table* t, int32_t layer, const v
 kvk_status mla_compress_layer(const kvk_table* t, int32_t layer, const void* latent,
                               const void* rope, int32_t in_dtype, int32_t n_tokens,
                               const int32_t* keep_idx, void* arena, hipStream_t stream);
+// The projected write of one layer of a per-sequence MLA table: one launch per
+// (kept width, bit-width) over the sequences whose plans store the layer so.
+kvk_status mla_compress_layer_project_batched(const kvk_table* t, int32_t layer, const void* x, const void* w_dkv,
+                                              int32_t d_model, const void* rope, int32_t n_tokens,
+                                              const int32_t* keep_idx, void* arena, hipStream_t stream);
 // The write of one layer of a per-sequence MLA table: one launch per (kept width,
 // bit-width) over the sequences whose plans store the layer so.
 kvk_status mla_compress_layer_batched(const kvk_table* t, int32_t layer, const void* latent, const void* rope,

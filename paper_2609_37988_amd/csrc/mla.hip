@@ -299,6 +299,12 @@ struct MlaProjectArgs {
   int32_t nb_cap;
   int32_t H;
   int32_t d;
+  // Per-sequence batches (n_seq > 0): launch row j writes sequence seq_of[j] (inputs
+  // indexed by the batch's sequence) into the stream seq_region[j] bytes after
+  // `region`; latent_out is then null.  n_seq = 0: row b is sequence b of one table.
+  int32_t n_seq;
+  int32_t seq_of[kMlaWriteSeqs];
+  int64_t seq_region[kMlaWriteSeqs];
 };
 
 __device__ __forceinline__ int mla_stored_pos(const int32_t* keep, int b, int n_stored, int n_tokens, int pos) {
@@ -366,7 +372,8 @@ __global__ __launch_bounds__(512) void mla_project_kernel(MlaProjectArgs a) {
   using P = ProjGeo<D>;
   __shared__ __attribute__((aligned(16))) uint16_t lds[P::LDS_HALFS];
   __shared__ uint32_t amax[2][32];
-  const int wg = blockIdx.x, b = blockIdx.y;
+  const int wg = blockIdx.x, j = blockIdx.y;
+  const int b = a.n_seq > 0 ? a.seq_of[j] : j;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6, i16 = lane & 15, kg = lane >> 4;
   const int wc = wv % P::WC, wt = wv / P::WC;
   const int row0 = P::TOK * wg;                         // first stored token of the tile
@@ -468,7 +475,7 @@ __global__ __launch_bounds__(512) void mla_project_kernel(MlaProjectArgs a) {
     if (slot > a.nbf) break;
     const bool tail = slot == a.nbf;
     const ProjectedRows src_rows{a, lds + 32 * k * P::LP, P::LP, b, 32 * slot, tail ? a.n_stored - 32 * slot : 32};
-    uint8_t* out = a.region + (int64_t)b * a.stream_bytes +
+    uint8_t* out = a.region + (a.n_seq > 0 ? a.seq_region[j] : (int64_t)j * a.stream_bytes) +
                    (tail ? (int64_t)a.nb_cap * a.block_bytes : (int64_t)slot * a.block_bytes);
     mla_write_block<BITS, KIVI>(src_rows, out, D, tail, amax, tid, 8);
     if constexpr (!KIVI) __syncthreads();  // amax is reused by the next block
@@ -1618,6 +1625,8 @@ kvk_status mla_append_token(const kvk_table* t, int32_t l0, int32_t l1, const vo
   return KVK_OK;
 }
 
+static kvk_status launch_w2p(const MlaProjectArgs& a, int bits, bool kivi, int32_t rows, hipStream_t stream);
+
 kvk_status mla_compress_layer_project(const kvk_table* t, int32_t layer, const void* x, const void* w_dkv,
                                       int32_t d_model, const void* rope, int32_t n_tokens,
                                       const int32_t* keep_idx, void* arena, void* latent_out, hipStream_t stream) {
@@ -1637,10 +1646,62 @@ kvk_status mla_compress_layer_project(const kvk_table* t, int32_t layer, const v
   a.nb_cap = t->nb_cap;
   a.H = d_model;
   a.d = t->rank[layer];
-  const int bits = t->bits[layer];
-  const bool kivi = d.qscheme == KVK_Q_KIVI32;
+  a.n_seq = 0;
+  return launch_w2p(a, t->bits[layer], d.qscheme == KVK_Q_KIVI32, d.batch, stream);
+}
+
+kvk_status mla_compress_layer_project_batched(const kvk_table* t, int32_t layer, const void* x, const void* w_dkv,
+                                              int32_t d_model, const void* rope, int32_t n_tokens,
+                                              const int32_t* keep_idx, void* arena, hipStream_t stream) {
+  const kvk_dims& d = t->d;
+  // One launch per (kept width, bit-width) for the sequences whose plans store the
+  // layer so; each sequence is written exactly as its one-sequence table writes it.
+  std::vector<char> done(d.batch, 0);
+  for (int b0 = 0; b0 < d.batch; ++b0) {
+    const kvk_table* s0 = t->seq[b0];
+    if (done[b0] || s0->plan[layer].inherit) continue;
+    MlaProjectArgs a;
+    a.x = static_cast<const uint16_t*>(x);
+    a.w = static_cast<const uint16_t*>(w_dkv);
+    a.rope = static_cast<const uint16_t*>(rope);
+    a.keep = keep_idx;
+    a.region = static_cast<uint8_t*>(arena);
+    a.latent_out = nullptr;
+    a.stream_bytes = s0->info.stream_bytes[layer];
+    a.block_bytes = s0->block_bytes[layer];
+    a.n_tokens = n_tokens;
+    a.n_stored = d.keep_tokens > 0 ? d.keep_tokens : n_tokens;
+    a.nbf = a.n_stored / KVK_GROUP;
+    a.nb_cap = t->nb_cap;
+    a.H = d_model;
+    a.d = s0->rank[layer];
+    a.n_seq = 0;
+    const int bits = s0->bits[layer];
+    for (int b = b0; b < d.batch; ++b) {
+      const kvk_table* s = t->seq[b];
+      if (done[b] || s->plan[layer].inherit || s->rank[layer] != a.d || s->bits[layer] != bits) continue;
+      done[b] = 1;
+      a.seq_of[a.n_seq] = b;
+      a.seq_region[a.n_seq] = t->seq_base[b] + s->info.layer_offset[layer];
+      if (++a.n_seq == kMlaWriteSeqs) {
+        const kvk_status st = launch_w2p(a, bits, d.qscheme == KVK_Q_KIVI32, a.n_seq, stream);
+        if (st != KVK_OK) return st;
+        a.n_seq = 0;
+      }
+    }
+    if (a.n_seq > 0) {
+      const kvk_status st = launch_w2p(a, bits, d.qscheme == KVK_Q_KIVI32, a.n_seq, stream);
+      if (st != KVK_OK) return st;
+    }
+  }
+  return KVK_OK;
+}
+
+// One projected-write launch: `rows` sequences (of one table, or the batch rows of
+// a.seq_of) at the arguments' kept width and the given bit-width.
+static kvk_status launch_w2p(const MlaProjectArgs& a, int bits, bool kivi, int32_t rows, hipStream_t stream) {
   const int tok = a.d > 512 ? ProjGeo<1024>::TOK : ProjGeo<512>::TOK;  // stored tokens per workgroup
-  const dim3 g3((unsigned)((a.nbf + 1 + tok / 32 - 1) / (tok / 32)), (unsigned)d.batch), b3(512);
+  const dim3 g3((unsigned)((a.nbf + 1 + tok / 32 - 1) / (tok / 32)), (unsigned)rows), b3(512);
 #define KVK_PROJ(DD)                                                                                          \
   if (a.d == DD) {                                                                                            \
     if (bits == 16) hipLaunchKernelGGL((mla_project_kernel<DD, 16, true>), g3, b3, 0, stream, a);              \
