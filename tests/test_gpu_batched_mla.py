@@ -166,6 +166,43 @@ def test_per_sequence_mla_projected_write():
             assert np.array_equal(got[base[l]:base[l] + nb], a1[info1.layer_offset[l]:info1.layer_offset[l] + nb].cpu().numpy())
 
 
+def test_per_sequence_projected_write_keep_lists_beyond_one_launch():
+    """70 sequences (more than one launch serves) with their own keep lists (32 of 40
+    positions, out of order): each sequence's bytes equal the same write on a
+    one-sequence table of its plan given its own rows and keep list."""
+    say("case batched mla projected write, 70 sequences, keep lists")
+    nb, n, H, keep = 70, 40, 256, 32
+    plans = [PLANS[b % len(PLANS)] for b in range(nb)]
+    dims = kvk.make_dims(kvk.MLA, L, HQ, 4, 128, R, 64, 128, 128, qscheme=kvk.KIVI32, batch=nb,
+                         max_tokens=n, keep_tokens=keep)
+    t = kvk.layer_table_batched(dims, [kvk.make_plan(p) for p in plans])
+    arena = _new(t)
+    X = synth.latent_random(210, nb, n, H).to(DEV)
+    W = synth.weights_random(211, 1, 1, R, H)[0, 0].contiguous().to(DEV)
+    Rk = synth.latent_random(212, nb, n, 64).to(DEV)
+    g = np.random.default_rng(213)
+    K = torch.from_numpy(np.stack([g.permutation(n)[:keep] for _ in range(nb)]).astype(np.int32)).to(DEV)
+    for l in range(L):
+        kvk.compress_layer_project(t, l, X, W, Rk, n, K, arena)
+    got = arena.cpu().numpy()
+    d1 = kvk.make_dims(kvk.MLA, L, HQ, 4, 128, R, 64, 128, 128, qscheme=kvk.KIVI32, batch=1,
+                       max_tokens=n, keep_tokens=keep)
+    for b in range(nb):
+        one = kvk.layer_table(d1, kvk.make_plan(plans[b]))
+        a1 = _new(one)
+        for l in range(L):
+            kvk.compress_layer_project(one, l, X[b:b + 1].contiguous(), W, Rk[b:b + 1].contiguous(), n,
+                                       K[b:b + 1].contiguous(), a1)
+        base = kvk.table_sequence_query(t, b).layer_offset
+        info1 = kvk.table_query(one)
+        for l in range(L):
+            if plans[b][l][0]:
+                continue
+            nbytes = info1.layer_bytes[l]
+            assert np.array_equal(got[base[l]:base[l] + nbytes],
+                                  a1[info1.layer_offset[l]:info1.layer_offset[l] + nbytes].cpu().numpy()), (b, l)
+
+
 def _one_table_decode(plan, inp_b, q_b, wk, wv, n, cap, qs=kvk.KIVI32):
     """Decode of one sequence through a one-sequence table of its plan."""
     one = kvk.layer_table(kvk.make_dims(kvk.MLA, len(plan), HQ, 4, 128, R, 64, 128, 128, qscheme=qs, batch=1,
